@@ -1,0 +1,156 @@
+"""fp64 CPU oracle of the variable-length LSTM time loop.
+
+TEST INFRASTRUCTURE ONLY: imported by the test suite, the smoke check and the
+benchmark's CPU-baseline leg, never by the product path.  It shares no code
+with the HIP library; the only module both sides use is ``workloads`` (seeded
+input generation, no arithmetic of the method).
+
+Two independent implementations live here:
+
+* ``forward``  -- plain C in double precision (``lstm_oracle.c``), the
+  definition of the masked recurrence of the paper's Section 9 "RNN cells"
+  experiment and Appendix A, with the standard LSTM cell.
+* ``brute.forward_per_sequence`` -- pure-Python ``math`` loops that run each
+  sequence on its own up to its own length, with no masking and no loop bound:
+  a brute-force cross-check for tiny cases.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "lstm_oracle.c")
+_LIB = os.path.join(_HERE, "liblstm_oracle.so")
+_lib = None
+
+OK, BAD_ARGS, BAD_LENGTHS, NOMEM = 0, 1, 2, 3
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def build(force: bool = True) -> str:
+    """Compile the C oracle into ``oracle/liblstm_oracle.so`` (gcc, OpenMP).
+
+    -ffp-contract=off keeps every multiply and add separately rounded, so the
+    result does not depend on the compiler's choice of fused operations.
+    """
+    stale = not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC)
+    if force or stale:
+        tmp = _LIB + f".tmp{os.getpid()}"
+        cmd = ["gcc", "-O3", "-ffp-contract=off", "-fno-fast-math", "-fopenmp", "-fPIC",
+               "-shared", _SRC, "-o", tmp, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+class _Lib:
+    """ctypes view of one build of ``lstm_oracle.c``."""
+
+    def __init__(self, path: str):
+        lib = ctypes.CDLL(path)
+        P = ctypes.c_void_p
+        lib.lstm_oracle_forward.argtypes = [ctypes.c_int] * 4 + [P] * 9 + [
+            ctypes.c_int, ctypes.c_int, P]
+        lib.lstm_oracle_forward.restype = ctypes.c_int
+        lib.lstm_oracle_max_threads.argtypes = []
+        lib.lstm_oracle_max_threads.restype = ctypes.c_int
+        self.lib = lib
+        self.path = path
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        build(force=False)
+        _lib = _Lib(_LIB)
+    return _lib
+
+
+def compile_variant(src_text: str, out_path: str) -> str:
+    """Compile C source text with the oracle's flags (used by the tests that
+    plant mistakes in a copy of the oracle to show the pins catch them)."""
+    src = out_path + ".c"
+    with open(src, "w") as f:
+        f.write(src_text)
+    subprocess.run(["gcc", "-O1", "-ffp-contract=off", "-fopenmp", "-fPIC", "-shared", src,
+                    "-o", out_path, "-lm"], check=True)
+    return out_path
+
+
+def source_text() -> str:
+    with open(_SRC) as f:
+        return f.read()
+
+
+def forward_with(path: str):
+    """A ``forward`` bound to the library at ``path``."""
+    lib = _Lib(path)
+
+    def fwd(*args, **kw):
+        return forward(*args, _lib_override=lib, **kw)
+    return fwd
+
+
+def max_threads() -> int:
+    return _load().lib.lstm_oracle_max_threads()
+
+
+def _f32(a):
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+def forward(x, lengths, W, U, b, h0, c0, literal: bool = False, threads: int = 0,
+            return_steps: bool = False, _lib_override=None):
+    """Final state (h, c) in float64 of the masked LSTM loop.
+
+    x [B, T, D], W [D, 4H], U [H, 4H], b [4H]: fp32 values (widen bf16 data
+    with ``workloads.bf16_bits_to_f32`` first); h0/c0 [B, H]: fp32 or fp64
+    values (held in fp64, so a run can resume from a returned state); lengths int32
+    [B] with 0 <= L[b] <= T, otherwise ``OracleError``.
+    """
+    lib = (_lib_override or _load()).lib
+    x, W, U, b = map(_f32, (x, W, U, b))
+    h0 = np.ascontiguousarray(h0, dtype=np.float64)
+    c0 = np.ascontiguousarray(c0, dtype=np.float64)
+    L = np.ascontiguousarray(lengths, dtype=np.int32)
+    B, T, D = x.shape
+    H = U.shape[0]
+    if W.shape != (D, 4 * H) or U.shape != (H, 4 * H) or b.shape != (4 * H,):
+        raise OracleError("weight shapes do not match x and U")
+    if L.shape != (B,) or h0.shape != (B, H) or c0.shape != (B, H):
+        raise OracleError("lengths/state shapes do not match x")
+    h = np.empty((B, H), np.float64)
+    c = np.empty((B, H), np.float64)
+    steps = ctypes.c_int64(0)
+    rc = lib.lstm_oracle_forward(B, T, D, H, x.ctypes.data, L.ctypes.data, W.ctypes.data,
+                                 U.ctypes.data, b.ctypes.data, h0.ctypes.data, c0.ctypes.data,
+                                 h.ctypes.data, c.ctypes.data, int(bool(literal)), int(threads),
+                                 ctypes.byref(steps))
+    if rc == BAD_LENGTHS:
+        raise OracleError("sequence lengths must lie in [0, T]")
+    if rc != OK:
+        raise OracleError(f"oracle failed with code {rc}")
+    if return_steps:
+        return h, c, int(steps.value)
+    return h, c
+
+
+def forward_inputs(inp, rows=None, literal: bool = False, threads: int = 0):
+    """``forward`` on a ``workloads.Inputs`` batch, optionally on a subset of rows.
+
+    Rows are independent in the definition, so running the oracle on rows
+    ``rows`` alone gives exactly those rows of the full batch's result.
+    """
+    x, W, U = inp.as_f32()
+    L, h0, c0 = inp.lengths, inp.h0, inp.c0
+    if rows is not None:
+        rows = np.asarray(rows, dtype=np.int64)
+        x, L, h0, c0 = x[rows], L[rows], h0[rows], c0[rows]
+    return forward(x, L, W, U, inp.b, h0, c0, literal=literal, threads=threads)

@@ -1,0 +1,66 @@
+"""Brute-force cross-check of the oracle for tiny cases (pure Python, ``math``).
+
+TEST INFRASTRUCTURE ONLY.  It runs every sequence on its own, for exactly its
+own number of steps (Section 9 "RNN cells": a sequence's state stops changing
+once its length is reached), with no batch, no mask, no select and no loop
+bound shared across rows.  It shares no code with ``lstm_oracle.c``; the cell
+is the standard LSTM (gate blocks i, f, g, o along 4H, one bias vector).
+"""
+from __future__ import annotations
+
+import math
+
+
+def _logistic(v: float) -> float:
+    return 1.0 / (1.0 + math.exp(-v))
+
+
+def run_sequence(xs, W, U, b, h, c):
+    """Run the cell over the rows of ``xs`` (a list of length-D lists).
+
+    W is D x 4H, U is H x 4H (nested lists), b has 4H entries; h, c have H.
+    Returns the final (h, c) as lists of floats.
+    """
+    H = len(h)
+    h = [float(v) for v in h]
+    c = [float(v) for v in c]
+    for xt in xs:
+        pre = []
+        for j in range(4 * H):
+            acc = 0.0
+            for k, xk in enumerate(xt):
+                acc += float(xk) * float(W[k][j])
+            for k in range(H):
+                acc += h[k] * float(U[k][j])
+            pre.append(acc + float(b[j]))
+        new_c = []
+        new_h = []
+        for u in range(H):
+            gi = _logistic(pre[u])
+            gf = _logistic(pre[H + u])
+            gg = math.tanh(pre[2 * H + u])
+            go = _logistic(pre[3 * H + u])
+            cu = gf * c[u] + gi * gg
+            new_c.append(cu)
+            new_h.append(go * math.tanh(cu))
+        h, c = new_h, new_c
+    return h, c
+
+
+def forward_per_sequence(x, lengths, W, U, b, h0, c0):
+    """Final (h, c) of each sequence run alone for its own length.
+
+    Arguments are numpy arrays or nested lists with the oracle's layouts;
+    returns two lists of B lists of H floats.
+    """
+    Wl = [list(map(float, row)) for row in W]
+    Ul = [list(map(float, row)) for row in U]
+    bl = list(map(float, b))
+    hs, cs = [], []
+    for r in range(len(lengths)):
+        n = int(lengths[r])
+        xs = [list(map(float, x[r][t])) for t in range(n)]
+        h, c = run_sequence(xs, Wl, Ul, bl, list(h0[r]), list(c0[r]))
+        hs.append(h)
+        cs.append(c)
+    return hs, cs

@@ -1,0 +1,172 @@
+/*
+ * lstm_oracle.c -- fp64 CPU oracle of the variable-length LSTM time loop.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may link, load or
+ * call this file; only the test suite, the smoke check and the benchmark's CPU
+ * baseline do.  It shares no code, header or constant with the HIP library.
+ *
+ * What it computes (AutoGraph paper, Section 9 "RNN cells", and the
+ * hand-written graph form of the same loop in Appendix A):
+ *
+ *   The state (h, c) starts at (h0, c0).  The loop bound is the largest
+ *   sequence length in the batch, max_len.  At step t = 0 .. max_len-1 every
+ *   row b with t < L[b] replaces its state by the cell applied to x[b, t] and
+ *   that state; every row with t >= L[b] keeps its state.  The masking is a
+ *   per-row select, not an arithmetic blend, so nothing computed for a
+ *   finished row can reach its state.  The result is the final state, which
+ *   for row b is the state after its own L[b] steps.
+ *
+ * The paper leaves rnn_cell abstract.  The cell here is the standard LSTM with
+ * one bias vector and gate blocks (i, f, g, o) along 4H:
+ *
+ *   z     = x_t W + h U + b          W [D][4H], U [H][4H], b [4H]
+ *   i = sig(z_i)  f = sig(z_f)  g = tanh(z_g)  o = sig(z_o)
+ *   c'    = f c + i g
+ *   h'    = o tanh(c')
+ *   sig(v) = 1 / (1 + exp(-v))
+ *
+ * Each dot product is summed in increasing k: the x part, then the h part,
+ * then the bias, so results do not depend on the thread count.
+ *
+ * Two forms of the masking are provided:
+ *   literal = 1 : every row runs the cell at every step and the new state is
+ *                 then selected per row.
+ *   literal = 0 : rows with t >= L[b] are skipped; the value the
+ *                 select would discard is never read, so the result is
+ *                 bitwise the same.
+ *
+ * x, W, U and b are fp32 (bf16 data is widened to fp32 exactly by the caller)
+ * and are widened to double here; the state is double; all arithmetic is in
+ * double.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* Return codes. */
+#define ORACLE_OK 0
+#define ORACLE_BAD_ARGS 1
+#define ORACLE_BAD_LENGTHS 2
+#define ORACLE_NOMEM 3
+
+static double sig(double v) { return 1.0 / (1.0 + exp(-v)); }
+
+/* One application of the LSTM cell to one row.
+ * xt: [D] input at this step; h, c: [H] current state (fp64);
+ * z: [4H] scratch; hn, cn: [H] new state. */
+static void lstm_cell_row(int D, int H, const float* xt, const float* W, const float* U,
+                          const float* bias, const double* h, const double* c,
+                          double* z, double* hn, double* cn) {
+    const int G = 4 * H;
+    for (int j = 0; j < G; ++j) z[j] = 0.0;
+    for (int k = 0; k < D; ++k) {              /* x_t W */
+        const double xk = (double)xt[k];
+        const float* wk = W + (size_t)k * G;
+        for (int j = 0; j < G; ++j) z[j] += xk * (double)wk[j];
+    }
+    for (int k = 0; k < H; ++k) {              /* + h U */
+        const double hk = h[k];
+        const float* uk = U + (size_t)k * G;
+        for (int j = 0; j < G; ++j) z[j] += hk * (double)uk[j];
+    }
+    for (int j = 0; j < G; ++j) z[j] += (double)bias[j];   /* + b */
+    for (int u = 0; u < H; ++u) {
+        const double ig = sig(z[u]);
+        const double fg = sig(z[H + u]);
+        const double gg = tanh(z[2 * H + u]);
+        const double og = sig(z[3 * H + u]);
+        const double cc = fg * c[u] + ig * gg;
+        cn[u] = cc;
+        hn[u] = og * tanh(cc);
+    }
+}
+
+/*
+ * lstm_oracle_forward
+ *   B, T, D, H   : batch, padded time extent, input width, hidden width (> 0)
+ *   x            : [B][T][D] fp32
+ *   L            : [B] int32 sequence lengths, each in [0, T]
+ *   W, U         : [D][4H], [H][4H] fp32
+ *   bias         : [4H] fp32
+ *   h0, c0       : [B][H] fp64 initial state (fp32 data widened exactly; fp64
+ *                  lets a run resume bitwise from a state this function wrote)
+ *   h_out, c_out : [B][H] fp64 final state (written)
+ *   literal      : 1 = compute every row then select, 0 = skip finished rows
+ *   nthreads     : OpenMP threads over the rows of one step (<= 0: default)
+ *   steps_out    : if non-NULL, receives the number of loop iterations run
+ * Returns ORACLE_OK, or an error code with the outputs untouched.
+ */
+int lstm_oracle_forward(int B, int T, int D, int H, const float* x, const int32_t* L,
+                        const float* W, const float* U, const float* bias,
+                        const double* h0, const double* c0, double* h_out, double* c_out,
+                        int literal, int nthreads, int64_t* steps_out) {
+    if (B <= 0 || T < 0 || D <= 0 || H <= 0 || !x || !L || !W || !U || !bias || !h0 || !c0 ||
+        !h_out || !c_out)
+        return ORACLE_BAD_ARGS;
+    int max_len = 0;
+    for (int b = 0; b < B; ++b) {
+        if (L[b] < 0 || L[b] > T) return ORACLE_BAD_LENGTHS;
+        if (L[b] > max_len) max_len = L[b];
+    }
+    const size_t BH = (size_t)B * H;
+    double* h = (double*)malloc(BH * sizeof(double));
+    double* c = (double*)malloc(BH * sizeof(double));
+    double* hn = (double*)malloc(BH * sizeof(double));
+    double* cn = (double*)malloc(BH * sizeof(double));
+    int nt = 1;
+#ifdef _OPENMP
+    nt = nthreads > 0 ? nthreads : omp_get_max_threads();
+#endif
+    double* zs = (double*)malloc((size_t)nt * 4 * H * sizeof(double));
+    if (!h || !c || !hn || !cn || !zs) {
+        free(h); free(c); free(hn); free(cn); free(zs);
+        return ORACLE_NOMEM;
+    }
+    for (size_t i = 0; i < BH; ++i) {            /* initial state */
+        h[i] = h0[i];
+        c[i] = c0[i];
+    }
+    for (int t = 0; t < max_len; ++t) {          /* t < max_len: the loop bound */
+#ifdef _OPENMP
+#pragma omp parallel for num_threads(nt) schedule(dynamic, 1)
+#endif
+        for (int b = 0; b < B; ++b) {
+            const int active = t < L[b];
+            if (!active && !literal) continue;
+            int tid = 0;
+#ifdef _OPENMP
+            tid = omp_get_thread_num();
+#endif
+            double* z = zs + (size_t)tid * 4 * H;
+            const float* xt = x + ((size_t)b * T + t) * D;
+            lstm_cell_row(D, H, xt, W, U, bias, h + (size_t)b * H, c + (size_t)b * H, z,
+                          hn + (size_t)b * H, cn + (size_t)b * H);
+        }
+        /* Per-row select: rows with t < L[b] take the new state, the others
+         * keep theirs.  Commits happen after every row of the step is done. */
+        for (int b = 0; b < B; ++b) {
+            if (t < L[b]) {
+                memcpy(h + (size_t)b * H, hn + (size_t)b * H, (size_t)H * sizeof(double));
+                memcpy(c + (size_t)b * H, cn + (size_t)b * H, (size_t)H * sizeof(double));
+            }
+        }
+    }
+    memcpy(h_out, h, BH * sizeof(double));
+    memcpy(c_out, c, BH * sizeof(double));
+    if (steps_out) *steps_out = max_len;
+    free(h); free(c); free(hn); free(cn); free(zs);
+    return ORACLE_OK;
+}
+
+/* Number of OpenMP threads a call with nthreads <= 0 would use. */
+int lstm_oracle_max_threads(void) {
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

@@ -1,0 +1,251 @@
+"""Pins of the fp64 oracle to facts that do not come from the oracle itself.
+
+Each ``pin_*`` takes a ``forward`` callable with the signature of
+``oracle.forward`` and raises AssertionError when the implementation disagrees
+with what the definition (AutoGraph Section 9 "RNN cells", Appendix A) or the
+mathematics fixes.  ``test_oracle.py`` runs every pin on the real oracle;
+``test_oracle_mutants.py`` runs them on copies of the oracle with planted
+mistakes and checks that each mistake is caught by at least one pin.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+import workloads
+from oracle import brute
+
+
+def _case(seed, B, D, H, T, lo=0, hi=None, state_var=0.1):
+    inp = workloads.random_case(seed, B, D, H, T, lo=lo, hi=hi, state_var=state_var)
+    return inp.x.copy(), inp.lengths.copy(), inp.W.copy(), inp.U.copy(), inp.b.copy(), \
+        inp.h0.copy(), inp.c0.copy()
+
+
+def _bits_equal(a, b):
+    return np.array_equal(np.asarray(a).view(np.uint64), np.asarray(b).view(np.uint64))
+
+
+def pin_zero_weights_closed_form(fwd):
+    """W = U = 0, b = 0: every sigmoid gate is exactly 1/2 and g = tanh(0) = 0,
+    so c after L steps is 2**-L * c0 (exact in binary floating point) and
+    h = tanh(c) / 2; a row of length 0 keeps (h0, c0)."""
+    B, D, H, T = 6, 5, 7, 9
+    x, L, W, U, b, h0, c0 = _case(11, B, D, H, T)
+    L[:] = [0, 1, 2, 5, 9, 3]
+    W[:] = 0
+    U[:] = 0
+    b[:] = 0
+    h, c = fwd(x, L, W, U, b, h0, c0)
+    c0d = c0.astype(np.float64)
+    for r in range(B):
+        n = int(L[r])
+        if n == 0:
+            assert _bits_equal(c[r], c0d[r]) and _bits_equal(h[r], h0[r].astype(np.float64))
+            continue
+        want_c = np.ldexp(c0d[r], -n)
+        assert _bits_equal(c[r], want_c), (r, c[r], want_c)
+        want_h = np.array([0.5 * math.tanh(v) for v in want_c])
+        assert np.max(np.abs(h[r] - want_h)) <= 1e-16
+
+
+def pin_forget_bias_closed_form(fwd):
+    """W = U = 0 and a forget-gate bias beta (gate blocks i, f, g, o): i = o = 1/2,
+    g = 0, f = logistic(beta), so c_L = logistic(beta)**L * c0, h = tanh(c_L) / 2."""
+    B, D, H, T = 4, 3, 5, 12
+    x, L, W, U, b, h0, c0 = _case(12, B, D, H, T)
+    L[:] = [12, 7, 1, 4]
+    W[:] = 0
+    U[:] = 0
+    b[:] = 0
+    beta = 1.0
+    b[H:2 * H] = beta
+    h, c = fwd(x, L, W, U, b, h0, c0)
+    f = 1.0 / (1.0 + math.exp(-beta))
+    for r in range(B):
+        want_c = c0[r].astype(np.float64) * f ** int(L[r])
+        assert np.max(np.abs(c[r] - want_c)) <= 1e-15 * max(1.0, np.max(np.abs(c0[r])))
+        want_h = 0.5 * np.tanh(want_c)
+        assert np.max(np.abs(h[r] - want_h)) <= 1e-15
+
+
+def pin_constant_input_geometric_series(fwd):
+    """U = 0 and x[b, t] the same vector at every step: the pre-activation
+    z = x W + b is constant per row, so the gates are constant and the cell
+    update c <- f c + i g is an affine recurrence with the closed form
+        c_L = f**L c0 + i g (1 - f**L) / (1 - f),   h_L = o tanh(c_L).
+    z is formed with numpy's matrix product; each gate block (i, f, g, o) gets
+    a different bias so a permuted gate order, a transposed W or a sign error
+    changes the result."""
+    B, D, H, T = 5, 4, 3, 10
+    x, L, W, U, b, h0, c0 = _case(13, B, D, H, T, lo=1)
+    L[:] = [10, 1, 3, 6, 8]
+    x[:] = x[:, :1, :]
+    U[:] = 0
+    b[:] = np.concatenate([np.full(H, 0.3), np.full(H, -0.7), np.full(H, 0.45), np.full(H, -0.2)])
+    b = b.astype(np.float32)
+    h, c = fwd(x, L, W, U, b, h0, c0)
+    z = x[:, 0, :].astype(np.float64) @ W.astype(np.float64) + b.astype(np.float64)
+    sig = lambda v: 1.0 / (1.0 + np.exp(-v))
+    gi, gf, gg, go = sig(z[:, :H]), sig(z[:, H:2 * H]), np.tanh(z[:, 2 * H:3 * H]), sig(z[:, 3 * H:])
+    n = L.astype(np.float64)[:, None]
+    fL = gf ** n
+    want_c = fL * c0.astype(np.float64) + gi * gg * (1.0 - fL) / (1.0 - gf)
+    want_h = go * np.tanh(want_c)
+    assert np.max(np.abs(c - want_c)) <= 1e-13
+    assert np.max(np.abs(h - want_h)) <= 1e-13
+
+
+def pin_length_zero(fwd):
+    """A row of length 0 never runs the cell: it returns (h0, c0) exactly."""
+    x, L, W, U, b, h0, c0 = _case(14, 5, 6, 4, 7)
+    L[:] = [0, 7, 0, 3, 0]
+    h, c = fwd(x, L, W, U, b, h0, c0)
+    for r in (0, 2, 4):
+        assert _bits_equal(h[r], h0[r].astype(np.float64))
+        assert _bits_equal(c[r], c0[r].astype(np.float64))
+    assert not np.array_equal(h[1], h0[1].astype(np.float64))
+
+
+def pin_all_lengths_zero(fwd):
+    """All lengths 0: the loop bound is 0 and the state is returned unchanged."""
+    x, L, W, U, b, h0, c0 = _case(15, 3, 4, 5, 6)
+    L[:] = 0
+    h, c = fwd(x, L, W, U, b, h0, c0)
+    assert _bits_equal(h, h0.astype(np.float64)) and _bits_equal(c, c0.astype(np.float64))
+
+
+def pin_freeze_poisoned_padding(fwd):
+    """Steps at t >= L[b] must not touch row b: NaN and Inf written into
+    x[b, t >= L[b]] leave every output bit unchanged (a select, not a blend)."""
+    x, L, W, U, b, h0, c0 = _case(16, 6, 5, 4, 9, lo=0)
+    L[:] = [9, 0, 4, 1, 7, 2]
+    h1, c1 = fwd(x, L, W, U, b, h0, c0)
+    xp = x.copy()
+    for r in range(len(L)):
+        xp[r, L[r]:, :] = np.nan
+        if L[r] + 1 < x.shape[1]:
+            xp[r, L[r] + 1, :] = np.inf
+    h2, c2 = fwd(xp, L, W, U, b, h0, c0)
+    assert _bits_equal(h1, h2) and _bits_equal(c1, c2)
+    assert np.isfinite(h2).all() and np.isfinite(c2).all()
+
+
+def pin_early_exit(fwd):
+    """Nothing at t >= max(L) is read: poisoning x[:, max_len:] changes nothing."""
+    x, L, W, U, b, h0, c0 = _case(17, 4, 3, 5, 12)
+    L[:] = [3, 5, 2, 0]
+    h1, c1 = fwd(x, L, W, U, b, h0, c0)
+    xp = x.copy()
+    xp[:, 5:, :] = np.nan
+    h2, c2 = fwd(xp, L, W, U, b, h0, c0)
+    assert _bits_equal(h1, h2) and _bits_equal(c1, c2)
+
+
+def pin_row_equals_own_run(fwd):
+    """Row b of a batch equals a batch of one holding x[b, :L[b]] alone."""
+    x, L, W, U, b, h0, c0 = _case(18, 5, 6, 5, 8, lo=1)
+    h, c = fwd(x, L, W, U, b, h0, c0)
+    for r in range(len(L)):
+        n = int(L[r])
+        hr, cr = fwd(x[r:r + 1, :n], L[r:r + 1], W, U, b, h0[r:r + 1], c0[r:r + 1])
+        assert _bits_equal(hr[0], h[r]) and _bits_equal(cr[0], c[r])
+
+
+def pin_permutation(fwd):
+    """Permuting the rows of (x, L, h0, c0) permutes the rows of the result."""
+    x, L, W, U, b, h0, c0 = _case(19, 7, 4, 6, 10)
+    h, c = fwd(x, L, W, U, b, h0, c0)
+    p = np.random.default_rng(0).permutation(len(L))
+    hp, cp = fwd(x[p], L[p], W, U, b, h0[p], c0[p])
+    assert _bits_equal(hp, h[p]) and _bits_equal(cp, c[p])
+
+
+def pin_chunked_resume(fwd):
+    """Running steps [0, t1) and then [t1, T) from the carried state, with
+    lengths min(L, t1) and max(L - t1, 0), equals the whole run."""
+    x, L, W, U, b, h0, c0 = _case(20, 6, 5, 4, 11)
+    h, c = fwd(x, L, W, U, b, h0, c0)
+    t1 = 4
+    ha, ca = fwd(x[:, :t1], np.minimum(L, t1), W, U, b, h0, c0)
+    hb, cb = fwd(x[:, t1:], np.maximum(L - t1, 0), W, U, b, ha, ca)
+    assert _bits_equal(hb, h) and _bits_equal(cb, c)
+
+
+def pin_brute_force(fwd, seeds=range(30)):
+    """Agreement (<= 1e-12) with running each sequence alone in pure Python,
+    on exhaustive-random tiny shapes B <= 4, D, H <= 3, T <= 6."""
+    for s in seeds:
+        rng = np.random.default_rng(1000 + s)
+        B, D, H, T = (int(rng.integers(1, 5)), int(rng.integers(1, 4)), int(rng.integers(1, 4)),
+                      int(rng.integers(1, 7)))
+        x, L, W, U, b, h0, c0 = _case(2000 + s, B, D, H, T)
+        b = (np.random.default_rng(s).standard_normal(4 * H) * 0.5).astype(np.float32)
+        h, c = fwd(x, L, W, U, b, h0, c0)
+        hb, cb = brute.forward_per_sequence(x, L, W, U, b, h0, c0)
+        assert np.max(np.abs(h - np.array(hb))) <= 1e-12, (s, B, D, H, T)
+        assert np.max(np.abs(c - np.array(cb))) <= 1e-12, (s, B, D, H, T)
+
+
+def pin_torch_lstm(fwd, shapes=((3, 4, 5, 6), (8, 24, 16, 12), (5, 1, 1, 9))):
+    """Agreement (<= 1e-12) with torch.nn.LSTM in float64 on packed sequences.
+
+    torch's LSTM computes the same cell with gate order (i, f, g, o) and
+    weights stored transposed: weight_ih = W^T, weight_hh = U^T, bias_ih = b,
+    bias_hh = 0.  Packing requires L >= 1."""
+    import torch
+    from torch.nn.utils.rnn import pack_padded_sequence
+    for k, (B, D, H, T) in enumerate(shapes):
+        x, L, W, U, b, h0, c0 = _case(3000 + k, B, D, H, T, lo=1)
+        b = (np.random.default_rng(k).standard_normal(4 * H) * 0.5).astype(np.float32)
+        h, c = fwd(x, L, W, U, b, h0, c0)
+        m = torch.nn.LSTM(D, H, batch_first=True).double()
+        with torch.no_grad():
+            m.weight_ih_l0.copy_(torch.from_numpy(W.astype(np.float64).T))
+            m.weight_hh_l0.copy_(torch.from_numpy(U.astype(np.float64).T))
+            m.bias_ih_l0.copy_(torch.from_numpy(b.astype(np.float64)))
+            m.bias_hh_l0.zero_()
+            packed = pack_padded_sequence(torch.from_numpy(x.astype(np.float64)),
+                                          torch.from_numpy(L.astype(np.int64)),
+                                          batch_first=True, enforce_sorted=False)
+            _, (hn, cn) = m(packed, (torch.from_numpy(h0.astype(np.float64))[None],
+                                     torch.from_numpy(c0.astype(np.float64))[None]))
+        assert np.max(np.abs(h - hn[0].numpy())) <= 1e-12, (B, D, H, T)
+        assert np.max(np.abs(c - cn[0].numpy())) <= 1e-12, (B, D, H, T)
+
+
+def pin_literal_equals_skip(fwd):
+    """Computing every row and selecting equals skipping finished rows, bitwise."""
+    x, L, W, U, b, h0, c0 = _case(21, 7, 6, 5, 10)
+    h1, c1 = fwd(x, L, W, U, b, h0, c0, literal=False)
+    h2, c2 = fwd(x, L, W, U, b, h0, c0, literal=True)
+    assert _bits_equal(h1, h2) and _bits_equal(c1, c2)
+
+
+def pin_bounds(fwd):
+    """|h| <= 1 always, and |c_L| <= |c0| + L (each step adds i g with |i g| < 1
+    to f c with 0 < f < 1)."""
+    x, L, W, U, b, h0, c0 = _case(22, 8, 6, 7, 15)
+    x *= 4.0
+    h, c = fwd(x, L, W, U, b, h0, c0)
+    assert np.all(np.abs(h) <= 1.0)
+    assert np.all(np.abs(c) <= np.abs(c0) + L[:, None] + 1e-12)
+
+
+PINS = [
+    pin_zero_weights_closed_form,
+    pin_forget_bias_closed_form,
+    pin_constant_input_geometric_series,
+    pin_length_zero,
+    pin_all_lengths_zero,
+    pin_freeze_poisoned_padding,
+    pin_early_exit,
+    pin_row_equals_own_run,
+    pin_permutation,
+    pin_chunked_resume,
+    pin_brute_force,
+    pin_torch_lstm,
+    pin_literal_equals_skip,
+    pin_bounds,
+]

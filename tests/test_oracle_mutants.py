@@ -1,0 +1,52 @@
+"""Plant plausible mistakes in copies of the C oracle and check that at least
+one pin catches each of them.  This shows the pins constrain every part of the
+definition: the input and recurrent products, the bias, the gate order and
+non-linearities, the cell update, the masking select and the loop bound.
+CPU only; the copies are compiled with gcc into a temporary directory."""
+import numpy as np
+import pytest
+
+import oracle
+from tests import oracle_pins
+
+MUTANTS = {
+    "drop_bias": ("z[j] += (double)bias[j];", "(void)bias[j];"),
+    "drop_recurrent_term": ("z[j] += hk * (double)uk[j];", "(void)(hk + uk[j]);"),
+    "drop_input_term": ("z[j] += xk * (double)wk[j];", "(void)(xk + wk[j]);"),
+    "transposed_W": ("z[j] += xk * (double)wk[j];", "z[j] += xk * (double)W[(size_t)j * D + k];"),
+    "transposed_U": ("z[j] += hk * (double)uk[j];", "z[j] += hk * (double)U[(size_t)j * H + k];"),
+    "swap_input_forget_gates": ("const double ig = sig(z[u]);\n        const double fg = sig(z[H + u]);",
+                                "const double ig = sig(z[H + u]);\n        const double fg = sig(z[u]);"),
+    "swap_cell_output_gates": ("const double gg = tanh(z[2 * H + u]);\n        const double og = sig(z[3 * H + u]);",
+                               "const double gg = tanh(z[3 * H + u]);\n        const double og = sig(z[2 * H + u]);"),
+    "sigmoid_sign": ("return 1.0 / (1.0 + exp(-v));", "return 1.0 / (1.0 + exp(v));"),
+    "output_gate_tanh": ("const double og = sig(z[3 * H + u]);", "const double og = tanh(z[3 * H + u]);"),
+    "cell_uses_output_gate": ("const double cc = fg * c[u] + ig * gg;", "const double cc = fg * c[u] + og * gg;"),
+    "forget_sign": ("const double cc = fg * c[u] + ig * gg;", "const double cc = -fg * c[u] + ig * gg;"),
+    "h_from_old_cell": ("hn[u] = og * tanh(cc);", "hn[u] = og * tanh(c[u]);"),
+    "mask_inclusive": ("if (t < L[b]) {", "if (t <= L[b]) {"),
+    "no_select": ("if (t < L[b]) {", "if (1) {"),
+    "loop_bound_short": ("for (int t = 0; t < max_len; ++t) {", "for (int t = 0; t < max_len - 1; ++t) {"),
+    "ignore_initial_cell": ("c[i] = c0[i];", "c[i] = 0.0; (void)c0[i];"),
+    "ignore_initial_hidden": ("h[i] = h0[i];", "h[i] = 0.0; (void)h0[i];"),
+    "gx_row_stride": ("const float* xt = x + ((size_t)b * T + t) * D;",
+                      "const float* xt = x + ((size_t)t * B + b) * D;"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_planted_mistake(name, tmp_path):
+    old, new = MUTANTS[name]
+    src = oracle.source_text()
+    assert src.count(old) == 1, f"mutation anchor for {name} not found exactly once"
+    lib = oracle.compile_variant(src.replace(old, new), str(tmp_path / f"mut_{name}.so"))
+    fwd = oracle.forward_with(lib)
+    caught = []
+    for pin in oracle_pins.PINS:
+        try:
+            with np.errstate(all="ignore"):
+                pin(fwd)
+        except (AssertionError, oracle.OracleError):
+            caught.append(pin.__name__)
+            break
+    assert caught, f"no pin caught mutant {name}"
