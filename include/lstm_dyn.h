@@ -1,0 +1,149 @@
+/*
+ * lstm_dyn.h -- C ABI of the MI355X (gfx950) variable-length LSTM time loop.
+ *
+ * The operation (AutoGraph paper, Section 9 "RNN cells", and its hand-written
+ * graph form in Appendix A): starting from (h0, c0), run an LSTM cell over the
+ * batch for t = 0, 1, ... while any sequence still has steps left; a sequence
+ * whose length L[b] has been reached keeps its state unchanged (a per-row
+ * select); the loop stops after max_b L[b] steps.  The result is the final
+ * state (h, c) of every sequence.  The paper leaves the cell abstract; here it
+ * is the standard LSTM with one bias vector and gate blocks (i, f, g, o):
+ *
+ *     z  = x[b, t] W + h U + b
+ *     c' = sigmoid(z_f) * c + sigmoid(z_i) * tanh(z_g)
+ *     h' = sigmoid(z_o) * tanh(c')
+ *
+ * Layouts (all row-major, contiguous, caller-owned DEVICE memory):
+ *     x        [B][T_max][D]   element type = dtype (fp32 or bf16)
+ *     lengths  [B]             int32, each expected in [0, T_max]
+ *     W        [D][4H]         element type = dtype
+ *     U        [H][4H]         element type = dtype
+ *     b        [4H]            fp32
+ *     h0, c0   [B][H]          fp32
+ *     out_h, out_c [B][H]      fp32 (written)
+ * Gate blocks along 4H are i = [0, H), f = [H, 2H), g = [2H, 3H), o = [3H, 4H).
+ * With bf16 data, every product is formed from bf16 operands and accumulated
+ * in fp32; the state (h, c) is kept in fp32.
+ *
+ * Threading: a handle may be used from one host thread at a time, and one
+ * forward may be in flight per handle.  Forward calls only enqueue work on the
+ * given stream (a hipStream_t; NULL = the default stream); inputs and outputs
+ * must stay valid until that work completes.
+ *
+ * Error classes mirror the paper's split of failures (Appendix B): argument
+ * problems found on the host are reported synchronously (LSTM_DYN_ERR_INVALID,
+ * LSTM_DYN_ERR_UNSUPPORTED); problems in device data (lengths outside
+ * [0, T_max]) are clamped for memory safety and reported by
+ * lstm_dyn_query(LSTM_DYN_Q_LAST_STATUS) after the forward has run.
+ */
+#ifndef LSTM_DYN_H
+#define LSTM_DYN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct lstm_dyn lstm_dyn_t; /* opaque handle */
+
+/* Element type of x, W and U. */
+enum { LSTM_DYN_F32 = 0, LSTM_DYN_BF16 = 1 };
+
+/* Execution mode.
+ * PERSISTENT: the time loop runs on the device inside one persistent kernel
+ *   (grid-wide synchronisation between steps, loop bound and early exit read
+ *   on the device); 3 launches per forward, none of them waits for the host.
+ * PER_STEP: the comparison path of the paper's eager-vs-graph experiment
+ *   (Section 9, Table 1): the loop bound is copied to the host (one
+ *   synchronisation), then the host issues two kernel launches per step. */
+enum { LSTM_DYN_PERSISTENT = 0, LSTM_DYN_PER_STEP = 1 };
+
+/* Status codes. */
+enum {
+    LSTM_DYN_OK = 0,
+    LSTM_DYN_ERR_INVALID = 1,     /* NULL handle/pointer, bad sizes, misaligned or overlapping buffers */
+    LSTM_DYN_ERR_HIP = 2,         /* a HIP runtime call failed */
+    LSTM_DYN_ERR_NOMEM = 3,       /* device workspace allocation failed */
+    LSTM_DYN_ERR_UNSUPPORTED = 4, /* sizes outside what this build's kernels cover */
+    LSTM_DYN_ERR_BAD_LENGTHS = 5, /* (device status) a length was outside [0, T_max] and was clamped */
+    LSTM_DYN_ERR_TIMEOUT = 6      /* (device status) a grid barrier wait exceeded its bound */
+};
+
+/* lstm_dyn_query selectors. */
+enum {
+    LSTM_DYN_Q_LAST_STATUS = 0,        /* status of the last forward (synchronises its stream) */
+    LSTM_DYN_Q_STEPS_EXECUTED = 1,     /* loop iterations of the last forward = max_b L[b] (synchronises) */
+    LSTM_DYN_Q_LAUNCHES_PER_FORWARD = 2, /* kernel launches issued by the last forward */
+    LSTM_DYN_Q_GROUPS = 3,             /* workgroups of the persistent kernel */
+    LSTM_DYN_Q_WORKSPACE_BYTES = 4,    /* device workspace owned by the handle */
+    LSTM_DYN_Q_TOTAL_ROWS = 5          /* sum of the (clamped) lengths of the last forward (synchronises) */
+};
+
+/* Launch plan of a handle: pure host arithmetic, no device access. */
+typedef struct {
+    int mt;             /* 16-column gate tiles per workgroup (4 hidden units each) */
+    int groups;         /* workgroups of the persistent kernel (at most one per CU) */
+    int ksw;            /* MFMA K-steps per wave over the hidden width */
+    int kswmax;         /* K-step capacity of the kernel variant that will run */
+    int hpad;           /* hidden width padded to the recurrent MFMA's K granularity */
+    int bpad;           /* batch padded to 16 rows */
+    int lds_bytes;      /* dynamic LDS of the persistent kernel */
+    int nstate;         /* (row tile, gate tile) pairs held per wave */
+    long long workspace_bytes; /* device workspace a handle allocates */
+} lstm_dyn_plan_t;
+
+/*
+ * lstm_dyn_create: validate sizes, choose a plan for the current HIP device
+ * and allocate the handle's device workspace (hipMalloc; freed by destroy).
+ *   B >= 1, D >= 1, H >= 1, T_max >= 1; dtype LSTM_DYN_F32/BF16; mode
+ *   LSTM_DYN_PERSISTENT/PER_STEP.  *out receives the handle (NULL on error).
+ * Returns LSTM_DYN_OK, ERR_INVALID (bad arguments; no HIP call is made),
+ * ERR_UNSUPPORTED (sizes this build's kernels do not cover), ERR_HIP, ERR_NOMEM.
+ */
+int lstm_dyn_create(lstm_dyn_t** out, int B, int D, int H, int T_max, int dtype, int mode);
+
+/*
+ * lstm_dyn_forward: enqueue one forward of the loop on `stream`.
+ * Pointer arguments are caller-owned device buffers with the layouts above;
+ * x, W and U must be 16-byte aligned, the others 4-byte aligned.  Outputs may
+ * alias their own initial state exactly (out_h == h0, out_c == c0); any other
+ * overlap between an output and an input or the other output is ERR_INVALID.
+ * Persistent mode never synchronises with the host; per-step mode performs
+ * exactly one device-to-host copy of the loop bound.
+ */
+int lstm_dyn_forward(lstm_dyn_t* h, const void* x, const int32_t* lengths, const void* W,
+                     const void* U, const float* b, const float* h0, const float* c0,
+                     float* out_h, float* out_c, void* stream);
+
+/* Free the handle and its workspace (synchronises the device).  NULL is a no-op. */
+int lstm_dyn_destroy(lstm_dyn_t* h);
+
+/* Read a property of the handle or of its last forward (see LSTM_DYN_Q_*). */
+int lstm_dyn_query(lstm_dyn_t* h, int what, long long* value);
+
+/* Static description of a status code (never NULL). */
+const char* lstm_dyn_strerror(int status);
+
+/*
+ * lstm_dyn_plan: the plan lstm_dyn_create would choose for a device with
+ * `num_cus` compute units.  Host arithmetic only.  Returns LSTM_DYN_OK,
+ * ERR_INVALID or ERR_UNSUPPORTED.
+ */
+int lstm_dyn_plan(int B, int D, int H, int T_max, int dtype, int mode, int num_cus,
+                  lstm_dyn_plan_t* out);
+
+/*
+ * lstm_dyn_check_args: the host-side argument checks of lstm_dyn_forward
+ * (NULL pointers, alignment, overlap) for the given sizes, without touching
+ * the pointed-to memory.  Returns LSTM_DYN_OK or ERR_INVALID.
+ */
+int lstm_dyn_check_args(int B, int D, int H, int T_max, int dtype, const void* x,
+                        const int32_t* lengths, const void* W, const void* U, const float* b,
+                        const float* h0, const float* c0, const float* out_h, const float* out_c);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LSTM_DYN_H */

@@ -1,0 +1,205 @@
+"""Variable-length LSTM time loop for MI355X (gfx950): Python binding.
+
+A thin ctypes layer over ``liblstm_dyn.so`` (C ABI in ``include/lstm_dyn.h``).
+Every step of the computation runs in the library's HIP kernels; torch is used
+only to own device memory and to name streams.  Importing this module does not
+need a GPU; calling ``lstm_dyn_create`` does.  If the library has not been
+built, loading it raises ``ImportError`` -- there is no fallback path.
+
+Functions mirror the C ABI (same names); ``LstmDyn`` wraps a handle for torch
+tensors.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+__all__ = [
+    "F32", "BF16", "PERSISTENT", "PER_STEP", "LstmDynError", "LstmDyn", "library_path",
+    "lstm_dyn_create", "lstm_dyn_forward", "lstm_dyn_destroy", "lstm_dyn_query",
+    "lstm_dyn_strerror", "lstm_dyn_plan", "lstm_dyn_check_args",
+]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "liblstm_dyn.so")
+
+F32, BF16 = 0, 1
+PERSISTENT, PER_STEP = 0, 1
+OK, ERR_INVALID, ERR_HIP, ERR_NOMEM, ERR_UNSUPPORTED, ERR_BAD_LENGTHS, ERR_TIMEOUT = range(7)
+Q_LAST_STATUS, Q_STEPS_EXECUTED, Q_LAUNCHES_PER_FORWARD, Q_GROUPS, Q_WORKSPACE_BYTES, \
+    Q_TOTAL_ROWS = range(6)
+
+_DTYPES = {"f32": F32, "fp32": F32, "float32": F32, "bf16": BF16, "bfloat16": BF16}
+_MODES = {"persistent": PERSISTENT, "per_step": PER_STEP}
+
+
+class LstmDynError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        super().__init__(f"{where}: {lstm_dyn_strerror(code)} (status {code})")
+
+
+class _Plan(ctypes.Structure):
+    _fields_ = [("mt", ctypes.c_int), ("groups", ctypes.c_int), ("ksw", ctypes.c_int),
+                ("kswmax", ctypes.c_int), ("hpad", ctypes.c_int), ("bpad", ctypes.c_int),
+                ("lds_bytes", ctypes.c_int), ("nstate", ctypes.c_int),
+                ("workspace_bytes", ctypes.c_longlong)]
+
+
+_lib = None
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(f"{_LIB_PATH} is missing: build it with "
+                          "`python -m paper_1810_08061_amd.build`")
+    lib = ctypes.CDLL(_LIB_PATH)
+    P, I, LL = ctypes.c_void_p, ctypes.c_int, ctypes.c_longlong
+    lib.lstm_dyn_create.argtypes = [ctypes.POINTER(P), I, I, I, I, I, I]
+    lib.lstm_dyn_create.restype = I
+    lib.lstm_dyn_forward.argtypes = [P] * 11
+    lib.lstm_dyn_forward.restype = I
+    lib.lstm_dyn_destroy.argtypes = [P]
+    lib.lstm_dyn_destroy.restype = I
+    lib.lstm_dyn_query.argtypes = [P, I, ctypes.POINTER(LL)]
+    lib.lstm_dyn_query.restype = I
+    lib.lstm_dyn_strerror.argtypes = [I]
+    lib.lstm_dyn_strerror.restype = ctypes.c_char_p
+    lib.lstm_dyn_plan.argtypes = [I] * 7 + [ctypes.POINTER(_Plan)]
+    lib.lstm_dyn_plan.restype = I
+    lib.lstm_dyn_check_args.argtypes = [I] * 5 + [P] * 9
+    lib.lstm_dyn_check_args.restype = I
+    _lib = lib
+    return lib
+
+
+# --- C ABI mirrors ----------------------------------------------------------
+
+def lstm_dyn_strerror(code: int) -> str:
+    return _load().lstm_dyn_strerror(int(code)).decode()
+
+
+def lstm_dyn_create(B: int, D: int, H: int, T_max: int, dtype: int, mode: int) -> int:
+    h = ctypes.c_void_p()
+    rc = _load().lstm_dyn_create(ctypes.byref(h), B, D, H, T_max, dtype, mode)
+    if rc != OK:
+        raise LstmDynError(rc, "lstm_dyn_create")
+    return h.value
+
+
+def lstm_dyn_forward(handle: int, x: int, lengths: int, W: int, U: int, b: int, h0: int, c0: int,
+                     out_h: int, out_c: int, stream: int = 0) -> None:
+    rc = _load().lstm_dyn_forward(handle, x, lengths, W, U, b, h0, c0, out_h, out_c, stream)
+    if rc != OK:
+        raise LstmDynError(rc, "lstm_dyn_forward")
+
+
+def lstm_dyn_destroy(handle: int) -> None:
+    rc = _load().lstm_dyn_destroy(handle)
+    if rc != OK:
+        raise LstmDynError(rc, "lstm_dyn_destroy")
+
+
+def lstm_dyn_query(handle: int, what: int) -> int:
+    v = ctypes.c_longlong(0)
+    rc = _load().lstm_dyn_query(handle, what, ctypes.byref(v))
+    if rc != OK:
+        raise LstmDynError(rc, "lstm_dyn_query")
+    return int(v.value)
+
+
+def lstm_dyn_plan(B: int, D: int, H: int, T_max: int, dtype: int, mode: int, num_cus: int) -> dict:
+    p = _Plan()
+    rc = _load().lstm_dyn_plan(B, D, H, T_max, dtype, mode, num_cus, ctypes.byref(p))
+    if rc != OK:
+        raise LstmDynError(rc, "lstm_dyn_plan")
+    return {name: getattr(p, name) for name, _ in _Plan._fields_}
+
+
+def lstm_dyn_check_args(B: int, D: int, H: int, T_max: int, dtype: int, x: int, lengths: int,
+                        W: int, U: int, b: int, h0: int, c0: int, out_h: int, out_c: int) -> int:
+    return _load().lstm_dyn_check_args(B, D, H, T_max, dtype, x, lengths, W, U, b, h0, c0,
+                                       out_h, out_c)
+
+
+# --- torch convenience wrapper ---------------------------------------------
+
+class LstmDyn:
+    """One handle of the library for fixed (B, D, H, T_max, dtype, mode).
+
+    ``forward`` takes CUDA (HIP) tensors in the layouts of the C ABI:
+    x [B, T_max, D] and W [D, 4H], U [H, 4H] in the handle's dtype
+    (torch.float32 or torch.bfloat16), lengths int32 [B], b float32 [4H],
+    h0/c0 float32 [B, H]; it returns (out_h, out_c) float32 [B, H].
+    """
+
+    def __init__(self, B: int, D: int, H: int, T_max: int, dtype="bf16", mode="persistent"):
+        self.B, self.D, self.H, self.T = B, D, H, T_max
+        self.dtype = _DTYPES[dtype] if isinstance(dtype, str) else int(dtype)
+        self.mode = _MODES[mode] if isinstance(mode, str) else int(mode)
+        self.handle = lstm_dyn_create(B, D, H, T_max, self.dtype, self.mode)
+
+    def _check(self, name, t, dtype, shape):
+        import torch
+        if not isinstance(t, torch.Tensor) or not t.is_cuda:
+            raise TypeError(f"{name} must be a device tensor")
+        if t.dtype != dtype:
+            raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+        if tuple(t.shape) != tuple(shape):
+            raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+
+    def forward(self, x, lengths, W, U, b, h0, c0, out_h=None, out_c=None, stream=None):
+        import torch
+        B, D, H, T = self.B, self.D, self.H, self.T
+        et = torch.bfloat16 if self.dtype == BF16 else torch.float32
+        self._check("x", x, et, (B, T, D))
+        self._check("lengths", lengths, torch.int32, (B,))
+        self._check("W", W, et, (D, 4 * H))
+        self._check("U", U, et, (H, 4 * H))
+        self._check("b", b, torch.float32, (4 * H,))
+        self._check("h0", h0, torch.float32, (B, H))
+        self._check("c0", c0, torch.float32, (B, H))
+        if out_h is None:
+            out_h = torch.empty((B, H), dtype=torch.float32, device=x.device)
+        if out_c is None:
+            out_c = torch.empty((B, H), dtype=torch.float32, device=x.device)
+        self._check("out_h", out_h, torch.float32, (B, H))
+        self._check("out_c", out_c, torch.float32, (B, H))
+        if stream is None:
+            stream = torch.cuda.current_stream(x.device)
+        s = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+        lstm_dyn_forward(self.handle, x.data_ptr(), lengths.data_ptr(), W.data_ptr(),
+                         U.data_ptr(), b.data_ptr(), h0.data_ptr(), c0.data_ptr(),
+                         out_h.data_ptr(), out_c.data_ptr(), s)
+        return out_h, out_c
+
+    __call__ = forward
+
+    def query(self, what: int) -> int:
+        return lstm_dyn_query(self.handle, what)
+
+    def close(self):
+        if getattr(self, "handle", None):
+            lstm_dyn_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()

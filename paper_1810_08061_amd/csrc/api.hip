@@ -1,0 +1,300 @@
+// api.hip -- the C ABI declared in include/lstm_dyn.h: argument checks,
+// launch plan, workspace ownership and the two execution modes.
+#include <new>
+#include <stdint.h>
+#include <string.h>
+
+#include "../../include/lstm_dyn.h"
+#include "launch.h"
+
+using namespace ldyn;
+
+struct lstm_dyn {
+    int B, D, H, T, dtype, mode;
+    int device, num_cus;
+    lstm_dyn_plan_t plan;
+    Dims dims;
+    Workspace ws;
+    void* block;               // the one device allocation behind ws
+    int32_t* host_maxlen;      // pinned host word for the per-step path's loop-bound copy
+    unsigned epoch;            // barrier values of the next forward start above this
+    unsigned long long timeout_ticks;
+    int inproj_grid;
+    long long launches_last;
+    hipStream_t last_stream;
+};
+
+namespace {
+
+constexpr int KW = 4;             // waves per persistent workgroup (split K)
+constexpr int LDS_TILES = 32;     // partial tiles per wave in LDS
+constexpr int PREP_MAX_B = 8192;
+constexpr unsigned EPOCH_LIMIT = 0xF0000000u;
+constexpr double BARRIER_TIMEOUT_S = 5.0;
+
+long long align_up(long long v, long long a) { return (v + a - 1) / a * a; }
+
+
+struct Layout {
+    long long meta, perm, offsets, rowsrc, gx, hx, flags, z, total;
+};
+
+Layout layout_of(int B, int H, int T, int bf16, int mode, int bpad, int hpad, int groups) {
+    Layout L{};
+    long long o = 0;
+    auto take = [&](long long bytes) {
+        const long long at = o;
+        o = align_up(o + bytes, 256);
+        return at;
+    };
+    L.meta = take(sizeof(Meta));
+    L.perm = take(4LL * B);
+    L.offsets = take(4LL * (T + 1));
+    L.rowsrc = take(4LL * B * T);
+    L.gx = take(16LL * H * B * T);
+    L.hx = take(2LL * bpad * hpad * (bf16 ? 2 : 4));
+    L.flags = take(4LL * groups);
+    L.z = take(mode == LSTM_DYN_PER_STEP ? 16LL * H * bpad : 0);
+    L.total = o;
+    return L;
+}
+
+bool overlaps(const void* a, long long na, const void* b, long long nb) {
+    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return x < y + (uintptr_t)nb && y < x + (uintptr_t)na;
+}
+
+}  // namespace
+
+extern "C" const char* lstm_dyn_strerror(int status) {
+    switch (status) {
+        case LSTM_DYN_OK: return "ok";
+        case LSTM_DYN_ERR_INVALID: return "invalid argument";
+        case LSTM_DYN_ERR_HIP: return "HIP runtime error";
+        case LSTM_DYN_ERR_NOMEM: return "device workspace allocation failed";
+        case LSTM_DYN_ERR_UNSUPPORTED: return "sizes not supported by this build";
+        case LSTM_DYN_ERR_BAD_LENGTHS: return "a sequence length was outside [0, T_max] and was clamped";
+        case LSTM_DYN_ERR_TIMEOUT: return "a grid barrier wait exceeded its bound";
+        default: return "unknown status";
+    }
+}
+
+extern "C" int lstm_dyn_plan(int B, int D, int H, int T, int dtype, int mode, int num_cus,
+                             lstm_dyn_plan_t* out) {
+    if (!out) return LSTM_DYN_ERR_INVALID;
+    memset(out, 0, sizeof(*out));
+    if (B < 1 || D < 1 || H < 1 || T < 1 || num_cus < 1) return LSTM_DYN_ERR_INVALID;
+    if (dtype != LSTM_DYN_F32 && dtype != LSTM_DYN_BF16) return LSTM_DYN_ERR_INVALID;
+    if (mode != LSTM_DYN_PERSISTENT && mode != LSTM_DYN_PER_STEP) return LSTM_DYN_ERR_INVALID;
+    if (B > PREP_MAX_B || (long long)B * T > 0x7fffffffLL || 4LL * H > 0x7fffffffLL / 4)
+        return LSTM_DYN_ERR_UNSUPPORTED;
+    const int bf16 = dtype == LSTM_DYN_BF16;
+    const int kstep = bf16 ? 32 : 4;
+    const int ksw = (H + kstep * KW - 1) / (kstep * KW);
+    const int ntmax = (B + 15) / 16;
+    // Gate tiles per workgroup: one workgroup for H <= 32 (no grid barrier),
+    // otherwise the fewest units per workgroup that fit one workgroup per CU.
+    int mt = 0, kswmax = 0, nst = 0, nstate = 0;
+    for (int cand : {8, 1, 2}) {
+        if (cand == 8 && H > 32) continue;
+        const int groups = (H + 4 * cand - 1) / (4 * cand);
+        if (groups > num_cus) continue;
+        nstate = (ntmax * cand + KW - 1) / KW;
+        if (mode == LSTM_DYN_PER_STEP) {
+            mt = cand;
+            break;
+        }
+        if (persistent_pick_variant(bf16, cand, ksw, nstate, &kswmax, &nst)) {
+            mt = cand;
+            break;
+        }
+    }
+    if (mt == 0) return LSTM_DYN_ERR_UNSUPPORTED;
+    out->mt = mt;
+    out->groups = (H + 4 * mt - 1) / (4 * mt);
+    out->ksw = ksw;
+    out->kswmax = kswmax;
+    out->hpad = ksw * kstep * KW;
+    out->bpad = ntmax * 16;
+    out->lds_bytes = KW * LDS_TILES * 64 * 16;
+    out->nstate = nst;
+    out->workspace_bytes =
+        layout_of(B, H, T, bf16, mode, out->bpad, out->hpad, out->groups).total;
+    return LSTM_DYN_OK;
+}
+
+extern "C" int lstm_dyn_check_args(int B, int D, int H, int T, int dtype, const void* x,
+                                   const int32_t* lengths, const void* W, const void* U,
+                                   const float* b, const float* h0, const float* c0,
+                                   const float* out_h, const float* out_c) {
+    if (B < 1 || D < 1 || H < 1 || T < 1) return LSTM_DYN_ERR_INVALID;
+    if (dtype != LSTM_DYN_F32 && dtype != LSTM_DYN_BF16) return LSTM_DYN_ERR_INVALID;
+    if (!x || !lengths || !W || !U || !b || !h0 || !c0 || !out_h || !out_c) return LSTM_DYN_ERR_INVALID;
+    auto al = [](const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; };
+    if (!al(x, 16) || !al(W, 16) || !al(U, 16)) return LSTM_DYN_ERR_INVALID;
+    if (!al(lengths, 4) || !al(b, 4) || !al(h0, 4) || !al(c0, 4) || !al(out_h, 4) || !al(out_c, 4))
+        return LSTM_DYN_ERR_INVALID;
+    const long long e = dtype == LSTM_DYN_BF16 ? 2 : 4;
+    const long long nx = (long long)B * T * D * e, nL = 4LL * B, nW = (long long)D * 4 * H * e,
+                    nU = (long long)H * 4 * H * e, nb = 16LL * H, ns = 4LL * B * H;
+    if (overlaps(out_h, ns, out_c, ns)) return LSTM_DYN_ERR_INVALID;
+    const void* ins[] = {x, lengths, W, U, b, h0, c0};
+    const long long nin[] = {nx, nL, nW, nU, nb, ns, ns};
+    for (int i = 0; i < 7; ++i) {
+        if (overlaps(out_h, ns, ins[i], nin[i]) && !(i == 5 && out_h == h0)) return LSTM_DYN_ERR_INVALID;
+        if (overlaps(out_c, ns, ins[i], nin[i]) && !(i == 6 && out_c == c0)) return LSTM_DYN_ERR_INVALID;
+    }
+    return LSTM_DYN_OK;
+}
+
+extern "C" int lstm_dyn_create(lstm_dyn_t** out, int B, int D, int H, int T, int dtype, int mode) {
+    if (!out) return LSTM_DYN_ERR_INVALID;
+    *out = nullptr;
+    lstm_dyn_plan_t plan;
+    int rc = lstm_dyn_plan(B, D, H, T, dtype, mode, 1 << 20, &plan);  // size checks only
+    if (rc != LSTM_DYN_OK) return rc;
+    int dev = 0, cus = 0, wclk_khz = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return LSTM_DYN_ERR_HIP;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return LSTM_DYN_ERR_HIP;
+    if (hipDeviceGetAttribute(&wclk_khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess)
+        return LSTM_DYN_ERR_HIP;
+    rc = lstm_dyn_plan(B, D, H, T, dtype, mode, cus, &plan);
+    if (rc != LSTM_DYN_OK) return rc;
+    const int bf16 = dtype == LSTM_DYN_BF16;
+    if (mode == LSTM_DYN_PERSISTENT) {
+        const int per_cu =
+            persistent_blocks_per_cu(bf16, plan.mt, plan.kswmax, plan.nstate, plan.lds_bytes);
+        if (per_cu < 1 || plan.groups > per_cu * cus) return LSTM_DYN_ERR_UNSUPPORTED;
+    }
+    lstm_dyn* h = new (std::nothrow) lstm_dyn();
+    if (!h) return LSTM_DYN_ERR_NOMEM;
+    h->B = B; h->D = D; h->H = H; h->T = T; h->dtype = dtype; h->mode = mode;
+    h->device = dev;
+    h->num_cus = cus;
+    h->plan = plan;
+    h->dims = Dims{B, D, H, T, bf16, plan.hpad, plan.bpad};
+    const Layout L = layout_of(B, H, T, bf16, mode, plan.bpad, plan.hpad, plan.groups);
+    if (hipMalloc(&h->block, (size_t)L.total) != hipSuccess) {
+        (void)hipGetLastError();
+        delete h;
+        return LSTM_DYN_ERR_NOMEM;
+    }
+    char* base = static_cast<char*>(h->block);
+    h->ws.meta = reinterpret_cast<Meta*>(base + L.meta);
+    h->ws.perm = reinterpret_cast<int32_t*>(base + L.perm);
+    h->ws.offsets = reinterpret_cast<int32_t*>(base + L.offsets);
+    h->ws.rowsrc = reinterpret_cast<int32_t*>(base + L.rowsrc);
+    h->ws.gx = reinterpret_cast<float*>(base + L.gx);
+    h->ws.hx = base + L.hx;
+    h->ws.flags = reinterpret_cast<unsigned*>(base + L.flags);
+    h->ws.z = mode == LSTM_DYN_PER_STEP ? reinterpret_cast<float*>(base + L.z) : nullptr;
+    // Zero the small tables and the operand buffer (its padding must stay zero).
+    if (hipMemset(base, 0, (size_t)L.gx) != hipSuccess ||
+        hipMemset(base + L.hx, 0, (size_t)(L.total - L.hx)) != hipSuccess) {
+        (void)hipFree(h->block);
+        delete h;
+        return LSTM_DYN_ERR_HIP;
+    }
+    if (hipHostMalloc(reinterpret_cast<void**>(&h->host_maxlen), sizeof(int32_t), hipHostMallocDefault) != hipSuccess) {
+        (void)hipFree(h->block);
+        delete h;
+        return LSTM_DYN_ERR_HIP;
+    }
+    h->epoch = 0;
+    h->timeout_ticks = (unsigned long long)(BARRIER_TIMEOUT_S * 1e3 * (double)wclk_khz);
+    const long long tiles = ((long long)B * T + 127) / 128 * ((4LL * H + 127) / 128);
+    h->inproj_grid = (int)(tiles < 4LL * cus ? tiles : 4LL * cus);
+    h->launches_last = 0;
+    h->last_stream = nullptr;
+    *out = h;
+    return LSTM_DYN_OK;
+}
+
+extern "C" int lstm_dyn_destroy(lstm_dyn_t* h) {
+    if (!h) return LSTM_DYN_OK;
+    int rc = LSTM_DYN_OK;
+    if (hipDeviceSynchronize() != hipSuccess) rc = LSTM_DYN_ERR_HIP;
+    if (h->block && hipFree(h->block) != hipSuccess) rc = LSTM_DYN_ERR_HIP;
+    if (h->host_maxlen && hipHostFree(h->host_maxlen) != hipSuccess) rc = LSTM_DYN_ERR_HIP;
+    delete h;
+    return rc;
+}
+
+extern "C" int lstm_dyn_forward(lstm_dyn_t* h, const void* x, const int32_t* lengths, const void* W,
+                                const void* U, const float* b, const float* h0, const float* c0,
+                                float* out_h, float* out_c, void* stream) {
+    if (!h) return LSTM_DYN_ERR_INVALID;
+    int rc = lstm_dyn_check_args(h->B, h->D, h->H, h->T, h->dtype, x, lengths, W, U, b, h0, c0,
+                                 out_h, out_c);
+    if (rc != LSTM_DYN_OK) return rc;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    h->last_stream = s;
+    h->launches_last = 0;
+    const Dims& d = h->dims;
+#define LD_CHECK(call)                                   \
+    do {                                                 \
+        if ((call) != hipSuccess) {                      \
+            (void)hipGetLastError();                     \
+            return LSTM_DYN_ERR_HIP;                     \
+        }                                                \
+    } while (0)
+
+    LD_CHECK(launch_prep(d, lengths, h->ws, s));
+    h->launches_last++;
+    if (h->mode == LSTM_DYN_PERSISTENT) {
+        if (h->epoch + 2u * (unsigned)(h->T + 1) > EPOCH_LIMIT) {
+            LD_CHECK(hipMemsetAsync(h->ws.flags, 0, sizeof(unsigned) * h->plan.groups, s));
+            h->epoch = 0;
+        }
+        LD_CHECK(launch_inproj(d, x, W, b, h->ws, h->inproj_grid, s));
+        h->launches_last++;
+        PersistentConfig pc{h->plan.mt,     h->plan.groups,    h->plan.ksw,
+                            h->plan.kswmax, h->plan.nstate,    h->plan.lds_bytes,
+                            h->epoch,       h->timeout_ticks};
+        LD_CHECK(launch_persistent(d, pc, U, h0, c0, out_h, out_c, h->ws, s));
+        h->launches_last++;
+        h->epoch += (unsigned)(h->T + 1);
+        return LSTM_DYN_OK;
+    }
+    // Per-step comparison path.
+    LD_CHECK(launch_step_init(d, h0, c0, out_h, out_c, h->ws, s));
+    h->launches_last++;
+    LD_CHECK(launch_inproj(d, x, W, b, h->ws, h->inproj_grid, s));
+    h->launches_last++;
+    LD_CHECK(hipMemcpyAsync(h->host_maxlen, &h->ws.meta->max_len, sizeof(int32_t),
+                            hipMemcpyDeviceToHost, s));
+    LD_CHECK(hipStreamSynchronize(s));
+    const int max_len = *h->host_maxlen;
+    for (int t = 0; t < max_len; ++t) {
+        LD_CHECK(launch_step_gemm(d, t, U, h->ws, s));
+        LD_CHECK(launch_step_gates(d, t, out_h, out_c, h->ws, s));
+        h->launches_last += 2;
+    }
+#undef LD_CHECK
+    return LSTM_DYN_OK;
+}
+
+extern "C" int lstm_dyn_query(lstm_dyn_t* h, int what, long long* value) {
+    if (!h || !value) return LSTM_DYN_ERR_INVALID;
+    switch (what) {
+        case LSTM_DYN_Q_LAUNCHES_PER_FORWARD: *value = h->launches_last; return LSTM_DYN_OK;
+        case LSTM_DYN_Q_GROUPS: *value = h->plan.groups; return LSTM_DYN_OK;
+        case LSTM_DYN_Q_WORKSPACE_BYTES: *value = h->plan.workspace_bytes; return LSTM_DYN_OK;
+        case LSTM_DYN_Q_LAST_STATUS:
+        case LSTM_DYN_Q_STEPS_EXECUTED:
+        case LSTM_DYN_Q_TOTAL_ROWS: {
+            if (hipStreamSynchronize(h->last_stream) != hipSuccess) return LSTM_DYN_ERR_HIP;
+            Meta m;
+            if (hipMemcpy(&m, h->ws.meta, sizeof(Meta), hipMemcpyDeviceToHost) != hipSuccess)
+                return LSTM_DYN_ERR_HIP;
+            if (what == LSTM_DYN_Q_STEPS_EXECUTED) *value = m.max_len;
+            else if (what == LSTM_DYN_Q_TOTAL_ROWS) *value = m.total_rows;
+            else if (m.status & STATUS_TIMEOUT) *value = LSTM_DYN_ERR_TIMEOUT;
+            else if (m.status & STATUS_BAD_LENGTHS) *value = LSTM_DYN_ERR_BAD_LENGTHS;
+            else *value = LSTM_DYN_OK;
+            return LSTM_DYN_OK;
+        }
+        default: return LSTM_DYN_ERR_INVALID;
+    }
+}

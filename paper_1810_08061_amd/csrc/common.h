@@ -1,0 +1,91 @@
+// common.h -- types, workspace layout and device helpers shared by the
+// kernels of the variable-length LSTM loop (gfx950 / CDNA4).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ldyn {
+
+// ---------------------------------------------------------------------------
+// Workspace written on the device by the preparation kernel.
+struct Meta {
+    int32_t max_len;     // loop bound: largest (clamped) length
+    int32_t total_rows;  // sum of (clamped) lengths = rows of the compact input projection
+    int32_t status;      // bit 0: a length was clamped; bit 1: a barrier wait timed out
+    int32_t pad;
+};
+constexpr int32_t STATUS_BAD_LENGTHS = 1;
+constexpr int32_t STATUS_TIMEOUT = 2;
+
+// Gate-interleaved column order used by the input projection Gx and by the
+// recurrent tiles: column c' = 4u + g holds gate g in (i, f, g, o) of hidden
+// unit u, which is column g*H + u of W, U and b.  A lane that owns c' = 4u..4u+3
+// of one row then holds all four gates of (row, u).
+__host__ __device__ inline int gate_col(int cprime, int H) { return (cprime & 3) * H + (cprime >> 2); }
+
+// ---------------------------------------------------------------------------
+// Element types.  MFMA 16x16xK fragments: lane l holds operand row/column
+// (l & 15) and the K slice [(l >> 4) * KPL, (l >> 4) * KPL + KPL); the 16x16
+// fp32 result gives lane l rows 4*(l >> 4) + j (j = 0..3) of column (l & 15).
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+struct EltF32 {
+    using store_t = float;
+    using frag_t = float;
+    static constexpr int KSTEP = 4;  // K per MFMA
+    static constexpr int KPL = 1;    // K values per lane
+    __device__ static inline f32x4_t mfma(frag_t a, frag_t b, f32x4_t c) {
+        return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+    }
+    __device__ static inline frag_t zero() { return 0.0f; }
+    __device__ static inline store_t from_f32(float v) { return v; }
+    __device__ static inline float to_f32(store_t v) { return v; }
+    // Load KPL consecutive elements at p (aligned to KPL elements).
+    __device__ static inline frag_t load(const store_t* p) { return *p; }
+};
+
+struct EltBF16 {
+    using store_t = __bf16;
+    using frag_t = bf16x8_t;
+    static constexpr int KSTEP = 32;
+    static constexpr int KPL = 8;
+    __device__ static inline f32x4_t mfma(frag_t a, frag_t b, f32x4_t c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+    }
+    __device__ static inline frag_t zero() {
+        frag_t z;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) z[i] = (__bf16)0.0f;
+        return z;
+    }
+    __device__ static inline store_t from_f32(float v) { return (__bf16)v; }
+    __device__ static inline float to_f32(store_t v) { return (float)v; }
+    __device__ static inline frag_t load(const store_t* p) {
+        return *reinterpret_cast<const frag_t*>(p);
+    }
+};
+
+// ---------------------------------------------------------------------------
+// Gate non-linearities in fp32 from the hardware exp2 and reciprocal.
+// sigmoid(0) and tanh(0) come out exactly 1/2 and 0.
+__device__ inline float rcp_f(float x) { return __builtin_amdgcn_rcpf(x); }
+__device__ inline float sigmoid_f(float z) { return rcp_f(1.0f + __expf(-z)); }
+__device__ inline float tanh_f(float z) {
+    // tanh|z| = (1 - e) / (1 + e) with e = exp(-2|z|) in (0, 1]: no overflow.
+    const float e = __expf(-2.0f * fabsf(z));
+    return copysignf((1.0f - e) * rcp_f(1.0f + e), z);
+}
+
+// One LSTM cell update from the four pre-activations of a (row, unit).
+__device__ inline void lstm_cell(f32x4_t z, float& c, float& h) {
+    const float ig = sigmoid_f(z[0]);
+    const float fg = sigmoid_f(z[1]);
+    const float gg = tanh_f(z[2]);
+    const float og = sigmoid_f(z[3]);
+    c = fg * c + ig * gg;
+    h = og * tanh_f(c);
+}
+
+}  // namespace ldyn

@@ -1,0 +1,59 @@
+// launch.h -- host-side launchers of the kernels (one translation unit per
+// kernel family) and the device workspace they share.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.h"
+
+namespace ldyn {
+
+// Device workspace of one handle (all pointers into one hipMalloc block).
+struct Workspace {
+    Meta* meta;         // loop bound, row count, status
+    int32_t* perm;      // [B] slot -> batch index; slots sorted by length, descending (stable)
+    int32_t* offsets;   // [T_max + 1] first compact row of step t; offsets[t+1]-offsets[t] = active rows
+    int32_t* rowsrc;    // [B * T_max] compact row -> b * T_max + t
+    float* gx;          // [B * T_max][4H] x W + b for valid (b, t), gate-interleaved columns
+    void* hx;           // [2][bpad][hpad] recurrent operand (dtype), slot order; padding stays zero
+    unsigned* flags;    // [groups] grid-barrier arrival values
+    float* z;           // [bpad][4H] per-step pre-activations (per-step mode only)
+};
+
+struct Dims {
+    int B, D, H, T;     // batch, input width, hidden width, padded time extent
+    int bf16;           // 1: x, W, U are bf16; 0: fp32
+    int hpad, bpad;     // padded hidden width / batch rows of the operand buffer
+};
+
+// Preparation: clamp and validate lengths, stable descending length sort,
+// per-step active counts and compact row offsets, compact row sources.
+hipError_t launch_prep(const Dims& d, const int32_t* lengths, const Workspace& ws, hipStream_t s);
+
+// Input projection over all valid (b, t): gx[r][c'] = x[rowsrc[r]] . W[:, col(c')] + b[col(c')].
+hipError_t launch_inproj(const Dims& d, const void* x, const void* W, const float* b,
+                         const Workspace& ws, int grid, hipStream_t s);
+
+// Persistent on-device time loop.
+struct PersistentConfig {
+    int mt, groups, ksw, kswmax, nst, lds_bytes;
+    unsigned epoch;               // barrier values of this forward start above epoch
+    unsigned long long timeout_ticks;  // barrier wait bound in wall-clock ticks
+};
+hipError_t launch_persistent(const Dims& d, const PersistentConfig& pc, const void* U,
+                             const float* h0, const float* c0, float* out_h, float* out_c,
+                             const Workspace& ws, hipStream_t s);
+// Occupancy check for the co-resident grid; returns blocks per CU (0 if none).
+int persistent_blocks_per_cu(int bf16, int mt, int kswmax, int nst, int lds_bytes);
+// Smallest compiled variant with K-step capacity >= ksw and state capacity >= nstate.
+bool persistent_pick_variant(int bf16, int mt, int ksw, int nstate, int* kswmax, int* nst);
+
+// Per-step comparison path.
+hipError_t launch_step_init(const Dims& d, const float* h0, const float* c0, float* out_h,
+                            float* out_c, const Workspace& ws, hipStream_t s);
+hipError_t launch_step_gemm(const Dims& d, int t, const void* U, const Workspace& ws, hipStream_t s);
+hipError_t launch_step_gates(const Dims& d, int t, float* out_h, float* out_c, const Workspace& ws,
+                             hipStream_t s);
+
+}  // namespace ldyn

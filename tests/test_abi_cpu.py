@@ -1,0 +1,122 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports
+every function include/lstm_dyn.h declares, plans launches as intended and
+rejects bad arguments before touching the device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_1810_08061_amd as ld
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    with open(os.path.join(ROOT, "include", "lstm_dyn.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"^\s*(?:int|const char\*)\s+(lstm_dyn_\w+)\s*\(", text, re.M)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = _declared_functions()
+    assert {"lstm_dyn_create", "lstm_dyn_forward", "lstm_dyn_destroy"} <= set(names)
+    lib = ctypes.CDLL(ld.library_path())
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_strerror_covers_codes():
+    for code in range(7):
+        assert ld.lstm_dyn_strerror(code) not in ("", "unknown status")
+    assert ld.lstm_dyn_strerror(99) == "unknown status"
+
+
+@pytest.mark.parametrize("B,D,H,T,dt,mt,groups,ksw", [
+    (4, 16, 32, 20, ld.F32, 8, 1, 2),          # tiny: one workgroup, no grid barrier
+    (32, 256, 256, 100, ld.F32, 1, 64, 16),
+    (64, 512, 512, 200, ld.BF16, 1, 128, 4),
+    (128, 1024, 1024, 500, ld.BF16, 1, 256, 8),
+    (256, 1024, 2048, 1000, ld.BF16, 2, 256, 16),
+])
+def test_plan_of_workloads(B, D, H, T, dt, mt, groups, ksw):
+    p = ld.lstm_dyn_plan(B, D, H, T, dt, ld.PERSISTENT, 256)
+    assert (p["mt"], p["groups"], p["ksw"]) == (mt, groups, ksw)
+    assert p["groups"] <= 256 and p["groups"] * 4 * p["mt"] >= H
+    assert p["kswmax"] >= p["ksw"]
+    kstep = 32 if dt == ld.BF16 else 4
+    assert p["hpad"] == p["ksw"] * kstep * 4 and p["hpad"] >= H
+    assert p["bpad"] % 16 == 0 and p["bpad"] >= B
+    assert p["nstate"] * 4 >= ((B + 15) // 16) * p["mt"]
+    assert p["lds_bytes"] <= 160 * 1024
+    gx = 16 * H * B * T
+    assert p["workspace_bytes"] >= gx
+
+
+@pytest.mark.parametrize("args", [
+    (0, 1, 1, 1, 0, 0), (1, 0, 1, 1, 0, 0), (1, 1, 0, 1, 0, 0), (1, 1, 1, 0, 0, 0),
+    (1, 1, 1, 1, 2, 0), (1, 1, 1, 1, 0, 2),
+])
+def test_plan_rejects_bad_sizes(args):
+    with pytest.raises(ld.LstmDynError) as e:
+        ld.lstm_dyn_plan(*args, 256)
+    assert e.value.code == ld.ERR_INVALID
+
+
+def test_plan_unsupported_sizes():
+    with pytest.raises(ld.LstmDynError) as e:   # fp32 H=4096 needs more K-steps than any variant
+        ld.lstm_dyn_plan(8, 8, 4096, 8, ld.F32, ld.PERSISTENT, 256)
+    assert e.value.code == ld.ERR_UNSUPPORTED
+    # the per-step path has no register-resident state limit
+    ld.lstm_dyn_plan(8, 8, 1024, 8, ld.F32, ld.PER_STEP, 256)
+
+
+def test_create_rejects_bad_sizes_without_device():
+    with pytest.raises(ld.LstmDynError) as e:
+        ld.lstm_dyn_create(0, 4, 4, 4, ld.F32, ld.PERSISTENT)
+    assert e.value.code == ld.ERR_INVALID
+
+
+def _ptrs(B, D, H, T, e):
+    """Disjoint fake device addresses, 256-byte aligned (never dereferenced)."""
+    sizes = [B * T * D * e, 4 * B, D * 4 * H * e, H * 4 * H * e, 16 * H, 4 * B * H, 4 * B * H,
+             4 * B * H, 4 * B * H]
+    out, at = [], 1 << 20
+    for s in sizes:
+        out.append(at)
+        at += (s + 255) // 256 * 256 + 256
+    return out
+
+
+def test_check_args():
+    B, D, H, T = 3, 5, 7, 4
+    p = _ptrs(B, D, H, T, 4)
+    assert ld.lstm_dyn_check_args(B, D, H, T, ld.F32, *p) == ld.OK
+    for i in range(9):                           # any NULL pointer
+        q = list(p)
+        q[i] = 0
+        assert ld.lstm_dyn_check_args(B, D, H, T, ld.F32, *q) == ld.ERR_INVALID
+    for i in (0, 2, 3):                          # x, W, U need 16-byte alignment
+        q = list(p)
+        q[i] += 4
+        assert ld.lstm_dyn_check_args(B, D, H, T, ld.F32, *q) == ld.ERR_INVALID
+    q = list(p)
+    q[5] += 2                                    # h0 needs 4-byte alignment
+    assert ld.lstm_dyn_check_args(B, D, H, T, ld.F32, *q) == ld.ERR_INVALID
+    # exact in-place state update is allowed
+    q = list(p)
+    q[7], q[8] = q[5], q[6]
+    assert ld.lstm_dyn_check_args(B, D, H, T, ld.F32, *q) == ld.OK
+    # partial overlap of an output with an input is not
+    q = list(p)
+    q[7] = q[5] + 4
+    assert ld.lstm_dyn_check_args(B, D, H, T, ld.F32, *q) == ld.ERR_INVALID
+    q = list(p)
+    q[8] = q[0]                                  # out_c on top of x
+    assert ld.lstm_dyn_check_args(B, D, H, T, ld.F32, *q) == ld.ERR_INVALID
+    q = list(p)
+    q[8] = q[7]                                  # out_c == out_h
+    assert ld.lstm_dyn_check_args(B, D, H, T, ld.F32, *q) == ld.ERR_INVALID
+    q = list(p)
+    q[7] = q[6]                                  # out_h on c0
+    assert ld.lstm_dyn_check_args(B, D, H, T, ld.F32, *q) == ld.ERR_INVALID
