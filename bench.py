@@ -1,0 +1,221 @@
+"""Throughput of the variable-length LSTM time loop on one MI355X.
+
+python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
+
+A step is one forward of the whole path (length preparation, input
+projection over all valid time steps, on-device time loop) on one batch of the
+seeded synthetic workload, with inputs resident in HBM.  W untimed forwards,
+then exactly K timed forwards between device synchronisations.  Prints one
+JSON line.
+
+value        valid seq*steps/s = sum of lengths / mean forward time
+roofline     the loop kernel (the dominant kernel): algorithmic recurrent
+             FLOPs (8 H^2 per valid seq*step) per launch / its mean launch
+             duration from HIP events recorded by the library on the
+             forward's stream, against the dense bf16 (or fp32) MFMA peak
+cpu_baseline the fp64 oracle on a bounded sample of the same workload, timed
+             on this host's cores
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import workloads  # noqa: E402
+
+PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}  # MI355X dense MFMA
+HBM_PEAK_GBS = 8000.0
+METRIC = "valid seq·steps/sec + MFMA util; speedup of on-device loop vs per-step launch"
+DEFAULT_WORKLOAD = "large2048_bf16"
+
+
+def _log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def to_device(inp, torch):
+    if inp.dtype == workloads.BF16:
+        conv = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda().view(torch.bfloat16)
+    else:
+        conv = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+    f32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+    return (conv(inp.x), torch.from_numpy(np.ascontiguousarray(inp.lengths, np.int32)).cuda(),
+            conv(inp.W), conv(inp.U), f32(inp.b), f32(inp.h0), f32(inp.c0))
+
+
+def time_forwards(torch, ld, model, dev, steps, warmup, out):
+    """Mean/std forward time (s) over `steps` forwards, and mean per-phase times."""
+    for _ in range(warmup):
+        model.forward(*dev, out_h=out[0], out_c=out[1])
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    per, loop_ns, inproj_ns, prep_ns = [], [], [], []
+    for _ in range(steps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        model.forward(*dev, out_h=out[0], out_c=out[1])
+        e1.record(stream)
+        e1.synchronize()
+        per.append(e0.elapsed_time(e1) * 1e-3)
+        loop_ns.append(model.query(ld.Q_TIME_LOOP_NS))
+        inproj_ns.append(model.query(ld.Q_TIME_INPROJ_NS))
+        prep_ns.append(model.query(ld.Q_TIME_PREP_NS))
+    torch.cuda.synchronize()
+    return (float(np.mean(per)), float(np.std(per)), float(np.mean(loop_ns)) * 1e-9,
+            float(np.mean(inproj_ns)) * 1e-9, float(np.mean(prep_ns)) * 1e-9)
+
+
+def time_whole(torch, model, dev, steps, warmup, out):
+    """Wall time of exactly `steps` back-to-back forwards (host clock, synchronised)."""
+    for _ in range(warmup):
+        model.forward(*dev, out_h=out[0], out_c=out[1])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        model.forward(*dev, out_h=out[0], out_c=out[1])
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) / steps
+
+
+def cpu_baseline(inp, budget_rows_steps):
+    """Time the fp64 oracle on the longest-first prefix of rows whose lengths
+    sum to about `budget_rows_steps` (all host cores)."""
+    import oracle
+    order = np.argsort(-inp.lengths, kind="stable")
+    L = inp.lengths[order]
+    # take rows from the middle of the length distribution so the sample's
+    # per-step row count resembles the workload's
+    mid = len(order) // 4
+    rows, total = [], 0
+    for r in list(order[mid:]) + list(order[:mid]):
+        if total >= budget_rows_steps:
+            break
+        rows.append(int(r))
+        total += int(inp.lengths[r])
+    threads = oracle.max_threads()
+    t0 = time.perf_counter()
+    oracle.forward_inputs(inp, rows=rows, threads=threads)
+    dt = time.perf_counter() - t0
+    del L
+    return {"value": total / dt, "unit": "seq·steps/s", "cores": threads, "kind": "oracle",
+            "sample": f"{len(rows)} of {inp.B} rows of the workload (sum of lengths {total}), "
+                      f"fp64 C oracle, OpenMP over rows, {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=workloads.ORDER)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--cpu-budget", type=int, default=3000,
+                    help="seq*steps of the oracle sample (about 10-30 s on a host)")
+    ap.add_argument("--per-step-reps", type=int, default=3)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(the batch would shard across GPUs with no exchange inside the loop).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_1810_08061_amd as ld
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    w = workloads.WORKLOADS[args.workload]
+    _log(f"generating {args.workload}")
+    inp = workloads.workload_inputs(args.workload)
+    sumL = int(inp.lengths.sum())
+    max_len = int(inp.lengths.max())
+    dev = to_device(inp, torch)
+    out = (torch.empty((w.B, w.H), device="cuda"), torch.empty((w.B, w.H), device="cuda"))
+
+    _log("persistent path")
+    model = ld.LstmDyn(w.B, w.D, w.H, w.T, w.dtype, "persistent")
+    model.set_option(ld.OPT_TIMING, 1)
+    t_fwd, t_std, t_loop, t_inproj, t_prep = time_forwards(torch, ld, model, dev, args.steps,
+                                                           args.warmup, out)
+    assert model.query(ld.Q_LAST_STATUS) == ld.OK
+    launches = model.query(ld.Q_LAUNCHES_PER_FORWARD)
+    groups = model.query(ld.Q_GROUPS)
+    model.set_option(ld.OPT_TIMING, 0)
+    t_wall = time_whole(torch, model, dev, args.steps, 1, out)
+
+    _log("per-step path")
+    ps = ld.LstmDyn(w.B, w.D, w.H, w.T, w.dtype, "per_step")
+    t_ps = time_whole(torch, ps, dev, args.per_step_reps, 1, out)
+    ps_launches = ps.query(ld.Q_LAUNCHES_PER_FORWARD)
+    ps.close()
+
+    # smallest workload: where the per-step launch overhead dominates
+    tw = workloads.WORKLOADS["tiny_f32"]
+    tin = workloads.workload_inputs("tiny_f32")
+    tdev = to_device(tin, torch)
+    tout = (torch.empty((tw.B, tw.H), device="cuda"), torch.empty((tw.B, tw.H), device="cuda"))
+    tm = ld.LstmDyn(tw.B, tw.D, tw.H, tw.T, tw.dtype, "persistent")
+    t_tiny = time_whole(torch, tm, tdev, 200, 20, tout)
+    tps = ld.LstmDyn(tw.B, tw.D, tw.H, tw.T, tw.dtype, "per_step")
+    t_tiny_ps = time_whole(torch, tps, tdev, 50, 5, tout)
+    tm.close()
+    tps.close()
+
+    dt = w.dtype
+    flops_fwd = 8.0 * w.H * (w.D + w.H) * sumL
+    flops_rec = 8.0 * w.H * w.H * sumL
+    flops_in = 8.0 * w.H * w.D * sumL
+    e = 2 if dt == workloads.BF16 else 4
+    bytes_alg = sumL * w.D * e + 4 * w.H * (w.D + w.H) * e + 16 * w.H + 16 * w.B * w.H + 4 * w.B
+    peak = PEAK_TFLOPS[dt]
+    achieved = flops_rec / t_loop / 1e12
+    line = {
+        "metric": METRIC,
+        "value": sumL / t_fwd,
+        "unit": "seq·steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": t_fwd * 1e3,
+        "ms_per_step_std": t_std * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dt,
+        "data": "synthetic (seeded generator; random-init weights)",
+        "config": {"workload": args.workload, "B": w.B, "D": w.D, "H": w.H, "T_max": w.T,
+                   "lengths": list(map(str, w.lengths)), "sum_lengths": sumL, "max_len": max_len,
+                   "parallelism": "none (1 GPU)", "persistent_groups": groups},
+        "roofline": {"bound": "mfma", "kernel": "persistent time loop (recurrent h U, gates)",
+                     "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                     "frac": achieved / peak, "traffic": None},
+        "mfma_frac_forward": flops_fwd / t_fwd / 1e12 / peak,
+        "hbm_frac_forward": bytes_alg / t_fwd / 1e9 / HBM_PEAK_GBS,
+        "phases_ms": {"prep": t_prep * 1e3, "input_projection": t_inproj * 1e3,
+                      "loop": t_loop * 1e3},
+        "input_projection_tflops": flops_in / t_inproj / 1e12,
+        "launches_per_forward": launches,
+        "wall_ms_per_step": t_wall * 1e3,
+        "per_step_path": {"ms_per_step": t_ps * 1e3, "launches_per_forward": ps_launches,
+                          "speedup_of_persistent": t_ps / t_wall},
+        "tiny_f32": {"persistent_us": t_tiny * 1e6, "per_step_us": t_tiny_ps * 1e6,
+                     "speedup_of_persistent": t_tiny_ps / t_tiny},
+    }
+    if not args.no_cpu:
+        _log("cpu baseline (oracle)")
+        line["cpu_baseline"] = cpu_baseline(inp, args.cpu_budget)
+    print(json.dumps(line), flush=True)
+    model.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -77,7 +77,17 @@ enum {
     LSTM_DYN_Q_LAUNCHES_PER_FORWARD = 2, /* kernel launches issued by the last forward */
     LSTM_DYN_Q_GROUPS = 3,             /* workgroups of the persistent kernel */
     LSTM_DYN_Q_WORKSPACE_BYTES = 4,    /* device workspace owned by the handle */
-    LSTM_DYN_Q_TOTAL_ROWS = 5          /* sum of the (clamped) lengths of the last forward (synchronises) */
+    LSTM_DYN_Q_TOTAL_ROWS = 5,         /* sum of the (clamped) lengths of the last forward (synchronises) */
+    LSTM_DYN_Q_TIME_PREP_NS = 6,       /* with LSTM_DYN_OPT_TIMING: device time of the length
+                                          preparation kernel in the last forward (synchronises) */
+    LSTM_DYN_Q_TIME_INPROJ_NS = 7,     /* ... of the input projection GEMM */
+    LSTM_DYN_Q_TIME_LOOP_NS = 8        /* ... of the time loop (the persistent kernel, or the
+                                          per-step path's host loop of launches) */
+};
+
+/* lstm_dyn_set_option selectors. */
+enum {
+    LSTM_DYN_OPT_TIMING = 0 /* 1: record HIP events on the forward's stream around each phase */
 };
 
 /* Launch plan of a handle: pure host arithmetic, no device access. */
@@ -85,7 +95,7 @@ typedef struct {
     int mt;             /* 16-column gate tiles per workgroup (4 hidden units each) */
     int groups;         /* workgroups of the persistent kernel (at most one per CU) */
     int ksw;            /* MFMA K-steps per wave over the hidden width */
-    int kswmax;         /* K-step capacity of the kernel variant that will run */
+    int kw;             /* waves per workgroup (they split the hidden width) */
     int hpad;           /* hidden width padded to the recurrent MFMA's K granularity */
     int bpad;           /* batch padded to 16 rows */
     int lds_bytes;      /* dynamic LDS of the persistent kernel */
@@ -121,6 +131,9 @@ int lstm_dyn_destroy(lstm_dyn_t* h);
 
 /* Read a property of the handle or of its last forward (see LSTM_DYN_Q_*). */
 int lstm_dyn_query(lstm_dyn_t* h, int what, long long* value);
+
+/* Set a handle option (see LSTM_DYN_OPT_*).  Returns LSTM_DYN_OK, ERR_INVALID or ERR_HIP. */
+int lstm_dyn_set_option(lstm_dyn_t* h, int option, long long value);
 
 /* Static description of a status code (never NULL). */
 const char* lstm_dyn_strerror(int status);

@@ -17,7 +17,7 @@ import os
 __all__ = [
     "F32", "BF16", "PERSISTENT", "PER_STEP", "LstmDynError", "LstmDyn", "library_path",
     "lstm_dyn_create", "lstm_dyn_forward", "lstm_dyn_destroy", "lstm_dyn_query",
-    "lstm_dyn_strerror", "lstm_dyn_plan", "lstm_dyn_check_args",
+    "lstm_dyn_strerror", "lstm_dyn_plan", "lstm_dyn_check_args", "lstm_dyn_set_option",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -27,7 +27,8 @@ F32, BF16 = 0, 1
 PERSISTENT, PER_STEP = 0, 1
 OK, ERR_INVALID, ERR_HIP, ERR_NOMEM, ERR_UNSUPPORTED, ERR_BAD_LENGTHS, ERR_TIMEOUT = range(7)
 Q_LAST_STATUS, Q_STEPS_EXECUTED, Q_LAUNCHES_PER_FORWARD, Q_GROUPS, Q_WORKSPACE_BYTES, \
-    Q_TOTAL_ROWS = range(6)
+    Q_TOTAL_ROWS, Q_TIME_PREP_NS, Q_TIME_INPROJ_NS, Q_TIME_LOOP_NS = range(9)
+OPT_TIMING = 0
 
 _DTYPES = {"f32": F32, "fp32": F32, "float32": F32, "bf16": BF16, "bfloat16": BF16}
 _MODES = {"persistent": PERSISTENT, "per_step": PER_STEP}
@@ -41,7 +42,7 @@ class LstmDynError(RuntimeError):
 
 class _Plan(ctypes.Structure):
     _fields_ = [("mt", ctypes.c_int), ("groups", ctypes.c_int), ("ksw", ctypes.c_int),
-                ("kswmax", ctypes.c_int), ("hpad", ctypes.c_int), ("bpad", ctypes.c_int),
+                ("kw", ctypes.c_int), ("hpad", ctypes.c_int), ("bpad", ctypes.c_int),
                 ("lds_bytes", ctypes.c_int), ("nstate", ctypes.c_int),
                 ("workspace_bytes", ctypes.c_longlong)]
 
@@ -70,6 +71,8 @@ def _load():
     lib.lstm_dyn_destroy.restype = I
     lib.lstm_dyn_query.argtypes = [P, I, ctypes.POINTER(LL)]
     lib.lstm_dyn_query.restype = I
+    lib.lstm_dyn_set_option.argtypes = [P, I, LL]
+    lib.lstm_dyn_set_option.restype = I
     lib.lstm_dyn_strerror.argtypes = [I]
     lib.lstm_dyn_strerror.restype = ctypes.c_char_p
     lib.lstm_dyn_plan.argtypes = [I] * 7 + [ctypes.POINTER(_Plan)]
@@ -113,6 +116,12 @@ def lstm_dyn_query(handle: int, what: int) -> int:
     if rc != OK:
         raise LstmDynError(rc, "lstm_dyn_query")
     return int(v.value)
+
+
+def lstm_dyn_set_option(handle: int, option: int, value: int) -> None:
+    rc = _load().lstm_dyn_set_option(handle, option, value)
+    if rc != OK:
+        raise LstmDynError(rc, "lstm_dyn_set_option")
 
 
 def lstm_dyn_plan(B: int, D: int, H: int, T_max: int, dtype: int, mode: int, num_cus: int) -> dict:
@@ -186,6 +195,9 @@ class LstmDyn:
 
     def query(self, what: int) -> int:
         return lstm_dyn_query(self.handle, what)
+
+    def set_option(self, option: int, value: int) -> None:
+        lstm_dyn_set_option(self.handle, option, value)
 
     def close(self):
         if getattr(self, "handle", None):

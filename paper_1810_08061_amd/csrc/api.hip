@@ -17,29 +17,27 @@ struct lstm_dyn {
     Workspace ws;
     void* block;               // the one device allocation behind ws
     int32_t* host_maxlen;      // pinned host word for the per-step path's loop-bound copy
-    unsigned epoch;            // barrier values of the next forward start above this
     unsigned long long timeout_ticks;
     int inproj_grid;
     long long launches_last;
     hipStream_t last_stream;
+    int timing;                // record phase events on the forward's stream
+    hipEvent_t ev[4];          // before prep, after prep, after input projection, after loop
 };
 
 namespace {
 
-constexpr int KW = 4;             // waves per persistent workgroup (split K)
-constexpr int LDS_TILES = 32;     // partial tiles per wave in LDS
 constexpr int PREP_MAX_B = 8192;
-constexpr unsigned EPOCH_LIMIT = 0xF0000000u;
 constexpr double BARRIER_TIMEOUT_S = 5.0;
 
 long long align_up(long long v, long long a) { return (v + a - 1) / a * a; }
 
 
 struct Layout {
-    long long meta, perm, offsets, rowsrc, gx, hx, flags, z, total;
+    long long meta, perm, offsets, rowsrc, gx, hx, bar, z, total;
 };
 
-Layout layout_of(int B, int H, int T, int bf16, int mode, int bpad, int hpad, int groups) {
+Layout layout_of(int B, int H, int T, int bf16, int mode, int bpad, int hpad) {
     Layout L{};
     long long o = 0;
     auto take = [&](long long bytes) {
@@ -53,7 +51,7 @@ Layout layout_of(int B, int H, int T, int bf16, int mode, int bpad, int hpad, in
     L.rowsrc = take(4LL * B * T);
     L.gx = take(16LL * H * B * T);
     L.hx = take(2LL * bpad * hpad * (bf16 ? 2 : 4));
-    L.flags = take(4LL * groups);
+    L.bar = take(4LL * BAR_WORDS);
     L.z = take(mode == LSTM_DYN_PER_STEP ? 16LL * H * bpad : 0);
     L.total = o;
     return L;
@@ -90,36 +88,34 @@ extern "C" int lstm_dyn_plan(int B, int D, int H, int T, int dtype, int mode, in
         return LSTM_DYN_ERR_UNSUPPORTED;
     const int bf16 = dtype == LSTM_DYN_BF16;
     const int kstep = bf16 ? 32 : 4;
-    const int ksw = (H + kstep * KW - 1) / (kstep * KW);
     const int ntmax = (B + 15) / 16;
-    // Gate tiles per workgroup: one workgroup for H <= 32 (no grid barrier),
-    // otherwise the fewest units per workgroup that fit one workgroup per CU.
-    int mt = 0, kswmax = 0, nst = 0, nstate = 0;
-    for (int cand : {8, 1, 2}) {
-        if (cand == 8 && H > 32) continue;
-        const int groups = (H + 4 * cand - 1) / (4 * cand);
-        if (groups > num_cus) continue;
-        nstate = (ntmax * cand + KW - 1) / KW;
-        if (mode == LSTM_DYN_PER_STEP) {
-            mt = cand;
-            break;
-        }
-        if (persistent_pick_variant(bf16, cand, ksw, nstate, &kswmax, &nst)) {
-            mt = cand;
-            break;
-        }
+    // Workgroup shape: 4*mt hidden units per workgroup (one workgroup per CU),
+    // kw waves splitting K = H into ksw MFMA K-steps each (a power of two; the
+    // operand buffer's padding columns are zero).
+    int mt = 1, kw = 4;
+    if (bf16 && H > 1024) {
+        mt = 2;
+        kw = 8;
     }
-    if (mt == 0) return LSTM_DYN_ERR_UNSUPPORTED;
+    const int groups = (H + 4 * mt - 1) / (4 * mt);
+    if (groups > num_cus) return LSTM_DYN_ERR_UNSUPPORTED;
+    const int kneed = (H + kstep * kw - 1) / (kstep * kw);
+    int ksw = 1;
+    while (ksw < kneed) ksw *= 2;
+    const int nstate = (ntmax * mt + kw - 1) / kw;
+    int nst = nstate;
+    if (mode == LSTM_DYN_PERSISTENT && !persistent_pick_variant(bf16, mt, kw, ksw, nstate, &nst))
+        return LSTM_DYN_ERR_UNSUPPORTED;
     out->mt = mt;
-    out->groups = (H + 4 * mt - 1) / (4 * mt);
+    out->groups = groups;
     out->ksw = ksw;
-    out->kswmax = kswmax;
-    out->hpad = ksw * kstep * KW;
+    out->kw = kw;
+    out->hpad = ksw * kstep * kw;
     out->bpad = ntmax * 16;
-    out->lds_bytes = KW * LDS_TILES * 64 * 16;
+    out->lds_bytes = persistent_lds_bytes(bf16, mt, out->hpad);
     out->nstate = nst;
     out->workspace_bytes =
-        layout_of(B, H, T, bf16, mode, out->bpad, out->hpad, out->groups).total;
+        layout_of(B, H, T, bf16, mode, out->bpad, out->hpad).total;
     return LSTM_DYN_OK;
 }
 
@@ -163,8 +159,8 @@ extern "C" int lstm_dyn_create(lstm_dyn_t** out, int B, int D, int H, int T, int
     if (rc != LSTM_DYN_OK) return rc;
     const int bf16 = dtype == LSTM_DYN_BF16;
     if (mode == LSTM_DYN_PERSISTENT) {
-        const int per_cu =
-            persistent_blocks_per_cu(bf16, plan.mt, plan.kswmax, plan.nstate, plan.lds_bytes);
+        const int per_cu = persistent_blocks_per_cu(bf16, plan.mt, plan.ksw, plan.kw, plan.nstate,
+                                                    plan.lds_bytes);
         if (per_cu < 1 || plan.groups > per_cu * cus) return LSTM_DYN_ERR_UNSUPPORTED;
     }
     lstm_dyn* h = new (std::nothrow) lstm_dyn();
@@ -174,7 +170,7 @@ extern "C" int lstm_dyn_create(lstm_dyn_t** out, int B, int D, int H, int T, int
     h->num_cus = cus;
     h->plan = plan;
     h->dims = Dims{B, D, H, T, bf16, plan.hpad, plan.bpad};
-    const Layout L = layout_of(B, H, T, bf16, mode, plan.bpad, plan.hpad, plan.groups);
+    const Layout L = layout_of(B, H, T, bf16, mode, plan.bpad, plan.hpad);
     if (hipMalloc(&h->block, (size_t)L.total) != hipSuccess) {
         (void)hipGetLastError();
         delete h;
@@ -187,7 +183,7 @@ extern "C" int lstm_dyn_create(lstm_dyn_t** out, int B, int D, int H, int T, int
     h->ws.rowsrc = reinterpret_cast<int32_t*>(base + L.rowsrc);
     h->ws.gx = reinterpret_cast<float*>(base + L.gx);
     h->ws.hx = base + L.hx;
-    h->ws.flags = reinterpret_cast<unsigned*>(base + L.flags);
+    h->ws.bar = reinterpret_cast<unsigned*>(base + L.bar);
     h->ws.z = mode == LSTM_DYN_PER_STEP ? reinterpret_cast<float*>(base + L.z) : nullptr;
     // Zero the small tables and the operand buffer (its padding must stay zero).
     if (hipMemset(base, 0, (size_t)L.gx) != hipSuccess ||
@@ -201,14 +197,28 @@ extern "C" int lstm_dyn_create(lstm_dyn_t** out, int B, int D, int H, int T, int
         delete h;
         return LSTM_DYN_ERR_HIP;
     }
-    h->epoch = 0;
     h->timeout_ticks = (unsigned long long)(BARRIER_TIMEOUT_S * 1e3 * (double)wclk_khz);
     const long long tiles = ((long long)B * T + 127) / 128 * ((4LL * H + 127) / 128);
     h->inproj_grid = (int)(tiles < 4LL * cus ? tiles : 4LL * cus);
     h->launches_last = 0;
     h->last_stream = nullptr;
+    h->timing = 0;
+    for (auto& e : h->ev) e = nullptr;
     *out = h;
     return LSTM_DYN_OK;
+}
+
+extern "C" int lstm_dyn_set_option(lstm_dyn_t* h, int option, long long value) {
+    if (!h) return LSTM_DYN_ERR_INVALID;
+    if (option == LSTM_DYN_OPT_TIMING) {
+        if (value && !h->ev[0]) {
+            for (auto& e : h->ev)
+                if (hipEventCreate(&e) != hipSuccess) return LSTM_DYN_ERR_HIP;
+        }
+        h->timing = value ? 1 : 0;
+        return LSTM_DYN_OK;
+    }
+    return LSTM_DYN_ERR_INVALID;
 }
 
 extern "C" int lstm_dyn_destroy(lstm_dyn_t* h) {
@@ -216,6 +226,8 @@ extern "C" int lstm_dyn_destroy(lstm_dyn_t* h) {
     int rc = LSTM_DYN_OK;
     if (hipDeviceSynchronize() != hipSuccess) rc = LSTM_DYN_ERR_HIP;
     if (h->block && hipFree(h->block) != hipSuccess) rc = LSTM_DYN_ERR_HIP;
+    for (auto& e : h->ev)
+        if (e && hipEventDestroy(e) != hipSuccess) rc = LSTM_DYN_ERR_HIP;
     if (h->host_maxlen && hipHostFree(h->host_maxlen) != hipSuccess) rc = LSTM_DYN_ERR_HIP;
     delete h;
     return rc;
@@ -240,21 +252,20 @@ extern "C" int lstm_dyn_forward(lstm_dyn_t* h, const void* x, const int32_t* len
         }                                                \
     } while (0)
 
+    auto mark = [&](int i) { return h->timing ? hipEventRecord(h->ev[i], s) : hipSuccess; };
+    LD_CHECK(mark(0));
     LD_CHECK(launch_prep(d, lengths, h->ws, s));
     h->launches_last++;
+    LD_CHECK(mark(1));
     if (h->mode == LSTM_DYN_PERSISTENT) {
-        if (h->epoch + 2u * (unsigned)(h->T + 1) > EPOCH_LIMIT) {
-            LD_CHECK(hipMemsetAsync(h->ws.flags, 0, sizeof(unsigned) * h->plan.groups, s));
-            h->epoch = 0;
-        }
         LD_CHECK(launch_inproj(d, x, W, b, h->ws, h->inproj_grid, s));
         h->launches_last++;
-        PersistentConfig pc{h->plan.mt,     h->plan.groups,    h->plan.ksw,
-                            h->plan.kswmax, h->plan.nstate,    h->plan.lds_bytes,
-                            h->epoch,       h->timeout_ticks};
+        LD_CHECK(mark(2));
+        PersistentConfig pc{h->plan.mt, h->plan.groups, h->plan.ksw,       h->plan.kw,
+                            h->plan.nstate, h->plan.lds_bytes, h->timeout_ticks};
         LD_CHECK(launch_persistent(d, pc, U, h0, c0, out_h, out_c, h->ws, s));
         h->launches_last++;
-        h->epoch += (unsigned)(h->T + 1);
+        LD_CHECK(mark(3));
         return LSTM_DYN_OK;
     }
     // Per-step comparison path.
@@ -262,6 +273,7 @@ extern "C" int lstm_dyn_forward(lstm_dyn_t* h, const void* x, const int32_t* len
     h->launches_last++;
     LD_CHECK(launch_inproj(d, x, W, b, h->ws, h->inproj_grid, s));
     h->launches_last++;
+    LD_CHECK(mark(2));
     LD_CHECK(hipMemcpyAsync(h->host_maxlen, &h->ws.meta->max_len, sizeof(int32_t),
                             hipMemcpyDeviceToHost, s));
     LD_CHECK(hipStreamSynchronize(s));
@@ -271,6 +283,7 @@ extern "C" int lstm_dyn_forward(lstm_dyn_t* h, const void* x, const int32_t* len
         LD_CHECK(launch_step_gates(d, t, out_h, out_c, h->ws, s));
         h->launches_last += 2;
     }
+    LD_CHECK(mark(3));
 #undef LD_CHECK
     return LSTM_DYN_OK;
 }
@@ -293,6 +306,17 @@ extern "C" int lstm_dyn_query(lstm_dyn_t* h, int what, long long* value) {
             else if (m.status & STATUS_TIMEOUT) *value = LSTM_DYN_ERR_TIMEOUT;
             else if (m.status & STATUS_BAD_LENGTHS) *value = LSTM_DYN_ERR_BAD_LENGTHS;
             else *value = LSTM_DYN_OK;
+            return LSTM_DYN_OK;
+        }
+        case LSTM_DYN_Q_TIME_PREP_NS:
+        case LSTM_DYN_Q_TIME_INPROJ_NS:
+        case LSTM_DYN_Q_TIME_LOOP_NS: {
+            if (!h->timing) return LSTM_DYN_ERR_INVALID;
+            const int i = what - LSTM_DYN_Q_TIME_PREP_NS;
+            if (hipEventSynchronize(h->ev[i + 1]) != hipSuccess) return LSTM_DYN_ERR_HIP;
+            float ms = 0.f;
+            if (hipEventElapsedTime(&ms, h->ev[i], h->ev[i + 1]) != hipSuccess) return LSTM_DYN_ERR_HIP;
+            *value = (long long)(ms * 1e6);
             return LSTM_DYN_OK;
         }
         default: return LSTM_DYN_ERR_INVALID;

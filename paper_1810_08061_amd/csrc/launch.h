@@ -17,7 +17,7 @@ struct Workspace {
     int32_t* rowsrc;    // [B * T_max] compact row -> b * T_max + t
     float* gx;          // [B * T_max][4H] x W + b for valid (b, t), gate-interleaved columns
     void* hx;           // [2][bpad][hpad] recurrent operand (dtype), slot order; padding stays zero
-    unsigned* flags;    // [groups] grid-barrier arrival values
+    unsigned* bar;      // grid-barrier counters: [0] global, [64 * (1 + x)] group x (zeroed by prep)
     float* z;           // [bpad][4H] per-step pre-activations (per-step mode only)
 };
 
@@ -37,17 +37,18 @@ hipError_t launch_inproj(const Dims& d, const void* x, const void* W, const floa
 
 // Persistent on-device time loop.
 struct PersistentConfig {
-    int mt, groups, ksw, kswmax, nst, lds_bytes;
-    unsigned epoch;               // barrier values of this forward start above epoch
+    int mt, groups, ksw, kw, nst, lds_bytes;
     unsigned long long timeout_ticks;  // barrier wait bound in wall-clock ticks
 };
+constexpr int BAR_WORDS = 64 * 9;  // global + 8 group counters, 256 bytes apart
 hipError_t launch_persistent(const Dims& d, const PersistentConfig& pc, const void* U,
                              const float* h0, const float* c0, float* out_h, float* out_c,
                              const Workspace& ws, hipStream_t s);
 // Occupancy check for the co-resident grid; returns blocks per CU (0 if none).
-int persistent_blocks_per_cu(int bf16, int mt, int kswmax, int nst, int lds_bytes);
-// Smallest compiled variant with K-step capacity >= ksw and state capacity >= nstate.
-bool persistent_pick_variant(int bf16, int mt, int ksw, int nstate, int* kswmax, int* nst);
+int persistent_blocks_per_cu(int bf16, int mt, int ksw, int kw, int nst, int lds_bytes);
+// Compiled variant with exactly (mt, kw, ksw) and the smallest state capacity >= nstate.
+bool persistent_pick_variant(int bf16, int mt, int kw, int ksw, int nstate, int* nst);
+int persistent_lds_bytes(int bf16, int mt, int hpad);
 
 // Per-step comparison path.
 hipError_t launch_step_init(const Dims& d, const float* h0, const float* c0, float* out_h,

@@ -6,24 +6,35 @@
 // (cooperative launch).  Workgroup g owns 4*MT hidden units, i.e. 16*MT
 // gate-interleaved columns of U, and keeps that slice of U in registers as
 // MFMA A-fragments for the whole loop.  Per step t:
-//   1. prefetch Gx[t] (input projection + bias) for the (row, unit) pairs it owns;
-//   2. wait at the grid barrier until every workgroup has published h_t;
-//   3. the four waves split K = H: each forms partial C^T = U_slice^T h_t^T for
-//      the active rows (slots [0, active(t)) after the length sort);
-//   4. partials meet in LDS; the owning wave adds them and Gx, applies the gate
-//      non-linearities, and updates c and h, which live in its registers;
-//      finished rows are not touched (the per-row select of the paper);
-//   5. it writes its slice of h_{t+1} (MFMA operand type) and publishes it.
+//   1. the KW waves split K = H; each forms partial C^T = U_slice^T h_t^T for
+//      the active rows (slots [0, active(t)) after the length sort), one
+//      16-row tile at a time, loading the next tile's h fragments before the
+//      current tile's MFMAs;
+//   2. partials meet in LDS; the owning wave adds them and the prefetched
+//      Gx[t] (input projection + bias), applies the gate non-linearities and
+//      updates c (in its registers) and h; finished rows are not touched (the
+//      per-row select of the paper);
+//   3. it writes its slice of h_{t+1} and arrives at the grid barrier, then
+//      prefetches Gx[t+1] while waiting for the other workgroups.
 // The loop bound max_len and active(t) are read on the device; when every row
-// is done the loop ends.  A grid of one workgroup synchronises with
-// __syncthreads only.
+// is done the loop ends.
+//
+// Exchange of h between workgroups (they sit on different XCDs, whose L2
+// caches are not coherent with each other): h is stored and loaded with
+// device-scope cache policy (sc1), so stores are written through to the
+// coherence point before a wave's store counter drains and loads are served
+// from it.  A wave drains its stores (s_waitcnt vmcnt(0)) before its
+// workgroup arrives at the barrier, so no L2 write-back or invalidate is
+// needed around the barrier.  The barrier is two-level: workgroups arrive on
+// one of eight group counters, the last arrival of a group bumps the global
+// counter, and every workgroup polls the global counter.  The counters are
+// zeroed by the preparation kernel that runs before this one.
 #include "launch.h"
 
 namespace ldyn {
 
-constexpr int P_WAVES = 4;               // waves per workgroup; they split K
-constexpr int P_THREADS = 64 * P_WAVES;
-constexpr int P_LDS_TILES = 32;          // (row tile, gate tile) partials per wave in LDS
+constexpr int P_LDS_PARTIAL_KB = 128;   // LDS for cross-wave partial sums
+constexpr int P_SC1 = 16;               // buffer-instruction cache policy: device scope
 
 struct PersistParams {
     const void* U;
@@ -33,12 +44,11 @@ struct PersistParams {
     float* out_c;
     const float* gx;
     void* hx;
-    unsigned* flags;
+    unsigned* bar;          // [0]: global counter, [64 * (1 + x)]: group counter x (256 bytes apart)
     Meta* meta;
     const int32_t* perm;
     const int32_t* offsets;
-    int B, H, hpad, bpad, groups, ksw;
-    unsigned epoch;
+    int B, H, hpad, bpad, groups;
     unsigned long long timeout_ticks;
 };
 
@@ -50,103 +60,138 @@ __device__ inline int logical_group(int bid, int groups) {
     return (bid & 7) * (groups >> 3) + (bid >> 3);
 }
 
-// Grid barrier on per-workgroup arrival values.  Workgroup g publishes
-// "h_k is written" by storing epoch + k + 1 into flags[g]; waiting for h_k
-// means every flag is at least that value.  Values grow across forwards
-// (epoch advances by T_max + 1 per forward), so no reset is needed.
-__device__ inline void grid_publish(const PersistParams& p, int g, unsigned value) {
-    // Each wave makes its own stores visible at device scope first.
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+__device__ inline void drain_stores() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Barrier k (k = 0, 1, ...), split in two so work can be issued between the
+// arrival and the wait.  Arrival happens only after every wave of the
+// workgroup has drained its stores.
+__device__ inline void grid_arrive(const PersistParams& p, int k) {
+    drain_stores();
     __syncthreads();
-    if (threadIdx.x == 0)
-        __hip_atomic_store(p.flags + g, value, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    if (threadIdx.x == 0 && p.groups > 1) {
+        const int x = blockIdx.x & 7;
+        const unsigned members = (unsigned)((p.groups - x + 7) >> 3);
+        const unsigned old = __hip_atomic_fetch_add(p.bar + 64 * (1 + x), 1u, __ATOMIC_RELAXED,
+                                                    __HIP_MEMORY_SCOPE_AGENT);
+        if (old + 1u == (unsigned)(k + 1) * members)
+            __hip_atomic_fetch_add(p.bar, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
 }
 
-// Returns false if the wait exceeded its bound (status flagged, loop abandoned).
-__device__ inline bool grid_wait(const PersistParams& p, unsigned value, int* lds_ok) {
-    if (threadIdx.x < 64) {
-        const int lane = threadIdx.x;
-        const unsigned long long t0 = wall_clock64();
-        bool ok = true;
-        while (true) {
-            bool mine = true;
-            for (int i = lane; i < p.groups; i += 64)
-                mine &= __hip_atomic_load(p.flags + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= value;
-            if (__all(mine)) break;
-            if (wall_clock64() - t0 > p.timeout_ticks) {
-                ok = false;
-                if (lane == 0)
+// Returns false if the wait exceeded its bound (the timeout status bit is set
+// and the caller abandons the loop).
+__device__ inline bool grid_wait(const PersistParams& p, int k, int* lds_ok) {
+    if (threadIdx.x == 0) {
+        int ok = 1;
+        if (p.groups > 1) {
+            const int ngroups = p.groups < 8 ? p.groups : 8;
+            const unsigned want = (unsigned)(k + 1) * (unsigned)ngroups;
+            const unsigned long long t0 = wall_clock64();
+            while (__hip_atomic_load(p.bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < want) {
+                if (wall_clock64() - t0 > p.timeout_ticks) {
+                    ok = 0;
                     __hip_atomic_fetch_or(&p.meta->status, STATUS_TIMEOUT, __ATOMIC_RELAXED,
                                           __HIP_MEMORY_SCOPE_AGENT);
-                break;
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
             }
-            __builtin_amdgcn_s_sleep(1);
         }
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-        if (lane == 0) *lds_ok = ok;
+        *lds_ok = ok;
     }
     __syncthreads();
     return *lds_ok;
 }
 
-template <typename E, int MT, int KSWMAX, int NST>
-__global__ void __launch_bounds__(P_THREADS, 1)
+// Device-scope loads/stores of the operand buffer through a buffer resource.
+template <typename E> struct HxIO;
+template <> struct HxIO<EltBF16> {
+    __device__ static inline bf16x8_t load(__amdgpu_buffer_rsrc_t R, unsigned byte_off) {
+        typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+        const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(R, byte_off, 0, P_SC1);
+        return __builtin_bit_cast(bf16x8_t, v);
+    }
+    __device__ static inline void store(__amdgpu_buffer_rsrc_t R, unsigned byte_off, float h) {
+        const __bf16 b = (__bf16)h;
+        __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, b), R, byte_off, 0, P_SC1);
+    }
+};
+template <> struct HxIO<EltF32> {
+    __device__ static inline float load(__amdgpu_buffer_rsrc_t R, unsigned byte_off) {
+        return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(R, byte_off, 0, P_SC1));
+    }
+    __device__ static inline void store(__amdgpu_buffer_rsrc_t R, unsigned byte_off, float h) {
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(h), R, byte_off, 0, P_SC1);
+    }
+};
+
+template <typename E, int MT, int KSW, int KW, int NST>
+__global__ void __launch_bounds__(KW * 64, 1)
 persistent_kernel(PersistParams p) {
     using S = typename E::store_t;
     using F = typename E::frag_t;
-    constexpr int NTC = P_LDS_TILES / MT;  // row tiles per LDS chunk
-    extern __shared__ __attribute__((aligned(16))) float lds[];  // [P_WAVES][NTC][MT][64][4]
+    using IO = HxIO<E>;
+    constexpr int NTC = P_LDS_PARTIAL_KB / (KW * MT);  // row tiles per LDS chunk
+    static_assert(NTC >= 1, "partial buffer too small");
+    extern __shared__ __attribute__((aligned(16))) float lds[];  // [KW][NTC][MT][64][4]
     __shared__ int lds_ok;
 
     const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
-    const int single = p.groups == 1;
     const int g = logical_group(blockIdx.x, p.groups);
     const int H = p.H, H4 = 4 * H, hpad = p.hpad;
     const int u0 = g * 4 * MT;
-    const int kw0 = w * p.ksw * E::KSTEP;
+    const int kw0 = w * KSW * E::KSTEP;
     const int B = p.B, ntmax = (B + 15) >> 4;
-    S* hx0 = static_cast<S*>(p.hx);
-    const size_t hx_stride = (size_t)p.bpad * hpad;
+    const unsigned hx_half = (unsigned)(p.bpad * hpad) * (unsigned)sizeof(S);
+    const __amdgpu_buffer_rsrc_t R =
+        __builtin_amdgcn_make_buffer_rsrc(p.hx, (short)0, (int)(2u * hx_half), 0x00020000);
+    F afrag[MT][KSW];
 
     // ---- U slice -> registers (A-fragments of U^T; rows = gate-interleaved columns).
-    const S* U = static_cast<const S*>(p.U);
-    F afrag[MT][KSWMAX];
+    // The slice is staged through LDS transposed, ust[c'][k], with rows padded
+    // by 16 bytes (spreads the 2/4-byte writes over banks, keeps the 16-byte
+    // fragment reads aligned).  Out-of-range k and units stage as zeros.
+    {
+        const S* U = static_cast<const S*>(p.U);
+        S* ust = reinterpret_cast<S*>(lds);
+        constexpr int NCOL = 16 * MT, UPG = 4 * MT;  // columns, units per gate segment
+        const int stride = hpad + 16 / (int)sizeof(S);
+        const int total = hpad * NCOL;
+        for (int e0 = 0; e0 < total; e0 += KW * 64 * 8) {
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        const int cp = (u0 + mt * 4) * 4 + (l & 15);  // global gate-interleaved column
-        const int u = cp >> 2;
-        const int col = gate_col(cp, H);
-#pragma unroll
-        for (int ks = 0; ks < KSWMAX; ++ks) {
-            F f = E::zero();
-            if (ks < p.ksw && u < H) {
-                const int kb = kw0 + ks * E::KSTEP + (l >> 4) * E::KPL;
-                if constexpr (E::KPL == 1) {
-                    if (kb < H) f = U[(size_t)kb * H4 + col];
-                } else {
-#pragma unroll
-                    for (int e = 0; e < E::KPL; ++e)
-                        if (kb + e < H) f[e] = U[(size_t)(kb + e) * H4 + col];
-                }
+            for (int r = 0; r < 8; ++r) {
+                const int e = e0 + r * KW * 64 + tid;
+                const int k = e / NCOL, c = e - k * NCOL;
+                const int gate = c / UPG, uu = c - gate * UPG;
+                const bool ok = e < total && k < H && u0 + uu < H;
+                const S v = U[ok ? (size_t)k * H4 + gate * H + u0 + uu : 0];
+                if (e < total) ust[(4 * uu + gate) * stride + k] = ok ? v : E::from_f32(0.0f);
             }
-            afrag[mt][ks] = f;
         }
+        __syncthreads();
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int ks = 0; ks < KSW; ++ks)
+                afrag[mt][ks] = E::load(ust + (mt * 16 + (l & 15)) * stride + kw0 + ks * E::KSTEP +
+                                        (l >> 4) * E::KPL);
+        __syncthreads();  // the LDS is reused for partial sums
     }
 
-    // ---- Owned state: pair q = i*P_WAVES + w -> row tile q / MT, gate tile q % MT.
+    // ---- Owned state: pair q = i*KW + w -> row tile q / MT, gate tile q % MT.
     // c lives in registers; h is written to out_h whenever it changes (rows
     // that never run keep h0, which is copied here).
     float cst[NST];
 #pragma unroll
     for (int i = 0; i < NST; ++i) {
-        const int q = i * P_WAVES + w, nt = q / MT, mt = q % MT;
+        const int q = i * KW + w, nt = q / MT, mt = q % MT;
         const int s = nt * 16 + (l & 15), u = u0 + mt * 4 + (l >> 4);
         cst[i] = 0.f;
         if (nt < ntmax && s < B && u < H) {
             const size_t ib = (size_t)p.perm[s] * H + u;
             const float hv = p.h0[ib];
             cst[i] = p.c0[ib];
-            hx0[(size_t)s * hpad + u] = E::from_f32(hv);
+            IO::store(R, (unsigned)(s * hpad + u) * (unsigned)sizeof(S), hv);
             p.out_h[ib] = hv;  // exact aliasing out_h == h0 is allowed: same element, same lane
         }
     }
@@ -158,48 +203,56 @@ persistent_kernel(PersistParams p) {
         const int act = p.offsets[t + 1] - off;
 #pragma unroll
         for (int i = 0; i < NST; ++i) {
-            const int q = i * P_WAVES + w, nt = q / MT, mt = q % MT;
+            const int q = i * KW + w, nt = q / MT, mt = q % MT;
             const int s = nt * 16 + (l & 15), u = u0 + mt * 4 + (l >> 4);
-            gxv[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-            if (s < act && u < H)
-                gxv[i] = *reinterpret_cast<const f32x4_t*>(p.gx + (size_t)(off + s) * H4 + 4 * u);
+            const bool ok = s < act && u < H;
+            const size_t row = ok ? (size_t)(off + s) : 0;
+            const f32x4_t v = *reinterpret_cast<const f32x4_t*>(p.gx + row * H4 + 4 * (ok ? u : 0));
+            gxv[i] = ok ? v : f32x4_t{0.f, 0.f, 0.f, 0.f};
         }
     };
 
     const int max_len = p.meta->max_len;
     bool alive = true;
     if (max_len > 0) {
+        grid_arrive(p, 0);
         prefetch_gx(0);
-        if (single) {
-            __syncthreads();
-        } else {
-            grid_publish(p, g, p.epoch + 1u);
-            alive = grid_wait(p, p.epoch + 1u, &lds_ok);
-        }
+        alive = grid_wait(p, 0, &lds_ok);
     }
 
+    const unsigned lane_off = (unsigned)((l & 15) * hpad + kw0 + (l >> 4) * E::KPL) * (unsigned)sizeof(S);
+    constexpr unsigned KSTEP_BYTES = E::KSTEP * sizeof(S);
+    const unsigned tile_bytes = (unsigned)(16 * hpad) * (unsigned)sizeof(S);
     for (int t = 0; t < max_len && alive; ++t) {
         const int act = p.offsets[t + 1] - p.offsets[t];
         const int nt_act = (act + 15) >> 4;
-        const S* hcur = hx0 + (size_t)(t & 1) * hx_stride;
-        S* hnext = hx0 + (size_t)((t + 1) & 1) * hx_stride;
+        const unsigned cur = (unsigned)(t & 1) * hx_half;
+        const unsigned nxt = (unsigned)((t + 1) & 1) * hx_half;
+
+        // One register set of h fragments, reloaded for the next row tile
+        // right after each MFMA consumes it, so the next tile's loads are in
+        // flight while this tile's MFMAs run.
+        F fr[KSW];
+        auto tile_base = [&](int nt) { return cur + (unsigned)nt * tile_bytes + lane_off; };
 
         for (int ntc0 = 0; ntc0 < nt_act; ntc0 += NTC) {
             const int nchunk = min(NTC, nt_act - ntc0);
-            // partial products over this wave's K range
+            {
+                const unsigned base = tile_base(ntc0);
+#pragma unroll
+                for (int ks = 0; ks < KSW; ++ks) fr[ks] = IO::load(R, base + ks * KSTEP_BYTES);
+            }
             for (int j = 0; j < nchunk; ++j) {
-                const int row = (ntc0 + j) * 16 + (l & 15);
-                const S* hrow = hcur + (size_t)row * hpad + kw0 + (l >> 4) * E::KPL;
+                // the last round reloads the same tile (harmless, keeps loads unconditional)
+                const unsigned nbase = tile_base(ntc0 + min(j + 1, nchunk - 1));
                 f32x4_t acc[MT];
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int ks = 0; ks < KSWMAX; ++ks) {
-                    if (ks < p.ksw) {
-                        const F bf = E::load(hrow + ks * E::KSTEP);
+                for (int ks = 0; ks < KSW; ++ks) {
 #pragma unroll
-                        for (int mt = 0; mt < MT; ++mt) acc[mt] = E::mfma(afrag[mt][ks], bf, acc[mt]);
-                    }
+                    for (int mt = 0; mt < MT; ++mt) acc[mt] = E::mfma(afrag[mt][ks], fr[ks], acc[mt]);
+                    fr[ks] = IO::load(R, nbase + ks * KSTEP_BYTES);
                 }
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt)
@@ -209,96 +262,95 @@ persistent_kernel(PersistParams p) {
             // reduce, gates, state update, own slice of h_{t+1}
 #pragma unroll
             for (int i = 0; i < NST; ++i) {
-                const int q = i * P_WAVES + w, nt = q / MT, mt = q % MT;
+                const int q = i * KW + w, nt = q / MT, mt = q % MT;
                 const int j = nt - ntc0;
                 if (j < 0 || j >= nchunk) continue;
                 const int s = nt * 16 + (l & 15), u = u0 + mt * 4 + (l >> 4);
                 if (s >= act || u >= H) continue;
                 f32x4_t z = gxv[i];
 #pragma unroll
-                for (int ww = 0; ww < P_WAVES; ++ww)
+                for (int ww = 0; ww < KW; ++ww)
                     z += *reinterpret_cast<const f32x4_t*>(lds + ((((ww * NTC + j) * MT + mt) * 64 + l) << 2));
                 float c = cst[i], h;
                 lstm_cell(z, c, h);
                 cst[i] = c;
-                hnext[(size_t)s * hpad + u] = E::from_f32(h);
+                IO::store(R, nxt + (unsigned)(s * hpad + u) * (unsigned)sizeof(S), h);
                 p.out_h[(size_t)p.perm[s] * H + u] = h;
             }
             __syncthreads();
         }
         if (t + 1 < max_len) {
-            if (single) {
-                prefetch_gx(t + 1);
-            } else {
-                grid_publish(p, g, p.epoch + (unsigned)(t + 2));
-                prefetch_gx(t + 1);
-                alive = grid_wait(p, p.epoch + (unsigned)(t + 2), &lds_ok);
-            }
+            grid_arrive(p, t + 1);
+            prefetch_gx(t + 1);  // in flight during the wait
+            alive = grid_wait(p, t + 1, &lds_ok);
         }
     }
 
     // ---- final cell state, batch order
 #pragma unroll
     for (int i = 0; i < NST; ++i) {
-        const int q = i * P_WAVES + w, nt = q / MT, mt = q % MT;
+        const int q = i * KW + w, nt = q / MT, mt = q % MT;
         const int s = nt * 16 + (l & 15), u = u0 + mt * 4 + (l >> 4);
         if (nt < ntmax && s < B && u < H) p.out_c[(size_t)p.perm[s] * H + u] = cst[i];
     }
 }
 
 // ---------------------------------------------------------------------------
-// Variants: (element type, gate tiles per workgroup, K-step capacity per wave,
-// owned pairs per wave).  Register arrays are sized by the last two, so the
-// plan picks the smallest variant that covers the problem.
+// Variants: (element type, gate tiles per workgroup, K-steps per wave, waves,
+// owned pairs per wave).  Register arrays are sized by these, so the plan
+// picks the variant whose K-steps equal the problem's (rounded up to a power
+// of two; the padding of the operand buffer is zero) and the smallest state
+// capacity that covers the batch.
 typedef void (*persist_fn)(PersistParams);
 
-struct Variant { int bf16, mt, kswmax, nst; persist_fn f; };
+struct Variant { int bf16, mt, ksw, kw, nst; persist_fn f; };
 
-#define PV(BF, ET, MT, KS, NS) {BF, MT, KS, NS, persistent_kernel<ET, MT, KS, NS>}
+#define PV(BF, ET, MT, KS, KW, NS) {BF, MT, KS, KW, NS, persistent_kernel<ET, MT, KS, KW, NS>}
+#define PV_NST(BF, ET, MT, KS, KW) PV(BF, ET, MT, KS, KW, 2), PV(BF, ET, MT, KS, KW, 8)
 static const Variant kVariants[] = {
-    // one workgroup, H <= 32
-    PV(0, EltF32, 8, 2, 2), PV(0, EltF32, 8, 2, 8), PV(0, EltF32, 8, 2, 16),
-    PV(1, EltBF16, 8, 1, 2), PV(1, EltBF16, 8, 1, 8), PV(1, EltBF16, 8, 1, 16),
-    // four hidden units per workgroup
-    PV(0, EltF32, 1, 16, 2), PV(0, EltF32, 1, 16, 8), PV(0, EltF32, 1, 16, 16),
-    PV(0, EltF32, 1, 64, 2), PV(0, EltF32, 1, 64, 8), PV(0, EltF32, 1, 64, 16),
-    PV(1, EltBF16, 1, 4, 2), PV(1, EltBF16, 1, 4, 8), PV(1, EltBF16, 1, 4, 16),
-    PV(1, EltBF16, 1, 8, 2), PV(1, EltBF16, 1, 8, 8), PV(1, EltBF16, 1, 8, 16),
-    // eight hidden units per workgroup (H up to 2048 on 256 CUs)
-    PV(1, EltBF16, 2, 16, 8), PV(1, EltBF16, 2, 16, 16),
+    PV_NST(0, EltF32, 1, 1, 4), PV_NST(0, EltF32, 1, 2, 4), PV_NST(0, EltF32, 1, 4, 4),
+    PV_NST(0, EltF32, 1, 8, 4), PV_NST(0, EltF32, 1, 16, 4), PV_NST(0, EltF32, 1, 32, 4),
+    PV_NST(0, EltF32, 1, 64, 4),
+    PV_NST(1, EltBF16, 1, 1, 4), PV_NST(1, EltBF16, 1, 2, 4), PV_NST(1, EltBF16, 1, 4, 4),
+    PV_NST(1, EltBF16, 1, 8, 4),
+    PV(1, EltBF16, 2, 8, 8, 4), PV(1, EltBF16, 2, 8, 8, 8),
 };
+#undef PV_NST
 #undef PV
 
-static persist_fn find_variant(int bf16, int mt, int kswmax, int nst) {
+static persist_fn find_variant(int bf16, int mt, int ksw, int kw, int nst) {
     for (const Variant& v : kVariants)
-        if (v.bf16 == bf16 && v.mt == mt && v.kswmax == kswmax && v.nst == nst) return v.f;
+        if (v.bf16 == bf16 && v.mt == mt && v.ksw == ksw && v.kw == kw && v.nst == nst) return v.f;
     return nullptr;
 }
 
-bool persistent_pick_variant(int bf16, int mt, int ksw, int nstate, int* kswmax, int* nst) {
-    int best_k = 0, best_n = 0;
+bool persistent_pick_variant(int bf16, int mt, int kw, int ksw, int nstate, int* nst) {
+    int best = 0;
     for (const Variant& v : kVariants) {
-        if (v.bf16 != bf16 || v.mt != mt || v.kswmax < ksw || v.nst < nstate) continue;
-        if (best_k == 0 || v.kswmax < best_k || (v.kswmax == best_k && v.nst < best_n)) {
-            best_k = v.kswmax;
-            best_n = v.nst;
-        }
+        if (v.bf16 != bf16 || v.mt != mt || v.kw != kw || v.ksw != ksw || v.nst < nstate) continue;
+        if (best == 0 || v.nst < best) best = v.nst;
     }
-    if (best_k == 0) return false;
-    *kswmax = best_k;
-    *nst = best_n;
+    if (best == 0) return false;
+    *nst = best;
     return true;
 }
 
-int persistent_blocks_per_cu(int bf16, int mt, int kswmax, int nst, int lds_bytes) {
-    persist_fn f = find_variant(bf16, mt, kswmax, nst);
+// Dynamic LDS: the partial-sum chunks, or the staged U slice if larger.
+int persistent_lds_bytes(int bf16, int mt, int hpad) {
+    const int esz = bf16 ? 2 : 4;
+    const int staged = 16 * mt * (hpad + 16 / esz) * esz;
+    return staged > P_LDS_PARTIAL_KB * 1024 ? staged : P_LDS_PARTIAL_KB * 1024;
+}
+
+int persistent_blocks_per_cu(int bf16, int mt, int ksw, int kw, int nst, int lds_bytes) {
+    persist_fn f = find_variant(bf16, mt, ksw, kw, nst);
     if (!f) return 0;
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(f),
                             hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes) != hipSuccess)
         return 0;
     int n = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, reinterpret_cast<const void*>(f),
-                                                     P_THREADS, lds_bytes) != hipSuccess)
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, reinterpret_cast<const void*>(f), kw * 64,
+                                                     lds_bytes) != hipSuccess)
         return 0;
     return n;
 }
@@ -306,7 +358,7 @@ int persistent_blocks_per_cu(int bf16, int mt, int kswmax, int nst, int lds_byte
 hipError_t launch_persistent(const Dims& d, const PersistentConfig& pc, const void* U,
                              const float* h0, const float* c0, float* out_h, float* out_c,
                              const Workspace& ws, hipStream_t s) {
-    persist_fn f = find_variant(d.bf16, pc.mt, pc.kswmax, pc.nst);
+    persist_fn f = find_variant(d.bf16, pc.mt, pc.ksw, pc.kw, pc.nst);
     if (!f) return hipErrorInvalidValue;
     PersistParams p{};
     p.U = U;
@@ -316,7 +368,7 @@ hipError_t launch_persistent(const Dims& d, const PersistentConfig& pc, const vo
     p.out_c = out_c;
     p.gx = ws.gx;
     p.hx = ws.hx;
-    p.flags = ws.flags;
+    p.bar = ws.bar;
     p.meta = ws.meta;
     p.perm = ws.perm;
     p.offsets = ws.offsets;
@@ -325,12 +377,10 @@ hipError_t launch_persistent(const Dims& d, const PersistentConfig& pc, const vo
     p.hpad = d.hpad;
     p.bpad = d.bpad;
     p.groups = pc.groups;
-    p.ksw = pc.ksw;
-    p.epoch = pc.epoch;
     p.timeout_ticks = pc.timeout_ticks;
     void* args[] = {&p};
     return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(f), dim3(pc.groups),
-                                      dim3(P_THREADS), args, (unsigned)pc.lds_bytes, s);
+                                      dim3(pc.kw * 64), args, (unsigned)pc.lds_bytes, s);
 }
 
 }  // namespace ldyn

@@ -15,7 +15,7 @@ constexpr int PREP_MAX_B = 8192;  // two int32 tables of B entries in LDS
 __global__ void __launch_bounds__(PREP_THREADS)
 prep_kernel(const int32_t* __restrict__ lengths, int B, int T, Meta* __restrict__ meta,
             int32_t* __restrict__ perm, int32_t* __restrict__ offsets,
-            int32_t* __restrict__ rowsrc) {
+            int32_t* __restrict__ rowsrc, unsigned* __restrict__ bar) {
     extern __shared__ int32_t sh[];
     int32_t* len = sh;       // [B] clamped lengths, batch order
     int32_t* sperm = sh + B; // [B] slot -> batch index
@@ -25,6 +25,7 @@ prep_kernel(const int32_t* __restrict__ lengths, int B, int T, Meta* __restrict_
         bad = 0;
         maxlen = 0;
     }
+    if (tid < BAR_WORDS / 64) bar[64 * tid] = 0u;  // grid-barrier counters of the loop kernel
     __syncthreads();
     for (int i = tid; i < B; i += PREP_THREADS) {
         int v = lengths[i];
@@ -55,14 +56,11 @@ prep_kernel(const int32_t* __restrict__ lengths, int B, int T, Meta* __restrict_
     }
     __syncthreads();
     const int ml = maxlen;
-    // Compact rows of step t are slots [0, active(t)), active(t) = #{b: L_b > t}.
+    // Compact rows of step t are slots [0, active(t)); one wave per step, lanes over slots.
     const int wave = tid >> 6, lane = tid & 63;
     for (int t = wave; t < ml; t += PREP_THREADS / 64) {
-        int act = 0, off = 0;
-        for (int j = 0; j < B; ++j) {
-            act += len[j] > t;
-            off += min(len[j], t);
-        }
+        const int off = offsets[t];
+        const int act = offsets[t + 1] - off;
         for (int s = lane; s < act; s += 64) rowsrc[off + s] = sperm[s] * T + t;
     }
     if (tid == 0) {
@@ -79,7 +77,7 @@ hipError_t launch_prep(const Dims& d, const int32_t* lengths, const Workspace& w
     if (d.B > PREP_MAX_B) return hipErrorInvalidValue;
     const size_t lds = (size_t)2 * d.B * sizeof(int32_t);
     hipLaunchKernelGGL(prep_kernel, dim3(1), dim3(PREP_THREADS), lds, s, lengths, d.B, d.T, ws.meta,
-                       ws.perm, ws.offsets, ws.rowsrc);
+                       ws.perm, ws.offsets, ws.rowsrc, ws.bar);
     return hipGetLastError();
 }
 

@@ -32,22 +32,21 @@ def test_strerror_covers_codes():
     assert ld.lstm_dyn_strerror(99) == "unknown status"
 
 
-@pytest.mark.parametrize("B,D,H,T,dt,mt,groups,ksw", [
-    (4, 16, 32, 20, ld.F32, 8, 1, 2),          # tiny: one workgroup, no grid barrier
-    (32, 256, 256, 100, ld.F32, 1, 64, 16),
-    (64, 512, 512, 200, ld.BF16, 1, 128, 4),
-    (128, 1024, 1024, 500, ld.BF16, 1, 256, 8),
-    (256, 1024, 2048, 1000, ld.BF16, 2, 256, 16),
+@pytest.mark.parametrize("B,D,H,T,dt,mt,groups,ksw,kw", [
+    (4, 16, 32, 20, ld.F32, 1, 8, 2, 4),
+    (32, 256, 256, 100, ld.F32, 1, 64, 16, 4),
+    (64, 512, 512, 200, ld.BF16, 1, 128, 4, 4),
+    (128, 1024, 1024, 500, ld.BF16, 1, 256, 8, 4),
+    (256, 1024, 2048, 1000, ld.BF16, 2, 256, 8, 8),
 ])
-def test_plan_of_workloads(B, D, H, T, dt, mt, groups, ksw):
+def test_plan_of_workloads(B, D, H, T, dt, mt, groups, ksw, kw):
     p = ld.lstm_dyn_plan(B, D, H, T, dt, ld.PERSISTENT, 256)
-    assert (p["mt"], p["groups"], p["ksw"]) == (mt, groups, ksw)
+    assert (p["mt"], p["groups"], p["ksw"], p["kw"]) == (mt, groups, ksw, kw)
     assert p["groups"] <= 256 and p["groups"] * 4 * p["mt"] >= H
-    assert p["kswmax"] >= p["ksw"]
     kstep = 32 if dt == ld.BF16 else 4
-    assert p["hpad"] == p["ksw"] * kstep * 4 and p["hpad"] >= H
+    assert p["hpad"] == p["ksw"] * kstep * p["kw"] and p["hpad"] >= H
     assert p["bpad"] % 16 == 0 and p["bpad"] >= B
-    assert p["nstate"] * 4 >= ((B + 15) // 16) * p["mt"]
+    assert p["nstate"] * p["kw"] >= ((B + 15) // 16) * p["mt"]
     assert p["lds_bytes"] <= 160 * 1024
     gx = 16 * H * B * T
     assert p["workspace_bytes"] >= gx

@@ -66,9 +66,12 @@ ORDER = ["tiny_f32", "lstm256_f32", "lstm512_bf16", "skewed1024_bf16", "large204
 
 def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
     """Round fp32 values to bf16 (nearest, ties to even); return uint16 bits."""
-    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    rounded = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
-    return rounded.astype(np.uint16)
+    u = np.array(a, dtype=np.float32, copy=True, order="C").view(np.uint32)
+    lsb = (u >> 16) & 1
+    u += 0x7FFF       # in place; only NaNs with the top payload bits set could wrap
+    u += lsb
+    u >>= 16
+    return u.astype(np.uint16)
 
 
 def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
