@@ -53,7 +53,9 @@ enum { LSTM_DYN_F32 = 0, LSTM_DYN_BF16 = 1 };
 /* Execution mode.
  * PERSISTENT: the time loop runs on the device inside one persistent kernel
  *   (grid-wide synchronisation between steps, loop bound and early exit read
- *   on the device); 3 launches per forward, none of them waits for the host.
+ *   on the device); 3 launches per forward (1 when the hidden width is at most
+ *   32 and the whole forward fits one workgroup), none of them waits for the
+ *   host.
  * PER_STEP: the comparison path of the paper's eager-vs-graph experiment
  *   (Section 9, Table 1): the loop bound is copied to the host (one
  *   synchronisation), then the host issues two kernel launches per step. */
@@ -101,6 +103,10 @@ typedef struct {
     int lds_bytes;      /* dynamic LDS of the persistent kernel */
     int nstate;         /* (row tile, gate tile) pairs held per wave */
     long long workspace_bytes; /* device workspace a handle allocates */
+    int single;         /* 1: persistent mode runs the whole forward as one launch of a
+                           single workgroup (hidden width <= 32); groups is then 1 */
+    int single_kd;      /* K-step capacity over D of that kernel */
+    int single_nt;      /* 16-row tiles of that kernel */
 } lstm_dyn_plan_t;
 
 /*

@@ -44,7 +44,8 @@ class _Plan(ctypes.Structure):
     _fields_ = [("mt", ctypes.c_int), ("groups", ctypes.c_int), ("ksw", ctypes.c_int),
                 ("kw", ctypes.c_int), ("hpad", ctypes.c_int), ("bpad", ctypes.c_int),
                 ("lds_bytes", ctypes.c_int), ("nstate", ctypes.c_int),
-                ("workspace_bytes", ctypes.c_longlong)]
+                ("workspace_bytes", ctypes.c_longlong), ("single", ctypes.c_int),
+                ("single_kd", ctypes.c_int), ("single_nt", ctypes.c_int)]
 
 
 _lib = None

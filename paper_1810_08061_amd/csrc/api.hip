@@ -116,6 +116,11 @@ extern "C" int lstm_dyn_plan(int B, int D, int H, int T, int dtype, int mode, in
     out->nstate = nst;
     out->workspace_bytes =
         layout_of(B, H, T, bf16, mode, out->bpad, out->hpad).total;
+    if (mode == LSTM_DYN_PERSISTENT && H <= 32 &&
+        small_pick(bf16, B, D, H, &out->single_kd, &out->single_nt)) {
+        out->single = 1;
+        out->groups = 1;
+    }
     return LSTM_DYN_OK;
 }
 
@@ -158,7 +163,7 @@ extern "C" int lstm_dyn_create(lstm_dyn_t** out, int B, int D, int H, int T, int
     rc = lstm_dyn_plan(B, D, H, T, dtype, mode, cus, &plan);
     if (rc != LSTM_DYN_OK) return rc;
     const int bf16 = dtype == LSTM_DYN_BF16;
-    if (mode == LSTM_DYN_PERSISTENT) {
+    if (mode == LSTM_DYN_PERSISTENT && !plan.single) {
         const int per_cu = persistent_blocks_per_cu(bf16, plan.mt, plan.ksw, plan.kw, plan.nstate,
                                                     plan.lds_bytes);
         if (per_cu < 1 || plan.groups > per_cu * cus) return LSTM_DYN_ERR_UNSUPPORTED;
@@ -253,6 +258,16 @@ extern "C" int lstm_dyn_forward(lstm_dyn_t* h, const void* x, const int32_t* len
     } while (0)
 
     auto mark = [&](int i) { return h->timing ? hipEventRecord(h->ev[i], s) : hipSuccess; };
+    if (h->mode == LSTM_DYN_PERSISTENT && h->plan.single) {
+        LD_CHECK(mark(0));
+        LD_CHECK(mark(1));
+        LD_CHECK(mark(2));
+        LD_CHECK(launch_small(d, h->plan.single_kd, h->plan.single_nt, x, lengths, W, U, b, h0, c0,
+                              out_h, out_c, h->ws, s));
+        h->launches_last = 1;
+        LD_CHECK(mark(3));
+        return LSTM_DYN_OK;
+    }
     LD_CHECK(mark(0));
     LD_CHECK(launch_prep(d, lengths, h->ws, s));
     h->launches_last++;

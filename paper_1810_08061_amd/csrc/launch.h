@@ -50,6 +50,13 @@ int persistent_blocks_per_cu(int bf16, int mt, int ksw, int kw, int nst, int lds
 bool persistent_pick_variant(int bf16, int mt, int kw, int ksw, int nstate, int* nst);
 int persistent_lds_bytes(int bf16, int mt, int hpad);
 
+// Whole forward in one single-workgroup launch (H <= 32).
+bool small_pick(int bf16, int B, int D, int H, int* kd, int* nt);
+hipError_t launch_small(const Dims& d, int kd, int nt, const void* x, const int32_t* lengths,
+                        const void* W, const void* U, const float* b, const float* h0,
+                        const float* c0, float* out_h, float* out_c, const Workspace& ws,
+                        hipStream_t s);
+
 // Per-step comparison path.
 hipError_t launch_step_init(const Dims& d, const float* h0, const float* c0, float* out_h,
                             float* out_c, const Workspace& ws, hipStream_t s);

@@ -1,0 +1,260 @@
+// small.hip -- the whole forward in one workgroup, one launch (H <= 32).
+//
+// When the 4H gate columns fit the 8 gate tiles of one workgroup, nothing
+// needs a grid: the loop bound is reduced in LDS, each step forms
+// z = x_t W + h U + b with MFMA (W and U slices held in registers, each wave
+// owning two gate tiles over the full K = D + H, so no cross-wave reduction),
+// applies the gates to the rows with t < L[b] (the per-row select of the
+// paper's loop, Section 9 "RNN cells"), and passes h to the next step through
+// LDS.  x for step t+1 is fetched while step t computes.  Rows stay in batch
+// order; finished rows are simply not updated.
+#include "launch.h"
+
+namespace ldyn {
+
+constexpr int SM_WAVES = 4;
+constexpr int SM_THREADS = 64 * SM_WAVES;
+constexpr int SM_MT = 2;  // gate tiles per wave: 4 waves x 2 x 16 columns = 4H <= 128
+
+struct SmallParams {
+    const void* x;
+    const int32_t* lengths;
+    const void* W;
+    const void* U;
+    const float* b;
+    const float* h0;
+    const float* c0;
+    float* out_h;
+    float* out_c;
+    Meta* meta;
+    int B, D, H, T;
+};
+
+template <typename E, int KD, int KH, int NT>
+__global__ void __launch_bounds__(SM_THREADS, 1)
+small_kernel(SmallParams p) {
+    using S = typename E::store_t;
+    using F = typename E::frag_t;
+    constexpr int HP = KH * E::KSTEP;      // padded hidden width of the LDS h rows
+    constexpr int HS = HP + 16 / sizeof(S);  // row stride (16-byte pad)
+    __shared__ __attribute__((aligned(16))) S hs[2][NT * 16 * HS];
+    __shared__ int len[NT * 16];
+    __shared__ int maxlen, bad;
+
+    const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
+    const int B = p.B, D = p.D, H = p.H, T = p.T, H4 = 4 * H;
+    const S* X = static_cast<const S*>(p.x);
+    const S* W = static_cast<const S*>(p.W);
+    const S* U = static_cast<const S*>(p.U);
+
+    if (tid == 0) {
+        maxlen = 0;
+        bad = 0;
+    }
+    __syncthreads();
+    for (int i = tid; i < NT * 16; i += SM_THREADS) {
+        int v = 0;
+        if (i < B) {
+            v = p.lengths[i];
+            if (v < 0 || v > T) {
+                atomicOr(&bad, 1);
+                v = v < 0 ? 0 : T;
+            }
+            atomicMax(&maxlen, v);
+        }
+        len[i] = v;
+    }
+    // h0 -> LDS (operand type); padding rows and columns are zero in both buffers
+    for (int i = tid; i < NT * 16 * HS; i += SM_THREADS) {
+        const int n = i / HS, k = i - n * HS;
+        hs[0][i] = E::from_f32((n < B && k < H) ? p.h0[(size_t)n * H + k] : 0.0f);
+        hs[1][i] = E::from_f32(0.0f);
+    }
+
+    // A-fragments of W^T and U^T for this wave's two gate tiles (clamped loads).
+    F wf[SM_MT][KD], uf[SM_MT][KH];
+    float bias[SM_MT][4];
+#pragma unroll
+    for (int mt = 0; mt < SM_MT; ++mt) {
+        const int cp = (w * SM_MT + mt) * 16 + (l & 15);
+        const bool uok = (cp >> 2) < H;
+        const int col = uok ? gate_col(cp, H) : 0;
+#pragma unroll
+        for (int ks = 0; ks < KD; ++ks) {
+            F f = E::zero();
+#pragma unroll
+            for (int e = 0; e < E::KPL; ++e) {
+                const int k = ks * E::KSTEP + (l >> 4) * E::KPL + e;
+                const S v = W[(size_t)min(k, D - 1) * H4 + col];
+                if constexpr (E::KPL == 1) f = (uok && k < D) ? v : 0.0f;
+                else f[e] = (uok && k < D) ? v : E::from_f32(0.0f);
+            }
+            wf[mt][ks] = f;
+        }
+#pragma unroll
+        for (int ks = 0; ks < KH; ++ks) {
+            F f = E::zero();
+#pragma unroll
+            for (int e = 0; e < E::KPL; ++e) {
+                const int k = ks * E::KSTEP + (l >> 4) * E::KPL + e;
+                const S v = U[(size_t)min(k, H - 1) * H4 + col];
+                if constexpr (E::KPL == 1) f = (uok && k < H) ? v : 0.0f;
+                else f[e] = (uok && k < H) ? v : E::from_f32(0.0f);
+            }
+            uf[mt][ks] = f;
+        }
+        // this lane's four gates belong to unit (cp0 >> 2) with cp0 = tile base + 4 * (l >> 4)
+        const int u = ((w * SM_MT + mt) * 16 + 4 * (l >> 4)) >> 2;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) bias[mt][g] = u < H ? p.b[g * H + u] : 0.0f;
+    }
+
+    // Owned state: lane holds (row nt*16 + (l & 15), unit of gate tile mt).
+    float cst[SM_MT][NT], hst[SM_MT][NT];
+#pragma unroll
+    for (int mt = 0; mt < SM_MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+            const int n = nt * 16 + (l & 15);
+            const int u = ((w * SM_MT + mt) * 16 + 4 * (l >> 4)) >> 2;
+            const bool ok = n < B && u < H;
+            cst[mt][nt] = ok ? p.c0[(size_t)n * H + u] : 0.0f;
+            hst[mt][nt] = ok ? p.h0[(size_t)n * H + u] : 0.0f;
+        }
+    __syncthreads();
+    const int ml = maxlen;
+
+    // x fragments of one step: lane holds row nt*16 + (l & 15), K slice of D.
+    F xf[NT][KD], xn[NT][KD];
+    auto load_x = [&](F (&dst)[NT][KD], int t) {
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+            const int n = nt * 16 + (l & 15);
+            const size_t row = (size_t)min(n, B - 1) * T + min(t, T - 1);
+#pragma unroll
+            for (int ks = 0; ks < KD; ++ks) {
+                F f = E::zero();
+#pragma unroll
+                for (int e = 0; e < E::KPL; ++e) {
+                    const int k = ks * E::KSTEP + (l >> 4) * E::KPL + e;
+                    const S v = X[row * D + min(k, D - 1)];
+                    if constexpr (E::KPL == 1) f = k < D ? v : 0.0f;
+                    else f[e] = k < D ? v : E::from_f32(0.0f);
+                }
+                dst[nt][ks] = f;
+            }
+        }
+    };
+    if (ml > 0) load_x(xf, 0);
+
+    for (int t = 0; t < ml; ++t) {
+        if (t + 1 < ml) load_x(xn, t + 1);
+        const S* hcur = hs[t & 1];
+        S* hnext = hs[(t + 1) & 1];
+        f32x4_t acc[SM_MT][NT];
+#pragma unroll
+        for (int mt = 0; mt < SM_MT; ++mt)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KD; ++ks)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+                for (int mt = 0; mt < SM_MT; ++mt) acc[mt][nt] = E::mfma(wf[mt][ks], xf[nt][ks], acc[mt][nt]);
+#pragma unroll
+        for (int ks = 0; ks < KH; ++ks)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+                const F hf = E::load(hcur + (nt * 16 + (l & 15)) * HS + ks * E::KSTEP + (l >> 4) * E::KPL);
+#pragma unroll
+                for (int mt = 0; mt < SM_MT; ++mt) acc[mt][nt] = E::mfma(uf[mt][ks], hf, acc[mt][nt]);
+            }
+#pragma unroll
+        for (int mt = 0; mt < SM_MT; ++mt)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+                const int n = nt * 16 + (l & 15);
+                const int u = ((w * SM_MT + mt) * 16 + 4 * (l >> 4)) >> 2;
+                if (u >= H) continue;
+                if (t < len[n]) {  // len[n] = 0 for padding rows
+                    f32x4_t z = acc[mt][nt];
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) z[g] += bias[mt][g];
+                    float c = cst[mt][nt], h;
+                    lstm_cell(z, c, h);
+                    cst[mt][nt] = c;
+                    hst[mt][nt] = h;
+                }
+                hnext[n * HS + u] = E::from_f32(hst[mt][nt]);
+            }
+        __syncthreads();
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+            for (int ks = 0; ks < KD; ++ks) xf[nt][ks] = xn[nt][ks];
+    }
+
+#pragma unroll
+    for (int mt = 0; mt < SM_MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+            const int n = nt * 16 + (l & 15);
+            const int u = ((w * SM_MT + mt) * 16 + 4 * (l >> 4)) >> 2;
+            if (n < B && u < H) {
+                p.out_h[(size_t)n * H + u] = hst[mt][nt];
+                p.out_c[(size_t)n * H + u] = cst[mt][nt];
+            }
+        }
+    if (tid == 0) {
+        int total = 0;
+        for (int i = 0; i < B; ++i) total += len[i];
+        p.meta->max_len = ml;
+        p.meta->total_rows = total;
+        p.meta->status = bad ? STATUS_BAD_LENGTHS : 0;
+        p.meta->pad = 0;
+    }
+}
+
+typedef void (*small_fn)(SmallParams);
+struct SmallVariant { int bf16, kd, kh, nt; small_fn f; };
+#define SV(BF, ET, KD, KH, NT) {BF, KD, KH, NT, small_kernel<ET, KD, KH, NT>}
+static const SmallVariant kSmall[] = {
+    // fp32: K-step 4; D <= 64, H <= 32; B <= 16 or 64
+    SV(0, EltF32, 4, 8, 1), SV(0, EltF32, 16, 8, 1), SV(0, EltF32, 4, 8, 4), SV(0, EltF32, 16, 8, 4),
+    // bf16: K-step 32; D <= 128, H <= 32
+    SV(1, EltBF16, 1, 1, 1), SV(1, EltBF16, 4, 1, 1), SV(1, EltBF16, 1, 1, 4), SV(1, EltBF16, 4, 1, 4),
+};
+#undef SV
+
+// Smallest variant covering (D, H, B); fills *kd, *nt.  Returns false if none.
+bool small_pick(int bf16, int B, int D, int H, int* kd, int* nt) {
+    const int kstep = bf16 ? 32 : 4;
+    const int kdn = (D + kstep - 1) / kstep, khn = (H + kstep - 1) / kstep;
+    const int ntn = (B + 15) / 16;
+    int best = -1;
+    for (int i = 0; i < (int)(sizeof(kSmall) / sizeof(kSmall[0])); ++i) {
+        const SmallVariant& v = kSmall[i];
+        if (v.bf16 != bf16 || v.kd < kdn || v.kh < khn || v.nt < ntn) continue;
+        if (best < 0 || v.kd * v.nt < kSmall[best].kd * kSmall[best].nt) best = i;
+    }
+    if (best < 0) return false;
+    *kd = kSmall[best].kd;
+    *nt = kSmall[best].nt;
+    return true;
+}
+
+hipError_t launch_small(const Dims& d, int kd, int nt, const void* x, const int32_t* lengths,
+                        const void* W, const void* U, const float* b, const float* h0,
+                        const float* c0, float* out_h, float* out_c, const Workspace& ws,
+                        hipStream_t s) {
+    small_fn f = nullptr;
+    for (const SmallVariant& v : kSmall)
+        if (v.bf16 == d.bf16 && v.kd == kd && v.nt == nt) f = v.f;
+    if (!f) return hipErrorInvalidValue;
+    SmallParams p{x, lengths, W, U, b, h0, c0, out_h, out_c, ws.meta, d.B, d.D, d.H, d.T};
+    hipLaunchKernelGGL(f, dim3(1), dim3(SM_THREADS), 0, s, p);
+    return hipGetLastError();
+}
+
+}  // namespace ldyn

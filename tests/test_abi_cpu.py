@@ -33,7 +33,7 @@ def test_strerror_covers_codes():
 
 
 @pytest.mark.parametrize("B,D,H,T,dt,mt,groups,ksw,kw", [
-    (4, 16, 32, 20, ld.F32, 1, 8, 2, 4),
+    (4, 16, 32, 20, ld.F32, 1, 1, 2, 4),          # one workgroup, one launch
     (32, 256, 256, 100, ld.F32, 1, 64, 16, 4),
     (64, 512, 512, 200, ld.BF16, 1, 128, 4, 4),
     (128, 1024, 1024, 500, ld.BF16, 1, 256, 8, 4),
@@ -42,7 +42,7 @@ def test_strerror_covers_codes():
 def test_plan_of_workloads(B, D, H, T, dt, mt, groups, ksw, kw):
     p = ld.lstm_dyn_plan(B, D, H, T, dt, ld.PERSISTENT, 256)
     assert (p["mt"], p["groups"], p["ksw"], p["kw"]) == (mt, groups, ksw, kw)
-    assert p["groups"] <= 256 and p["groups"] * 4 * p["mt"] >= H
+    assert p["groups"] <= 256 and (p["single"] or p["groups"] * 4 * p["mt"] >= H)
     kstep = 32 if dt == ld.BF16 else 4
     assert p["hpad"] == p["ksw"] * kstep * p["kw"] and p["hpad"] >= H
     assert p["bpad"] % 16 == 0 and p["bpad"] >= B
@@ -50,6 +50,9 @@ def test_plan_of_workloads(B, D, H, T, dt, mt, groups, ksw, kw):
     assert p["lds_bytes"] <= 160 * 1024
     gx = 16 * H * B * T
     assert p["workspace_bytes"] >= gx
+    assert p["single"] == (1 if H <= 32 else 0)
+    if p["single"]:
+        assert p["groups"] == 1 and p["single_nt"] * 16 >= B
 
 
 @pytest.mark.parametrize("args", [
