@@ -34,10 +34,10 @@ long long align_up(long long v, long long a) { return (v + a - 1) / a * a; }
 
 
 struct Layout {
-    long long meta, perm, offsets, rowsrc, gx, hx, bar, z, total;
+    long long meta, perm, offsets, rowsrc, gx, hx, bar, z, wt, total;
 };
 
-Layout layout_of(int B, int H, int T, int bf16, int mode, int bpad, int hpad) {
+Layout layout_of(int B, int D, int H, int T, int bf16, int mode, int bpad, int hpad) {
     Layout L{};
     long long o = 0;
     auto take = [&](long long bytes) {
@@ -53,6 +53,14 @@ Layout layout_of(int B, int H, int T, int bf16, int mode, int bpad, int hpad) {
     L.hx = take(2LL * bpad * hpad * (bf16 ? 2 : 4));
     L.bar = take(4LL * BAR_WORDS);
     L.z = take(mode == LSTM_DYN_PER_STEP ? 16LL * H * bpad : 0);
+    if (bf16) {
+        Dims d{B, D, H, T, 1, hpad, bpad};
+        int np, dp;
+        inproj_bf16_wt_shape(d, &np, &dp);
+        L.wt = take(2LL * np * dp);
+    } else {
+        L.wt = take(0);
+    }
     L.total = o;
     return L;
 }
@@ -115,7 +123,7 @@ extern "C" int lstm_dyn_plan(int B, int D, int H, int T, int dtype, int mode, in
     out->lds_bytes = persistent_lds_bytes(bf16, mt, out->hpad);
     out->nstate = nst;
     out->workspace_bytes =
-        layout_of(B, H, T, bf16, mode, out->bpad, out->hpad).total;
+        layout_of(B, D, H, T, bf16, mode, out->bpad, out->hpad).total;
     if (mode == LSTM_DYN_PERSISTENT && H <= 32 &&
         small_pick(bf16, B, D, H, &out->single_kd, &out->single_nt)) {
         out->single = 1;
@@ -175,7 +183,7 @@ extern "C" int lstm_dyn_create(lstm_dyn_t** out, int B, int D, int H, int T, int
     h->num_cus = cus;
     h->plan = plan;
     h->dims = Dims{B, D, H, T, bf16, plan.hpad, plan.bpad};
-    const Layout L = layout_of(B, H, T, bf16, mode, plan.bpad, plan.hpad);
+    const Layout L = layout_of(B, D, H, T, bf16, mode, plan.bpad, plan.hpad);
     if (hipMalloc(&h->block, (size_t)L.total) != hipSuccess) {
         (void)hipGetLastError();
         delete h;
@@ -190,6 +198,7 @@ extern "C" int lstm_dyn_create(lstm_dyn_t** out, int B, int D, int H, int T, int
     h->ws.hx = base + L.hx;
     h->ws.bar = reinterpret_cast<unsigned*>(base + L.bar);
     h->ws.z = mode == LSTM_DYN_PER_STEP ? reinterpret_cast<float*>(base + L.z) : nullptr;
+    h->ws.wt = bf16 ? base + L.wt : nullptr;
     // Zero the small tables and the operand buffer (its padding must stay zero).
     if (hipMemset(base, 0, (size_t)L.gx) != hipSuccess ||
         hipMemset(base + L.hx, 0, (size_t)(L.total - L.hx)) != hipSuccess) {
@@ -203,8 +212,19 @@ extern "C" int lstm_dyn_create(lstm_dyn_t** out, int B, int D, int H, int T, int
         return LSTM_DYN_ERR_HIP;
     }
     h->timeout_ticks = (unsigned long long)(BARRIER_TIMEOUT_S * 1e3 * (double)wclk_khz);
-    const long long tiles = ((long long)B * T + 127) / 128 * ((4LL * H + 127) / 128);
-    h->inproj_grid = (int)(tiles < 4LL * cus ? tiles : 4LL * cus);
+    if (bf16) {
+        if (inproj_bf16_setup() != hipSuccess) {
+            (void)hipFree(h->block);
+            (void)hipHostFree(h->host_maxlen);
+            delete h;
+            return LSTM_DYN_ERR_HIP;
+        }
+        const long long tiles = inproj_bf16_tiles_max(h->dims);
+        h->inproj_grid = (int)(tiles < cus ? tiles : cus);
+    } else {
+        const long long tiles = ((long long)B * T + 127) / 128 * ((4LL * H + 127) / 128);
+        h->inproj_grid = (int)(tiles < 4LL * cus ? tiles : 4LL * cus);
+    }
     h->launches_last = 0;
     h->last_stream = nullptr;
     h->timing = 0;
@@ -236,6 +256,22 @@ extern "C" int lstm_dyn_destroy(lstm_dyn_t* h) {
     if (h->host_maxlen && hipHostFree(h->host_maxlen) != hipSuccess) rc = LSTM_DYN_ERR_HIP;
     delete h;
     return rc;
+}
+
+// Input projection over all valid steps: bf16 goes through the transposed-W
+// tiled GEMM (two launches), fp32 through the generic MFMA GEMM (one launch).
+static hipError_t input_projection(lstm_dyn* h, const void* x, const void* W, const float* b,
+                                   hipStream_t s) {
+    hipError_t e;
+    if (h->dims.bf16) {
+        if ((e = launch_transpose_w(h->dims, W, h->ws, s)) != hipSuccess) return e;
+        h->launches_last++;
+        e = launch_inproj_bf16(h->dims, x, b, h->ws, h->inproj_grid, s);
+    } else {
+        e = launch_inproj(h->dims, x, W, b, h->ws, h->inproj_grid, s);
+    }
+    h->launches_last++;
+    return e;
 }
 
 extern "C" int lstm_dyn_forward(lstm_dyn_t* h, const void* x, const int32_t* lengths, const void* W,
@@ -273,8 +309,7 @@ extern "C" int lstm_dyn_forward(lstm_dyn_t* h, const void* x, const int32_t* len
     h->launches_last++;
     LD_CHECK(mark(1));
     if (h->mode == LSTM_DYN_PERSISTENT) {
-        LD_CHECK(launch_inproj(d, x, W, b, h->ws, h->inproj_grid, s));
-        h->launches_last++;
+        LD_CHECK(input_projection(h, x, W, b, s));
         LD_CHECK(mark(2));
         PersistentConfig pc{h->plan.mt, h->plan.groups, h->plan.ksw,       h->plan.kw,
                             h->plan.nstate, h->plan.lds_bytes, h->timeout_ticks};
@@ -286,8 +321,7 @@ extern "C" int lstm_dyn_forward(lstm_dyn_t* h, const void* x, const int32_t* len
     // Per-step comparison path.
     LD_CHECK(launch_step_init(d, h0, c0, out_h, out_c, h->ws, s));
     h->launches_last++;
-    LD_CHECK(launch_inproj(d, x, W, b, h->ws, h->inproj_grid, s));
-    h->launches_last++;
+    LD_CHECK(input_projection(h, x, W, b, s));
     LD_CHECK(mark(2));
     LD_CHECK(hipMemcpyAsync(h->host_maxlen, &h->ws.meta->max_len, sizeof(int32_t),
                             hipMemcpyDeviceToHost, s));

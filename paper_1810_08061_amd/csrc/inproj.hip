@@ -1,0 +1,206 @@
+// inproj.hip -- the input projection over all valid time steps, bf16 inputs.
+//
+// x does not depend on the recurrent state, so x[b, t] W + b for every valid
+// (b, t) -- one row per sequence step, sum of lengths rows in all -- is one GEMM
+// hoisted out of the time loop: Gx[r][c'] = x[rowsrc[r]] . Wt[c'] + b[col(c')],
+// with c' the gate-interleaved column (4u + gate).
+//
+// W arrives as [D][4H] (N contiguous).  MFMA wants both operands contiguous
+// along K, so a first kernel writes Wt[c'][k] (gate-interleaved rows, zero
+// padded to whole tiles); the GEMM then loads both operands with 16-byte
+// vector loads.  Tiles are 256 columns x 256 rows x 64 K, four waves of
+// 128 x 128 each (8 x 8 MFMA 16x16x32 tiles), two LDS stages; the next
+// K-block is loaded into registers while the current one is multiplied.
+// C^T = Wt x^T is formed so each lane's four results are the four gates of
+// one (row, unit) and leave as one 16-byte store.
+#include "launch.h"
+
+namespace ldyn {
+
+constexpr int IP_TILE = 256;            // rows and columns per tile
+constexpr int IP_BK = 64;               // K per block
+constexpr int IP_LDK = IP_BK + 8;       // padded LDS row: 144 bytes
+constexpr int IP_THREADS = 256;
+constexpr int IP_STAGE = 2 * IP_TILE * IP_LDK;  // bf16 elements per stage (A and B)
+constexpr int IP_LDS_BYTES = 2 * IP_STAGE * 2;
+
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+
+// Wt[c'][k] = W[k][col(c')] for c' < 4H, k < D; zero elsewhere (np x dp).
+__global__ void __launch_bounds__(256)
+transpose_w_kernel(const __bf16* __restrict__ W, __bf16* __restrict__ Wt, int D, int H, int np, int dp) {
+    __shared__ __bf16 tile[64][64 + 2];
+    const int k0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    const int H4 = 4 * H;
+    // read: rows k, columns c' (gathered through the gate interleave)
+    for (int i = ty; i < 64; i += 4) {
+        const int k = k0 + i, cp = c0 + tx;
+        const bool ok = k < D && cp < H4;
+        const __bf16 v = W[ok ? (size_t)k * H4 + gate_col(cp, H) : 0];
+        tile[tx][i] = ok ? v : (__bf16)0.0f;
+    }
+    __syncthreads();
+    for (int i = ty; i < 64; i += 4) {
+        const int cp = c0 + i, k = k0 + tx;
+        if (cp < np && k < dp) Wt[(size_t)cp * dp + k] = tile[i][tx];
+    }
+}
+
+struct InprojParams {
+    const __bf16* x;       // [B*T][D]
+    const __bf16* wt;      // [np][dp]
+    const float* bias;     // [4H]
+    float* gx;             // [rows][4H]
+    const Meta* meta;
+    const int32_t* rowsrc;
+    int D, H, dp;
+};
+
+template <bool KFULL>
+__global__ void __launch_bounds__(IP_THREADS, 1)
+inproj_bf16_kernel(InprojParams p) {
+    extern __shared__ __attribute__((aligned(16))) __bf16 smem[];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;      // wave's 128 columns, 128 rows
+    const int H = p.H, N4 = 4 * H, D = p.D;
+    const int nrows = p.meta->total_rows;
+    const int ntc = (N4 + IP_TILE - 1) / IP_TILE;
+    const int ntr = (nrows + IP_TILE - 1) / IP_TILE;
+    const int ntiles = ntc * ntr;
+    const int nkb = (D + IP_BK - 1) / IP_BK;
+    const int ldr = tid >> 3, chunk = tid & 7;     // this thread loads chunk of rows ldr + 32 i
+
+    for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+        const int tr = tile / ntc, tc = tile - tr * ntc;
+        const int r0 = tr * IP_TILE, c0 = tc * IP_TILE;
+
+        const __bf16* xrow[8];   // row starts of x
+        const __bf16* wrow[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int r = min(r0 + ldr + 32 * i, nrows - 1);
+            xrow[i] = p.x + (size_t)p.rowsrc[r] * D;
+            wrow[i] = p.wt + (size_t)(c0 + ldr + 32 * i) * p.dp + chunk * 8;
+        }
+        u32x4_t ra[8], rb[8];
+        auto gload = [&](int kb) {
+            const int k = kb * IP_BK;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int kk = k + chunk * 8;  // first element of this thread's chunk
+                if (KFULL) {
+                    ra[i] = *reinterpret_cast<const u32x4_t*>(xrow[i] + kk);
+                } else {
+                    // ragged D: elementwise with addresses clamped into the row, zeros past D
+                    __bf16 e[8];
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        const __bf16 v = xrow[i][min(kk + j, D - 1)];
+                        e[j] = kk + j < D ? v : (__bf16)0.0f;
+                    }
+                    ra[i] = __builtin_bit_cast(u32x4_t, e);
+                }
+                rb[i] = *reinterpret_cast<const u32x4_t*>(wrow[i] + k);
+            }
+        };
+        auto lstore = [&](int stage) {
+            __bf16* sa = smem + stage * IP_STAGE;
+            __bf16* sb = sa + IP_TILE * IP_LDK;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                *reinterpret_cast<u32x4_t*>(sa + (ldr + 32 * i) * IP_LDK + chunk * 8) = ra[i];
+                *reinterpret_cast<u32x4_t*>(sb + (ldr + 32 * i) * IP_LDK + chunk * 8) = rb[i];
+            }
+        };
+
+        f32x4_t acc[8][8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+#pragma unroll
+            for (int j = 0; j < 8; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+        gload(0);
+        __syncthreads();  // the previous tile's readers are done with both stages
+        lstore(0);
+        __syncthreads();
+        for (int kb = 0; kb < nkb; ++kb) {
+            if (kb + 1 < nkb) gload(kb + 1);
+            const __bf16* sa = smem + (kb & 1) * IP_STAGE;
+            const __bf16* sb = sa + IP_TILE * IP_LDK;
+#pragma unroll
+            for (int ks = 0; ks < IP_BK / 32; ++ks) {
+                const int koff = ks * 32 + (lane >> 4) * 8;
+                bf16x8_t af[8], bf[8];
+#pragma unroll
+                for (int i = 0; i < 8; ++i)
+                    af[i] = *reinterpret_cast<const bf16x8_t*>(sb + (wm * 128 + i * 16 + (lane & 15)) * IP_LDK + koff);
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    bf[j] = *reinterpret_cast<const bf16x8_t*>(sa + (wn * 128 + j * 16 + (lane & 15)) * IP_LDK + koff);
+#pragma unroll
+                for (int i = 0; i < 8; ++i)
+#pragma unroll
+                    for (int j = 0; j < 8; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+            }
+            if (kb + 1 < nkb) lstore((kb + 1) & 1);
+            __syncthreads();
+        }
+
+        // epilogue: lane holds gates 0..3 of unit u for one row
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int cp = c0 + wm * 128 + i * 16 + 4 * (lane >> 4);
+            const int u = cp >> 2;
+            if (u >= H) continue;
+            const f32x4_t bv = f32x4_t{p.bias[u], p.bias[H + u], p.bias[2 * H + u], p.bias[3 * H + u]};
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int r = r0 + wn * 128 + j * 16 + (lane & 15);
+                if (r < nrows) *reinterpret_cast<f32x4_t*>(p.gx + (size_t)r * N4 + cp) = acc[i][j] + bv;
+            }
+        }
+    }
+}
+
+int inproj_bf16_tiles_max(const Dims& d) {
+    return (int)(((long long)d.B * d.T + IP_TILE - 1) / IP_TILE) * ((4 * d.H + IP_TILE - 1) / IP_TILE);
+}
+
+void inproj_bf16_wt_shape(const Dims& d, int* np, int* dp) {
+    *np = (4 * d.H + IP_TILE - 1) / IP_TILE * IP_TILE;
+    *dp = (d.D + IP_BK - 1) / IP_BK * IP_BK;
+}
+
+hipError_t inproj_bf16_setup() {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(inproj_bf16_kernel<true>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, IP_LDS_BYTES);
+    if (e != hipSuccess) return e;
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(inproj_bf16_kernel<false>),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, IP_LDS_BYTES);
+}
+
+hipError_t launch_transpose_w(const Dims& d, const void* W, const Workspace& ws, hipStream_t s) {
+    int np, dp;
+    inproj_bf16_wt_shape(d, &np, &dp);
+    hipLaunchKernelGGL(transpose_w_kernel, dim3(dp / 64, np / 64), dim3(256), 0, s,
+                       static_cast<const __bf16*>(W), static_cast<__bf16*>(ws.wt), d.D, d.H, np, dp);
+    return hipGetLastError();
+}
+
+hipError_t launch_inproj_bf16(const Dims& d, const void* x, const float* b, const Workspace& ws,
+                              int grid, hipStream_t s) {
+    int np, dp;
+    inproj_bf16_wt_shape(d, &np, &dp);
+    InprojParams p{static_cast<const __bf16*>(x), static_cast<const __bf16*>(ws.wt), b, ws.gx,
+                   ws.meta, ws.rowsrc, d.D, d.H, dp};
+    const bool kfull = (d.D % IP_BK) == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0;
+    if (kfull)
+        hipLaunchKernelGGL(inproj_bf16_kernel<true>, dim3(grid), dim3(IP_THREADS), IP_LDS_BYTES, s, p);
+    else
+        hipLaunchKernelGGL(inproj_bf16_kernel<false>, dim3(grid), dim3(IP_THREADS), IP_LDS_BYTES, s, p);
+    return hipGetLastError();
+}
+
+}  // namespace ldyn

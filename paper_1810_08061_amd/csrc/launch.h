@@ -19,6 +19,7 @@ struct Workspace {
     void* hx;           // [2][bpad][hpad] recurrent operand (dtype), slot order; padding stays zero
     unsigned* bar;      // grid-barrier counters: [0] global, [64 * (1 + x)] group x (zeroed by prep)
     float* z;           // [bpad][4H] per-step pre-activations (per-step mode only)
+    void* wt;           // bf16: W transposed to [np][dp] (gate-interleaved rows, zero padded)
 };
 
 struct Dims {
@@ -34,6 +35,14 @@ hipError_t launch_prep(const Dims& d, const int32_t* lengths, const Workspace& w
 // Input projection over all valid (b, t): gx[r][c'] = x[rowsrc[r]] . W[:, col(c')] + b[col(c')].
 hipError_t launch_inproj(const Dims& d, const void* x, const void* W, const float* b,
                          const Workspace& ws, int grid, hipStream_t s);
+
+// bf16 input projection: W -> Wt, then the tiled GEMM (inproj.hip).
+void inproj_bf16_wt_shape(const Dims& d, int* np, int* dp);
+int inproj_bf16_tiles_max(const Dims& d);
+hipError_t inproj_bf16_setup();
+hipError_t launch_transpose_w(const Dims& d, const void* W, const Workspace& ws, hipStream_t s);
+hipError_t launch_inproj_bf16(const Dims& d, const void* x, const float* b, const Workspace& ws,
+                              int grid, hipStream_t s);
 
 // Persistent on-device time loop.
 struct PersistentConfig {

@@ -166,12 +166,13 @@ def test_out_of_range_lengths_are_clamped_and_flagged(mode):
 def test_launch_counts():
     inp = workloads.random_case(11, 12, 16, 64, 10, dtype="bf16")
     _, _, m = run(inp, "persistent")
-    assert m.query(ld.Q_LAUNCHES_PER_FORWARD) == 3
+    # prep, W transpose (bf16), input projection, loop
+    assert m.query(ld.Q_LAUNCHES_PER_FORWARD) == 4
     small = workloads.random_case(11, 12, 16, 32, 10, dtype="bf16")
     _, _, ms = run(small, "persistent")
     assert ms.query(ld.Q_LAUNCHES_PER_FORWARD) == 1 and ms.query(ld.Q_GROUPS) == 1
     _, _, m2 = run(inp, "per_step")
-    assert m2.query(ld.Q_LAUNCHES_PER_FORWARD) == 3 + 2 * int(inp.lengths.max())
+    assert m2.query(ld.Q_LAUNCHES_PER_FORWARD) == 4 + 2 * int(inp.lengths.max())
     assert m.query(ld.Q_TOTAL_ROWS) == int(inp.lengths.sum())
 
 
