@@ -89,7 +89,9 @@ enum {
 
 /* lstm_dyn_set_option selectors. */
 enum {
-    LSTM_DYN_OPT_TIMING = 0 /* 1: record HIP events on the forward's stream around each phase */
+    LSTM_DYN_OPT_TIMING = 0,    /* 1: record HIP events on the forward's stream around each phase */
+    LSTM_DYN_OPT_STEP_TRACE = 1 /* 1: the persistent kernel records device wall-clock
+                                   timestamps within each step (diagnostics) */
 };
 
 /* Launch plan of a handle: pure host arithmetic, no device access. */
@@ -140,6 +142,17 @@ int lstm_dyn_query(lstm_dyn_t* h, int what, long long* value);
 
 /* Set a handle option (see LSTM_DYN_OPT_*).  Returns LSTM_DYN_OK, ERR_INVALID or ERR_HIP. */
 int lstm_dyn_set_option(lstm_dyn_t* h, int option, long long value);
+
+/*
+ * lstm_dyn_step_trace: with LSTM_DYN_OPT_STEP_TRACE set, copy the last
+ * forward's step timestamps of workgroup 0 (device wall-clock ticks; four per
+ * step -- step start after the barrier wait, partial products done, state
+ * update done, barrier arrival -- then the loop end) into
+ * ticks[0 .. capacity), synchronising the forward's stream; *count receives
+ * the number of entries and *khz the clock rate.
+ * Returns LSTM_DYN_OK, ERR_INVALID (option not set, NULL arguments) or ERR_HIP.
+ */
+int lstm_dyn_step_trace(lstm_dyn_t* h, long long* ticks, int capacity, int* count, int* khz);
 
 /* Static description of a status code (never NULL). */
 const char* lstm_dyn_strerror(int status);

@@ -18,6 +18,7 @@ __all__ = [
     "F32", "BF16", "PERSISTENT", "PER_STEP", "LstmDynError", "LstmDyn", "library_path",
     "lstm_dyn_create", "lstm_dyn_forward", "lstm_dyn_destroy", "lstm_dyn_query",
     "lstm_dyn_strerror", "lstm_dyn_plan", "lstm_dyn_check_args", "lstm_dyn_set_option",
+    "lstm_dyn_step_trace",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -28,7 +29,7 @@ PERSISTENT, PER_STEP = 0, 1
 OK, ERR_INVALID, ERR_HIP, ERR_NOMEM, ERR_UNSUPPORTED, ERR_BAD_LENGTHS, ERR_TIMEOUT = range(7)
 Q_LAST_STATUS, Q_STEPS_EXECUTED, Q_LAUNCHES_PER_FORWARD, Q_GROUPS, Q_WORKSPACE_BYTES, \
     Q_TOTAL_ROWS, Q_TIME_PREP_NS, Q_TIME_INPROJ_NS, Q_TIME_LOOP_NS = range(9)
-OPT_TIMING = 0
+OPT_TIMING, OPT_STEP_TRACE = 0, 1
 
 _DTYPES = {"f32": F32, "fp32": F32, "float32": F32, "bf16": BF16, "bfloat16": BF16}
 _MODES = {"persistent": PERSISTENT, "per_step": PER_STEP}
@@ -74,6 +75,8 @@ def _load():
     lib.lstm_dyn_query.restype = I
     lib.lstm_dyn_set_option.argtypes = [P, I, LL]
     lib.lstm_dyn_set_option.restype = I
+    lib.lstm_dyn_step_trace.argtypes = [P, ctypes.POINTER(LL), I, ctypes.POINTER(I), ctypes.POINTER(I)]
+    lib.lstm_dyn_step_trace.restype = I
     lib.lstm_dyn_strerror.argtypes = [I]
     lib.lstm_dyn_strerror.restype = ctypes.c_char_p
     lib.lstm_dyn_plan.argtypes = [I] * 7 + [ctypes.POINTER(_Plan)]
@@ -123,6 +126,19 @@ def lstm_dyn_set_option(handle: int, option: int, value: int) -> None:
     rc = _load().lstm_dyn_set_option(handle, option, value)
     if rc != OK:
         raise LstmDynError(rc, "lstm_dyn_set_option")
+
+
+def lstm_dyn_step_trace(handle: int, capacity: int):
+    """Step timestamps of the last forward (seconds, relative to the first):
+    four per step (start, partials done, state done, arrival) and the loop
+    end; requires OPT_STEP_TRACE."""
+    buf = (ctypes.c_longlong * capacity)()
+    n, khz = ctypes.c_int(0), ctypes.c_int(0)
+    rc = _load().lstm_dyn_step_trace(handle, buf, capacity, ctypes.byref(n), ctypes.byref(khz))
+    if rc != OK:
+        raise LstmDynError(rc, "lstm_dyn_step_trace")
+    t = [buf[i] for i in range(n.value)]
+    return [(v - t[0]) / (khz.value * 1e3) for v in t] if t else []
 
 
 def lstm_dyn_plan(B: int, D: int, H: int, T_max: int, dtype: int, mode: int, num_cus: int) -> dict:
@@ -199,6 +215,9 @@ class LstmDyn:
 
     def set_option(self, option: int, value: int) -> None:
         lstm_dyn_set_option(self.handle, option, value)
+
+    def step_trace(self) -> list:
+        return lstm_dyn_step_trace(self.handle, 4 * self.T + 1)
 
     def close(self):
         if getattr(self, "handle", None):

@@ -22,6 +22,8 @@ struct lstm_dyn {
     long long launches_last;
     hipStream_t last_stream;
     int timing;                // record phase events on the forward's stream
+    unsigned long long* trace; // per-step timestamps (diagnostics), [T + 1], or null
+    int wclk_khz;
     hipEvent_t ev[4];          // before prep, after prep, after input projection, after loop
 };
 
@@ -228,6 +230,8 @@ extern "C" int lstm_dyn_create(lstm_dyn_t** out, int B, int D, int H, int T, int
     h->launches_last = 0;
     h->last_stream = nullptr;
     h->timing = 0;
+    h->trace = nullptr;
+    h->wclk_khz = wclk_khz;
     for (auto& e : h->ev) e = nullptr;
     *out = h;
     return LSTM_DYN_OK;
@@ -243,7 +247,33 @@ extern "C" int lstm_dyn_set_option(lstm_dyn_t* h, int option, long long value) {
         h->timing = value ? 1 : 0;
         return LSTM_DYN_OK;
     }
+    if (option == LSTM_DYN_OPT_STEP_TRACE) {
+        if (value && !h->trace) {
+            if (hipMalloc(&h->trace, sizeof(unsigned long long) * 4 * (h->T + 1)) != hipSuccess) {
+                h->trace = nullptr;
+                return LSTM_DYN_ERR_NOMEM;
+            }
+        } else if (!value && h->trace) {
+            if (hipDeviceSynchronize() != hipSuccess || hipFree(h->trace) != hipSuccess) return LSTM_DYN_ERR_HIP;
+            h->trace = nullptr;
+        }
+        return LSTM_DYN_OK;
+    }
     return LSTM_DYN_ERR_INVALID;
+}
+
+extern "C" int lstm_dyn_step_trace(lstm_dyn_t* h, long long* ticks, int capacity, int* count, int* khz) {
+    if (!h || !ticks || !count || !khz || !h->trace || capacity < 0) return LSTM_DYN_ERR_INVALID;
+    if (hipStreamSynchronize(h->last_stream) != hipSuccess) return LSTM_DYN_ERR_HIP;
+    Meta m;
+    if (hipMemcpy(&m, h->ws.meta, sizeof(Meta), hipMemcpyDeviceToHost) != hipSuccess) return LSTM_DYN_ERR_HIP;
+    const int n = m.max_len > 0 ? 4 * m.max_len + 1 : 0;
+    const int c = n < capacity ? n : capacity;
+    if (c > 0 && hipMemcpy(ticks, h->trace, sizeof(long long) * c, hipMemcpyDeviceToHost) != hipSuccess)
+        return LSTM_DYN_ERR_HIP;
+    *count = c;
+    *khz = h->wclk_khz;
+    return LSTM_DYN_OK;
 }
 
 extern "C" int lstm_dyn_destroy(lstm_dyn_t* h) {
@@ -254,6 +284,7 @@ extern "C" int lstm_dyn_destroy(lstm_dyn_t* h) {
     for (auto& e : h->ev)
         if (e && hipEventDestroy(e) != hipSuccess) rc = LSTM_DYN_ERR_HIP;
     if (h->host_maxlen && hipHostFree(h->host_maxlen) != hipSuccess) rc = LSTM_DYN_ERR_HIP;
+    if (h->trace && hipFree(h->trace) != hipSuccess) rc = LSTM_DYN_ERR_HIP;
     delete h;
     return rc;
 }
@@ -312,7 +343,7 @@ extern "C" int lstm_dyn_forward(lstm_dyn_t* h, const void* x, const int32_t* len
         LD_CHECK(input_projection(h, x, W, b, s));
         LD_CHECK(mark(2));
         PersistentConfig pc{h->plan.mt, h->plan.groups, h->plan.ksw,       h->plan.kw,
-                            h->plan.nstate, h->plan.lds_bytes, h->timeout_ticks};
+                            h->plan.nstate, h->plan.lds_bytes, h->timeout_ticks, h->trace};
         LD_CHECK(launch_persistent(d, pc, U, h0, c0, out_h, out_c, h->ws, s));
         h->launches_last++;
         LD_CHECK(mark(3));

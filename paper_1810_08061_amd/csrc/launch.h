@@ -48,6 +48,7 @@ hipError_t launch_inproj_bf16(const Dims& d, const void* x, const float* b, cons
 struct PersistentConfig {
     int mt, groups, ksw, kw, nst, lds_bytes;
     unsigned long long timeout_ticks;  // barrier wait bound in wall-clock ticks
+    unsigned long long* trace;         // per-step timestamps (diagnostics) or null
 };
 constexpr int BAR_WORDS = 64 * 9;  // global + 8 group counters, 256 bytes apart
 hipError_t launch_persistent(const Dims& d, const PersistentConfig& pc, const void* U,

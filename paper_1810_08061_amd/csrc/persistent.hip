@@ -29,6 +29,8 @@
 // one of eight group counters, the last arrival of a group bumps the global
 // counter, and every workgroup polls the global counter.  The counters are
 // zeroed by the preparation kernel that runs before this one.
+#include <type_traits>
+
 #include "launch.h"
 
 namespace ldyn {
@@ -50,6 +52,7 @@ struct PersistParams {
     const int32_t* offsets;
     int B, H, hpad, bpad, groups;
     unsigned long long timeout_ticks;
+    unsigned long long* trace;  // [T + 1][4] timestamps from workgroup 0, or null
 };
 
 // Logical workgroup index: consecutive workgroups are dispatched to different
@@ -125,6 +128,17 @@ template <> struct HxIO<EltF32> {
     }
 };
 
+// K index (relative to the wave's K range) of the first value lane l holds for
+// MFMA K-step ks.  bf16: 8 consecutive k per lane per step.  fp32 with at
+// least four steps: each lane holds 4 consecutive k for a group of four
+// steps (one 16-byte load feeds four MFMAs); the A- and B-fragments use the
+// same assignment, so the sum over k is unchanged.
+template <typename E, int KSW>
+__device__ inline int kslot(int ks, int l) {
+    if constexpr (E::KPL == 1 && KSW >= 4) return 16 * (ks >> 2) + 4 * (l >> 4) + (ks & 3);
+    else return ks * E::KSTEP + (l >> 4) * E::KPL;
+}
+
 template <typename E, int MT, int KSW, int KW, int NST>
 __global__ void __launch_bounds__(KW * 64, 1)
 persistent_kernel(PersistParams p) {
@@ -157,24 +171,40 @@ persistent_kernel(PersistParams p) {
         constexpr int NCOL = 16 * MT, UPG = 4 * MT;  // columns, units per gate segment
         const int stride = hpad + 16 / (int)sizeof(S);
         const int total = hpad * NCOL;
-        for (int e0 = 0; e0 < total; e0 += KW * 64 * 8) {
+        auto src_of = [&](int e, bool& ok) {
+            const int k = e / NCOL, c = e - k * NCOL;
+            const int gate = c / UPG, uu = c - gate * UPG;
+            ok = k < H && u0 + uu < H;
+            return ok ? (size_t)k * H4 + gate * H + u0 + uu : (size_t)0;
+        };
+        auto dst_of = [&](int e) {
+            const int k = e / NCOL, c = e - k * NCOL;
+            const int gate = c / UPG, uu = c - gate * UPG;
+            return (4 * uu + gate) * stride + k;
+        };
+        auto stage = [&](int e) {
+            bool ok;
+            const S v = U[src_of(e, ok)];
+            ust[dst_of(e)] = ok ? v : E::from_f32(0.0f);
+        };
+        constexpr int ROUND = KW * 64 * 8;
+        const int full = total / ROUND * ROUND;
+        for (int e0 = 0; e0 < full; e0 += ROUND) {  // unguarded: eight loads in flight per thread
+            S v[8];
+            bool ok[8];
 #pragma unroll
-            for (int r = 0; r < 8; ++r) {
-                const int e = e0 + r * KW * 64 + tid;
-                const int k = e / NCOL, c = e - k * NCOL;
-                const int gate = c / UPG, uu = c - gate * UPG;
-                const bool ok = e < total && k < H && u0 + uu < H;
-                const S v = U[ok ? (size_t)k * H4 + gate * H + u0 + uu : 0];
-                if (e < total) ust[(4 * uu + gate) * stride + k] = ok ? v : E::from_f32(0.0f);
-            }
+            for (int r = 0; r < 8; ++r) v[r] = U[src_of(e0 + r * KW * 64 + tid, ok[r])];
+#pragma unroll
+            for (int r = 0; r < 8; ++r)
+                ust[dst_of(e0 + r * KW * 64 + tid)] = ok[r] ? v[r] : E::from_f32(0.0f);
         }
+        for (int e = full + tid; e < total; e += KW * 64) stage(e);
         __syncthreads();
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
             for (int ks = 0; ks < KSW; ++ks)
-                afrag[mt][ks] = E::load(ust + (mt * 16 + (l & 15)) * stride + kw0 + ks * E::KSTEP +
-                                        (l >> 4) * E::KPL);
+                afrag[mt][ks] = E::load(ust + (mt * 16 + (l & 15)) * stride + kw0 + kslot<E, KSW>(ks, l));
         __syncthreads();  // the LDS is reused for partial sums
     }
 
@@ -182,13 +212,16 @@ persistent_kernel(PersistParams p) {
     // c lives in registers; h is written to out_h whenever it changes (rows
     // that never run keep h0, which is copied here).
     float cst[NST];
+    int obase[NST];  // out_h / out_c element offset of the owned (row, unit), batch order
 #pragma unroll
     for (int i = 0; i < NST; ++i) {
         const int q = i * KW + w, nt = q / MT, mt = q % MT;
         const int s = nt * 16 + (l & 15), u = u0 + mt * 4 + (l >> 4);
         cst[i] = 0.f;
+        obase[i] = 0;
         if (nt < ntmax && s < B && u < H) {
             const size_t ib = (size_t)p.perm[s] * H + u;
+            obase[i] = (int)ib;
             const float hv = p.h0[ib];
             cst[i] = p.c0[ib];
             IO::store(R, (unsigned)(s * hpad + u) * (unsigned)sizeof(S), hv);
@@ -220,10 +253,14 @@ persistent_kernel(PersistParams p) {
         alive = grid_wait(p, 0, &lds_ok);
     }
 
-    const unsigned lane_off = (unsigned)((l & 15) * hpad + kw0 + (l >> 4) * E::KPL) * (unsigned)sizeof(S);
+    constexpr bool GROUPED = E::KPL == 1 && KSW >= 4;  // fp32: 16-byte loads of 4 k
+    const unsigned lane_off =
+        (unsigned)((l & 15) * hpad + kw0 + (GROUPED ? 4 : E::KPL) * (l >> 4)) * (unsigned)sizeof(S);
     constexpr unsigned KSTEP_BYTES = E::KSTEP * sizeof(S);
     const unsigned tile_bytes = (unsigned)(16 * hpad) * (unsigned)sizeof(S);
     for (int t = 0; t < max_len && alive; ++t) {
+        const bool tr = p.trace && blockIdx.x == 0 && tid == 0;
+        if (tr) p.trace[4 * t] = wall_clock64();
         const int act = p.offsets[t + 1] - p.offsets[t];
         const int nt_act = (act + 15) >> 4;
         const unsigned cur = (unsigned)(t & 1) * hx_half;
@@ -234,17 +271,32 @@ persistent_kernel(PersistParams p) {
         // flight while this tile's MFMAs run.
         F fr[KSW];
         auto tile_base = [&](int nt) { return cur + (unsigned)nt * tile_bytes + lane_off; };
+        // fragment loads of one row tile: ks, or the group of four starting at ks
+        auto load_frag = [&](unsigned base, int ks) {
+            if constexpr (GROUPED) {
+                if ((ks & 3) == 0) {
+                    typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+                    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(R, base + (ks >> 2) * 64u, 0, P_SC1);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) fr[ks + j] = __uint_as_float(v[j]);
+                }
+            } else {
+                fr[ks] = IO::load(R, base + ks * KSTEP_BYTES);
+            }
+        };
 
         for (int ntc0 = 0; ntc0 < nt_act; ntc0 += NTC) {
             const int nchunk = min(NTC, nt_act - ntc0);
             {
                 const unsigned base = tile_base(ntc0);
 #pragma unroll
-                for (int ks = 0; ks < KSW; ++ks) fr[ks] = IO::load(R, base + ks * KSTEP_BYTES);
+                for (int ks = 0; ks < KSW; ++ks) load_frag(base, ks);
             }
-            for (int j = 0; j < nchunk; ++j) {
-                // the last round reloads the same tile (harmless, keeps loads unconditional)
-                const unsigned nbase = tile_base(ntc0 + min(j + 1, nchunk - 1));
+            // one row tile's partial products; with RELOAD, each fragment register
+            // is refilled from tile j + 1 right after its MFMA has consumed it
+            auto mma_tile = [&](int j, auto reload_tag) {
+                constexpr bool RELOAD = decltype(reload_tag)::value;
+                const unsigned nbase = tile_base(ntc0 + j + 1);
                 f32x4_t acc[MT];
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -252,13 +304,22 @@ persistent_kernel(PersistParams p) {
                 for (int ks = 0; ks < KSW; ++ks) {
 #pragma unroll
                     for (int mt = 0; mt < MT; ++mt) acc[mt] = E::mfma(afrag[mt][ks], fr[ks], acc[mt]);
-                    fr[ks] = IO::load(R, nbase + ks * KSTEP_BYTES);
+                    if constexpr (RELOAD) {
+                        if constexpr (GROUPED) {
+                            if ((ks & 3) == 3) load_frag(nbase, ks - 3);
+                        } else {
+                            load_frag(nbase, ks);
+                        }
+                    }
                 }
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt)
                     *reinterpret_cast<f32x4_t*>(lds + ((((w * NTC + j) * MT + mt) * 64 + l) << 2)) = acc[mt];
-            }
+            };
+            for (int j = 0; j + 1 < nchunk; ++j) mma_tile(j, std::true_type{});
+            mma_tile(nchunk - 1, std::false_type{});  // last tile: nothing left to load
             __syncthreads();
+            if (tr) p.trace[4 * t + 1] = wall_clock64();
             // reduce, gates, state update, own slice of h_{t+1}
 #pragma unroll
             for (int i = 0; i < NST; ++i) {
@@ -275,23 +336,26 @@ persistent_kernel(PersistParams p) {
                 lstm_cell(z, c, h);
                 cst[i] = c;
                 IO::store(R, nxt + (unsigned)(s * hpad + u) * (unsigned)sizeof(S), h);
-                p.out_h[(size_t)p.perm[s] * H + u] = h;
+                p.out_h[obase[i]] = h;
             }
             __syncthreads();
         }
+        if (tr) p.trace[4 * t + 2] = wall_clock64();
         if (t + 1 < max_len) {
             grid_arrive(p, t + 1);
+            if (tr) p.trace[4 * t + 3] = wall_clock64();
             prefetch_gx(t + 1);  // in flight during the wait
             alive = grid_wait(p, t + 1, &lds_ok);
         }
     }
 
+    if (p.trace && blockIdx.x == 0 && tid == 0) p.trace[4 * max_len] = wall_clock64();
     // ---- final cell state, batch order
 #pragma unroll
     for (int i = 0; i < NST; ++i) {
         const int q = i * KW + w, nt = q / MT, mt = q % MT;
         const int s = nt * 16 + (l & 15), u = u0 + mt * 4 + (l >> 4);
-        if (nt < ntmax && s < B && u < H) p.out_c[(size_t)p.perm[s] * H + u] = cst[i];
+        if (nt < ntmax && s < B && u < H) p.out_c[obase[i]] = cst[i];
     }
 }
 
@@ -378,6 +442,7 @@ hipError_t launch_persistent(const Dims& d, const PersistentConfig& pc, const vo
     p.bpad = d.bpad;
     p.groups = pc.groups;
     p.timeout_ticks = pc.timeout_ticks;
+    p.trace = pc.trace;
     void* args[] = {&p};
     return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(f), dim3(pc.groups),
                                       dim3(pc.kw * 64), args, (unsigned)pc.lds_bytes, s);
