@@ -19,6 +19,7 @@ cpu_baseline the fp64 oracle on a bounded sample of the same workload, timed
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -33,6 +34,8 @@ if ROOT not in sys.path:
 import workloads  # noqa: E402
 
 PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}  # MI355X dense MFMA
+LOOP_SOURCE = os.path.join(ROOT, "paper_1810_08061_amd", "csrc", "persistent.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "loop_{workload}_traffic.json")
 HBM_PEAK_GBS = 8000.0
 METRIC = "valid seq·steps/sec + MFMA util; speedup of on-device loop vs per-step launch"
 DEFAULT_WORKLOAD = "large2048_bf16"
@@ -87,6 +90,35 @@ def time_whole(torch, model, dev, steps, warmup, out):
     return (time.perf_counter() - t0) / steps
 
 
+def loop_source_sha256():
+    with open(LOOP_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(workload):
+    """HBM bytes per launch of the loop kernel from the committed rocprofv3
+    counter summary, or None when absent or taken from another kernel source."""
+    path = TRAFFIC_FILE.format(workload=workload)
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_sha256") != loop_source_sha256():
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def copy_calibration(torch, mib=512, reps=5):
+    """A plain device copy of known size, for scaling FETCH_SIZE/WRITE_SIZE."""
+    n = mib * (1 << 20) // 4
+    a = torch.ones(n, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(reps):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_each_way": n * 4, "dispatches": reps}), flush=True)
+
+
 def cpu_baseline(inp, budget_rows_steps):
     """Time the fp64 oracle on the longest-first prefix of rows whose lengths
     sum to about `budget_rows_steps` (all host cores)."""
@@ -121,7 +153,11 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--cpu-budget", type=int, default=3000,
                     help="seq*steps of the oracle sample (about 10-30 s on a host)")
-    ap.add_argument("--per-step-reps", type=int, default=3)
+    ap.add_argument("--per-step-reps", type=int, default=3,
+                    help="forwards of the per-step path to time (0: skip)")
+    ap.add_argument("--no-tiny", action="store_true", help="skip the tiny_f32 launch-overhead leg")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain copy of known size (for scaling HBM counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -133,6 +169,9 @@ def main():
     import paper_1810_08061_amd as ld
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.copy_calibration:
+        copy_calibration(torch)
+        return
     w = workloads.WORKLOADS[args.workload]
     _log(f"generating {args.workload}")
     inp = workloads.workload_inputs(args.workload)
@@ -152,23 +191,31 @@ def main():
     model.set_option(ld.OPT_TIMING, 0)
     t_wall = time_whole(torch, model, dev, args.steps, 1, out)
 
-    _log("per-step path")
-    ps = ld.LstmDyn(w.B, w.D, w.H, w.T, w.dtype, "per_step")
-    t_ps = time_whole(torch, ps, dev, args.per_step_reps, 1, out)
-    ps_launches = ps.query(ld.Q_LAUNCHES_PER_FORWARD)
-    ps.close()
+    per_step = None
+    if args.per_step_reps > 0:
+        _log("per-step path")
+        ps = ld.LstmDyn(w.B, w.D, w.H, w.T, w.dtype, "per_step")
+        t_ps = time_whole(torch, ps, dev, args.per_step_reps, 1, out)
+        per_step = {"ms_per_step": t_ps * 1e3, "launches_per_forward": ps.query(ld.Q_LAUNCHES_PER_FORWARD),
+                    "speedup_of_persistent": t_ps / t_wall}
+        ps.close()
 
-    # smallest workload: where the per-step launch overhead dominates
-    tw = workloads.WORKLOADS["tiny_f32"]
-    tin = workloads.workload_inputs("tiny_f32")
-    tdev = to_device(tin, torch)
-    tout = (torch.empty((tw.B, tw.H), device="cuda"), torch.empty((tw.B, tw.H), device="cuda"))
-    tm = ld.LstmDyn(tw.B, tw.D, tw.H, tw.T, tw.dtype, "persistent")
-    t_tiny = time_whole(torch, tm, tdev, 200, 20, tout)
-    tps = ld.LstmDyn(tw.B, tw.D, tw.H, tw.T, tw.dtype, "per_step")
-    t_tiny_ps = time_whole(torch, tps, tdev, 50, 5, tout)
-    tm.close()
-    tps.close()
+    tiny = None
+    if not args.no_tiny:
+        # smallest workload: where the per-step launch overhead dominates
+        tw = workloads.WORKLOADS["tiny_f32"]
+        tin = workloads.workload_inputs("tiny_f32")
+        tdev = to_device(tin, torch)
+        tout = (torch.empty((tw.B, tw.H), device="cuda"), torch.empty((tw.B, tw.H), device="cuda"))
+        tm = ld.LstmDyn(tw.B, tw.D, tw.H, tw.T, tw.dtype, "persistent")
+        t_tiny = time_whole(torch, tm, tdev, 200, 20, tout)
+        tps = ld.LstmDyn(tw.B, tw.D, tw.H, tw.T, tw.dtype, "per_step")
+        t_tiny_ps = time_whole(torch, tps, tdev, 50, 5, tout)
+        tiny = {"persistent_us": t_tiny * 1e6, "per_step_us": t_tiny_ps * 1e6,
+                "speedup_of_persistent": t_tiny_ps / t_tiny,
+                "launches_per_forward": tm.query(ld.Q_LAUNCHES_PER_FORWARD)}
+        tm.close()
+        tps.close()
 
     dt = w.dtype
     flops_fwd = 8.0 * w.H * (w.D + w.H) * sumL
@@ -197,7 +244,9 @@ def main():
                    "parallelism": "none (1 GPU)", "persistent_groups": groups},
         "roofline": {"bound": "mfma", "kernel": "persistent time loop (recurrent h U, gates)",
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
-                     "frac": achieved / peak, "traffic": None},
+                     "frac": achieved / peak, "traffic": measured_traffic(args.workload),
+                     "algorithmic_flops_per_launch": flops_rec,
+                     "mean_launch_ms": t_loop * 1e3},
         "mfma_frac_forward": flops_fwd / t_fwd / 1e12 / peak,
         "hbm_frac_forward": bytes_alg / t_fwd / 1e9 / HBM_PEAK_GBS,
         "phases_ms": {"prep": t_prep * 1e3, "input_projection": t_inproj * 1e3,
@@ -205,10 +254,8 @@ def main():
         "input_projection_tflops": flops_in / t_inproj / 1e12,
         "launches_per_forward": launches,
         "wall_ms_per_step": t_wall * 1e3,
-        "per_step_path": {"ms_per_step": t_ps * 1e3, "launches_per_forward": ps_launches,
-                          "speedup_of_persistent": t_ps / t_wall},
-        "tiny_f32": {"persistent_us": t_tiny * 1e6, "per_step_us": t_tiny_ps * 1e6,
-                     "speedup_of_persistent": t_tiny_ps / t_tiny},
+        "per_step_path": per_step,
+        "tiny_f32": tiny,
     }
     if not args.no_cpu:
         _log("cpu baseline (oracle)")

@@ -149,6 +149,10 @@ persistent_kernel(PersistParams p) {
     static_assert(NTC >= 1, "partial buffer too small");
     extern __shared__ __attribute__((aligned(16))) float lds[];  // [KW][NTC][MT][64][4]
     __shared__ int lds_ok;
+    constexpr int UPW = 4 * MT;                      // hidden units per workgroup
+    constexpr int SEG_BYTES = UPW * (int)sizeof(S);  // one row of this workgroup's h slice
+    static_assert(SEG_BYTES == 8 || SEG_BYTES == 16, "h row segment must be 8 or 16 bytes");
+    __shared__ __attribute__((aligned(16))) S hstage[NTC * 16 * UPW];
 
     const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
     const int g = logical_group(blockIdx.x, p.groups);
@@ -209,23 +213,22 @@ persistent_kernel(PersistParams p) {
     }
 
     // ---- Owned state: pair q = i*KW + w -> row tile q / MT, gate tile q % MT.
-    // c lives in registers; h is written to out_h whenever it changes (rows
-    // that never run keep h0, which is copied here).
-    float cst[NST];
+    // c and h live in registers and reach out_c / out_h once, after the loop.
+    float cst[NST], hst[NST];
     int obase[NST];  // out_h / out_c element offset of the owned (row, unit), batch order
 #pragma unroll
     for (int i = 0; i < NST; ++i) {
         const int q = i * KW + w, nt = q / MT, mt = q % MT;
         const int s = nt * 16 + (l & 15), u = u0 + mt * 4 + (l >> 4);
         cst[i] = 0.f;
+        hst[i] = 0.f;
         obase[i] = 0;
         if (nt < ntmax && s < B && u < H) {
             const size_t ib = (size_t)p.perm[s] * H + u;
             obase[i] = (int)ib;
-            const float hv = p.h0[ib];
+            hst[i] = p.h0[ib];  // read before the final write: exact aliasing out_h == h0 is allowed
             cst[i] = p.c0[ib];
-            IO::store(R, (unsigned)(s * hpad + u) * (unsigned)sizeof(S), hv);
-            p.out_h[ib] = hv;  // exact aliasing out_h == h0 is allowed: same element, same lane
+            IO::store(R, (unsigned)(s * hpad + u) * (unsigned)sizeof(S), hst[i]);
         }
     }
 
@@ -327,7 +330,11 @@ persistent_kernel(PersistParams p) {
                 const int j = nt - ntc0;
                 if (j < 0 || j >= nchunk) continue;
                 const int s = nt * 16 + (l & 15), u = u0 + mt * 4 + (l >> 4);
-                if (s >= act || u >= H) continue;
+                if (s >= act) continue;
+                if (u >= H) {  // ragged last workgroup: its padding units stay zero
+                    hstage[(s - ntc0 * 16) * UPW + (u - u0)] = E::from_f32(0.0f);
+                    continue;
+                }
                 f32x4_t z = gxv[i];
 #pragma unroll
                 for (int ww = 0; ww < KW; ++ww)
@@ -335,10 +342,27 @@ persistent_kernel(PersistParams p) {
                 float c = cst[i], h;
                 lstm_cell(z, c, h);
                 cst[i] = c;
-                IO::store(R, nxt + (unsigned)(s * hpad + u) * (unsigned)sizeof(S), h);
-                p.out_h[obase[i]] = h;
+                hst[i] = h;
+                hstage[(s - ntc0 * 16) * UPW + (u - u0)] = E::from_f32(h);
             }
             __syncthreads();
+            // this workgroup's slice of h_{t+1}: one UPW-unit row segment per active row
+            {
+                const int rows = min(act - ntc0 * 16, nchunk * 16);
+                for (int r = tid; r < rows; r += KW * 64) {
+                    const int s = ntc0 * 16 + r;
+                    const unsigned off = nxt + (unsigned)(s * hpad + u0) * (unsigned)sizeof(S);
+                    if constexpr (SEG_BYTES == 16) {
+                        typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+                        __builtin_amdgcn_raw_buffer_store_b128(
+                            *reinterpret_cast<const u32x4*>(hstage + r * UPW), R, off, 0, P_SC1);
+                    } else {
+                        typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+                        __builtin_amdgcn_raw_buffer_store_b64(
+                            *reinterpret_cast<const u32x2*>(hstage + r * UPW), R, off, 0, P_SC1);
+                    }
+                }
+            }
         }
         if (tr) p.trace[4 * t + 2] = wall_clock64();
         if (t + 1 < max_len) {
@@ -350,12 +374,15 @@ persistent_kernel(PersistParams p) {
     }
 
     if (p.trace && blockIdx.x == 0 && tid == 0) p.trace[4 * max_len] = wall_clock64();
-    // ---- final cell state, batch order
+    // ---- final state, batch order
 #pragma unroll
     for (int i = 0; i < NST; ++i) {
         const int q = i * KW + w, nt = q / MT, mt = q % MT;
         const int s = nt * 16 + (l & 15), u = u0 + mt * 4 + (l >> 4);
-        if (nt < ntmax && s < B && u < H) p.out_c[obase[i]] = cst[i];
+        if (nt < ntmax && s < B && u < H) {
+            p.out_c[obase[i]] = cst[i];
+            p.out_h[obase[i]] = hst[i];
+        }
     }
 }
 
