@@ -151,7 +151,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=workloads.ORDER)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
-    ap.add_argument("--cpu-budget", type=int, default=3000,
+    ap.add_argument("--cpu-budget", type=int, default=24000,
                     help="seq*steps of the oracle sample (about 10-30 s on a host)")
     ap.add_argument("--per-step-reps", type=int, default=3,
                     help="forwards of the per-step path to time (0: skip)")
@@ -160,7 +160,7 @@ def main():
                     help="only run a plain copy of known size (for scaling HBM counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path "
+        print("bench.py measures one GPU: the library has no multi-GPU path "
               "(the batch would shard across GPUs with no exchange inside the loop).",
               file=sys.stderr)
         sys.exit(2)

@@ -67,7 +67,7 @@ enum {
     LSTM_DYN_ERR_INVALID = 1,     /* NULL handle/pointer, bad sizes, misaligned or overlapping buffers */
     LSTM_DYN_ERR_HIP = 2,         /* a HIP runtime call failed */
     LSTM_DYN_ERR_NOMEM = 3,       /* device workspace allocation failed */
-    LSTM_DYN_ERR_UNSUPPORTED = 4, /* sizes outside what this build's kernels cover */
+    LSTM_DYN_ERR_UNSUPPORTED = 4, /* sizes outside what the compiled kernel variants cover */
     LSTM_DYN_ERR_BAD_LENGTHS = 5, /* (device status) a length was outside [0, T_max] and was clamped */
     LSTM_DYN_ERR_TIMEOUT = 6      /* (device status) a grid barrier wait exceeded its bound */
 };
@@ -117,7 +117,7 @@ typedef struct {
  *   B >= 1, D >= 1, H >= 1, T_max >= 1; dtype LSTM_DYN_F32/BF16; mode
  *   LSTM_DYN_PERSISTENT/PER_STEP.  *out receives the handle (NULL on error).
  * Returns LSTM_DYN_OK, ERR_INVALID (bad arguments; no HIP call is made),
- * ERR_UNSUPPORTED (sizes this build's kernels do not cover), ERR_HIP, ERR_NOMEM.
+ * ERR_UNSUPPORTED (sizes the compiled kernel variants do not cover), ERR_HIP, ERR_NOMEM.
  */
 int lstm_dyn_create(lstm_dyn_t** out, int B, int D, int H, int T_max, int dtype, int mode);
 

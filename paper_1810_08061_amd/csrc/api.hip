@@ -80,7 +80,7 @@ extern "C" const char* lstm_dyn_strerror(int status) {
         case LSTM_DYN_ERR_INVALID: return "invalid argument";
         case LSTM_DYN_ERR_HIP: return "HIP runtime error";
         case LSTM_DYN_ERR_NOMEM: return "device workspace allocation failed";
-        case LSTM_DYN_ERR_UNSUPPORTED: return "sizes not supported by this build";
+        case LSTM_DYN_ERR_UNSUPPORTED: return "sizes not covered by the compiled kernel variants";
         case LSTM_DYN_ERR_BAD_LENGTHS: return "a sequence length was outside [0, T_max] and was clamped";
         case LSTM_DYN_ERR_TIMEOUT: return "a grid barrier wait exceeded its bound";
         default: return "unknown status";
