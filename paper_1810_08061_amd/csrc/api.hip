@@ -110,7 +110,7 @@ extern "C" int lstm_dyn_plan(int B, int D, int H, int T, int dtype, int mode, in
     const int groups = (H + 4 * mt - 1) / (4 * mt);
     if (groups > num_cus) return LSTM_DYN_ERR_UNSUPPORTED;
     const int kneed = (H + kstep * kw - 1) / (kstep * kw);
-    int ksw = 1;
+    int ksw = bf16 ? 1 : 4;  // fp32 lanes load K-steps in groups of four
     while (ksw < kneed) ksw *= 2;
     const int nstate = (ntmax * mt + kw - 1) / kw;
     int nst = nstate;

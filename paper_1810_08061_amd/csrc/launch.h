@@ -16,7 +16,8 @@ struct Workspace {
     int32_t* offsets;   // [T_max + 1] first compact row of step t; offsets[t+1]-offsets[t] = active rows
     int32_t* rowsrc;    // [B * T_max] compact row -> b * T_max + t
     float* gx;          // [B * T_max][4H] x W + b for valid (b, t), gate-interleaved columns
-    void* hx;           // [2][bpad][hpad] recurrent operand (dtype), slot order; padding stays zero
+    void* hx;           // [2][bpad][hpad] recurrent operand (dtype), slot order; padding stays zero;
+                        // row-major for the per-step path, MFMA fragment order for the persistent loop
     unsigned* bar;      // grid-barrier counters: [0] global, [64 * (1 + x)] group x (zeroed by prep)
     float* z;           // [bpad][4H] per-step pre-activations (per-step mode only)
     void* wt;           // bf16: W transposed to [np][dp] (gate-interleaved rows, zero padded)

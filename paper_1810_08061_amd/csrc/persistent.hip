@@ -8,8 +8,8 @@
 // MFMA A-fragments for the whole loop.  Per step t:
 //   1. the KW waves split K = H; each forms partial C^T = U_slice^T h_t^T for
 //      the active rows (slots [0, active(t)) after the length sort), one
-//      16-row tile at a time, loading the next tile's h fragments before the
-//      current tile's MFMAs;
+//      16-row tile at a time, with the h fragments of the next two tiles
+//      loading while the current tile's MFMAs run;
 //   2. partials meet in LDS; the owning wave adds them and the prefetched
 //      Gx[t] (input projection + bias), applies the gate non-linearities and
 //      updates c (in its registers) and h; finished rows are not touched (the
@@ -29,8 +29,6 @@
 // one of eight group counters, the last arrival of a group bumps the global
 // counter, and every workgroup polls the global counter.  The counters are
 // zeroed by the preparation kernel that runs before this one.
-#include <type_traits>
-
 #include "launch.h"
 
 namespace ldyn {
@@ -139,6 +137,23 @@ __device__ inline int kslot(int ks, int l) {
     else return ks * E::KSTEP + (l >> 4) * E::KPL;
 }
 
+// The operand buffer holds h in MFMA fragment order rather than row-major:
+// 16-row tiles, each cut along k into 1 KB blocks of 64 sixteen-byte chunks;
+// chunk q * 16 + r of a block holds row r of the tile and the q-th run of
+// 16 / sizeof(element) consecutive k.  Lane l's fragment of one K-step (or,
+// for fp32, of a group of four K-steps) is chunk l of one block, so a wave's
+// load is 1 KB of consecutive addresses (every lane quad hits one 64-byte
+// segment), and a workgroup's row segment of UPW <= 16 bytes stays inside
+// one chunk.  Byte offset of h[s][k] within one half of the buffer:
+template <typename E>
+__device__ inline unsigned hx_off(int s, int k, int hpad) {
+    constexpr int CK = 16 / (int)sizeof(typename E::store_t);  // elements per chunk
+    constexpr int KB = 4 * CK;                                 // k per block
+    const int blk = (s >> 4) * (hpad / KB) + k / KB;
+    const int chunk = ((k % KB) / CK) * 16 + (s & 15);
+    return (unsigned)(blk * 64 + chunk) * 16u + (unsigned)(k % CK) * (unsigned)sizeof(typename E::store_t);
+}
+
 template <typename E, int MT, int KSW, int KW, int NST>
 __global__ void __launch_bounds__(KW * 64, 1)
 persistent_kernel(PersistParams p) {
@@ -215,20 +230,17 @@ persistent_kernel(PersistParams p) {
     // ---- Owned state: pair q = i*KW + w -> row tile q / MT, gate tile q % MT.
     // c and h live in registers and reach out_c / out_h once, after the loop.
     float cst[NST], hst[NST];
-    int obase[NST];  // out_h / out_c element offset of the owned (row, unit), batch order
 #pragma unroll
     for (int i = 0; i < NST; ++i) {
         const int q = i * KW + w, nt = q / MT, mt = q % MT;
         const int s = nt * 16 + (l & 15), u = u0 + mt * 4 + (l >> 4);
         cst[i] = 0.f;
         hst[i] = 0.f;
-        obase[i] = 0;
         if (nt < ntmax && s < B && u < H) {
             const size_t ib = (size_t)p.perm[s] * H + u;
-            obase[i] = (int)ib;
             hst[i] = p.h0[ib];  // read before the final write: exact aliasing out_h == h0 is allowed
             cst[i] = p.c0[ib];
-            IO::store(R, (unsigned)(s * hpad + u) * (unsigned)sizeof(S), hst[i]);
+            IO::store(R, hx_off<E>(s, u, hpad), hst[i]);
         }
     }
 
@@ -256,10 +268,13 @@ persistent_kernel(PersistParams p) {
         alive = grid_wait(p, 0, &lds_ok);
     }
 
-    constexpr bool GROUPED = E::KPL == 1 && KSW >= 4;  // fp32: 16-byte loads of 4 k
-    const unsigned lane_off =
-        (unsigned)((l & 15) * hpad + kw0 + (GROUPED ? 4 : E::KPL) * (l >> 4)) * (unsigned)sizeof(S);
-    constexpr unsigned KSTEP_BYTES = E::KSTEP * sizeof(S);
+    // fp32 lanes take 4 consecutive k for a group of four K-steps (one 16-byte
+    // load); bf16 lanes take 8 consecutive k per K-step.  Either way a load is
+    // one 1 KB block of the fragment-ordered buffer.
+    static_assert(E::KPL == 8 || KSW % 4 == 0, "fp32 variants need whole groups of four K-steps");
+    constexpr bool GROUPED = E::KPL == 1;
+    constexpr int KB = GROUPED ? 16 : 32;  // k per 1 KB block
+    const unsigned lane_off = (unsigned)(kw0 / KB) * 1024u + (unsigned)l * 16u;
     const unsigned tile_bytes = (unsigned)(16 * hpad) * (unsigned)sizeof(S);
     for (int t = 0; t < max_len && alive; ++t) {
         const bool tr = p.trace && blockIdx.x == 0 && tid == 0;
@@ -269,58 +284,103 @@ persistent_kernel(PersistParams p) {
         const unsigned cur = (unsigned)(t & 1) * hx_half;
         const unsigned nxt = (unsigned)((t + 1) & 1) * hx_half;
 
-        // One register set of h fragments, reloaded for the next row tile
-        // right after each MFMA consumes it, so the next tile's loads are in
-        // flight while this tile's MFMAs run.
-        F fr[KSW];
-        auto tile_base = [&](int nt) { return cur + (unsigned)nt * tile_bytes + lane_off; };
-        // fragment loads of one row tile: ks, or the group of four starting at ks
-        auto load_frag = [&](unsigned base, int ks) {
+        // Register sets of h fragments pipeline the row tiles of a chunk: with
+        // three sets, tiles j+1 and j+2 are loading while tile j is
+        // multiplied; variants whose U slice leaves too few registers use two.
+        // The chunk is run by one of a few straight-line schedules (short
+        // chunks, then a steady loop followed by a tail), so every load is for
+        // a real tile and on every path the compiler waits for exactly the set
+        // about to be consumed.
+        constexpr int FRAG_REGS = KSW * (int)sizeof(F) / 4;
+        constexpr int DEPTH = MT * FRAG_REGS + 3 * FRAG_REGS <= 128 ? 3 : 2;
+        F f0[KSW], f1[KSW], f2[DEPTH == 3 ? KSW : 1];
+        auto load_tile = [&](F* f, int nt) {
+            const unsigned base = cur + (unsigned)nt * tile_bytes + lane_off;
             if constexpr (GROUPED) {
-                if ((ks & 3) == 0) {
-                    typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-                    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(R, base + (ks >> 2) * 64u, 0, P_SC1);
+                typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) fr[ks + j] = __uint_as_float(v[j]);
+                for (int ks = 0; ks < KSW; ks += 4) {
+                    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(R, base + (ks >> 2) * 1024u, 0, P_SC1);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) f[ks + j] = __uint_as_float(v[j]);
                 }
             } else {
-                fr[ks] = IO::load(R, base + ks * KSTEP_BYTES);
+#pragma unroll
+                for (int ks = 0; ks < KSW; ++ks) f[ks] = IO::load(R, base + ks * 1024u);
             }
         };
 
         for (int ntc0 = 0; ntc0 < nt_act; ntc0 += NTC) {
             const int nchunk = min(NTC, nt_act - ntc0);
-            {
-                const unsigned base = tile_base(ntc0);
-#pragma unroll
-                for (int ks = 0; ks < KSW; ++ks) load_frag(base, ks);
-            }
-            // one row tile's partial products; with RELOAD, each fragment register
-            // is refilled from tile j + 1 right after its MFMA has consumed it
-            auto mma_tile = [&](int j, auto reload_tag) {
-                constexpr bool RELOAD = decltype(reload_tag)::value;
-                const unsigned nbase = tile_base(ntc0 + j + 1);
+            // partial products of row tile j of the chunk into its LDS slot
+            auto mma_tile = [&](const F* f, int j) {
                 f32x4_t acc[MT];
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int ks = 0; ks < KSW; ++ks) {
+                for (int ks = 0; ks < KSW; ++ks)
 #pragma unroll
-                    for (int mt = 0; mt < MT; ++mt) acc[mt] = E::mfma(afrag[mt][ks], fr[ks], acc[mt]);
-                    if constexpr (RELOAD) {
-                        if constexpr (GROUPED) {
-                            if ((ks & 3) == 3) load_frag(nbase, ks - 3);
-                        } else {
-                            load_frag(nbase, ks);
-                        }
-                    }
-                }
+                    for (int mt = 0; mt < MT; ++mt) acc[mt] = E::mfma(afrag[mt][ks], f[ks], acc[mt]);
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt)
                     *reinterpret_cast<f32x4_t*>(lds + ((((w * NTC + j) * MT + mt) * 64 + l) << 2)) = acc[mt];
             };
-            for (int j = 0; j + 1 < nchunk; ++j) mma_tile(j, std::true_type{});
-            mma_tile(nchunk - 1, std::false_type{});  // last tile: nothing left to load
+            if (nchunk == 1) {
+                load_tile(f0, ntc0);
+                mma_tile(f0, 0);
+            } else if (nchunk == 2 || DEPTH == 2) {
+                load_tile(f0, ntc0);
+                load_tile(f1, ntc0 + 1);
+                int j = 0;
+                for (; j + 3 < nchunk; j += 2) {
+                    mma_tile(f0, j);
+                    load_tile(f0, ntc0 + j + 2);
+                    mma_tile(f1, j + 1);
+                    load_tile(f1, ntc0 + j + 3);
+                }
+                if (nchunk - j == 2) {  // 2 or 3 tiles left, the first two loaded
+                    mma_tile(f0, j);
+                    mma_tile(f1, j + 1);
+                } else {
+                    mma_tile(f0, j);
+                    load_tile(f0, ntc0 + j + 2);
+                    mma_tile(f1, j + 1);
+                    mma_tile(f0, j + 2);
+                }
+            } else if constexpr (DEPTH == 3) {
+                load_tile(f0, ntc0);
+                load_tile(f1, ntc0 + 1);
+                load_tile(f2, ntc0 + 2);
+                int j = 0;
+                for (; j + 5 < nchunk; j += 3) {
+                    mma_tile(f0, j);
+                    load_tile(f0, ntc0 + j + 3);
+                    mma_tile(f1, j + 1);
+                    load_tile(f1, ntc0 + j + 4);
+                    mma_tile(f2, j + 2);
+                    load_tile(f2, ntc0 + j + 5);
+                }
+                const int rest = nchunk - j;  // 3, 4 or 5 tiles, the first three loaded
+                if (rest == 3) {
+                    mma_tile(f0, j);
+                    mma_tile(f1, j + 1);
+                    mma_tile(f2, j + 2);
+                } else if (rest == 4) {
+                    mma_tile(f0, j);
+                    load_tile(f0, ntc0 + j + 3);
+                    mma_tile(f1, j + 1);
+                    mma_tile(f2, j + 2);
+                    mma_tile(f0, j + 3);
+                } else {
+                    mma_tile(f0, j);
+                    load_tile(f0, ntc0 + j + 3);
+                    mma_tile(f1, j + 1);
+                    load_tile(f1, ntc0 + j + 4);
+                    mma_tile(f2, j + 2);
+                    mma_tile(f0, j + 3);
+                    mma_tile(f1, j + 4);
+                }
+            }
             __syncthreads();
             if (tr) p.trace[4 * t + 1] = wall_clock64();
             // reduce, gates, state update, own slice of h_{t+1}
@@ -351,7 +411,7 @@ persistent_kernel(PersistParams p) {
                 const int rows = min(act - ntc0 * 16, nchunk * 16);
                 for (int r = tid; r < rows; r += KW * 64) {
                     const int s = ntc0 * 16 + r;
-                    const unsigned off = nxt + (unsigned)(s * hpad + u0) * (unsigned)sizeof(S);
+                    const unsigned off = nxt + hx_off<E>(s, u0, hpad);
                     if constexpr (SEG_BYTES == 16) {
                         typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
                         __builtin_amdgcn_raw_buffer_store_b128(
@@ -380,8 +440,9 @@ persistent_kernel(PersistParams p) {
         const int q = i * KW + w, nt = q / MT, mt = q % MT;
         const int s = nt * 16 + (l & 15), u = u0 + mt * 4 + (l >> 4);
         if (nt < ntmax && s < B && u < H) {
-            p.out_c[obase[i]] = cst[i];
-            p.out_h[obase[i]] = hst[i];
+            const size_t ib = (size_t)p.perm[s] * H + u;
+            p.out_c[ib] = cst[i];
+            p.out_h[ib] = hst[i];
         }
     }
 }
@@ -399,7 +460,7 @@ struct Variant { int bf16, mt, ksw, kw, nst; persist_fn f; };
 #define PV(BF, ET, MT, KS, KW, NS) {BF, MT, KS, KW, NS, persistent_kernel<ET, MT, KS, KW, NS>}
 #define PV_NST(BF, ET, MT, KS, KW) PV(BF, ET, MT, KS, KW, 2), PV(BF, ET, MT, KS, KW, 8)
 static const Variant kVariants[] = {
-    PV_NST(0, EltF32, 1, 1, 4), PV_NST(0, EltF32, 1, 2, 4), PV_NST(0, EltF32, 1, 4, 4),
+    PV_NST(0, EltF32, 1, 4, 4),
     PV_NST(0, EltF32, 1, 8, 4), PV_NST(0, EltF32, 1, 16, 4), PV_NST(0, EltF32, 1, 32, 4),
     PV_NST(0, EltF32, 1, 64, 4),
     PV_NST(1, EltBF16, 1, 1, 4), PV_NST(1, EltBF16, 1, 2, 4), PV_NST(1, EltBF16, 1, 4, 4),

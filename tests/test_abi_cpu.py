@@ -33,7 +33,7 @@ def test_strerror_covers_codes():
 
 
 @pytest.mark.parametrize("B,D,H,T,dt,mt,groups,ksw,kw", [
-    (4, 16, 32, 20, ld.F32, 1, 1, 2, 4),          # one workgroup, one launch
+    (4, 16, 32, 20, ld.F32, 1, 1, 4, 4),          # one workgroup, one launch
     (32, 256, 256, 100, ld.F32, 1, 64, 16, 4),
     (64, 512, 512, 200, ld.BF16, 1, 128, 4, 4),
     (128, 1024, 1024, 500, ld.BF16, 1, 256, 8, 4),
