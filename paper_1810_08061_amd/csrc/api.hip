@@ -52,7 +52,7 @@ Layout layout_of(int B, int D, int H, int T, int bf16, int mode, int bpad, int h
     L.offsets = take(4LL * (T + 1));
     L.rowsrc = take(4LL * B * T);
     L.gx = take(16LL * H * B * T);
-    L.hx = take(2LL * bpad * hpad * (bf16 ? 2 : 4));
+    L.hx = take(4LL * bpad * hpad * (bf16 ? 2 : 4));
     L.bar = take(4LL * BAR_WORDS);
     L.z = take(mode == LSTM_DYN_PER_STEP ? 16LL * H * bpad : 0);
     if (bf16) {
@@ -122,7 +122,7 @@ extern "C" int lstm_dyn_plan(int B, int D, int H, int T, int dtype, int mode, in
     out->kw = kw;
     out->hpad = ksw * kstep * kw;
     out->bpad = ntmax * 16;
-    out->lds_bytes = persistent_lds_bytes(bf16, mt, out->hpad);
+    out->lds_bytes = persistent_lds_bytes(bf16, mt, kw, nst, out->hpad);
     out->nstate = nst;
     out->workspace_bytes =
         layout_of(B, D, H, T, bf16, mode, out->bpad, out->hpad).total;

@@ -16,8 +16,8 @@ struct Workspace {
     int32_t* offsets;   // [T_max + 1] first compact row of step t; offsets[t+1]-offsets[t] = active rows
     int32_t* rowsrc;    // [B * T_max] compact row -> b * T_max + t
     float* gx;          // [B * T_max][4H] x W + b for valid (b, t), gate-interleaved columns
-    void* hx;           // [2][bpad][hpad] recurrent operand (dtype), slot order; padding stays zero;
-                        // row-major for the per-step path, MFMA fragment order for the persistent loop
+    void* hx;           // [4][bpad][hpad] recurrent operand (dtype), slot order; row-major in two
+                        // buffers for the per-step path, MFMA fragment order in four for the persistent loop
     unsigned* bar;      // grid-barrier counters: [0] global, [64 * (1 + x)] group x (zeroed by prep)
     float* z;           // [bpad][4H] per-step pre-activations (per-step mode only)
     void* wt;           // bf16: W transposed to [np][dp] (gate-interleaved rows, zero padded)
@@ -59,7 +59,7 @@ hipError_t launch_persistent(const Dims& d, const PersistentConfig& pc, const vo
 int persistent_blocks_per_cu(int bf16, int mt, int ksw, int kw, int nst, int lds_bytes);
 // Compiled variant with exactly (mt, kw, ksw) and the smallest state capacity >= nstate.
 bool persistent_pick_variant(int bf16, int mt, int kw, int ksw, int nstate, int* nst);
-int persistent_lds_bytes(int bf16, int mt, int hpad);
+int persistent_lds_bytes(int bf16, int mt, int kw, int nst, int hpad);
 
 // Whole forward in one single-workgroup launch (H <= 32).
 bool small_pick(int bf16, int B, int D, int H, int* kd, int* nt);

@@ -33,7 +33,7 @@
 
 namespace ldyn {
 
-constexpr int P_LDS_PARTIAL_KB = 128;   // LDS for cross-wave partial sums
+constexpr int P_LDS_KB = 144;           // dynamic LDS for partial sums and the Gx prefetch
 constexpr int P_SC1 = 16;               // buffer-instruction cache policy: device scope
 
 struct PersistParams {
@@ -62,6 +62,15 @@ __device__ inline int logical_group(int bid, int groups) {
 }
 
 __device__ inline void drain_stores() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Wave-uniform read of data written before this kernel started, through the
+// scalar data cache, so that it does not queue behind the vector loads in
+// flight.
+__device__ inline int load_uniform(const int32_t* ptr) {
+    int v;
+    asm volatile("s_load_dword %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(v) : "s"(ptr) : "memory");
+    return v;
+}
 
 // Barrier k (k = 0, 1, ...), split in two so work can be issued between the
 // arrival and the wait.  Arrival happens only after every wave of the
@@ -105,6 +114,9 @@ __device__ inline bool grid_wait(const PersistParams& p, int k, int* lds_ok) {
 }
 
 // Device-scope loads/stores of the operand buffer through a buffer resource.
+// An operand slot whose value for the coming step has not arrived yet holds
+// the all-ones pattern (a NaN).  operand() never produces it: a NaN h that
+// would convert to it is stored as the canonical quiet NaN instead.
 template <typename E> struct HxIO;
 template <> struct HxIO<EltBF16> {
     __device__ static inline bf16x8_t load(__amdgpu_buffer_rsrc_t R, unsigned byte_off) {
@@ -112,17 +124,49 @@ template <> struct HxIO<EltBF16> {
         const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(R, byte_off, 0, P_SC1);
         return __builtin_bit_cast(bf16x8_t, v);
     }
+    __device__ static inline __bf16 operand(float h) {
+        const unsigned short b = __builtin_bit_cast(unsigned short, (__bf16)h);
+        return __builtin_bit_cast(__bf16, b == 0xffffu ? (unsigned short)0x7fc0u : b);
+    }
     __device__ static inline void store(__amdgpu_buffer_rsrc_t R, unsigned byte_off, float h) {
-        const __bf16 b = (__bf16)h;
-        __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, b), R, byte_off, 0, P_SC1);
+        __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, operand(h)), R, byte_off, 0,
+                                              P_SC1);
+    }
+    // true if any of the KSW fragments holds the marker in one of its elements
+    template <int KSW>
+    __device__ static inline bool has_marker(const bf16x8_t* f) {
+        typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+        typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+        u16x2 m = {0, 0};
+#pragma unroll
+        for (int ks = 0; ks < KSW; ++ks) {
+            const u32x4 v = __builtin_bit_cast(u32x4, f[ks]);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const unsigned d = v[j];  // (a bit_cast of the subscript itself reads element 0)
+                m = __builtin_elementwise_max(m, __builtin_bit_cast(u16x2, d));
+            }
+        }
+        return m[0] == 0xffffu || m[1] == 0xffffu;
     }
 };
 template <> struct HxIO<EltF32> {
     __device__ static inline float load(__amdgpu_buffer_rsrc_t R, unsigned byte_off) {
         return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(R, byte_off, 0, P_SC1));
     }
+    __device__ static inline float operand(float h) {
+        const unsigned b = __float_as_uint(h);
+        return __uint_as_float(b == 0xffffffffu ? 0x7fc00000u : b);
+    }
     __device__ static inline void store(__amdgpu_buffer_rsrc_t R, unsigned byte_off, float h) {
-        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(h), R, byte_off, 0, P_SC1);
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(operand(h)), R, byte_off, 0, P_SC1);
+    }
+    template <int KSW>
+    __device__ static inline bool has_marker(const float* f) {
+        unsigned m = 0;
+#pragma unroll
+        for (int ks = 0; ks < KSW; ++ks) m = max(m, __float_as_uint(f[ks]));
+        return m == 0xffffffffu;
     }
 };
 
@@ -154,30 +198,51 @@ __device__ inline unsigned hx_off(int s, int k, int hpad) {
     return (unsigned)(blk * 64 + chunk) * 16u + (unsigned)(k % CK) * (unsigned)sizeof(typename E::store_t);
 }
 
+// Dynamic LDS of one workgroup during the loop: partial sums of NTC row tiles
+// ([KW][NTC][MT][64 lanes][4 floats]) followed by the prefetched Gx of the
+// owned pairs ([NST][KW][64 lanes][4 floats]).
+template <int MT, int KW, int NST>
+struct PLayout {
+    static constexpr int GX_KB = NST * KW;
+    static constexpr int NTC = (P_LDS_KB - GX_KB) / (KW * MT);  // row tiles per chunk
+    static constexpr int GX_OFF = NTC * KW * MT * 256;          // in floats
+    static constexpr int BYTES = (NTC * KW * MT + GX_KB) * 1024;
+};
+
 template <typename E, int MT, int KSW, int KW, int NST>
 __global__ void __launch_bounds__(KW * 64, 1)
 persistent_kernel(PersistParams p) {
     using S = typename E::store_t;
     using F = typename E::frag_t;
     using IO = HxIO<E>;
-    constexpr int NTC = P_LDS_PARTIAL_KB / (KW * MT);  // row tiles per LDS chunk
+    using LY = PLayout<MT, KW, NST>;
+    constexpr int NTC = LY::NTC;
     static_assert(NTC >= 1, "partial buffer too small");
-    extern __shared__ __attribute__((aligned(16))) float lds[];  // [KW][NTC][MT][64][4]
-    __shared__ int lds_ok;
+    extern __shared__ __attribute__((aligned(16))) float lds[];
+    __shared__ int lds_ok, lds_abort, lds_nan;
     constexpr int UPW = 4 * MT;                      // hidden units per workgroup
     constexpr int SEG_BYTES = UPW * (int)sizeof(S);  // one row of this workgroup's h slice
     static_assert(SEG_BYTES == 8 || SEG_BYTES == 16, "h row segment must be 8 or 16 bytes");
     __shared__ __attribute__((aligned(16))) S hstage[NTC * 16 * UPW];
 
-    const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
+    // tid and l are re-read through empty asm statements at the top of each
+    // step and chunk, so values derived from them (addresses, row indices)
+    // are recomputed where used instead of being kept live across the loop.
+    int tid = threadIdx.x, l = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    float* const gxs = lds + LY::GX_OFF + w * 256;  // this wave's Gx slots, 1 KB per owned pair
     const int g = logical_group(blockIdx.x, p.groups);
     const int H = p.H, H4 = 4 * H, hpad = p.hpad;
     const int u0 = g * 4 * MT;
     const int kw0 = w * KSW * E::KSTEP;
     const int B = p.B, ntmax = (B + 15) >> 4;
-    const unsigned hx_half = (unsigned)(p.bpad * hpad) * (unsigned)sizeof(S);
+    const unsigned hx_part = (unsigned)(p.bpad * hpad) * (unsigned)sizeof(S);  // one of four buffers
     const __amdgpu_buffer_rsrc_t R =
-        __builtin_amdgcn_make_buffer_rsrc(p.hx, (short)0, (int)(2u * hx_half), 0x00020000);
+        __builtin_amdgcn_make_buffer_rsrc(p.hx, (short)0, (int)(4u * hx_part), 0x00020000);
+    if (tid == 0) {
+        lds_abort = 0;
+        lds_nan = 0;
+    }
     F afrag[MT][KSW];
 
     // ---- U slice -> registers (A-fragments of U^T; rows = gate-interleaved columns).
@@ -227,6 +292,21 @@ persistent_kernel(PersistParams p) {
         __syncthreads();  // the LDS is reused for partial sums
     }
 
+    const int max_len = p.meta->max_len;
+    // Marks this workgroup's slice of rows [0, rows) of one buffer as not yet written.
+    auto mark_rows = [&](unsigned part, int rows) {
+        for (int r = tid; r < rows; r += KW * 64) {
+            const unsigned off = part + hx_off<E>(r, u0, hpad);
+            if constexpr (SEG_BYTES == 16) {
+                typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+                __builtin_amdgcn_raw_buffer_store_b128(u32x4{~0u, ~0u, ~0u, ~0u}, R, off, 0, P_SC1);
+            } else {
+                typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+                __builtin_amdgcn_raw_buffer_store_b64(u32x2{~0u, ~0u}, R, off, 0, P_SC1);
+            }
+        }
+    };
+
     // ---- Owned state: pair q = i*KW + w -> row tile q / MT, gate tile q % MT.
     // c and h live in registers and reach out_c / out_h once, after the loop.
     float cst[NST], hst[NST];
@@ -244,27 +324,35 @@ persistent_kernel(PersistParams p) {
         }
     }
 
-    // Gx[t] for the owned pairs, prefetched while the barrier wait is pending.
-    f32x4_t gxv[NST];
-    auto prefetch_gx = [&](int t) {
-        const int off = p.offsets[t];
-        const int act = p.offsets[t + 1] - off;
+    // Gx[t] of the owned pairs goes straight from memory into this wave's LDS
+    // slots (no registers held while it is in flight); lanes of pairs that
+    // are not active fetch row 0 instead, which is never read.
+    auto prefetch_gx = [&](int off, int act) {
+        int lo = l;
+        asm volatile("" : "+v"(lo));
 #pragma unroll
         for (int i = 0; i < NST; ++i) {
             const int q = i * KW + w, nt = q / MT, mt = q % MT;
-            const int s = nt * 16 + (l & 15), u = u0 + mt * 4 + (l >> 4);
+            const int s = nt * 16 + (lo & 15), u = u0 + mt * 4 + (lo >> 4);
             const bool ok = s < act && u < H;
-            const size_t row = ok ? (size_t)(off + s) : 0;
-            const f32x4_t v = *reinterpret_cast<const f32x4_t*>(p.gx + row * H4 + 4 * (ok ? u : 0));
-            gxv[i] = ok ? v : f32x4_t{0.f, 0.f, 0.f, 0.f};
+            const float* src = p.gx + (ok ? (size_t)(off + s) * H4 + 4 * u : 0);
+            __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)(gxs + i * KW * 256),
+                                             16, 0, 0);
         }
     };
 
-    const int max_len = p.meta->max_len;
+    // Row offsets of steps t .. t+3 travel in registers; the one for t+4 is
+    // loaded a step ahead.
+    auto offset_at = [&](int t) { return load_uniform(p.offsets + min(t, max_len)); };
+    int o0 = offset_at(0), o1 = offset_at(1), o2 = offset_at(2), o3 = offset_at(3);
+
+    // h_0 sits in buffer 0 and buffer 1 is marked for h_1; one grid barrier
+    // makes both visible.  After that the steps synchronise through the data.
+    mark_rows(hx_part, o2 - o1);
     bool alive = true;
     if (max_len > 0) {
         grid_arrive(p, 0);
-        prefetch_gx(0);
+        prefetch_gx(o0, o1 - o0);
         alive = grid_wait(p, 0, &lds_ok);
     }
 
@@ -277,23 +365,37 @@ persistent_kernel(PersistParams p) {
     const unsigned lane_off = (unsigned)(kw0 / KB) * 1024u + (unsigned)l * 16u;
     const unsigned tile_bytes = (unsigned)(16 * hpad) * (unsigned)sizeof(S);
     for (int t = 0; t < max_len && alive; ++t) {
+        asm volatile("" : "+v"(tid), "+v"(l));
         const bool tr = p.trace && blockIdx.x == 0 && tid == 0;
         if (tr) p.trace[4 * t] = wall_clock64();
-        const int act = p.offsets[t + 1] - p.offsets[t];
+        const int o4 = offset_at(t + 4);  // used next step
+        const int act = o1 - o0;
         const int nt_act = (act + 15) >> 4;
-        const unsigned cur = (unsigned)(t & 1) * hx_half;
-        const unsigned nxt = (unsigned)((t + 1) & 1) * hx_half;
+        const unsigned cur = (unsigned)(t & 3) * hx_part;        // h_t
+        const unsigned nxt = (unsigned)((t + 1) & 3) * hx_part;  // h_{t+1}
+        // Buffer (t+2) mod 4 still holds h_{t-2}.  Having seen rows [0, act(t-1))
+        // of every workgroup's h_{t-1}, this workgroup knows that every
+        // workgroup is done reading h_{t-2} except for row tiles at or beyond
+        // act(t-1) >= act(t+2), so rows [0, act(t+2)) can be marked for h_{t+2}.
+        // The marks drain before this step's first h_{t+1} store; a reader
+        // sees that row before it moves on to h_{t+2}.
+        mark_rows((unsigned)((t + 2) & 3) * hx_part, o3 - o2);
 
         // Register sets of h fragments pipeline the row tiles of a chunk: with
         // three sets, tiles j+1 and j+2 are loading while tile j is
-        // multiplied; variants whose U slice leaves too few registers use two.
+        // multiplied; variants whose U slice leaves fewer registers use two,
+        // or one set whose K-steps are reloaded for the next tile as soon as
+        // their MFMAs have been issued.
         // The chunk is run by one of a few straight-line schedules (short
         // chunks, then a steady loop followed by a tail), so every load is for
         // a real tile and on every path the compiler waits for exactly the set
         // about to be consumed.
         constexpr int FRAG_REGS = KSW * (int)sizeof(F) / 4;
-        constexpr int DEPTH = MT * FRAG_REGS + 3 * FRAG_REGS <= 128 ? 3 : 2;
-        F f0[KSW], f1[KSW], f2[DEPTH == 3 ? KSW : 1];
+        constexpr int REG_BUDGET = KW <= 8 ? 256 : 2048 / KW;  // VGPRs per lane with KW / 4 waves per SIMD
+        constexpr int DEPTH = (MT + 3) * FRAG_REGS <= REG_BUDGET / 2   ? 3
+                              : (MT + 2) * FRAG_REGS <= REG_BUDGET / 2 ? 2
+                                                                       : 1;
+        F f0[KSW], f1[DEPTH >= 2 ? KSW : 1], f2[DEPTH == 3 ? KSW : 1];
         auto load_tile = [&](F* f, int nt) {
             const unsigned base = cur + (unsigned)nt * tile_bytes + lane_off;
             if constexpr (GROUPED) {
@@ -310,9 +412,60 @@ persistent_kernel(PersistParams p) {
             }
         };
 
+        bool aborted = false;
         for (int ntc0 = 0; ntc0 < nt_act; ntc0 += NTC) {
+            asm volatile("" : "+v"(tid), "+v"(l));
             const int nchunk = min(NTC, nt_act - ntc0);
-            // partial products of row tile j of the chunk into its LDS slot
+            // Bounded waits: past the deadline the wave gives up, flags the
+            // workgroup and the status, and the loop ends after this chunk.
+            auto expired = [&](unsigned long long t0) {
+                if (wall_clock64() - t0 <= p.timeout_ticks) return false;
+                if (l == 0) {
+                    lds_abort = 1;
+                    __hip_atomic_fetch_or(&p.meta->status, STATUS_TIMEOUT, __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT);
+                }
+                return true;
+            };
+            // Reloads tile j until its active rows hold no marker.
+            auto poll_tile = [&](F* f, int j) {
+                const bool mine = ntc0 * 16 + j * 16 + (l & 15) < act;
+                if (__builtin_amdgcn_ballot_w64(mine && IO::template has_marker<KSW>(f)) == 0) return;
+                const unsigned long long t0 = wall_clock64();
+                do {
+                    if (expired(t0)) return;
+                    __builtin_amdgcn_s_sleep(1);
+                    load_tile(f, ntc0 + j);
+                } while (__builtin_amdgcn_ballot_w64(mine && IO::template has_marker<KSW>(f)) != 0);
+            };
+            // Tile j's products with each K-step's fragment reloaded from tile
+            // j+1 right after its MFMAs (one register set in flight).
+            auto mma_roll = [&](F* f, int j) {
+                f32x4_t acc[MT];
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+                const unsigned next = cur + (unsigned)(ntc0 + j + 1) * tile_bytes + lane_off;
+#pragma unroll
+                for (int ks = 0; ks < KSW; ++ks) {
+#pragma unroll
+                    for (int mt = 0; mt < MT; ++mt) acc[mt] = E::mfma(afrag[mt][ks], f[ks], acc[mt]);
+                    if constexpr (GROUPED) {
+                        if ((ks & 3) == 3) {
+                            typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+                            const u32x4 v =
+                                __builtin_amdgcn_raw_buffer_load_b128(R, next + (ks >> 2) * 1024u, 0, P_SC1);
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) f[ks - 3 + e] = __uint_as_float(v[e]);
+                        }
+                    } else {
+                        f[ks] = IO::load(R, next + ks * 1024u);
+                    }
+                }
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+                    *reinterpret_cast<f32x4_t*>(lds + ((((w * NTC + j) * MT + mt) * 64 + l) << 2)) = acc[mt];
+            };
+            // Partial products of row tile j of the chunk into its LDS slot.
             auto mma_tile = [&](const F* f, int j) {
                 f32x4_t acc[MT];
 #pragma unroll
@@ -324,87 +477,145 @@ persistent_kernel(PersistParams p) {
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt)
                     *reinterpret_cast<f32x4_t*>(lds + ((((w * NTC + j) * MT + mt) * 64 + l) << 2)) = acc[mt];
+                // keep the reload of this register set after its MFMAs, so the
+                // set is reused rather than renamed
+                __builtin_amdgcn_sched_barrier(0);
             };
-            if (nchunk == 1) {
-                load_tile(f0, ntc0);
-                mma_tile(f0, 0);
-            } else if (nchunk == 2 || DEPTH == 2) {
-                load_tile(f0, ntc0);
-                load_tile(f1, ntc0 + 1);
-                int j = 0;
-                for (; j + 3 < nchunk; j += 2) {
-                    mma_tile(f0, j);
-                    load_tile(f0, ntc0 + j + 2);
-                    mma_tile(f1, j + 1);
-                    load_tile(f1, ntc0 + j + 3);
-                }
-                if (nchunk - j == 2) {  // 2 or 3 tiles left, the first two loaded
-                    mma_tile(f0, j);
-                    mma_tile(f1, j + 1);
+
+            // The chunk's first tile is polled until complete: that is where
+            // a workgroup waits for the others.  Later tiles are nearly always
+            // complete by then and are used as loaded.  A marker is a NaN, so
+            // one that slipped into an active row shows up as a NaN in that
+            // row's pre-activations; the chunk is then redone with every tile
+            // polled.  (A NaN that the redo reproduces comes from the data and
+            // is kept.)
+            bool exact = false;
+            for (;;) {
+                if (!exact) {
+                    load_tile(f0, ntc0);
+                    poll_tile(f0, 0);
+                    if (nchunk == 1) {
+                        mma_tile(f0, 0);
+                    } else if constexpr (DEPTH == 1) {
+                        for (int j = 0; j + 1 < nchunk; ++j) mma_roll(f0, j);
+                        mma_tile(f0, nchunk - 1);
+                    } else if (nchunk == 2 || DEPTH == 2) {
+                        load_tile(f1, ntc0 + 1);
+                        int j = 0;
+                        for (; j + 3 < nchunk; j += 2) {
+                            mma_tile(f0, j);
+                            load_tile(f0, ntc0 + j + 2);
+                            mma_tile(f1, j + 1);
+                            load_tile(f1, ntc0 + j + 3);
+                        }
+                        if (nchunk - j == 2) {  // 2 or 3 tiles left, the first two loaded
+                            mma_tile(f0, j);
+                            mma_tile(f1, j + 1);
+                        } else {
+                            mma_tile(f0, j);
+                            load_tile(f0, ntc0 + j + 2);
+                            mma_tile(f1, j + 1);
+                            mma_tile(f0, j + 2);
+                        }
+                    } else if constexpr (DEPTH == 3) {
+                        load_tile(f1, ntc0 + 1);
+                        load_tile(f2, ntc0 + 2);
+                        int j = 0;
+                        for (; j + 5 < nchunk; j += 3) {
+                            mma_tile(f0, j);
+                            load_tile(f0, ntc0 + j + 3);
+                            mma_tile(f1, j + 1);
+                            load_tile(f1, ntc0 + j + 4);
+                            mma_tile(f2, j + 2);
+                            load_tile(f2, ntc0 + j + 5);
+                        }
+                        const int rest = nchunk - j;  // 3, 4 or 5 tiles, the first three loaded
+                        if (rest == 3) {
+                            mma_tile(f0, j);
+                            mma_tile(f1, j + 1);
+                            mma_tile(f2, j + 2);
+                        } else if (rest == 4) {
+                            mma_tile(f0, j);
+                            load_tile(f0, ntc0 + j + 3);
+                            mma_tile(f1, j + 1);
+                            mma_tile(f2, j + 2);
+                            mma_tile(f0, j + 3);
+                        } else {
+                            mma_tile(f0, j);
+                            load_tile(f0, ntc0 + j + 3);
+                            mma_tile(f1, j + 1);
+                            load_tile(f1, ntc0 + j + 4);
+                            mma_tile(f2, j + 2);
+                            mma_tile(f0, j + 3);
+                            mma_tile(f1, j + 4);
+                        }
+                    }
                 } else {
-                    mma_tile(f0, j);
-                    load_tile(f0, ntc0 + j + 2);
-                    mma_tile(f1, j + 1);
-                    mma_tile(f0, j + 2);
+                    for (int j = 0; j < nchunk; ++j) {
+                        load_tile(f0, ntc0 + j);
+                        poll_tile(f0, j);
+                        mma_tile(f0, j);
+                    }
                 }
-            } else if constexpr (DEPTH == 3) {
-                load_tile(f0, ntc0);
-                load_tile(f1, ntc0 + 1);
-                load_tile(f2, ntc0 + 2);
-                int j = 0;
-                for (; j + 5 < nchunk; j += 3) {
-                    mma_tile(f0, j);
-                    load_tile(f0, ntc0 + j + 3);
-                    mma_tile(f1, j + 1);
-                    load_tile(f1, ntc0 + j + 4);
-                    mma_tile(f2, j + 2);
-                    load_tile(f2, ntc0 + j + 5);
+                __syncthreads();
+                if (lds_abort) {  // read by every wave between the same two barriers
+                    aborted = true;
+                    break;
                 }
-                const int rest = nchunk - j;  // 3, 4 or 5 tiles, the first three loaded
-                if (rest == 3) {
-                    mma_tile(f0, j);
-                    mma_tile(f1, j + 1);
-                    mma_tile(f2, j + 2);
-                } else if (rest == 4) {
-                    mma_tile(f0, j);
-                    load_tile(f0, ntc0 + j + 3);
-                    mma_tile(f1, j + 1);
-                    mma_tile(f2, j + 2);
-                    mma_tile(f0, j + 3);
-                } else {
-                    mma_tile(f0, j);
-                    load_tile(f0, ntc0 + j + 3);
-                    mma_tile(f1, j + 1);
-                    load_tile(f1, ntc0 + j + 4);
-                    mma_tile(f2, j + 2);
-                    mma_tile(f0, j + 3);
-                    mma_tile(f1, j + 4);
+                if (tr && ntc0 == 0 && !exact) p.trace[4 * t + 1] = wall_clock64();
+                // pre-activations of the owned pairs of this chunk.  The lane id
+                // passes through an empty asm so the per-pair indices are
+                // recomputed here rather than kept live across the loop.
+                int lo = l;
+                asm volatile("" : "+v"(lo));
+                asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's Gx prefetch has landed
+                bool nan = false;
+#pragma unroll
+                for (int i = 0; i < NST; ++i) {
+                    const int q = i * KW + w, nt = q / MT, mt = q % MT;
+                    const int j = nt - ntc0;
+                    const int s = nt * 16 + (lo & 15), u = u0 + mt * 4 + (lo >> 4);
+                    if (j < 0 || j >= nchunk || s >= act || u >= H) continue;
+                    f32x4_t z = *reinterpret_cast<const f32x4_t*>(gxs + i * KW * 256 + 4 * lo);
+#pragma unroll
+                    for (int ww = 0; ww < KW; ++ww)
+                        z += *reinterpret_cast<const f32x4_t*>(lds + ((((ww * NTC + j) * MT + mt) * 64 + lo) << 2));
+                    nan |= (z[0] != z[0]) | (z[1] != z[1]) | (z[2] != z[2]) | (z[3] != z[3]);
+                    // kept in the first wave's partial slot of the pair, which
+                    // only this lane reads from here on
+                    *reinterpret_cast<f32x4_t*>(lds + (((j * MT + mt) * 64 + lo) << 2)) = z;
                 }
+                if (exact) break;
+                if (__builtin_amdgcn_ballot_w64(nan) != 0 && l == 0) lds_nan = 1;
+                __syncthreads();
+                const bool redo = lds_nan != 0;
+                if (!redo) break;
+                __syncthreads();  // every wave has read the flag
+                if (tid == 0) lds_nan = 0;
+                exact = true;
             }
-            __syncthreads();
-            if (tr) p.trace[4 * t + 1] = wall_clock64();
-            // reduce, gates, state update, own slice of h_{t+1}
+            if (aborted) break;
+            // gates, state update, own slice of h_{t+1}
+            int lo = l;
+            asm volatile("" : "+v"(lo));
 #pragma unroll
             for (int i = 0; i < NST; ++i) {
                 const int q = i * KW + w, nt = q / MT, mt = q % MT;
                 const int j = nt - ntc0;
                 if (j < 0 || j >= nchunk) continue;
-                const int s = nt * 16 + (l & 15), u = u0 + mt * 4 + (l >> 4);
+                const int s = nt * 16 + (lo & 15), u = u0 + mt * 4 + (lo >> 4);
                 if (s >= act) continue;
                 if (u >= H) {  // ragged last workgroup: its padding units stay zero
                     hstage[(s - ntc0 * 16) * UPW + (u - u0)] = E::from_f32(0.0f);
                     continue;
                 }
-                f32x4_t z = gxv[i];
-#pragma unroll
-                for (int ww = 0; ww < KW; ++ww)
-                    z += *reinterpret_cast<const f32x4_t*>(lds + ((((ww * NTC + j) * MT + mt) * 64 + l) << 2));
                 float c = cst[i], h;
-                lstm_cell(z, c, h);
+                lstm_cell(*reinterpret_cast<const f32x4_t*>(lds + (((j * MT + mt) * 64 + lo) << 2)), c, h);
                 cst[i] = c;
                 hst[i] = h;
-                hstage[(s - ntc0 * 16) * UPW + (u - u0)] = E::from_f32(h);
+                hstage[(s - ntc0 * 16) * UPW + (u - u0)] = IO::operand(h);
             }
+            if (ntc0 == 0) drain_stores();  // the marks above
             __syncthreads();
             // this workgroup's slice of h_{t+1}: one UPW-unit row segment per active row
             {
@@ -424,13 +635,17 @@ persistent_kernel(PersistParams p) {
                 }
             }
         }
-        if (tr) p.trace[4 * t + 2] = wall_clock64();
-        if (t + 1 < max_len) {
-            grid_arrive(p, t + 1);
-            if (tr) p.trace[4 * t + 3] = wall_clock64();
-            prefetch_gx(t + 1);  // in flight during the wait
-            alive = grid_wait(p, t + 1, &lds_ok);
+        if (aborted) {
+            alive = false;
+            break;
         }
+        if (tr) p.trace[4 * t + 2] = wall_clock64();
+        if (t + 1 < max_len) prefetch_gx(o1, o2 - o1);  // in flight while h_{t+1} arrives
+        o0 = o1;
+        o1 = o2;
+        o2 = o3;
+        o3 = o4;
+        if (tr) p.trace[4 * t + 3] = wall_clock64();
     }
 
     if (p.trace && blockIdx.x == 0 && tid == 0) p.trace[4 * max_len] = wall_clock64();
@@ -455,9 +670,10 @@ persistent_kernel(PersistParams p) {
 // capacity that covers the batch.
 typedef void (*persist_fn)(PersistParams);
 
-struct Variant { int bf16, mt, ksw, kw, nst; persist_fn f; };
+struct Variant { int bf16, mt, ksw, kw, nst, lds_bytes; persist_fn f; };
 
-#define PV(BF, ET, MT, KS, KW, NS) {BF, MT, KS, KW, NS, persistent_kernel<ET, MT, KS, KW, NS>}
+#define PV(BF, ET, MT, KS, KW, NS) \
+    {BF, MT, KS, KW, NS, PLayout<MT, KW, NS>::BYTES, persistent_kernel<ET, MT, KS, KW, NS>}
 #define PV_NST(BF, ET, MT, KS, KW) PV(BF, ET, MT, KS, KW, 2), PV(BF, ET, MT, KS, KW, 8)
 static const Variant kVariants[] = {
     PV_NST(0, EltF32, 1, 4, 4),
@@ -488,10 +704,13 @@ bool persistent_pick_variant(int bf16, int mt, int kw, int ksw, int nstate, int*
 }
 
 // Dynamic LDS: the partial-sum chunks, or the staged U slice if larger.
-int persistent_lds_bytes(int bf16, int mt, int hpad) {
+int persistent_lds_bytes(int bf16, int mt, int kw, int nst, int hpad) {
     const int esz = bf16 ? 2 : 4;
-    const int staged = 16 * mt * (hpad + 16 / esz) * esz;
-    return staged > P_LDS_PARTIAL_KB * 1024 ? staged : P_LDS_PARTIAL_KB * 1024;
+    const int staged = 16 * mt * (hpad + 16 / esz) * esz;  // the U slice before the loop
+    int loop = 0;
+    for (const Variant& v : kVariants)
+        if (v.bf16 == bf16 && v.mt == mt && v.kw == kw && v.nst == nst) loop = v.lds_bytes;
+    return staged > loop ? staged : loop;
 }
 
 int persistent_blocks_per_cu(int bf16, int mt, int ksw, int kw, int nst, int lds_bytes) {
