@@ -164,6 +164,161 @@ inproj_bf16_kernel(InprojParams p) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// Variant fed by LDS DMA: both operand tiles go from memory straight into a
+// four-stage LDS ring (global/buffer load with an LDS destination), K = 32 per
+// stage, so three stages are in flight while one is multiplied and no
+// registers hold data in transit.  A DMA instruction writes 64 lanes x 16
+// bytes contiguously; with 64-byte operand rows that is 16 rows, and each
+// lane fetches the 16-byte chunk that belongs at its position under the XOR
+// swizzle chunk' = chunk ^ ((row >> 1) & 3), which spreads the MFMA fragment
+// reads (16 rows, one chunk) over all banks.  x rows past D (the K tail) are
+// fetched at an offset outside the buffer, which yields zeros.  Requires D a
+// multiple of 8, x 16-byte aligned and under 2 GiB.
+constexpr int GD_TILE = 256;
+constexpr int GD_BK = 32;
+constexpr int GD_STAGES = 4;
+constexpr int GD_HALF = GD_TILE * GD_BK * 2;  // bytes of one operand tile per stage
+constexpr int GD_STAGE = 2 * GD_HALF;
+constexpr int GD_OUT_LD = GD_TILE + 4;         // padded row of the output staging (floats)
+constexpr int GD_LDS_BYTES = 128 * GD_OUT_LD * 4;  // >= GD_STAGES * GD_STAGE
+static_assert(GD_LDS_BYTES >= GD_STAGES * GD_STAGE, "staging must cover the stages");
+
+struct InprojDmaParams {
+    InprojParams b;
+    unsigned x_bytes, wt_bytes;
+};
+
+__device__ inline int gd_swz(int r) { return (r >> 1) & 3; }
+
+__global__ void __launch_bounds__(IP_THREADS, 1)
+inproj_dma_kernel(InprojDmaParams q) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char gsm[];
+    const InprojParams& p = q.b;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;  // wave's 128 columns, 128 rows
+    const int H = p.H, N4 = 4 * H, D = p.D;
+    const int nrows = p.meta->total_rows;
+    const int ntc = (N4 + GD_TILE - 1) / GD_TILE;
+    const int ntiles = ntc * ((nrows + GD_TILE - 1) / GD_TILE);
+    const int nkb = p.dp / GD_BK;
+    const __amdgpu_buffer_rsrc_t Rx =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<__bf16*>(p.x), (short)0, (int)q.x_bytes, 0x00020000);
+    const __amdgpu_buffer_rsrc_t Rw =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<__bf16*>(p.wt), (short)0, (int)q.wt_bytes, 0x00020000);
+    typedef __attribute__((address_space(3))) void* lds_ptr_t;
+    // Consecutive workgroups sit on different XCDs: give each XCD a run of
+    // 32 consecutive tile numbers, and number the tiles so that such a run
+    // is a block of 4 row tiles x 8 column tiles: each x block is then shared
+    // by 8 workgroups of one L2 and each Wt block by 4.
+    const int g = (gridDim.x & 7) == 0 ? (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3) : blockIdx.x;
+    const int ntr = (nrows + GD_TILE - 1) / GD_TILE;
+    const bool blocked = (ntc & 7) == 0;
+    const int nnum = blocked ? (ntr + 3) / 4 * 4 * ntc : ntiles;
+
+    for (int tile = g; tile < nnum; tile += gridDim.x) {
+        int tr, tc;
+        if (blocked) {
+            const int sb = tile / (4 * ntc), t = tile - sb * 4 * ntc;
+            tr = sb * 4 + ((t & 31) >> 3);
+            tc = (t >> 5) * 8 + (t & 7);
+            if (tr >= ntr) continue;
+        } else {
+            tr = tile / ntc;
+            tc = tile - tr * ntc;
+        }
+        const int r0 = tr * GD_TILE, c0 = tc * GD_TILE;
+        // this lane's DMA sources: rows 16 * (4 * wave + qq) + (lane >> 2) of both tiles
+        unsigned xoff[4], woff[4];
+        int kchunk[4];
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq) {
+            const int r = 16 * (4 * wave + qq) + (lane >> 2);
+            const int c = (lane & 3) ^ gd_swz(r);
+            const int row = min(r0 + r, nrows - 1);
+            kchunk[qq] = 8 * c;
+            xoff[qq] = ((unsigned)p.rowsrc[row] * (unsigned)D + 8u * c) * 2u;
+            woff[qq] = ((unsigned)(c0 + r) * (unsigned)p.dp + 8u * c) * 2u;
+        }
+        auto issue = [&](int kb) {
+            unsigned char* st = gsm + (kb & (GD_STAGES - 1)) * GD_STAGE;
+#pragma unroll
+            for (int qq = 0; qq < 4; ++qq) {
+                const bool in = kb * GD_BK + kchunk[qq] < D;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(Rx, (lds_ptr_t)(st + (4 * wave + qq) * 1024),
+                                                     16, in ? xoff[qq] + kb * GD_BK * 2u : 0x80000000u, 0, 0, 0);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(Rw, (lds_ptr_t)(st + GD_HALF + (4 * wave + qq) * 1024),
+                                                     16, woff[qq] + kb * GD_BK * 2u, 0, 0, 0);
+            }
+        };
+
+        f32x4_t acc[8][8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+#pragma unroll
+            for (int j = 0; j < 8; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+        __syncthreads();  // every wave is done with the previous tile's stages
+        for (int kb = 0; kb < 3 && kb < nkb; ++kb) issue(kb);
+        for (int kb = 0; kb < nkb; ++kb) {
+            // this wave's DMAs for stage kb have landed: at most the later
+            // stages' eight instructions each are still outstanding
+            if (kb + 2 < nkb) asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+            else if (kb + 1 < nkb) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+            else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            __syncthreads();  // ... and every other wave's; all are done reading stage kb - 1
+            if (kb + 3 < nkb) issue(kb + 3);
+            const unsigned char* st = gsm + (kb & (GD_STAGES - 1)) * GD_STAGE;
+            const int c = lane >> 4;
+            bf16x8_t af[8], bfr[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int r = wm * 128 + i * 16 + (lane & 15);
+                af[i] = *reinterpret_cast<const bf16x8_t*>(st + GD_HALF + r * 64 + 16 * (c ^ gd_swz(r)));
+            }
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int r = wn * 128 + j * 16 + (lane & 15);
+                bfr[j] = *reinterpret_cast<const bf16x8_t*>(st + r * 64 + 16 * (c ^ gd_swz(r)));
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+        }
+
+        // Epilogue through LDS, in two halves of 128 rows: the two waves of a
+        // half park their quadrants as [row][column] (rows padded by 16 bytes),
+        // then every wave writes whole 1 KB rows, lane l holding the four gates
+        // of unit (c0 + 4 l) / 4.
+        float* const out = reinterpret_cast<float*>(gsm);
+        const int cl = 4 * lane, cp = c0 + cl;
+        const bool col_ok = cp < N4;
+        const int ub = col_ok ? cp >> 2 : 0;
+        const f32x4_t bv = f32x4_t{p.bias[ub], p.bias[H + ub], p.bias[2 * H + ub], p.bias[3 * H + ub]};
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            __syncthreads();  // stages (or the previous half) no longer read
+            if (wn == half) {
+#pragma unroll
+                for (int i = 0; i < 8; ++i)
+#pragma unroll
+                    for (int j = 0; j < 8; ++j)
+                        *reinterpret_cast<f32x4_t*>(out + (j * 16 + (lane & 15)) * GD_OUT_LD + wm * 128 + i * 16 +
+                                                    4 * (lane >> 4)) = acc[i][j];
+            }
+            __syncthreads();
+            for (int rr = wave; rr < 128; rr += 4) {
+                const int r = r0 + half * 128 + rr;
+                if (r >= nrows) break;
+                const f32x4_t v = *reinterpret_cast<const f32x4_t*>(out + rr * GD_OUT_LD + cl);
+                if (col_ok) *reinterpret_cast<f32x4_t*>(p.gx + (size_t)r * N4 + cp) = v + bv;
+            }
+        }
+    }
+}
+
 int inproj_bf16_tiles_max(const Dims& d) {
     return (int)(((long long)d.B * d.T + IP_TILE - 1) / IP_TILE) * ((4 * d.H + IP_TILE - 1) / IP_TILE);
 }
@@ -176,6 +331,9 @@ void inproj_bf16_wt_shape(const Dims& d, int* np, int* dp) {
 hipError_t inproj_bf16_setup() {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(inproj_bf16_kernel<true>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, IP_LDS_BYTES);
+    if (e != hipSuccess) return e;
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(inproj_dma_kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, GD_LDS_BYTES);
     if (e != hipSuccess) return e;
     return hipFuncSetAttribute(reinterpret_cast<const void*>(inproj_bf16_kernel<false>),
                                hipFuncAttributeMaxDynamicSharedMemorySize, IP_LDS_BYTES);
@@ -195,7 +353,14 @@ hipError_t launch_inproj_bf16(const Dims& d, const void* x, const float* b, cons
     inproj_bf16_wt_shape(d, &np, &dp);
     InprojParams p{static_cast<const __bf16*>(x), static_cast<const __bf16*>(ws.wt), b, ws.gx,
                    ws.meta, ws.rowsrc, d.D, d.H, dp};
-    const bool kfull = (d.D % IP_BK) == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0;
+    const bool aligned = (reinterpret_cast<uintptr_t>(x) & 15) == 0;
+    const long long x_bytes = 2LL * d.B * d.T * d.D, wt_bytes = 2LL * np * dp;
+    if (aligned && d.D % 8 == 0 && x_bytes < (1LL << 31) && wt_bytes < (1LL << 31)) {
+        InprojDmaParams q{p, (unsigned)x_bytes, (unsigned)wt_bytes};
+        hipLaunchKernelGGL(inproj_dma_kernel, dim3(grid), dim3(IP_THREADS), GD_LDS_BYTES, s, q);
+        return hipGetLastError();
+    }
+    const bool kfull = (d.D % IP_BK) == 0 && aligned;
     if (kfull)
         hipLaunchKernelGGL(inproj_bf16_kernel<true>, dim3(grid), dim3(IP_THREADS), IP_LDS_BYTES, s, p);
     else
