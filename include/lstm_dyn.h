@@ -146,8 +146,9 @@ int lstm_dyn_set_option(lstm_dyn_t* h, int option, long long value);
 /*
  * lstm_dyn_step_trace: with LSTM_DYN_OPT_STEP_TRACE set, copy the last
  * forward's step timestamps of workgroup 0 (device wall-clock ticks; four per
- * step -- step start after the barrier wait, partial products done, state
- * update done, barrier arrival -- then the loop end) into
+ * step -- step start, partial products of the first row-tile chunk done,
+ * state update and h stores done, first row tile of h_t complete (the end of
+ * the wait for the other workgroups) -- then the loop end) into
  * ticks[0 .. capacity), synchronising the forward's stream; *count receives
  * the number of entries and *khz the clock rate.
  * Returns LSTM_DYN_OK, ERR_INVALID (option not set, NULL arguments) or ERR_HIP.

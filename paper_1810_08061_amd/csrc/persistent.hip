@@ -392,7 +392,7 @@ persistent_kernel(PersistParams p) {
         // about to be consumed.
         constexpr int FRAG_REGS = KSW * (int)sizeof(F) / 4;
         constexpr int REG_BUDGET = KW <= 8 ? 256 : 2048 / KW;  // VGPRs per lane with KW / 4 waves per SIMD
-        constexpr int DEPTH = (MT + 3) * FRAG_REGS <= REG_BUDGET / 2   ? 3
+        constexpr int DEPTH = (MT + 3) * FRAG_REGS < REG_BUDGET / 2    ? 3
                               : (MT + 2) * FRAG_REGS <= REG_BUDGET / 2 ? 2
                                                                        : 1;
         F f0[KSW], f1[DEPTH >= 2 ? KSW : 1], f2[DEPTH == 3 ? KSW : 1];
@@ -490,10 +490,12 @@ persistent_kernel(PersistParams p) {
             // polled.  (A NaN that the redo reproduces comes from the data and
             // is kept.)
             bool exact = false;
+            float cn[NST], hn[NST];  // state update of this chunk, kept until it is verified
             for (;;) {
                 if (!exact) {
                     load_tile(f0, ntc0);
                     poll_tile(f0, 0);
+                    if (tr && ntc0 == 0) p.trace[4 * t + 3] = wall_clock64();
                     if (nchunk == 1) {
                         mma_tile(f0, 0);
                     } else if constexpr (DEPTH == 1) {
@@ -576,16 +578,26 @@ persistent_kernel(PersistParams p) {
                     const int j = nt - ntc0;
                     const int s = nt * 16 + (lo & 15), u = u0 + mt * 4 + (lo >> 4);
                     if (j < 0 || j >= nchunk || s >= act || u >= H) continue;
-                    f32x4_t z = *reinterpret_cast<const f32x4_t*>(gxs + i * KW * 256 + 4 * lo);
+                    // all partial reads first, then a tree sum (the reads overlap)
+                    f32x4_t pv[KW + 1];
 #pragma unroll
                     for (int ww = 0; ww < KW; ++ww)
-                        z += *reinterpret_cast<const f32x4_t*>(lds + ((((ww * NTC + j) * MT + mt) * 64 + lo) << 2));
+                        pv[ww] = *reinterpret_cast<const f32x4_t*>(lds + ((((ww * NTC + j) * MT + mt) * 64 + lo) << 2));
+                    pv[KW] = *reinterpret_cast<const f32x4_t*>(gxs + i * KW * 256 + 4 * lo);
+#pragma unroll
+                    for (int span = 1; span <= KW; span *= 2)
+#pragma unroll
+                        for (int a = 0; a + span <= KW; a += 2 * span) pv[a] += pv[a + span];
+                    const f32x4_t z = pv[0];
                     nan |= (z[0] != z[0]) | (z[1] != z[1]) | (z[2] != z[2]) | (z[3] != z[3]);
-                    // kept in the first wave's partial slot of the pair, which
-                    // only this lane reads from here on
-                    *reinterpret_cast<f32x4_t*>(lds + (((j * MT + mt) * 64 + lo) << 2)) = z;
+                    float c = cst[i], h;
+                    lstm_cell(z, c, h);
+                    cn[i] = c;
+                    hn[i] = h;
+                    hstage[(s - ntc0 * 16) * UPW + (u - u0)] = IO::operand(h);
                 }
-                if (exact) break;
+                // a one-tile chunk was polled in full: nothing left to verify
+                if (exact || nchunk == 1) break;
                 if (__builtin_amdgcn_ballot_w64(nan) != 0 && l == 0) lds_nan = 1;
                 __syncthreads();
                 const bool redo = lds_nan != 0;
@@ -595,25 +607,24 @@ persistent_kernel(PersistParams p) {
                 exact = true;
             }
             if (aborted) break;
-            // gates, state update, own slice of h_{t+1}
-            int lo = l;
-            asm volatile("" : "+v"(lo));
+            // commit the state update; padding units of a ragged last
+            // workgroup stay zero in h
+            {
+                int lo = l;
+                asm volatile("" : "+v"(lo));
 #pragma unroll
-            for (int i = 0; i < NST; ++i) {
-                const int q = i * KW + w, nt = q / MT, mt = q % MT;
-                const int j = nt - ntc0;
-                if (j < 0 || j >= nchunk) continue;
-                const int s = nt * 16 + (lo & 15), u = u0 + mt * 4 + (lo >> 4);
-                if (s >= act) continue;
-                if (u >= H) {  // ragged last workgroup: its padding units stay zero
-                    hstage[(s - ntc0 * 16) * UPW + (u - u0)] = E::from_f32(0.0f);
-                    continue;
+                for (int i = 0; i < NST; ++i) {
+                    const int q = i * KW + w, nt = q / MT, mt = q % MT;
+                    const int j = nt - ntc0;
+                    const int s = nt * 16 + (lo & 15), u = u0 + mt * 4 + (lo >> 4);
+                    if (j < 0 || j >= nchunk || s >= act) continue;
+                    if (u >= H) {
+                        hstage[(s - ntc0 * 16) * UPW + (u - u0)] = E::from_f32(0.0f);
+                        continue;
+                    }
+                    cst[i] = cn[i];
+                    hst[i] = hn[i];
                 }
-                float c = cst[i], h;
-                lstm_cell(*reinterpret_cast<const f32x4_t*>(lds + (((j * MT + mt) * 64 + lo) << 2)), c, h);
-                cst[i] = c;
-                hst[i] = h;
-                hstage[(s - ntc0 * 16) * UPW + (u - u0)] = IO::operand(h);
             }
             if (ntc0 == 0) drain_stores();  // the marks above
             __syncthreads();
@@ -645,7 +656,6 @@ persistent_kernel(PersistParams p) {
         o1 = o2;
         o2 = o3;
         o3 = o4;
-        if (tr) p.trace[4 * t + 3] = wall_clock64();
     }
 
     if (p.trace && blockIdx.x == 0 && tid == 0) p.trace[4 * max_len] = wall_clock64();
