@@ -63,14 +63,10 @@ __device__ inline int logical_group(int bid, int groups) {
 
 __device__ inline void drain_stores() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
-// Wave-uniform read of data written before this kernel started, through the
-// scalar data cache, so that it does not queue behind the vector loads in
-// flight.
-__device__ inline int load_uniform(const int32_t* ptr) {
-    int v;
-    asm volatile("s_load_dword %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(v) : "s"(ptr) : "memory");
-    return v;
-}
+// Data written before this kernel started and only read by it, seen through
+// the constant address space: wave-uniform reads of it become scalar loads,
+// which do not queue behind the vector loads in flight.
+typedef const __attribute__((address_space(4))) int32_t const_i32;
 
 // Barrier k (k = 0, 1, ...), split in two so work can be issued between the
 // arrival and the wait.  Arrival happens only after every wave of the
@@ -343,7 +339,8 @@ persistent_kernel(PersistParams p) {
 
     // Row offsets of steps t .. t+3 travel in registers; the one for t+4 is
     // loaded a step ahead.
-    auto offset_at = [&](int t) { return load_uniform(p.offsets + min(t, max_len)); };
+    const_i32* const offs = (const_i32*)p.offsets;
+    auto offset_at = [&](int t) { return offs[min(t, max_len)]; };
     int o0 = offset_at(0), o1 = offset_at(1), o2 = offset_at(2), o3 = offset_at(3);
 
     // h_0 sits in buffer 0 and buffer 1 is marked for h_1; one grid barrier
