@@ -30,6 +30,9 @@ SHAPES = [
     (37, 40, 33, 17, "f32"), (37, 40, 33, 17, "bf16"),   # H just above one workgroup
     (20, 64, 72, 12, "f32"), (33, 96, 100, 10, "bf16"),
     (70, 130, 136, 8, "bf16"), (16, 8, 260, 5, "f32"),
+    # the widest variants: fp32 with 64 K-steps per wave, bf16 with two gate
+    # tiles per workgroup (H > 1024) at both state capacities
+    (8, 16, 700, 4, "f32"), (20, 40, 1100, 5, "bf16"), (272, 24, 1056, 4, "bf16"),
 ]
 
 
