@@ -177,12 +177,13 @@ inproj_bf16_kernel(InprojParams p) {
 // multiple of 8, x 16-byte aligned and under 2 GiB.
 constexpr int GD_TILE = 256;
 constexpr int GD_BK = 32;
-constexpr int GD_STAGES = 4;
+constexpr int GD_STAGES = 4;  // LDS ring depth: GD_STAGES - 1 stages in flight
 constexpr int GD_HALF = GD_TILE * GD_BK * 2;  // bytes of one operand tile per stage
 constexpr int GD_STAGE = 2 * GD_HALF;
+constexpr int GD_WAVES = 8;
 constexpr int GD_OUT_LD = GD_TILE + 4;         // padded row of the output staging (floats)
-constexpr int GD_LDS_BYTES = 128 * GD_OUT_LD * 4;  // >= GD_STAGES * GD_STAGE
-static_assert(GD_LDS_BYTES >= GD_STAGES * GD_STAGE, "staging must cover the stages");
+constexpr int GD_LDS_BYTES =
+    128 * GD_OUT_LD * 4 > GD_STAGES * GD_STAGE ? 128 * GD_OUT_LD * 4 : GD_STAGES * GD_STAGE;
 
 struct InprojDmaParams {
     InprojParams b;
@@ -191,12 +192,29 @@ struct InprojDmaParams {
 
 __device__ inline int gd_swz(int r) { return (r >> 1) & 3; }
 
-__global__ void __launch_bounds__(IP_THREADS, 1)
+// One LDS-DMA instruction: 16 bytes per lane from byte offset off of R into
+// dst + 16 * lane.  (A plain function: the address-space cast is device-only.)
+__device__ inline void dma16(__amdgpu_buffer_rsrc_t R, unsigned char* dst, unsigned off) {
+    typedef __attribute__((address_space(3))) void* lds_ptr_t;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(R, (lds_ptr_t)dst, 16, off, 0, 0, 0);
+}
+
+template <int N>
+__device__ inline void wait_vm() { asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory"); }
+
+// WAVES = 4: each wave owns 128 columns x 128 rows (one wave per SIMD);
+// WAVES = 8: 128 columns x 64 rows, two waves per SIMD, so one wave's LDS
+// reads overlap the other's MFMAs.
+template <int WAVES>
+__global__ void __launch_bounds__(WAVES * 64, 1)
 inproj_dma_kernel(InprojDmaParams q) {
+    constexpr int RW = GD_TILE * 2 / WAVES;  // rows per wave
+    constexpr int JT = RW / 16;              // row tiles per wave
+    constexpr int QQ = 16 / WAVES;           // DMA instructions per operand, stage and wave
     extern __shared__ __attribute__((aligned(16))) unsigned char gsm[];
     const InprojParams& p = q.b;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;  // wave's 128 columns, 128 rows
+    const int wm = wave / (WAVES / 2), wn = wave % (WAVES / 2);  // wave's 128 columns, RW rows
     const int H = p.H, N4 = 4 * H, D = p.D;
     const int nrows = p.meta->total_rows;
     const int ntc = (N4 + GD_TILE - 1) / GD_TILE;
@@ -206,7 +224,6 @@ inproj_dma_kernel(InprojDmaParams q) {
         __builtin_amdgcn_make_buffer_rsrc(const_cast<__bf16*>(p.x), (short)0, (int)q.x_bytes, 0x00020000);
     const __amdgpu_buffer_rsrc_t Rw =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<__bf16*>(p.wt), (short)0, (int)q.wt_bytes, 0x00020000);
-    typedef __attribute__((address_space(3))) void* lds_ptr_t;
     // Consecutive workgroups sit on different XCDs: give each XCD a run of
     // 32 consecutive tile numbers, and number the tiles so that such a run
     // is a block of 4 row tiles x 8 column tiles: each x block is then shared
@@ -228,12 +245,12 @@ inproj_dma_kernel(InprojDmaParams q) {
             tc = tile - tr * ntc;
         }
         const int r0 = tr * GD_TILE, c0 = tc * GD_TILE;
-        // this lane's DMA sources: rows 16 * (4 * wave + qq) + (lane >> 2) of both tiles
-        unsigned xoff[4], woff[4];
-        int kchunk[4];
+        // this lane's DMA sources: rows 16 * (QQ * wave + qq) + (lane >> 2) of both tiles
+        unsigned xoff[QQ], woff[QQ];
+        int kchunk[QQ];
 #pragma unroll
-        for (int qq = 0; qq < 4; ++qq) {
-            const int r = 16 * (4 * wave + qq) + (lane >> 2);
+        for (int qq = 0; qq < QQ; ++qq) {
+            const int r = 16 * (QQ * wave + qq) + (lane >> 2);
             const int c = (lane & 3) ^ gd_swz(r);
             const int row = min(r0 + r, nrows - 1);
             kchunk[qq] = 8 * c;
@@ -241,50 +258,51 @@ inproj_dma_kernel(InprojDmaParams q) {
             woff[qq] = ((unsigned)(c0 + r) * (unsigned)p.dp + 8u * c) * 2u;
         }
         auto issue = [&](int kb) {
-            unsigned char* st = gsm + (kb & (GD_STAGES - 1)) * GD_STAGE;
+            unsigned char* st = gsm + (kb % GD_STAGES) * GD_STAGE;
 #pragma unroll
-            for (int qq = 0; qq < 4; ++qq) {
+            for (int qq = 0; qq < QQ; ++qq) {
                 const bool in = kb * GD_BK + kchunk[qq] < D;
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(Rx, (lds_ptr_t)(st + (4 * wave + qq) * 1024),
-                                                     16, in ? xoff[qq] + kb * GD_BK * 2u : 0x80000000u, 0, 0, 0);
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(Rw, (lds_ptr_t)(st + GD_HALF + (4 * wave + qq) * 1024),
-                                                     16, woff[qq] + kb * GD_BK * 2u, 0, 0, 0);
+                dma16(Rx, st + (QQ * wave + qq) * 1024, in ? xoff[qq] + kb * GD_BK * 2u : 0x80000000u);
+                dma16(Rw, st + GD_HALF + (QQ * wave + qq) * 1024, woff[qq] + kb * GD_BK * 2u);
             }
         };
 
-        f32x4_t acc[8][8];
+        f32x4_t acc[8][JT];
 #pragma unroll
         for (int i = 0; i < 8; ++i)
 #pragma unroll
-            for (int j = 0; j < 8; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            for (int j = 0; j < JT; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
         __syncthreads();  // every wave is done with the previous tile's stages
-        for (int kb = 0; kb < 3 && kb < nkb; ++kb) issue(kb);
+        for (int kb = 0; kb < GD_STAGES - 1 && kb < nkb; ++kb) issue(kb);
         for (int kb = 0; kb < nkb; ++kb) {
             // this wave's DMAs for stage kb have landed: at most the later
-            // stages' eight instructions each are still outstanding
-            if (kb + 2 < nkb) asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
-            else if (kb + 1 < nkb) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
-            else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            // stages' 2 QQ instructions each are still outstanding
+            static_assert(GD_STAGES <= 5, "wait counts below cover up to three later stages");
+            const int later = min(GD_STAGES - 2, nkb - 1 - kb);
+            if (later >= 3) wait_vm<6 * QQ>();
+            else if (later == 2) wait_vm<4 * QQ>();
+            else if (later == 1) wait_vm<2 * QQ>();
+            else wait_vm<0>();
             __syncthreads();  // ... and every other wave's; all are done reading stage kb - 1
-            if (kb + 3 < nkb) issue(kb + 3);
-            const unsigned char* st = gsm + (kb & (GD_STAGES - 1)) * GD_STAGE;
+            if (kb + GD_STAGES - 1 < nkb) issue(kb + GD_STAGES - 1);
+            const unsigned char* st = gsm + (kb % GD_STAGES) * GD_STAGE;
             const int c = lane >> 4;
-            bf16x8_t af[8], bfr[8];
+            bf16x8_t af[8], bfr[JT];
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
                 const int r = wm * 128 + i * 16 + (lane & 15);
                 af[i] = *reinterpret_cast<const bf16x8_t*>(st + GD_HALF + r * 64 + 16 * (c ^ gd_swz(r)));
             }
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const int r = wn * 128 + j * 16 + (lane & 15);
+            for (int j = 0; j < JT; ++j) {
+                const int r = wn * RW + j * 16 + (lane & 15);
                 bfr[j] = *reinterpret_cast<const bf16x8_t*>(st + r * 64 + 16 * (c ^ gd_swz(r)));
             }
 #pragma unroll
             for (int i = 0; i < 8; ++i)
 #pragma unroll
-                for (int j = 0; j < 8; ++j)
+                for (int j = 0; j < JT; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
         }
 
@@ -300,16 +318,17 @@ inproj_dma_kernel(InprojDmaParams q) {
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
             __syncthreads();  // stages (or the previous half) no longer read
-            if (wn == half) {
+            if (wn * RW / 128 == half) {
+                const int rl = wn * RW - half * 128;  // first row of this wave within the half
 #pragma unroll
                 for (int i = 0; i < 8; ++i)
 #pragma unroll
-                    for (int j = 0; j < 8; ++j)
-                        *reinterpret_cast<f32x4_t*>(out + (j * 16 + (lane & 15)) * GD_OUT_LD + wm * 128 + i * 16 +
+                    for (int j = 0; j < JT; ++j)
+                        *reinterpret_cast<f32x4_t*>(out + (rl + j * 16 + (lane & 15)) * GD_OUT_LD + wm * 128 + i * 16 +
                                                     4 * (lane >> 4)) = acc[i][j];
             }
             __syncthreads();
-            for (int rr = wave; rr < 128; rr += 4) {
+            for (int rr = wave; rr < 128; rr += WAVES) {
                 const int r = r0 + half * 128 + rr;
                 if (r >= nrows) break;
                 const f32x4_t v = *reinterpret_cast<const f32x4_t*>(out + rr * GD_OUT_LD + cl);
@@ -332,7 +351,7 @@ hipError_t inproj_bf16_setup() {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(inproj_bf16_kernel<true>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, IP_LDS_BYTES);
     if (e != hipSuccess) return e;
-    e = hipFuncSetAttribute(reinterpret_cast<const void*>(inproj_dma_kernel),
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(inproj_dma_kernel<GD_WAVES>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, GD_LDS_BYTES);
     if (e != hipSuccess) return e;
     return hipFuncSetAttribute(reinterpret_cast<const void*>(inproj_bf16_kernel<false>),
@@ -357,7 +376,7 @@ hipError_t launch_inproj_bf16(const Dims& d, const void* x, const float* b, cons
     const long long x_bytes = 2LL * d.B * d.T * d.D, wt_bytes = 2LL * np * dp;
     if (aligned && d.D % 8 == 0 && x_bytes < (1LL << 31) && wt_bytes < (1LL << 31)) {
         InprojDmaParams q{p, (unsigned)x_bytes, (unsigned)wt_bytes};
-        hipLaunchKernelGGL(inproj_dma_kernel, dim3(grid), dim3(IP_THREADS), GD_LDS_BYTES, s, q);
+        hipLaunchKernelGGL(inproj_dma_kernel<GD_WAVES>, dim3(grid), dim3(GD_WAVES * 64), GD_LDS_BYTES, s, q);
         return hipGetLastError();
     }
     const bool kfull = (d.D % IP_BK) == 0 && aligned;
