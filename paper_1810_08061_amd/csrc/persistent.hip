@@ -214,12 +214,15 @@ persistent_kernel(PersistParams p) {
     using LY = PLayout<MT, KW, NST>;
     constexpr int NTC = LY::NTC;
     static_assert(NTC >= 1, "partial buffer too small");
+    static_assert(NST % MT == 0, "a wave owns whole row tiles");
+    constexpr int NOT = NST / MT;  // row tiles owned per wave
     extern __shared__ __attribute__((aligned(16))) float lds[];
     __shared__ int lds_ok, lds_abort, lds_nan;
     constexpr int UPW = 4 * MT;                      // hidden units per workgroup
     constexpr int SEG_BYTES = UPW * (int)sizeof(S);  // one row of this workgroup's h slice
     static_assert(SEG_BYTES == 8 || SEG_BYTES == 16, "h row segment must be 8 or 16 bytes");
-    __shared__ __attribute__((aligned(16))) S hstage[NTC * 16 * UPW];
+    // per-wave gather of one owned row tile's h before its row segments are stored
+    __shared__ __attribute__((aligned(16))) S hstage[KW][16 * UPW];
 
     // tid and l are re-read through empty asm statements at the top of each
     // step and chunk, so values derived from them (addresses, row indices)
@@ -289,50 +292,74 @@ persistent_kernel(PersistParams p) {
     }
 
     const int max_len = p.meta->max_len;
-    // Marks this workgroup's slice of rows [0, rows) of one buffer as not yet written.
-    auto mark_rows = [&](unsigned part, int rows) {
-        for (int r = tid; r < rows; r += KW * 64) {
-            const unsigned off = part + hx_off<E>(r, u0, hpad);
-            if constexpr (SEG_BYTES == 16) {
-                typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-                __builtin_amdgcn_raw_buffer_store_b128(u32x4{~0u, ~0u, ~0u, ~0u}, R, off, 0, P_SC1);
-            } else {
-                typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
-                __builtin_amdgcn_raw_buffer_store_b64(u32x2{~0u, ~0u}, R, off, 0, P_SC1);
-            }
-        }
+    typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+    typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+    // One row's segment of this workgroup's h slice (UPW units), device scope.
+    auto seg_store = [&](unsigned off, const S* v) {
+        if constexpr (SEG_BYTES == 16)
+            __builtin_amdgcn_raw_buffer_store_b128(*reinterpret_cast<const u32x4*>(v), R, off, 0, P_SC1);
+        else
+            __builtin_amdgcn_raw_buffer_store_b64(*reinterpret_cast<const u32x2*>(v), R, off, 0, P_SC1);
     };
-
-    // ---- Owned state: pair q = i*KW + w -> row tile q / MT, gate tile q % MT.
-    // c and h live in registers and reach out_c / out_h once, after the loop.
-    float cst[NST], hst[NST];
-#pragma unroll
-    for (int i = 0; i < NST; ++i) {
-        const int q = i * KW + w, nt = q / MT, mt = q % MT;
-        const int s = nt * 16 + (l & 15), u = u0 + mt * 4 + (l >> 4);
-        cst[i] = 0.f;
-        hst[i] = 0.f;
-        if (nt < ntmax && s < B && u < H) {
-            const size_t ib = (size_t)p.perm[s] * H + u;
-            hst[i] = p.h0[ib];  // read before the final write: exact aliasing out_h == h0 is allowed
-            cst[i] = p.c0[ib];
-            IO::store(R, hx_off<E>(s, u, hpad), hst[i]);
-        }
-    }
-
-    // Gx[t] of the owned pairs goes straight from memory into this wave's LDS
-    // slots (no registers held while it is in flight); lanes of pairs that
-    // are not active fetch row 0 instead, which is never read.
-    auto prefetch_gx = [&](int off, int act) {
+    auto seg_mark = [&](unsigned off) {
+        if constexpr (SEG_BYTES == 16)
+            __builtin_amdgcn_raw_buffer_store_b128(u32x4{~0u, ~0u, ~0u, ~0u}, R, off, 0, P_SC1);
+        else
+            __builtin_amdgcn_raw_buffer_store_b64(u32x2{~0u, ~0u}, R, off, 0, P_SC1);
+    };
+    // Wave w owns row tiles a * KW + w (a < NOT) with all MT gate tiles of this
+    // workgroup: pair i = a * MT + mt.  It alone computes, stores and marks
+    // their rows of this workgroup's h slice (lanes 0..15 hold the 16 rows), so
+    // the marks of a segment and its later data come from the same wave.
+    // Marks rows [0, rows) of the owned tiles in one buffer as not yet written.
+    auto mark_owned = [&](unsigned part, int rows) {
         int lo = l;
         asm volatile("" : "+v"(lo));
 #pragma unroll
-        for (int i = 0; i < NST; ++i) {
-            const int q = i * KW + w, nt = q / MT, mt = q % MT;
+        for (int a = 0; a < NOT; ++a) {
+            const int s = (a * KW + w) * 16 + lo;
+            if (lo < 16 && s < rows) seg_mark(part + hx_off<E>(s, u0, hpad));
+        }
+    };
+
+    // ---- Owned state.  c and h live in registers and reach out_c / out_h
+    // once, after the loop.  h_0 goes to buffer 0 as whole row segments (the
+    // padding units of a ragged last workgroup as zeros).
+    float cst[NST], hst[NST];
+#pragma unroll
+    for (int a = 0; a < NOT; ++a) {
+        const int nt = a * KW + w;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            const int i = a * MT + mt;
+            const int s = nt * 16 + (l & 15), u = u0 + mt * 4 + (l >> 4);
+            cst[i] = 0.f;
+            hst[i] = 0.f;
+            if (nt < ntmax && s < B && u < H) {
+                const size_t ib = (size_t)p.perm[s] * H + u;
+                hst[i] = p.h0[ib];  // read before the final write: exact aliasing out_h == h0 is allowed
+                cst[i] = p.c0[ib];
+            }
+            hstage[w][(l & 15) * UPW + mt * 4 + (l >> 4)] = IO::operand(hst[i]);
+        }
+        __builtin_amdgcn_wave_barrier();
+        if (nt < ntmax && l < 16 && nt * 16 + l < B) seg_store(hx_off<E>(nt * 16 + l, u0, hpad), &hstage[w][l * UPW]);
+        __builtin_amdgcn_wave_barrier();
+    }
+
+    // Gx[t] of one owned tile goes straight from memory into this wave's LDS
+    // slots (no registers held while it is in flight); lanes of rows that are
+    // not active fetch row 0 instead, which is never read.
+    auto prefetch_tile = [&](int a, int off, int act) {
+        int lo = l;
+        asm volatile("" : "+v"(lo));
+        const int nt = a * KW + w;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
             const int s = nt * 16 + (lo & 15), u = u0 + mt * 4 + (lo >> 4);
             const bool ok = s < act && u < H;
             const float* src = p.gx + (ok ? (size_t)(off + s) * H4 + 4 * u : 0);
-            __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)(gxs + i * KW * 256),
+            __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)(gxs + (a * MT + mt) * KW * 256),
                                              16, 0, 0);
         }
     };
@@ -343,13 +370,17 @@ persistent_kernel(PersistParams p) {
     auto offset_at = [&](int t) { return offs[min(t, max_len)]; };
     int o0 = offset_at(0), o1 = offset_at(1), o2 = offset_at(2), o3 = offset_at(3);
 
-    // h_0 sits in buffer 0 and buffer 1 is marked for h_1; one grid barrier
-    // makes both visible.  After that the steps synchronise through the data.
-    mark_rows(hx_part, o2 - o1);
+    // h_0 sits in buffer 0 and buffers 1 and 2 are marked for h_1 and h_2; one
+    // grid barrier (which drains every store) makes all of it visible.  After
+    // that the steps synchronise through the data.
+    mark_owned(hx_part, o2 - o1);
+    mark_owned(2u * hx_part, o3 - o2);
     bool alive = true;
     if (max_len > 0) {
         grid_arrive(p, 0);
-        prefetch_gx(o0, o1 - o0);
+#pragma unroll
+        for (int a = 0; a < NOT; ++a)
+            if ((a * KW + w) * 16 < o1 - o0) prefetch_tile(a, o0, o1 - o0);
         alive = grid_wait(p, 0, &lds_ok);
     }
 
@@ -366,35 +397,31 @@ persistent_kernel(PersistParams p) {
         const bool tr = p.trace && blockIdx.x == 0 && tid == 0;
         if (tr) p.trace[4 * t] = wall_clock64();
         const int o4 = offset_at(t + 4);  // used next step
-        const int act = o1 - o0;
+        const int act = o1 - o0, act1 = o2 - o1;
         const int nt_act = (act + 15) >> 4;
         const unsigned cur = (unsigned)(t & 3) * hx_part;        // h_t
         const unsigned nxt = (unsigned)((t + 1) & 3) * hx_part;  // h_{t+1}
-        // Buffer (t+2) mod 4 still holds h_{t-2}.  Having seen rows [0, act(t-1))
-        // of every workgroup's h_{t-1}, this workgroup knows that every
-        // workgroup is done reading h_{t-2} except for row tiles at or beyond
-        // act(t-1) >= act(t+2), so rows [0, act(t+2)) can be marked for h_{t+2}.
-        // The marks drain before this step's first h_{t+1} store; a reader
-        // sees that row before it moves on to h_{t+2}.
-        mark_rows((unsigned)((t + 2) & 3) * hx_part, o3 - o2);
+        // The owners of the previous step's row tiles may still be reading its
+        // partial sums.
+        __syncthreads();
 
-        // Register sets of h fragments pipeline the row tiles of a chunk: with
-        // three sets, tiles j+1 and j+2 are loading while tile j is
-        // multiplied; variants whose U slice leaves fewer registers use two,
-        // or one set whose K-steps are reloaded for the next tile as soon as
-        // their MFMAs have been issued.
-        // The chunk is run by one of a few straight-line schedules (short
-        // chunks, then a steady loop followed by a tail), so every load is for
-        // a real tile and on every path the compiler waits for exactly the set
-        // about to be consumed.
         constexpr int FRAG_REGS = KSW * (int)sizeof(F) / 4;
         constexpr int REG_BUDGET = KW <= 8 ? 256 : 2048 / KW;  // VGPRs per lane with KW / 4 waves per SIMD
         constexpr int DEPTH = (MT + 3) * FRAG_REGS < REG_BUDGET / 2    ? 3
                               : (MT + 2) * FRAG_REGS <= REG_BUDGET / 2 ? 2
                                                                        : 1;
         F f0[KSW], f1[DEPTH >= 2 ? KSW : 1], f2[DEPTH == 3 ? KSW : 1];
+        // Lanes whose row of the tile is not active read row 0's chunk of
+        // their k-run instead of their own: it lies in the same 64-byte
+        // segment as the active rows' chunks, so the load moves no extra
+        // lines, and the value only reaches the products of the inactive row,
+        // which are never used.
+        auto tile_base = [&](int nt) {
+            const unsigned skip = (l & 15) >= act - nt * 16 ? (unsigned)(l & 15) * 16u : 0u;
+            return cur + (unsigned)nt * tile_bytes + lane_off - skip;
+        };
         auto load_tile = [&](F* f, int nt) {
-            const unsigned base = cur + (unsigned)nt * tile_bytes + lane_off;
+            const unsigned base = tile_base(nt);
             if constexpr (GROUPED) {
                 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 #pragma unroll
@@ -441,7 +468,7 @@ persistent_kernel(PersistParams p) {
                 f32x4_t acc[MT];
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-                const unsigned next = cur + (unsigned)(ntc0 + j + 1) * tile_bytes + lane_off;
+                const unsigned next = tile_base(ntc0 + j + 1);
 #pragma unroll
                 for (int ks = 0; ks < KSW; ++ks) {
 #pragma unroll
@@ -567,31 +594,36 @@ persistent_kernel(PersistParams p) {
                 // recomputed here rather than kept live across the loop.
                 int lo = l;
                 asm volatile("" : "+v"(lo));
-                asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's Gx prefetch has landed
+                // this wave's Gx prefetch has landed, and so have its marks and
+                // h stores of earlier steps
+                asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
                 bool nan = false;
 #pragma unroll
-                for (int i = 0; i < NST; ++i) {
-                    const int q = i * KW + w, nt = q / MT, mt = q % MT;
-                    const int j = nt - ntc0;
-                    const int s = nt * 16 + (lo & 15), u = u0 + mt * 4 + (lo >> 4);
-                    if (j < 0 || j >= nchunk || s >= act || u >= H) continue;
-                    // all partial reads first, then a tree sum (the reads overlap)
-                    f32x4_t pv[KW + 1];
+                for (int a = 0; a < NOT; ++a) {
+                    const int j = a * KW + w - ntc0;
+                    if (j < 0 || j >= nchunk) continue;
 #pragma unroll
-                    for (int ww = 0; ww < KW; ++ww)
-                        pv[ww] = *reinterpret_cast<const f32x4_t*>(lds + ((((ww * NTC + j) * MT + mt) * 64 + lo) << 2));
-                    pv[KW] = *reinterpret_cast<const f32x4_t*>(gxs + i * KW * 256 + 4 * lo);
+                    for (int mt = 0; mt < MT; ++mt) {
+                        const int i = a * MT + mt;
+                        // all partial reads first, then a tree sum (the reads overlap)
+                        f32x4_t pv[KW + 1];
 #pragma unroll
-                    for (int span = 1; span <= KW; span *= 2)
+                        for (int ww = 0; ww < KW; ++ww)
+                            pv[ww] = *reinterpret_cast<const f32x4_t*>(lds + ((((ww * NTC + j) * MT + mt) * 64 + lo) << 2));
+                        pv[KW] = *reinterpret_cast<const f32x4_t*>(gxs + i * KW * 256 + 4 * lo);
 #pragma unroll
-                        for (int a = 0; a + span <= KW; a += 2 * span) pv[a] += pv[a + span];
-                    const f32x4_t z = pv[0];
-                    nan |= (z[0] != z[0]) | (z[1] != z[1]) | (z[2] != z[2]) | (z[3] != z[3]);
-                    float c = cst[i], h;
-                    lstm_cell(z, c, h);
-                    cn[i] = c;
-                    hn[i] = h;
-                    hstage[(s - ntc0 * 16) * UPW + (u - u0)] = IO::operand(h);
+                        for (int span = 1; span <= KW; span *= 2)
+#pragma unroll
+                            for (int b = 0; b + span <= KW; b += 2 * span) pv[b] += pv[b + span];
+                        const f32x4_t z = pv[0];
+                        const int s = (j + ntc0) * 16 + (lo & 15);
+                        const bool live = s < act;
+                        nan |= live & ((z[0] != z[0]) | (z[1] != z[1]) | (z[2] != z[2]) | (z[3] != z[3]));
+                        float c = cst[i], h;
+                        lstm_cell(z, c, h);
+                        cn[i] = c;
+                        hn[i] = h;
+                    }
                 }
                 // a one-tile chunk was polled in full: nothing left to verify
                 if (exact || nchunk == 1) break;
@@ -604,42 +636,32 @@ persistent_kernel(PersistParams p) {
                 exact = true;
             }
             if (aborted) break;
-            // commit the state update; padding units of a ragged last
-            // workgroup stay zero in h
+            // Commit the owned tiles of the chunk; gather each tile's h rows in
+            // this wave's staging slot and store one segment per active row
+            // (padding units of a ragged last workgroup as zeros).
             {
                 int lo = l;
                 asm volatile("" : "+v"(lo));
 #pragma unroll
-                for (int i = 0; i < NST; ++i) {
-                    const int q = i * KW + w, nt = q / MT, mt = q % MT;
+                for (int a = 0; a < NOT; ++a) {
+                    const int nt = a * KW + w;
                     const int j = nt - ntc0;
-                    const int s = nt * 16 + (lo & 15), u = u0 + mt * 4 + (lo >> 4);
-                    if (j < 0 || j >= nchunk || s >= act) continue;
-                    if (u >= H) {
-                        hstage[(s - ntc0 * 16) * UPW + (u - u0)] = E::from_f32(0.0f);
-                        continue;
+                    if (j < 0 || j >= nchunk) continue;
+#pragma unroll
+                    for (int mt = 0; mt < MT; ++mt) {
+                        const int i = a * MT + mt;
+                        const int s = nt * 16 + (lo & 15), u = u0 + mt * 4 + (lo >> 4);
+                        if (s < act && u < H) {
+                            cst[i] = cn[i];
+                            hst[i] = hn[i];
+                        }
+                        hstage[w][(lo & 15) * UPW + mt * 4 + (lo >> 4)] =
+                            u < H ? IO::operand(hst[i]) : E::from_f32(0.0f);
                     }
-                    cst[i] = cn[i];
-                    hst[i] = hn[i];
-                }
-            }
-            if (ntc0 == 0) drain_stores();  // the marks above
-            __syncthreads();
-            // this workgroup's slice of h_{t+1}: one UPW-unit row segment per active row
-            {
-                const int rows = min(act - ntc0 * 16, nchunk * 16);
-                for (int r = tid; r < rows; r += KW * 64) {
-                    const int s = ntc0 * 16 + r;
-                    const unsigned off = nxt + hx_off<E>(s, u0, hpad);
-                    if constexpr (SEG_BYTES == 16) {
-                        typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-                        __builtin_amdgcn_raw_buffer_store_b128(
-                            *reinterpret_cast<const u32x4*>(hstage + r * UPW), R, off, 0, P_SC1);
-                    } else {
-                        typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
-                        __builtin_amdgcn_raw_buffer_store_b64(
-                            *reinterpret_cast<const u32x2*>(hstage + r * UPW), R, off, 0, P_SC1);
-                    }
+                    __builtin_amdgcn_wave_barrier();
+                    if (lo < 16 && nt * 16 + lo < act)
+                        seg_store(nxt + hx_off<E>(nt * 16 + lo, u0, hpad), &hstage[w][lo * UPW]);
+                    __builtin_amdgcn_wave_barrier();
                 }
             }
         }
@@ -648,7 +670,21 @@ persistent_kernel(PersistParams p) {
             break;
         }
         if (tr) p.trace[4 * t + 2] = wall_clock64();
-        if (t + 1 < max_len) prefetch_gx(o1, o2 - o1);  // in flight while h_{t+1} arrives
+        // Gx[t+1] of the owned tiles, into the slots the gate math has read; it
+        // is in flight while h_{t+1} arrives.  (Issued only now: the gate math
+        // of a later chunk waits for every load of this wave.)
+        if (t + 1 < max_len) {
+#pragma unroll
+            for (int a = 0; a < NOT; ++a)
+                if ((a * KW + w) * 16 < act1) prefetch_tile(a, o1, act1);
+        }
+        // Buffer (t+3) mod 4 still holds h_{t-1}.  This workgroup has seen rows
+        // [0, act(t)) of every workgroup's h_t, so every workgroup has finished
+        // reading h_{t-1} in those rows, which include every row active at t+3.
+        // The marks drain before this wave's h_{t+2} stores of the same
+        // segments (the wait before the gate math), so a reader that saw a
+        // segment of h_{t+2} then sees its mark in buffer (t+3) mod 4.
+        mark_owned((unsigned)((t + 3) & 3) * hx_part, o4 - o3);
         o0 = o1;
         o1 = o2;
         o2 = o3;
@@ -659,7 +695,7 @@ persistent_kernel(PersistParams p) {
     // ---- final state, batch order
 #pragma unroll
     for (int i = 0; i < NST; ++i) {
-        const int q = i * KW + w, nt = q / MT, mt = q % MT;
+        const int nt = (i / MT) * KW + w, mt = i % MT;
         const int s = nt * 16 + (l & 15), u = u0 + mt * 4 + (l >> 4);
         if (nt < ntmax && s < B && u < H) {
             const size_t ib = (size_t)p.perm[s] * H + u;
