@@ -199,6 +199,13 @@ __device__ inline void dma16(__amdgpu_buffer_rsrc_t R, unsigned char* dst, unsig
     __builtin_amdgcn_raw_ptr_buffer_load_lds(R, (lds_ptr_t)dst, 16, off, 0, 0, 0);
 }
 
+// Workgroup barrier after this wave's LDS accesses have completed.  The
+// kernel's waits for its LDS DMA are explicit (wait_vm); __syncthreads()
+// would in addition wait for every outstanding vector memory operation --
+// the DMA of the stages still in flight, and the stores of Gx -- and so
+// drain the operand pipeline at every K-block.
+__device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 template <int N>
 __device__ inline void wait_vm() { asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory"); }
 
@@ -273,7 +280,7 @@ inproj_dma_kernel(InprojDmaParams q) {
 #pragma unroll
             for (int j = 0; j < JT; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-        __syncthreads();  // every wave is done with the previous tile's stages
+        lds_barrier();  // every wave is done with the previous tile's stages
         for (int kb = 0; kb < GD_STAGES - 1 && kb < nkb; ++kb) issue(kb);
         for (int kb = 0; kb < nkb; ++kb) {
             // this wave's DMAs for stage kb have landed: at most the later
@@ -284,7 +291,7 @@ inproj_dma_kernel(InprojDmaParams q) {
             else if (later == 2) wait_vm<4 * QQ>();
             else if (later == 1) wait_vm<2 * QQ>();
             else wait_vm<0>();
-            __syncthreads();  // ... and every other wave's; all are done reading stage kb - 1
+            lds_barrier();  // ... and every other wave's; all are done reading stage kb - 1
             if (kb + GD_STAGES - 1 < nkb) issue(kb + GD_STAGES - 1);
             const unsigned char* st = gsm + (kb % GD_STAGES) * GD_STAGE;
             const int c = lane >> 4;
@@ -317,7 +324,7 @@ inproj_dma_kernel(InprojDmaParams q) {
         const f32x4_t bv = f32x4_t{p.bias[ub], p.bias[H + ub], p.bias[2 * H + ub], p.bias[3 * H + ub]};
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
-            __syncthreads();  // stages (or the previous half) no longer read
+            lds_barrier();  // stages (or the previous half) no longer read
             if (wn * RW / 128 == half) {
                 const int rl = wn * RW - half * 128;  // first row of this wave within the half
 #pragma unroll
@@ -327,7 +334,7 @@ inproj_dma_kernel(InprojDmaParams q) {
                         *reinterpret_cast<f32x4_t*>(out + (rl + j * 16 + (lane & 15)) * GD_OUT_LD + wm * 128 + i * 16 +
                                                     4 * (lane >> 4)) = acc[i][j];
             }
-            __syncthreads();
+            lds_barrier();
             for (int rr = wave; rr < 128; rr += WAVES) {
                 const int r = r0 + half * 128 + rr;
                 if (r >= nrows) break;
