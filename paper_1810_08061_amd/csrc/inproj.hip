@@ -8,11 +8,15 @@
 // W arrives as [D][4H] (N contiguous).  MFMA wants both operands contiguous
 // along K, so a first kernel writes Wt[c'][k] (gate-interleaved rows, zero
 // padded to whole tiles); the GEMM then loads both operands with 16-byte
-// vector loads.  Tiles are 256 columns x 256 rows x 64 K, four waves of
-// 128 x 128 each (8 x 8 MFMA 16x16x32 tiles), two LDS stages; the next
-// K-block is loaded into registers while the current one is multiplied.
-// C^T = Wt x^T is formed so each lane's four results are the four gates of
-// one (row, unit) and leave as one 16-byte store.
+// vector loads.  C^T = Wt x^T is formed so each lane's four results are the
+// four gates of one (row, unit).
+//
+// Two GEMMs: inproj_dma_kernel (below; D a multiple of 8), whose operands
+// reach LDS by DMA, and the fallback inproj_bf16_kernel for any D: tiles of
+// 256 columns x 256 rows x 64 K, four waves of 128 x 128 each (8 x 8 MFMA
+// 16x16x32 tiles), two LDS stages, the next K-block loaded into registers
+// while the current one is multiplied, each result leaving as one 16-byte
+// store.
 #include "launch.h"
 
 namespace ldyn {
@@ -166,31 +170,33 @@ inproj_bf16_kernel(InprojParams p) {
 
 // ---------------------------------------------------------------------------
 // Variant fed by LDS DMA: both operand tiles go from memory straight into a
-// four-stage LDS ring (global/buffer load with an LDS destination), K = 32 per
-// stage, so three stages are in flight while one is multiplied and no
-// registers hold data in transit.  A DMA instruction writes 64 lanes x 16
-// bytes contiguously; with 64-byte operand rows that is 16 rows, and each
+// two-stage LDS ring (buffer load with an LDS destination), K = 64 per stage:
+// while one stage is multiplied the next is in flight, and no registers hold
+// data in transit.  A DMA instruction writes 64 lanes x 16 bytes
+// contiguously; with 128-byte operand rows that is 8 whole rows, and each
 // lane fetches the 16-byte chunk that belongs at its position under the XOR
-// swizzle chunk' = chunk ^ ((row >> 1) & 3), which spreads the MFMA fragment
-// reads (16 rows, one chunk) over all banks.  x rows past D (the K tail) are
+// swizzle chunk' = chunk ^ (row & 7), which spreads the MFMA fragment reads
+// (16 rows, one chunk) over all banks.  x rows past D (the K tail) are
 // fetched at an offset outside the buffer, which yields zeros.  Requires D a
 // multiple of 8, x 16-byte aligned and under 2 GiB.
+//
+// Eight waves (two per SIMD) each own 128 columns x 64 rows of the 256 x 256
+// tile, so one wave's LDS reads overlap the other's MFMAs; a wave reads both
+// K-steps' fragments of a stage before its first MFMA.
 constexpr int GD_TILE = 256;
-constexpr int GD_BK = 32;
-constexpr int GD_STAGES = 4;  // LDS ring depth: GD_STAGES - 1 stages in flight
+constexpr int GD_BK = 64;
 constexpr int GD_HALF = GD_TILE * GD_BK * 2;  // bytes of one operand tile per stage
 constexpr int GD_STAGE = 2 * GD_HALF;
 constexpr int GD_WAVES = 8;
 constexpr int GD_OUT_LD = GD_TILE + 4;         // padded row of the output staging (floats)
 constexpr int GD_LDS_BYTES =
-    128 * GD_OUT_LD * 4 > GD_STAGES * GD_STAGE ? 128 * GD_OUT_LD * 4 : GD_STAGES * GD_STAGE;
+    128 * GD_OUT_LD * 4 > 2 * GD_STAGE ? 128 * GD_OUT_LD * 4 : 2 * GD_STAGE;
+static_assert(GD_BK == IP_BK, "the padded K of Wt is a whole number of stages");
 
 struct InprojDmaParams {
     InprojParams b;
     unsigned x_bytes, wt_bytes;
 };
-
-__device__ inline int gd_swz(int r) { return (r >> 1) & 3; }
 
 // One LDS-DMA instruction: 16 bytes per lane from byte offset off of R into
 // dst + 16 * lane.  (A plain function: the address-space cast is device-only.)
@@ -200,28 +206,21 @@ __device__ inline void dma16(__amdgpu_buffer_rsrc_t R, unsigned char* dst, unsig
 }
 
 // Workgroup barrier after this wave's LDS accesses have completed.  The
-// kernel's waits for its LDS DMA are explicit (wait_vm); __syncthreads()
-// would in addition wait for every outstanding vector memory operation --
-// the DMA of the stages still in flight, and the stores of Gx -- and so
-// drain the operand pipeline at every K-block.
+// kernel's waits for its LDS DMA are explicit; __syncthreads() would in
+// addition wait for every outstanding vector memory operation -- the DMA of
+// the stage in flight, and the stores of Gx -- and so drain the operand
+// pipeline at every K-block.
 __device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-template <int N>
-__device__ inline void wait_vm() { asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory"); }
-
-// WAVES = 4: each wave owns 128 columns x 128 rows (one wave per SIMD);
-// WAVES = 8: 128 columns x 64 rows, two waves per SIMD, so one wave's LDS
-// reads overlap the other's MFMAs.
-template <int WAVES>
-__global__ void __launch_bounds__(WAVES * 64, 1)
+__global__ void __launch_bounds__(GD_WAVES * 64, 1)
 inproj_dma_kernel(InprojDmaParams q) {
-    constexpr int RW = GD_TILE * 2 / WAVES;  // rows per wave
-    constexpr int JT = RW / 16;              // row tiles per wave
-    constexpr int QQ = 16 / WAVES;           // DMA instructions per operand, stage and wave
+    constexpr int RW = GD_TILE * 2 / GD_WAVES;  // rows per wave
+    constexpr int JT = RW / 16;                 // row tiles per wave
+    constexpr int QQ = 32 / GD_WAVES;           // DMA instructions per operand, stage and wave
     extern __shared__ __attribute__((aligned(16))) unsigned char gsm[];
     const InprojParams& p = q.b;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave / (WAVES / 2), wn = wave % (WAVES / 2);  // wave's 128 columns, RW rows
+    const int wm = wave / (GD_WAVES / 2), wn = wave % (GD_WAVES / 2);  // wave's 128 columns, RW rows
     const int H = p.H, N4 = 4 * H, D = p.D;
     const int nrows = p.meta->total_rows;
     const int ntc = (N4 + GD_TILE - 1) / GD_TILE;
@@ -252,20 +251,20 @@ inproj_dma_kernel(InprojDmaParams q) {
             tc = tile - tr * ntc;
         }
         const int r0 = tr * GD_TILE, c0 = tc * GD_TILE;
-        // this lane's DMA sources: rows 16 * (QQ * wave + qq) + (lane >> 2) of both tiles
+        // this lane's DMA sources: rows 8 * (QQ * wave + qq) + (lane >> 3) of both tiles
         unsigned xoff[QQ], woff[QQ];
         int kchunk[QQ];
 #pragma unroll
         for (int qq = 0; qq < QQ; ++qq) {
-            const int r = 16 * (QQ * wave + qq) + (lane >> 2);
-            const int c = (lane & 3) ^ gd_swz(r);
+            const int r = 8 * (QQ * wave + qq) + (lane >> 3);
+            const int c = (lane & 7) ^ (r & 7);
             const int row = min(r0 + r, nrows - 1);
             kchunk[qq] = 8 * c;
             xoff[qq] = ((unsigned)p.rowsrc[row] * (unsigned)D + 8u * c) * 2u;
             woff[qq] = ((unsigned)(c0 + r) * (unsigned)p.dp + 8u * c) * 2u;
         }
         auto issue = [&](int kb) {
-            unsigned char* st = gsm + (kb % GD_STAGES) * GD_STAGE;
+            unsigned char* st = gsm + (kb & 1) * GD_STAGE;
 #pragma unroll
             for (int qq = 0; qq < QQ; ++qq) {
                 const bool in = kb * GD_BK + kchunk[qq] < D;
@@ -281,36 +280,37 @@ inproj_dma_kernel(InprojDmaParams q) {
             for (int j = 0; j < JT; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
         lds_barrier();  // every wave is done with the previous tile's stages
-        for (int kb = 0; kb < GD_STAGES - 1 && kb < nkb; ++kb) issue(kb);
+        issue(0);
         for (int kb = 0; kb < nkb; ++kb) {
-            // this wave's DMAs for stage kb have landed: at most the later
-            // stages' 2 QQ instructions each are still outstanding
-            static_assert(GD_STAGES <= 5, "wait counts below cover up to three later stages");
-            const int later = min(GD_STAGES - 2, nkb - 1 - kb);
-            if (later >= 3) wait_vm<6 * QQ>();
-            else if (later == 2) wait_vm<4 * QQ>();
-            else if (later == 1) wait_vm<2 * QQ>();
-            else wait_vm<0>();
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's DMAs of stage kb have landed
             lds_barrier();  // ... and every other wave's; all are done reading stage kb - 1
-            if (kb + GD_STAGES - 1 < nkb) issue(kb + GD_STAGES - 1);
-            const unsigned char* st = gsm + (kb % GD_STAGES) * GD_STAGE;
-            const int c = lane >> 4;
-            bf16x8_t af[8], bfr[JT];
+            if (kb + 1 < nkb) issue(kb + 1);
+            const unsigned char* st = gsm + (kb & 1) * GD_STAGE;
+            // both K-steps' fragments are read before any MFMA, so the second
+            // step's reads are in flight while the first step multiplies
+            bf16x8_t af[2][8], bfr[2][JT];
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const int r = wm * 128 + i * 16 + (lane & 15);
-                af[i] = *reinterpret_cast<const bf16x8_t*>(st + GD_HALF + r * 64 + 16 * (c ^ gd_swz(r)));
+            for (int ks = 0; ks < 2; ++ks) {
+                const int c = ks * 4 + (lane >> 4);
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    const int r = wm * 128 + i * 16 + (lane & 15);
+                    af[ks][i] = *reinterpret_cast<const bf16x8_t*>(st + GD_HALF + r * 128 + 16 * (c ^ (r & 7)));
+                }
+#pragma unroll
+                for (int j = 0; j < JT; ++j) {
+                    const int r = wn * RW + j * 16 + (lane & 15);
+                    bfr[ks][j] = *reinterpret_cast<const bf16x8_t*>(st + r * 128 + 16 * (c ^ (r & 7)));
+                }
             }
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int j = 0; j < JT; ++j) {
-                const int r = wn * RW + j * 16 + (lane & 15);
-                bfr[j] = *reinterpret_cast<const bf16x8_t*>(st + r * 64 + 16 * (c ^ gd_swz(r)));
-            }
+            for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-            for (int i = 0; i < 8; ++i)
+                for (int i = 0; i < 8; ++i)
 #pragma unroll
-                for (int j = 0; j < JT; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+                    for (int j = 0; j < JT; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[ks][i], bfr[ks][j], acc[i][j], 0, 0, 0);
         }
 
         // Epilogue through LDS, in two halves of 128 rows: the two waves of a
@@ -335,7 +335,7 @@ inproj_dma_kernel(InprojDmaParams q) {
                                                     4 * (lane >> 4)) = acc[i][j];
             }
             lds_barrier();
-            for (int rr = wave; rr < 128; rr += WAVES) {
+            for (int rr = wave; rr < 128; rr += GD_WAVES) {
                 const int r = r0 + half * 128 + rr;
                 if (r >= nrows) break;
                 const f32x4_t v = *reinterpret_cast<const f32x4_t*>(out + rr * GD_OUT_LD + cl);
@@ -358,7 +358,7 @@ hipError_t inproj_bf16_setup() {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(inproj_bf16_kernel<true>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, IP_LDS_BYTES);
     if (e != hipSuccess) return e;
-    e = hipFuncSetAttribute(reinterpret_cast<const void*>(inproj_dma_kernel<GD_WAVES>),
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(inproj_dma_kernel),
                             hipFuncAttributeMaxDynamicSharedMemorySize, GD_LDS_BYTES);
     if (e != hipSuccess) return e;
     return hipFuncSetAttribute(reinterpret_cast<const void*>(inproj_bf16_kernel<false>),
@@ -383,7 +383,7 @@ hipError_t launch_inproj_bf16(const Dims& d, const void* x, const float* b, cons
     const long long x_bytes = 2LL * d.B * d.T * d.D, wt_bytes = 2LL * np * dp;
     if (aligned && d.D % 8 == 0 && x_bytes < (1LL << 31) && wt_bytes < (1LL << 31)) {
         InprojDmaParams q{p, (unsigned)x_bytes, (unsigned)wt_bytes};
-        hipLaunchKernelGGL(inproj_dma_kernel<GD_WAVES>, dim3(grid), dim3(GD_WAVES * 64), GD_LDS_BYTES, s, q);
+        hipLaunchKernelGGL(inproj_dma_kernel, dim3(grid), dim3(GD_WAVES * 64), GD_LDS_BYTES, s, q);
         return hipGetLastError();
     }
     const bool kfull = (d.D % IP_BK) == 0 && aligned;
