@@ -59,6 +59,9 @@ class _Lib:
         lib.lstm_oracle_forward.argtypes = [ctypes.c_int] * 4 + [P] * 9 + [
             ctypes.c_int, ctypes.c_int, P]
         lib.lstm_oracle_forward.restype = ctypes.c_int
+        lib.lstm_oracle_forward_seq.argtypes = [ctypes.c_int] * 4 + [P] * 9 + [
+            ctypes.c_int, ctypes.c_int, P, P]
+        lib.lstm_oracle_forward_seq.restype = ctypes.c_int
         lib.lstm_oracle_max_threads.argtypes = []
         lib.lstm_oracle_max_threads.restype = ctypes.c_int
         self.lib = lib
@@ -107,8 +110,12 @@ def _f32(a):
 
 
 def forward(x, lengths, W, U, b, h0, c0, literal: bool = False, threads: int = 0,
-            return_steps: bool = False, _lib_override=None):
+            return_steps: bool = False, return_seq: bool = False, _lib_override=None):
     """Final state (h, c) in float64 of the masked LSTM loop.
+
+    With ``return_seq`` also the output sequence [B, T, H] (float64): the
+    hidden state of row b after step t for t < L[b], zero for t >= L[b]; it
+    is returned after (h, c) and before the step count.
 
     x [B, T, D], W [D, 4H], U [H, 4H], b [4H]: fp32 values (widen bf16 data
     with ``workloads.bf16_bits_to_f32`` first); h0/c0 [B, H]: fp32 or fp64
@@ -129,20 +136,26 @@ def forward(x, lengths, W, U, b, h0, c0, literal: bool = False, threads: int = 0
     h = np.empty((B, H), np.float64)
     c = np.empty((B, H), np.float64)
     steps = ctypes.c_int64(0)
-    rc = lib.lstm_oracle_forward(B, T, D, H, x.ctypes.data, L.ctypes.data, W.ctypes.data,
-                                 U.ctypes.data, b.ctypes.data, h0.ctypes.data, c0.ctypes.data,
-                                 h.ctypes.data, c.ctypes.data, int(bool(literal)), int(threads),
-                                 ctypes.byref(steps))
+    args = (B, T, D, H, x.ctypes.data, L.ctypes.data, W.ctypes.data, U.ctypes.data,
+            b.ctypes.data, h0.ctypes.data, c0.ctypes.data, h.ctypes.data, c.ctypes.data,
+            int(bool(literal)), int(threads), ctypes.byref(steps))
+    seq = None
+    if return_seq:
+        seq = np.full((B, T, H), np.nan)  # every entry must be written
+        rc = lib.lstm_oracle_forward_seq(*args, seq.ctypes.data)
+    else:
+        rc = lib.lstm_oracle_forward(*args)
     if rc == BAD_LENGTHS:
         raise OracleError("sequence lengths must lie in [0, T]")
     if rc != OK:
         raise OracleError(f"oracle failed with code {rc}")
+    out = (h, c) if seq is None else (h, c, seq)
     if return_steps:
-        return h, c, int(steps.value)
-    return h, c
+        return (*out, int(steps.value))
+    return out
 
 
-def forward_inputs(inp, rows=None, literal: bool = False, threads: int = 0):
+def forward_inputs(inp, rows=None, literal: bool = False, threads: int = 0, seq: bool = False):
     """``forward`` on a ``workloads.Inputs`` batch, optionally on a subset of rows.
 
     Rows are independent in the definition, so running the oracle on rows
@@ -153,4 +166,4 @@ def forward_inputs(inp, rows=None, literal: bool = False, threads: int = 0):
     if rows is not None:
         rows = np.asarray(rows, dtype=np.int64)
         x, L, h0, c0 = x[rows], L[rows], h0[rows], c0[rows]
-    return forward(x, L, W, U, inp.b, h0, c0, literal=literal, threads=threads)
+    return forward(x, L, W, U, inp.b, h0, c0, literal=literal, threads=threads, return_seq=seq)

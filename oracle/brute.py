@@ -15,11 +15,12 @@ def _logistic(v: float) -> float:
     return 1.0 / (1.0 + math.exp(-v))
 
 
-def run_sequence(xs, W, U, b, h, c):
+def run_sequence(xs, W, U, b, h, c, outputs=None):
     """Run the cell over the rows of ``xs`` (a list of length-D lists).
 
     W is D x 4H, U is H x 4H (nested lists), b has 4H entries; h, c have H.
-    Returns the final (h, c) as lists of floats.
+    Returns the final (h, c) as lists of floats; if ``outputs`` is a list, the
+    hidden state after each step is appended to it.
     """
     H = len(h)
     h = [float(v) for v in h]
@@ -44,6 +45,8 @@ def run_sequence(xs, W, U, b, h, c):
             new_c.append(cu)
             new_h.append(go * math.tanh(cu))
         h, c = new_h, new_c
+        if outputs is not None:
+            outputs.append(list(h))
     return h, c
 
 
@@ -64,3 +67,21 @@ def forward_per_sequence(x, lengths, W, U, b, h0, c0):
         hs.append(h)
         cs.append(c)
     return hs, cs
+
+
+def sequence_per_sequence(x, lengths, W, U, b, h0, c0):
+    """Output sequence of each sequence run alone: out[r][t] is its hidden
+    state after step t for t < L[r] and H zeros for the remaining steps up to
+    the padded extent T (the padding convention of the output sequence)."""
+    Wl = [list(map(float, row)) for row in W]
+    Ul = [list(map(float, row)) for row in U]
+    bl = list(map(float, b))
+    T, H = len(x[0]), len(h0[0])
+    out = []
+    for r in range(len(lengths)):
+        n = int(lengths[r])
+        xs = [list(map(float, x[r][t])) for t in range(n)]
+        steps = []
+        run_sequence(xs, Wl, Ul, bl, list(h0[r]), list(c0[r]), outputs=steps)
+        out.append(steps + [[0.0] * H for _ in range(T - n)])
+    return out

@@ -28,6 +28,12 @@
  * Each dot product is summed in increasing k: the x part, then the h part,
  * then the bias, so results do not depend on the thread count.
  *
+ * Optionally the per-step output sequence is returned as well: out_seq[b][t]
+ * is the hidden state row b holds after step t, i.e. the cell's output at
+ * that step, for t < L[b], and zero for t >= L[b] (the listings append the
+ * cell output at every step; no value is defined past a sequence's length,
+ * and zero is the padding convention chosen for it).
+ *
  * Two forms of the masking are provided:
  *   literal = 1 : every row runs the cell at every step and the new state is
  *                 then selected per row.
@@ -86,7 +92,7 @@ static void lstm_cell_row(int D, int H, const float* xt, const float* W, const f
 }
 
 /*
- * lstm_oracle_forward
+ * forward_impl (exported as lstm_oracle_forward and lstm_oracle_forward_seq)
  *   B, T, D, H   : batch, padded time extent, input width, hidden width (> 0)
  *   x            : [B][T][D] fp32
  *   L            : [B] int32 sequence lengths, each in [0, T]
@@ -98,12 +104,13 @@ static void lstm_cell_row(int D, int H, const float* xt, const float* W, const f
  *   literal      : 1 = compute every row then select, 0 = skip finished rows
  *   nthreads     : OpenMP threads over the rows of one step (<= 0: default)
  *   steps_out    : if non-NULL, receives the number of loop iterations run
+ *   seq_out      : if non-NULL, [B][T][H] fp64 output sequence (written)
  * Returns ORACLE_OK, or an error code with the outputs untouched.
  */
-int lstm_oracle_forward(int B, int T, int D, int H, const float* x, const int32_t* L,
+static int forward_impl(int B, int T, int D, int H, const float* x, const int32_t* L,
                         const float* W, const float* U, const float* bias,
                         const double* h0, const double* c0, double* h_out, double* c_out,
-                        int literal, int nthreads, int64_t* steps_out) {
+                        int literal, int nthreads, int64_t* steps_out, double* seq_out) {
     if (B <= 0 || T < 0 || D <= 0 || H <= 0 || !x || !L || !W || !U || !bias || !h0 || !c0 ||
         !h_out || !c_out)
         return ORACLE_BAD_ARGS;
@@ -130,6 +137,7 @@ int lstm_oracle_forward(int B, int T, int D, int H, const float* x, const int32_
         h[i] = h0[i];
         c[i] = c0[i];
     }
+    if (seq_out) memset(seq_out, 0, BH * (size_t)T * sizeof(double));  /* zero past each length */
     for (int t = 0; t < max_len; ++t) {          /* t < max_len: the loop bound */
 #ifdef _OPENMP
 #pragma omp parallel for num_threads(nt) schedule(dynamic, 1)
@@ -152,6 +160,8 @@ int lstm_oracle_forward(int B, int T, int D, int H, const float* x, const int32_
             if (t < L[b]) {
                 memcpy(h + (size_t)b * H, hn + (size_t)b * H, (size_t)H * sizeof(double));
                 memcpy(c + (size_t)b * H, cn + (size_t)b * H, (size_t)H * sizeof(double));
+                if (seq_out)                     /* the cell's output at step t */
+                    memcpy(seq_out + ((size_t)b * T + t) * H, h + (size_t)b * H, (size_t)H * sizeof(double));
             }
         }
     }
@@ -160,6 +170,24 @@ int lstm_oracle_forward(int B, int T, int D, int H, const float* x, const int32_
     if (steps_out) *steps_out = max_len;
     free(h); free(c); free(hn); free(cn); free(zs);
     return ORACLE_OK;
+}
+
+int lstm_oracle_forward(int B, int T, int D, int H, const float* x, const int32_t* L,
+                        const float* W, const float* U, const float* bias,
+                        const double* h0, const double* c0, double* h_out, double* c_out,
+                        int literal, int nthreads, int64_t* steps_out) {
+    return forward_impl(B, T, D, H, x, L, W, U, bias, h0, c0, h_out, c_out, literal, nthreads,
+                        steps_out, NULL);
+}
+
+/* As lstm_oracle_forward, and also the output sequence seq_out [B][T][H]. */
+int lstm_oracle_forward_seq(int B, int T, int D, int H, const float* x, const int32_t* L,
+                            const float* W, const float* U, const float* bias,
+                            const double* h0, const double* c0, double* h_out, double* c_out,
+                            int literal, int nthreads, int64_t* steps_out, double* seq_out) {
+    if (!seq_out) return ORACLE_BAD_ARGS;
+    return forward_impl(B, T, D, H, x, L, W, U, bias, h0, c0, h_out, c_out, literal, nthreads,
+                        steps_out, seq_out);
 }
 
 /* Number of OpenMP threads a call with nthreads <= 0 would use. */

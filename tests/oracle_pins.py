@@ -233,6 +233,74 @@ def pin_bounds(fwd):
     assert np.all(np.abs(c) <= np.abs(c0) + L[:, None] + 1e-12)
 
 
+def pin_seq_ends_and_padding(fwd):
+    """The output sequence holds the final state at the last step of each
+    sequence (bitwise) and zeros at every later step; a row of length 0 is all
+    zeros."""
+    x, L, W, U, b, h0, c0 = _case(23, 6, 4, 5, 9)
+    L[:] = [9, 0, 4, 1, 6, 2]
+    h, c, seq = fwd(x, L, W, U, b, h0, c0, return_seq=True)
+    assert seq.shape == (6, 9, 5)
+    for r in range(len(L)):
+        n = int(L[r])
+        if n:
+            assert _bits_equal(seq[r, n - 1], h[r])
+        assert np.all(seq[r, n:] == 0.0) and not np.signbit(seq[r, n:]).any()
+    h2, c2 = fwd(x, L, W, U, b, h0, c0)
+    assert _bits_equal(h, h2) and _bits_equal(c, c2)
+
+
+def pin_seq_prefixes(fwd):
+    """Step t of the output sequence equals the final hidden state of the run
+    whose lengths are cut to min(L, t + 1), for every row still active at t
+    (bitwise: the same steps in the same order)."""
+    x, L, W, U, b, h0, c0 = _case(24, 5, 3, 4, 7)
+    _, _, seq = fwd(x, L, W, U, b, h0, c0, return_seq=True)
+    for t in range(x.shape[1]):
+        ht, _ = fwd(x, np.minimum(L, t + 1).astype(np.int32), W, U, b, h0, c0)
+        for r in range(len(L)):
+            if t < L[r]:
+                assert _bits_equal(seq[r, t], ht[r]), (t, r)
+
+
+def pin_seq_brute_force(fwd, seeds=range(12)):
+    """Agreement (<= 1e-12) of the output sequence with each sequence run
+    alone in pure Python, padded with zeros past its length."""
+    for s in seeds:
+        rng = np.random.default_rng(4000 + s)
+        B, D, H, T = (int(rng.integers(1, 5)), int(rng.integers(1, 4)), int(rng.integers(1, 4)),
+                      int(rng.integers(1, 7)))
+        x, L, W, U, b, h0, c0 = _case(5000 + s, B, D, H, T)
+        b = (np.random.default_rng(s).standard_normal(4 * H) * 0.5).astype(np.float32)
+        _, _, seq = fwd(x, L, W, U, b, h0, c0, return_seq=True)
+        want = np.array(brute.sequence_per_sequence(x, L, W, U, b, h0, c0))
+        assert np.max(np.abs(seq - want)) <= 1e-12, (s, B, D, H, T)
+
+
+def pin_seq_torch_lstm(fwd, shapes=((3, 4, 5, 6), (6, 10, 8, 9))):
+    """Agreement (<= 1e-12) with torch.nn.LSTM in float64 on packed sequences,
+    unpacked with zero padding to the full extent T."""
+    import torch
+    from torch.nn.utils.rnn import pack_padded_sequence, pad_packed_sequence
+    for k, (B, D, H, T) in enumerate(shapes):
+        x, L, W, U, b, h0, c0 = _case(6000 + k, B, D, H, T, lo=1)
+        b = (np.random.default_rng(k).standard_normal(4 * H) * 0.5).astype(np.float32)
+        _, _, seq = fwd(x, L, W, U, b, h0, c0, return_seq=True)
+        m = torch.nn.LSTM(D, H, batch_first=True).double()
+        with torch.no_grad():
+            m.weight_ih_l0.copy_(torch.from_numpy(W.astype(np.float64).T))
+            m.weight_hh_l0.copy_(torch.from_numpy(U.astype(np.float64).T))
+            m.bias_ih_l0.copy_(torch.from_numpy(b.astype(np.float64)))
+            m.bias_hh_l0.zero_()
+            packed = pack_padded_sequence(torch.from_numpy(x.astype(np.float64)),
+                                          torch.from_numpy(L.astype(np.int64)),
+                                          batch_first=True, enforce_sorted=False)
+            out, _ = m(packed, (torch.from_numpy(h0.astype(np.float64))[None],
+                                torch.from_numpy(c0.astype(np.float64))[None]))
+            out, _ = pad_packed_sequence(out, batch_first=True, total_length=T)
+        assert np.max(np.abs(seq - out.numpy())) <= 1e-12, (B, D, H, T)
+
+
 PINS = [
     pin_zero_weights_closed_form,
     pin_forget_bias_closed_form,
@@ -248,4 +316,8 @@ PINS = [
     pin_torch_lstm,
     pin_literal_equals_skip,
     pin_bounds,
+    pin_seq_ends_and_padding,
+    pin_seq_prefixes,
+    pin_seq_brute_force,
+    pin_seq_torch_lstm,
 ]

@@ -31,6 +31,11 @@ MUTANTS = {
     "ignore_initial_hidden": ("h[i] = h0[i];", "h[i] = 0.0; (void)h0[i];"),
     "gx_row_stride": ("const float* xt = x + ((size_t)b * T + t) * D;",
                       "const float* xt = x + ((size_t)t * B + b) * D;"),
+    # the output sequence
+    "seq_holds_cell_state": ("memcpy(seq_out + ((size_t)b * T + t) * H, h + (size_t)b * H,",
+                             "memcpy(seq_out + ((size_t)b * T + t) * H, c + (size_t)b * H,"),
+    "seq_time_major": ("memcpy(seq_out + ((size_t)b * T + t) * H,", "memcpy(seq_out + ((size_t)t * B + b) * H,"),
+    "seq_padding_not_zeroed": ("if (seq_out) memset(seq_out, 0, BH", "if (seq_out) memset(seq_out, 0, 0 * BH"),
 }
 
 
