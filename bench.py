@@ -156,6 +156,8 @@ def main():
     ap.add_argument("--per-step-reps", type=int, default=3,
                     help="forwards of the per-step path to time (0: skip)")
     ap.add_argument("--no-tiny", action="store_true", help="skip the tiny_f32 launch-overhead leg")
+    ap.add_argument("--no-seq", action="store_true",
+                    help="skip timing the forward that also writes the output sequence")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain copy of known size (for scaling HBM counters)")
     args = ap.parse_args()
@@ -190,6 +192,23 @@ def main():
     groups = model.query(ld.Q_GROUPS)
     model.set_option(ld.OPT_TIMING, 0)
     t_wall = time_whole(torch, model, dev, args.steps, 1, out)
+
+    seq_leg = None
+    if not args.no_seq:
+        # the same forward, also writing out_seq [B, T, H] (zeros past each length)
+        _log("persistent path with the output sequence")
+        out_seq = torch.empty((w.B, w.T, w.H), device="cuda")
+        for _ in range(2):
+            model.forward_seq(*dev, out_h=out[0], out_c=out[1], out_seq=out_seq)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(5):
+            model.forward_seq(*dev, out_h=out[0], out_c=out[1], out_seq=out_seq)
+        torch.cuda.synchronize()
+        t_seq = (time.perf_counter() - t0) / 5
+        seq_leg = {"ms_per_forward": t_seq * 1e3, "launches_per_forward": model.query(ld.Q_LAUNCHES_PER_FORWARD),
+                   "out_seq_bytes": 4 * w.B * w.T * w.H}
+        del out_seq
 
     per_step = None
     if args.per_step_reps > 0:
@@ -255,6 +274,7 @@ def main():
         "launches_per_forward": launches,
         "wall_ms_per_step": t_wall * 1e3,
         "per_step_path": per_step,
+        "forward_seq": seq_leg,
         "tiny_f32": tiny,
     }
     if not args.no_cpu:

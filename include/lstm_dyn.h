@@ -134,6 +134,24 @@ int lstm_dyn_forward(lstm_dyn_t* h, const void* x, const int32_t* lengths, const
                      const void* U, const float* b, const float* h0, const float* c0,
                      float* out_h, float* out_c, void* stream);
 
+/*
+ * lstm_dyn_forward_seq: lstm_dyn_forward, and also the output sequence.  The
+ * paper's loop (Section 9 "RNN cells"; Appendix A) appends the cell's output
+ * at every step; here
+ *     out_seq [B][T_max][H] fp32 (caller-owned device memory, 4-byte aligned,
+ *     written in full): out_seq[b][t] = the hidden state of sequence b after
+ *     step t for t < L[b] (so out_seq[b][L[b]-1] = out_h[b]), and zero for
+ *     t >= L[b] (no output is defined past a sequence's length; zero is the
+ *     padding chosen).  Lengths outside [0, T_max] are clamped as in
+ *     lstm_dyn_forward.
+ * out_seq may not overlap any other argument.  One more kernel launch than
+ * lstm_dyn_forward (it writes the zeros past each length and, in persistent
+ * mode, moves the step outputs into place).  Returns as lstm_dyn_forward.
+ */
+int lstm_dyn_forward_seq(lstm_dyn_t* h, const void* x, const int32_t* lengths, const void* W,
+                         const void* U, const float* b, const float* h0, const float* c0,
+                         float* out_h, float* out_c, float* out_seq, void* stream);
+
 /* Free the handle and its workspace (synchronises the device).  NULL is a no-op. */
 int lstm_dyn_destroy(lstm_dyn_t* h);
 
@@ -174,6 +192,13 @@ int lstm_dyn_plan(int B, int D, int H, int T_max, int dtype, int mode, int num_c
 int lstm_dyn_check_args(int B, int D, int H, int T_max, int dtype, const void* x,
                         const int32_t* lengths, const void* W, const void* U, const float* b,
                         const float* h0, const float* c0, const float* out_h, const float* out_c);
+
+/* lstm_dyn_check_args, and the checks of out_seq for lstm_dyn_forward_seq
+ * (NULL, 4-byte alignment, overlap with any other argument). */
+int lstm_dyn_check_seq_args(int B, int D, int H, int T_max, int dtype, const void* x,
+                            const int32_t* lengths, const void* W, const void* U, const float* b,
+                            const float* h0, const float* c0, const float* out_h,
+                            const float* out_c, const float* out_seq);
 
 #ifdef __cplusplus
 }

@@ -18,7 +18,7 @@ __all__ = [
     "F32", "BF16", "PERSISTENT", "PER_STEP", "LstmDynError", "LstmDyn", "library_path",
     "lstm_dyn_create", "lstm_dyn_forward", "lstm_dyn_destroy", "lstm_dyn_query",
     "lstm_dyn_strerror", "lstm_dyn_plan", "lstm_dyn_check_args", "lstm_dyn_set_option",
-    "lstm_dyn_step_trace",
+    "lstm_dyn_step_trace", "lstm_dyn_forward_seq", "lstm_dyn_check_seq_args",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -69,6 +69,10 @@ def _load():
     lib.lstm_dyn_create.restype = I
     lib.lstm_dyn_forward.argtypes = [P] * 11
     lib.lstm_dyn_forward.restype = I
+    lib.lstm_dyn_forward_seq.argtypes = [P] * 12
+    lib.lstm_dyn_forward_seq.restype = I
+    lib.lstm_dyn_check_seq_args.argtypes = [I] * 5 + [P] * 10
+    lib.lstm_dyn_check_seq_args.restype = I
     lib.lstm_dyn_destroy.argtypes = [P]
     lib.lstm_dyn_destroy.restype = I
     lib.lstm_dyn_query.argtypes = [P, I, ctypes.POINTER(LL)]
@@ -106,6 +110,14 @@ def lstm_dyn_forward(handle: int, x: int, lengths: int, W: int, U: int, b: int, 
     rc = _load().lstm_dyn_forward(handle, x, lengths, W, U, b, h0, c0, out_h, out_c, stream)
     if rc != OK:
         raise LstmDynError(rc, "lstm_dyn_forward")
+
+
+def lstm_dyn_forward_seq(handle: int, x: int, lengths: int, W: int, U: int, b: int, h0: int,
+                         c0: int, out_h: int, out_c: int, out_seq: int, stream: int = 0) -> None:
+    rc = _load().lstm_dyn_forward_seq(handle, x, lengths, W, U, b, h0, c0, out_h, out_c, out_seq,
+                                      stream)
+    if rc != OK:
+        raise LstmDynError(rc, "lstm_dyn_forward_seq")
 
 
 def lstm_dyn_destroy(handle: int) -> None:
@@ -153,6 +165,13 @@ def lstm_dyn_check_args(B: int, D: int, H: int, T_max: int, dtype: int, x: int, 
                         W: int, U: int, b: int, h0: int, c0: int, out_h: int, out_c: int) -> int:
     return _load().lstm_dyn_check_args(B, D, H, T_max, dtype, x, lengths, W, U, b, h0, c0,
                                        out_h, out_c)
+
+
+def lstm_dyn_check_seq_args(B: int, D: int, H: int, T_max: int, dtype: int, x: int, lengths: int,
+                            W: int, U: int, b: int, h0: int, c0: int, out_h: int, out_c: int,
+                            out_seq: int) -> int:
+    return _load().lstm_dyn_check_seq_args(B, D, H, T_max, dtype, x, lengths, W, U, b, h0, c0,
+                                           out_h, out_c, out_seq)
 
 
 # --- torch convenience wrapper ---------------------------------------------
@@ -209,6 +228,37 @@ class LstmDyn:
         return out_h, out_c
 
     __call__ = forward
+
+    def forward_seq(self, x, lengths, W, U, b, h0, c0, out_h=None, out_c=None, out_seq=None,
+                    stream=None):
+        """``forward``, and also the output sequence out_seq float32 [B, T_max, H]:
+        the hidden state of row b after step t for t < L[b], zero after.
+        Returns (out_h, out_c, out_seq)."""
+        import torch
+        B, D, H, T = self.B, self.D, self.H, self.T
+        et = torch.bfloat16 if self.dtype == BF16 else torch.float32
+        for name, t, dt, shape in (("x", x, et, (B, T, D)), ("lengths", lengths, torch.int32, (B,)),
+                                   ("W", W, et, (D, 4 * H)), ("U", U, et, (H, 4 * H)),
+                                   ("b", b, torch.float32, (4 * H,)),
+                                   ("h0", h0, torch.float32, (B, H)),
+                                   ("c0", c0, torch.float32, (B, H))):
+            self._check(name, t, dt, shape)
+        if out_h is None:
+            out_h = torch.empty((B, H), dtype=torch.float32, device=x.device)
+        if out_c is None:
+            out_c = torch.empty((B, H), dtype=torch.float32, device=x.device)
+        if out_seq is None:
+            out_seq = torch.empty((B, T, H), dtype=torch.float32, device=x.device)
+        self._check("out_h", out_h, torch.float32, (B, H))
+        self._check("out_c", out_c, torch.float32, (B, H))
+        self._check("out_seq", out_seq, torch.float32, (B, T, H))
+        if stream is None:
+            stream = torch.cuda.current_stream(x.device)
+        s = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+        lstm_dyn_forward_seq(self.handle, x.data_ptr(), lengths.data_ptr(), W.data_ptr(),
+                             U.data_ptr(), b.data_ptr(), h0.data_ptr(), c0.data_ptr(),
+                             out_h.data_ptr(), out_c.data_ptr(), out_seq.data_ptr(), s)
+        return out_h, out_c, out_seq
 
     def query(self, what: int) -> int:
         return lstm_dyn_query(self.handle, what)

@@ -158,6 +158,24 @@ extern "C" int lstm_dyn_check_args(int B, int D, int H, int T, int dtype, const 
     return LSTM_DYN_OK;
 }
 
+extern "C" int lstm_dyn_check_seq_args(int B, int D, int H, int T, int dtype, const void* x,
+                                       const int32_t* lengths, const void* W, const void* U,
+                                       const float* b, const float* h0, const float* c0,
+                                       const float* out_h, const float* out_c, const float* out_seq) {
+    const int rc = lstm_dyn_check_args(B, D, H, T, dtype, x, lengths, W, U, b, h0, c0, out_h, out_c);
+    if (rc != LSTM_DYN_OK) return rc;
+    if (!out_seq || (reinterpret_cast<uintptr_t>(out_seq) & 3) != 0) return LSTM_DYN_ERR_INVALID;
+    const long long e = dtype == LSTM_DYN_BF16 ? 2 : 4;
+    const long long nseq = 4LL * B * T * H;
+    const void* others[] = {x, lengths, W, U, b, h0, c0, out_h, out_c};
+    const long long sizes[] = {(long long)B * T * D * e, 4LL * B, (long long)D * 4 * H * e,
+                               (long long)H * 4 * H * e, 16LL * H, 4LL * B * H, 4LL * B * H,
+                               4LL * B * H, 4LL * B * H};
+    for (int i = 0; i < 9; ++i)
+        if (overlaps(out_seq, nseq, others[i], sizes[i])) return LSTM_DYN_ERR_INVALID;
+    return LSTM_DYN_OK;
+}
+
 extern "C" int lstm_dyn_create(lstm_dyn_t** out, int B, int D, int H, int T, int dtype, int mode) {
     if (!out) return LSTM_DYN_ERR_INVALID;
     *out = nullptr;
@@ -305,13 +323,10 @@ static hipError_t input_projection(lstm_dyn* h, const void* x, const void* W, co
     return e;
 }
 
-extern "C" int lstm_dyn_forward(lstm_dyn_t* h, const void* x, const int32_t* lengths, const void* W,
-                                const void* U, const float* b, const float* h0, const float* c0,
-                                float* out_h, float* out_c, void* stream) {
-    if (!h) return LSTM_DYN_ERR_INVALID;
-    int rc = lstm_dyn_check_args(h->B, h->D, h->H, h->T, h->dtype, x, lengths, W, U, b, h0, c0,
-                                 out_h, out_c);
-    if (rc != LSTM_DYN_OK) return rc;
+// The forward of both entry points; out_seq is null for lstm_dyn_forward.
+static int forward_impl(lstm_dyn_t* h, const void* x, const int32_t* lengths, const void* W,
+                        const void* U, const float* b, const float* h0, const float* c0,
+                        float* out_h, float* out_c, float* out_seq, void* stream) {
     hipStream_t s = static_cast<hipStream_t>(stream);
     h->last_stream = s;
     h->launches_last = 0;
@@ -330,9 +345,13 @@ extern "C" int lstm_dyn_forward(lstm_dyn_t* h, const void* x, const int32_t* len
         LD_CHECK(mark(1));
         LD_CHECK(mark(2));
         LD_CHECK(launch_small(d, h->plan.single_kd, h->plan.single_nt, x, lengths, W, U, b, h0, c0,
-                              out_h, out_c, h->ws, s));
+                              out_h, out_c, out_seq, h->ws, s));
         h->launches_last = 1;
         LD_CHECK(mark(3));
+        if (out_seq) {
+            LD_CHECK(launch_seq_finish(d, out_seq, false, 4, lengths, h->ws, h->num_cus, s));
+            h->launches_last++;
+        }
         return LSTM_DYN_OK;
     }
     LD_CHECK(mark(0));
@@ -342,11 +361,16 @@ extern "C" int lstm_dyn_forward(lstm_dyn_t* h, const void* x, const int32_t* len
     if (h->mode == LSTM_DYN_PERSISTENT) {
         LD_CHECK(input_projection(h, x, W, b, s));
         LD_CHECK(mark(2));
-        PersistentConfig pc{h->plan.mt, h->plan.groups, h->plan.ksw,       h->plan.kw,
-                            h->plan.nstate, h->plan.lds_bytes, h->timeout_ticks, h->trace};
+        PersistentConfig pc{h->plan.mt,     h->plan.groups,    h->plan.ksw, h->plan.kw,
+                            h->plan.nstate, h->plan.lds_bytes, h->timeout_ticks, h->trace,
+                            out_seq != nullptr};
         LD_CHECK(launch_persistent(d, pc, U, h0, c0, out_h, out_c, h->ws, s));
         h->launches_last++;
         LD_CHECK(mark(3));
+        if (out_seq) {
+            LD_CHECK(launch_seq_finish(d, out_seq, true, 4 * h->plan.mt, lengths, h->ws, h->num_cus, s));
+            h->launches_last++;
+        }
         return LSTM_DYN_OK;
     }
     // Per-step comparison path.
@@ -360,12 +384,37 @@ extern "C" int lstm_dyn_forward(lstm_dyn_t* h, const void* x, const int32_t* len
     const int max_len = *h->host_maxlen;
     for (int t = 0; t < max_len; ++t) {
         LD_CHECK(launch_step_gemm(d, t, U, h->ws, s));
-        LD_CHECK(launch_step_gates(d, t, out_h, out_c, h->ws, s));
+        LD_CHECK(launch_step_gates(d, t, out_h, out_c, out_seq, h->ws, s));
         h->launches_last += 2;
     }
     LD_CHECK(mark(3));
+    if (out_seq) {
+        LD_CHECK(launch_seq_finish(d, out_seq, false, 4, lengths, h->ws, h->num_cus, s));
+        h->launches_last++;
+    }
 #undef LD_CHECK
     return LSTM_DYN_OK;
+}
+
+extern "C" int lstm_dyn_forward(lstm_dyn_t* h, const void* x, const int32_t* lengths, const void* W,
+                                const void* U, const float* b, const float* h0, const float* c0,
+                                float* out_h, float* out_c, void* stream) {
+    if (!h) return LSTM_DYN_ERR_INVALID;
+    const int rc = lstm_dyn_check_args(h->B, h->D, h->H, h->T, h->dtype, x, lengths, W, U, b, h0,
+                                       c0, out_h, out_c);
+    if (rc != LSTM_DYN_OK) return rc;
+    return forward_impl(h, x, lengths, W, U, b, h0, c0, out_h, out_c, nullptr, stream);
+}
+
+extern "C" int lstm_dyn_forward_seq(lstm_dyn_t* h, const void* x, const int32_t* lengths,
+                                    const void* W, const void* U, const float* b, const float* h0,
+                                    const float* c0, float* out_h, float* out_c, float* out_seq,
+                                    void* stream) {
+    if (!h) return LSTM_DYN_ERR_INVALID;
+    const int rc = lstm_dyn_check_seq_args(h->B, h->D, h->H, h->T, h->dtype, x, lengths, W, U, b,
+                                           h0, c0, out_h, out_c, out_seq);
+    if (rc != LSTM_DYN_OK) return rc;
+    return forward_impl(h, x, lengths, W, U, b, h0, c0, out_h, out_c, out_seq, stream);
 }
 
 extern "C" int lstm_dyn_query(lstm_dyn_t* h, int what, long long* value) {

@@ -50,6 +50,7 @@ struct PersistentConfig {
     int mt, groups, ksw, kw, nst, lds_bytes;
     unsigned long long timeout_ticks;  // barrier wait bound in wall-clock ticks
     unsigned long long* trace;         // per-step timestamps (diagnostics) or null
+    int seq;                           // 1: keep each step's h in the dead Gx rows (output sequence)
 };
 constexpr int BAR_WORDS = 64 * 9;  // global + 8 group counters, 256 bytes apart
 hipError_t launch_persistent(const Dims& d, const PersistentConfig& pc, const void* U,
@@ -65,14 +66,20 @@ int persistent_lds_bytes(int bf16, int mt, int kw, int nst, int hpad);
 bool small_pick(int bf16, int B, int D, int H, int* kd, int* nt);
 hipError_t launch_small(const Dims& d, int kd, int nt, const void* x, const int32_t* lengths,
                         const void* W, const void* U, const float* b, const float* h0,
-                        const float* c0, float* out_h, float* out_c, const Workspace& ws,
-                        hipStream_t s);
+                        const float* c0, float* out_h, float* out_c, float* seq,
+                        const Workspace& ws, hipStream_t s);
 
 // Per-step comparison path.
 hipError_t launch_step_init(const Dims& d, const float* h0, const float* c0, float* out_h,
                             float* out_c, const Workspace& ws, hipStream_t s);
 hipError_t launch_step_gemm(const Dims& d, int t, const void* U, const Workspace& ws, hipStream_t s);
-hipError_t launch_step_gates(const Dims& d, int t, float* out_h, float* out_c, const Workspace& ws,
-                             hipStream_t s);
+hipError_t launch_step_gates(const Dims& d, int t, float* out_h, float* out_c, float* seq,
+                             const Workspace& ws, hipStream_t s);
+
+// Output sequence: moves the persistent loop's step outputs (kept in the
+// dead Gx rows, unit slices of upw) to seq [B][T][H] when from_gx, and
+// writes zeros past each length.
+hipError_t launch_seq_finish(const Dims& d, float* seq, bool from_gx, int upw, const int32_t* lengths,
+                             const Workspace& ws, int num_cus, hipStream_t s);
 
 }  // namespace ldyn

@@ -51,6 +51,7 @@ struct PersistParams {
     int B, H, hpad, bpad, groups;
     unsigned long long timeout_ticks;
     unsigned long long* trace;  // [T + 1][4] timestamps from workgroup 0, or null
+    int seq;                    // 1: also keep each step's h (fp32) for the output sequence
 };
 
 // Logical workgroup index: consecutive workgroups are dispatched to different
@@ -662,6 +663,18 @@ persistent_kernel(PersistParams p) {
                     if (lo < 16 && nt * 16 + lo < act)
                         seg_store(nxt + hx_off<E>(nt * 16 + lo, u0, hpad), &hstage[w][lo * UPW]);
                     __builtin_amdgcn_wave_barrier();
+                    if (p.seq) {
+                        // the output sequence: h of (row, unit) in fp32, kept in the
+                        // first UPW floats of this workgroup's columns of the row's
+                        // Gx, which nothing reads again (its own Gx prefetch of
+                        // this step has landed; no other workgroup reads them)
+                        float* const row = const_cast<float*>(p.gx) + (size_t)(o0 + nt * 16 + (lo & 15)) * H4 + 4 * u0;
+#pragma unroll
+                        for (int mt = 0; mt < MT; ++mt) {
+                            const int u = u0 + mt * 4 + (lo >> 4);
+                            if (nt * 16 + (lo & 15) < act && u < H) row[mt * 4 + (lo >> 4)] = hst[a * MT + mt];
+                        }
+                    }
                 }
             }
         }
@@ -793,6 +806,7 @@ hipError_t launch_persistent(const Dims& d, const PersistentConfig& pc, const vo
     p.groups = pc.groups;
     p.timeout_ticks = pc.timeout_ticks;
     p.trace = pc.trace;
+    p.seq = pc.seq;
     void* args[] = {&p};
     return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(f), dim3(pc.groups),
                                       dim3(pc.kw * 64), args, (unsigned)pc.lds_bytes, s);

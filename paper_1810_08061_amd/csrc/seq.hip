@@ -1,0 +1,79 @@
+// seq.hip -- the output sequence of the loop.
+//
+// The loop of the paper (Section 9 "RNN cells", Appendix A) appends the
+// cell's output at every step.  out_seq[b][t] is the hidden state of row b
+// after step t for t < L[b]; past a sequence's length the output is zero (no
+// value is defined there; zero is the padding convention chosen).
+//
+// The persistent loop leaves the step outputs of compact row r (one valid
+// (b, t), numbered as the input projection numbers them) inside that row's
+// Gx, whose values it no longer needs: unit u of workgroup slice q = u / UPW
+// at float q * 4 UPW + u mod UPW.  This kernel moves those rows to
+// out_seq[b][t] and writes the zeros past each length; the other modes write
+// their valid outputs directly and use it for the zeros only.
+#include "launch.h"
+
+namespace ldyn {
+
+struct SeqParams {
+    float* seq;              // [B][T][H]
+    const float* gx;         // compact rows with the step outputs inside, or null
+    const int32_t* rowsrc;   // compact row -> b * T + t
+    const Meta* meta;        // total_rows (read only when gx is set)
+    const int32_t* lengths;  // [B] as passed (clamped here to [0, T])
+    int B, T, H, upw;
+};
+
+// One wave per output row; float4 accesses when H is a multiple of 4 (rows of
+// out_seq and of Gx are then 16-byte aligned).
+template <bool VEC>
+__global__ void __launch_bounds__(256)
+seq_finish_kernel(SeqParams p) {
+    const int lane = threadIdx.x & 63;
+    const long wave = ((long)blockIdx.x * 256 + threadIdx.x) >> 6;
+    const long nwaves = (long)gridDim.x * 4;
+    const int H = p.H, T = p.T, upw = p.upw;
+    if (p.gx) {
+        const long rows = p.meta->total_rows;
+        for (long r = wave; r < rows; r += nwaves) {
+            const float* src = p.gx + (size_t)r * 4 * H;
+            float* dst = p.seq + (size_t)p.rowsrc[r] * H;
+            if constexpr (VEC) {
+                for (int u = 4 * lane; u < H; u += 256)  // u .. u+3 lie in one slice (upw is 4 or 8)
+                    *reinterpret_cast<f32x4_t*>(dst + u) =
+                        *reinterpret_cast<const f32x4_t*>(src + (u / upw) * 4 * upw + u % upw);
+            } else {
+                for (int u = lane; u < H; u += 64) dst[u] = src[(u / upw) * 4 * upw + u % upw];
+            }
+        }
+    }
+    const long nrows = (long)p.B * T;
+    for (long row = wave; row < nrows; row += nwaves) {
+        const int b = (int)(row / T), t = (int)(row - (long)b * T);
+        const int L = min(max(p.lengths[b], 0), T);
+        if (t < L) continue;
+        float* dst = p.seq + (size_t)row * H;
+        if constexpr (VEC) {
+            for (int u = 4 * lane; u < H; u += 256) *reinterpret_cast<f32x4_t*>(dst + u) = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        } else {
+            for (int u = lane; u < H; u += 64) dst[u] = 0.0f;
+        }
+    }
+}
+
+hipError_t launch_seq_finish(const Dims& d, float* seq, bool from_gx, int upw, const int32_t* lengths,
+                             const Workspace& ws, int num_cus, hipStream_t s) {
+    SeqParams p{seq, from_gx ? ws.gx : nullptr, ws.rowsrc, ws.meta, lengths, d.B, d.T, d.H, upw};
+    const long rows = (long)d.B * d.T;
+    long grid = (rows + 3) / 4;
+    if (grid > 8L * num_cus) grid = 8L * num_cus;
+    if (grid < 1) grid = 1;
+    const bool vec = d.H % 4 == 0 && (reinterpret_cast<uintptr_t>(seq) & 15) == 0;
+    if (vec)
+        hipLaunchKernelGGL(seq_finish_kernel<true>, dim3((unsigned)grid), dim3(256), 0, s, p);
+    else
+        hipLaunchKernelGGL(seq_finish_kernel<false>, dim3((unsigned)grid), dim3(256), 0, s, p);
+    return hipGetLastError();
+}
+
+}  // namespace ldyn

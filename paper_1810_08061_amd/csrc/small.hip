@@ -26,6 +26,7 @@ struct SmallParams {
     const float* c0;
     float* out_h;
     float* out_c;
+    float* seq;  // [B][T][H] output sequence (valid steps only), or null
     Meta* meta;
     int B, D, H, T;
 };
@@ -185,6 +186,7 @@ small_kernel(SmallParams p) {
                     lstm_cell(z, c, h);
                     cst[mt][nt] = c;
                     hst[mt][nt] = h;
+                    if (p.seq) p.seq[((size_t)n * T + t) * H + u] = h;  // output at step t
                 }
                 hnext[n * HS + u] = E::from_f32(hst[mt][nt]);
             }
@@ -246,13 +248,13 @@ bool small_pick(int bf16, int B, int D, int H, int* kd, int* nt) {
 
 hipError_t launch_small(const Dims& d, int kd, int nt, const void* x, const int32_t* lengths,
                         const void* W, const void* U, const float* b, const float* h0,
-                        const float* c0, float* out_h, float* out_c, const Workspace& ws,
-                        hipStream_t s) {
+                        const float* c0, float* out_h, float* out_c, float* seq,
+                        const Workspace& ws, hipStream_t s) {
     small_fn f = nullptr;
     for (const SmallVariant& v : kSmall)
         if (v.bf16 == d.bf16 && v.kd == kd && v.nt == nt) f = v.f;
     if (!f) return hipErrorInvalidValue;
-    SmallParams p{x, lengths, W, U, b, h0, c0, out_h, out_c, ws.meta, d.B, d.D, d.H, d.T};
+    SmallParams p{x, lengths, W, U, b, h0, c0, out_h, out_c, seq, ws.meta, d.B, d.D, d.H, d.T};
     hipLaunchKernelGGL(f, dim3(1), dim3(SM_THREADS), 0, s, p);
     return hipGetLastError();
 }

@@ -33,7 +33,7 @@ template <typename E>
 __global__ void __launch_bounds__(256)
 step_gates_kernel(const float* __restrict__ z, float* out_h, float* out_c,
                   const int32_t* __restrict__ perm, const int32_t* __restrict__ offsets,
-                  typename E::store_t* hx, int t, int H, int hpad) {
+                  typename E::store_t* hx, int t, int H, int hpad, float* seq, int T) {
     const int act = offsets[t + 1] - offsets[t];
     const long n = (long)act * H;
     for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += (long)gridDim.x * 256) {
@@ -46,6 +46,7 @@ step_gates_kernel(const float* __restrict__ z, float* out_h, float* out_c,
         out_c[ib] = c;
         out_h[ib] = h;
         hx[(long)s * hpad + u] = E::from_f32(h);
+        if (seq) seq[((size_t)b * T + t) * H + u] = h;  // the output sequence at step t
     }
 }
 
@@ -68,15 +69,15 @@ hipError_t launch_step_init(const Dims& d, const float* h0, const float* c0, flo
     return hipGetLastError();
 }
 
-hipError_t launch_step_gates(const Dims& d, int t, float* out_h, float* out_c, const Workspace& ws,
-                             hipStream_t s) {
+hipError_t launch_step_gates(const Dims& d, int t, float* out_h, float* out_c, float* seq,
+                             const Workspace& ws, hipStream_t s) {
     const int grid = grid_for((long)d.B * d.H);
     if (d.bf16)
         hipLaunchKernelGGL(step_gates_kernel<EltBF16>, dim3(grid), dim3(256), 0, s, ws.z, out_h,
-                           out_c, ws.perm, ws.offsets, static_cast<__bf16*>(ws.hx), t, d.H, d.hpad);
+                           out_c, ws.perm, ws.offsets, static_cast<__bf16*>(ws.hx), t, d.H, d.hpad, seq, d.T);
     else
         hipLaunchKernelGGL(step_gates_kernel<EltF32>, dim3(grid), dim3(256), 0, s, ws.z, out_h,
-                           out_c, ws.perm, ws.offsets, static_cast<float*>(ws.hx), t, d.H, d.hpad);
+                           out_c, ws.perm, ws.offsets, static_cast<float*>(ws.hx), t, d.H, d.hpad, seq, d.T);
     return hipGetLastError();
 }
 

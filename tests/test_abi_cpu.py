@@ -122,3 +122,17 @@ def test_check_args():
     q = list(p)
     q[7] = q[6]                                  # out_h on c0
     assert ld.lstm_dyn_check_args(B, D, H, T, ld.F32, *q) == ld.ERR_INVALID
+
+
+def test_check_seq_args():
+    B, D, H, T = 3, 5, 7, 4
+    p = _ptrs(B, D, H, T, 4)
+    seq = p[-1] + (4 * B * H + 255) // 256 * 256 + 512       # after every other buffer
+    assert ld.lstm_dyn_check_seq_args(B, D, H, T, ld.F32, *p, seq) == ld.OK
+    assert ld.lstm_dyn_check_seq_args(B, D, H, T, ld.F32, *p, 0) == ld.ERR_INVALID
+    assert ld.lstm_dyn_check_seq_args(B, D, H, T, ld.F32, *p, seq + 2) == ld.ERR_INVALID
+    for i in range(9):                           # out_seq on top of any other argument
+        assert ld.lstm_dyn_check_seq_args(B, D, H, T, ld.F32, *p, p[i]) == ld.ERR_INVALID
+    q = list(p)
+    q[0] = 0                                     # the plain checks still apply
+    assert ld.lstm_dyn_check_seq_args(B, D, H, T, ld.F32, *q, seq) == ld.ERR_INVALID
