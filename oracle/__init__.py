@@ -62,6 +62,9 @@ class _Lib:
         lib.lstm_oracle_forward_seq.argtypes = [ctypes.c_int] * 4 + [P] * 9 + [
             ctypes.c_int, ctypes.c_int, P, P]
         lib.lstm_oracle_forward_seq.restype = ctypes.c_int
+        lib.lstm_oracle_forward_gru.argtypes = [ctypes.c_int] * 4 + [P] * 10 + [
+            ctypes.c_int, ctypes.c_int, P, P]
+        lib.lstm_oracle_forward_gru.restype = ctypes.c_int
         lib.lstm_oracle_max_threads.argtypes = []
         lib.lstm_oracle_max_threads.restype = ctypes.c_int
         self.lib = lib
@@ -153,6 +156,45 @@ def forward(x, lengths, W, U, b, h0, c0, literal: bool = False, threads: int = 0
     if return_steps:
         return (*out, int(steps.value))
     return out
+
+
+def forward_gru(x, lengths, W, U, b_ih, b_hh, h0, literal: bool = False, threads: int = 0,
+                return_seq: bool = False, return_steps: bool = False, _lib_override=None):
+    """Final hidden state h in float64 of the masked loop with the GRU cell.
+
+    x [B, T, D], W [D, 3H], U [H, 3H] with gate blocks (r, u, n), b_ih, b_hh
+    [3H]: fp32 values; h0 [B, H] fp32 or fp64; lengths as for ``forward``.
+    With ``return_seq`` also the output sequence [B, T, H] (zeros past each
+    length).
+    """
+    lib = (_lib_override or _load()).lib
+    x, W, U, b_ih, b_hh = map(_f32, (x, W, U, b_ih, b_hh))
+    h0 = np.ascontiguousarray(h0, dtype=np.float64)
+    L = np.ascontiguousarray(lengths, dtype=np.int32)
+    B, T, D = x.shape
+    H = U.shape[0]
+    if W.shape != (D, 3 * H) or U.shape != (H, 3 * H) or b_ih.shape != (3 * H,) or b_hh.shape != (3 * H,):
+        raise OracleError("GRU weight shapes do not match x and U")
+    if L.shape != (B,) or h0.shape != (B, H):
+        raise OracleError("lengths/state shapes do not match x")
+    c0 = np.zeros((B, H), np.float64)
+    h = np.empty((B, H), np.float64)
+    c = np.empty((B, H), np.float64)
+    seq = np.full((B, T, H), np.nan) if return_seq else None
+    steps = ctypes.c_int64(0)
+    rc = lib.lstm_oracle_forward_gru(B, T, D, H, x.ctypes.data, L.ctypes.data, W.ctypes.data,
+                                     U.ctypes.data, b_ih.ctypes.data, b_hh.ctypes.data,
+                                     h0.ctypes.data, c0.ctypes.data, h.ctypes.data, c.ctypes.data,
+                                     int(bool(literal)), int(threads), ctypes.byref(steps),
+                                     seq.ctypes.data if seq is not None else None)
+    if rc == BAD_LENGTHS:
+        raise OracleError("sequence lengths must lie in [0, T]")
+    if rc != OK:
+        raise OracleError(f"oracle failed with code {rc}")
+    out = (h,) if seq is None else (h, seq)
+    if return_steps:
+        out = (*out, int(steps.value))
+    return out[0] if len(out) == 1 else out
 
 
 def forward_inputs(inp, rows=None, literal: bool = False, threads: int = 0, seq: bool = False):

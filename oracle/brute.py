@@ -85,3 +85,39 @@ def sequence_per_sequence(x, lengths, W, U, b, h0, c0):
         run_sequence(xs, Wl, Ul, bl, list(h0[r]), list(c0[r]), outputs=steps)
         out.append(steps + [[0.0] * H for _ in range(T - n)])
     return out
+
+
+def run_sequence_gru(xs, W, U, b_ih, b_hh, h, outputs=None):
+    """GRU cell over the rows of ``xs``: W is D x 3H, U is H x 3H (gate blocks
+    r, u, n), b_ih and b_hh have 3H entries each, h has H.  Returns the final
+    h; if ``outputs`` is a list, h after each step is appended to it."""
+    H = len(h)
+    h = [float(v) for v in h]
+    for xt in xs:
+        ax = [sum(float(xk) * float(W[k][j]) for k, xk in enumerate(xt)) + float(b_ih[j]) for j in range(3 * H)]
+        ah = [sum(h[k] * float(U[k][j]) for k in range(H)) + float(b_hh[j]) for j in range(3 * H)]
+        new_h = []
+        for v in range(H):
+            r = _logistic(ax[v] + ah[v])
+            u = _logistic(ax[H + v] + ah[H + v])
+            n = math.tanh(ax[2 * H + v] + r * ah[2 * H + v])
+            new_h.append((1.0 - u) * n + u * h[v])
+        h = new_h
+        if outputs is not None:
+            outputs.append(list(h))
+    return h
+
+
+def gru_per_sequence(x, lengths, W, U, b_ih, b_hh, h0):
+    """Final h and the zero-padded output sequence of each sequence run alone
+    with the GRU cell."""
+    T, H = len(x[0]), len(h0[0])
+    hs, seqs = [], []
+    for r in range(len(lengths)):
+        n = int(lengths[r])
+        steps = []
+        h = run_sequence_gru([list(map(float, x[r][t])) for t in range(n)], W, U, b_ih, b_hh,
+                             list(h0[r]), outputs=steps)
+        hs.append(h)
+        seqs.append(steps + [[0.0] * H for _ in range(T - n)])
+    return hs, seqs

@@ -34,6 +34,17 @@
  * cell output at every step; no value is defined past a sequence's length,
  * and zero is the padding convention chosen for it).
  *
+ * The same loop with a GRU cell (the paper's rnn_cell is a parameter) is
+ * lstm_oracle_forward_gru: W [D][3H], U [H][3H] with gate blocks (r, u, n)
+ * and biases b_ih, b_hh [3H] each,
+ *
+ *   r  = sig(x_t W_r + b_ir + h U_r + b_hr)
+ *   u  = sig(x_t W_u + b_iu + h U_u + b_hu)
+ *   n  = tanh(x_t W_n + b_in + r * (h U_n + b_hn))
+ *   h' = (1 - u) n + u h
+ *
+ * and no cell state (c is carried unchanged).
+ *
  * Two forms of the masking are provided:
  *   literal = 1 : every row runs the cell at every step and the new state is
  *                 then selected per row.
@@ -91,8 +102,43 @@ static void lstm_cell_row(int D, int H, const float* xt, const float* W, const f
     }
 }
 
+/* One application of the GRU cell to one row.  W [D][3H], U [H][3H],
+ * bih, bhh [3H]; zx, zh: [3H] scratch (input and recurrent parts, each with
+ * its bias); hn: [H] new hidden state. */
+static void gru_cell_row(int D, int H, const float* xt, const float* W, const float* U,
+                         const float* bih, const float* bhh, const double* h, double* zx,
+                         double* zh, double* hn) {
+    const int G = 3 * H;
+    for (int j = 0; j < G; ++j) {
+        zx[j] = 0.0;
+        zh[j] = 0.0;
+    }
+    for (int k = 0; k < D; ++k) {              /* x_t W */
+        const double xk = (double)xt[k];
+        const float* wk = W + (size_t)k * G;
+        for (int j = 0; j < G; ++j) zx[j] += xk * (double)wk[j];
+    }
+    for (int k = 0; k < H; ++k) {              /* h U */
+        const double hk = h[k];
+        const float* uk = U + (size_t)k * G;
+        for (int j = 0; j < G; ++j) zh[j] += hk * (double)uk[j];
+    }
+    for (int j = 0; j < G; ++j) {
+        zx[j] += (double)bih[j];
+        zh[j] += (double)bhh[j];
+    }
+    for (int v = 0; v < H; ++v) {
+        const double rg = sig(zx[v] + zh[v]);
+        const double ug = sig(zx[H + v] + zh[H + v]);
+        const double ng = tanh(zx[2 * H + v] + rg * zh[2 * H + v]);
+        hn[v] = (1.0 - ug) * ng + ug * h[v];
+    }
+}
+
 /*
- * forward_impl (exported as lstm_oracle_forward and lstm_oracle_forward_seq)
+ * forward_impl (exported as lstm_oracle_forward and lstm_oracle_forward_seq;
+ * with gru = 1 as lstm_oracle_forward_gru, where W, U are [D][3H], [H][3H],
+ * bias is b_ih [3H] and bhh is b_hh [3H])
  *   B, T, D, H   : batch, padded time extent, input width, hidden width (> 0)
  *   x            : [B][T][D] fp32
  *   L            : [B] int32 sequence lengths, each in [0, T]
@@ -110,7 +156,8 @@ static void lstm_cell_row(int D, int H, const float* xt, const float* W, const f
 static int forward_impl(int B, int T, int D, int H, const float* x, const int32_t* L,
                         const float* W, const float* U, const float* bias,
                         const double* h0, const double* c0, double* h_out, double* c_out,
-                        int literal, int nthreads, int64_t* steps_out, double* seq_out) {
+                        int literal, int nthreads, int64_t* steps_out, double* seq_out,
+                        int gru, const float* bhh) {
     if (B <= 0 || T < 0 || D <= 0 || H <= 0 || !x || !L || !W || !U || !bias || !h0 || !c0 ||
         !h_out || !c_out)
         return ORACLE_BAD_ARGS;
@@ -128,7 +175,7 @@ static int forward_impl(int B, int T, int D, int H, const float* x, const int32_
 #ifdef _OPENMP
     nt = nthreads > 0 ? nthreads : omp_get_max_threads();
 #endif
-    double* zs = (double*)malloc((size_t)nt * 4 * H * sizeof(double));
+    double* zs = (double*)malloc((size_t)nt * 6 * H * sizeof(double));  /* 4H (LSTM) or 2 x 3H (GRU) */
     if (!h || !c || !hn || !cn || !zs) {
         free(h); free(c); free(hn); free(cn); free(zs);
         return ORACLE_NOMEM;
@@ -149,10 +196,16 @@ static int forward_impl(int B, int T, int D, int H, const float* x, const int32_
 #ifdef _OPENMP
             tid = omp_get_thread_num();
 #endif
-            double* z = zs + (size_t)tid * 4 * H;
+            double* z = zs + (size_t)tid * 6 * H;
             const float* xt = x + ((size_t)b * T + t) * D;
-            lstm_cell_row(D, H, xt, W, U, bias, h + (size_t)b * H, c + (size_t)b * H, z,
-                          hn + (size_t)b * H, cn + (size_t)b * H);
+            if (gru) {
+                gru_cell_row(D, H, xt, W, U, bias, bhh, h + (size_t)b * H, z, z + 3 * H,
+                             hn + (size_t)b * H);
+                memcpy(cn + (size_t)b * H, c + (size_t)b * H, (size_t)H * sizeof(double));
+            } else {
+                lstm_cell_row(D, H, xt, W, U, bias, h + (size_t)b * H, c + (size_t)b * H, z,
+                              hn + (size_t)b * H, cn + (size_t)b * H);
+            }
         }
         /* Per-row select: rows with t < L[b] take the new state, the others
          * keep theirs.  Commits happen after every row of the step is done. */
@@ -177,7 +230,7 @@ int lstm_oracle_forward(int B, int T, int D, int H, const float* x, const int32_
                         const double* h0, const double* c0, double* h_out, double* c_out,
                         int literal, int nthreads, int64_t* steps_out) {
     return forward_impl(B, T, D, H, x, L, W, U, bias, h0, c0, h_out, c_out, literal, nthreads,
-                        steps_out, NULL);
+                        steps_out, NULL, 0, NULL);
 }
 
 /* As lstm_oracle_forward, and also the output sequence seq_out [B][T][H]. */
@@ -187,7 +240,18 @@ int lstm_oracle_forward_seq(int B, int T, int D, int H, const float* x, const in
                             int literal, int nthreads, int64_t* steps_out, double* seq_out) {
     if (!seq_out) return ORACLE_BAD_ARGS;
     return forward_impl(B, T, D, H, x, L, W, U, bias, h0, c0, h_out, c_out, literal, nthreads,
-                        steps_out, seq_out);
+                        steps_out, seq_out, 0, NULL);
+}
+
+/* The loop with the GRU cell: W [D][3H], U [H][3H], bih = b_ih [3H],
+ * bhh = b_hh [3H]; c0 is carried to c_out unchanged; seq_out may be NULL. */
+int lstm_oracle_forward_gru(int B, int T, int D, int H, const float* x, const int32_t* L,
+                            const float* W, const float* U, const float* bih, const float* bhh,
+                            const double* h0, const double* c0, double* h_out, double* c_out,
+                            int literal, int nthreads, int64_t* steps_out, double* seq_out) {
+    if (!bhh) return ORACLE_BAD_ARGS;
+    return forward_impl(B, T, D, H, x, L, W, U, bih, h0, c0, h_out, c_out, literal, nthreads,
+                        steps_out, seq_out, 1, bhh);
 }
 
 /* Number of OpenMP threads a call with nthreads <= 0 would use. */

@@ -321,3 +321,131 @@ PINS = [
     pin_seq_brute_force,
     pin_seq_torch_lstm,
 ]
+
+
+# ---------------------------------------------------------------------------
+# The loop with the GRU cell (gate blocks r, u, n; biases b_ih, b_hh).  Each
+# pin takes a callable with the signature of ``oracle.forward_gru``.
+
+def _gru_case(seed, B, D, H, T, lo=0):
+    inp = workloads.random_case(seed, B, D, H, T, lo=lo)
+    rng = np.random.default_rng(seed + 7)
+    W = (rng.standard_normal((D, 3 * H)) / math.sqrt(H)).astype(np.float32)
+    U = (rng.standard_normal((H, 3 * H)) / math.sqrt(H)).astype(np.float32)
+    bih = (rng.standard_normal(3 * H) * 0.5).astype(np.float32)
+    bhh = (rng.standard_normal(3 * H) * 0.5).astype(np.float32)
+    return inp.x.copy(), inp.lengths.copy(), W, U, bih, bhh, inp.h0.copy()
+
+
+def gpin_zero_weights_closed_form(fwd):
+    """W = U = 0 and zero biases: r = u = 1/2 and n = tanh(0) = 0, so each
+    step halves h: h_L = 2**-L h0, exactly."""
+    x, L, W, U, bih, bhh, h0 = _gru_case(40, 5, 4, 6, 8)
+    L[:] = [0, 1, 3, 8, 5]
+    W[:] = 0
+    U[:] = 0
+    bih[:] = 0
+    bhh[:] = 0
+    h = fwd(x, L, W, U, bih, bhh, h0)
+    assert _bits_equal(h, np.ldexp(h0.astype(np.float64), -L[:, None]))
+
+
+def gpin_constant_input_closed_form(fwd):
+    """U = 0 and x[b, t] constant per row: r, u and n are constant per row
+    (n = tanh(x W_n + b_in + r b_hn)), so h' = (1 - u) n + u h is affine with
+    h_L = u**L h0 + n (1 - u**L).  Every gate block and both biases of every
+    block take different values, so a swapped block, a reset gate applied to
+    the input part, or a misplaced bias changes the result."""
+    x, L, W, U, bih, bhh, h0 = _gru_case(41, 5, 3, 4, 9, lo=1)
+    L[:] = [9, 1, 4, 6, 2]
+    x[:] = x[:, :1, :]
+    U[:] = 0
+    H = 4
+    bih[:] = np.concatenate([np.full(H, 0.4), np.full(H, -0.3), np.full(H, 0.25)]).astype(np.float32)
+    bhh[:] = np.concatenate([np.full(H, -0.1), np.full(H, 0.6), np.full(H, -0.8)]).astype(np.float32)
+    h = fwd(x, L, W, U, bih, bhh, h0)
+    zx = x[:, 0, :].astype(np.float64) @ W.astype(np.float64) + bih.astype(np.float64)
+    zh = np.broadcast_to(bhh.astype(np.float64), zx.shape)
+    sig = lambda v: 1.0 / (1.0 + np.exp(-v))
+    r = sig(zx[:, :H] + zh[:, :H])
+    u = sig(zx[:, H:2 * H] + zh[:, H:2 * H])
+    n = np.tanh(zx[:, 2 * H:] + r * zh[:, 2 * H:])
+    uL = u ** L.astype(np.float64)[:, None]
+    want = uL * h0.astype(np.float64) + n * (1.0 - uL)
+    assert np.max(np.abs(h - want)) <= 1e-13
+
+
+def gpin_length_zero_and_poisoned_padding(fwd):
+    """A row of length 0 keeps h0 exactly, and NaN/Inf in x past each length
+    changes no bit of the result or of the output sequence."""
+    x, L, W, U, bih, bhh, h0 = _gru_case(42, 6, 5, 4, 9)
+    L[:] = [9, 0, 4, 1, 7, 0]
+    h1, s1 = fwd(x, L, W, U, bih, bhh, h0, return_seq=True)
+    for r in (1, 5):
+        assert _bits_equal(h1[r], h0[r].astype(np.float64))
+    xp = x.copy()
+    for r in range(len(L)):
+        xp[r, L[r]:, :] = np.nan
+        if L[r] + 1 < x.shape[1]:
+            xp[r, L[r] + 1, :] = np.inf
+    h2, s2 = fwd(xp, L, W, U, bih, bhh, h0, return_seq=True)
+    assert _bits_equal(h1, h2) and _bits_equal(s1, s2)
+
+
+def gpin_row_equals_own_run(fwd):
+    """Each row of a batch equals a batch of one holding that row alone."""
+    x, L, W, U, bih, bhh, h0 = _gru_case(43, 5, 4, 5, 7, lo=1)
+    h = fwd(x, L, W, U, bih, bhh, h0)
+    for r in range(len(L)):
+        hr = fwd(x[r:r + 1, :int(L[r])], L[r:r + 1], W, U, bih, bhh, h0[r:r + 1])
+        assert _bits_equal(hr[0], h[r])
+
+
+def gpin_brute_force(fwd, seeds=range(20)):
+    """Agreement (<= 1e-12) of h and of the output sequence with each sequence
+    run alone in pure Python."""
+    for s in seeds:
+        rng = np.random.default_rng(7000 + s)
+        B, D, H, T = (int(rng.integers(1, 5)), int(rng.integers(1, 4)), int(rng.integers(1, 4)),
+                      int(rng.integers(1, 7)))
+        x, L, W, U, bih, bhh, h0 = _gru_case(8000 + s, B, D, H, T)
+        h, seq = fwd(x, L, W, U, bih, bhh, h0, return_seq=True)
+        hb, sb = brute.gru_per_sequence(x, L, W.tolist(), U.tolist(), bih.tolist(), bhh.tolist(),
+                                        h0.tolist())
+        assert np.max(np.abs(h - np.array(hb))) <= 1e-12, (s, B, D, H, T)
+        assert np.max(np.abs(seq - np.array(sb))) <= 1e-12, (s, B, D, H, T)
+
+
+def gpin_torch_gru(fwd, shapes=((3, 4, 5, 6), (7, 12, 9, 10))):
+    """Agreement (<= 1e-12) with torch.nn.GRU in float64 on packed sequences:
+    torch's gate order is (r, z, n) with z the update gate, weight_ih = W^T,
+    weight_hh = U^T, bias_ih = b_ih, bias_hh = b_hh; the output sequence is
+    unpacked with zero padding."""
+    import torch
+    from torch.nn.utils.rnn import pack_padded_sequence, pad_packed_sequence
+    for k, (B, D, H, T) in enumerate(shapes):
+        x, L, W, U, bih, bhh, h0 = _gru_case(9000 + k, B, D, H, T, lo=1)
+        h, seq = fwd(x, L, W, U, bih, bhh, h0, return_seq=True)
+        m = torch.nn.GRU(D, H, batch_first=True).double()
+        with torch.no_grad():
+            m.weight_ih_l0.copy_(torch.from_numpy(W.astype(np.float64).T))
+            m.weight_hh_l0.copy_(torch.from_numpy(U.astype(np.float64).T))
+            m.bias_ih_l0.copy_(torch.from_numpy(bih.astype(np.float64)))
+            m.bias_hh_l0.copy_(torch.from_numpy(bhh.astype(np.float64)))
+            packed = pack_padded_sequence(torch.from_numpy(x.astype(np.float64)),
+                                          torch.from_numpy(L.astype(np.int64)),
+                                          batch_first=True, enforce_sorted=False)
+            out, hn = m(packed, torch.from_numpy(h0.astype(np.float64))[None])
+            out, _ = pad_packed_sequence(out, batch_first=True, total_length=T)
+        assert np.max(np.abs(h - hn[0].numpy())) <= 1e-12, (B, D, H, T)
+        assert np.max(np.abs(seq - out.numpy())) <= 1e-12, (B, D, H, T)
+
+
+GRU_PINS = [
+    gpin_zero_weights_closed_form,
+    gpin_constant_input_closed_form,
+    gpin_length_zero_and_poisoned_padding,
+    gpin_row_equals_own_run,
+    gpin_brute_force,
+    gpin_torch_gru,
+]

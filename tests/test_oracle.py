@@ -79,3 +79,8 @@ def test_golden_tiny_workload():
     want_h = np.array([[float.fromhex(v) for v in row] for row in rec["h"]])
     want_c = np.array([[float.fromhex(v) for v in row] for row in rec["c"]])
     assert np.array_equal(h, want_h) and np.array_equal(c, want_c)
+
+
+@pytest.mark.parametrize("pin", oracle_pins.GRU_PINS, ids=lambda f: f.__name__)
+def test_gru_pin(pin):
+    pin(oracle.forward_gru)

@@ -55,3 +55,36 @@ def test_pins_catch_planted_mistake(name, tmp_path):
             caught.append(pin.__name__)
             break
     assert caught, f"no pin caught mutant {name}"
+
+
+GRU_MUTANTS = {
+    "gru_reset_on_input_part": ("const double ng = tanh(zx[2 * H + v] + rg * zh[2 * H + v]);",
+                                "const double ng = tanh(rg * zx[2 * H + v] + zh[2 * H + v]);"),
+    "gru_update_swapped": ("hn[v] = (1.0 - ug) * ng + ug * h[v];", "hn[v] = ug * ng + (1.0 - ug) * h[v];"),
+    "gru_gates_swapped": ("const double rg = sig(zx[v] + zh[v]);\n        const double ug = sig(zx[H + v] + zh[H + v]);",
+                          "const double rg = sig(zx[H + v] + zh[H + v]);\n        const double ug = sig(zx[v] + zh[v]);"),
+    "gru_hidden_bias_outside_reset": ("zh[j] += (double)bhh[j];", "zx[j] += (double)bhh[j];"),
+    "gru_no_recurrent_term": ("for (int j = 0; j < G; ++j) zh[j] += hk * (double)uk[j];",
+                              "for (int j = 0; j < G; ++j) (void)(hk + uk[j]);"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(GRU_MUTANTS))
+def test_gru_pins_catch_planted_mistake(name, tmp_path):
+    old, new = GRU_MUTANTS[name]
+    src = oracle.source_text()
+    assert src.count(old) == 1, f"mutation anchor for {name} not found exactly once"
+    lib = oracle.compile_variant(src.replace(old, new), str(tmp_path / f"mut_{name}.so"))
+    low = oracle._Lib(lib)
+
+    def fwd(*args, **kw):
+        return oracle.forward_gru(*args, _lib_override=low, **kw)
+    caught = []
+    for pin in oracle_pins.GRU_PINS:
+        try:
+            with np.errstate(all="ignore"):
+                pin(fwd)
+        except (AssertionError, oracle.OracleError):
+            caught.append(pin.__name__)
+            break
+    assert caught, f"no pin caught mutant {name}"
