@@ -61,6 +61,20 @@ enum { LSTM_DYN_F32 = 0, LSTM_DYN_BF16 = 1 };
  *   synchronisation), then the host issues two kernel launches per step. */
 enum { LSTM_DYN_PERSISTENT = 0, LSTM_DYN_PER_STEP = 1 };
 
+/* Recurrent cell run by the loop (lstm_dyn_create_cell).
+ * LSTM: the cell above (the default of lstm_dyn_create).
+ * GRU:  the gated recurrent unit, the other common cell the paper's RNN loop
+ *   (Section 9 "RNN cells") can run; gate blocks (r, u, n) along 3H and two
+ *   bias vectors, b = [b_ih (3H) ++ b_hh (3H)]:
+ *       a = x[b, t] W + b_ih,   e = h U + b_hh
+ *       r = sigmoid(a_r + e_r),  u = sigmoid(a_u + e_u)
+ *       n = tanh(a_n + r * e_n)
+ *       h' = (1 - u) * n + u * h
+ *   Layouts: W [D][3H], U [H][3H] (element type = dtype), b [6H] fp32.
+ *   There is no cell state: c0 is ignored (may be NULL) and out_c is written
+ *   with zeros. */
+enum { LSTM_DYN_CELL_LSTM = 0, LSTM_DYN_CELL_GRU = 1 };
+
 /* Status codes. */
 enum {
     LSTM_DYN_OK = 0,
@@ -81,7 +95,8 @@ enum {
     LSTM_DYN_Q_WORKSPACE_BYTES = 4,    /* device workspace owned by the handle */
     LSTM_DYN_Q_TOTAL_ROWS = 5,         /* sum of the (clamped) lengths of the last forward (synchronises) */
     LSTM_DYN_Q_TIME_PREP_NS = 6,       /* with LSTM_DYN_OPT_TIMING: device time of the length
-                                          preparation kernel in the last forward (synchronises) */
+                                          preparation kernel (and, for a GRU handle, the weight
+                                          repacking) in the last forward (synchronises) */
     LSTM_DYN_Q_TIME_INPROJ_NS = 7,     /* ... of the input projection GEMM */
     LSTM_DYN_Q_TIME_LOOP_NS = 8        /* ... of the time loop (the persistent kernel, or the
                                           per-step path's host loop of launches) */
@@ -120,6 +135,17 @@ typedef struct {
  * ERR_UNSUPPORTED (sizes the compiled kernel variants do not cover), ERR_HIP, ERR_NOMEM.
  */
 int lstm_dyn_create(lstm_dyn_t** out, int B, int D, int H, int T_max, int dtype, int mode);
+
+/*
+ * lstm_dyn_create_cell: lstm_dyn_create for the cell `cell` (LSTM_DYN_CELL_*).
+ * A GRU handle takes the GRU layouts above in lstm_dyn_forward and
+ * lstm_dyn_forward_seq; its forward first repacks W, U and b into the
+ * handle's workspace (one more kernel launch), so the loop kernels see the
+ * LSTM's four-column layout.  Returns as lstm_dyn_create; an unknown cell is
+ * ERR_INVALID.
+ */
+int lstm_dyn_create_cell(lstm_dyn_t** out, int B, int D, int H, int T_max, int dtype, int mode,
+                         int cell);
 
 /*
  * lstm_dyn_forward: enqueue one forward of the loop on `stream`.
@@ -199,6 +225,14 @@ int lstm_dyn_check_seq_args(int B, int D, int H, int T_max, int dtype, const voi
                             const int32_t* lengths, const void* W, const void* U, const float* b,
                             const float* h0, const float* c0, const float* out_h,
                             const float* out_c, const float* out_seq);
+
+/* The checks of lstm_dyn_forward (out_seq NULL) or lstm_dyn_forward_seq
+ * (out_seq not NULL) for a handle of cell `cell`, with that cell's sizes of
+ * W, U and b.  Returns LSTM_DYN_OK or ERR_INVALID. */
+int lstm_dyn_check_cell_args(int B, int D, int H, int T_max, int dtype, int cell, const void* x,
+                             const int32_t* lengths, const void* W, const void* U, const float* b,
+                             const float* h0, const float* c0, const float* out_h,
+                             const float* out_c, const float* out_seq);
 
 #ifdef __cplusplus
 }

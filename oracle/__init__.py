@@ -209,3 +209,15 @@ def forward_inputs(inp, rows=None, literal: bool = False, threads: int = 0, seq:
         rows = np.asarray(rows, dtype=np.int64)
         x, L, h0, c0 = x[rows], L[rows], h0[rows], c0[rows]
     return forward(x, L, W, U, inp.b, h0, c0, literal=literal, threads=threads, return_seq=seq)
+
+
+def forward_gru_inputs(inp, rows=None, literal: bool = False, threads: int = 0, seq: bool = False):
+    """``forward_gru`` on a ``workloads.GruInputs`` batch, optionally on a
+    subset of rows (rows are independent, as for ``forward_inputs``)."""
+    x, W, U = inp.as_f32()
+    L, h0 = inp.lengths, inp.h0
+    if rows is not None:
+        rows = np.asarray(rows, dtype=np.int64)
+        x, L, h0 = x[rows], L[rows], h0[rows]
+    return forward_gru(x, L, W, U, inp.b_ih, inp.b_hh, h0, literal=literal, threads=threads,
+                       return_seq=seq)

@@ -19,6 +19,7 @@ __all__ = [
     "lstm_dyn_create", "lstm_dyn_forward", "lstm_dyn_destroy", "lstm_dyn_query",
     "lstm_dyn_strerror", "lstm_dyn_plan", "lstm_dyn_check_args", "lstm_dyn_set_option",
     "lstm_dyn_step_trace", "lstm_dyn_forward_seq", "lstm_dyn_check_seq_args",
+    "lstm_dyn_create_cell", "lstm_dyn_check_cell_args", "CELL_LSTM", "CELL_GRU",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -26,6 +27,7 @@ _LIB_PATH = os.path.join(_HERE, "liblstm_dyn.so")
 
 F32, BF16 = 0, 1
 PERSISTENT, PER_STEP = 0, 1
+CELL_LSTM, CELL_GRU = 0, 1
 OK, ERR_INVALID, ERR_HIP, ERR_NOMEM, ERR_UNSUPPORTED, ERR_BAD_LENGTHS, ERR_TIMEOUT = range(7)
 Q_LAST_STATUS, Q_STEPS_EXECUTED, Q_LAUNCHES_PER_FORWARD, Q_GROUPS, Q_WORKSPACE_BYTES, \
     Q_TOTAL_ROWS, Q_TIME_PREP_NS, Q_TIME_INPROJ_NS, Q_TIME_LOOP_NS = range(9)
@@ -33,6 +35,7 @@ OPT_TIMING, OPT_STEP_TRACE = 0, 1
 
 _DTYPES = {"f32": F32, "fp32": F32, "float32": F32, "bf16": BF16, "bfloat16": BF16}
 _MODES = {"persistent": PERSISTENT, "per_step": PER_STEP}
+_CELLS = {"lstm": CELL_LSTM, "gru": CELL_GRU}
 
 
 class LstmDynError(RuntimeError):
@@ -67,6 +70,10 @@ def _load():
     P, I, LL = ctypes.c_void_p, ctypes.c_int, ctypes.c_longlong
     lib.lstm_dyn_create.argtypes = [ctypes.POINTER(P), I, I, I, I, I, I]
     lib.lstm_dyn_create.restype = I
+    lib.lstm_dyn_create_cell.argtypes = [ctypes.POINTER(P), I, I, I, I, I, I, I]
+    lib.lstm_dyn_create_cell.restype = I
+    lib.lstm_dyn_check_cell_args.argtypes = [I] * 6 + [P] * 10
+    lib.lstm_dyn_check_cell_args.restype = I
     lib.lstm_dyn_forward.argtypes = [P] * 11
     lib.lstm_dyn_forward.restype = I
     lib.lstm_dyn_forward_seq.argtypes = [P] * 12
@@ -102,6 +109,15 @@ def lstm_dyn_create(B: int, D: int, H: int, T_max: int, dtype: int, mode: int) -
     rc = _load().lstm_dyn_create(ctypes.byref(h), B, D, H, T_max, dtype, mode)
     if rc != OK:
         raise LstmDynError(rc, "lstm_dyn_create")
+    return h.value
+
+
+def lstm_dyn_create_cell(B: int, D: int, H: int, T_max: int, dtype: int, mode: int,
+                         cell: int) -> int:
+    h = ctypes.c_void_p()
+    rc = _load().lstm_dyn_create_cell(ctypes.byref(h), B, D, H, T_max, dtype, mode, cell)
+    if rc != OK:
+        raise LstmDynError(rc, "lstm_dyn_create_cell")
     return h.value
 
 
@@ -174,22 +190,33 @@ def lstm_dyn_check_seq_args(B: int, D: int, H: int, T_max: int, dtype: int, x: i
                                            out_h, out_c, out_seq)
 
 
+def lstm_dyn_check_cell_args(B: int, D: int, H: int, T_max: int, dtype: int, cell: int, x: int,
+                             lengths: int, W: int, U: int, b: int, h0: int, c0: int, out_h: int,
+                             out_c: int, out_seq: int) -> int:
+    return _load().lstm_dyn_check_cell_args(B, D, H, T_max, dtype, cell, x, lengths, W, U, b,
+                                            h0, c0, out_h, out_c, out_seq)
+
+
 # --- torch convenience wrapper ---------------------------------------------
 
 class LstmDyn:
-    """One handle of the library for fixed (B, D, H, T_max, dtype, mode).
+    """One handle of the library for fixed (B, D, H, T_max, dtype, mode, cell).
 
     ``forward`` takes CUDA (HIP) tensors in the layouts of the C ABI:
-    x [B, T_max, D] and W [D, 4H], U [H, 4H] in the handle's dtype
-    (torch.float32 or torch.bfloat16), lengths int32 [B], b float32 [4H],
+    x [B, T_max, D] and W [D, G], U [H, G] in the handle's dtype
+    (torch.float32 or torch.bfloat16), lengths int32 [B], b float32,
     h0/c0 float32 [B, H]; it returns (out_h, out_c) float32 [B, H].
+    LSTM: G = 4H, b [4H].  GRU: G = 3H, b [6H] = b_ih ++ b_hh, c0 is
+    ignored (may be None) and out_c is zeros.
     """
 
-    def __init__(self, B: int, D: int, H: int, T_max: int, dtype="bf16", mode="persistent"):
+    def __init__(self, B: int, D: int, H: int, T_max: int, dtype="bf16", mode="persistent",
+                 cell="lstm"):
         self.B, self.D, self.H, self.T = B, D, H, T_max
         self.dtype = _DTYPES[dtype] if isinstance(dtype, str) else int(dtype)
         self.mode = _MODES[mode] if isinstance(mode, str) else int(mode)
-        self.handle = lstm_dyn_create(B, D, H, T_max, self.dtype, self.mode)
+        self.cell = _CELLS[cell] if isinstance(cell, str) else int(cell)
+        self.handle = lstm_dyn_create_cell(B, D, H, T_max, self.dtype, self.mode, self.cell)
 
     def _check(self, name, t, dtype, shape):
         import torch
@@ -202,17 +229,20 @@ class LstmDyn:
         if not t.is_contiguous():
             raise ValueError(f"{name} must be contiguous")
 
-    def forward(self, x, lengths, W, U, b, h0, c0, out_h=None, out_c=None, stream=None):
+    def _inputs(self, x, lengths, W, U, b, h0, c0, out_h, out_c, stream):
+        """Check the inputs, allocate missing outputs; returns (c0 pointer,
+        out_h, out_c, stream handle)."""
         import torch
         B, D, H, T = self.B, self.D, self.H, self.T
         et = torch.bfloat16 if self.dtype == BF16 else torch.float32
-        self._check("x", x, et, (B, T, D))
-        self._check("lengths", lengths, torch.int32, (B,))
-        self._check("W", W, et, (D, 4 * H))
-        self._check("U", U, et, (H, 4 * H))
-        self._check("b", b, torch.float32, (4 * H,))
-        self._check("h0", h0, torch.float32, (B, H))
-        self._check("c0", c0, torch.float32, (B, H))
+        G, nb = (3 * H, 6 * H) if self.cell == CELL_GRU else (4 * H, 4 * H)
+        for name, t, dt, shape in (("x", x, et, (B, T, D)), ("lengths", lengths, torch.int32, (B,)),
+                                   ("W", W, et, (D, G)), ("U", U, et, (H, G)),
+                                   ("b", b, torch.float32, (nb,)),
+                                   ("h0", h0, torch.float32, (B, H))):
+            self._check(name, t, dt, shape)
+        if c0 is not None or self.cell != CELL_GRU:
+            self._check("c0", c0, torch.float32, (B, H))
         if out_h is None:
             out_h = torch.empty((B, H), dtype=torch.float32, device=x.device)
         if out_c is None:
@@ -222,41 +252,29 @@ class LstmDyn:
         if stream is None:
             stream = torch.cuda.current_stream(x.device)
         s = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+        return (c0.data_ptr() if c0 is not None else 0), out_h, out_c, s
+
+    def forward(self, x, lengths, W, U, b, h0, c0=None, out_h=None, out_c=None, stream=None):
+        c0p, out_h, out_c, s = self._inputs(x, lengths, W, U, b, h0, c0, out_h, out_c, stream)
         lstm_dyn_forward(self.handle, x.data_ptr(), lengths.data_ptr(), W.data_ptr(),
-                         U.data_ptr(), b.data_ptr(), h0.data_ptr(), c0.data_ptr(),
+                         U.data_ptr(), b.data_ptr(), h0.data_ptr(), c0p,
                          out_h.data_ptr(), out_c.data_ptr(), s)
         return out_h, out_c
 
     __call__ = forward
 
-    def forward_seq(self, x, lengths, W, U, b, h0, c0, out_h=None, out_c=None, out_seq=None,
+    def forward_seq(self, x, lengths, W, U, b, h0, c0=None, out_h=None, out_c=None, out_seq=None,
                     stream=None):
         """``forward``, and also the output sequence out_seq float32 [B, T_max, H]:
         the hidden state of row b after step t for t < L[b], zero after.
         Returns (out_h, out_c, out_seq)."""
         import torch
-        B, D, H, T = self.B, self.D, self.H, self.T
-        et = torch.bfloat16 if self.dtype == BF16 else torch.float32
-        for name, t, dt, shape in (("x", x, et, (B, T, D)), ("lengths", lengths, torch.int32, (B,)),
-                                   ("W", W, et, (D, 4 * H)), ("U", U, et, (H, 4 * H)),
-                                   ("b", b, torch.float32, (4 * H,)),
-                                   ("h0", h0, torch.float32, (B, H)),
-                                   ("c0", c0, torch.float32, (B, H))):
-            self._check(name, t, dt, shape)
-        if out_h is None:
-            out_h = torch.empty((B, H), dtype=torch.float32, device=x.device)
-        if out_c is None:
-            out_c = torch.empty((B, H), dtype=torch.float32, device=x.device)
+        c0p, out_h, out_c, s = self._inputs(x, lengths, W, U, b, h0, c0, out_h, out_c, stream)
         if out_seq is None:
-            out_seq = torch.empty((B, T, H), dtype=torch.float32, device=x.device)
-        self._check("out_h", out_h, torch.float32, (B, H))
-        self._check("out_c", out_c, torch.float32, (B, H))
-        self._check("out_seq", out_seq, torch.float32, (B, T, H))
-        if stream is None:
-            stream = torch.cuda.current_stream(x.device)
-        s = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+            out_seq = torch.empty((self.B, self.T, self.H), dtype=torch.float32, device=x.device)
+        self._check("out_seq", out_seq, torch.float32, (self.B, self.T, self.H))
         lstm_dyn_forward_seq(self.handle, x.data_ptr(), lengths.data_ptr(), W.data_ptr(),
-                             U.data_ptr(), b.data_ptr(), h0.data_ptr(), c0.data_ptr(),
+                             U.data_ptr(), b.data_ptr(), h0.data_ptr(), c0p,
                              out_h.data_ptr(), out_c.data_ptr(), out_seq.data_ptr(), s)
         return out_h, out_c, out_seq
 

@@ -78,6 +78,18 @@ __device__ inline float tanh_f(float z) {
     return copysignf((1.0f - e) * rcp_f(1.0f + e), z);
 }
 
+// The GRU cell (gate blocks r, u, n) in the four columns of a unit: the loop's
+// weights are packed so that the pre-activations hold
+//   z[0] = r, z[1] = u (input and recurrent parts and both biases),
+//   z[2] = h U_n + b_hn (the recurrent part of n), z[3] = x W_n + b_in;
+// then n = tanh(z[3] + r z[2]) and h' = (1 - u) n + u h.  No cell state.
+__device__ inline void gru_cell(f32x4_t z, float& h) {
+    const float rg = sigmoid_f(z[0]);
+    const float ug = sigmoid_f(z[1]);
+    const float ng = tanh_f(z[3] + rg * z[2]);
+    h = (1.0f - ug) * ng + ug * h;
+}
+
 // One LSTM cell update from the four pre-activations of a (row, unit).
 __device__ inline void lstm_cell(f32x4_t z, float& c, float& h) {
     const float ig = sigmoid_f(z[0]);

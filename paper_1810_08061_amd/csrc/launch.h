@@ -27,7 +27,15 @@ struct Dims {
     int B, D, H, T;     // batch, input width, hidden width, padded time extent
     int bf16;           // 1: x, W, U are bf16; 0: fp32
     int hpad, bpad;     // padded hidden width / batch rows of the operand buffer
+    int gru;            // 1: GRU cell (weights packed to four columns per unit), 0: LSTM
 };
+
+// GRU: the caller's W [D][3H], U [H][3H] (gate blocks r, u, n) and biases
+// b_ih, b_hh [3H] (b [6H]) packed into the four-column layout of the LSTM
+// path: W4 [D][4H] = (W_r, W_u, 0, W_n), U4 [H][4H] = (U_r, U_u, U_n, 0),
+// b4 [4H] = (b_ir + b_hr, b_iu + b_hu, b_hn, b_in).
+hipError_t launch_gru_pack(const Dims& d, const void* W, const void* U, const float* b, void* W4,
+                           void* U4, float* b4, hipStream_t s);
 
 // Preparation: clamp and validate lengths, stable descending length sort,
 // per-step active counts and compact row offsets, compact row sources.

@@ -52,6 +52,7 @@ struct PersistParams {
     unsigned long long timeout_ticks;
     unsigned long long* trace;  // [T + 1][4] timestamps from workgroup 0, or null
     int seq;                    // 1: also keep each step's h (fp32) for the output sequence
+    int gru;                    // 1: GRU cell (no cell state), 0: LSTM
 };
 
 // Logical workgroup index: consecutive workgroups are dispatched to different
@@ -339,7 +340,7 @@ persistent_kernel(PersistParams p) {
             if (nt < ntmax && s < B && u < H) {
                 const size_t ib = (size_t)p.perm[s] * H + u;
                 hst[i] = p.h0[ib];  // read before the final write: exact aliasing out_h == h0 is allowed
-                cst[i] = p.c0[ib];
+                if (!p.gru) cst[i] = p.c0[ib];
             }
             hstage[w][(l & 15) * UPW + mt * 4 + (l >> 4)] = IO::operand(hst[i]);
         }
@@ -620,8 +621,9 @@ persistent_kernel(PersistParams p) {
                         const int s = (j + ntc0) * 16 + (lo & 15);
                         const bool live = s < act;
                         nan |= live & ((z[0] != z[0]) | (z[1] != z[1]) | (z[2] != z[2]) | (z[3] != z[3]));
-                        float c = cst[i], h;
-                        lstm_cell(z, c, h);
+                        float c = cst[i], h = hst[i];
+                        if (p.gru) gru_cell(z, h);
+                        else lstm_cell(z, c, h);
                         cn[i] = c;
                         hn[i] = h;
                     }
@@ -807,6 +809,7 @@ hipError_t launch_persistent(const Dims& d, const PersistentConfig& pc, const vo
     p.timeout_ticks = pc.timeout_ticks;
     p.trace = pc.trace;
     p.seq = pc.seq;
+    p.gru = d.gru;
     void* args[] = {&p};
     return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(f), dim3(pc.groups),
                                       dim3(pc.kw * 64), args, (unsigned)pc.lds_bytes, s);

@@ -29,6 +29,7 @@ struct SmallParams {
     float* seq;  // [B][T][H] output sequence (valid steps only), or null
     Meta* meta;
     int B, D, H, T;
+    int gru;  // 1: GRU cell, 0: LSTM
 };
 
 template <typename E, int KD, int KH, int NT>
@@ -119,7 +120,7 @@ small_kernel(SmallParams p) {
             const int n = nt * 16 + (l & 15);
             const int u = ((w * SM_MT + mt) * 16 + 4 * (l >> 4)) >> 2;
             const bool ok = n < B && u < H;
-            cst[mt][nt] = ok ? p.c0[(size_t)n * H + u] : 0.0f;
+            cst[mt][nt] = ok && !p.gru ? p.c0[(size_t)n * H + u] : 0.0f;
             hst[mt][nt] = ok ? p.h0[(size_t)n * H + u] : 0.0f;
         }
     __syncthreads();
@@ -182,8 +183,9 @@ small_kernel(SmallParams p) {
                     f32x4_t z = acc[mt][nt];
 #pragma unroll
                     for (int g = 0; g < 4; ++g) z[g] += bias[mt][g];
-                    float c = cst[mt][nt], h;
-                    lstm_cell(z, c, h);
+                    float c = cst[mt][nt], h = hst[mt][nt];
+                    if (p.gru) gru_cell(z, h);
+                    else lstm_cell(z, c, h);
                     cst[mt][nt] = c;
                     hst[mt][nt] = h;
                     if (p.seq) p.seq[((size_t)n * T + t) * H + u] = h;  // output at step t
@@ -254,7 +256,7 @@ hipError_t launch_small(const Dims& d, int kd, int nt, const void* x, const int3
     for (const SmallVariant& v : kSmall)
         if (v.bf16 == d.bf16 && v.kd == kd && v.nt == nt) f = v.f;
     if (!f) return hipErrorInvalidValue;
-    SmallParams p{x, lengths, W, U, b, h0, c0, out_h, out_c, seq, ws.meta, d.B, d.D, d.H, d.T};
+    SmallParams p{x, lengths, W, U, b, h0, c0, out_h, out_c, seq, ws.meta, d.B, d.D, d.H, d.T, d.gru};
     hipLaunchKernelGGL(f, dim3(1), dim3(SM_THREADS), 0, s, p);
     return hipGetLastError();
 }

@@ -136,3 +136,49 @@ def test_check_seq_args():
     q = list(p)
     q[0] = 0                                     # the plain checks still apply
     assert ld.lstm_dyn_check_seq_args(B, D, H, T, ld.F32, *q, seq) == ld.ERR_INVALID
+
+
+def _gru_ptrs(B, D, H, T, e):
+    """Disjoint fake addresses with the GRU's sizes (W, U with 3H columns, b 6H)."""
+    sizes = [B * T * D * e, 4 * B, D * 3 * H * e, H * 3 * H * e, 24 * H, 4 * B * H, 4 * B * H,
+             4 * B * H, 4 * B * H, 4 * B * T * H]
+    out, at = [], 1 << 20
+    for s in sizes:
+        out.append(at)
+        at += (s + 255) // 256 * 256 + 256
+    return out
+
+
+def test_check_cell_args_gru():
+    B, D, H, T = 3, 5, 7, 4
+    *p, seq = _gru_ptrs(B, D, H, T, 2)
+    chk = ld.lstm_dyn_check_cell_args
+    assert chk(B, D, H, T, ld.BF16, ld.CELL_GRU, *p, 0) == ld.OK
+    assert chk(B, D, H, T, ld.BF16, ld.CELL_GRU, *p, seq) == ld.OK
+    assert chk(B, D, H, T, ld.BF16, 2, *p, 0) == ld.ERR_INVALID          # unknown cell
+    q = list(p)
+    q[6] = 0                                      # c0 is ignored by the GRU and may be NULL
+    assert chk(B, D, H, T, ld.BF16, ld.CELL_GRU, *q, seq) == ld.OK
+    assert chk(B, D, H, T, ld.BF16, ld.CELL_LSTM, *q, 0) == ld.ERR_INVALID
+    q = list(p)
+    q[7] = q[6]                                   # out_h may sit on the ignored c0
+    assert chk(B, D, H, T, ld.BF16, ld.CELL_GRU, *q, 0) == ld.OK
+    for i in (0, 1, 2, 3, 4, 5):                  # but not on a real input
+        q = list(p)
+        q[7] = q[i] + (4 if i != 5 else 4)
+        assert chk(B, D, H, T, ld.BF16, ld.CELL_GRU, *q, 0) == ld.ERR_INVALID, i
+    # the bias is 6H floats (24H bytes): an output 20H bytes past its start overlaps it
+    q = list(p)
+    q[8] = q[4] + 20 * H
+    assert chk(B, D, H, T, ld.BF16, ld.CELL_GRU, *q, 0) == ld.ERR_INVALID
+    assert chk(B, D, H, T, ld.BF16, ld.CELL_LSTM, *q, 0) == ld.OK        # LSTM bias is 4H
+    for i in range(9):                            # out_seq on top of any used argument
+        if i == 6:
+            continue
+        assert chk(B, D, H, T, ld.BF16, ld.CELL_GRU, *p, p[i]) == ld.ERR_INVALID, i
+
+
+def test_create_cell_rejects_unknown_cell_without_device():
+    with pytest.raises(ld.LstmDynError) as e:
+        ld.lstm_dyn_create_cell(4, 4, 4, 4, ld.F32, ld.PERSISTENT, 7)
+    assert e.value.code == ld.ERR_INVALID

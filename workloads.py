@@ -161,6 +161,77 @@ def make_inputs(B: int, D: int, H: int, T: int, dtype: str, lengths_spec: tuple,
     return Inputs(x=x, lengths=L, W=W, U=U, b=b, h0=h0, c0=c0, dtype=dtype)
 
 
+@dataclass
+class GruInputs:
+    """One batch for the GRU cell in the boundary's layouts (C-contiguous).
+
+    x [B, T, D], W [D, 3H], U [H, 3H]: float32, or uint16 bf16 bits, gate
+    blocks (r, u, n) along 3H.  lengths int32 [B]; b float32 [6H] =
+    b_ih [3H] followed by b_hh [3H]; h0 float32 [B, H].
+    """
+    x: np.ndarray
+    lengths: np.ndarray
+    W: np.ndarray
+    U: np.ndarray
+    b: np.ndarray
+    h0: np.ndarray
+    dtype: str
+
+    B = Inputs.B
+    T = Inputs.T
+    D = Inputs.D
+    H = Inputs.H
+    as_f32 = Inputs.as_f32
+
+    @property
+    def b_ih(self):
+        return self.b[:3 * self.H]
+
+    @property
+    def b_hh(self):
+        return self.b[3 * self.H:]
+
+
+def make_gru_inputs(B: int, D: int, H: int, T: int, dtype: str, lengths_spec: tuple,
+                    seed: int, force: Optional[tuple] = None, state_var: float = 0.0,
+                    bias_var: float = 0.1) -> GruInputs:
+    """GRU batch.  Draw order: lengths, x, W, U, b_ih, b_hh, h0 (h0 only when
+    ``state_var`` > 0); W, U ~ N(0, 1/H), biases ~ N(0, bias_var)."""
+    rng = np.random.default_rng(seed)
+    L = draw_lengths(rng, B, lengths_spec)
+    x = rng.standard_normal((B, T, D)).astype(np.float32)
+    W = (rng.standard_normal((D, 3 * H)) * (1.0 / np.sqrt(H))).astype(np.float32)
+    U = (rng.standard_normal((H, 3 * H)) * (1.0 / np.sqrt(H))).astype(np.float32)
+    b = (rng.standard_normal(6 * H) * np.sqrt(bias_var)).astype(np.float32)
+    if state_var > 0:
+        h0 = (rng.standard_normal((B, H)) * np.sqrt(state_var)).astype(np.float32)
+    else:
+        h0 = np.zeros((B, H), np.float32)
+    if force is not None:
+        L[force[0]] = force[1]
+    if dtype == BF16:
+        x, W, U = f32_to_bf16_bits(x), f32_to_bf16_bits(W), f32_to_bf16_bits(U)
+    elif dtype != F32:
+        raise ValueError(f"unknown dtype {dtype!r}")
+    return GruInputs(x=x, lengths=L, W=W, U=U, b=b, h0=h0, dtype=dtype)
+
+
+def gru_workload_inputs(name: str) -> GruInputs:
+    """The GRU batch of workload ``name``: its shapes, dtype and state
+    distribution with GRU weights; the same seed, so the lengths and x are
+    those of the LSTM batch."""
+    w = WORKLOADS[name]
+    return make_gru_inputs(w.B, w.D, w.H, w.T, w.dtype, w.lengths, w.seed, w.force,
+                           w.state_var)
+
+
+def random_gru_case(seed: int, B: int, D: int, H: int, T: int, dtype: str = F32,
+                    lo: int = 0, hi: Optional[int] = None, state_var: float = 0.1) -> GruInputs:
+    """A small seeded GRU case with uniform lengths in [lo, hi] (hi defaults to T)."""
+    return make_gru_inputs(B, D, H, T, dtype, ("uniform", lo, T if hi is None else hi), seed,
+                           state_var=state_var)
+
+
 def workload_inputs(name: str) -> Inputs:
     w = WORKLOADS[name]
     return make_inputs(w.B, w.D, w.H, w.T, w.dtype, w.lengths, w.seed, w.force, w.state_var)
