@@ -13,6 +13,10 @@ Two independent implementations live here:
 * ``brute.forward_per_sequence`` -- pure-Python ``math`` loops that run each
   sequence on its own up to its own length, with no masking and no loop bound:
   a brute-force cross-check for tiny cases.
+
+The same loop with the GRU cell (``forward_gru``) and the tanh RNN cell
+(``forward_rnn``) is there too: the paper's loop takes the cell as a
+parameter.
 """
 from __future__ import annotations
 
@@ -65,6 +69,9 @@ class _Lib:
         lib.lstm_oracle_forward_gru.argtypes = [ctypes.c_int] * 4 + [P] * 10 + [
             ctypes.c_int, ctypes.c_int, P, P]
         lib.lstm_oracle_forward_gru.restype = ctypes.c_int
+        lib.lstm_oracle_forward_rnn.argtypes = [ctypes.c_int] * 4 + [P] * 9 + [
+            ctypes.c_int, ctypes.c_int, P, P]
+        lib.lstm_oracle_forward_rnn.restype = ctypes.c_int
         lib.lstm_oracle_max_threads.argtypes = []
         lib.lstm_oracle_max_threads.restype = ctypes.c_int
         self.lib = lib
@@ -197,6 +204,45 @@ def forward_gru(x, lengths, W, U, b_ih, b_hh, h0, literal: bool = False, threads
     return out[0] if len(out) == 1 else out
 
 
+def forward_rnn(x, lengths, W, U, b, h0, literal: bool = False, threads: int = 0,
+                return_seq: bool = False, return_steps: bool = False, _lib_override=None):
+    """Final hidden state h in float64 of the masked loop with the tanh RNN
+    cell h' = tanh(x W + h U + b).
+
+    x [B, T, D], W [D, H], U [H, H], b [H]: fp32 values; h0 [B, H] fp32 or
+    fp64; lengths as for ``forward``.  With ``return_seq`` also the output
+    sequence [B, T, H] (zeros past each length).
+    """
+    lib = (_lib_override or _load()).lib
+    x, W, U, b = map(_f32, (x, W, U, b))
+    h0 = np.ascontiguousarray(h0, dtype=np.float64)
+    L = np.ascontiguousarray(lengths, dtype=np.int32)
+    B, T, D = x.shape
+    H = U.shape[0]
+    if W.shape != (D, H) or U.shape != (H, H) or b.shape != (H,):
+        raise OracleError("RNN weight shapes do not match x and U")
+    if L.shape != (B,) or h0.shape != (B, H):
+        raise OracleError("lengths/state shapes do not match x")
+    c0 = np.zeros((B, H), np.float64)
+    h = np.empty((B, H), np.float64)
+    c = np.empty((B, H), np.float64)
+    seq = np.full((B, T, H), np.nan) if return_seq else None
+    steps = ctypes.c_int64(0)
+    rc = lib.lstm_oracle_forward_rnn(B, T, D, H, x.ctypes.data, L.ctypes.data, W.ctypes.data,
+                                     U.ctypes.data, b.ctypes.data, h0.ctypes.data, c0.ctypes.data,
+                                     h.ctypes.data, c.ctypes.data, int(bool(literal)), int(threads),
+                                     ctypes.byref(steps),
+                                     seq.ctypes.data if seq is not None else None)
+    if rc == BAD_LENGTHS:
+        raise OracleError("sequence lengths must lie in [0, T]")
+    if rc != OK:
+        raise OracleError(f"oracle failed with code {rc}")
+    out = (h,) if seq is None else (h, seq)
+    if return_steps:
+        out = (*out, int(steps.value))
+    return out[0] if len(out) == 1 else out
+
+
 def forward_inputs(inp, rows=None, literal: bool = False, threads: int = 0, seq: bool = False):
     """``forward`` on a ``workloads.Inputs`` batch, optionally on a subset of rows.
 
@@ -221,3 +267,14 @@ def forward_gru_inputs(inp, rows=None, literal: bool = False, threads: int = 0, 
         x, L, h0 = x[rows], L[rows], h0[rows]
     return forward_gru(x, L, W, U, inp.b_ih, inp.b_hh, h0, literal=literal, threads=threads,
                        return_seq=seq)
+
+
+def forward_rnn_inputs(inp, rows=None, literal: bool = False, threads: int = 0, seq: bool = False):
+    """``forward_rnn`` on a ``workloads.CellInputs`` batch of the RNN cell,
+    optionally on a subset of rows."""
+    x, W, U = inp.as_f32()
+    L, h0 = inp.lengths, inp.h0
+    if rows is not None:
+        rows = np.asarray(rows, dtype=np.int64)
+        x, L, h0 = x[rows], L[rows], h0[rows]
+    return forward_rnn(x, L, W, U, inp.b, h0, literal=literal, threads=threads, return_seq=seq)

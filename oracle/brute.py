@@ -121,3 +121,36 @@ def gru_per_sequence(x, lengths, W, U, b_ih, b_hh, h0):
         hs.append(h)
         seqs.append(steps + [[0.0] * H for _ in range(T - n)])
     return hs, seqs
+
+
+def run_sequence_rnn(xs, W, U, b, h, outputs=None):
+    """tanh RNN cell over the rows of ``xs``: W is D x H, U is H x H, b has H
+    entries, h has H.  Returns the final h; if ``outputs`` is a list, h after
+    each step is appended to it."""
+    H = len(h)
+    h = [float(v) for v in h]
+    for xt in xs:
+        new_h = []
+        for v in range(H):
+            acc = sum(float(xk) * float(W[k][v]) for k, xk in enumerate(xt))
+            acc += sum(h[k] * float(U[k][v]) for k in range(H))
+            new_h.append(math.tanh(acc + float(b[v])))
+        h = new_h
+        if outputs is not None:
+            outputs.append(list(h))
+    return h
+
+
+def rnn_per_sequence(x, lengths, W, U, b, h0):
+    """Final h and the zero-padded output sequence of each sequence run alone
+    with the tanh RNN cell."""
+    T, H = len(x[0]), len(h0[0])
+    hs, seqs = [], []
+    for r in range(len(lengths)):
+        n = int(lengths[r])
+        steps = []
+        h = run_sequence_rnn([list(map(float, x[r][t])) for t in range(n)], W, U, b,
+                             list(h0[r]), outputs=steps)
+        hs.append(h)
+        seqs.append(steps + [[0.0] * H for _ in range(T - n)])
+    return hs, seqs

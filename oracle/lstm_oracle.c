@@ -45,6 +45,13 @@
  *
  * and no cell state (c is carried unchanged).
  *
+ * And with the plain tanh RNN cell, lstm_oracle_forward_rnn: W [D][H],
+ * U [H][H], one bias b [H],
+ *
+ *   h' = tanh(x_t W + h U + b)
+ *
+ * again with no cell state.
+ *
  * Two forms of the masking are provided:
  *   literal = 1 : every row runs the cell at every step and the new state is
  *                 then selected per row.
@@ -69,6 +76,11 @@
 #define ORACLE_BAD_ARGS 1
 #define ORACLE_BAD_LENGTHS 2
 #define ORACLE_NOMEM 3
+
+/* Cells. */
+#define CELL_LSTM 0
+#define CELL_GRU 1
+#define CELL_RNN 2
 
 static double sig(double v) { return 1.0 / (1.0 + exp(-v)); }
 
@@ -135,10 +147,30 @@ static void gru_cell_row(int D, int H, const float* xt, const float* W, const fl
     }
 }
 
+/* One application of the tanh RNN cell to one row.  W [D][H], U [H][H],
+ * bias [H]; a: [H] scratch; hn: [H] new hidden state. */
+static void rnn_cell_row(int D, int H, const float* xt, const float* W, const float* U,
+                         const float* bias, const double* h, double* a, double* hn) {
+    for (int v = 0; v < H; ++v) a[v] = 0.0;
+    for (int k = 0; k < D; ++k) {              /* x_t W */
+        const double xv = (double)xt[k];
+        const float* wrow = W + (size_t)k * H;
+        for (int v = 0; v < H; ++v) a[v] += xv * (double)wrow[v];
+    }
+    for (int k = 0; k < H; ++k) {              /* + h U */
+        const double hv = h[k];
+        const float* urow = U + (size_t)k * H;
+        for (int v = 0; v < H; ++v) a[v] += hv * (double)urow[v];
+    }
+    for (int v = 0; v < H; ++v) hn[v] = tanh(a[v] + (double)bias[v]);   /* + b, tanh */
+}
+
 /*
- * forward_impl (exported as lstm_oracle_forward and lstm_oracle_forward_seq;
- * with gru = 1 as lstm_oracle_forward_gru, where W, U are [D][3H], [H][3H],
- * bias is b_ih [3H] and bhh is b_hh [3H])
+ * forward_impl (exported as lstm_oracle_forward and lstm_oracle_forward_seq
+ * with cell = CELL_LSTM; as lstm_oracle_forward_gru with cell = CELL_GRU,
+ * where W, U are [D][3H], [H][3H], bias is b_ih [3H] and bhh is b_hh [3H];
+ * as lstm_oracle_forward_rnn with cell = CELL_RNN, where W, U are [D][H],
+ * [H][H] and bias is [H])
  *   B, T, D, H   : batch, padded time extent, input width, hidden width (> 0)
  *   x            : [B][T][D] fp32
  *   L            : [B] int32 sequence lengths, each in [0, T]
@@ -157,7 +189,7 @@ static int forward_impl(int B, int T, int D, int H, const float* x, const int32_
                         const float* W, const float* U, const float* bias,
                         const double* h0, const double* c0, double* h_out, double* c_out,
                         int literal, int nthreads, int64_t* steps_out, double* seq_out,
-                        int gru, const float* bhh) {
+                        int cell, const float* bhh) {
     if (B <= 0 || T < 0 || D <= 0 || H <= 0 || !x || !L || !W || !U || !bias || !h0 || !c0 ||
         !h_out || !c_out)
         return ORACLE_BAD_ARGS;
@@ -198,9 +230,12 @@ static int forward_impl(int B, int T, int D, int H, const float* x, const int32_
 #endif
             double* z = zs + (size_t)tid * 6 * H;
             const float* xt = x + ((size_t)b * T + t) * D;
-            if (gru) {
+            if (cell == CELL_GRU) {
                 gru_cell_row(D, H, xt, W, U, bias, bhh, h + (size_t)b * H, z, z + 3 * H,
                              hn + (size_t)b * H);
+                memcpy(cn + (size_t)b * H, c + (size_t)b * H, (size_t)H * sizeof(double));
+            } else if (cell == CELL_RNN) {
+                rnn_cell_row(D, H, xt, W, U, bias, h + (size_t)b * H, z, hn + (size_t)b * H);
                 memcpy(cn + (size_t)b * H, c + (size_t)b * H, (size_t)H * sizeof(double));
             } else {
                 lstm_cell_row(D, H, xt, W, U, bias, h + (size_t)b * H, c + (size_t)b * H, z,
@@ -230,7 +265,7 @@ int lstm_oracle_forward(int B, int T, int D, int H, const float* x, const int32_
                         const double* h0, const double* c0, double* h_out, double* c_out,
                         int literal, int nthreads, int64_t* steps_out) {
     return forward_impl(B, T, D, H, x, L, W, U, bias, h0, c0, h_out, c_out, literal, nthreads,
-                        steps_out, NULL, 0, NULL);
+                        steps_out, NULL, CELL_LSTM, NULL);
 }
 
 /* As lstm_oracle_forward, and also the output sequence seq_out [B][T][H]. */
@@ -240,7 +275,7 @@ int lstm_oracle_forward_seq(int B, int T, int D, int H, const float* x, const in
                             int literal, int nthreads, int64_t* steps_out, double* seq_out) {
     if (!seq_out) return ORACLE_BAD_ARGS;
     return forward_impl(B, T, D, H, x, L, W, U, bias, h0, c0, h_out, c_out, literal, nthreads,
-                        steps_out, seq_out, 0, NULL);
+                        steps_out, seq_out, CELL_LSTM, NULL);
 }
 
 /* The loop with the GRU cell: W [D][3H], U [H][3H], bih = b_ih [3H],
@@ -251,7 +286,17 @@ int lstm_oracle_forward_gru(int B, int T, int D, int H, const float* x, const in
                             int literal, int nthreads, int64_t* steps_out, double* seq_out) {
     if (!bhh) return ORACLE_BAD_ARGS;
     return forward_impl(B, T, D, H, x, L, W, U, bih, h0, c0, h_out, c_out, literal, nthreads,
-                        steps_out, seq_out, 1, bhh);
+                        steps_out, seq_out, CELL_GRU, bhh);
+}
+
+/* The loop with the tanh RNN cell: W [D][H], U [H][H], bias [H]; c0 is
+ * carried to c_out unchanged; seq_out may be NULL. */
+int lstm_oracle_forward_rnn(int B, int T, int D, int H, const float* x, const int32_t* L,
+                            const float* W, const float* U, const float* bias,
+                            const double* h0, const double* c0, double* h_out, double* c_out,
+                            int literal, int nthreads, int64_t* steps_out, double* seq_out) {
+    return forward_impl(B, T, D, H, x, L, W, U, bias, h0, c0, h_out, c_out, literal, nthreads,
+                        steps_out, seq_out, CELL_RNN, NULL);
 }
 
 /* Number of OpenMP threads a call with nthreads <= 0 would use. */

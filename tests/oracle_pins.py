@@ -449,3 +449,132 @@ GRU_PINS = [
     gpin_brute_force,
     gpin_torch_gru,
 ]
+
+
+# ---------------------------------------------------------------------------
+# The loop with the tanh RNN cell h' = tanh(x W + h U + b).  Each pin takes a
+# callable with the signature of ``oracle.forward_rnn``.
+
+def _rnn_case(seed, B, D, H, T, lo=0):
+    inp = workloads.random_case(seed, B, D, H, T, lo=lo)
+    rng = np.random.default_rng(seed + 11)
+    W = (rng.standard_normal((D, H)) / math.sqrt(H)).astype(np.float32)
+    U = (rng.standard_normal((H, H)) / math.sqrt(H)).astype(np.float32)
+    b = (rng.standard_normal(H) * 0.5).astype(np.float32)
+    return inp.x.copy(), inp.lengths.copy(), W, U, b, inp.h0.copy()
+
+
+def rpin_no_recurrence_closed_form(fwd):
+    """U = 0: each step's output depends on its own input only,
+    out[b, t] = tanh(x[b, t] W + b) for t < L[b] and zero after, and the final
+    state is the last of them (h0 for length 0).  Pins W's orientation, the
+    bias, the non-linearity, the time index and the padding."""
+    x, L, W, U, b, h0 = _rnn_case(60, 5, 4, 6, 8)
+    L[:] = [0, 1, 3, 8, 5]
+    U[:] = 0
+    h, seq = fwd(x, L, W, U, b, h0, return_seq=True)
+    want = np.tanh(x.astype(np.float64) @ W.astype(np.float64) + b.astype(np.float64))
+    t = np.arange(x.shape[1])[None, :, None]
+    want = np.where(t < L[:, None, None], want, 0.0)
+    assert np.max(np.abs(seq - want)) <= 1e-15
+    for r in range(len(L)):
+        last = want[r, L[r] - 1] if L[r] > 0 else h0[r].astype(np.float64)
+        assert np.max(np.abs(h[r] - last)) <= 1e-15
+
+
+def rpin_one_hot_state_reads_a_row_of_U(fwd):
+    """W = 0, b = 0 and h0 = e_k: one step gives tanh(e_k U) = tanh(U[k, :]),
+    the k-th ROW of U (a transposed U gives its column instead)."""
+    x, L, W, U, b, h0 = _rnn_case(61, 5, 3, 5, 4)
+    L[:] = 1
+    W[:] = 0
+    b[:] = 0
+    h0[:] = 0
+    for r in range(5):
+        h0[r, r] = 1.0
+    h = fwd(x, L, W, U, b, h0)
+    want = np.array([[math.tanh(float(u)) for u in row] for row in U])  # libm's tanh, as the C
+    assert _bits_equal(h, want)
+
+
+def rpin_diagonal_recurrence(fwd):
+    """W = 0, b = 0, U = diag(a): every unit follows its own scalar map
+    h <- tanh(a_v h), iterated L[b] times in plain Python."""
+    x, L, W, U, b, h0 = _rnn_case(62, 4, 3, 5, 9, lo=0)
+    L[:] = [9, 0, 4, 7]
+    W[:] = 0
+    b[:] = 0
+    a = np.array([1.5, -0.7, 0.3, 2.0, -1.2], np.float32)
+    U[:] = np.diag(a)
+    h = fwd(x, L, W, U, b, h0)
+    for r in range(4):
+        for v in range(5):
+            s = float(h0[r, v])
+            for _ in range(int(L[r])):
+                s = math.tanh(float(a[v]) * s)
+            assert h[r, v] == s, (r, v)
+
+
+def rpin_length_zero_and_poisoned_padding(fwd):
+    """A row of length 0 keeps h0 exactly, and NaN/Inf in x past each length
+    changes no bit of the result or of the output sequence."""
+    x, L, W, U, b, h0 = _rnn_case(63, 6, 5, 4, 9)
+    L[:] = [9, 0, 4, 1, 7, 0]
+    h1, s1 = fwd(x, L, W, U, b, h0, return_seq=True)
+    for r in (1, 5):
+        assert _bits_equal(h1[r], h0[r].astype(np.float64))
+    xp = x.copy()
+    for r in range(len(L)):
+        xp[r, L[r]:, :] = np.nan
+        if L[r] + 1 < x.shape[1]:
+            xp[r, L[r] + 1, :] = np.inf
+    h2, s2 = fwd(xp, L, W, U, b, h0, return_seq=True)
+    assert _bits_equal(h1, h2) and _bits_equal(s1, s2)
+
+
+def rpin_brute_force(fwd, seeds=range(20)):
+    """Agreement (<= 1e-12) of h and of the output sequence with each sequence
+    run alone in pure Python."""
+    for s in seeds:
+        rng = np.random.default_rng(7100 + s)
+        B, D, H, T = (int(rng.integers(1, 5)), int(rng.integers(1, 4)), int(rng.integers(1, 5)),
+                      int(rng.integers(1, 7)))
+        x, L, W, U, b, h0 = _rnn_case(8100 + s, B, D, H, T)
+        h, seq = fwd(x, L, W, U, b, h0, return_seq=True)
+        hb, sb = brute.rnn_per_sequence(x, L, W.tolist(), U.tolist(), b.tolist(), h0.tolist())
+        assert np.max(np.abs(h - np.array(hb))) <= 1e-12, (s, B, D, H, T)
+        assert np.max(np.abs(seq - np.array(sb))) <= 1e-12, (s, B, D, H, T)
+
+
+def rpin_torch_rnn(fwd, shapes=((3, 4, 5, 6), (7, 12, 9, 10))):
+    """Agreement (<= 1e-12) with torch.nn.RNN (tanh) in float64 on packed
+    sequences: weight_ih = W^T, weight_hh = U^T, bias_ih = b, bias_hh = 0;
+    the output sequence is unpacked with zero padding."""
+    import torch
+    from torch.nn.utils.rnn import pack_padded_sequence, pad_packed_sequence
+    for k, (B, D, H, T) in enumerate(shapes):
+        x, L, W, U, b, h0 = _rnn_case(9100 + k, B, D, H, T, lo=1)
+        h, seq = fwd(x, L, W, U, b, h0, return_seq=True)
+        m = torch.nn.RNN(D, H, nonlinearity="tanh", batch_first=True).double()
+        with torch.no_grad():
+            m.weight_ih_l0.copy_(torch.from_numpy(W.astype(np.float64).T))
+            m.weight_hh_l0.copy_(torch.from_numpy(U.astype(np.float64).T))
+            m.bias_ih_l0.copy_(torch.from_numpy(b.astype(np.float64)))
+            m.bias_hh_l0.zero_()
+            packed = pack_padded_sequence(torch.from_numpy(x.astype(np.float64)),
+                                          torch.from_numpy(L.astype(np.int64)),
+                                          batch_first=True, enforce_sorted=False)
+            out, hn = m(packed, torch.from_numpy(h0.astype(np.float64))[None])
+            out, _ = pad_packed_sequence(out, batch_first=True, total_length=T)
+        assert np.max(np.abs(h - hn[0].numpy())) <= 1e-12, (B, D, H, T)
+        assert np.max(np.abs(seq - out.numpy())) <= 1e-12, (B, D, H, T)
+
+
+RNN_PINS = [
+    rpin_no_recurrence_closed_form,
+    rpin_one_hot_state_reads_a_row_of_U,
+    rpin_diagonal_recurrence,
+    rpin_length_zero_and_poisoned_padding,
+    rpin_brute_force,
+    rpin_torch_rnn,
+]

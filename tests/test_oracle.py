@@ -84,3 +84,8 @@ def test_golden_tiny_workload():
 @pytest.mark.parametrize("pin", oracle_pins.GRU_PINS, ids=lambda f: f.__name__)
 def test_gru_pin(pin):
     pin(oracle.forward_gru)
+
+
+@pytest.mark.parametrize("pin", oracle_pins.RNN_PINS, ids=lambda f: f.__name__)
+def test_rnn_pin(pin):
+    pin(oracle.forward_rnn)

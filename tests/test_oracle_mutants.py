@@ -88,3 +88,33 @@ def test_gru_pins_catch_planted_mistake(name, tmp_path):
             caught.append(pin.__name__)
             break
     assert caught, f"no pin caught mutant {name}"
+
+
+RNN_MUTANTS = {
+    "rnn_transposed_U": ("a[v] += hv * (double)urow[v];", "a[v] += hv * (double)U[(size_t)v * H + k];"),
+    "rnn_transposed_W": ("a[v] += xv * (double)wrow[v];", "a[v] += xv * (double)W[(size_t)v * D + k];"),
+    "rnn_no_recurrent_term": ("a[v] += hv * (double)urow[v];", "(void)(hv + urow[v]);"),
+    "rnn_drop_bias": ("hn[v] = tanh(a[v] + (double)bias[v]);", "hn[v] = tanh(a[v]);"),
+    "rnn_sigmoid_instead_of_tanh": ("hn[v] = tanh(a[v] + (double)bias[v]);", "hn[v] = sig(a[v] + (double)bias[v]);"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(RNN_MUTANTS))
+def test_rnn_pins_catch_planted_mistake(name, tmp_path):
+    old, new = RNN_MUTANTS[name]
+    src = oracle.source_text()
+    assert src.count(old) == 1, f"mutation anchor for {name} not found exactly once"
+    lib = oracle.compile_variant(src.replace(old, new), str(tmp_path / f"mut_{name}.so"))
+    low = oracle._Lib(lib)
+
+    def fwd(*args, **kw):
+        return oracle.forward_rnn(*args, _lib_override=low, **kw)
+    caught = []
+    for pin in oracle_pins.RNN_PINS:
+        try:
+            with np.errstate(all="ignore"):
+                pin(fwd)
+        except (AssertionError, oracle.OracleError):
+            caught.append(pin.__name__)
+            break
+    assert caught, f"no pin caught mutant {name}"

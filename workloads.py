@@ -162,12 +162,13 @@ def make_inputs(B: int, D: int, H: int, T: int, dtype: str, lengths_spec: tuple,
 
 
 @dataclass
-class GruInputs:
-    """One batch for the GRU cell in the boundary's layouts (C-contiguous).
+class CellInputs:
+    """One batch for the GRU or the tanh RNN cell in the boundary's layouts
+    (C-contiguous).  ``cell`` is "gru" or "rnn"; G = 3H (GRU) or H (RNN).
 
-    x [B, T, D], W [D, 3H], U [H, 3H]: float32, or uint16 bf16 bits, gate
-    blocks (r, u, n) along 3H.  lengths int32 [B]; b float32 [6H] =
-    b_ih [3H] followed by b_hh [3H]; h0 float32 [B, H].
+    x [B, T, D], W [D, G], U [H, G]: float32, or uint16 bf16 bits; GRU gate
+    blocks (r, u, n) along 3H.  lengths int32 [B]; h0 float32 [B, H];
+    b float32: GRU [6H] = b_ih [3H] followed by b_hh [3H], RNN [H].
     """
     x: np.ndarray
     lengths: np.ndarray
@@ -176,6 +177,7 @@ class GruInputs:
     b: np.ndarray
     h0: np.ndarray
     dtype: str
+    cell: str = "gru"
 
     B = Inputs.B
     T = Inputs.T
@@ -192,17 +194,22 @@ class GruInputs:
         return self.b[3 * self.H:]
 
 
-def make_gru_inputs(B: int, D: int, H: int, T: int, dtype: str, lengths_spec: tuple,
-                    seed: int, force: Optional[tuple] = None, state_var: float = 0.0,
-                    bias_var: float = 0.1) -> GruInputs:
-    """GRU batch.  Draw order: lengths, x, W, U, b_ih, b_hh, h0 (h0 only when
+GruInputs = CellInputs
+_CELL_COLS = {"gru": (3, 6), "rnn": (1, 1)}   # (columns of W and U, bias entries) per hidden unit
+
+
+def make_cell_inputs(cell: str, B: int, D: int, H: int, T: int, dtype: str, lengths_spec: tuple,
+                     seed: int, force: Optional[tuple] = None, state_var: float = 0.0,
+                     bias_var: float = 0.1) -> CellInputs:
+    """GRU or RNN batch.  Draw order: lengths, x, W, U, b, h0 (h0 only when
     ``state_var`` > 0); W, U ~ N(0, 1/H), biases ~ N(0, bias_var)."""
+    g, nb = _CELL_COLS[cell]
     rng = np.random.default_rng(seed)
     L = draw_lengths(rng, B, lengths_spec)
     x = rng.standard_normal((B, T, D)).astype(np.float32)
-    W = (rng.standard_normal((D, 3 * H)) * (1.0 / np.sqrt(H))).astype(np.float32)
-    U = (rng.standard_normal((H, 3 * H)) * (1.0 / np.sqrt(H))).astype(np.float32)
-    b = (rng.standard_normal(6 * H) * np.sqrt(bias_var)).astype(np.float32)
+    W = (rng.standard_normal((D, g * H)) * (1.0 / np.sqrt(H))).astype(np.float32)
+    U = (rng.standard_normal((H, g * H)) * (1.0 / np.sqrt(H))).astype(np.float32)
+    b = (rng.standard_normal(nb * H) * np.sqrt(bias_var)).astype(np.float32)
     if state_var > 0:
         h0 = (rng.standard_normal((B, H)) * np.sqrt(state_var)).astype(np.float32)
     else:
@@ -213,23 +220,36 @@ def make_gru_inputs(B: int, D: int, H: int, T: int, dtype: str, lengths_spec: tu
         x, W, U = f32_to_bf16_bits(x), f32_to_bf16_bits(W), f32_to_bf16_bits(U)
     elif dtype != F32:
         raise ValueError(f"unknown dtype {dtype!r}")
-    return GruInputs(x=x, lengths=L, W=W, U=U, b=b, h0=h0, dtype=dtype)
+    return CellInputs(x=x, lengths=L, W=W, U=U, b=b, h0=h0, dtype=dtype, cell=cell)
 
 
-def gru_workload_inputs(name: str) -> GruInputs:
-    """The GRU batch of workload ``name``: its shapes, dtype and state
-    distribution with GRU weights; the same seed, so the lengths and x are
-    those of the LSTM batch."""
+def make_gru_inputs(*args, **kw) -> CellInputs:
+    return make_cell_inputs("gru", *args, **kw)
+
+
+def cell_workload_inputs(cell: str, name: str) -> CellInputs:
+    """The GRU or RNN batch of workload ``name``: its shapes, dtype and state
+    distribution with that cell's weights; the same seed, so the lengths and
+    x are those of the LSTM batch."""
     w = WORKLOADS[name]
-    return make_gru_inputs(w.B, w.D, w.H, w.T, w.dtype, w.lengths, w.seed, w.force,
-                           w.state_var)
+    return make_cell_inputs(cell, w.B, w.D, w.H, w.T, w.dtype, w.lengths, w.seed, w.force,
+                            w.state_var)
 
 
-def random_gru_case(seed: int, B: int, D: int, H: int, T: int, dtype: str = F32,
-                    lo: int = 0, hi: Optional[int] = None, state_var: float = 0.1) -> GruInputs:
-    """A small seeded GRU case with uniform lengths in [lo, hi] (hi defaults to T)."""
-    return make_gru_inputs(B, D, H, T, dtype, ("uniform", lo, T if hi is None else hi), seed,
-                           state_var=state_var)
+def gru_workload_inputs(name: str) -> CellInputs:
+    return cell_workload_inputs("gru", name)
+
+
+def random_cell_case(cell: str, seed: int, B: int, D: int, H: int, T: int, dtype: str = F32,
+                     lo: int = 0, hi: Optional[int] = None, state_var: float = 0.1) -> CellInputs:
+    """A small seeded GRU or RNN case with uniform lengths in [lo, hi] (hi
+    defaults to T)."""
+    return make_cell_inputs(cell, B, D, H, T, dtype, ("uniform", lo, T if hi is None else hi),
+                            seed, state_var=state_var)
+
+
+def random_gru_case(*args, **kw) -> CellInputs:
+    return random_cell_case("gru", *args, **kw)
 
 
 def workload_inputs(name: str) -> Inputs:
