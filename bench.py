@@ -46,6 +46,7 @@ def _log(*a):
 
 
 def to_device(inp, torch, cell="lstm"):
+    """Device tensors in the C ABI's argument order; GRU and RNN have no c0."""
     if inp.dtype == workloads.BF16:
         conv = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda().view(torch.bfloat16)
     else:
@@ -53,12 +54,7 @@ def to_device(inp, torch, cell="lstm"):
     f32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
     head = (conv(inp.x), torch.from_numpy(np.ascontiguousarray(inp.lengths, np.int32)).cuda(),
             conv(inp.W), conv(inp.U), f32(inp.b), f32(inp.h0))
-    return head if cell == "gru" else (*head, f32(inp.c0))
-
-
-def gru_to_device(inp, torch):
-    """GRU inputs: (x, lengths, W [D, 3H], U [H, 3H], b [6H], h0); no c0."""
-    return to_device(inp, torch, cell="gru")
+    return head if cell != "lstm" else (*head, f32(inp.c0))
 
 
 def time_forwards(torch, ld, model, dev, steps, warmup, out):
@@ -164,8 +160,8 @@ def main():
     ap.add_argument("--no-tiny", action="store_true", help="skip the tiny_f32 launch-overhead leg")
     ap.add_argument("--no-seq", action="store_true",
                     help="skip timing the forward that also writes the output sequence")
-    ap.add_argument("--no-gru", action="store_true",
-                    help="skip timing the GRU cell on the same workload shape")
+    ap.add_argument("--no-cells", action="store_true",
+                    help="skip timing the GRU and RNN cells on the same workload shape")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain copy of known size (for scaling HBM counters)")
     args = ap.parse_args()
@@ -218,29 +214,34 @@ def main():
                    "out_seq_bytes": 4 * w.B * w.T * w.H}
         del out_seq
 
-    gru_leg = None
-    if not args.no_gru:
-        # the same shapes and lengths with the GRU cell (W, U with 3H columns,
-        # repacked on the device into the four-block layout every forward)
-        _log("persistent path, GRU cell")
-        gin = workloads.gru_workload_inputs(args.workload)
-        assert np.array_equal(gin.lengths, inp.lengths)
-        gdev = gru_to_device(gin, torch)
-        gm = ld.LstmDyn(w.B, w.D, w.H, w.T, w.dtype, "persistent", cell="gru")
-        gm.set_option(ld.OPT_TIMING, 1)
-        g_fwd, g_std, g_loop, g_inproj, g_prep = time_forwards(torch, ld, gm, gdev, args.steps,
-                                                               args.warmup, out)
-        assert gm.query(ld.Q_LAST_STATUS) == ld.OK
-        g_rec = 6.0 * w.H * w.H * sumL
-        gru_leg = {"value": sumL / g_fwd, "unit": "seq·steps/s", "ms_per_forward": g_fwd * 1e3,
-                   "ms_per_forward_std": g_std * 1e3,
-                   "phases_ms": {"prep_and_pack": g_prep * 1e3, "input_projection": g_inproj * 1e3,
-                                 "loop": g_loop * 1e3},
-                   "loop_algorithmic_tflops": g_rec / g_loop / 1e12,
-                   "loop_frac": g_rec / g_loop / 1e12 / PEAK_TFLOPS[w.dtype],
-                   "launches_per_forward": gm.query(ld.Q_LAUNCHES_PER_FORWARD)}
-        gm.close()
-        del gdev, gin
+    cell_legs = None
+    if not args.no_cells:
+        # the same shapes, lengths and x with the GRU and the tanh RNN cells
+        # (their weights are repacked on the device into the four-block
+        # layout every forward); recurrent FLOPs per valid seq*step: 6H^2 (GRU),
+        # 2H^2 (RNN)
+        cell_legs = {}
+        for cell, rec_per_h2 in (("gru", 6.0), ("rnn", 2.0)):
+            _log(f"persistent path, {cell} cell")
+            cin = workloads.cell_workload_inputs(cell, args.workload)
+            assert np.array_equal(cin.lengths, inp.lengths)
+            cdev = to_device(cin, torch, cell=cell)
+            cm = ld.LstmDyn(w.B, w.D, w.H, w.T, w.dtype, "persistent", cell=cell)
+            cm.set_option(ld.OPT_TIMING, 1)
+            c_fwd, c_std, c_loop, c_inproj, c_prep = time_forwards(torch, ld, cm, cdev, args.steps,
+                                                                   args.warmup, out)
+            assert cm.query(ld.Q_LAST_STATUS) == ld.OK
+            c_rec = rec_per_h2 * w.H * w.H * sumL
+            cell_legs[cell] = {
+                "value": sumL / c_fwd, "unit": "seq·steps/s", "ms_per_forward": c_fwd * 1e3,
+                "ms_per_forward_std": c_std * 1e3,
+                "phases_ms": {"prep_and_pack": c_prep * 1e3, "input_projection": c_inproj * 1e3,
+                              "loop": c_loop * 1e3},
+                "loop_algorithmic_tflops": c_rec / c_loop / 1e12,
+                "loop_frac": c_rec / c_loop / 1e12 / PEAK_TFLOPS[w.dtype],
+                "launches_per_forward": cm.query(ld.Q_LAUNCHES_PER_FORWARD)}
+            cm.close()
+            del cdev, cin
 
     per_step = None
     if args.per_step_reps > 0:
@@ -307,7 +308,7 @@ def main():
         "wall_ms_per_step": t_wall * 1e3,
         "per_step_path": per_step,
         "forward_seq": seq_leg,
-        "gru": gru_leg,
+        "cells": cell_legs,
         "tiny_f32": tiny,
     }
     if not args.no_cpu:

@@ -71,9 +71,12 @@ enum { LSTM_DYN_PERSISTENT = 0, LSTM_DYN_PER_STEP = 1 };
  *       n = tanh(a_n + r * e_n)
  *       h' = (1 - u) * n + u * h
  *   Layouts: W [D][3H], U [H][3H] (element type = dtype), b [6H] fp32.
- *   There is no cell state: c0 is ignored (may be NULL) and out_c is written
- *   with zeros. */
-enum { LSTM_DYN_CELL_LSTM = 0, LSTM_DYN_CELL_GRU = 1 };
+ * RNN:  the plain tanh recurrent cell with one bias vector,
+ *       h' = tanh(x[b, t] W + h U + b)
+ *   Layouts: W [D][H], U [H][H] (element type = dtype), b [H] fp32.
+ * GRU and RNN have no cell state: c0 is ignored (may be NULL) and out_c is
+ * written with zeros. */
+enum { LSTM_DYN_CELL_LSTM = 0, LSTM_DYN_CELL_GRU = 1, LSTM_DYN_CELL_RNN = 2 };
 
 /* Status codes. */
 enum {
@@ -95,7 +98,7 @@ enum {
     LSTM_DYN_Q_WORKSPACE_BYTES = 4,    /* device workspace owned by the handle */
     LSTM_DYN_Q_TOTAL_ROWS = 5,         /* sum of the (clamped) lengths of the last forward (synchronises) */
     LSTM_DYN_Q_TIME_PREP_NS = 6,       /* with LSTM_DYN_OPT_TIMING: device time of the length
-                                          preparation kernel (and, for a GRU handle, the weight
+                                          preparation kernel (and, for a GRU or RNN handle, the weight
                                           repacking) in the last forward (synchronises) */
     LSTM_DYN_Q_TIME_INPROJ_NS = 7,     /* ... of the input projection GEMM */
     LSTM_DYN_Q_TIME_LOOP_NS = 8        /* ... of the time loop (the persistent kernel, or the
@@ -138,10 +141,10 @@ int lstm_dyn_create(lstm_dyn_t** out, int B, int D, int H, int T_max, int dtype,
 
 /*
  * lstm_dyn_create_cell: lstm_dyn_create for the cell `cell` (LSTM_DYN_CELL_*).
- * A GRU handle takes the GRU layouts above in lstm_dyn_forward and
- * lstm_dyn_forward_seq; its forward first repacks W, U and b into the
+ * A GRU or RNN handle takes that cell's layouts above in lstm_dyn_forward
+ * and lstm_dyn_forward_seq; its forward first repacks W, U and b into the
  * handle's workspace (one more kernel launch), so the loop kernels see the
- * LSTM's four-column layout.  Returns as lstm_dyn_create; an unknown cell is
+ * LSTM's four gate blocks (the RNN's three unused blocks hold zeros).  Returns as lstm_dyn_create; an unknown cell is
  * ERR_INVALID.
  */
 int lstm_dyn_create_cell(lstm_dyn_t** out, int B, int D, int H, int T_max, int dtype, int mode,

@@ -19,7 +19,7 @@ __all__ = [
     "lstm_dyn_create", "lstm_dyn_forward", "lstm_dyn_destroy", "lstm_dyn_query",
     "lstm_dyn_strerror", "lstm_dyn_plan", "lstm_dyn_check_args", "lstm_dyn_set_option",
     "lstm_dyn_step_trace", "lstm_dyn_forward_seq", "lstm_dyn_check_seq_args",
-    "lstm_dyn_create_cell", "lstm_dyn_check_cell_args", "CELL_LSTM", "CELL_GRU",
+    "lstm_dyn_create_cell", "lstm_dyn_check_cell_args", "CELL_LSTM", "CELL_GRU", "CELL_RNN",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -27,7 +27,7 @@ _LIB_PATH = os.path.join(_HERE, "liblstm_dyn.so")
 
 F32, BF16 = 0, 1
 PERSISTENT, PER_STEP = 0, 1
-CELL_LSTM, CELL_GRU = 0, 1
+CELL_LSTM, CELL_GRU, CELL_RNN = 0, 1, 2
 OK, ERR_INVALID, ERR_HIP, ERR_NOMEM, ERR_UNSUPPORTED, ERR_BAD_LENGTHS, ERR_TIMEOUT = range(7)
 Q_LAST_STATUS, Q_STEPS_EXECUTED, Q_LAUNCHES_PER_FORWARD, Q_GROUPS, Q_WORKSPACE_BYTES, \
     Q_TOTAL_ROWS, Q_TIME_PREP_NS, Q_TIME_INPROJ_NS, Q_TIME_LOOP_NS = range(9)
@@ -35,7 +35,8 @@ OPT_TIMING, OPT_STEP_TRACE = 0, 1
 
 _DTYPES = {"f32": F32, "fp32": F32, "float32": F32, "bf16": BF16, "bfloat16": BF16}
 _MODES = {"persistent": PERSISTENT, "per_step": PER_STEP}
-_CELLS = {"lstm": CELL_LSTM, "gru": CELL_GRU}
+_CELLS = {"lstm": CELL_LSTM, "gru": CELL_GRU, "rnn": CELL_RNN}
+_CELL_SHAPES = {CELL_LSTM: (4, 4), CELL_GRU: (3, 6), CELL_RNN: (1, 1)}  # W/U columns, bias, per unit
 
 
 class LstmDynError(RuntimeError):
@@ -206,8 +207,8 @@ class LstmDyn:
     x [B, T_max, D] and W [D, G], U [H, G] in the handle's dtype
     (torch.float32 or torch.bfloat16), lengths int32 [B], b float32,
     h0/c0 float32 [B, H]; it returns (out_h, out_c) float32 [B, H].
-    LSTM: G = 4H, b [4H].  GRU: G = 3H, b [6H] = b_ih ++ b_hh, c0 is
-    ignored (may be None) and out_c is zeros.
+    LSTM: G = 4H, b [4H].  GRU: G = 3H, b [6H] = b_ih ++ b_hh.  RNN: G = H,
+    b [H].  GRU and RNN: c0 is ignored (may be None) and out_c is zeros.
     """
 
     def __init__(self, B: int, D: int, H: int, T_max: int, dtype="bf16", mode="persistent",
@@ -235,13 +236,14 @@ class LstmDyn:
         import torch
         B, D, H, T = self.B, self.D, self.H, self.T
         et = torch.bfloat16 if self.dtype == BF16 else torch.float32
-        G, nb = (3 * H, 6 * H) if self.cell == CELL_GRU else (4 * H, 4 * H)
+        g, nbias = _CELL_SHAPES[self.cell]
+        G, nb = g * H, nbias * H
         for name, t, dt, shape in (("x", x, et, (B, T, D)), ("lengths", lengths, torch.int32, (B,)),
                                    ("W", W, et, (D, G)), ("U", U, et, (H, G)),
                                    ("b", b, torch.float32, (nb,)),
                                    ("h0", h0, torch.float32, (B, H))):
             self._check(name, t, dt, shape)
-        if c0 is not None or self.cell != CELL_GRU:
+        if c0 is not None or self.cell == CELL_LSTM:
             self._check("c0", c0, torch.float32, (B, H))
         if out_h is None:
             out_h = torch.empty((B, H), dtype=torch.float32, device=x.device)

@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "liblstm_dyn.so")
-SOURCES = ["api.hip", "prep.hip", "gemm.hip", "persistent.hip", "step.hip", "small.hip", "inproj.hip", "seq.hip", "gru.hip"]
+SOURCES = ["api.hip", "prep.hip", "gemm.hip", "persistent.hip", "step.hip", "small.hip", "inproj.hip", "seq.hip", "pack.hip"]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # Packed fp32 instructions are disabled for all device code.

@@ -11,7 +11,7 @@ using namespace ldyn;
 
 struct lstm_dyn {
     int B, D, H, T, dtype, mode, cell;
-    void* w4;                  // GRU: the packed W4, U4, b4 (gru.hip); else null
+    void* w4;                  // GRU, RNN: the packed W4, U4, b4 (pack.hip); else null
     void* u4;
     float* b4;
     long long workspace;       // bytes of the device workspace
@@ -43,7 +43,7 @@ struct Layout {
     long long meta, perm, offsets, rowsrc, gx, hx, bar, z, wt, w4, u4, b4, total;
 };
 
-Layout layout_of(int B, int D, int H, int T, int bf16, int mode, int bpad, int hpad, int gru = 0) {
+Layout layout_of(int B, int D, int H, int T, int bf16, int mode, int bpad, int hpad, int packed = 0) {
     Layout L{};
     long long o = 0;
     auto take = [&](long long bytes) {
@@ -68,12 +68,23 @@ Layout layout_of(int B, int D, int H, int T, int bf16, int mode, int bpad, int h
         L.wt = take(0);
     }
     const long long e = bf16 ? 2 : 4;
-    L.w4 = take(gru ? e * D * 4 * H : 0);
-    L.u4 = take(gru ? e * H * 4 * H : 0);
-    L.b4 = take(gru ? 16LL * H : 0);
+    L.w4 = take(packed ? e * D * 4 * H : 0);
+    L.u4 = take(packed ? e * H * 4 * H : 0);
+    L.b4 = take(packed ? 16LL * H : 0);
     L.total = o;
     return L;
 }
+
+static_assert(LSTM_DYN_CELL_LSTM == CELL_LSTM && LSTM_DYN_CELL_GRU == CELL_GRU &&
+                  LSTM_DYN_CELL_RNN == CELL_RNN,
+              "the C ABI's cell numbers are the kernels' CellKind");
+
+bool valid_cell(int cell) {
+    return cell == LSTM_DYN_CELL_LSTM || cell == LSTM_DYN_CELL_GRU || cell == LSTM_DYN_CELL_RNN;
+}
+// Columns of W and U, and bias floats, per hidden unit of each cell.
+int cell_cols(int cell) { return cell == LSTM_DYN_CELL_GRU ? 3 : cell == LSTM_DYN_CELL_RNN ? 1 : 4; }
+int cell_bias(int cell) { return cell == LSTM_DYN_CELL_GRU ? 6 : cell == LSTM_DYN_CELL_RNN ? 1 : 4; }
 
 bool overlaps(const void* a, long long na, const void* b, long long nb) {
     const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
@@ -142,28 +153,30 @@ extern "C" int lstm_dyn_plan(int B, int D, int H, int T, int dtype, int mode, in
     return LSTM_DYN_OK;
 }
 
-// Argument checks for either cell: W [D][G], U [H][G], b [NB] with G = 4H,
-// NB = 4H (LSTM) or G = 3H, NB = 6H (GRU).
-static int check_args_cell(int B, int D, int H, int T, int dtype, int gru, const void* x,
+// Argument checks for a cell: W [D][G], U [H][G], b [NB] with G = NB = 4H
+// (LSTM), G = 3H and NB = 6H (GRU), G = NB = H (RNN); only the LSTM reads c0.
+static int check_args_cell(int B, int D, int H, int T, int dtype, int cell, const void* x,
                            const int32_t* lengths, const void* W, const void* U, const float* b,
                            const float* h0, const float* c0, const float* out_h,
                            const float* out_c) {
     if (B < 1 || D < 1 || H < 1 || T < 1) return LSTM_DYN_ERR_INVALID;
     if (dtype != LSTM_DYN_F32 && dtype != LSTM_DYN_BF16) return LSTM_DYN_ERR_INVALID;
-    if (gru) c0 = nullptr;  // the GRU has no cell state: c0 is ignored and may be NULL
-    if (!x || !lengths || !W || !U || !b || !h0 || (!c0 && !gru) || !out_h || !out_c)
+    if (!valid_cell(cell)) return LSTM_DYN_ERR_INVALID;
+    const bool has_c = cell == LSTM_DYN_CELL_LSTM;
+    if (!has_c) c0 = nullptr;  // no cell state: c0 is ignored and may be NULL
+    if (!x || !lengths || !W || !U || !b || !h0 || (!c0 && has_c) || !out_h || !out_c)
         return LSTM_DYN_ERR_INVALID;
     auto al = [](const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; };
     if (!al(x, 16) || !al(W, 16) || !al(U, 16)) return LSTM_DYN_ERR_INVALID;
     if (!al(lengths, 4) || !al(b, 4) || !al(h0, 4) || !al(c0, 4) || !al(out_h, 4) || !al(out_c, 4))
         return LSTM_DYN_ERR_INVALID;
     const long long e = dtype == LSTM_DYN_BF16 ? 2 : 4;
-    const long long G = gru ? 3LL * H : 4LL * H;
+    const long long G = (long long)cell_cols(cell) * H;
     const long long nx = (long long)B * T * D * e, nL = 4LL * B, nW = (long long)D * G * e,
-                    nU = (long long)H * G * e, nb = (gru ? 24LL : 16LL) * H, ns = 4LL * B * H;
+                    nU = (long long)H * G * e, nb = 4LL * cell_bias(cell) * H, ns = 4LL * B * H;
     if (overlaps(out_h, ns, out_c, ns)) return LSTM_DYN_ERR_INVALID;
     const void* ins[] = {x, lengths, W, U, b, h0, c0};
-    const long long nin[] = {nx, nL, nW, nU, nb, ns, gru ? 0 : ns};
+    const long long nin[] = {nx, nL, nW, nU, nb, ns, has_c ? ns : 0};
     for (int i = 0; i < 7; ++i) {
         if (overlaps(out_h, ns, ins[i], nin[i]) && !(i == 5 && out_h == h0)) return LSTM_DYN_ERR_INVALID;
         if (overlaps(out_c, ns, ins[i], nin[i]) && !(i == 6 && out_c == c0)) return LSTM_DYN_ERR_INVALID;
@@ -178,7 +191,7 @@ extern "C" int lstm_dyn_check_args(int B, int D, int H, int T, int dtype, const 
     return check_args_cell(B, D, H, T, dtype, 0, x, lengths, W, U, b, h0, c0, out_h, out_c);
 }
 
-static int check_seq_args_cell(int B, int D, int H, int T, int dtype, int gru, const void* x,
+static int check_seq_args_cell(int B, int D, int H, int T, int dtype, int cell, const void* x,
                                const int32_t* lengths, const void* W, const void* U,
                                const float* b, const float* h0, const float* c0,
                                const float* out_h, const float* out_c, const float* out_seq);
@@ -191,20 +204,21 @@ extern "C" int lstm_dyn_check_seq_args(int B, int D, int H, int T, int dtype, co
                                out_seq);
 }
 
-static int check_seq_args_cell(int B, int D, int H, int T, int dtype, int gru, const void* x,
+static int check_seq_args_cell(int B, int D, int H, int T, int dtype, int cell, const void* x,
                                const int32_t* lengths, const void* W, const void* U,
                                const float* b, const float* h0, const float* c0,
                                const float* out_h, const float* out_c, const float* out_seq) {
-    const int rc = check_args_cell(B, D, H, T, dtype, gru, x, lengths, W, U, b, h0, c0, out_h, out_c);
+    const int rc = check_args_cell(B, D, H, T, dtype, cell, x, lengths, W, U, b, h0, c0, out_h, out_c);
     if (rc != LSTM_DYN_OK) return rc;
     if (!out_seq || (reinterpret_cast<uintptr_t>(out_seq) & 3) != 0) return LSTM_DYN_ERR_INVALID;
     const long long e = dtype == LSTM_DYN_BF16 ? 2 : 4;
-    const long long G = gru ? 3LL * H : 4LL * H;
+    const long long G = (long long)cell_cols(cell) * H;
     const long long nseq = 4LL * B * T * H;
     const void* others[] = {x, lengths, W, U, b, h0, c0, out_h, out_c};
     const long long sizes[] = {(long long)B * T * D * e, 4LL * B, (long long)D * G * e,
-                               (long long)H * G * e, (gru ? 24LL : 16LL) * H, 4LL * B * H,
-                               gru ? 0 : 4LL * B * H, 4LL * B * H, 4LL * B * H};
+                               (long long)H * G * e, 4LL * cell_bias(cell) * H, 4LL * B * H,
+                               cell == LSTM_DYN_CELL_LSTM ? 4LL * B * H : 0, 4LL * B * H,
+                               4LL * B * H};
     for (int i = 0; i < 9; ++i)
         if (overlaps(out_seq, nseq, others[i], sizes[i])) return LSTM_DYN_ERR_INVALID;
     return LSTM_DYN_OK;
@@ -215,11 +229,9 @@ extern "C" int lstm_dyn_check_cell_args(int B, int D, int H, int T, int dtype, i
                                         const void* U, const float* b, const float* h0,
                                         const float* c0, const float* out_h, const float* out_c,
                                         const float* out_seq) {
-    if (cell != LSTM_DYN_CELL_LSTM && cell != LSTM_DYN_CELL_GRU) return LSTM_DYN_ERR_INVALID;
-    const int gru = cell == LSTM_DYN_CELL_GRU;
     if (!out_seq)
-        return check_args_cell(B, D, H, T, dtype, gru, x, lengths, W, U, b, h0, c0, out_h, out_c);
-    return check_seq_args_cell(B, D, H, T, dtype, gru, x, lengths, W, U, b, h0, c0, out_h, out_c,
+        return check_args_cell(B, D, H, T, dtype, cell, x, lengths, W, U, b, h0, c0, out_h, out_c);
+    return check_seq_args_cell(B, D, H, T, dtype, cell, x, lengths, W, U, b, h0, c0, out_h, out_c,
                                out_seq);
 }
 
@@ -231,8 +243,8 @@ extern "C" int lstm_dyn_create_cell(lstm_dyn_t** out, int B, int D, int H, int T
                                     int mode, int cell) {
     if (!out) return LSTM_DYN_ERR_INVALID;
     *out = nullptr;
-    if (cell != LSTM_DYN_CELL_LSTM && cell != LSTM_DYN_CELL_GRU) return LSTM_DYN_ERR_INVALID;
-    const int gru = cell == LSTM_DYN_CELL_GRU;
+    if (!valid_cell(cell)) return LSTM_DYN_ERR_INVALID;
+    const int packed = cell != LSTM_DYN_CELL_LSTM;
     lstm_dyn_plan_t plan;
     int rc = lstm_dyn_plan(B, D, H, T, dtype, mode, 1 << 20, &plan);  // size checks only
     if (rc != LSTM_DYN_OK) return rc;
@@ -247,7 +259,7 @@ extern "C" int lstm_dyn_create_cell(lstm_dyn_t** out, int B, int D, int H, int T
     const int bf16 = dtype == LSTM_DYN_BF16;
     if (mode == LSTM_DYN_PERSISTENT && !plan.single) {
         const int per_cu = persistent_blocks_per_cu(bf16, plan.mt, plan.ksw, plan.kw, plan.nstate,
-                                                    plan.lds_bytes);
+                                                    plan.lds_bytes, cell);
         if (per_cu < 1 || plan.groups > per_cu * cus) return LSTM_DYN_ERR_UNSUPPORTED;
     }
     lstm_dyn* h = new (std::nothrow) lstm_dyn();
@@ -256,8 +268,8 @@ extern "C" int lstm_dyn_create_cell(lstm_dyn_t** out, int B, int D, int H, int T
     h->device = dev;
     h->num_cus = cus;
     h->plan = plan;
-    h->dims = Dims{B, D, H, T, bf16, plan.hpad, plan.bpad, gru};
-    const Layout L = layout_of(B, D, H, T, bf16, mode, plan.bpad, plan.hpad, gru);
+    h->dims = Dims{B, D, H, T, bf16, plan.hpad, plan.bpad, cell};
+    const Layout L = layout_of(B, D, H, T, bf16, mode, plan.bpad, plan.hpad, packed);
     h->workspace = L.total;
     if (hipMalloc(&h->block, (size_t)L.total) != hipSuccess) {
         (void)hipGetLastError();
@@ -274,9 +286,9 @@ extern "C" int lstm_dyn_create_cell(lstm_dyn_t** out, int B, int D, int H, int T
     h->ws.bar = reinterpret_cast<unsigned*>(base + L.bar);
     h->ws.z = mode == LSTM_DYN_PER_STEP ? reinterpret_cast<float*>(base + L.z) : nullptr;
     h->ws.wt = bf16 ? base + L.wt : nullptr;
-    h->w4 = gru ? base + L.w4 : nullptr;
-    h->u4 = gru ? base + L.u4 : nullptr;
-    h->b4 = gru ? reinterpret_cast<float*>(base + L.b4) : nullptr;
+    h->w4 = packed ? base + L.w4 : nullptr;
+    h->u4 = packed ? base + L.u4 : nullptr;
+    h->b4 = packed ? reinterpret_cast<float*>(base + L.b4) : nullptr;
     // Zero the small tables and the operand buffer (its padding must stay zero).
     if (hipMemset(base, 0, (size_t)L.gx) != hipSuccess ||
         hipMemset(base + L.hx, 0, (size_t)(L.total - L.hx)) != hipSuccess) {
@@ -399,14 +411,15 @@ static int forward_impl(lstm_dyn_t* h, const void* x, const int32_t* lengths, co
 
     auto mark = [&](int i) { return h->timing ? hipEventRecord(h->ev[i], s) : hipSuccess; };
     LD_CHECK(mark(0));
-    if (h->cell == LSTM_DYN_CELL_GRU) {
-        // the GRU's weights in the four-block layout the kernels use (timed with prep)
-        LD_CHECK(launch_gru_pack(d, W, U, b, h->w4, h->u4, h->b4, s));
+    const bool packed = h->cell != LSTM_DYN_CELL_LSTM;
+    if (packed) {
+        // the cell's weights in the four-block layout the kernels use (timed with prep)
+        LD_CHECK(launch_cell_pack(d, W, U, b, h->w4, h->u4, h->b4, s));
         W = h->w4;
         U = h->u4;
         b = h->b4;
     }
-    const long long pack_launches = h->cell == LSTM_DYN_CELL_GRU ? 1 : 0;
+    const long long pack_launches = packed ? 1 : 0;
     if (h->mode == LSTM_DYN_PERSISTENT && h->plan.single) {
         LD_CHECK(mark(1));
         LD_CHECK(mark(2));
@@ -465,7 +478,7 @@ extern "C" int lstm_dyn_forward(lstm_dyn_t* h, const void* x, const int32_t* len
                                 const void* U, const float* b, const float* h0, const float* c0,
                                 float* out_h, float* out_c, void* stream) {
     if (!h) return LSTM_DYN_ERR_INVALID;
-    const int rc = check_args_cell(h->B, h->D, h->H, h->T, h->dtype, h->cell == LSTM_DYN_CELL_GRU,
+    const int rc = check_args_cell(h->B, h->D, h->H, h->T, h->dtype, h->cell,
                                    x, lengths, W, U, b, h0, c0, out_h, out_c);
     if (rc != LSTM_DYN_OK) return rc;
     return forward_impl(h, x, lengths, W, U, b, h0, c0, out_h, out_c, nullptr, stream);
@@ -477,7 +490,7 @@ extern "C" int lstm_dyn_forward_seq(lstm_dyn_t* h, const void* x, const int32_t*
                                     void* stream) {
     if (!h) return LSTM_DYN_ERR_INVALID;
     const int rc = check_seq_args_cell(h->B, h->D, h->H, h->T, h->dtype,
-                                       h->cell == LSTM_DYN_CELL_GRU, x, lengths, W, U, b, h0, c0,
+                                       h->cell, x, lengths, W, U, b, h0, c0,
                                        out_h, out_c, out_seq);
     if (rc != LSTM_DYN_OK) return rc;
     return forward_impl(h, x, lengths, W, U, b, h0, c0, out_h, out_c, out_seq, stream);

@@ -28,11 +28,15 @@ __host__ __device__ inline int gate_col(int cprime, int H) { return (cprime & 3)
 // Element types.  MFMA 16x16xK fragments: lane l holds operand row/column
 // (l & 15) and the K slice [(l >> 4) * KPL, (l >> 4) * KPL + KPL); the 16x16
 // fp32 result gives lane l rows 4*(l >> 4) + j (j = 0..3) of column (l & 15).
+// src_t is the element type of the caller's U (and of x, W); store_t the
+// type of the MFMA operands the kernels keep (U fragments, the h operand).
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 struct EltF32 {
     using store_t = float;
+    using src_t = float;
     using frag_t = float;
     static constexpr int KSTEP = 4;  // K per MFMA
     static constexpr int KPL = 1;    // K values per lane
@@ -42,12 +46,14 @@ struct EltF32 {
     __device__ static inline frag_t zero() { return 0.0f; }
     __device__ static inline store_t from_f32(float v) { return v; }
     __device__ static inline float to_f32(store_t v) { return v; }
+    __device__ static inline store_t from_src(src_t v) { return v; }
     // Load KPL consecutive elements at p (aligned to KPL elements).
     __device__ static inline frag_t load(const store_t* p) { return *p; }
 };
 
 struct EltBF16 {
     using store_t = __bf16;
+    using src_t = __bf16;
     using frag_t = bf16x8_t;
     static constexpr int KSTEP = 32;
     static constexpr int KPL = 8;
@@ -62,6 +68,36 @@ struct EltBF16 {
     }
     __device__ static inline store_t from_f32(float v) { return (__bf16)v; }
     __device__ static inline float to_f32(store_t v) { return (float)v; }
+    __device__ static inline store_t from_src(src_t v) { return v; }
+    __device__ static inline frag_t load(const store_t* p) {
+        return *reinterpret_cast<const frag_t*>(p);
+    }
+};
+
+// bf16 data with fp16 recurrent operands: U is widened from bf16 to fp16
+// (exact for 2^-14 <= |U| <= 65504, the fp16 normal range; smaller entries
+// land on the fp16 subnormal grid, an absolute error <= 2^-25) and h is
+// rounded to fp16 for the product h U.  h lies in (-1, 1) after the first
+// step of every cell here, where fp16 keeps 11 significant bits against
+// bf16's 8 at the same MFMA rate.
+struct EltH16 {
+    using store_t = _Float16;
+    using src_t = __bf16;
+    using frag_t = f16x8_t;
+    static constexpr int KSTEP = 32;
+    static constexpr int KPL = 8;
+    __device__ static inline f32x4_t mfma(frag_t a, frag_t b, f32x4_t c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+    }
+    __device__ static inline frag_t zero() {
+        frag_t z;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) z[i] = (_Float16)0.0f;
+        return z;
+    }
+    __device__ static inline store_t from_f32(float v) { return (_Float16)v; }
+    __device__ static inline float to_f32(store_t v) { return (float)v; }
+    __device__ static inline store_t from_src(src_t v) { return (_Float16)(float)v; }
     __device__ static inline frag_t load(const store_t* p) {
         return *reinterpret_cast<const frag_t*>(p);
     }
@@ -90,6 +126,10 @@ __device__ inline void gru_cell(f32x4_t z, float& h) {
     h = (1.0f - ug) * ng + ug * h;
 }
 
+// The tanh RNN cell in the four columns of a unit: the weights are packed so
+// that z[0] = x W + h U + b and the other three columns are zero.
+__device__ inline void rnn_cell(f32x4_t z, float& h) { h = tanh_f(z[0]); }
+
 // One LSTM cell update from the four pre-activations of a (row, unit).
 __device__ inline void lstm_cell(f32x4_t z, float& c, float& h) {
     const float ig = sigmoid_f(z[0]);
@@ -98,6 +138,17 @@ __device__ inline void lstm_cell(f32x4_t z, float& c, float& h) {
     const float og = sigmoid_f(z[3]);
     c = fg * c + ig * gg;
     h = og * tanh_f(c);
+}
+
+// Cells of the loop (the kinds the C ABI's cell argument names).
+enum CellKind { CELL_LSTM = 0, CELL_GRU = 1, CELL_RNN = 2 };
+
+// The update of `cell` from the four pre-activations of a (row, unit); c is
+// the LSTM's cell state and left unchanged by the other cells.
+__device__ inline void apply_cell(int cell, f32x4_t z, float& c, float& h) {
+    if (cell == CELL_GRU) gru_cell(z, h);
+    else if (cell == CELL_RNN) rnn_cell(z, h);
+    else lstm_cell(z, c, h);
 }
 
 }  // namespace ldyn

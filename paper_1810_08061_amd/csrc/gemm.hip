@@ -5,7 +5,9 @@
 //     the state, so x[b, t] W + b for every valid (b, t) is one GEMM over all
 //     time steps, M = sum of lengths (compact rows), N = 4H, K = D;
 //   * the per-step comparison path's recurrent product h U + Gx[t] for the
-//     rows active at step t, M = active(t), N = 4H, K = H.
+//     rows active at step t, M = active(t), N = 4H, K = H (with bf16 data in
+//     fp16 operands, as in the persistent loop: U is widened from bf16 on its
+//     way into LDS, h is kept in fp16).
 //
 // C^T is formed as (W^T)(A^T): MFMA rows are gate-interleaved columns c', MFMA
 // columns are data rows, so each lane's four fp32 results are the four gates
@@ -47,6 +49,8 @@ template <typename E, int MODE>
 __global__ void __launch_bounds__(G_THREADS)
 gemm_kernel(GemmParams p) {
     using S = typename E::store_t;
+    using Src = typename E::src_t;  // element type of Bw (the caller's W or U)
+    static_assert(sizeof(Src) == sizeof(S), "operand and source elements have one size");
     using F = typename E::frag_t;
     using TL = GemmTile<E>;
     constexpr int VE = TL::VE, BK = TL::BK, LDK = TL::LDK, KS = TL::KS, UV = TL::UV;
@@ -67,7 +71,7 @@ gemm_kernel(GemmParams p) {
     const int ntr = (nrows + G_RN - 1) / G_RN;
     const int ntiles = ntc * ntr;
     const S* __restrict__ A = static_cast<const S*>(p.A);
-    const S* __restrict__ Bw = static_cast<const S*>(p.Bw);
+    const Src* __restrict__ Bw = static_cast<const Src*>(p.Bw);
     const int nkb = (K + BK - 1) / BK;
 
     for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
@@ -99,7 +103,8 @@ gemm_kernel(GemmParams p) {
             bkk[j] = v / (UV * 4);
         }
 
-        S areg[2][VE], breg[2][VE];
+        S areg[2][VE];
+        Src breg[2][VE];
         auto load_tiles = [&](int k0) {
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
@@ -116,16 +121,16 @@ gemm_kernel(GemmParams p) {
                 }
                 const int kb = k0 + bkk[j];
                 const int u = ubase + bseg[j] * VE;
-                const S* src = Bw + (long)kb * N4 + bg[j] * H + u;
+                const Src* src = Bw + (long)kb * N4 + bg[j] * H + u;
                 if (kb < K && p.b_vec && u + VE <= H) {
                     const uint4 v = *reinterpret_cast<const uint4*>(src);
-                    const S* vs = reinterpret_cast<const S*>(&v);
+                    const Src* vs = reinterpret_cast<const Src*>(&v);
 #pragma unroll
                     for (int e = 0; e < VE; ++e) breg[j][e] = vs[e];
                 } else {
 #pragma unroll
                     for (int e = 0; e < VE; ++e)
-                        breg[j][e] = (kb < K && u + e < H) ? src[e] : E::from_f32(0.0f);
+                        breg[j][e] = (kb < K && u + e < H) ? src[e] : (Src)0.0f;
                 }
             }
         };
@@ -137,7 +142,7 @@ gemm_kernel(GemmParams p) {
                 for (int e = 0; e < VE; ++e) dst[e] = areg[j][e];
 #pragma unroll
                 for (int e = 0; e < VE; ++e)
-                    Bs[(4 * (bseg[j] * VE + e) + bg[j]) * LDK + bkk[j]] = breg[j][e];
+                    Bs[(4 * (bseg[j] * VE + e) + bg[j]) * LDK + bkk[j]] = E::from_src(breg[j][e]);
             }
         };
 
@@ -240,7 +245,7 @@ hipError_t launch_step_gemm(const Dims& d, int t, const void* U, const Workspace
     p.b_vec = (d.H % ve == 0) && aligned16(U);
     const int grid = ((4 * d.H + G_CM - 1) / G_CM) * ((d.B + G_RN - 1) / G_RN);
     if (d.bf16)
-        hipLaunchKernelGGL((gemm_kernel<EltBF16, MODE_STEP>), dim3(grid), dim3(G_THREADS), 0, s, p);
+        hipLaunchKernelGGL((gemm_kernel<EltH16, MODE_STEP>), dim3(grid), dim3(G_THREADS), 0, s, p);
     else
         hipLaunchKernelGGL((gemm_kernel<EltF32, MODE_STEP>), dim3(grid), dim3(G_THREADS), 0, s, p);
     return hipGetLastError();

@@ -27,15 +27,17 @@ struct Dims {
     int B, D, H, T;     // batch, input width, hidden width, padded time extent
     int bf16;           // 1: x, W, U are bf16; 0: fp32
     int hpad, bpad;     // padded hidden width / batch rows of the operand buffer
-    int gru;            // 1: GRU cell (weights packed to four columns per unit), 0: LSTM
+    int cell;           // CellKind; GRU and RNN weights are packed into the LSTM's four gate blocks
 };
 
-// GRU: the caller's W [D][3H], U [H][3H] (gate blocks r, u, n) and biases
-// b_ih, b_hh [3H] (b [6H]) packed into the four-column layout of the LSTM
-// path: W4 [D][4H] = (W_r, W_u, 0, W_n), U4 [H][4H] = (U_r, U_u, U_n, 0),
-// b4 [4H] = (b_ir + b_hr, b_iu + b_hu, b_hn, b_in).
-hipError_t launch_gru_pack(const Dims& d, const void* W, const void* U, const float* b, void* W4,
-                           void* U4, float* b4, hipStream_t s);
+// GRU and RNN: the caller's weights packed into the four gate blocks of the
+// LSTM path (d.cell selects the packing).  GRU: W [D][3H], U [H][3H] (gate
+// blocks r, u, n), b [6H] = b_ih ++ b_hh -> W4 [D][4H] = (W_r, W_u, 0, W_n),
+// U4 [H][4H] = (U_r, U_u, U_n, 0), b4 [4H] = (b_ir + b_hr, b_iu + b_hu, b_hn,
+// b_in).  RNN: W [D][H], U [H][H], b [H] -> (W, 0, 0, 0), (U, 0, 0, 0),
+// (b, 0, 0, 0).
+hipError_t launch_cell_pack(const Dims& d, const void* W, const void* U, const float* b, void* W4,
+                            void* U4, float* b4, hipStream_t s);
 
 // Preparation: clamp and validate lengths, stable descending length sort,
 // per-step active counts and compact row offsets, compact row sources.
@@ -65,7 +67,7 @@ hipError_t launch_persistent(const Dims& d, const PersistentConfig& pc, const vo
                              const float* h0, const float* c0, float* out_h, float* out_c,
                              const Workspace& ws, hipStream_t s);
 // Occupancy check for the co-resident grid; returns blocks per CU (0 if none).
-int persistent_blocks_per_cu(int bf16, int mt, int ksw, int kw, int nst, int lds_bytes);
+int persistent_blocks_per_cu(int bf16, int mt, int ksw, int kw, int nst, int lds_bytes, int cell);
 // Compiled variant with exactly (mt, kw, ksw) and the smallest state capacity >= nstate.
 bool persistent_pick_variant(int bf16, int mt, int kw, int ksw, int nstate, int* nst);
 int persistent_lds_bytes(int bf16, int mt, int kw, int nst, int hpad);

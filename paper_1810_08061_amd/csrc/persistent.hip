@@ -52,7 +52,6 @@ struct PersistParams {
     unsigned long long timeout_ticks;
     unsigned long long* trace;  // [T + 1][4] timestamps from workgroup 0, or null
     int seq;                    // 1: also keep each step's h (fp32) for the output sequence
-    int gru;                    // 1: GRU cell (no cell state), 0: LSTM
 };
 
 // Logical workgroup index: consecutive workgroups are dispatched to different
@@ -116,15 +115,17 @@ __device__ inline bool grid_wait(const PersistParams& p, int k, int* lds_ok) {
 // the all-ones pattern (a NaN).  operand() never produces it: a NaN h that
 // would convert to it is stored as the canonical quiet NaN instead.
 template <typename E> struct HxIO;
-template <> struct HxIO<EltBF16> {
-    __device__ static inline bf16x8_t load(__amdgpu_buffer_rsrc_t R, unsigned byte_off) {
+// 16-bit operands (bf16 or fp16): T the element, V eight of them, QNAN the
+// canonical quiet NaN's bits.
+template <typename T, typename V, unsigned short QNAN> struct HxIO16 {
+    __device__ static inline V load(__amdgpu_buffer_rsrc_t R, unsigned byte_off) {
         typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
         const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(R, byte_off, 0, P_SC1);
-        return __builtin_bit_cast(bf16x8_t, v);
+        return __builtin_bit_cast(V, v);
     }
-    __device__ static inline __bf16 operand(float h) {
-        const unsigned short b = __builtin_bit_cast(unsigned short, (__bf16)h);
-        return __builtin_bit_cast(__bf16, b == 0xffffu ? (unsigned short)0x7fc0u : b);
+    __device__ static inline T operand(float h) {
+        const unsigned short b = __builtin_bit_cast(unsigned short, (T)h);
+        return __builtin_bit_cast(T, b == 0xffffu ? QNAN : b);
     }
     __device__ static inline void store(__amdgpu_buffer_rsrc_t R, unsigned byte_off, float h) {
         __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, operand(h)), R, byte_off, 0,
@@ -132,7 +133,7 @@ template <> struct HxIO<EltBF16> {
     }
     // true if any of the KSW fragments holds the marker in one of its elements
     template <int KSW>
-    __device__ static inline bool has_marker(const bf16x8_t* f) {
+    __device__ static inline bool has_marker(const V* f) {
         typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
         typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
         u16x2 m = {0, 0};
@@ -148,6 +149,8 @@ template <> struct HxIO<EltBF16> {
         return m[0] == 0xffffu || m[1] == 0xffffu;
     }
 };
+template <> struct HxIO<EltH16> : HxIO16<_Float16, f16x8_t, 0x7e00> {};
+
 template <> struct HxIO<EltF32> {
     __device__ static inline float load(__amdgpu_buffer_rsrc_t R, unsigned byte_off) {
         return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(R, byte_off, 0, P_SC1));
@@ -207,7 +210,7 @@ struct PLayout {
     static constexpr int BYTES = (NTC * KW * MT + GX_KB) * 1024;
 };
 
-template <typename E, int MT, int KSW, int KW, int NST>
+template <typename E, int MT, int KSW, int KW, int NST, int CELL>
 __global__ void __launch_bounds__(KW * 64, 1)
 persistent_kernel(PersistParams p) {
     using S = typename E::store_t;
@@ -251,7 +254,8 @@ persistent_kernel(PersistParams p) {
     // by 16 bytes (spreads the 2/4-byte writes over banks, keeps the 16-byte
     // fragment reads aligned).  Out-of-range k and units stage as zeros.
     {
-        const S* U = static_cast<const S*>(p.U);
+        using Src = typename E::src_t;
+        const Src* U = static_cast<const Src*>(p.U);
         S* ust = reinterpret_cast<S*>(lds);
         constexpr int NCOL = 16 * MT, UPG = 4 * MT;  // columns, units per gate segment
         const int stride = hpad + 16 / (int)sizeof(S);
@@ -269,19 +273,19 @@ persistent_kernel(PersistParams p) {
         };
         auto stage = [&](int e) {
             bool ok;
-            const S v = U[src_of(e, ok)];
+            const S v = E::from_src(U[src_of(e, ok)]);
             ust[dst_of(e)] = ok ? v : E::from_f32(0.0f);
         };
         constexpr int ROUND = KW * 64 * 8;
         const int full = total / ROUND * ROUND;
         for (int e0 = 0; e0 < full; e0 += ROUND) {  // unguarded: eight loads in flight per thread
-            S v[8];
+            Src v[8];
             bool ok[8];
 #pragma unroll
             for (int r = 0; r < 8; ++r) v[r] = U[src_of(e0 + r * KW * 64 + tid, ok[r])];
 #pragma unroll
             for (int r = 0; r < 8; ++r)
-                ust[dst_of(e0 + r * KW * 64 + tid)] = ok[r] ? v[r] : E::from_f32(0.0f);
+                ust[dst_of(e0 + r * KW * 64 + tid)] = ok[r] ? E::from_src(v[r]) : E::from_f32(0.0f);
         }
         for (int e = full + tid; e < total; e += KW * 64) stage(e);
         __syncthreads();
@@ -340,7 +344,7 @@ persistent_kernel(PersistParams p) {
             if (nt < ntmax && s < B && u < H) {
                 const size_t ib = (size_t)p.perm[s] * H + u;
                 hst[i] = p.h0[ib];  // read before the final write: exact aliasing out_h == h0 is allowed
-                if (!p.gru) cst[i] = p.c0[ib];
+                if constexpr (CELL == CELL_LSTM) cst[i] = p.c0[ib];
             }
             hstage[w][(l & 15) * UPW + mt * 4 + (l >> 4)] = IO::operand(hst[i]);
         }
@@ -622,8 +626,7 @@ persistent_kernel(PersistParams p) {
                         const bool live = s < act;
                         nan |= live & ((z[0] != z[0]) | (z[1] != z[1]) | (z[2] != z[2]) | (z[3] != z[3]));
                         float c = cst[i], h = hst[i];
-                        if (p.gru) gru_cell(z, h);
-                        else lstm_cell(z, c, h);
+                        apply_cell(CELL, z, c, h);  // CELL is a template argument: no branch
                         cn[i] = c;
                         hn[i] = h;
                     }
@@ -728,25 +731,31 @@ persistent_kernel(PersistParams p) {
 // capacity that covers the batch.
 typedef void (*persist_fn)(PersistParams);
 
-struct Variant { int bf16, mt, ksw, kw, nst, lds_bytes; persist_fn f; };
+// f[cell]: the variant compiled for each CellKind, so the gate step has no
+// branch on the cell (a uniform branch there cost about 4% of the loop).
+struct Variant { int bf16, mt, ksw, kw, nst, lds_bytes; persist_fn f[3]; };
 
-#define PV(BF, ET, MT, KS, KW, NS) \
-    {BF, MT, KS, KW, NS, PLayout<MT, KW, NS>::BYTES, persistent_kernel<ET, MT, KS, KW, NS>}
+#define PV(BF, ET, MT, KS, KW, NS)                                                       \
+    {BF, MT, KS, KW, NS, PLayout<MT, KW, NS>::BYTES,                                      \
+     {persistent_kernel<ET, MT, KS, KW, NS, CELL_LSTM>, persistent_kernel<ET, MT, KS, KW, NS, CELL_GRU>, \
+      persistent_kernel<ET, MT, KS, KW, NS, CELL_RNN>}}
 #define PV_NST(BF, ET, MT, KS, KW) PV(BF, ET, MT, KS, KW, 2), PV(BF, ET, MT, KS, KW, 8)
 static const Variant kVariants[] = {
     PV_NST(0, EltF32, 1, 4, 4),
     PV_NST(0, EltF32, 1, 8, 4), PV_NST(0, EltF32, 1, 16, 4), PV_NST(0, EltF32, 1, 32, 4),
     PV_NST(0, EltF32, 1, 64, 4),
-    PV_NST(1, EltBF16, 1, 1, 4), PV_NST(1, EltBF16, 1, 2, 4), PV_NST(1, EltBF16, 1, 4, 4),
-    PV_NST(1, EltBF16, 1, 8, 4),
-    PV(1, EltBF16, 2, 8, 8, 4), PV(1, EltBF16, 2, 8, 8, 8),
+    PV_NST(1, EltH16, 1, 1, 4), PV_NST(1, EltH16, 1, 2, 4), PV_NST(1, EltH16, 1, 4, 4),
+    PV_NST(1, EltH16, 1, 8, 4),
+    PV(1, EltH16, 2, 8, 8, 4), PV(1, EltH16, 2, 8, 8, 8),
 };
 #undef PV_NST
 #undef PV
 
-static persist_fn find_variant(int bf16, int mt, int ksw, int kw, int nst) {
+static persist_fn find_variant(int bf16, int mt, int ksw, int kw, int nst, int cell) {
+    if (cell < CELL_LSTM || cell > CELL_RNN) return nullptr;
     for (const Variant& v : kVariants)
-        if (v.bf16 == bf16 && v.mt == mt && v.ksw == ksw && v.kw == kw && v.nst == nst) return v.f;
+        if (v.bf16 == bf16 && v.mt == mt && v.ksw == ksw && v.kw == kw && v.nst == nst)
+            return v.f[cell];
     return nullptr;
 }
 
@@ -771,8 +780,8 @@ int persistent_lds_bytes(int bf16, int mt, int kw, int nst, int hpad) {
     return staged > loop ? staged : loop;
 }
 
-int persistent_blocks_per_cu(int bf16, int mt, int ksw, int kw, int nst, int lds_bytes) {
-    persist_fn f = find_variant(bf16, mt, ksw, kw, nst);
+int persistent_blocks_per_cu(int bf16, int mt, int ksw, int kw, int nst, int lds_bytes, int cell) {
+    persist_fn f = find_variant(bf16, mt, ksw, kw, nst, cell);
     if (!f) return 0;
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(f),
                             hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes) != hipSuccess)
@@ -787,7 +796,7 @@ int persistent_blocks_per_cu(int bf16, int mt, int ksw, int kw, int nst, int lds
 hipError_t launch_persistent(const Dims& d, const PersistentConfig& pc, const void* U,
                              const float* h0, const float* c0, float* out_h, float* out_c,
                              const Workspace& ws, hipStream_t s) {
-    persist_fn f = find_variant(d.bf16, pc.mt, pc.ksw, pc.kw, pc.nst);
+    persist_fn f = find_variant(d.bf16, pc.mt, pc.ksw, pc.kw, pc.nst, d.cell);
     if (!f) return hipErrorInvalidValue;
     PersistParams p{};
     p.U = U;
@@ -809,7 +818,6 @@ hipError_t launch_persistent(const Dims& d, const PersistentConfig& pc, const vo
     p.timeout_ticks = pc.timeout_ticks;
     p.trace = pc.trace;
     p.seq = pc.seq;
-    p.gru = d.gru;
     void* args[] = {&p};
     return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(f), dim3(pc.groups),
                                       dim3(pc.kw * 64), args, (unsigned)pc.lds_bytes, s);

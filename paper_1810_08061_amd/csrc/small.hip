@@ -7,7 +7,9 @@
 // applies the gates to the rows with t < L[b] (the per-row select of the
 // paper's loop, Section 9 "RNN cells"), and passes h to the next step through
 // LDS.  x for step t+1 is fetched while step t computes.  Rows stay in batch
-// order; finished rows are simply not updated.
+// order; finished rows are simply not updated.  With bf16 data, x W takes bf16
+// operands and h U fp16 operands (U widened from bf16), as in the persistent
+// loop.
 #include "launch.h"
 
 namespace ldyn {
@@ -29,17 +31,21 @@ struct SmallParams {
     float* seq;  // [B][T][H] output sequence (valid steps only), or null
     Meta* meta;
     int B, D, H, T;
-    int gru;  // 1: GRU cell, 0: LSTM
+    int cell;  // CellKind (only the LSTM has a cell state)
 };
 
-template <typename E, int KD, int KH, int NT>
+// E: element type of x and W; EH: of the recurrent operands (U, h).
+template <typename E, typename EH, int KD, int KH, int NT>
 __global__ void __launch_bounds__(SM_THREADS, 1)
 small_kernel(SmallParams p) {
     using S = typename E::store_t;
     using F = typename E::frag_t;
-    constexpr int HP = KH * E::KSTEP;      // padded hidden width of the LDS h rows
-    constexpr int HS = HP + 16 / sizeof(S);  // row stride (16-byte pad)
-    __shared__ __attribute__((aligned(16))) S hs[2][NT * 16 * HS];
+    using SH = typename EH::store_t;
+    using FH = typename EH::frag_t;
+    static_assert(E::KSTEP == EH::KSTEP && E::KPL == EH::KPL, "one fragment shape");
+    constexpr int HP = KH * EH::KSTEP;      // padded hidden width of the LDS h rows
+    constexpr int HS = HP + 16 / sizeof(SH);  // row stride (16-byte pad)
+    __shared__ __attribute__((aligned(16))) SH hs[2][NT * 16 * HS];
     __shared__ int len[NT * 16];
     __shared__ int maxlen, bad;
 
@@ -47,7 +53,7 @@ small_kernel(SmallParams p) {
     const int B = p.B, D = p.D, H = p.H, T = p.T, H4 = 4 * H;
     const S* X = static_cast<const S*>(p.x);
     const S* W = static_cast<const S*>(p.W);
-    const S* U = static_cast<const S*>(p.U);
+    const typename EH::src_t* U = static_cast<const typename EH::src_t*>(p.U);
 
     if (tid == 0) {
         maxlen = 0;
@@ -69,12 +75,13 @@ small_kernel(SmallParams p) {
     // h0 -> LDS (operand type); padding rows and columns are zero in both buffers
     for (int i = tid; i < NT * 16 * HS; i += SM_THREADS) {
         const int n = i / HS, k = i - n * HS;
-        hs[0][i] = E::from_f32((n < B && k < H) ? p.h0[(size_t)n * H + k] : 0.0f);
-        hs[1][i] = E::from_f32(0.0f);
+        hs[0][i] = EH::from_f32((n < B && k < H) ? p.h0[(size_t)n * H + k] : 0.0f);
+        hs[1][i] = EH::from_f32(0.0f);
     }
 
     // A-fragments of W^T and U^T for this wave's two gate tiles (clamped loads).
-    F wf[SM_MT][KD], uf[SM_MT][KH];
+    F wf[SM_MT][KD];
+    FH uf[SM_MT][KH];
     float bias[SM_MT][4];
 #pragma unroll
     for (int mt = 0; mt < SM_MT; ++mt) {
@@ -95,13 +102,13 @@ small_kernel(SmallParams p) {
         }
 #pragma unroll
         for (int ks = 0; ks < KH; ++ks) {
-            F f = E::zero();
+            FH f = EH::zero();
 #pragma unroll
-            for (int e = 0; e < E::KPL; ++e) {
-                const int k = ks * E::KSTEP + (l >> 4) * E::KPL + e;
-                const S v = U[(size_t)min(k, H - 1) * H4 + col];
-                if constexpr (E::KPL == 1) f = (uok && k < H) ? v : 0.0f;
-                else f[e] = (uok && k < H) ? v : E::from_f32(0.0f);
+            for (int e = 0; e < EH::KPL; ++e) {
+                const int k = ks * EH::KSTEP + (l >> 4) * EH::KPL + e;
+                const SH v = EH::from_src(U[(size_t)min(k, H - 1) * H4 + col]);
+                if constexpr (EH::KPL == 1) f = (uok && k < H) ? v : 0.0f;
+                else f[e] = (uok && k < H) ? v : EH::from_f32(0.0f);
             }
             uf[mt][ks] = f;
         }
@@ -120,7 +127,7 @@ small_kernel(SmallParams p) {
             const int n = nt * 16 + (l & 15);
             const int u = ((w * SM_MT + mt) * 16 + 4 * (l >> 4)) >> 2;
             const bool ok = n < B && u < H;
-            cst[mt][nt] = ok && !p.gru ? p.c0[(size_t)n * H + u] : 0.0f;
+            cst[mt][nt] = ok && p.cell == CELL_LSTM ? p.c0[(size_t)n * H + u] : 0.0f;
             hst[mt][nt] = ok ? p.h0[(size_t)n * H + u] : 0.0f;
         }
     __syncthreads();
@@ -151,8 +158,8 @@ small_kernel(SmallParams p) {
 
     for (int t = 0; t < ml; ++t) {
         if (t + 1 < ml) load_x(xn, t + 1);
-        const S* hcur = hs[t & 1];
-        S* hnext = hs[(t + 1) & 1];
+        const SH* hcur = hs[t & 1];
+        SH* hnext = hs[(t + 1) & 1];
         f32x4_t acc[SM_MT][NT];
 #pragma unroll
         for (int mt = 0; mt < SM_MT; ++mt)
@@ -168,9 +175,9 @@ small_kernel(SmallParams p) {
         for (int ks = 0; ks < KH; ++ks)
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt) {
-                const F hf = E::load(hcur + (nt * 16 + (l & 15)) * HS + ks * E::KSTEP + (l >> 4) * E::KPL);
+                const FH hf = EH::load(hcur + (nt * 16 + (l & 15)) * HS + ks * EH::KSTEP + (l >> 4) * EH::KPL);
 #pragma unroll
-                for (int mt = 0; mt < SM_MT; ++mt) acc[mt][nt] = E::mfma(uf[mt][ks], hf, acc[mt][nt]);
+                for (int mt = 0; mt < SM_MT; ++mt) acc[mt][nt] = EH::mfma(uf[mt][ks], hf, acc[mt][nt]);
             }
 #pragma unroll
         for (int mt = 0; mt < SM_MT; ++mt)
@@ -184,13 +191,12 @@ small_kernel(SmallParams p) {
 #pragma unroll
                     for (int g = 0; g < 4; ++g) z[g] += bias[mt][g];
                     float c = cst[mt][nt], h = hst[mt][nt];
-                    if (p.gru) gru_cell(z, h);
-                    else lstm_cell(z, c, h);
+                    apply_cell(p.cell, z, c, h);
                     cst[mt][nt] = c;
                     hst[mt][nt] = h;
                     if (p.seq) p.seq[((size_t)n * T + t) * H + u] = h;  // output at step t
                 }
-                hnext[n * HS + u] = E::from_f32(hst[mt][nt]);
+                hnext[n * HS + u] = EH::from_f32(hst[mt][nt]);
             }
         __syncthreads();
 #pragma unroll
@@ -222,12 +228,14 @@ small_kernel(SmallParams p) {
 
 typedef void (*small_fn)(SmallParams);
 struct SmallVariant { int bf16, kd, kh, nt; small_fn f; };
-#define SV(BF, ET, KD, KH, NT) {BF, KD, KH, NT, small_kernel<ET, KD, KH, NT>}
+#define SV(BF, ET, EH, KD, KH, NT) {BF, KD, KH, NT, small_kernel<ET, EH, KD, KH, NT>}
 static const SmallVariant kSmall[] = {
     // fp32: K-step 4; D <= 64, H <= 32; B <= 16 or 64
-    SV(0, EltF32, 4, 8, 1), SV(0, EltF32, 16, 8, 1), SV(0, EltF32, 4, 8, 4), SV(0, EltF32, 16, 8, 4),
-    // bf16: K-step 32; D <= 128, H <= 32
-    SV(1, EltBF16, 1, 1, 1), SV(1, EltBF16, 4, 1, 1), SV(1, EltBF16, 1, 1, 4), SV(1, EltBF16, 4, 1, 4),
+    SV(0, EltF32, EltF32, 4, 8, 1), SV(0, EltF32, EltF32, 16, 8, 1), SV(0, EltF32, EltF32, 4, 8, 4),
+    SV(0, EltF32, EltF32, 16, 8, 4),
+    // bf16 data (fp16 recurrent operands): K-step 32; D <= 128, H <= 32
+    SV(1, EltBF16, EltH16, 1, 1, 1), SV(1, EltBF16, EltH16, 4, 1, 1), SV(1, EltBF16, EltH16, 1, 1, 4),
+    SV(1, EltBF16, EltH16, 4, 1, 4),
 };
 #undef SV
 
@@ -256,7 +264,7 @@ hipError_t launch_small(const Dims& d, int kd, int nt, const void* x, const int3
     for (const SmallVariant& v : kSmall)
         if (v.bf16 == d.bf16 && v.kd == kd && v.nt == nt) f = v.f;
     if (!f) return hipErrorInvalidValue;
-    SmallParams p{x, lengths, W, U, b, h0, c0, out_h, out_c, seq, ws.meta, d.B, d.D, d.H, d.T, d.gru};
+    SmallParams p{x, lengths, W, U, b, h0, c0, out_h, out_c, seq, ws.meta, d.B, d.D, d.H, d.T, d.cell};
     hipLaunchKernelGGL(f, dim3(1), dim3(SM_THREADS), 0, s, p);
     return hipGetLastError();
 }

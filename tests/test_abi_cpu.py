@@ -155,7 +155,7 @@ def test_check_cell_args_gru():
     chk = ld.lstm_dyn_check_cell_args
     assert chk(B, D, H, T, ld.BF16, ld.CELL_GRU, *p, 0) == ld.OK
     assert chk(B, D, H, T, ld.BF16, ld.CELL_GRU, *p, seq) == ld.OK
-    assert chk(B, D, H, T, ld.BF16, 2, *p, 0) == ld.ERR_INVALID          # unknown cell
+    assert chk(B, D, H, T, ld.BF16, 3, *p, 0) == ld.ERR_INVALID          # unknown cell
     q = list(p)
     q[6] = 0                                      # c0 is ignored by the GRU and may be NULL
     assert chk(B, D, H, T, ld.BF16, ld.CELL_GRU, *q, seq) == ld.OK
@@ -182,3 +182,25 @@ def test_create_cell_rejects_unknown_cell_without_device():
     with pytest.raises(ld.LstmDynError) as e:
         ld.lstm_dyn_create_cell(4, 4, 4, 4, ld.F32, ld.PERSISTENT, 7)
     assert e.value.code == ld.ERR_INVALID
+
+
+def test_check_cell_args_rnn():
+    """The RNN's W [D][H], U [H][H], b [H]: sizes for the overlap checks."""
+    B, D, H, T = 3, 5, 7, 4
+    sizes = [B * T * D * 4, 4 * B, D * H * 4, H * H * 4, 4 * H, 4 * B * H, 4 * B * H,
+             4 * B * H, 4 * B * H]
+    p, at = [], 1 << 20
+    for s in sizes:
+        p.append(at)
+        at += s                                   # packed back to back: no slack between
+    chk = ld.lstm_dyn_check_cell_args
+    p = [v + (-v % 16) for v in p]                # keep the 16-byte alignment of x, W, U
+    assert chk(B, D, H, T, ld.F32, ld.CELL_RNN, *p, 0) == ld.OK
+    # with the LSTM's sizes (4x wider W and U) the same buffers overlap
+    assert chk(B, D, H, T, ld.F32, ld.CELL_LSTM, *p, 0) == ld.ERR_INVALID
+    q = list(p)
+    q[6] = 0                                      # c0 ignored
+    assert chk(B, D, H, T, ld.F32, ld.CELL_RNN, *q, 0) == ld.OK
+    q = list(p)
+    q[7] = q[4] + 4 * H - 4                       # out_h on the last bias float
+    assert chk(B, D, H, T, ld.F32, ld.CELL_RNN, *q, 0) == ld.ERR_INVALID

@@ -1,8 +1,8 @@
-"""Parity of the GRU cell (lstm_dyn_create_cell(..., LSTM_DYN_CELL_GRU), through
-the C ABI) with the fp64 oracle's GRU: final h and the output sequence, both
-execution modes, the small-case shapes and the five workload shapes with GRU
-weights.  Tolerances as for the LSTM: max-abs 1e-5 with fp32 x/W/U, 3e-3 with
-bf16."""
+"""Parity of the GRU and tanh RNN cells (lstm_dyn_create_cell, through the C
+ABI) with the fp64 oracle's GRU and RNN: final h and the output sequence, both
+execution modes, the small-case shapes and the five workload shapes with that
+cell's weights.  Tolerances as for the LSTM: max-abs 1e-5 with fp32 x/W/U,
+3e-3 with bf16."""
 import numpy as np
 import pytest
 
@@ -15,6 +15,12 @@ pytestmark = pytest.mark.gpu
 
 TOL = {workloads.F32: 1e-5, workloads.BF16: 3e-3}
 MODES = ["persistent", "per_step"]
+CELLS = ["gru", "rnn"]
+
+
+def oracle_of(inp, rows=None, seq=False):
+    f = oracle.forward_gru_inputs if inp.cell == "gru" else oracle.forward_rnn_inputs
+    return f(inp, rows=rows, seq=seq)
 
 
 def gru_device(inp, device="cuda"):
@@ -29,7 +35,7 @@ def gru_device(inp, device="cuda"):
 
 
 def gru_model(inp, mode):
-    return ld.LstmDyn(inp.B, inp.D, inp.H, inp.T, inp.dtype, mode, cell="gru")
+    return ld.LstmDyn(inp.B, inp.D, inp.H, inp.T, inp.dtype, mode, cell=inp.cell)
 
 
 def run_gru(inp, mode, model=None, seq=False):
@@ -59,15 +65,16 @@ SHAPES = [
 ]
 
 
+@pytest.mark.parametrize("cell", CELLS)
 @pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
-def test_gru_small_shapes(shape, mode):
+def test_cell_small_shapes(shape, mode, cell):
     B, D, H, T, dt = shape
-    inp = workloads.random_gru_case(500 + B + D + H, B, D, H, T, dtype=dt)
-    say(f"case gru {shape} {mode} lengths={inp.lengths.tolist()[:8]}")
+    inp = workloads.random_cell_case(cell, 500 + B + D + H, B, D, H, T, dtype=dt)
+    say(f"case {cell} {shape} {mode} lengths={inp.lengths.tolist()[:8]}")
     h, c, seq, m = run_gru(inp, mode, seq=True)
     h, c, seq = h.cpu().numpy(), c.cpu().numpy(), seq.cpu().numpy()
-    ho, so = oracle.forward_gru_inputs(inp, seq=True)
+    ho, so = oracle_of(inp, seq=True)
     tol = TOL[dt]
     eh, es = max_err(h, ho), max_err(seq, so)
     say(f"  max|dh|={eh:.3g} max|dseq|={es:.3g}")
@@ -81,13 +88,14 @@ def test_gru_small_shapes(shape, mode):
 SAMPLED = {"large2048_bf16"}
 
 
+@pytest.mark.parametrize("cell", CELLS)
 @pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("name", workloads.ORDER)
-def test_gru_workloads(name, mode):
+def test_cell_workloads(name, mode, cell):
     import torch
     w = workloads.WORKLOADS[name]
-    inp = workloads.gru_workload_inputs(name)
-    say(f"case gru workload {name} {mode}")
+    inp = workloads.cell_workload_inputs(cell, name)
+    say(f"case {cell} workload {name} {mode}")
     h, c, seq, m = run_gru(inp, mode, seq=True)
     assert m.query(ld.Q_STEPS_EXECUTED) == int(inp.lengths.max())
     if name in SAMPLED:
@@ -97,7 +105,7 @@ def test_gru_workloads(name, mode):
         idx = torch.tensor(rows, device=seq.device)
         seq_s = seq.index_select(0, idx).cpu().numpy()
         h_s = h.cpu().numpy()[rows]
-        ho, so = oracle.forward_gru_inputs(inp, rows=rows, seq=True)
+        ho, so = oracle_of(inp, rows=rows, seq=True)
         _check_padding_and_last(seq_s, h_s, L[rows])
         t = torch.arange(inp.T, device=seq.device)[None, :, None]
         Ld = torch.from_numpy(L).to(seq.device)[:, None, None]
@@ -105,13 +113,30 @@ def test_gru_workloads(name, mode):
         seq, h = seq_s, h_s
     else:
         seq, h = seq.cpu().numpy(), h.cpu().numpy()
-        ho, so = oracle.forward_gru_inputs(inp, seq=True)
+        ho, so = oracle_of(inp, seq=True)
         _check_padding_and_last(seq, h, inp.lengths)
     eh, es = max_err(h, ho), max_err(seq, so)
     say(f"  max|dh|={eh:.3g} max|dseq|={es:.3g} tol={w.tol}")
     assert eh <= w.tol and es <= w.tol
     assert int(torch.count_nonzero(c)) == 0
     m.close()
+
+
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_rnn_zero_weights_zeroes_state_exactly(mode, dt):
+    """W = U = 0 and b = 0: h' = tanh(0) = +0.0 after every step; rows of
+    length 0 keep h0 bit for bit; the sequence is zero everywhere."""
+    inp = workloads.random_cell_case("rnn", 46, 7, 9, 40, 12, dtype=dt)
+    inp.lengths[:] = [0, 1, 2, 5, 12, 7, 3]
+    inp.W[:] = 0
+    inp.U[:] = 0
+    inp.b[:] = 0
+    h, c, seq, m = run_gru(inp, mode, seq=True)
+    want = np.where(inp.lengths[:, None] > 0, np.float32(0), inp.h0).astype(np.float32)
+    assert np.array_equal(np.abs(h.cpu().numpy()), np.abs(want))
+    assert np.array_equal(h.cpu().numpy()[0].view(np.uint32), inp.h0[0].view(np.uint32))
+    assert int(seq.count_nonzero()) == 0
 
 
 @pytest.mark.parametrize("mode", MODES)
@@ -134,12 +159,13 @@ def test_gru_zero_weights_halves_state_exactly(mode, dt):
             assert np.array_equal(s[r, t], np.ldexp(inp.h0[r], -(t + 1)).astype(np.float32))
 
 
+@pytest.mark.parametrize("cell", CELLS)
 @pytest.mark.parametrize("mode", MODES)
-def test_gru_launches_c0_and_poisoned_padding(mode):
+def test_cell_launches_c0_and_poisoned_padding(mode, cell):
     """One pack launch more than the LSTM handle of the same sizes; c0 may be
     None or anything (ignored); NaN in x past each length reaches nothing."""
     import torch
-    inp = workloads.random_gru_case(43, 9, 20, 48, 14, dtype="bf16")
+    inp = workloads.random_cell_case(cell, 43, 9, 20, 48, 14, dtype="bf16")
     h1, c1, s1, m = run_gru(inp, mode, seq=True)
     n_gru = m.query(ld.Q_LAUNCHES_PER_FORWARD)
     lstm = workloads.random_case(43, 9, 20, 48, 14, dtype="bf16")
@@ -163,21 +189,25 @@ def test_gru_launches_c0_and_poisoned_padding(mode):
     assert torch.equal(h1, h3) and torch.equal(s1, s3)
 
 
-def test_gru_single_workgroup_kernel():
-    """H <= 32: the whole GRU forward is the pack launch plus one."""
-    inp = workloads.random_gru_case(44, 6, 12, 16, 10, dtype="f32")
+@pytest.mark.parametrize("cell", CELLS)
+def test_cell_single_workgroup_kernel(cell):
+    """H <= 32: the whole forward is the pack launch plus one."""
+    inp = workloads.random_cell_case(cell, 44, 6, 12, 16, 10, dtype="f32")
     h, c, m = run_gru(inp, "persistent")
     assert m.query(ld.Q_GROUPS) == 1 and m.query(ld.Q_LAUNCHES_PER_FORWARD) == 2
-    ho = oracle.forward_gru_inputs(inp)
+    ho = oracle_of(inp)
     assert max_err(h.cpu().numpy(), ho) <= 1e-5
 
 
-def test_gru_and_lstm_handles_interleave():
-    """A GRU handle and an LSTM handle on one stream do not disturb each
-    other's results (separate workspaces)."""
+def test_cell_handles_interleave():
+    """GRU, RNN and LSTM handles on one stream do not disturb each other's
+    results (separate workspaces)."""
     import torch
     from tests.gpu_util import to_device
     g = workloads.random_gru_case(45, 11, 30, 70, 9, dtype="bf16")
+    r = workloads.random_cell_case("rnn", 45, 11, 30, 70, 9, dtype="bf16")
+    mr = gru_model(r, "persistent")
+    hr1, _ = mr.forward(*gru_device(r))
     l = workloads.random_case(45, 11, 30, 70, 9, dtype="bf16")
     mg, ml = gru_model(g, "persistent"), ld.LstmDyn(l.B, l.D, l.H, l.T, l.dtype, "persistent")
     dg, dl = gru_device(g), to_device(l)
@@ -187,5 +217,27 @@ def test_gru_and_lstm_handles_interleave():
     torch.cuda.synchronize()
     assert torch.equal(hg1, hg2)
     assert max_err(hg1.cpu().numpy(), oracle.forward_gru_inputs(g)) <= 3e-3
+    assert max_err(hr1.cpu().numpy(), oracle.forward_rnn_inputs(r)) <= 3e-3
     ho, co = oracle.forward_inputs(l)
     assert max_err(hl1.cpu().numpy(), ho) <= 3e-3 and max_err(cl1.cpu().numpy(), co) <= 3e-3
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_recurrent_operand_keeps_fp16_precision(mode):
+    """With bf16 data the recurrent product takes h in fp16, not bf16: RNN with
+    W = 0, b = 0, U = diag(1/2) and h0 = 1 + 2^-10 (exact in fp16; bf16 rounds
+    it to 1) gives after one step tanh((1 + 2^-10) / 2); a bf16 operand would
+    give tanh(1/2), 3.9e-4 away."""
+    inp = workloads.random_cell_case("rnn", 47, 3, 8, 64, 4, dtype="bf16")
+    inp.lengths[:] = 1
+    inp.W[:] = 0
+    inp.b[:] = 0
+    inp.U[:] = 0
+    half = workloads.f32_to_bf16_bits(np.array([0.5], np.float32))[0]
+    inp.U[np.arange(64), np.arange(64)] = half
+    inp.h0[:] = np.float32(1 + 2.0 ** -10)
+    h, c, m = run_gru(inp, mode)
+    want = np.tanh((1 + 2.0 ** -10) / 2)
+    err = float(np.max(np.abs(h.cpu().numpy().astype(np.float64) - want)))
+    say(f"  |h - tanh(v/2)| = {err:.3g}")
+    assert err <= 2e-6

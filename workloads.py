@@ -196,19 +196,27 @@ class CellInputs:
 
 GruInputs = CellInputs
 _CELL_COLS = {"gru": (3, 6), "rnn": (1, 1)}   # (columns of W and U, bias entries) per hidden unit
+# Variance of W and U times H: 1 for the GRU (as for the LSTM); 1/3 for the tanh
+# RNN, the variance of the uniform(-1/sqrt(H), 1/sqrt(H)) initialisation that
+# torch.nn.RNN uses by default.  At 1 the plain tanh recurrence sits at the edge
+# of chaos (recurrent gain about 1), where any rounding of h, bf16 or fp32,
+# grows with the step count instead of dying out.
+_CELL_WVAR = {"gru": 1.0, "rnn": 1.0 / 3.0}
 
 
 def make_cell_inputs(cell: str, B: int, D: int, H: int, T: int, dtype: str, lengths_spec: tuple,
                      seed: int, force: Optional[tuple] = None, state_var: float = 0.0,
                      bias_var: float = 0.1) -> CellInputs:
     """GRU or RNN batch.  Draw order: lengths, x, W, U, b, h0 (h0 only when
-    ``state_var`` > 0); W, U ~ N(0, 1/H), biases ~ N(0, bias_var)."""
+    ``state_var`` > 0); W, U ~ N(0, 1/H) (GRU) or N(0, 1/(3H)) (RNN),
+    biases ~ N(0, bias_var)."""
     g, nb = _CELL_COLS[cell]
+    ws = np.sqrt(_CELL_WVAR[cell] / H)
     rng = np.random.default_rng(seed)
     L = draw_lengths(rng, B, lengths_spec)
     x = rng.standard_normal((B, T, D)).astype(np.float32)
-    W = (rng.standard_normal((D, g * H)) * (1.0 / np.sqrt(H))).astype(np.float32)
-    U = (rng.standard_normal((H, g * H)) * (1.0 / np.sqrt(H))).astype(np.float32)
+    W = (rng.standard_normal((D, g * H)) * ws).astype(np.float32)
+    U = (rng.standard_normal((H, g * H)) * ws).astype(np.float32)
     b = (rng.standard_normal(nb * H) * np.sqrt(bias_var)).astype(np.float32)
     if state_var > 0:
         h0 = (rng.standard_normal((B, H)) * np.sqrt(state_var)).astype(np.float32)
