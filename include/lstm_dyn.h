@@ -22,8 +22,10 @@
  *     h0, c0   [B][H]          fp32
  *     out_h, out_c [B][H]      fp32 (written)
  * Gate blocks along 4H are i = [0, H), f = [H, 2H), g = [2H, 3H), o = [3H, 4H).
- * With bf16 data, every product is formed from bf16 operands and accumulated
- * in fp32; the state (h, c) is kept in fp32.
+ * With bf16 data, x W is formed from bf16 operands; the recurrent product h U
+ * from fp16 operands (U widened from bf16, exact for 2^-14 <= |U| <= 65504;
+ * h rounded to fp16, so h0 entries must lie within +-65504); every product
+ * is accumulated in fp32 and the state (h, c) is kept in fp32.
  *
  * Threading: a handle may be used from one host thread at a time, and one
  * forward may be in flight per handle.  Forward calls only enqueue work on the
