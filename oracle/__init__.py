@@ -72,6 +72,9 @@ class _Lib:
         lib.lstm_oracle_forward_rnn.argtypes = [ctypes.c_int] * 4 + [P] * 9 + [
             ctypes.c_int, ctypes.c_int, P, P]
         lib.lstm_oracle_forward_rnn.restype = ctypes.c_int
+        lib.lstm_oracle_forward_stop.argtypes = [ctypes.c_int] * 4 + [P] * 6 + [ctypes.c_int, P,
+                                                 ctypes.c_double] + [P] * 7 + [ctypes.c_int]
+        lib.lstm_oracle_forward_stop.restype = ctypes.c_int
         lib.lstm_oracle_max_threads.argtypes = []
         lib.lstm_oracle_max_threads.restype = ctypes.c_int
         self.lib = lib
@@ -241,6 +244,57 @@ def forward_rnn(x, lengths, W, U, b, h0, literal: bool = False, threads: int = 0
     if return_steps:
         out = (*out, int(steps.value))
     return out[0] if len(out) == 1 else out
+
+
+_CELL_IDS = {"lstm": 0, "gru": 1, "rnn": 2}
+
+
+def forward_stop(x, lengths, W, U, b, h0, c0, v, c_stop, cell: str = "lstm", b_hh=None,
+                 threads: int = 0, return_seq: bool = False, _lib_override=None):
+    """The loop whose termination is computed from the state: row b runs step
+    t while t < L[b] (a cap) and it has not terminated; it terminates after a
+    step that leaves its halting score v . h + c_stop positive; the loop ends
+    at the first step with no running row.
+
+    Returns (h, c, steps, iters) -- float64 [B, H] twice, int32 [B] steps each
+    row ran, the loop iterations -- and the output sequence [B, T, H] after
+    them with ``return_seq``.  Layouts as for ``forward`` (cell "lstm"),
+    ``forward_gru`` (b = b_ih, ``b_hh``) or ``forward_rnn``; v float [H];
+    c0 is carried unchanged for GRU and RNN.
+    """
+    lib = (_lib_override or _load()).lib
+    x, W, U, b, v = map(_f32, (x, W, U, b, v))
+    bhh = _f32(b_hh) if b_hh is not None else None
+    h0 = np.ascontiguousarray(h0, dtype=np.float64)
+    c0 = np.ascontiguousarray(c0, dtype=np.float64)
+    L = np.ascontiguousarray(lengths, dtype=np.int32)
+    B, T, D = x.shape
+    H = U.shape[0]
+    g = {"lstm": 4, "gru": 3, "rnn": 1}[cell]
+    if W.shape != (D, g * H) or U.shape != (H, g * H) or v.shape != (H,):
+        raise OracleError("weight shapes do not match x, U and the cell")
+    if L.shape != (B,) or h0.shape != (B, H) or c0.shape != (B, H):
+        raise OracleError("lengths/state shapes do not match x")
+    if cell == "gru" and (bhh is None or bhh.shape != (3 * H,)):
+        raise OracleError("the GRU needs b_hh [3H]")
+    h = np.empty((B, H), np.float64)
+    c = np.empty((B, H), np.float64)
+    steps = np.zeros(B, np.int32)
+    iters = ctypes.c_int64(0)
+    seq = np.full((B, T, H), np.nan) if return_seq else None
+    rc = lib.lstm_oracle_forward_stop(B, T, D, H, x.ctypes.data, L.ctypes.data, W.ctypes.data,
+                                      U.ctypes.data, b.ctypes.data,
+                                      bhh.ctypes.data if bhh is not None else None,
+                                      _CELL_IDS[cell], v.ctypes.data, float(c_stop),
+                                      h0.ctypes.data, c0.ctypes.data, h.ctypes.data, c.ctypes.data,
+                                      steps.ctypes.data, ctypes.byref(iters),
+                                      seq.ctypes.data if seq is not None else None, int(threads))
+    if rc == BAD_LENGTHS:
+        raise OracleError("sequence lengths must lie in [0, T]")
+    if rc != OK:
+        raise OracleError(f"oracle failed with code {rc}")
+    out = (h, c, steps, int(iters.value))
+    return (*out, seq) if return_seq else out
 
 
 def forward_inputs(inp, rows=None, literal: bool = False, threads: int = 0, seq: bool = False):

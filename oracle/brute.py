@@ -154,3 +154,34 @@ def rnn_per_sequence(x, lengths, W, U, b, h0):
         hs.append(h)
         seqs.append(steps + [[0.0] * H for _ in range(T - n)])
     return hs, seqs
+
+
+def stop_per_sequence(x, lengths, W, U, b, h0, c0, v, c_stop, cell="lstm", b_hh=None):
+    """Each sequence run alone, one step at a time, until its cap L[r] or the
+    first step after which v . h + c_stop > 0.  Returns (hs, cs, steps):
+    final states as lists and the number of steps each sequence ran."""
+    Wl = [list(map(float, row)) for row in W]
+    Ul = [list(map(float, row)) for row in U]
+    bl = list(map(float, b))
+    vl = list(map(float, v))
+    bhl = list(map(float, b_hh)) if b_hh is not None else None
+    hs, cs, steps = [], [], []
+    for r in range(len(lengths)):
+        h = [float(a) for a in h0[r]]
+        c = [float(a) for a in c0[r]]
+        n = 0
+        for t in range(int(lengths[r])):
+            xt = [list(map(float, x[r][t]))]
+            if cell == "lstm":
+                h, c = run_sequence(xt, Wl, Ul, bl, h, c)
+            elif cell == "gru":
+                h = run_sequence_gru(xt, Wl, Ul, bl, bhl, h)
+            else:
+                h = run_sequence_rnn(xt, Wl, Ul, bl, h)
+            n = t + 1
+            if sum(vk * hk for vk, hk in zip(vl, h)) + float(c_stop) > 0.0:
+                break
+        hs.append(h)
+        cs.append(c)
+        steps.append(n)
+    return hs, cs, steps

@@ -299,6 +299,108 @@ int lstm_oracle_forward_rnn(int B, int T, int D, int H, const float* x, const in
                         steps_out, seq_out, CELL_RNN, NULL);
 }
 
+/*
+ * lstm_oracle_forward_stop: the loop with its termination computed from the
+ * state.  The paper's decoders (beam search and seq2seq, Appendix D) leave the
+ * loop once every candidate sequence has terminated; here a row terminates
+ * when a linear read-out of its state, the halting score
+ *
+ *   s = (sum over k of v[k] h[k]) + c_stop,      summed in increasing k,
+ *
+ * is positive after one of its steps.  L[b] caps the steps of row b (x holds
+ * data for t < L[b]).  At step t a row is running if t < L[b] and it has not
+ * terminated; the loop stops at the first step with no running row.  Running
+ * rows take the cell's new state, the others keep theirs.
+ *   cell        : CELL_LSTM, CELL_GRU (bias = b_ih, bhh = b_hh) or CELL_RNN
+ *   v [H], c_stop: the read-out
+ *   steps_out   : [B] int32, the steps row b ran
+ *   iters_out   : loop iterations run (= the largest entry of steps_out)
+ *   seq_out     : if non-NULL, [B][T][H] hidden state after each step a row
+ *                 ran, zero after its last
+ * Returns ORACLE_OK or an error code.
+ */
+int lstm_oracle_forward_stop(int B, int T, int D, int H, const float* x, const int32_t* L,
+                             const float* W, const float* U, const float* bias, const float* bhh,
+                             int cell, const float* v, double c_stop, const double* h0,
+                             const double* c0, double* h_out, double* c_out, int32_t* steps_out,
+                             int64_t* iters_out, double* seq_out, int nthreads) {
+    if (B <= 0 || T < 0 || D <= 0 || H <= 0 || !x || !L || !W || !U || !bias || !v || !h0 ||
+        !c0 || !h_out || !c_out || !steps_out || (cell == CELL_GRU && !bhh))
+        return ORACLE_BAD_ARGS;
+    if (cell != CELL_LSTM && cell != CELL_GRU && cell != CELL_RNN) return ORACLE_BAD_ARGS;
+    int max_len = 0;
+    for (int b = 0; b < B; ++b) {
+        if (L[b] < 0 || L[b] > T) return ORACLE_BAD_LENGTHS;
+        if (L[b] > max_len) max_len = L[b];
+    }
+    const size_t BH = (size_t)B * H;
+    double* h = (double*)malloc(BH * sizeof(double));
+    double* c = (double*)malloc(BH * sizeof(double));
+    double* hn = (double*)malloc(BH * sizeof(double));
+    double* cn = (double*)malloc(BH * sizeof(double));
+    unsigned char* done = (unsigned char*)calloc((size_t)B, 1);
+    int nt = 1;
+#ifdef _OPENMP
+    nt = nthreads > 0 ? nthreads : omp_get_max_threads();
+#endif
+    double* zs = (double*)malloc((size_t)nt * 6 * H * sizeof(double));
+    if (!h || !c || !hn || !cn || !done || !zs) {
+        free(h); free(c); free(hn); free(cn); free(done); free(zs);
+        return ORACLE_NOMEM;
+    }
+    memcpy(h, h0, BH * sizeof(double));          /* initial state */
+    memcpy(c, c0, BH * sizeof(double));
+    for (int b = 0; b < B; ++b) steps_out[b] = 0;
+    if (seq_out) memset(seq_out, 0, (size_t)T * BH * sizeof(double));  /* zero after each row's last step */
+    int64_t iters = 0;
+    for (int t = 0; t < max_len; t++) {
+        int any = 0;                             /* leave the loop once no row runs */
+        for (int b = 0; b < B; ++b) any |= (t < L[b]) && !done[b];
+        if (!any) break;
+#ifdef _OPENMP
+#pragma omp parallel for num_threads(nt) schedule(dynamic, 1)
+#endif
+        for (int b = 0; b < B; ++b) {
+            if (!(t < L[b]) || done[b]) continue;
+            int tid = 0;
+#ifdef _OPENMP
+            tid = omp_get_thread_num();
+#endif
+            double* z = zs + (size_t)tid * 6 * H;
+            const float* xrow = x + ((size_t)b * T + t) * D;
+            double* hb = h + (size_t)b * H;
+            if (cell == CELL_GRU) {
+                gru_cell_row(D, H, xrow, W, U, bias, bhh, hb, z, z + 3 * H, hn + (size_t)b * H);
+                memcpy(cn + (size_t)b * H, c + (size_t)b * H, (size_t)H * sizeof(double));
+            } else if (cell == CELL_RNN) {
+                rnn_cell_row(D, H, xrow, W, U, bias, hb, z, hn + (size_t)b * H);
+                memcpy(cn + (size_t)b * H, c + (size_t)b * H, (size_t)H * sizeof(double));
+            } else {
+                lstm_cell_row(D, H, xrow, W, U, bias, hb, c + (size_t)b * H, z, hn + (size_t)b * H,
+                              cn + (size_t)b * H);
+            }
+        }
+        for (int b = 0; b < B; ++b) {            /* commit the running rows, then test them */
+            if (!(t < L[b]) || done[b]) continue;
+            memcpy(h + (size_t)b * H, hn + (size_t)b * H, (size_t)H * sizeof(double));
+            memcpy(c + (size_t)b * H, cn + (size_t)b * H, (size_t)H * sizeof(double));
+            steps_out[b] = t + 1;
+            if (seq_out)                         /* the row's output at step t */
+                memcpy(&seq_out[((size_t)b * T + t) * H], &h[(size_t)b * H], (size_t)H * sizeof(double));
+            double score = 0.0;
+            for (int k = 0; k < H; ++k) score += (double)v[k] * h[(size_t)b * H + k];
+            score += c_stop;
+            if (score > 0.0) done[b] = 1;       /* terminated after this step */
+        }
+        iters = t + 1;
+    }
+    memcpy(h_out, h, BH * sizeof(double));
+    memcpy(c_out, c, BH * sizeof(double));
+    if (iters_out) *iters_out = iters;
+    free(h); free(c); free(hn); free(cn); free(done); free(zs);
+    return ORACLE_OK;
+}
+
 /* Number of OpenMP threads a call with nthreads <= 0 would use. */
 int lstm_oracle_max_threads(void) {
 #ifdef _OPENMP

@@ -14,6 +14,7 @@ import math
 import numpy as np
 
 import workloads
+import oracle
 from oracle import brute
 
 
@@ -577,4 +578,154 @@ RNN_PINS = [
     rpin_length_zero_and_poisoned_padding,
     rpin_brute_force,
     rpin_torch_rnn,
+]
+
+
+# ---------------------------------------------------------------------------
+# The loop with termination computed from the state (halting score
+# v . h + c_stop > 0 after a step ends a row; lengths are caps).  Each pin
+# takes a callable with the signature of ``oracle.forward_stop``.
+
+def _stop_case(seed, B, D, H, T, lo=0):
+    inp = workloads.random_case(seed, B, D, H, T, lo=lo)
+    x, W, U = inp.as_f32()
+    return x.copy(), inp.lengths.copy(), W, U, inp.b.copy(), inp.h0.copy(), inp.c0.copy()
+
+
+def spin_never_stopping_equals_plain_loop(fwd):
+    """v = 0, c_stop < 0 (and c_stop = 0: the score must be positive): no row
+    ever terminates, so the result is the plain masked loop's bit for bit,
+    every row runs to its cap and the loop runs max(L) iterations."""
+    x, L, W, U, b, h0, c0 = _stop_case(70, 6, 5, 7, 9)
+    h, c, steps, iters = fwd(x, L, W, U, b, h0, c0, np.zeros(7, np.float32), -1.0)
+    hp, cp = oracle.forward(x, L, W, U, b, h0, c0)
+    assert _bits_equal(h, hp) and _bits_equal(c, cp)
+    assert np.array_equal(steps, L) and iters == int(L.max())
+    # a score of exactly zero does not end a row (the rule is score > 0)
+    h0s, _, steps0, _ = fwd(x, L, W, U, b, h0, c0, np.zeros(7, np.float32), 0.0)
+    assert np.array_equal(steps0, L) and _bits_equal(h0s, hp)
+
+
+def spin_always_stopping_runs_one_step(fwd):
+    """v = 0, c_stop > 0: every row terminates after its first step: steps =
+    min(L, 1), the state is the plain loop's with lengths min(L, 1), and the
+    loop runs one iteration (none if every cap is 0)."""
+    x, L, W, U, b, h0, c0 = _stop_case(71, 6, 5, 7, 9)
+    L[2] = 0
+    h, c, steps, iters = fwd(x, L, W, U, b, h0, c0, np.zeros(7, np.float32), 0.5)
+    L1 = np.minimum(L, 1)
+    hp, cp = oracle.forward(x, L1, W, U, b, h0, c0)
+    assert _bits_equal(h, hp) and _bits_equal(c, cp)
+    assert np.array_equal(steps, L1) and iters == 1
+    _, _, steps0, iters0 = fwd(x, np.zeros_like(L), W, U, b, h0, c0, np.zeros(7, np.float32), 0.5)
+    assert iters0 == 0 and not steps0.any()
+
+
+def spin_zero_weights_stopping_step(fwd):
+    """W = U = 0, b = 0: every gate is 1/2, so c_t = 2^-t c0 and h_t = tanh(c_t)/2
+    exactly.  With v = -e_0 and c_stop = thr a row terminates after the first
+    step t >= 1 with tanh(2^-t c0[0])/2 < thr; the step is found by a plain
+    Python loop over t and thresholds sit between consecutive values (no ties)."""
+    x, L, W, U, b, h0, c0 = _stop_case(72, 5, 3, 4, 12)
+    W[:] = 0
+    U[:] = 0
+    b[:] = 0
+    L[:] = [12, 12, 3, 12, 0]
+    c0[:, 0] = [6.0, 3.0, 6.0, -2.0, 5.0]
+    v = np.zeros(4, np.float32)
+    v[0] = -1.0
+    thr = 0.5 * (0.5 * math.tanh(6.0 / 2 ** 4) + 0.5 * math.tanh(6.0 / 2 ** 5))  # between t = 4 and 5
+    h, c, steps, iters = fwd(x, L, W, U, b, h0, c0, v, thr)
+    want = []
+    for r in range(5):
+        n = 0
+        for t in range(1, int(L[r]) + 1):
+            n = t
+            if -0.5 * math.tanh(float(c0[r, 0]) / 2 ** t) + thr > 0:
+                break
+        want.append(n)
+    assert steps.tolist() == want, (steps.tolist(), want)
+    assert want[0] == 5 and want[2] == 3 and want[3] == 1 and want[4] == 0
+    assert iters == max(want)
+    for r in range(5):
+        assert _bits_equal(c[r], np.ldexp(c0[r].astype(np.float64), -want[r]))
+
+
+def spin_consistent_with_plain_loop_trace(fwd):
+    """A random read-out that ends most rows early: (1) the state equals the
+    plain loop run with lengths = steps, bit for bit; (2) along the plain loop's
+    output sequence (caps as lengths) the halting score is <= 0 after every
+    step before a row's last and > 0 after its last unless it reached its cap;
+    (3) the loop ran max(steps) iterations."""
+    x, L, W, U, b, h0, c0 = _stop_case(73, 12, 6, 10, 16, lo=8)
+    rng = np.random.default_rng(74)
+    v = rng.standard_normal(10).astype(np.float32)
+    h, c, steps, iters = fwd(x, L, W, U, b, h0, c0, v, -0.6)
+    assert (steps < L).sum() >= 4                        # the read-out does end rows early
+    hp, cp = oracle.forward(x, steps, W, U, b, h0, c0)
+    assert _bits_equal(h, hp) and _bits_equal(c, cp)
+    _, _, seq = oracle.forward(x, L, W, U, b, h0, c0, return_seq=True)
+    score = seq @ v.astype(np.float64) - 0.6            # [B, T]
+    for r in range(len(L)):
+        n = int(steps[r])
+        assert np.all(score[r, :n - 1] <= 1e-12), r
+        if n < L[r]:
+            assert n >= 1 and score[r, n - 1] > -1e-12, r
+    assert iters == int(steps.max())
+
+
+def spin_brute_force(fwd, seeds=range(12)):
+    """Agreement with each sequence run alone in pure Python under the same
+    stopping rule, for the three cells: steps exactly, states <= 1e-12."""
+    for s in seeds:
+        rng = np.random.default_rng(7300 + s)
+        B, D, H, T = (int(rng.integers(1, 5)), int(rng.integers(1, 4)), int(rng.integers(1, 4)),
+                      int(rng.integers(1, 8)))
+        cell = ("lstm", "gru", "rnn")[s % 3]
+        g = {"lstm": 4, "gru": 3, "rnn": 1}[cell]
+        x, L, _, _, _, h0, c0 = _stop_case(8300 + s, B, D, H, T)
+        W = (rng.standard_normal((D, g * H)) / math.sqrt(H)).astype(np.float32)
+        U = (rng.standard_normal((H, g * H)) / math.sqrt(H)).astype(np.float32)
+        b = (rng.standard_normal(g * H) * 0.5).astype(np.float32)
+        bhh = (rng.standard_normal(3 * H) * 0.5).astype(np.float32) if cell == "gru" else None
+        if cell != "lstm":
+            c0 = np.zeros_like(c0)
+        v = rng.standard_normal(H).astype(np.float32)
+        cs = float(rng.standard_normal() * 0.3)
+        h, c, steps, iters = fwd(x, L, W, U, b, h0, c0, v, cs, cell=cell, b_hh=bhh)
+        hb, cb, sb = brute.stop_per_sequence(x, L, W, U, b, h0, c0, v, cs, cell=cell, b_hh=bhh)
+        assert steps.tolist() == sb, (s, cell, steps.tolist(), sb)
+        assert np.max(np.abs(h - np.array(hb))) <= 1e-12, (s, cell)
+        assert np.max(np.abs(c - np.array(cb))) <= 1e-12, (s, cell)
+        assert iters == (max(sb) if sb else 0)
+
+
+def spin_other_cells_match_their_plain_loops(fwd):
+    """GRU and RNN under the stopping rule equal their plain loops run with
+    lengths = steps, bit for bit, and their output sequences agree on the
+    steps run (zero after)."""
+    for cell in ("gru", "rnn"):
+        inp = workloads.random_cell_case(cell, 75, 8, 5, 9, 12, lo=6)
+        x, W, U = inp.as_f32()
+        rng = np.random.default_rng(76)
+        v = rng.standard_normal(9).astype(np.float32)
+        c0 = np.zeros_like(inp.h0)
+        bias = inp.b_ih if cell == "gru" else inp.b
+        h, c, steps, iters, seq = fwd(x, inp.lengths, W, U, bias, inp.h0, c0, v, -0.3, cell=cell,
+                                      b_hh=inp.b_hh if cell == "gru" else None, return_seq=True)
+        assert (steps < inp.lengths).any(), cell
+        if cell == "gru":
+            hp, sp = oracle.forward_gru(x, steps, W, U, inp.b_ih, inp.b_hh, inp.h0, return_seq=True)
+        else:
+            hp, sp = oracle.forward_rnn(x, steps, W, U, inp.b, inp.h0, return_seq=True)
+        assert _bits_equal(h, hp) and _bits_equal(seq, sp), cell
+
+
+STOP_PINS = [
+    spin_never_stopping_equals_plain_loop,
+    spin_always_stopping_runs_one_step,
+    spin_zero_weights_stopping_step,
+    spin_consistent_with_plain_loop_trace,
+    spin_brute_force,
+    spin_other_cells_match_their_plain_loops,
 ]

@@ -89,3 +89,8 @@ def test_gru_pin(pin):
 @pytest.mark.parametrize("pin", oracle_pins.RNN_PINS, ids=lambda f: f.__name__)
 def test_rnn_pin(pin):
     pin(oracle.forward_rnn)
+
+
+@pytest.mark.parametrize("pin", oracle_pins.STOP_PINS, ids=lambda f: f.__name__)
+def test_stop_pin(pin):
+    pin(oracle.forward_stop)

@@ -118,3 +118,41 @@ def test_rnn_pins_catch_planted_mistake(name, tmp_path):
             caught.append(pin.__name__)
             break
     assert caught, f"no pin caught mutant {name}"
+
+
+STOP_MUTANTS = {
+    # the score of the state before a step decides whether the row runs it
+    "stop_tested_before_the_step": [("            if (!(t < L[b]) || done[b]) continue;\n            int tid = 0;",
+                                     "            if (!(t < L[b]) || done[b]) continue;\n            { double s0 = c_stop; for (int k = 0; k < H; ++k) s0 += (double)v[k] * h[(size_t)b * H + k]; if (t > 0 && s0 > 0.0) { done[b] = 1; continue; } }\n            int tid = 0;"),
+                                    ("if (score > 0.0) done[b] = 1;", "(void)score;")],
+    "stop_on_zero_score": ("if (score > 0.0) done[b] = 1;", "if (score >= 0.0) done[b] = 1;"),
+    "stop_without_bias": ("            score += c_stop;\n", ""),
+    "loop_ends_when_any_row_ends": ("for (int b = 0; b < B; ++b) any |= (t < L[b]) && !done[b];",
+                                    "for (int b = 0; b < B; ++b) any |= 1; for (int b = 0; b < B; ++b) if (done[b]) any = 0;"),
+    "terminated_rows_keep_running": ("            if (!(t < L[b]) || done[b]) continue;\n            memcpy(h + (size_t)b * H",
+                                     "            if (!(t < L[b])) continue;\n            memcpy(h + (size_t)b * H"),
+    "steps_count_from_zero": ("            steps_out[b] = t + 1;", "            steps_out[b] = t;"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(STOP_MUTANTS))
+def test_stop_pins_catch_planted_mistake(name, tmp_path):
+    edits = STOP_MUTANTS[name]
+    src = oracle.source_text()
+    for old, new in (edits if isinstance(edits, list) else [edits]):
+        assert src.count(old) == 1, f"mutation anchor for {name} not found exactly once"
+        src = src.replace(old, new)
+    lib = oracle.compile_variant(src, str(tmp_path / f"mut_{name}.so"))
+    low = oracle._Lib(lib)
+
+    def fwd(*args, **kw):
+        return oracle.forward_stop(*args, _lib_override=low, **kw)
+    caught = []
+    for pin in oracle_pins.STOP_PINS:
+        try:
+            with np.errstate(all="ignore"):
+                pin(fwd)
+        except (AssertionError, oracle.OracleError):
+            caught.append(pin.__name__)
+            break
+    assert caught, f"no pin caught mutant {name}"
