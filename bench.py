@@ -162,6 +162,8 @@ def main():
                     help="skip timing the forward that also writes the output sequence")
     ap.add_argument("--no-cells", action="store_true",
                     help="skip timing the GRU and RNN cells on the same workload shape")
+    ap.add_argument("--no-stop", action="store_true",
+                    help="skip timing the loop with termination computed from the state")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain copy of known size (for scaling HBM counters)")
     args = ap.parse_args()
@@ -243,6 +245,30 @@ def main():
             cm.close()
             del cdev, cin
 
+    stop_leg = None
+    if not args.no_stop:
+        # the same forward with a halting read-out v . h + c > 0 ending rows
+        # before their caps (v ~ N(0, 1/H) from seed 900, c = -0.5); the
+        # loop leaves on the device once no row runs
+        _log("persistent path, termination from the state")
+        v = (np.random.default_rng(900).standard_normal(w.H) / np.sqrt(w.H)).astype(np.float32)
+        vd = torch.from_numpy(v).cuda()
+        steps = torch.empty((w.B,), dtype=torch.int32, device="cuda")
+        for _ in range(2):
+            model.forward_stop(*dev[:6], dev[6], vd, -0.5, out_h=out[0], out_c=out[1], out_steps=steps)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(5):
+            model.forward_stop(*dev[:6], dev[6], vd, -0.5, out_h=out[0], out_c=out[1], out_steps=steps)
+        torch.cuda.synchronize()
+        t_stop = (time.perf_counter() - t0) / 5
+        st = steps.cpu().numpy()
+        stop_leg = {"ms_per_forward": t_stop * 1e3, "stop_c": -0.5,
+                    "loop_steps_run": model.query(ld.Q_STEPS_EXECUTED), "loop_bound": max_len,
+                    "rows_ended_early": int((st < inp.lengths).sum()),
+                    "valid_seq_steps_run": int(st.sum()),
+                    "launches_per_forward": model.query(ld.Q_LAUNCHES_PER_FORWARD)}
+
     per_step = None
     if args.per_step_reps > 0:
         _log("per-step path")
@@ -308,6 +334,7 @@ def main():
         "wall_ms_per_step": t_wall * 1e3,
         "per_step_path": per_step,
         "forward_seq": seq_leg,
+        "forward_stop": stop_leg,
         "cells": cell_legs,
         "tiny_f32": tiny,
     }

@@ -183,6 +183,36 @@ int lstm_dyn_forward_seq(lstm_dyn_t* h, const void* x, const int32_t* lengths, c
                          const void* U, const float* b, const float* h0, const float* c0,
                          float* out_h, float* out_c, float* out_seq, void* stream);
 
+/*
+ * lstm_dyn_forward_stop: the loop with its termination computed on the device
+ * from the state.  The paper's decoders (beam search, seq2seq; Appendix D)
+ * leave their loop once every candidate sequence has terminated; here a
+ * sequence terminates when a linear read-out of its hidden state, the halting
+ * score
+ *     s = v . h + stop_c        (v = stop_v [H] fp32, device memory),
+ * is positive after one of its steps.  lengths[b] is now a cap: row b runs
+ * step t while t < L[b] and it has not terminated; a terminated row keeps its
+ * state.  The loop ends on the device at the first step in which no row runs
+ * (lstm_dyn_query(LSTM_DYN_Q_STEPS_EXECUTED) gives the steps in which some
+ * row ran).
+ *     out_steps [B] int32 (written): the steps row b ran (<= its clamped cap).
+ *     out_seq: NULL, or the output sequence as in lstm_dyn_forward_seq, zero
+ *     from step out_steps[b] on.
+ * The score is formed from h in the precision of the recurrent operand (fp16
+ * with bf16 data, fp32 with fp32 data) and accumulated in fp32, so a score
+ * within rounding of zero may be decided either way.  In per-step mode the
+ * host reads the number of running rows after every step (the eager form of
+ * the loop condition).  stop_v is 4-byte aligned and may not overlap an
+ * output; out_steps is 4-byte aligned and may not overlap any argument; NaN
+ * stop_c is ERR_INVALID.  Returns as lstm_dyn_forward, or ERR_UNSUPPORTED if
+ * the persistent variant with the halting score does not fit the device for
+ * this handle's sizes.
+ */
+int lstm_dyn_forward_stop(lstm_dyn_t* h, const void* x, const int32_t* lengths, const void* W,
+                          const void* U, const float* b, const float* h0, const float* c0,
+                          const float* stop_v, float stop_c, float* out_h, float* out_c,
+                          int32_t* out_steps, float* out_seq, void* stream);
+
 /* Free the handle and its workspace (synchronises the device).  NULL is a no-op. */
 int lstm_dyn_destroy(lstm_dyn_t* h);
 
@@ -238,6 +268,14 @@ int lstm_dyn_check_cell_args(int B, int D, int H, int T_max, int dtype, int cell
                              const int32_t* lengths, const void* W, const void* U, const float* b,
                              const float* h0, const float* c0, const float* out_h,
                              const float* out_c, const float* out_seq);
+
+/* The checks of lstm_dyn_forward_stop for a handle of cell `cell` (out_seq
+ * may be NULL).  Returns LSTM_DYN_OK or ERR_INVALID. */
+int lstm_dyn_check_stop_args(int B, int D, int H, int T_max, int dtype, int cell, const void* x,
+                             const int32_t* lengths, const void* W, const void* U, const float* b,
+                             const float* h0, const float* c0, const float* stop_v,
+                             const float* out_h, const float* out_c, const int32_t* out_steps,
+                             const float* out_seq);
 
 #ifdef __cplusplus
 }

@@ -20,6 +20,7 @@ __all__ = [
     "lstm_dyn_strerror", "lstm_dyn_plan", "lstm_dyn_check_args", "lstm_dyn_set_option",
     "lstm_dyn_step_trace", "lstm_dyn_forward_seq", "lstm_dyn_check_seq_args",
     "lstm_dyn_create_cell", "lstm_dyn_check_cell_args", "CELL_LSTM", "CELL_GRU", "CELL_RNN",
+    "lstm_dyn_forward_stop", "lstm_dyn_check_stop_args",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -75,6 +76,10 @@ def _load():
     lib.lstm_dyn_create_cell.restype = I
     lib.lstm_dyn_check_cell_args.argtypes = [I] * 6 + [P] * 10
     lib.lstm_dyn_check_cell_args.restype = I
+    lib.lstm_dyn_forward_stop.argtypes = [P] * 9 + [ctypes.c_float] + [P] * 5
+    lib.lstm_dyn_forward_stop.restype = I
+    lib.lstm_dyn_check_stop_args.argtypes = [I] * 6 + [P] * 12
+    lib.lstm_dyn_check_stop_args.restype = I
     lib.lstm_dyn_forward.argtypes = [P] * 11
     lib.lstm_dyn_forward.restype = I
     lib.lstm_dyn_forward_seq.argtypes = [P] * 12
@@ -137,6 +142,16 @@ def lstm_dyn_forward_seq(handle: int, x: int, lengths: int, W: int, U: int, b: i
         raise LstmDynError(rc, "lstm_dyn_forward_seq")
 
 
+def lstm_dyn_forward_stop(handle: int, x: int, lengths: int, W: int, U: int, b: int, h0: int,
+                          c0: int, stop_v: int, stop_c: float, out_h: int, out_c: int,
+                          out_steps: int, out_seq: int = 0, stream: int = 0) -> None:
+    rc = _load().lstm_dyn_forward_stop(handle, x, lengths, W, U, b, h0, c0, stop_v,
+                                       ctypes.c_float(stop_c), out_h, out_c, out_steps, out_seq,
+                                       stream)
+    if rc != OK:
+        raise LstmDynError(rc, "lstm_dyn_forward_stop")
+
+
 def lstm_dyn_destroy(handle: int) -> None:
     rc = _load().lstm_dyn_destroy(handle)
     if rc != OK:
@@ -196,6 +211,13 @@ def lstm_dyn_check_cell_args(B: int, D: int, H: int, T_max: int, dtype: int, cel
                              out_c: int, out_seq: int) -> int:
     return _load().lstm_dyn_check_cell_args(B, D, H, T_max, dtype, cell, x, lengths, W, U, b,
                                             h0, c0, out_h, out_c, out_seq)
+
+
+def lstm_dyn_check_stop_args(B: int, D: int, H: int, T_max: int, dtype: int, cell: int, x: int,
+                             lengths: int, W: int, U: int, b: int, h0: int, c0: int, stop_v: int,
+                             out_h: int, out_c: int, out_steps: int, out_seq: int) -> int:
+    return _load().lstm_dyn_check_stop_args(B, D, H, T_max, dtype, cell, x, lengths, W, U, b, h0,
+                                            c0, stop_v, out_h, out_c, out_steps, out_seq)
 
 
 # --- torch convenience wrapper ---------------------------------------------
@@ -279,6 +301,29 @@ class LstmDyn:
                              U.data_ptr(), b.data_ptr(), h0.data_ptr(), c0p,
                              out_h.data_ptr(), out_c.data_ptr(), out_seq.data_ptr(), s)
         return out_h, out_c, out_seq
+
+    def forward_stop(self, x, lengths, W, U, b, h0, c0, stop_v, stop_c, out_h=None, out_c=None,
+                     out_steps=None, out_seq=None, with_seq=False, stream=None):
+        """The loop with its termination computed from the state: row b ends
+        after a step that leaves stop_v . h + stop_c > 0 (stop_v float32 [H]);
+        lengths are caps.  Returns (out_h, out_c, out_steps) and, with
+        ``with_seq`` or a given ``out_seq``, the output sequence after them."""
+        import torch
+        c0p, out_h, out_c, s = self._inputs(x, lengths, W, U, b, h0, c0, out_h, out_c, stream)
+        self._check("stop_v", stop_v, torch.float32, (self.H,))
+        if out_steps is None:
+            out_steps = torch.empty((self.B,), dtype=torch.int32, device=x.device)
+        self._check("out_steps", out_steps, torch.int32, (self.B,))
+        if out_seq is None and with_seq:
+            out_seq = torch.empty((self.B, self.T, self.H), dtype=torch.float32, device=x.device)
+        if out_seq is not None:
+            self._check("out_seq", out_seq, torch.float32, (self.B, self.T, self.H))
+        lstm_dyn_forward_stop(self.handle, x.data_ptr(), lengths.data_ptr(), W.data_ptr(),
+                              U.data_ptr(), b.data_ptr(), h0.data_ptr(), c0p, stop_v.data_ptr(),
+                              float(stop_c), out_h.data_ptr(), out_c.data_ptr(),
+                              out_steps.data_ptr(),
+                              out_seq.data_ptr() if out_seq is not None else 0, s)
+        return (out_h, out_c, out_steps) if out_seq is None else (out_h, out_c, out_steps, out_seq)
 
     def query(self, what: int) -> int:
         return lstm_dyn_query(self.handle, what)

@@ -20,7 +20,9 @@ struct lstm_dyn {
     Dims dims;
     Workspace ws;
     void* block;               // the one device allocation behind ws
-    int32_t* host_maxlen;      // pinned host word for the per-step path's loop-bound copy
+    int32_t* host_maxlen;      // pinned host words for the per-step path: [0] loop bound,
+                               // [1] rows still running, [2] iterations run
+    int stop_ok;               // the persistent variant with termination from the state fits
     unsigned long long timeout_ticks;
     int inproj_grid;
     long long launches_last;
@@ -40,7 +42,7 @@ long long align_up(long long v, long long a) { return (v + a - 1) / a * a; }
 
 
 struct Layout {
-    long long meta, perm, offsets, rowsrc, gx, hx, bar, z, wt, w4, u4, b4, total;
+    long long meta, perm, offsets, rowsrc, gx, hx, bar, z, wt, w4, u4, b4, stopped, running, total;
 };
 
 Layout layout_of(int B, int D, int H, int T, int bf16, int mode, int bpad, int hpad, int packed = 0) {
@@ -71,6 +73,8 @@ Layout layout_of(int B, int D, int H, int T, int bf16, int mode, int bpad, int h
     L.w4 = take(packed ? e * D * 4 * H : 0);
     L.u4 = take(packed ? e * H * 4 * H : 0);
     L.b4 = take(packed ? 16LL * H : 0);
+    L.stopped = take(4LL * B);
+    L.running = take(4LL * T);
     L.total = o;
     return L;
 }
@@ -257,14 +261,19 @@ extern "C" int lstm_dyn_create_cell(lstm_dyn_t** out, int B, int D, int H, int T
     rc = lstm_dyn_plan(B, D, H, T, dtype, mode, cus, &plan);
     if (rc != LSTM_DYN_OK) return rc;
     const int bf16 = dtype == LSTM_DYN_BF16;
+    int stop_ok = 1;
     if (mode == LSTM_DYN_PERSISTENT && !plan.single) {
         const int per_cu = persistent_blocks_per_cu(bf16, plan.mt, plan.ksw, plan.kw, plan.nstate,
-                                                    plan.lds_bytes, cell);
+                                                    plan.lds_bytes, cell, 0);
         if (per_cu < 1 || plan.groups > per_cu * cus) return LSTM_DYN_ERR_UNSUPPORTED;
+        const int per_cu_stop = persistent_blocks_per_cu(bf16, plan.mt, plan.ksw, plan.kw,
+                                                         plan.nstate, plan.lds_bytes, cell, 1);
+        stop_ok = per_cu_stop >= 1 && plan.groups <= per_cu_stop * cus;
     }
     lstm_dyn* h = new (std::nothrow) lstm_dyn();
     if (!h) return LSTM_DYN_ERR_NOMEM;
     h->B = B; h->D = D; h->H = H; h->T = T; h->dtype = dtype; h->mode = mode; h->cell = cell;
+    h->stop_ok = stop_ok;
     h->device = dev;
     h->num_cus = cus;
     h->plan = plan;
@@ -289,6 +298,8 @@ extern "C" int lstm_dyn_create_cell(lstm_dyn_t** out, int B, int D, int H, int T
     h->w4 = packed ? base + L.w4 : nullptr;
     h->u4 = packed ? base + L.u4 : nullptr;
     h->b4 = packed ? reinterpret_cast<float*>(base + L.b4) : nullptr;
+    h->ws.stopped = reinterpret_cast<int32_t*>(base + L.stopped);
+    h->ws.running = reinterpret_cast<int32_t*>(base + L.running);
     // Zero the small tables and the operand buffer (its padding must stay zero).
     if (hipMemset(base, 0, (size_t)L.gx) != hipSuccess ||
         hipMemset(base + L.hx, 0, (size_t)(L.total - L.hx)) != hipSuccess) {
@@ -296,7 +307,7 @@ extern "C" int lstm_dyn_create_cell(lstm_dyn_t** out, int B, int D, int H, int T
         delete h;
         return LSTM_DYN_ERR_HIP;
     }
-    if (hipHostMalloc(reinterpret_cast<void**>(&h->host_maxlen), sizeof(int32_t), hipHostMallocDefault) != hipSuccess) {
+    if (hipHostMalloc(reinterpret_cast<void**>(&h->host_maxlen), 4 * sizeof(int32_t), hipHostMallocDefault) != hipSuccess) {
         (void)hipFree(h->block);
         delete h;
         return LSTM_DYN_ERR_HIP;
@@ -396,7 +407,8 @@ static hipError_t input_projection(lstm_dyn* h, const void* x, const void* W, co
 // The forward of both entry points; out_seq is null for lstm_dyn_forward.
 static int forward_impl(lstm_dyn_t* h, const void* x, const int32_t* lengths, const void* W,
                         const void* U, const float* b, const float* h0, const float* c0,
-                        float* out_h, float* out_c, float* out_seq, void* stream) {
+                        float* out_h, float* out_c, float* out_seq, const StopArgs* stop,
+                        void* stream) {
     hipStream_t s = static_cast<hipStream_t>(stream);
     h->last_stream = s;
     h->launches_last = 0;
@@ -420,15 +432,18 @@ static int forward_impl(lstm_dyn_t* h, const void* x, const int32_t* lengths, co
         b = h->b4;
     }
     const long long pack_launches = packed ? 1 : 0;
+    // the output sequence is zero past each row's last step: its cap, or the
+    // step it ended at
+    const int32_t* seq_ends = stop ? stop->steps : lengths;
     if (h->mode == LSTM_DYN_PERSISTENT && h->plan.single) {
         LD_CHECK(mark(1));
         LD_CHECK(mark(2));
         LD_CHECK(launch_small(d, h->plan.single_kd, h->plan.single_nt, x, lengths, W, U, b, h0, c0,
-                              out_h, out_c, out_seq, h->ws, s));
+                              out_h, out_c, out_seq, stop, h->ws, s));
         h->launches_last = 1 + pack_launches;
         LD_CHECK(mark(3));
         if (out_seq) {
-            LD_CHECK(launch_seq_finish(d, out_seq, false, 4, lengths, h->ws, h->num_cus, s));
+            LD_CHECK(launch_seq_finish(d, out_seq, false, 4, seq_ends, h->ws, h->num_cus, s));
             h->launches_last++;
         }
         return LSTM_DYN_OK;
@@ -441,12 +456,12 @@ static int forward_impl(lstm_dyn_t* h, const void* x, const int32_t* lengths, co
         LD_CHECK(mark(2));
         PersistentConfig pc{h->plan.mt,     h->plan.groups,    h->plan.ksw, h->plan.kw,
                             h->plan.nstate, h->plan.lds_bytes, h->timeout_ticks, h->trace,
-                            out_seq != nullptr};
+                            out_seq != nullptr, stop};
         LD_CHECK(launch_persistent(d, pc, U, h0, c0, out_h, out_c, h->ws, s));
         h->launches_last++;
         LD_CHECK(mark(3));
         if (out_seq) {
-            LD_CHECK(launch_seq_finish(d, out_seq, true, 4 * h->plan.mt, lengths, h->ws, h->num_cus, s));
+            LD_CHECK(launch_seq_finish(d, out_seq, true, 4 * h->plan.mt, seq_ends, h->ws, h->num_cus, s));
             h->launches_last++;
         }
         return LSTM_DYN_OK;
@@ -454,20 +469,42 @@ static int forward_impl(lstm_dyn_t* h, const void* x, const int32_t* lengths, co
     // Per-step comparison path.
     LD_CHECK(launch_step_init(d, h0, c0, out_h, out_c, h->ws, s));
     h->launches_last++;
+    if (stop) {
+        LD_CHECK(launch_step_stop_init(d, *stop, h->ws, s));
+        h->launches_last++;
+    }
     LD_CHECK(input_projection(h, x, W, b, s));
     LD_CHECK(mark(2));
     LD_CHECK(hipMemcpyAsync(h->host_maxlen, &h->ws.meta->max_len, sizeof(int32_t),
                             hipMemcpyDeviceToHost, s));
     LD_CHECK(hipStreamSynchronize(s));
     const int max_len = *h->host_maxlen;
+    int iters = max_len;
     for (int t = 0; t < max_len; ++t) {
         LD_CHECK(launch_step_gemm(d, t, U, h->ws, s));
-        LD_CHECK(launch_step_gates(d, t, out_h, out_c, out_seq, h->ws, s));
+        LD_CHECK(launch_step_gates(d, t, out_h, out_c, out_seq, stop != nullptr, h->ws, s));
         h->launches_last += 2;
+        if (stop) {
+            // the eager loop condition: read on the host after every step
+            LD_CHECK(launch_step_stop(d, t, *stop, h->ws, s));
+            h->launches_last++;
+            LD_CHECK(hipMemcpyAsync(h->host_maxlen + 1, h->ws.running + t, sizeof(int32_t),
+                                    hipMemcpyDeviceToHost, s));
+            LD_CHECK(hipStreamSynchronize(s));
+            if (h->host_maxlen[1] == 0) {
+                iters = t + 1;
+                break;
+            }
+        }
+    }
+    if (stop) {
+        h->host_maxlen[2] = iters;
+        LD_CHECK(hipMemcpyAsync(&h->ws.meta->iters, h->host_maxlen + 2, sizeof(int32_t),
+                                hipMemcpyHostToDevice, s));
     }
     LD_CHECK(mark(3));
     if (out_seq) {
-        LD_CHECK(launch_seq_finish(d, out_seq, false, 4, lengths, h->ws, h->num_cus, s));
+        LD_CHECK(launch_seq_finish(d, out_seq, false, 4, seq_ends, h->ws, h->num_cus, s));
         h->launches_last++;
     }
 #undef LD_CHECK
@@ -481,7 +518,7 @@ extern "C" int lstm_dyn_forward(lstm_dyn_t* h, const void* x, const int32_t* len
     const int rc = check_args_cell(h->B, h->D, h->H, h->T, h->dtype, h->cell,
                                    x, lengths, W, U, b, h0, c0, out_h, out_c);
     if (rc != LSTM_DYN_OK) return rc;
-    return forward_impl(h, x, lengths, W, U, b, h0, c0, out_h, out_c, nullptr, stream);
+    return forward_impl(h, x, lengths, W, U, b, h0, c0, out_h, out_c, nullptr, nullptr, stream);
 }
 
 extern "C" int lstm_dyn_forward_seq(lstm_dyn_t* h, const void* x, const int32_t* lengths,
@@ -493,7 +530,65 @@ extern "C" int lstm_dyn_forward_seq(lstm_dyn_t* h, const void* x, const int32_t*
                                        h->cell, x, lengths, W, U, b, h0, c0,
                                        out_h, out_c, out_seq);
     if (rc != LSTM_DYN_OK) return rc;
-    return forward_impl(h, x, lengths, W, U, b, h0, c0, out_h, out_c, out_seq, stream);
+    return forward_impl(h, x, lengths, W, U, b, h0, c0, out_h, out_c, out_seq, nullptr, stream);
+}
+
+static int check_stop_args_cell(int B, int D, int H, int T, int dtype, int cell, const void* x,
+                                const int32_t* lengths, const void* W, const void* U,
+                                const float* b, const float* h0, const float* c0,
+                                const float* stop_v, const float* out_h, const float* out_c,
+                                const int32_t* out_steps, const float* out_seq) {
+    const int rc = out_seq ? check_seq_args_cell(B, D, H, T, dtype, cell, x, lengths, W, U, b, h0,
+                                                 c0, out_h, out_c, out_seq)
+                           : check_args_cell(B, D, H, T, dtype, cell, x, lengths, W, U, b, h0, c0,
+                                             out_h, out_c);
+    if (rc != LSTM_DYN_OK) return rc;
+    if (!stop_v || !out_steps) return LSTM_DYN_ERR_INVALID;
+    if ((reinterpret_cast<uintptr_t>(stop_v) & 3) || (reinterpret_cast<uintptr_t>(out_steps) & 3))
+        return LSTM_DYN_ERR_INVALID;
+    const long long e = dtype == LSTM_DYN_BF16 ? 2 : 4;
+    const long long G = (long long)cell_cols(cell) * H;
+    const bool has_c = cell == LSTM_DYN_CELL_LSTM;
+    const long long nv = 4LL * H, nst = 4LL * B, ns = 4LL * B * H;
+    const long long nseq = out_seq ? 4LL * B * T * H : 0;
+    // out_steps overlaps nothing; v overlaps no output
+    const void* all[] = {x, lengths, W, U, b, h0, has_c ? c0 : nullptr, stop_v, out_h, out_c, out_seq};
+    const long long sz[] = {(long long)B * T * D * e, 4LL * B, (long long)D * G * e,
+                            (long long)H * G * e, 4LL * cell_bias(cell) * H, ns, has_c ? ns : 0, nv,
+                            ns, ns, nseq};
+    for (int i = 0; i < 11; ++i)
+        if (all[i] && overlaps(out_steps, nst, all[i], sz[i])) return LSTM_DYN_ERR_INVALID;
+    const void* outs[] = {out_h, out_c, out_seq};
+    const long long osz[] = {ns, ns, nseq};
+    for (int i = 0; i < 3; ++i)
+        if (outs[i] && overlaps(stop_v, nv, outs[i], osz[i])) return LSTM_DYN_ERR_INVALID;
+    return LSTM_DYN_OK;
+}
+
+extern "C" int lstm_dyn_check_stop_args(int B, int D, int H, int T, int dtype, int cell,
+                                        const void* x, const int32_t* lengths, const void* W,
+                                        const void* U, const float* b, const float* h0,
+                                        const float* c0, const float* stop_v, const float* out_h,
+                                        const float* out_c, const int32_t* out_steps,
+                                        const float* out_seq) {
+    if (!valid_cell(cell)) return LSTM_DYN_ERR_INVALID;
+    return check_stop_args_cell(B, D, H, T, dtype, cell, x, lengths, W, U, b, h0, c0, stop_v,
+                                out_h, out_c, out_steps, out_seq);
+}
+
+extern "C" int lstm_dyn_forward_stop(lstm_dyn_t* h, const void* x, const int32_t* lengths,
+                                     const void* W, const void* U, const float* b, const float* h0,
+                                     const float* c0, const float* stop_v, float stop_c,
+                                     float* out_h, float* out_c, int32_t* out_steps,
+                                     float* out_seq, void* stream) {
+    if (!h) return LSTM_DYN_ERR_INVALID;
+    const int rc = check_stop_args_cell(h->B, h->D, h->H, h->T, h->dtype, h->cell, x, lengths, W,
+                                        U, b, h0, c0, stop_v, out_h, out_c, out_steps, out_seq);
+    if (rc != LSTM_DYN_OK) return rc;
+    if (!h->stop_ok) return LSTM_DYN_ERR_UNSUPPORTED;
+    if (stop_c != stop_c) return LSTM_DYN_ERR_INVALID;  // NaN
+    const StopArgs stop{stop_v, stop_c, out_steps, lengths};
+    return forward_impl(h, x, lengths, W, U, b, h0, c0, out_h, out_c, out_seq, &stop, stream);
 }
 
 extern "C" int lstm_dyn_query(lstm_dyn_t* h, int what, long long* value) {
@@ -509,7 +604,7 @@ extern "C" int lstm_dyn_query(lstm_dyn_t* h, int what, long long* value) {
             Meta m;
             if (hipMemcpy(&m, h->ws.meta, sizeof(Meta), hipMemcpyDeviceToHost) != hipSuccess)
                 return LSTM_DYN_ERR_HIP;
-            if (what == LSTM_DYN_Q_STEPS_EXECUTED) *value = m.max_len;
+            if (what == LSTM_DYN_Q_STEPS_EXECUTED) *value = m.iters;
             else if (what == LSTM_DYN_Q_TOTAL_ROWS) *value = m.total_rows;
             else if (m.status & STATUS_TIMEOUT) *value = LSTM_DYN_ERR_TIMEOUT;
             else if (m.status & STATUS_BAD_LENGTHS) *value = LSTM_DYN_ERR_BAD_LENGTHS;

@@ -13,7 +13,7 @@ struct Meta {
     int32_t max_len;     // loop bound: largest (clamped) length
     int32_t total_rows;  // sum of (clamped) lengths = rows of the compact input projection
     int32_t status;      // bit 0: a length was clamped; bit 1: a barrier wait timed out
-    int32_t pad;
+    int32_t iters;       // loop iterations in which some row ran (= max_len unless rows end early)
 };
 constexpr int32_t STATUS_BAD_LENGTHS = 1;
 constexpr int32_t STATUS_TIMEOUT = 2;

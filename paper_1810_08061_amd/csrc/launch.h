@@ -21,6 +21,8 @@ struct Workspace {
     unsigned* bar;      // grid-barrier counters: [0] global, [64 * (1 + x)] group x (zeroed by prep)
     float* z;           // [bpad][4H] per-step pre-activations (per-step mode only)
     void* wt;           // bf16: W transposed to [np][dp] (gate-interleaved rows, zero padded)
+    int32_t* stopped;   // [B] per-step path, termination from the state: 1 once row b ended
+    int32_t* running;   // [T_max] per-step path: rows still running after step t
 };
 
 struct Dims {
@@ -56,18 +58,29 @@ hipError_t launch_inproj_bf16(const Dims& d, const void* x, const float* b, cons
                               int grid, hipStream_t s);
 
 // Persistent on-device time loop.
+// Termination computed from the state: a row ends after a step that leaves
+// its halting score v . h + c positive.
+struct StopArgs {
+    const float* v;          // [H]
+    float c;
+    int32_t* steps;          // [B] (batch order), written: the steps each row ran
+    const int32_t* lengths;  // [B] caps
+};
+
 struct PersistentConfig {
     int mt, groups, ksw, kw, nst, lds_bytes;
     unsigned long long timeout_ticks;  // barrier wait bound in wall-clock ticks
     unsigned long long* trace;         // per-step timestamps (diagnostics) or null
     int seq;                           // 1: keep each step's h in the dead Gx rows (output sequence)
+    const StopArgs* stop;              // termination from the state, or null
 };
 constexpr int BAR_WORDS = 64 * 9;  // global + 8 group counters, 256 bytes apart
 hipError_t launch_persistent(const Dims& d, const PersistentConfig& pc, const void* U,
                              const float* h0, const float* c0, float* out_h, float* out_c,
                              const Workspace& ws, hipStream_t s);
 // Occupancy check for the co-resident grid; returns blocks per CU (0 if none).
-int persistent_blocks_per_cu(int bf16, int mt, int ksw, int kw, int nst, int lds_bytes, int cell);
+int persistent_blocks_per_cu(int bf16, int mt, int ksw, int kw, int nst, int lds_bytes, int cell,
+                             int stop);
 // Compiled variant with exactly (mt, kw, ksw) and the smallest state capacity >= nstate.
 bool persistent_pick_variant(int bf16, int mt, int kw, int ksw, int nstate, int* nst);
 int persistent_lds_bytes(int bf16, int mt, int kw, int nst, int hpad);
@@ -77,14 +90,21 @@ bool small_pick(int bf16, int B, int D, int H, int* kd, int* nt);
 hipError_t launch_small(const Dims& d, int kd, int nt, const void* x, const int32_t* lengths,
                         const void* W, const void* U, const float* b, const float* h0,
                         const float* c0, float* out_h, float* out_c, float* seq,
-                        const Workspace& ws, hipStream_t s);
+                        const StopArgs* stop, const Workspace& ws, hipStream_t s);
 
 // Per-step comparison path.
 hipError_t launch_step_init(const Dims& d, const float* h0, const float* c0, float* out_h,
                             float* out_c, const Workspace& ws, hipStream_t s);
 hipError_t launch_step_gemm(const Dims& d, int t, const void* U, const Workspace& ws, hipStream_t s);
 hipError_t launch_step_gates(const Dims& d, int t, float* out_h, float* out_c, float* seq,
-                             const Workspace& ws, hipStream_t s);
+                             bool stop, const Workspace& ws, hipStream_t s);
+// Termination from the state on the per-step path: init (steps = caps, no row
+// ended, counters zero), then after the gates of each step the halting scores
+// of the rows that ran; running[t] counts the rows that run at step t + 1.
+hipError_t launch_step_stop_init(const Dims& d, const StopArgs& stop, const Workspace& ws,
+                                 hipStream_t s);
+hipError_t launch_step_stop(const Dims& d, int t, const StopArgs& stop, const Workspace& ws,
+                            hipStream_t s);
 
 // Output sequence: moves the persistent loop's step outputs (kept in the
 // dead Gx rows, unit slices of upw) to seq [B][T][H] when from_gx, and

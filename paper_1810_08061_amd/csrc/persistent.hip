@@ -52,6 +52,13 @@ struct PersistParams {
     unsigned long long timeout_ticks;
     unsigned long long* trace;  // [T + 1][4] timestamps from workgroup 0, or null
     int seq;                    // 1: also keep each step's h (fp32) for the output sequence
+    // Termination from the state (variants with STOP): a row ends after a step
+    // that leaves v . h + c > 0; steps[b] receives the steps row b ran.
+    const float* stop_v;        // [H]
+    float stop_c;
+    int32_t* steps;             // [B], batch order; written by workgroup 0
+    const int32_t* lengths;     // [B] caps (clamped to [0, T] here)
+    int T;
 };
 
 // Logical workgroup index: consecutive workgroups are dispatched to different
@@ -210,7 +217,7 @@ struct PLayout {
     static constexpr int BYTES = (NTC * KW * MT + GX_KB) * 1024;
 };
 
-template <typename E, int MT, int KSW, int KW, int NST, int CELL>
+template <typename E, int MT, int KSW, int KW, int NST, int CELL, bool STOP>
 __global__ void __launch_bounds__(KW * 64, 1)
 persistent_kernel(PersistParams p) {
     using S = typename E::store_t;
@@ -228,6 +235,13 @@ persistent_kernel(PersistParams p) {
     static_assert(SEG_BYTES == 8 || SEG_BYTES == 16, "h row segment must be 8 or 16 bytes");
     // per-wave gather of one owned row tile's h before its row segments are stored
     __shared__ __attribute__((aligned(16))) S hstage[KW][16 * UPW];
+    // STOP: the read-out v in operand precision over the padded K range, each
+    // wave's partial halting scores of the chunk's row tiles, and whether any
+    // row ran at step t (slot t & 1)
+    constexpr int VST = STOP ? KW * KSW * E::KSTEP : 1;
+    __shared__ __attribute__((aligned(16))) S vst[VST];
+    __shared__ float s_part[STOP ? KW : 1][STOP ? NTC : 1][16];
+    __shared__ int lds_run[2];
 
     // tid and l are re-read through empty asm statements at the top of each
     // step and chunk, so values derived from them (addresses, row indices)
@@ -246,6 +260,11 @@ persistent_kernel(PersistParams p) {
     if (tid == 0) {
         lds_abort = 0;
         lds_nan = 0;
+        lds_run[0] = 0;
+        lds_run[1] = 0;
+    }
+    if constexpr (STOP) {
+        for (int k = tid; k < VST; k += KW * 64) vst[k] = E::from_f32(k < H ? p.stop_v[k] : 0.0f);
     }
     F afrag[MT][KSW];
 
@@ -351,6 +370,13 @@ persistent_kernel(PersistParams p) {
         __builtin_amdgcn_wave_barrier();
         if (nt < ntmax && l < 16 && nt * 16 + l < B) seg_store(hx_off<E>(nt * 16 + l, u0, hpad), &hstage[w][l * UPW]);
         __builtin_amdgcn_wave_barrier();
+        if constexpr (STOP) {
+            // a row that never ends early runs to its cap
+            if (g == 0 && nt < ntmax && l < 16 && nt * 16 + l < B) {
+                const int b = p.perm[nt * 16 + l];
+                p.steps[b] = min(max(p.lengths[b], 0), p.T);
+            }
+        }
     }
 
     // Gx[t] of one owned tile goes straight from memory into this wave's LDS
@@ -398,7 +424,10 @@ persistent_kernel(PersistParams p) {
     constexpr int KB = GROUPED ? 16 : 32;  // k per 1 KB block
     const unsigned lane_off = (unsigned)(kw0 / KB) * 1024u + (unsigned)l * 16u;
     const unsigned tile_bytes = (unsigned)(16 * hpad) * (unsigned)sizeof(S);
-    for (int t = 0; t < max_len && alive; ++t) {
+    unsigned stopped = 0;  // STOP: bit a set once the lane's row of owned tile a has ended
+    int iters = 0;         // STOP: steps in which some row ran
+    int t = 0;
+    for (; t < max_len && alive; ++t) {
         asm volatile("" : "+v"(tid), "+v"(l));
         const bool tr = p.trace && blockIdx.x == 0 && tid == 0;
         if (tr) p.trace[4 * t] = wall_clock64();
@@ -410,9 +439,20 @@ persistent_kernel(PersistParams p) {
         // The owners of the previous step's row tiles may still be reading its
         // partial sums.
         __syncthreads();
+        if constexpr (STOP) {
+            // Every workgroup takes the same decisions from the same h, so all
+            // leave together: once no row ran at step t-1, none runs again
+            // (ended rows stay ended, caps only shrink the active prefix).
+            if (t > 0) {
+                if (lds_run[(t - 1) & 1] == 0) break;
+                iters = t;
+            }
+            if (tid == 0) lds_run[t & 1] = 0;
+        }
 
         constexpr int FRAG_REGS = KSW * (int)sizeof(F) / 4;
-        constexpr int REG_BUDGET = KW <= 8 ? 256 : 2048 / KW;  // VGPRs per lane with KW / 4 waves per SIMD
+        // VGPRs per lane with KW / 4 waves per SIMD (less the halting score's with STOP)
+        constexpr int REG_BUDGET = (KW <= 8 ? 256 : 2048 / KW) - (STOP ? 16 : 0);
         constexpr int DEPTH = (MT + 3) * FRAG_REGS < REG_BUDGET / 2    ? 3
                               : (MT + 2) * FRAG_REGS <= REG_BUDGET / 2 ? 2
                                                                        : 1;
@@ -474,11 +514,13 @@ persistent_kernel(PersistParams p) {
                 f32x4_t acc[MT];
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+                f32x4_t sacc = f32x4_t{0.f, 0.f, 0.f, 0.f};
                 const unsigned next = tile_base(ntc0 + j + 1);
 #pragma unroll
                 for (int ks = 0; ks < KSW; ++ks) {
 #pragma unroll
                     for (int mt = 0; mt < MT; ++mt) acc[mt] = E::mfma(afrag[mt][ks], f[ks], acc[mt]);
+                    if constexpr (STOP) sacc = E::mfma(E::load(vst + kw0 + kslot<E, KSW>(ks, l)), f[ks], sacc);
                     if constexpr (GROUPED) {
                         if ((ks & 3) == 3) {
                             typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
@@ -494,6 +536,9 @@ persistent_kernel(PersistParams p) {
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt)
                     *reinterpret_cast<f32x4_t*>(lds + ((((w * NTC + j) * MT + mt) * 64 + l) << 2)) = acc[mt];
+                if constexpr (STOP) {
+                    if (l < 16) s_part[w][j][l] = sacc[0];
+                }
             };
             // Partial products of row tile j of the chunk into its LDS slot.
             auto mma_tile = [&](const F* f, int j) {
@@ -507,6 +552,15 @@ persistent_kernel(PersistParams p) {
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt)
                     *reinterpret_cast<f32x4_t*>(lds + ((((w * NTC + j) * MT + mt) * 64 + l) << 2)) = acc[mt];
+                if constexpr (STOP) {
+                    // halting score: every row of the A operand is v, so lane l
+                    // gets this wave's partial v . h of row (l & 15) of the tile
+                    f32x4_t sacc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int ks = 0; ks < KSW; ++ks)
+                        sacc = E::mfma(E::load(vst + kw0 + kslot<E, KSW>(ks, l)), f[ks], sacc);
+                    if (l < 16) s_part[w][j][l] = sacc[0];
+                }
                 // keep the reload of this register set after its MFMAs, so the
                 // set is reused rather than renamed
                 __builtin_amdgcn_sched_barrier(0);
@@ -521,6 +575,7 @@ persistent_kernel(PersistParams p) {
             // is kept.)
             bool exact = false;
             float cn[NST], hn[NST];  // state update of this chunk, kept until it is verified
+            unsigned ends = 0;       // STOP: owned tiles whose lane row ends before step t
             for (;;) {
                 if (!exact) {
                     load_tile(f0, ntc0);
@@ -604,10 +659,19 @@ persistent_kernel(PersistParams p) {
                 // h stores of earlier steps
                 asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
                 bool nan = false;
+                ends = 0;
 #pragma unroll
                 for (int a = 0; a < NOT; ++a) {
                     const int j = a * KW + w - ntc0;
                     if (j < 0 || j >= nchunk) continue;
+                    if constexpr (STOP) {
+                        // halting score of the row's h_t: the waves' partials in
+                        // a fixed order, then c; positive after step t-1 ends it
+                        float sum = 0.f;
+#pragma unroll
+                        for (int ww = 0; ww < KW; ++ww) sum += s_part[ww][j][lo & 15];
+                        if (t > 0 && sum + p.stop_c > 0.f) ends |= 1u << a;
+                    }
 #pragma unroll
                     for (int mt = 0; mt < MT; ++mt) {
                         const int i = a * MT + mt;
@@ -653,11 +717,21 @@ persistent_kernel(PersistParams p) {
                     const int nt = a * KW + w;
                     const int j = nt - ntc0;
                     if (j < 0 || j >= nchunk) continue;
+                    bool runs = true;
+                    if constexpr (STOP) {
+                        const int s = nt * 16 + (lo & 15);
+                        if (((ends & ~stopped) >> a) & 1) {  // ends now: it ran t steps
+                            if (g == 0 && lo < 16 && s < act) p.steps[p.perm[s]] = t;
+                        }
+                        stopped |= ends & (1u << a);
+                        runs = !((stopped >> a) & 1);
+                        if (runs && s < act) lds_run[t & 1] = 1;
+                    }
 #pragma unroll
                     for (int mt = 0; mt < MT; ++mt) {
                         const int i = a * MT + mt;
                         const int s = nt * 16 + (lo & 15), u = u0 + mt * 4 + (lo >> 4);
-                        if (s < act && u < H) {
+                        if (s < act && u < H && runs) {
                             cst[i] = cn[i];
                             hst[i] = hn[i];
                         }
@@ -709,6 +783,15 @@ persistent_kernel(PersistParams p) {
         o3 = o4;
     }
 
+    // Nothing of this wave may still be in flight when it ends (a loop left
+    // early has a Gx prefetch into LDS outstanding).
+    drain_stores();
+    if constexpr (STOP) {
+        // a loop that ran to max_len: did some row run in its last step?
+        __syncthreads();
+        if (alive && t == max_len && max_len > 0 && lds_run[(max_len - 1) & 1] != 0) iters = max_len;
+        if (g == 0 && tid == 0) p.meta->iters = iters;
+    }
     if (p.trace && blockIdx.x == 0 && tid == 0) p.trace[4 * max_len] = wall_clock64();
     // ---- final state, batch order
 #pragma unroll
@@ -731,14 +814,17 @@ persistent_kernel(PersistParams p) {
 // capacity that covers the batch.
 typedef void (*persist_fn)(PersistParams);
 
-// f[cell]: the variant compiled for each CellKind, so the gate step has no
-// branch on the cell (a uniform branch there cost about 4% of the loop).
-struct Variant { int bf16, mt, ksw, kw, nst, lds_bytes; persist_fn f[3]; };
+// f[cell][stop]: the variant compiled for each CellKind, with and without
+// termination from the state, so the gate step has no branch on either (a
+// uniform branch on the cell there cost about 4% of the loop).
+struct Variant { int bf16, mt, ksw, kw, nst, lds_bytes; persist_fn f[3][2]; };
 
-#define PV(BF, ET, MT, KS, KW, NS)                                                       \
-    {BF, MT, KS, KW, NS, PLayout<MT, KW, NS>::BYTES,                                      \
-     {persistent_kernel<ET, MT, KS, KW, NS, CELL_LSTM>, persistent_kernel<ET, MT, KS, KW, NS, CELL_GRU>, \
-      persistent_kernel<ET, MT, KS, KW, NS, CELL_RNN>}}
+#define PV_CELL(ET, MT, KS, KW, NS, C) \
+    {persistent_kernel<ET, MT, KS, KW, NS, C, false>, persistent_kernel<ET, MT, KS, KW, NS, C, true>}
+#define PV(BF, ET, MT, KS, KW, NS)                                             \
+    {BF, MT, KS, KW, NS, PLayout<MT, KW, NS>::BYTES,                            \
+     {PV_CELL(ET, MT, KS, KW, NS, CELL_LSTM), PV_CELL(ET, MT, KS, KW, NS, CELL_GRU), \
+      PV_CELL(ET, MT, KS, KW, NS, CELL_RNN)}}
 #define PV_NST(BF, ET, MT, KS, KW) PV(BF, ET, MT, KS, KW, 2), PV(BF, ET, MT, KS, KW, 8)
 static const Variant kVariants[] = {
     PV_NST(0, EltF32, 1, 4, 4),
@@ -750,12 +836,13 @@ static const Variant kVariants[] = {
 };
 #undef PV_NST
 #undef PV
+#undef PV_CELL
 
-static persist_fn find_variant(int bf16, int mt, int ksw, int kw, int nst, int cell) {
+static persist_fn find_variant(int bf16, int mt, int ksw, int kw, int nst, int cell, int stop) {
     if (cell < CELL_LSTM || cell > CELL_RNN) return nullptr;
     for (const Variant& v : kVariants)
         if (v.bf16 == bf16 && v.mt == mt && v.ksw == ksw && v.kw == kw && v.nst == nst)
-            return v.f[cell];
+            return v.f[cell][stop ? 1 : 0];
     return nullptr;
 }
 
@@ -780,8 +867,9 @@ int persistent_lds_bytes(int bf16, int mt, int kw, int nst, int hpad) {
     return staged > loop ? staged : loop;
 }
 
-int persistent_blocks_per_cu(int bf16, int mt, int ksw, int kw, int nst, int lds_bytes, int cell) {
-    persist_fn f = find_variant(bf16, mt, ksw, kw, nst, cell);
+int persistent_blocks_per_cu(int bf16, int mt, int ksw, int kw, int nst, int lds_bytes, int cell,
+                             int stop) {
+    persist_fn f = find_variant(bf16, mt, ksw, kw, nst, cell, stop);
     if (!f) return 0;
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(f),
                             hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes) != hipSuccess)
@@ -796,7 +884,7 @@ int persistent_blocks_per_cu(int bf16, int mt, int ksw, int kw, int nst, int lds
 hipError_t launch_persistent(const Dims& d, const PersistentConfig& pc, const void* U,
                              const float* h0, const float* c0, float* out_h, float* out_c,
                              const Workspace& ws, hipStream_t s) {
-    persist_fn f = find_variant(d.bf16, pc.mt, pc.ksw, pc.kw, pc.nst, d.cell);
+    persist_fn f = find_variant(d.bf16, pc.mt, pc.ksw, pc.kw, pc.nst, d.cell, pc.stop != nullptr);
     if (!f) return hipErrorInvalidValue;
     PersistParams p{};
     p.U = U;
@@ -818,6 +906,13 @@ hipError_t launch_persistent(const Dims& d, const PersistentConfig& pc, const vo
     p.timeout_ticks = pc.timeout_ticks;
     p.trace = pc.trace;
     p.seq = pc.seq;
+    if (pc.stop) {
+        p.stop_v = pc.stop->v;
+        p.stop_c = pc.stop->c;
+        p.steps = pc.stop->steps;
+        p.lengths = pc.stop->lengths;
+        p.T = d.T;
+    }
     void* args[] = {&p};
     return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(f), dim3(pc.groups),
                                       dim3(pc.kw * 64), args, (unsigned)pc.lds_bytes, s);

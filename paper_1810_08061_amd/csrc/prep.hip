@@ -69,7 +69,7 @@ prep_kernel(const int32_t* __restrict__ lengths, int B, int T, Meta* __restrict_
         meta->max_len = ml;
         meta->total_rows = total;
         meta->status = bad ? STATUS_BAD_LENGTHS : 0;
-        meta->pad = 0;
+        meta->iters = ml;
     }
 }
 

@@ -2,7 +2,8 @@
 //
 // The loop of the paper (Section 9 "RNN cells", Appendix A) appends the
 // cell's output at every step.  out_seq[b][t] is the hidden state of row b
-// after step t for t < L[b]; past a sequence's length the output is zero (no
+// after step t for t < L[b]; past a sequence's length (or past the step at
+// which a row ended, with termination from the state) the output is zero (no
 // value is defined there; zero is the padding convention chosen).
 //
 // The persistent loop leaves the step outputs of compact row r (one valid
@@ -20,7 +21,8 @@ struct SeqParams {
     const float* gx;         // compact rows with the step outputs inside, or null
     const int32_t* rowsrc;   // compact row -> b * T + t
     const Meta* meta;        // total_rows (read only when gx is set)
-    const int32_t* lengths;  // [B] as passed (clamped here to [0, T])
+    const int32_t* lengths;  // [B] last step + 1 of each row: its length as passed, or the
+                             // step it ended at (clamped here to [0, T])
     int B, T, H, upw;
 };
 
@@ -36,8 +38,12 @@ seq_finish_kernel(SeqParams p) {
     if (p.gx) {
         const long rows = p.meta->total_rows;
         for (long r = wave; r < rows; r += nwaves) {
+            // rows at or past a row's last step belong to the zero fill below
+            // (a row that ended before its length has compact rows past it)
+            const int bt = p.rowsrc[r], b = bt / T;
+            if (bt - b * T >= min(max(p.lengths[b], 0), T)) continue;
             const float* src = p.gx + (size_t)r * 4 * H;
-            float* dst = p.seq + (size_t)p.rowsrc[r] * H;
+            float* dst = p.seq + (size_t)bt * H;
             if constexpr (VEC) {
                 for (int u = 4 * lane; u < H; u += 256)  // u .. u+3 lie in one slice (upw is 4 or 8)
                     *reinterpret_cast<f32x4_t*>(dst + u) =

@@ -32,6 +32,11 @@ struct SmallParams {
     Meta* meta;
     int B, D, H, T;
     int cell;  // CellKind (only the LSTM has a cell state)
+    // termination from the state (stop_v null: none): a row ends after a step
+    // that leaves v . h + c > 0; steps[b] receives the steps it ran
+    const float* stop_v;
+    float stop_c;
+    int32_t* steps;
 };
 
 // E: element type of x and W; EH: of the recurrent operands (U, h).
@@ -48,6 +53,8 @@ small_kernel(SmallParams p) {
     __shared__ __attribute__((aligned(16))) SH hs[2][NT * 16 * HS];
     __shared__ int len[NT * 16];
     __shared__ int maxlen, bad;
+    __shared__ int ended[NT * 16];  // termination from the state: 1 once the row ended
+    __shared__ int ran[2];          // some row ran at step t (slot t & 1)
 
     const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
     const int B = p.B, D = p.D, H = p.H, T = p.T, H4 = 4 * H;
@@ -58,6 +65,8 @@ small_kernel(SmallParams p) {
     if (tid == 0) {
         maxlen = 0;
         bad = 0;
+        ran[0] = 0;
+        ran[1] = 0;
     }
     __syncthreads();
     for (int i = tid; i < NT * 16; i += SM_THREADS) {
@@ -71,6 +80,8 @@ small_kernel(SmallParams p) {
             atomicMax(&maxlen, v);
         }
         len[i] = v;
+        ended[i] = 0;
+        if (p.stop_v && i < B) p.steps[i] = v;  // a row that never ends runs to its cap
     }
     // h0 -> LDS (operand type); padding rows and columns are zero in both buffers
     for (int i = tid; i < NT * 16 * HS; i += SM_THREADS) {
@@ -156,10 +167,35 @@ small_kernel(SmallParams p) {
     };
     if (ml > 0) load_x(xf, 0);
 
-    for (int t = 0; t < ml; ++t) {
-        if (t + 1 < ml) load_x(xn, t + 1);
+    int iters = 0;  // termination from the state: steps in which some row ran
+    int t = 0;
+    for (; t < ml; ++t) {
         const SH* hcur = hs[t & 1];
         SH* hnext = hs[(t + 1) & 1];
+        if (p.stop_v) {
+            // Halting scores of h_t (the operand in LDS, k in order): a row
+            // that ran step t-1 and scores > 0 has ended.  Every lane of a row
+            // computes the same score; lane (row, unit 0) records it.
+            if (t > 0) {
+                if (ran[(t - 1) & 1] == 0) break;  // no row ran at step t-1: none runs again
+                iters = t;
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt) {
+                    const int n = nt * 16 + (l & 15);
+                    float sc = 0.f;
+                    for (int k = 0; k < H; ++k) sc += p.stop_v[k] * EH::to_f32(hcur[n * HS + k]);
+                    const bool ends = n < B && t - 1 < len[n] && !ended[n] && sc + p.stop_c > 0.f;
+                    __syncthreads();  // every lane has read ended[] before it changes
+                    if (ends && w == 0 && (l >> 4) == 0) {
+                        ended[n] = 1;
+                        p.steps[n] = t;
+                    }
+                }
+            }
+            if (tid == 0) ran[t & 1] = 0;
+            __syncthreads();
+        }
+        if (t + 1 < ml) load_x(xn, t + 1);
         f32x4_t acc[SM_MT][NT];
 #pragma unroll
         for (int mt = 0; mt < SM_MT; ++mt)
@@ -186,7 +222,8 @@ small_kernel(SmallParams p) {
                 const int n = nt * 16 + (l & 15);
                 const int u = ((w * SM_MT + mt) * 16 + 4 * (l >> 4)) >> 2;
                 if (u >= H) continue;
-                if (t < len[n]) {  // len[n] = 0 for padding rows
+                if (t < len[n] && !ended[n]) {  // len[n] = 0 for padding rows
+                    if (p.stop_v) ran[t & 1] = 1;
                     f32x4_t z = acc[mt][nt];
 #pragma unroll
                     for (int g = 0; g < 4; ++g) z[g] += bias[mt][g];
@@ -222,7 +259,9 @@ small_kernel(SmallParams p) {
         p.meta->max_len = ml;
         p.meta->total_rows = total;
         p.meta->status = bad ? STATUS_BAD_LENGTHS : 0;
-        p.meta->pad = 0;
+        // a loop that ran to ml: did some row run in its last step?
+        if (p.stop_v && t == ml && ml > 0 && ran[(ml - 1) & 1] != 0) iters = ml;
+        p.meta->iters = p.stop_v ? iters : ml;
     }
 }
 
@@ -259,12 +298,13 @@ bool small_pick(int bf16, int B, int D, int H, int* kd, int* nt) {
 hipError_t launch_small(const Dims& d, int kd, int nt, const void* x, const int32_t* lengths,
                         const void* W, const void* U, const float* b, const float* h0,
                         const float* c0, float* out_h, float* out_c, float* seq,
-                        const Workspace& ws, hipStream_t s) {
+                        const StopArgs* stop, const Workspace& ws, hipStream_t s) {
     small_fn f = nullptr;
     for (const SmallVariant& v : kSmall)
         if (v.bf16 == d.bf16 && v.kd == kd && v.nt == nt) f = v.f;
     if (!f) return hipErrorInvalidValue;
-    SmallParams p{x, lengths, W, U, b, h0, c0, out_h, out_c, seq, ws.meta, d.B, d.D, d.H, d.T, d.cell};
+    SmallParams p{x, lengths, W, U, b, h0, c0, out_h, out_c, seq, ws.meta, d.B, d.D, d.H, d.T, d.cell,
+                  stop ? stop->v : nullptr, stop ? stop->c : 0.0f, stop ? stop->steps : nullptr};
     hipLaunchKernelGGL(f, dim3(1), dim3(SM_THREADS), 0, s, p);
     return hipGetLastError();
 }

@@ -204,3 +204,24 @@ def test_check_cell_args_rnn():
     q = list(p)
     q[7] = q[4] + 4 * H - 4                       # out_h on the last bias float
     assert chk(B, D, H, T, ld.F32, ld.CELL_RNN, *q, 0) == ld.ERR_INVALID
+
+
+def test_check_stop_args():
+    B, D, H, T = 3, 5, 7, 4
+    *p, seq = _gru_ptrs(B, D, H, T, 2)              # GRU-sized buffers; then v and out_steps
+    v = seq + (4 * B * T * H + 255) // 256 * 256 + 256
+    st = v + 512
+    chk = ld.lstm_dyn_check_stop_args
+    assert chk(B, D, H, T, ld.BF16, ld.CELL_GRU, *p[:7], v, p[7], p[8], st, seq) == ld.OK
+    assert chk(B, D, H, T, ld.BF16, ld.CELL_GRU, *p[:7], v, p[7], p[8], st, 0) == ld.OK   # no sequence
+    assert chk(B, D, H, T, ld.BF16, ld.CELL_GRU, *p[:7], 0, p[7], p[8], st, 0) == ld.ERR_INVALID
+    assert chk(B, D, H, T, ld.BF16, ld.CELL_GRU, *p[:7], v, p[7], p[8], 0, 0) == ld.ERR_INVALID
+    assert chk(B, D, H, T, ld.BF16, ld.CELL_GRU, *p[:7], v + 2, p[7], p[8], st, 0) == ld.ERR_INVALID
+    assert chk(B, D, H, T, ld.BF16, ld.CELL_GRU, *p[:7], v, p[7], p[8], st + 2, 0) == ld.ERR_INVALID
+    for i in (0, 1, 2, 3, 4, 5, 7, 8):            # out_steps on any used argument
+        q = p[i]
+        assert chk(B, D, H, T, ld.BF16, ld.CELL_GRU, *p[:7], v, p[7], p[8], q, 0) == ld.ERR_INVALID, i
+    assert chk(B, D, H, T, ld.BF16, ld.CELL_GRU, *p[:7], v, p[7], p[8], v, 0) == ld.ERR_INVALID
+    # v may not lie under an output, but may share memory with an input
+    assert chk(B, D, H, T, ld.BF16, ld.CELL_GRU, *p[:7], p[7], p[7], p[8], st, 0) == ld.ERR_INVALID
+    assert chk(B, D, H, T, ld.BF16, ld.CELL_GRU, *p[:7], p[5], p[7], p[8], st, 0) == ld.OK
