@@ -75,6 +75,8 @@ class _Lib:
         lib.lstm_oracle_forward_stop.argtypes = [ctypes.c_int] * 4 + [P] * 6 + [ctypes.c_int, P,
                                                  ctypes.c_double] + [P] * 7 + [ctypes.c_int]
         lib.lstm_oracle_forward_stop.restype = ctypes.c_int
+        lib.lstm_oracle_backward.argtypes = [ctypes.c_int] * 4 + [P] * 16
+        lib.lstm_oracle_backward.restype = ctypes.c_int
         lib.lstm_oracle_max_threads.argtypes = []
         lib.lstm_oracle_max_threads.restype = ctypes.c_int
         self.lib = lib
@@ -244,6 +246,41 @@ def forward_rnn(x, lengths, W, U, b, h0, literal: bool = False, threads: int = 0
     if return_steps:
         out = (*out, int(steps.value))
     return out[0] if len(out) == 1 else out
+
+
+def backward(x, lengths, W, U, b, h0, c0, dh_out, dc_out, dseq=None, _lib_override=None):
+    """Gradients of the masked LSTM loop (backpropagation through time): given
+    the upstream gradients of the final state (dh_out, dc_out [B, H]) and
+    optionally of the output sequence (dseq [B, T, H]), returns a dict of
+    float64 arrays dx [B, T, D], dW [D, 4H], dU [H, 4H], db [4H], dh0, dc0
+    [B, H].  Layouts as for ``forward``."""
+    lib = (_lib_override or _load()).lib
+    x, W, U, b = map(_f32, (x, W, U, b))
+    f64 = lambda a: np.ascontiguousarray(a, dtype=np.float64)
+    h0, c0, dh_out, dc_out = map(f64, (h0, c0, dh_out, dc_out))
+    L = np.ascontiguousarray(lengths, dtype=np.int32)
+    B, T, D = x.shape
+    H = U.shape[0]
+    if W.shape != (D, 4 * H) or U.shape != (H, 4 * H) or b.shape != (4 * H,):
+        raise OracleError("weight shapes do not match x and U")
+    for a in (h0, c0, dh_out, dc_out):
+        if a.shape != (B, H):
+            raise OracleError("state shapes do not match x")
+    ds = f64(dseq) if dseq is not None else None
+    if ds is not None and ds.shape != (B, T, H):
+        raise OracleError("dseq must be [B, T, H]")
+    out = {"dx": np.empty((B, T, D)), "dW": np.empty((D, 4 * H)), "dU": np.empty((H, 4 * H)),
+           "db": np.empty(4 * H), "dh0": np.empty((B, H)), "dc0": np.empty((B, H))}
+    rc = lib.lstm_oracle_backward(B, T, D, H, x.ctypes.data, L.ctypes.data, W.ctypes.data,
+                                  U.ctypes.data, b.ctypes.data, h0.ctypes.data, c0.ctypes.data,
+                                  dh_out.ctypes.data, dc_out.ctypes.data,
+                                  ds.ctypes.data if ds is not None else None,
+                                  *(out[k].ctypes.data for k in ("dx", "dW", "dU", "db", "dh0", "dc0")))
+    if rc == BAD_LENGTHS:
+        raise OracleError("sequence lengths must lie in [0, T]")
+    if rc != OK:
+        raise OracleError(f"oracle failed with code {rc}")
+    return out
 
 
 _CELL_IDS = {"lstm": 0, "gru": 1, "rnn": 2}

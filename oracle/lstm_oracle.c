@@ -401,6 +401,111 @@ int lstm_oracle_forward_stop(int B, int T, int D, int H, const float* x, const i
     return ORACLE_OK;
 }
 
+/*
+ * lstm_oracle_backward: gradients of the masked LSTM loop (backpropagation
+ * through time; the paper trains its staged models in-graph, Section 9).
+ * Given the upstream gradients of the final state (dh_out, dc_out [B][H])
+ * and, optionally, of the output sequence (dseq [B][T][H], may be NULL;
+ * entries at t >= L[b] have no effect), it returns the gradients of the loss
+ * with respect to x [B][T][D], W [D][4H], U [H][4H], b [4H], h0, c0 [B][H].
+ *
+ * A step that a row does not take passes its state through unchanged, so
+ * the gradient of such a step is the identity; each row is therefore
+ * differentiated through its own L[b] steps, backwards from the last:
+ *   dh += dseq[t]
+ *   o-gate:  do  = dh * tanh(c_t)
+ *   cell:    dct = dc + dh * o * (1 - tanh(c_t)^2)
+ *   di = dct * g, df = dct * c_{t-1}, dg = dct * i, dc <- dct * f
+ *   dz = (di i (1 - i), df f (1 - f), dg (1 - g^2), do o (1 - o))
+ *   db += dz, dW += x_t^T dz, dU += h_{t-1}^T dz, dx_t = dz W^T, dh <- dz U^T
+ * with (i, f, g, o) and c_t recomputed by the forward in double precision.
+ * Rows run one after another in order 0 .. B-1 and the weight gradients are
+ * summed in that order.
+ */
+int lstm_oracle_backward(int B, int T, int D, int H, const float* x, const int32_t* L,
+                         const float* W, const float* U, const float* bias, const double* h0,
+                         const double* c0, const double* dh_out, const double* dc_out,
+                         const double* dseq, double* dx, double* dW, double* dU, double* db,
+                         double* dh0, double* dc0) {
+    if (B <= 0 || T < 0 || D <= 0 || H <= 0 || !x || !L || !W || !U || !bias || !h0 || !c0 ||
+        !dh_out || !dc_out || !dx || !dW || !dU || !db || !dh0 || !dc0)
+        return ORACLE_BAD_ARGS;
+    for (int b = 0; b < B; ++b)
+        if (L[b] < 0 || L[b] > T) return ORACLE_BAD_LENGTHS;
+    const int G = 4 * H;
+    double* zs = (double*)malloc((size_t)(T > 0 ? T : 1) * G * sizeof(double));   /* z_t per step */
+    double* cs = (double*)malloc((size_t)(T + 1) * H * sizeof(double));            /* c_{t-1}, t = 0..T */
+    double* hs = (double*)malloc((size_t)(T + 1) * H * sizeof(double));            /* h_{t-1} */
+    double* dz = (double*)malloc((size_t)G * sizeof(double));
+    double* dh = (double*)malloc((size_t)H * sizeof(double));
+    double* dc = (double*)malloc((size_t)H * sizeof(double));
+    double* nh = (double*)malloc((size_t)H * sizeof(double));
+    if (!zs || !cs || !hs || !dz || !dh || !dc || !nh) {
+        free(zs); free(cs); free(hs); free(dz); free(dh); free(dc); free(nh);
+        return ORACLE_NOMEM;
+    }
+    memset(dx, 0, (size_t)B * T * D * sizeof(double));
+    memset(dW, 0, (size_t)D * G * sizeof(double));
+    memset(dU, 0, (size_t)H * G * sizeof(double));
+    memset(db, 0, (size_t)G * sizeof(double));
+    for (int b = 0; b < B; ++b) {
+        const int n = L[b];
+        /* forward through the row's own steps, keeping z_t, c and h */
+        memcpy(hs, h0 + (size_t)b * H, (size_t)H * sizeof(double));
+        memcpy(cs, c0 + (size_t)b * H, (size_t)H * sizeof(double));
+        for (int t = 0; t < n; ++t) {
+            const float* xt = x + ((size_t)b * T + t) * D;
+            lstm_cell_row(D, H, xt, W, U, bias, hs + (size_t)t * H, cs + (size_t)t * H,
+                          zs + (size_t)t * G, hs + (size_t)(t + 1) * H, cs + (size_t)(t + 1) * H);
+        }
+        memcpy(dh, dh_out + (size_t)b * H, (size_t)H * sizeof(double));
+        memcpy(dc, dc_out + (size_t)b * H, (size_t)H * sizeof(double));
+        for (int t = n - 1; t >= 0; --t) {
+            if (dseq)
+                for (int u = 0; u < H; ++u) dh[u] += dseq[((size_t)b * T + t) * H + u];
+            const double* z = zs + (size_t)t * G;
+            const double* cprev = cs + (size_t)t * H;
+            const double* cnew = cs + (size_t)(t + 1) * H;
+            for (int u = 0; u < H; ++u) {
+                const double ig = sig(z[u]), fg = sig(z[H + u]);
+                const double gg = tanh(z[2 * H + u]), og = sig(z[3 * H + u]);
+                const double tc = tanh(cnew[u]);
+                const double d_o = dh[u] * tc;
+                const double dct = dc[u] + dh[u] * og * (1.0 - tc * tc);
+                dz[u] = dct * gg * ig * (1.0 - ig);
+                dz[H + u] = dct * cprev[u] * fg * (1.0 - fg);
+                dz[2 * H + u] = dct * ig * (1.0 - gg * gg);
+                dz[3 * H + u] = d_o * og * (1.0 - og);
+                dc[u] = dct * fg;
+            }
+            for (int j = 0; j < G; ++j) db[j] += dz[j];
+            const float* xt = x + ((size_t)b * T + t) * D;
+            for (int k = 0; k < D; ++k) {      /* dW += x_t^T dz, dx_t = dz W^T */
+                double acc = 0.0;
+                for (int j = 0; j < G; ++j) {
+                    dW[(size_t)k * G + j] += (double)xt[k] * dz[j];
+                    acc += dz[j] * (double)W[(size_t)k * G + j];
+                }
+                dx[((size_t)b * T + t) * D + k] = acc;
+            }
+            const double* hprev = hs + (size_t)t * H;
+            for (int k = 0; k < H; ++k) {      /* dU += h_{t-1}^T dz, dh = dz U^T */
+                double acc = 0.0;
+                for (int j = 0; j < G; ++j) {
+                    dU[(size_t)k * G + j] += hprev[k] * dz[j];
+                    acc += dz[j] * (double)U[(size_t)k * G + j];
+                }
+                nh[k] = acc;
+            }
+            memcpy(dh, nh, (size_t)H * sizeof(double));
+        }
+        memcpy(dh0 + (size_t)b * H, dh, (size_t)H * sizeof(double));
+        memcpy(dc0 + (size_t)b * H, dc, (size_t)H * sizeof(double));
+    }
+    free(zs); free(cs); free(hs); free(dz); free(dh); free(dc); free(nh);
+    return ORACLE_OK;
+}
+
 /* Number of OpenMP threads a call with nthreads <= 0 would use. */
 int lstm_oracle_max_threads(void) {
 #ifdef _OPENMP

@@ -729,3 +729,156 @@ STOP_PINS = [
     spin_brute_force,
     spin_other_cells_match_their_plain_loops,
 ]
+
+
+# ---------------------------------------------------------------------------
+# The backward pass of the masked LSTM loop.  Each pin takes a callable with
+# the signature of ``oracle.backward``.  The loss whose gradients these are is
+#   loss = sum(dh_out * h_final) + sum(dc_out * c_final) + sum(dseq * seq)
+# with seq the output sequence (zero past each length).
+
+def _bwd_case(seed, B, D, H, T, lo=0):
+    x, L, W, U, b, h0, c0 = _stop_case(seed, B, D, H, T, lo=lo)
+    rng = np.random.default_rng(seed + 13)
+    b = (b + rng.standard_normal(b.shape) * 0.3).astype(np.float32)   # every gate's bias non-zero
+    dh = rng.standard_normal((B, H))
+    dc = rng.standard_normal((B, H))
+    ds = rng.standard_normal((B, T, H))
+    return x, L, W, U, b, h0.astype(np.float64), c0.astype(np.float64), dh, dc, ds
+
+
+def _loss(x, L, W, U, b, h0, c0, dh, dc, ds):
+    h, c, seq = oracle.forward(x, L, W, U, b, h0, c0, return_seq=True)
+    return float(np.sum(dh * h) + np.sum(dc * c) + np.sum(ds * seq))
+
+
+def bpin_finite_differences(bwd):
+    """Central differences of the loss, entry by entry, for x (valid steps and
+    padding), W, U, b, h0 and c0.  x, W, U, b are fp32, so each is moved to
+    the neighbouring fp32 values v(1 +- 2^-10) and the difference quotient
+    uses the exact distance between them; agreement to 2e-6 relative."""
+    x, L, W, U, b, h0, c0, dh, dc, ds = _bwd_case(90, 3, 2, 3, 4)
+    L[:] = [4, 2, 0]
+    g = bwd(x, L, W, U, b, h0, c0, dh, dc, ds)
+
+    def check(name, arr, grad, f32):
+        flat = arr.reshape(-1)
+        for i in range(flat.size):
+            v = float(flat[i])
+            if f32:
+                step = max(abs(v), 0.05) * 2.0 ** -10
+                vp, vm = np.float32(v + step), np.float32(v - step)
+            else:
+                step = max(abs(v), 0.05) * 1e-5
+                vp, vm = v + step, v - step
+            flat[i] = vp
+            lp = _loss(x, L, W, U, b, h0, c0, dh, dc, ds)
+            flat[i] = vm
+            lm = _loss(x, L, W, U, b, h0, c0, dh, dc, ds)
+            flat[i] = v
+            fd = (lp - lm) / (float(vp) - float(vm))
+            gi = float(grad.reshape(-1)[i])
+            assert abs(fd - gi) <= 2e-6 * max(1.0, abs(gi)), (name, i, fd, gi)
+
+    check("x", x, g["dx"], True)
+    check("W", W, g["dW"], True)
+    check("U", U, g["dU"], True)
+    check("b", b, g["db"], True)
+    check("h0", h0, g["dh0"], False)
+    check("c0", c0, g["dc0"], False)
+
+
+def bpin_torch_autograd(bwd, shapes=((3, 4, 5, 6), (7, 12, 9, 10))):
+    """Agreement (<= 1e-11) with torch.nn.LSTM's autograd in float64 on packed
+    sequences (weight_ih = W^T, weight_hh = U^T, bias_ih = b, bias_hh = 0),
+    for the same loss: the gradients of the weights (dW = weight_ih.grad^T
+    etc., db = bias_ih.grad), of the padded input, of h0 and of c0."""
+    import torch
+    from torch.nn.utils.rnn import pack_padded_sequence, pad_packed_sequence
+    for k, (B, D, H, T) in enumerate(shapes):
+        x, L, W, U, b, h0, c0, dh, dc, ds = _bwd_case(9200 + k, B, D, H, T, lo=1)
+        g = bwd(x, L, W, U, b, h0, c0, dh, dc, ds)
+        m = torch.nn.LSTM(D, H, batch_first=True).double()
+        with torch.no_grad():
+            m.weight_ih_l0.copy_(torch.from_numpy(W.astype(np.float64).T))
+            m.weight_hh_l0.copy_(torch.from_numpy(U.astype(np.float64).T))
+            m.bias_ih_l0.copy_(torch.from_numpy(b.astype(np.float64)))
+            m.bias_hh_l0.zero_()
+        xt = torch.from_numpy(x.astype(np.float64)).requires_grad_()
+        h0t = torch.from_numpy(h0).requires_grad_()
+        c0t = torch.from_numpy(c0).requires_grad_()
+        packed = pack_padded_sequence(xt, torch.from_numpy(L.astype(np.int64)), batch_first=True,
+                                      enforce_sorted=False)
+        out, (hn, cn) = m(packed, (h0t[None], c0t[None]))
+        out, _ = pad_packed_sequence(out, batch_first=True, total_length=T)
+        loss = (torch.from_numpy(dh) * hn[0]).sum() + (torch.from_numpy(dc) * cn[0]).sum() + \
+               (torch.from_numpy(ds) * out).sum()
+        loss.backward()
+        pairs = [("dW", m.weight_ih_l0.grad.T), ("dU", m.weight_hh_l0.grad.T),
+                 ("db", m.bias_ih_l0.grad), ("dx", xt.grad), ("dh0", h0t.grad), ("dc0", c0t.grad)]
+        for name, ref in pairs:
+            err = np.max(np.abs(g[name] - ref.numpy()))
+            assert err <= 1e-11 * max(1.0, float(np.max(np.abs(ref.numpy())))), (k, name, err)
+
+
+def bpin_masking_facts(bwd):
+    """Padding gets no gradient (dx = 0 exactly at t >= L[b]); a row of length
+    0 passes its upstream gradients to (dh0, dc0) bit for bit and adds nothing
+    to the weight gradients; dseq past a length has no effect."""
+    x, L, W, U, b, h0, c0, dh, dc, ds = _bwd_case(91, 5, 3, 4, 7)
+    L[:] = [7, 0, 3, 5, 0]
+    g = bwd(x, L, W, U, b, h0, c0, dh, dc, ds)
+    for r in range(5):
+        assert not np.any(g["dx"][r, L[r]:]), r
+    for r in (1, 4):
+        assert _bits_equal(g["dh0"][r], dh[r]) and _bits_equal(g["dc0"][r], dc[r])
+    ds2 = ds.copy()
+    for r in range(5):
+        ds2[r, L[r]:] = 1e3
+    g2 = bwd(x, L, W, U, b, h0, c0, dh, dc, ds2)
+    assert all(_bits_equal(g[k], g2[k]) for k in g)
+    keep = [0, 2, 3]                              # the rows of length 0 contribute nothing
+    g3 = bwd(x[keep], L[keep], W, U, b, h0[keep], c0[keep], dh[keep], dc[keep], ds[keep])
+    for k in ("dW", "dU", "db"):
+        assert np.max(np.abs(g[k] - g3[k])) <= 1e-13 * max(1.0, np.max(np.abs(g[k]))), k
+
+
+def bpin_linear_in_upstream(bwd):
+    """The gradients are linear in the upstream gradients:
+    grad(a g1 + g2) = a grad(g1) + grad(g2)."""
+    x, L, W, U, b, h0, c0, dh, dc, ds = _bwd_case(92, 4, 3, 5, 6)
+    rng = np.random.default_rng(93)
+    dh2, dc2, ds2 = rng.standard_normal(dh.shape), rng.standard_normal(dc.shape), rng.standard_normal(ds.shape)
+    a = -1.75
+    g1 = bwd(x, L, W, U, b, h0, c0, dh, dc, ds)
+    g2 = bwd(x, L, W, U, b, h0, c0, dh2, dc2, ds2)
+    g = bwd(x, L, W, U, b, h0, c0, a * dh + dh2, a * dc + dc2, a * ds + ds2)
+    for k in g:
+        ref = a * g1[k] + g2[k]
+        assert np.max(np.abs(g[k] - ref)) <= 1e-12 * max(1.0, np.max(np.abs(ref))), k
+
+
+def bpin_rows_add_up(bwd):
+    """The weight gradients of a batch are the sums of its rows' gradients,
+    and each row's (dx, dh0, dc0) is the batch-of-one result."""
+    x, L, W, U, b, h0, c0, dh, dc, ds = _bwd_case(94, 4, 3, 4, 6, lo=1)
+    g = bwd(x, L, W, U, b, h0, c0, dh, dc, ds)
+    acc = {k: 0.0 for k in ("dW", "dU", "db")}
+    for r in range(4):
+        s = slice(r, r + 1)
+        gr = bwd(x[s], L[s], W, U, b, h0[s], c0[s], dh[s], dc[s], ds[s])
+        for k in acc:
+            acc[k] = acc[k] + gr[k]
+        for k in ("dx", "dh0", "dc0"):
+            assert _bits_equal(gr[k][0], g[k][r]), (k, r)
+    for k in acc:
+        assert np.max(np.abs(g[k] - acc[k])) <= 1e-13 * max(1.0, np.max(np.abs(acc[k]))), k
+
+
+BWD_PINS = [
+    bpin_finite_differences,
+    bpin_torch_autograd,
+    bpin_masking_facts,
+    bpin_linear_in_upstream,
+    bpin_rows_add_up,
+]

@@ -94,3 +94,8 @@ def test_rnn_pin(pin):
 @pytest.mark.parametrize("pin", oracle_pins.STOP_PINS, ids=lambda f: f.__name__)
 def test_stop_pin(pin):
     pin(oracle.forward_stop)
+
+
+@pytest.mark.parametrize("pin", oracle_pins.BWD_PINS, ids=lambda f: f.__name__)
+def test_backward_pin(pin):
+    pin(oracle.backward)

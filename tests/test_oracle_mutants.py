@@ -156,3 +156,37 @@ def test_stop_pins_catch_planted_mistake(name, tmp_path):
             caught.append(pin.__name__)
             break
     assert caught, f"no pin caught mutant {name}"
+
+
+BWD_MUTANTS = {
+    "bwd_cell_gradient_not_carried": ("                dc[u] = dct * fg;\n", "                dc[u] = dct;\n"),
+    "bwd_tanh_derivative_sign": ("const double dct = dc[u] + dh[u] * og * (1.0 - tc * tc);",
+                                 "const double dct = dc[u] + dh[u] * og * (1.0 + tc * tc);"),
+    "bwd_sequence_gradient_ignored": ("for (int u = 0; u < H; ++u) dh[u] += dseq[((size_t)b * T + t) * H + u];",
+                                      "for (int u = 0; u < H; ++u) (void)dseq[((size_t)b * T + t) * H + u];"),
+    "bwd_dU_uses_new_state": ("const double* hprev = hs + (size_t)t * H;", "const double* hprev = hs + (size_t)(t + 1) * H;"),
+    "bwd_forget_gate_uses_new_cell": ("dz[H + u] = dct * cprev[u] * fg * (1.0 - fg);", "dz[H + u] = dct * cnew[u] * fg * (1.0 - fg);"),
+    "bwd_starts_at_padded_end": ("for (int t = n - 1; t >= 0; --t) {", "for (int t = (n > 0 ? T : 0) - 1; t >= 0; --t) {"),
+    "bwd_output_gate_without_derivative": ("dz[3 * H + u] = d_o * og * (1.0 - og);", "dz[3 * H + u] = d_o;"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(BWD_MUTANTS))
+def test_backward_pins_catch_planted_mistake(name, tmp_path):
+    old, new = BWD_MUTANTS[name]
+    src = oracle.source_text()
+    assert src.count(old) == 1, f"mutation anchor for {name} not found exactly once"
+    lib = oracle.compile_variant(src.replace(old, new), str(tmp_path / f"mut_{name}.so"))
+    low = oracle._Lib(lib)
+
+    def bwd(*args, **kw):
+        return oracle.backward(*args, _lib_override=low, **kw)
+    caught = []
+    for pin in oracle_pins.BWD_PINS:
+        try:
+            with np.errstate(all="ignore"):
+                pin(bwd)
+        except (AssertionError, oracle.OracleError):
+            caught.append(pin.__name__)
+            break
+    assert caught, f"no pin caught mutant {name}"
