@@ -454,8 +454,8 @@ int lstm_oracle_backward(int B, int T, int D, int H, const float* x, const int32
         memcpy(hs, h0 + (size_t)b * H, (size_t)H * sizeof(double));
         memcpy(cs, c0 + (size_t)b * H, (size_t)H * sizeof(double));
         for (int t = 0; t < n; ++t) {
-            const float* xt = x + ((size_t)b * T + t) * D;
-            lstm_cell_row(D, H, xt, W, U, bias, hs + (size_t)t * H, cs + (size_t)t * H,
+            const float* xin = &x[((size_t)b * T + t) * D];
+            lstm_cell_row(D, H, xin, W, U, bias, hs + (size_t)t * H, cs + (size_t)t * H,
                           zs + (size_t)t * G, hs + (size_t)(t + 1) * H, cs + (size_t)(t + 1) * H);
         }
         memcpy(dh, dh_out + (size_t)b * H, (size_t)H * sizeof(double));
@@ -479,11 +479,11 @@ int lstm_oracle_backward(int B, int T, int D, int H, const float* x, const int32
                 dc[u] = dct * fg;
             }
             for (int j = 0; j < G; ++j) db[j] += dz[j];
-            const float* xt = x + ((size_t)b * T + t) * D;
+            const float* xin = &x[((size_t)b * T + t) * D];
             for (int k = 0; k < D; ++k) {      /* dW += x_t^T dz, dx_t = dz W^T */
                 double acc = 0.0;
                 for (int j = 0; j < G; ++j) {
-                    dW[(size_t)k * G + j] += (double)xt[k] * dz[j];
+                    dW[(size_t)k * G + j] += (double)xin[k] * dz[j];
                     acc += dz[j] * (double)W[(size_t)k * G + j];
                 }
                 dx[((size_t)b * T + t) * D + k] = acc;
