@@ -20,7 +20,8 @@ __all__ = [
     "lstm_dyn_strerror", "lstm_dyn_plan", "lstm_dyn_check_args", "lstm_dyn_set_option",
     "lstm_dyn_step_trace", "lstm_dyn_forward_seq", "lstm_dyn_check_seq_args",
     "lstm_dyn_create_cell", "lstm_dyn_check_cell_args", "CELL_LSTM", "CELL_GRU", "CELL_RNN",
-    "lstm_dyn_forward_stop", "lstm_dyn_check_stop_args",
+    "lstm_dyn_forward_stop", "lstm_dyn_check_stop_args", "lstm_dyn_forward_train",
+    "lstm_dyn_backward", "lstm_dyn_check_backward_args",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -80,6 +81,12 @@ def _load():
     lib.lstm_dyn_forward_stop.restype = I
     lib.lstm_dyn_check_stop_args.argtypes = [I] * 6 + [P] * 12
     lib.lstm_dyn_check_stop_args.restype = I
+    lib.lstm_dyn_forward_train.argtypes = [P] * 12
+    lib.lstm_dyn_forward_train.restype = I
+    lib.lstm_dyn_backward.argtypes = [P] * 18
+    lib.lstm_dyn_backward.restype = I
+    lib.lstm_dyn_check_backward_args.argtypes = [I] * 5 + [P] * 16
+    lib.lstm_dyn_check_backward_args.restype = I
     lib.lstm_dyn_forward.argtypes = [P] * 11
     lib.lstm_dyn_forward.restype = I
     lib.lstm_dyn_forward_seq.argtypes = [P] * 12
@@ -150,6 +157,29 @@ def lstm_dyn_forward_stop(handle: int, x: int, lengths: int, W: int, U: int, b: 
                                        stream)
     if rc != OK:
         raise LstmDynError(rc, "lstm_dyn_forward_stop")
+
+
+def lstm_dyn_forward_train(handle: int, x: int, lengths: int, W: int, U: int, b: int, h0: int,
+                           c0: int, out_h: int, out_c: int, out_seq: int = 0, stream: int = 0) -> None:
+    rc = _load().lstm_dyn_forward_train(handle, x, lengths, W, U, b, h0, c0, out_h, out_c, out_seq,
+                                        stream)
+    if rc != OK:
+        raise LstmDynError(rc, "lstm_dyn_forward_train")
+
+
+def lstm_dyn_backward(handle: int, x: int, lengths: int, W: int, U: int, b: int, h0: int, c0: int,
+                      d_out_h: int, d_out_c: int, d_seq: int, dx: int, dW: int, dU: int, db: int,
+                      dh0: int, dc0: int, stream: int = 0) -> None:
+    rc = _load().lstm_dyn_backward(handle, x, lengths, W, U, b, h0, c0, d_out_h, d_out_c, d_seq,
+                                   dx, dW, dU, db, dh0, dc0, stream)
+    if rc != OK:
+        raise LstmDynError(rc, "lstm_dyn_backward")
+
+
+def lstm_dyn_check_backward_args(B: int, D: int, H: int, T_max: int, dtype: int, *ptrs) -> int:
+    """Pointers in the order of lstm_dyn_backward: x, lengths, W, U, b, h0, c0,
+    d_out_h, d_out_c, d_seq, dx, dW, dU, db, dh0, dc0."""
+    return _load().lstm_dyn_check_backward_args(B, D, H, T_max, dtype, *ptrs)
 
 
 def lstm_dyn_destroy(handle: int) -> None:
@@ -324,6 +354,45 @@ class LstmDyn:
                               out_steps.data_ptr(),
                               out_seq.data_ptr() if out_seq is not None else 0, s)
         return (out_h, out_c, out_steps) if out_seq is None else (out_h, out_c, out_steps, out_seq)
+
+    def forward_train(self, x, lengths, W, U, b, h0, c0, out_h=None, out_c=None, out_seq=None,
+                      with_seq=False, stream=None):
+        """``forward`` that also keeps what ``backward`` needs (LSTM handles).
+        Returns (out_h, out_c) and, with ``with_seq`` or a given ``out_seq``,
+        the output sequence after them."""
+        import torch
+        c0p, out_h, out_c, s = self._inputs(x, lengths, W, U, b, h0, c0, out_h, out_c, stream)
+        if out_seq is None and with_seq:
+            out_seq = torch.empty((self.B, self.T, self.H), dtype=torch.float32, device=x.device)
+        if out_seq is not None:
+            self._check("out_seq", out_seq, torch.float32, (self.B, self.T, self.H))
+        lstm_dyn_forward_train(self.handle, x.data_ptr(), lengths.data_ptr(), W.data_ptr(),
+                               U.data_ptr(), b.data_ptr(), h0.data_ptr(), c0p, out_h.data_ptr(),
+                               out_c.data_ptr(), out_seq.data_ptr() if out_seq is not None else 0, s)
+        return (out_h, out_c) if out_seq is None else (out_h, out_c, out_seq)
+
+    def backward(self, x, lengths, W, U, b, h0, c0, d_out_h, d_out_c, d_seq=None, stream=None):
+        """Gradients after ``forward_train`` with the same inputs; returns a
+        dict of float32 tensors dx [B, T, D], dW [D, 4H], dU [H, 4H], db [4H],
+        dh0, dc0 [B, H]."""
+        import torch
+        B, D, H, T = self.B, self.D, self.H, self.T
+        dev = x.device
+        for name, t, shape in (("d_out_h", d_out_h, (B, H)), ("d_out_c", d_out_c, (B, H))):
+            self._check(name, t, torch.float32, shape)
+        if d_seq is not None:
+            self._check("d_seq", d_seq, torch.float32, (B, T, H))
+        out = {"dx": torch.empty((B, T, D), device=dev), "dW": torch.empty((D, 4 * H), device=dev),
+               "dU": torch.empty((H, 4 * H), device=dev), "db": torch.empty((4 * H,), device=dev),
+               "dh0": torch.empty((B, H), device=dev), "dc0": torch.empty((B, H), device=dev)}
+        if stream is None:
+            stream = torch.cuda.current_stream(dev)
+        s = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+        lstm_dyn_backward(self.handle, x.data_ptr(), lengths.data_ptr(), W.data_ptr(), U.data_ptr(),
+                          b.data_ptr(), h0.data_ptr(), c0.data_ptr(), d_out_h.data_ptr(),
+                          d_out_c.data_ptr(), d_seq.data_ptr() if d_seq is not None else 0,
+                          *(out[k].data_ptr() for k in ("dx", "dW", "dU", "db", "dh0", "dc0")), s)
+        return out
 
     def query(self, what: int) -> int:
         return lstm_dyn_query(self.handle, what)

@@ -4,8 +4,29 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <rocblas/rocblas.h>
+
 #include "../../include/lstm_dyn.h"
 #include "launch.h"
+
+// Workspace of the forward for training and the backward pass, allocated at
+// the first lstm_dyn_forward_train of a handle.
+struct TrainWs {
+    void* block;
+    float* save_h;  // [B*T][H] the state each step started from, compact rows
+    float* save_c;  // [B*T][H]
+    float* xc;      // [B*T][D] x in compact rows (fp32), then the rows of dx
+    float* w_il;    // [D][4H] W in fp32, gate-interleaved columns
+    float* u_il;    // [H][4H]
+    float* dw_il;   // [D][4H] weight gradients, gate-interleaved columns
+    float* du_il;   // [H][4H]
+    float* db_il;   // [4H]
+    float* dH;      // [B][H] gradient of h in slot order
+    float* dC;      // [B][H]
+    float* z;       // [bpad][4H] per-step pre-activations (handles not in per-step mode)
+    int32_t* host_offsets;  // pinned [T + 2]: step offsets, then the sum of lengths
+    rocblas_handle rb;
+};
 
 using namespace ldyn;
 
@@ -23,6 +44,9 @@ struct lstm_dyn {
     int32_t* host_maxlen;      // pinned host words for the per-step path: [0] loop bound,
                                // [1] rows still running, [2] iterations run
     int stop_ok;               // the persistent variant with termination from the state fits
+    int save_ok;               // the persistent variant of the forward for training fits
+    TrainWs* train;            // null until the first forward for training
+    int saved;                 // 1: the workspace holds a forward for training not yet used
     unsigned long long timeout_ticks;
     int inproj_grid;
     long long launches_last;
@@ -261,7 +285,7 @@ extern "C" int lstm_dyn_create_cell(lstm_dyn_t** out, int B, int D, int H, int T
     rc = lstm_dyn_plan(B, D, H, T, dtype, mode, cus, &plan);
     if (rc != LSTM_DYN_OK) return rc;
     const int bf16 = dtype == LSTM_DYN_BF16;
-    int stop_ok = 1;
+    int stop_ok = 1, save_ok = 1;
     if (mode == LSTM_DYN_PERSISTENT && !plan.single) {
         const int per_cu = persistent_blocks_per_cu(bf16, plan.mt, plan.ksw, plan.kw, plan.nstate,
                                                     plan.lds_bytes, cell, 0);
@@ -269,11 +293,17 @@ extern "C" int lstm_dyn_create_cell(lstm_dyn_t** out, int B, int D, int H, int T
         const int per_cu_stop = persistent_blocks_per_cu(bf16, plan.mt, plan.ksw, plan.kw,
                                                          plan.nstate, plan.lds_bytes, cell, 1);
         stop_ok = per_cu_stop >= 1 && plan.groups <= per_cu_stop * cus;
+        if (cell == LSTM_DYN_CELL_LSTM) {
+            const int per_cu_save = persistent_blocks_per_cu(bf16, plan.mt, plan.ksw, plan.kw,
+                                                             plan.nstate, plan.lds_bytes, cell, 2);
+            save_ok = per_cu_save >= 1 && plan.groups <= per_cu_save * cus;
+        }
     }
     lstm_dyn* h = new (std::nothrow) lstm_dyn();
     if (!h) return LSTM_DYN_ERR_NOMEM;
     h->B = B; h->D = D; h->H = H; h->T = T; h->dtype = dtype; h->mode = mode; h->cell = cell;
     h->stop_ok = stop_ok;
+    h->save_ok = save_ok;
     h->device = dev;
     h->num_cus = cus;
     h->plan = plan;
@@ -384,6 +414,14 @@ extern "C" int lstm_dyn_destroy(lstm_dyn_t* h) {
         if (e && hipEventDestroy(e) != hipSuccess) rc = LSTM_DYN_ERR_HIP;
     if (h->host_maxlen && hipHostFree(h->host_maxlen) != hipSuccess) rc = LSTM_DYN_ERR_HIP;
     if (h->trace && hipFree(h->trace) != hipSuccess) rc = LSTM_DYN_ERR_HIP;
+    if (h->train) {
+        if (h->train->rb && rocblas_destroy_handle(h->train->rb) != rocblas_status_success)
+            rc = LSTM_DYN_ERR_HIP;
+        if (h->train->block && hipFree(h->train->block) != hipSuccess) rc = LSTM_DYN_ERR_HIP;
+        if (h->train->host_offsets && hipHostFree(h->train->host_offsets) != hipSuccess)
+            rc = LSTM_DYN_ERR_HIP;
+        delete h->train;
+    }
     delete h;
     return rc;
 }
@@ -412,6 +450,7 @@ static int forward_impl(lstm_dyn_t* h, const void* x, const int32_t* lengths, co
     hipStream_t s = static_cast<hipStream_t>(stream);
     h->last_stream = s;
     h->launches_last = 0;
+    h->saved = 0;  // this forward overwrites what a forward for training kept
     const Dims& d = h->dims;
 #define LD_CHECK(call)                                   \
     do {                                                 \
@@ -589,6 +628,250 @@ extern "C" int lstm_dyn_forward_stop(lstm_dyn_t* h, const void* x, const int32_t
     if (stop_c != stop_c) return LSTM_DYN_ERR_INVALID;  // NaN
     const StopArgs stop{stop_v, stop_c, out_steps, lengths};
     return forward_impl(h, x, lengths, W, U, b, h0, c0, out_h, out_c, out_seq, &stop, stream);
+}
+
+// ---------------------------------------------------------------------------
+// Forward for training and the backward pass (LSTM handles).
+
+static int ensure_train(lstm_dyn* h) {
+    if (h->train) return LSTM_DYN_OK;
+    TrainWs* tw = new (std::nothrow) TrainWs();
+    if (!tw) return LSTM_DYN_ERR_NOMEM;
+    const long long B = h->B, D = h->D, H = h->H, T = h->T, bpad = h->dims.bpad;
+    long long o = 0;
+    auto take = [&](long long bytes) {
+        const long long at = o;
+        o = align_up(o + bytes, 256);
+        return at;
+    };
+    const long long oh = take(4 * B * T * H), oc = take(4 * B * T * H), ox = take(4 * B * T * D),
+                    ow = take(4 * D * 4 * H), ou = take(4 * H * 4 * H), odw = take(4 * D * 4 * H),
+                    odu = take(4 * H * 4 * H), odb = take(16 * H), odh = take(4 * B * H),
+                    odc = take(4 * B * H), oz = take(16 * H * bpad);
+    if (hipMalloc(&tw->block, (size_t)o) != hipSuccess) {
+        (void)hipGetLastError();
+        delete tw;
+        return LSTM_DYN_ERR_NOMEM;
+    }
+    char* base = static_cast<char*>(tw->block);
+    tw->save_h = reinterpret_cast<float*>(base + oh);
+    tw->save_c = reinterpret_cast<float*>(base + oc);
+    tw->xc = reinterpret_cast<float*>(base + ox);
+    tw->w_il = reinterpret_cast<float*>(base + ow);
+    tw->u_il = reinterpret_cast<float*>(base + ou);
+    tw->dw_il = reinterpret_cast<float*>(base + odw);
+    tw->du_il = reinterpret_cast<float*>(base + odu);
+    tw->db_il = reinterpret_cast<float*>(base + odb);
+    tw->dH = reinterpret_cast<float*>(base + odh);
+    tw->dC = reinterpret_cast<float*>(base + odc);
+    tw->z = reinterpret_cast<float*>(base + oz);
+    if (hipHostMalloc(reinterpret_cast<void**>(&tw->host_offsets), (size_t)(T + 2) * sizeof(int32_t),
+                      hipHostMallocDefault) != hipSuccess) {
+        (void)hipFree(tw->block);
+        delete tw;
+        return LSTM_DYN_ERR_HIP;
+    }
+    if (rocblas_create_handle(&tw->rb) != rocblas_status_success) {
+        (void)hipFree(tw->block);
+        (void)hipHostFree(tw->host_offsets);
+        delete tw;
+        return LSTM_DYN_ERR_HIP;
+    }
+    h->train = tw;
+    h->workspace += o;
+    return LSTM_DYN_OK;
+}
+
+extern "C" int lstm_dyn_forward_train(lstm_dyn_t* h, const void* x, const int32_t* lengths,
+                                      const void* W, const void* U, const float* b,
+                                      const float* h0, const float* c0, float* out_h,
+                                      float* out_c, float* out_seq, void* stream) {
+    if (!h) return LSTM_DYN_ERR_INVALID;
+    const int rc = out_seq ? check_seq_args_cell(h->B, h->D, h->H, h->T, h->dtype, h->cell, x,
+                                                 lengths, W, U, b, h0, c0, out_h, out_c, out_seq)
+                           : check_args_cell(h->B, h->D, h->H, h->T, h->dtype, h->cell, x, lengths,
+                                             W, U, b, h0, c0, out_h, out_c);
+    if (rc != LSTM_DYN_OK) return rc;
+    if (h->cell != LSTM_DYN_CELL_LSTM) return LSTM_DYN_ERR_UNSUPPORTED;
+    if (out_h == h0 || out_c == c0) return LSTM_DYN_ERR_INVALID;  // the backward reads h0, c0
+    const int trc = ensure_train(h);
+    if (trc != LSTM_DYN_OK) return trc;
+    TrainWs* tw = h->train;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    h->last_stream = s;
+    h->launches_last = 0;
+    h->saved = 0;
+    const Dims& d = h->dims;
+#define LD_CHECK(call)              \
+    do {                            \
+        if ((call) != hipSuccess) { \
+            (void)hipGetLastError(); \
+            return LSTM_DYN_ERR_HIP; \
+        }                           \
+    } while (0)
+    auto mark = [&](int i) { return h->timing ? hipEventRecord(h->ev[i], s) : hipSuccess; };
+    LD_CHECK(mark(0));
+    LD_CHECK(launch_prep(d, lengths, h->ws, s));
+    LD_CHECK(mark(1));
+    h->launches_last = 1;
+    if (h->mode == LSTM_DYN_PERSISTENT && !h->plan.single && h->save_ok) {
+        LD_CHECK(input_projection(h, x, W, b, s));
+        LD_CHECK(mark(2));
+        PersistentConfig pc{h->plan.mt,     h->plan.groups,    h->plan.ksw, h->plan.kw,
+                            h->plan.nstate, h->plan.lds_bytes, h->timeout_ticks, h->trace,
+                            0,              nullptr,           tw->save_h,  tw->save_c};
+        LD_CHECK(launch_persistent(d, pc, U, h0, c0, out_h, out_c, h->ws, s));
+        h->launches_last++;
+    } else {
+        // the per-step kernels (single-workgroup sizes, per-step handles)
+        Workspace ws = h->ws;
+        if (!ws.z) ws.z = tw->z;
+        LD_CHECK(launch_step_init(d, h0, c0, out_h, out_c, ws, s));
+        h->launches_last++;
+        LD_CHECK(input_projection(h, x, W, b, s));
+        LD_CHECK(mark(2));
+        LD_CHECK(hipMemcpyAsync(h->host_maxlen, &ws.meta->max_len, sizeof(int32_t),
+                                hipMemcpyDeviceToHost, s));
+        LD_CHECK(hipStreamSynchronize(s));
+        const int max_len = *h->host_maxlen;
+        for (int t = 0; t < max_len; ++t) {
+            LD_CHECK(launch_step_gemm(d, t, U, ws, s));
+            LD_CHECK(launch_step_gates(d, t, out_h, out_c, nullptr, false, ws, s, tw->save_h, tw->save_c));
+            h->launches_last += 2;
+        }
+    }
+    LD_CHECK(mark(3));
+    if (out_seq) {
+        LD_CHECK(launch_seq_from_saved(d, out_seq, tw->save_h, out_h, lengths, h->ws, h->num_cus, s));
+        h->launches_last++;
+    }
+#undef LD_CHECK
+    h->saved = 1;
+    return LSTM_DYN_OK;
+}
+
+static int check_backward_args(int B, int D, int H, int T, int dtype, const void* x,
+                               const int32_t* lengths, const void* W, const void* U,
+                               const float* b, const float* h0, const float* c0,
+                               const float* d_out_h, const float* d_out_c, const float* d_seq,
+                               const float* dx, const float* dW, const float* dU,
+                               const float* db, const float* dh0, const float* dc0) {
+    if (B < 1 || D < 1 || H < 1 || T < 1) return LSTM_DYN_ERR_INVALID;
+    if (dtype != LSTM_DYN_F32 && dtype != LSTM_DYN_BF16) return LSTM_DYN_ERR_INVALID;
+    const void* ins[] = {x, lengths, W, U, b, h0, c0, d_out_h, d_out_c, d_seq};
+    const void* outs[] = {dx, dW, dU, db, dh0, dc0};
+    const long long e = dtype == LSTM_DYN_BF16 ? 2 : 4;
+    const long long nin[] = {(long long)B * T * D * e, 4LL * B, (long long)D * 4 * H * e,
+                             (long long)H * 4 * H * e, 16LL * H, 4LL * B * H, 4LL * B * H,
+                             4LL * B * H, 4LL * B * H, d_seq ? 4LL * B * T * H : 0};
+    const long long nout[] = {4LL * B * T * D, 16LL * D * H, 16LL * H * H, 16LL * H, 4LL * B * H,
+                              4LL * B * H};
+    for (int i = 0; i < 10; ++i) {
+        if (!ins[i] && i != 9) return LSTM_DYN_ERR_INVALID;
+        if (ins[i] && (reinterpret_cast<uintptr_t>(ins[i]) & 3)) return LSTM_DYN_ERR_INVALID;
+    }
+    for (int i = 0; i < 6; ++i) {
+        if (!outs[i] || (reinterpret_cast<uintptr_t>(outs[i]) & 3)) return LSTM_DYN_ERR_INVALID;
+        for (int j = 0; j < 10; ++j)
+            if (ins[j] && overlaps(outs[i], nout[i], ins[j], nin[j])) return LSTM_DYN_ERR_INVALID;
+        for (int j = 0; j < i; ++j)
+            if (overlaps(outs[i], nout[i], outs[j], nout[j])) return LSTM_DYN_ERR_INVALID;
+    }
+    return LSTM_DYN_OK;
+}
+
+extern "C" int lstm_dyn_check_backward_args(int B, int D, int H, int T, int dtype, const void* x,
+                                            const int32_t* lengths, const void* W, const void* U,
+                                            const float* b, const float* h0, const float* c0,
+                                            const float* d_out_h, const float* d_out_c,
+                                            const float* d_seq, const float* dx, const float* dW,
+                                            const float* dU, const float* db, const float* dh0,
+                                            const float* dc0) {
+    return check_backward_args(B, D, H, T, dtype, x, lengths, W, U, b, h0, c0, d_out_h, d_out_c,
+                               d_seq, dx, dW, dU, db, dh0, dc0);
+}
+
+extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* lengths,
+                                 const void* W, const void* U, const float* b, const float* h0,
+                                 const float* c0, const float* d_out_h, const float* d_out_c,
+                                 const float* d_seq, float* dx, float* dW, float* dU, float* db,
+                                 float* dh0, float* dc0, void* stream) {
+    if (!h) return LSTM_DYN_ERR_INVALID;
+    const int rc = check_backward_args(h->B, h->D, h->H, h->T, h->dtype, x, lengths, W, U, b, h0,
+                                       c0, d_out_h, d_out_c, d_seq, dx, dW, dU, db, dh0, dc0);
+    if (rc != LSTM_DYN_OK) return rc;
+    if (h->cell != LSTM_DYN_CELL_LSTM) return LSTM_DYN_ERR_UNSUPPORTED;
+    if (!h->saved || !h->train) return LSTM_DYN_ERR_INVALID;  // needs a forward for training
+    TrainWs* tw = h->train;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    h->last_stream = s;
+    h->launches_last = 0;
+    h->saved = 0;  // the backward overwrites the kept pre-activations
+    const Dims& d = h->dims;
+    const int H4 = 4 * d.H;
+#define LD_CHECK(call)              \
+    do {                            \
+        if ((call) != hipSuccess) { \
+            (void)hipGetLastError(); \
+            return LSTM_DYN_ERR_HIP; \
+        }                           \
+    } while (0)
+#define RB_CHECK(call)                                 \
+    do {                                               \
+        if ((call) != rocblas_status_success) return LSTM_DYN_ERR_HIP; \
+    } while (0)
+    RB_CHECK(rocblas_set_stream(tw->rb, s));
+    // step offsets and the sum of lengths of the forward, on the host
+    LD_CHECK(hipMemcpyAsync(tw->host_offsets, h->ws.offsets, (size_t)(d.T + 1) * sizeof(int32_t),
+                            hipMemcpyDeviceToHost, s));
+    LD_CHECK(hipMemcpyAsync(tw->host_offsets + d.T + 1, &h->ws.meta->total_rows, sizeof(int32_t),
+                            hipMemcpyDeviceToHost, s));
+    LD_CHECK(hipMemcpyAsync(h->host_maxlen, &h->ws.meta->max_len, sizeof(int32_t),
+                            hipMemcpyDeviceToHost, s));
+    LD_CHECK(hipStreamSynchronize(s));
+    const int32_t* off = tw->host_offsets;
+    const int rows = off[d.T + 1], max_len = *h->host_maxlen;
+    const float one = 1.0f, zero = 0.0f;
+    LD_CHECK(launch_bwd_weights(d, W, d.D, tw->w_il, s));
+    LD_CHECK(launch_bwd_weights(d, U, d.H, tw->u_il, s));
+    LD_CHECK(launch_bwd_init(d, d_out_h, d_out_c, tw->dH, tw->dC, h->ws, s));
+    h->launches_last += 3;
+    for (int t = max_len - 1; t >= 0; --t) {
+        const int act = off[t + 1] - off[t];
+        LD_CHECK(launch_bwd_cell(d, t, act, tw->save_c, d_seq, tw->dH, tw->dC, h->ws, s));
+        // dH[0:act] = dz_t U^T (column-major: dH^T = U_il^T-as-stored^T dz_t^T)
+        RB_CHECK(rocblas_sgemm(tw->rb, rocblas_operation_transpose, rocblas_operation_none, d.H,
+                               act, H4, &one, tw->u_il, H4, h->ws.gx + (size_t)off[t] * H4, H4,
+                               &zero, tw->dH, d.H));
+        h->launches_last += 2;
+    }
+    LD_CHECK(launch_bwd_state_out(d, tw->dH, tw->dC, dh0, dc0, h->ws, s));
+    h->launches_last++;
+    if (rows > 0) {
+        LD_CHECK(launch_bwd_gather_x(d, x, rows, tw->xc, h->ws, s));
+        // dW = X^T dz, dU = H_prev^T dz (K = the sum of lengths)
+        RB_CHECK(rocblas_sgemm(tw->rb, rocblas_operation_none, rocblas_operation_transpose, H4,
+                               d.D, rows, &one, h->ws.gx, H4, tw->xc, d.D, &zero, tw->dw_il, H4));
+        RB_CHECK(rocblas_sgemm(tw->rb, rocblas_operation_none, rocblas_operation_transpose, H4,
+                               d.H, rows, &one, h->ws.gx, H4, tw->save_h, d.H, &zero, tw->du_il, H4));
+        LD_CHECK(launch_bwd_colsum(d, tw->db_il, h->ws, s));
+        // dx rows = dz W^T, over the gathered x (already used)
+        RB_CHECK(rocblas_sgemm(tw->rb, rocblas_operation_transpose, rocblas_operation_none, d.D,
+                               rows, H4, &one, tw->w_il, H4, h->ws.gx, H4, &zero, tw->xc, d.D));
+        h->launches_last += 5;
+    } else {
+        LD_CHECK(hipMemsetAsync(tw->dw_il, 0, (size_t)d.D * H4 * sizeof(float), s));
+        LD_CHECK(hipMemsetAsync(tw->du_il, 0, (size_t)d.H * H4 * sizeof(float), s));
+        LD_CHECK(hipMemsetAsync(tw->db_il, 0, (size_t)H4 * sizeof(float), s));
+    }
+    LD_CHECK(launch_bwd_permute(d, tw->dw_il, dW, d.D, s));
+    LD_CHECK(launch_bwd_permute(d, tw->du_il, dU, d.H, s));
+    LD_CHECK(launch_bwd_permute(d, tw->db_il, db, 1, s));
+    LD_CHECK(launch_bwd_dx(d, tw->xc, rows, lengths, dx, h->ws, s));
+    h->launches_last += 4;
+#undef RB_CHECK
+#undef LD_CHECK
+    return LSTM_DYN_OK;
 }
 
 extern "C" int lstm_dyn_query(lstm_dyn_t* h, int what, long long* value) {

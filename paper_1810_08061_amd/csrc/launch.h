@@ -73,14 +73,17 @@ struct PersistentConfig {
     unsigned long long* trace;         // per-step timestamps (diagnostics) or null
     int seq;                           // 1: keep each step's h in the dead Gx rows (output sequence)
     const StopArgs* stop;              // termination from the state, or null
+    float* save_h;                     // forward for training: the state each step starts from,
+    float* save_c;                     // [compact rows][H] (z is kept in place of Gx); else null
 };
 constexpr int BAR_WORDS = 64 * 9;  // global + 8 group counters, 256 bytes apart
 hipError_t launch_persistent(const Dims& d, const PersistentConfig& pc, const void* U,
                              const float* h0, const float* c0, float* out_h, float* out_c,
                              const Workspace& ws, hipStream_t s);
 // Occupancy check for the co-resident grid; returns blocks per CU (0 if none).
+// mode: 0 plain, 1 termination from the state, 2 forward for training (LSTM only)
 int persistent_blocks_per_cu(int bf16, int mt, int ksw, int kw, int nst, int lds_bytes, int cell,
-                             int stop);
+                             int mode);
 // Compiled variant with exactly (mt, kw, ksw) and the smallest state capacity >= nstate.
 bool persistent_pick_variant(int bf16, int mt, int kw, int ksw, int nstate, int* nst);
 int persistent_lds_bytes(int bf16, int mt, int kw, int nst, int hpad);
@@ -97,7 +100,8 @@ hipError_t launch_step_init(const Dims& d, const float* h0, const float* c0, flo
                             float* out_c, const Workspace& ws, hipStream_t s);
 hipError_t launch_step_gemm(const Dims& d, int t, const void* U, const Workspace& ws, hipStream_t s);
 hipError_t launch_step_gates(const Dims& d, int t, float* out_h, float* out_c, float* seq,
-                             bool stop, const Workspace& ws, hipStream_t s);
+                             bool stop, const Workspace& ws, hipStream_t s,
+                             float* save_h = nullptr, float* save_c = nullptr);
 // Termination from the state on the per-step path: init (steps = caps, no row
 // ended, counters zero), then after the gates of each step the halting scores
 // of the rows that ran; running[t] counts the rows that run at step t + 1.
@@ -105,6 +109,26 @@ hipError_t launch_step_stop_init(const Dims& d, const StopArgs& stop, const Work
                                  hipStream_t s);
 hipError_t launch_step_stop(const Dims& d, int t, const StopArgs& stop, const Workspace& ws,
                             hipStream_t s);
+
+// Backward pass (bwd.hip).
+hipError_t launch_bwd_weights(const Dims& d, const void* W, int rows, float* Wil, hipStream_t s);
+hipError_t launch_bwd_init(const Dims& d, const float* dh_out, const float* dc_out, float* dH,
+                           float* dC, const Workspace& ws, hipStream_t s);
+hipError_t launch_bwd_cell(const Dims& d, int t, int act, const float* save_c, const float* dseq,
+                           float* dH, float* dC, const Workspace& ws, hipStream_t s);
+hipError_t launch_bwd_state_out(const Dims& d, const float* dH, const float* dC, float* dh0,
+                                float* dc0, const Workspace& ws, hipStream_t s);
+hipError_t launch_bwd_gather_x(const Dims& d, const void* x, long rows, float* xc,
+                               const Workspace& ws, hipStream_t s);
+hipError_t launch_bwd_colsum(const Dims& d, float* db_il, const Workspace& ws, hipStream_t s);
+hipError_t launch_bwd_permute(const Dims& d, const float* il, float* out, int rows, hipStream_t s);
+hipError_t launch_bwd_dx(const Dims& d, const float* dxc, long rows, const int32_t* lengths,
+                         float* dx, const Workspace& ws, hipStream_t s);
+// Forward for training from the saved state: out_seq[b][t] for t < L[b]
+// (the state after step t is the one step t + 1 started from, or out_h).
+hipError_t launch_seq_from_saved(const Dims& d, float* seq, const float* save_h, const float* out_h,
+                                 const int32_t* lengths, const Workspace& ws, int num_cus,
+                                 hipStream_t s);
 
 // Output sequence: moves the persistent loop's step outputs (kept in the
 // dead Gx rows, unit slices of upw) to seq [B][T][H] when from_gx, and

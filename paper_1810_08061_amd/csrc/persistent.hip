@@ -59,7 +59,15 @@ struct PersistParams {
     int32_t* steps;             // [B], batch order; written by workgroup 0
     const int32_t* lengths;     // [B] caps (clamped to [0, T] here)
     int T;
+    // Forward for training (variants with SAVE): each step keeps, per compact
+    // row, the pre-activations z in place of the row's Gx and the state the
+    // step started from in save_h, save_c ([rows][H], fp32).
+    float* save_h;
+    float* save_c;
 };
+
+// What a variant of the loop does besides the plain forward.
+enum LoopMode { LM_PLAIN = 0, LM_STOP = 1, LM_SAVE = 2 };
 
 // Logical workgroup index: consecutive workgroups are dispatched to different
 // XCDs (round robin over 8); give the workgroups of one XCD adjacent unit
@@ -217,9 +225,11 @@ struct PLayout {
     static constexpr int BYTES = (NTC * KW * MT + GX_KB) * 1024;
 };
 
-template <typename E, int MT, int KSW, int KW, int NST, int CELL, bool STOP>
+template <typename E, int MT, int KSW, int KW, int NST, int CELL, int LMODE>
 __global__ void __launch_bounds__(KW * 64, 1)
 persistent_kernel(PersistParams p) {
+    constexpr bool STOP = LMODE == LM_STOP;
+    constexpr bool SAVE = LMODE == LM_SAVE;
     using S = typename E::store_t;
     using F = typename E::frag_t;
     using IO = HxIO<E>;
@@ -688,6 +698,13 @@ persistent_kernel(PersistParams p) {
                         const f32x4_t z = pv[0];
                         const int s = (j + ntc0) * 16 + (lo & 15);
                         const bool live = s < act;
+                        if constexpr (SAVE) {
+                            // z in place of this pair's Gx (its prefetch has landed);
+                            // a redo pass stores again, last
+                            const int u = u0 + mt * 4 + (lo >> 4);
+                            if (live && u < H)
+                                *reinterpret_cast<f32x4_t*>(const_cast<float*>(p.gx) + (size_t)(o0 + s) * H4 + 4 * u) = z;
+                        }
                         nan |= live & ((z[0] != z[0]) | (z[1] != z[1]) | (z[2] != z[2]) | (z[3] != z[3]));
                         float c = cst[i], h = hst[i];
                         apply_cell(CELL, z, c, h);  // CELL is a template argument: no branch
@@ -731,6 +748,12 @@ persistent_kernel(PersistParams p) {
                     for (int mt = 0; mt < MT; ++mt) {
                         const int i = a * MT + mt;
                         const int s = nt * 16 + (lo & 15), u = u0 + mt * 4 + (lo >> 4);
+                        if constexpr (SAVE) {
+                            if (s < act && u < H) {  // the state this step started from
+                                p.save_h[(size_t)(o0 + s) * H + u] = hst[i];
+                                p.save_c[(size_t)(o0 + s) * H + u] = cst[i];
+                            }
+                        }
                         if (s < act && u < H && runs) {
                             cst[i] = cn[i];
                             hst[i] = hn[i];
@@ -814,13 +837,14 @@ persistent_kernel(PersistParams p) {
 // capacity that covers the batch.
 typedef void (*persist_fn)(PersistParams);
 
-// f[cell][stop]: the variant compiled for each CellKind, with and without
-// termination from the state, so the gate step has no branch on either (a
-// uniform branch on the cell there cost about 4% of the loop).
-struct Variant { int bf16, mt, ksw, kw, nst, lds_bytes; persist_fn f[3][2]; };
+// f[cell][mode]: the variant compiled for each CellKind and LoopMode, so the
+// gate step has no branch on either (a uniform branch on the cell there cost
+// about 4% of the loop).  The forward for training exists for the LSTM only.
+struct Variant { int bf16, mt, ksw, kw, nst, lds_bytes; persist_fn f[3][3]; };
 
-#define PV_CELL(ET, MT, KS, KW, NS, C) \
-    {persistent_kernel<ET, MT, KS, KW, NS, C, false>, persistent_kernel<ET, MT, KS, KW, NS, C, true>}
+#define PV_CELL(ET, MT, KS, KW, NS, C)                                                       \
+    {persistent_kernel<ET, MT, KS, KW, NS, C, LM_PLAIN>, persistent_kernel<ET, MT, KS, KW, NS, C, LM_STOP>, \
+     C == CELL_LSTM ? persistent_kernel<ET, MT, KS, KW, NS, CELL_LSTM, LM_SAVE> : nullptr}
 #define PV(BF, ET, MT, KS, KW, NS)                                             \
     {BF, MT, KS, KW, NS, PLayout<MT, KW, NS>::BYTES,                            \
      {PV_CELL(ET, MT, KS, KW, NS, CELL_LSTM), PV_CELL(ET, MT, KS, KW, NS, CELL_GRU), \
@@ -838,11 +862,11 @@ static const Variant kVariants[] = {
 #undef PV
 #undef PV_CELL
 
-static persist_fn find_variant(int bf16, int mt, int ksw, int kw, int nst, int cell, int stop) {
-    if (cell < CELL_LSTM || cell > CELL_RNN) return nullptr;
+static persist_fn find_variant(int bf16, int mt, int ksw, int kw, int nst, int cell, int mode) {
+    if (cell < CELL_LSTM || cell > CELL_RNN || mode < LM_PLAIN || mode > LM_SAVE) return nullptr;
     for (const Variant& v : kVariants)
         if (v.bf16 == bf16 && v.mt == mt && v.ksw == ksw && v.kw == kw && v.nst == nst)
-            return v.f[cell][stop ? 1 : 0];
+            return v.f[cell][mode];
     return nullptr;
 }
 
@@ -868,8 +892,8 @@ int persistent_lds_bytes(int bf16, int mt, int kw, int nst, int hpad) {
 }
 
 int persistent_blocks_per_cu(int bf16, int mt, int ksw, int kw, int nst, int lds_bytes, int cell,
-                             int stop) {
-    persist_fn f = find_variant(bf16, mt, ksw, kw, nst, cell, stop);
+                             int mode) {
+    persist_fn f = find_variant(bf16, mt, ksw, kw, nst, cell, mode);
     if (!f) return 0;
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(f),
                             hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes) != hipSuccess)
@@ -884,7 +908,8 @@ int persistent_blocks_per_cu(int bf16, int mt, int ksw, int kw, int nst, int lds
 hipError_t launch_persistent(const Dims& d, const PersistentConfig& pc, const void* U,
                              const float* h0, const float* c0, float* out_h, float* out_c,
                              const Workspace& ws, hipStream_t s) {
-    persist_fn f = find_variant(d.bf16, pc.mt, pc.ksw, pc.kw, pc.nst, d.cell, pc.stop != nullptr);
+    const int mode = pc.stop ? LM_STOP : pc.save_h ? LM_SAVE : LM_PLAIN;
+    persist_fn f = find_variant(d.bf16, pc.mt, pc.ksw, pc.kw, pc.nst, d.cell, mode);
     if (!f) return hipErrorInvalidValue;
     PersistParams p{};
     p.U = U;
@@ -906,6 +931,8 @@ hipError_t launch_persistent(const Dims& d, const PersistentConfig& pc, const vo
     p.timeout_ticks = pc.timeout_ticks;
     p.trace = pc.trace;
     p.seq = pc.seq;
+    p.save_h = pc.save_h;
+    p.save_c = pc.save_c;
     if (pc.stop) {
         p.stop_v = pc.stop->v;
         p.stop_c = pc.stop->c;

@@ -67,6 +67,40 @@ seq_finish_kernel(SeqParams p) {
     }
 }
 
+// Output sequence of the forward for training: the state after step t of a
+// row is the state step t + 1 started from (kept per compact row), or its
+// final state after its last step.  Zeros past each length.
+__global__ void __launch_bounds__(256)
+seq_from_saved_kernel(float* seq, const float* __restrict__ save_h, const float* __restrict__ out_h,
+                      const int32_t* __restrict__ perm, const int32_t* __restrict__ offsets,
+                      const int32_t* __restrict__ lengths, int B, int T, int H) {
+    // one slot s per workgroup row; slot order is the length order
+    const long n = (long)B * T * H;
+    for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += (long)gridDim.x * 256) {
+        const long bt = i / H;
+        const int u = (int)(i - bt * H);
+        const int s = (int)(bt / T), t = (int)(bt - (long)s * T);
+        const int b = perm[s];
+        const int L = min(max(lengths[b], 0), T);
+        float v = 0.0f;
+        if (t + 1 < L) v = save_h[(long)(offsets[t + 1] + s) * H + u];
+        else if (t + 1 == L) v = out_h[(long)b * H + u];
+        seq[((long)b * T + t) * H + u] = v;
+    }
+}
+
+hipError_t launch_seq_from_saved(const Dims& d, float* seq, const float* save_h, const float* out_h,
+                                 const int32_t* lengths, const Workspace& ws, int num_cus,
+                                 hipStream_t s) {
+    const long n = (long)d.B * d.T * d.H;
+    long grid = (n + 255) / 256;
+    if (grid > 16L * num_cus) grid = 16L * num_cus;
+    if (grid < 1) grid = 1;
+    hipLaunchKernelGGL(seq_from_saved_kernel, dim3((unsigned)grid), dim3(256), 0, s, seq, save_h,
+                       out_h, ws.perm, ws.offsets, lengths, d.B, d.T, d.H);
+    return hipGetLastError();
+}
+
 hipError_t launch_seq_finish(const Dims& d, float* seq, bool from_gx, int upw, const int32_t* lengths,
                              const Workspace& ws, int num_cus, hipStream_t s) {
     SeqParams p{seq, from_gx ? ws.gx : nullptr, ws.rowsrc, ws.meta, lengths, d.B, d.T, d.H, upw};

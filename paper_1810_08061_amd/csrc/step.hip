@@ -36,7 +36,7 @@ __global__ void __launch_bounds__(256)
 step_gates_kernel(const float* __restrict__ z, float* out_h, float* out_c,
                   const int32_t* __restrict__ perm, const int32_t* __restrict__ offsets,
                   typename E::store_t* hx, int t, int H, int hpad, float* seq, int T, int cell,
-                  const int32_t* __restrict__ stopped) {
+                  const int32_t* __restrict__ stopped, float* gx, float* save_h, float* save_c) {
     const int act = offsets[t + 1] - offsets[t];
     const long n = (long)act * H;
     for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += (long)gridDim.x * 256) {
@@ -46,6 +46,12 @@ step_gates_kernel(const float* __restrict__ z, float* out_h, float* out_c,
         const f32x4_t zz = *reinterpret_cast<const f32x4_t*>(z + (long)s * 4 * H + 4 * u);
         const long ib = (long)b * H + u;
         float c = out_c[ib], h = out_h[ib];
+        if (save_h) {  // forward for training: z in place of Gx, the state the step starts from
+            const long r = offsets[t] + s;
+            *reinterpret_cast<f32x4_t*>(gx + r * 4 * H + 4 * u) = zz;
+            save_h[r * H + u] = h;
+            save_c[r * H + u] = c;
+        }
         apply_cell(cell, zz, c, h);
         out_c[ib] = c;
         out_h[ib] = h;
@@ -74,17 +80,18 @@ hipError_t launch_step_init(const Dims& d, const float* h0, const float* c0, flo
 }
 
 hipError_t launch_step_gates(const Dims& d, int t, float* out_h, float* out_c, float* seq,
-                             bool stop, const Workspace& ws, hipStream_t s) {
+                             bool stop, const Workspace& ws, hipStream_t s, float* save_h,
+                             float* save_c) {
     const int grid = grid_for((long)d.B * d.H);
     const int32_t* stopped = stop ? ws.stopped : nullptr;
     if (d.bf16)
         hipLaunchKernelGGL(step_gates_kernel<EltH16>, dim3(grid), dim3(256), 0, s, ws.z, out_h,
                            out_c, ws.perm, ws.offsets, static_cast<_Float16*>(ws.hx), t, d.H, d.hpad, seq, d.T, d.cell,
-                           stopped);
+                           stopped, ws.gx, save_h, save_c);
     else
         hipLaunchKernelGGL(step_gates_kernel<EltF32>, dim3(grid), dim3(256), 0, s, ws.z, out_h,
                            out_c, ws.perm, ws.offsets, static_cast<float*>(ws.hx), t, d.H, d.hpad, seq, d.T, d.cell,
-                           stopped);
+                           stopped, ws.gx, save_h, save_c);
     return hipGetLastError();
 }
 

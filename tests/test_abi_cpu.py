@@ -225,3 +225,33 @@ def test_check_stop_args():
     # v may not lie under an output, but may share memory with an input
     assert chk(B, D, H, T, ld.BF16, ld.CELL_GRU, *p[:7], p[7], p[7], p[8], st, 0) == ld.ERR_INVALID
     assert chk(B, D, H, T, ld.BF16, ld.CELL_GRU, *p[:7], p[5], p[7], p[8], st, 0) == ld.OK
+
+
+def test_check_backward_args():
+    B, D, H, T = 3, 5, 7, 4
+    sizes = [B * T * D * 4, 4 * B, D * 4 * H * 4, H * 4 * H * 4, 16 * H, 4 * B * H, 4 * B * H,
+             4 * B * H, 4 * B * H, 4 * B * T * H,                                  # inputs
+             4 * B * T * D, 16 * D * H, 16 * H * H, 16 * H, 4 * B * H, 4 * B * H]   # outputs
+    p, at = [], 1 << 20
+    for s in sizes:
+        p.append(at)
+        at += (s + 255) // 256 * 256 + 256
+    chk = ld.lstm_dyn_check_backward_args
+    assert chk(B, D, H, T, ld.F32, *p) == ld.OK
+    q = list(p)
+    q[9] = 0                                      # d_seq is optional
+    assert chk(B, D, H, T, ld.F32, *q) == ld.OK
+    for i in list(range(9)) + list(range(10, 16)):
+        q = list(p)
+        q[i] = 0
+        assert chk(B, D, H, T, ld.F32, *q) == ld.ERR_INVALID, i
+    for i in range(10, 16):                       # an output on an input or on another output
+        for j in range(16):
+            if j == i:
+                continue
+            q = list(p)
+            q[i] = q[j]
+            assert chk(B, D, H, T, ld.F32, *q) == ld.ERR_INVALID, (i, j)
+    q = list(p)
+    q[11] += 2                                    # misaligned dW
+    assert chk(B, D, H, T, ld.F32, *q) == ld.ERR_INVALID
