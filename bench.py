@@ -164,6 +164,8 @@ def main():
                     help="skip timing the GRU and RNN cells on the same workload shape")
     ap.add_argument("--no-stop", action="store_true",
                     help="skip timing the loop with termination computed from the state")
+    ap.add_argument("--no-train", action="store_true",
+                    help="skip timing the forward for training and the backward pass")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain copy of known size (for scaling HBM counters)")
     args = ap.parse_args()
@@ -269,6 +271,36 @@ def main():
                     "valid_seq_steps_run": int(st.sum()),
                     "launches_per_forward": model.query(ld.Q_LAUNCHES_PER_FORWARD)}
 
+    train_leg = None
+    if not args.no_train:
+        # one training step of the loop: the forward that keeps its state, then
+        # the backward pass (gradients of x, W, U, b, h0, c0) from random
+        # upstream gradients of the final state
+        _log("forward for training + backward")
+        rng = np.random.default_rng(5)
+        dh = torch.from_numpy(rng.standard_normal((w.B, w.H)).astype(np.float32)).cuda()
+        dc = torch.from_numpy(rng.standard_normal((w.B, w.H)).astype(np.float32)).cuda()
+        for _ in range(2):
+            model.forward_train(*dev, out_h=out[0], out_c=out[1])
+            model.backward(*dev, dh, dc)
+        torch.cuda.synchronize()
+        tf = tb = 0.0
+        reps = 3
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            model.forward_train(*dev, out_h=out[0], out_c=out[1])
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            model.backward(*dev, dh, dc)
+            torch.cuda.synchronize()
+            tf += t1 - t0
+            tb += time.perf_counter() - t1
+        tf, tb = tf / reps, tb / reps
+        train_leg = {"forward_train_ms": tf * 1e3, "backward_ms": tb * 1e3,
+                     "step_ms": (tf + tb) * 1e3, "value": sumL / (tf + tb), "unit": "seq·steps/s",
+                     "backward_launches": model.query(ld.Q_LAUNCHES_PER_FORWARD),
+                     "backward_algorithmic_tflops": 16.0 * w.H * (w.D + w.H) * sumL / tb / 1e12}
+
     per_step = None
     if args.per_step_reps > 0:
         _log("per-step path")
@@ -335,6 +367,7 @@ def main():
         "per_step_path": per_step,
         "forward_seq": seq_leg,
         "forward_stop": stop_leg,
+        "train_step": train_leg,
         "cells": cell_legs,
         "tiny_f32": tiny,
     }

@@ -1,5 +1,6 @@
 // api.hip -- the C ABI declared in include/lstm_dyn.h: argument checks,
 // launch plan, workspace ownership and the two execution modes.
+#include <math.h>
 #include <new>
 #include <stdint.h>
 #include <string.h>
@@ -24,7 +25,17 @@ struct TrainWs {
     float* dH;      // [B][H] gradient of h in slot order
     float* dC;      // [B][H]
     float* z;       // [bpad][4H] per-step pre-activations (handles not in per-step mode)
-    int32_t* host_offsets;  // pinned [T + 2]: step offsets, then the sum of lengths
+    float* ones;    // [B*T] 1.0: db = dz^T 1
+    // bf16 data: fp16 operands of the weight-gradient GEMMs (scaled by powers of two)
+    _Float16* dz16; // [B*T][4H]
+    _Float16* x16;  // [B*T][D]
+    _Float16* h16;  // [B*T][H]
+    _Float16* w16;  // [D][4H]
+    _Float16* u16;  // [H][4H] U (gate-interleaved), scaled
+    _Float16* dzs16;// [B][4H] one step's dz, each row scaled by srow
+    float* srow;    // [B] scale of each row's dH
+    unsigned* amax; // [5] largest magnitudes (float bits) of dz, x, h_prev, W, U
+    int32_t* host_offsets;  // pinned [T + 8]: step offsets, the sum of lengths, then amax
     rocblas_handle rb;
 };
 
@@ -633,6 +644,18 @@ extern "C" int lstm_dyn_forward_stop(lstm_dyn_t* h, const void* x, const int32_t
 // ---------------------------------------------------------------------------
 // Forward for training and the backward pass (LSTM handles).
 
+// The power of two that brings a largest magnitude (float bits) into
+// [2^13, 2^14): fp16 keeps its 11 bits there, far from overflow.
+static float f16_scale(unsigned bits) {
+    float m;
+    memcpy(&m, &bits, sizeof(m));
+    if (!(m > 0.0f) || !(m < 3.0e38f)) return 1.0f;
+    int e;
+    (void)frexpf(m, &e);
+    const int k = 14 - e;
+    return ldexpf(1.0f, k < 126 ? k : 126);
+}
+
 static int ensure_train(lstm_dyn* h) {
     if (h->train) return LSTM_DYN_OK;
     TrainWs* tw = new (std::nothrow) TrainWs();
@@ -647,7 +670,12 @@ static int ensure_train(lstm_dyn* h) {
     const long long oh = take(4 * B * T * H), oc = take(4 * B * T * H), ox = take(4 * B * T * D),
                     ow = take(4 * D * 4 * H), ou = take(4 * H * 4 * H), odw = take(4 * D * 4 * H),
                     odu = take(4 * H * 4 * H), odb = take(16 * H), odh = take(4 * B * H),
-                    odc = take(4 * B * H), oz = take(16 * H * bpad);
+                    odc = take(4 * B * H), oz = take(16 * H * bpad), o1 = take(4 * B * T);
+    const bool h16 = h->dtype == LSTM_DYN_BF16;
+    const long long odz16 = take(h16 ? 2 * B * T * 4 * H : 0), ox16 = take(h16 ? 2 * B * T * D : 0),
+                    oh16 = take(h16 ? 2 * B * T * H : 0), ow16 = take(h16 ? 2 * D * 4 * H : 0),
+                    ou16 = take(h16 ? 2 * H * 4 * H : 0), odzs = take(h16 ? 2 * B * 4 * H : 0),
+                    osr = take(4 * B), osm = take(256);
     if (hipMalloc(&tw->block, (size_t)o) != hipSuccess) {
         (void)hipGetLastError();
         delete tw;
@@ -665,7 +693,21 @@ static int ensure_train(lstm_dyn* h) {
     tw->dH = reinterpret_cast<float*>(base + odh);
     tw->dC = reinterpret_cast<float*>(base + odc);
     tw->z = reinterpret_cast<float*>(base + oz);
-    if (hipHostMalloc(reinterpret_cast<void**>(&tw->host_offsets), (size_t)(T + 2) * sizeof(int32_t),
+    tw->ones = reinterpret_cast<float*>(base + o1);
+    tw->dz16 = h16 ? reinterpret_cast<_Float16*>(base + odz16) : nullptr;
+    tw->x16 = h16 ? reinterpret_cast<_Float16*>(base + ox16) : nullptr;
+    tw->h16 = h16 ? reinterpret_cast<_Float16*>(base + oh16) : nullptr;
+    tw->w16 = h16 ? reinterpret_cast<_Float16*>(base + ow16) : nullptr;
+    tw->u16 = h16 ? reinterpret_cast<_Float16*>(base + ou16) : nullptr;
+    tw->dzs16 = h16 ? reinterpret_cast<_Float16*>(base + odzs) : nullptr;
+    tw->srow = reinterpret_cast<float*>(base + osr);
+    tw->amax = reinterpret_cast<unsigned*>(base + osm);
+    if (hipMemsetD32(reinterpret_cast<hipDeviceptr_t>(tw->ones), 0x3f800000, (size_t)(B * T)) != hipSuccess) {
+        (void)hipFree(tw->block);
+        delete tw;
+        return LSTM_DYN_ERR_HIP;
+    }
+    if (hipHostMalloc(reinterpret_cast<void**>(&tw->host_offsets), (size_t)(T + 8) * sizeof(int32_t),
                       hipHostMallocDefault) != hipSuccess) {
         (void)hipFree(tw->block);
         delete tw;
@@ -821,6 +863,16 @@ extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* le
         if ((call) != rocblas_status_success) return LSTM_DYN_ERR_HIP; \
     } while (0)
     RB_CHECK(rocblas_set_stream(tw->rb, s));
+    LD_CHECK(launch_bwd_weights(d, W, d.D, tw->w_il, s));
+    LD_CHECK(launch_bwd_weights(d, U, d.H, tw->u_il, s));
+    h->launches_last += 2;
+    if (d.bf16) {  // the largest |U|, for U's fp16 scale
+        LD_CHECK(hipMemsetAsync(tw->amax, 0, 5 * sizeof(unsigned), s));
+        LD_CHECK(launch_bwd_absmax(tw->u_il, (long)d.H * H4, tw->amax + 4, s));
+        LD_CHECK(hipMemcpyAsync(tw->host_offsets + d.T + 2, tw->amax + 4, sizeof(unsigned),
+                                hipMemcpyDeviceToHost, s));
+        h->launches_last++;
+    }
     // step offsets and the sum of lengths of the forward, on the host
     LD_CHECK(hipMemcpyAsync(tw->host_offsets, h->ws.offsets, (size_t)(d.T + 1) * sizeof(int32_t),
                             hipMemcpyDeviceToHost, s));
@@ -832,33 +884,91 @@ extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* le
     const int32_t* off = tw->host_offsets;
     const int rows = off[d.T + 1], max_len = *h->host_maxlen;
     const float one = 1.0f, zero = 0.0f;
-    LD_CHECK(launch_bwd_weights(d, W, d.D, tw->w_il, s));
-    LD_CHECK(launch_bwd_weights(d, U, d.H, tw->u_il, s));
     LD_CHECK(launch_bwd_init(d, d_out_h, d_out_c, tw->dH, tw->dC, h->ws, s));
-    h->launches_last += 3;
-    for (int t = max_len - 1; t >= 0; --t) {
-        const int act = off[t + 1] - off[t];
-        LD_CHECK(launch_bwd_cell(d, t, act, tw->save_c, d_seq, tw->dH, tw->dC, h->ws, s));
-        // dH[0:act] = dz_t U^T (column-major: dH^T = U_il^T-as-stored^T dz_t^T)
-        RB_CHECK(rocblas_sgemm(tw->rb, rocblas_operation_transpose, rocblas_operation_none, d.H,
-                               act, H4, &one, tw->u_il, H4, h->ws.gx + (size_t)off[t] * H4, H4,
-                               &zero, tw->dH, d.H));
+    h->launches_last++;
+    if (!d.bf16) {
+        for (int t = max_len - 1; t >= 0; --t) {
+            const int act = off[t + 1] - off[t];
+            LD_CHECK(launch_bwd_cell(d, t, act, tw->save_c, d_seq, tw->dH, tw->dC, h->ws, s));
+            // dH[0:act] = dz_t U^T (column-major: dH^T = U_il^T-as-stored^T dz_t^T)
+            RB_CHECK(rocblas_sgemm(tw->rb, rocblas_operation_transpose, rocblas_operation_none, d.H,
+                                   act, H4, &one, tw->u_il, H4, h->ws.gx + (size_t)off[t] * H4, H4,
+                                   &zero, tw->dH, d.H));
+            h->launches_last += 2;
+        }
+        LD_CHECK(launch_bwd_state_out(d, tw->dH, tw->dC, nullptr, dh0, dc0, h->ws, s));
+    } else {
+        // bf16 data: dh = dz U^T on fp16 operands, U scaled once, each row's dz
+        // by its own power of two (kept in srow and divided out when dH is read)
+        const float su = f16_scale(static_cast<unsigned>(off[d.T + 2])), alpha_u = 1.0f / su;
+        LD_CHECK(launch_bwd_to_f16(tw->u_il, tw->u16, (long)d.H * H4, su, s));
+        LD_CHECK(launch_bwd_ones(tw->srow, d.B, s));
         h->launches_last += 2;
+        for (int t = max_len - 1; t >= 0; --t) {
+            const int act = off[t + 1] - off[t];
+            LD_CHECK(launch_bwd_cell16(d, t, act, tw->save_c, d_seq, tw->dH, tw->dC, tw->srow,
+                                       tw->dzs16, h->ws, s));
+            RB_CHECK(rocblas_gemm_ex(tw->rb, rocblas_operation_transpose, rocblas_operation_none,
+                                     d.H, act, H4, &alpha_u, tw->u16, rocblas_datatype_f16_r, H4,
+                                     tw->dzs16, rocblas_datatype_f16_r, H4, &zero, tw->dH,
+                                     rocblas_datatype_f32_r, d.H, tw->dH, rocblas_datatype_f32_r,
+                                     d.H, rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0, 0));
+            h->launches_last += 2;
+        }
+        LD_CHECK(launch_bwd_state_out(d, tw->dH, tw->dC, tw->srow, dh0, dc0, h->ws, s));
     }
-    LD_CHECK(launch_bwd_state_out(d, tw->dH, tw->dC, dh0, dc0, h->ws, s));
     h->launches_last++;
     if (rows > 0) {
         LD_CHECK(launch_bwd_gather_x(d, x, rows, tw->xc, h->ws, s));
-        // dW = X^T dz, dU = H_prev^T dz (K = the sum of lengths)
-        RB_CHECK(rocblas_sgemm(tw->rb, rocblas_operation_none, rocblas_operation_transpose, H4,
-                               d.D, rows, &one, h->ws.gx, H4, tw->xc, d.D, &zero, tw->dw_il, H4));
-        RB_CHECK(rocblas_sgemm(tw->rb, rocblas_operation_none, rocblas_operation_transpose, H4,
-                               d.H, rows, &one, h->ws.gx, H4, tw->save_h, d.H, &zero, tw->du_il, H4));
-        LD_CHECK(launch_bwd_colsum(d, tw->db_il, h->ws, s));
-        // dx rows = dz W^T, over the gathered x (already used)
-        RB_CHECK(rocblas_sgemm(tw->rb, rocblas_operation_transpose, rocblas_operation_none, d.D,
-                               rows, H4, &one, tw->w_il, H4, h->ws.gx, H4, &zero, tw->xc, d.D));
-        h->launches_last += 5;
+        // db = dz^T 1 (K = the sum of lengths)
+        RB_CHECK(rocblas_sgemv(tw->rb, rocblas_operation_none, H4, rows, &one, h->ws.gx, H4,
+                               tw->ones, 1, &zero, tw->db_il, 1));
+        h->launches_last += 2;
+        if (!d.bf16) {
+            // dW = X^T dz, dU = H_prev^T dz, then dx rows = dz W^T over the gathered x
+            RB_CHECK(rocblas_sgemm(tw->rb, rocblas_operation_none, rocblas_operation_transpose, H4,
+                                   d.D, rows, &one, h->ws.gx, H4, tw->xc, d.D, &zero, tw->dw_il, H4));
+            RB_CHECK(rocblas_sgemm(tw->rb, rocblas_operation_none, rocblas_operation_transpose, H4,
+                                   d.H, rows, &one, h->ws.gx, H4, tw->save_h, d.H, &zero, tw->du_il,
+                                   H4));
+            RB_CHECK(rocblas_sgemm(tw->rb, rocblas_operation_transpose, rocblas_operation_none, d.D,
+                                   rows, H4, &one, tw->w_il, H4, h->ws.gx, H4, &zero, tw->xc, d.D));
+            h->launches_last += 3;
+        } else {
+            // bf16 data: the same GEMMs on fp16 operands, each scaled by a power
+            // of two (its largest magnitude into [2^13, 2^14)), fp32 accumulation,
+            // alpha undoing the scales
+            const long n_dz = (long)rows * H4, n_x = (long)rows * d.D, n_h = (long)rows * d.H,
+                       n_w = (long)d.D * H4;
+            LD_CHECK(launch_bwd_absmax(h->ws.gx, n_dz, tw->amax + 0, s));
+            LD_CHECK(launch_bwd_absmax(tw->xc, n_x, tw->amax + 1, s));
+            LD_CHECK(launch_bwd_absmax(tw->save_h, n_h, tw->amax + 2, s));
+            LD_CHECK(launch_bwd_absmax(tw->w_il, n_w, tw->amax + 3, s));
+            unsigned* am = reinterpret_cast<unsigned*>(tw->host_offsets + d.T + 3);
+            LD_CHECK(hipMemcpyAsync(am, tw->amax, 4 * sizeof(unsigned), hipMemcpyDeviceToHost, s));
+            LD_CHECK(hipStreamSynchronize(s));
+            const float sz = f16_scale(am[0]), sx = f16_scale(am[1]), sh = f16_scale(am[2]),
+                        sw = f16_scale(am[3]);
+            LD_CHECK(launch_bwd_to_f16(h->ws.gx, tw->dz16, n_dz, sz, s));
+            LD_CHECK(launch_bwd_to_f16(tw->xc, tw->x16, n_x, sx, s));
+            LD_CHECK(launch_bwd_to_f16(tw->save_h, tw->h16, n_h, sh, s));
+            LD_CHECK(launch_bwd_to_f16(tw->w_il, tw->w16, n_w, sw, s));
+            const rocblas_datatype f16 = rocblas_datatype_f16_r, f32 = rocblas_datatype_f32_r;
+            const float a_w = 1.0f / (sz * sx), a_u = 1.0f / (sz * sh), a_x = 1.0f / (sz * sw);
+            RB_CHECK(rocblas_gemm_ex(tw->rb, rocblas_operation_none, rocblas_operation_transpose, H4,
+                                     d.D, rows, &a_w, tw->dz16, f16, H4, tw->x16, f16, d.D, &zero,
+                                     tw->dw_il, f32, H4, tw->dw_il, f32, H4, f32,
+                                     rocblas_gemm_algo_standard, 0, 0));
+            RB_CHECK(rocblas_gemm_ex(tw->rb, rocblas_operation_none, rocblas_operation_transpose, H4,
+                                     d.H, rows, &a_u, tw->dz16, f16, H4, tw->h16, f16, d.H, &zero,
+                                     tw->du_il, f32, H4, tw->du_il, f32, H4, f32,
+                                     rocblas_gemm_algo_standard, 0, 0));
+            RB_CHECK(rocblas_gemm_ex(tw->rb, rocblas_operation_transpose, rocblas_operation_none, d.D,
+                                     rows, H4, &a_x, tw->w16, f16, H4, tw->dz16, f16, H4, &zero,
+                                     tw->xc, f32, d.D, tw->xc, f32, d.D, f32,
+                                     rocblas_gemm_algo_standard, 0, 0));
+            h->launches_last += 11;
+        }
     } else {
         LD_CHECK(hipMemsetAsync(tw->dw_il, 0, (size_t)d.D * H4 * sizeof(float), s));
         LD_CHECK(hipMemsetAsync(tw->du_il, 0, (size_t)d.H * H4 * sizeof(float), s));

@@ -15,9 +15,10 @@
 //     gradient of the output sequence at t), written over z; dc <- dc_total f;
 //   * dh <- dz U^T for those rows, a GEMM (K = 4H) issued by the host;
 // and after the last one the weight gradients are GEMMs over all compact
-// rows (K = sum of lengths): dW = X^T dz, dU = H_prev^T dz, db = column sums,
+// rows (K = sum of lengths): dW = X^T dz, dU = H_prev^T dz, db = dz^T 1,
 // dx = dz W^T, in gate-interleaved columns, permuted back to the caller's
-// gate blocks at the end.
+// gate blocks at the end.  With bf16 data the three GEMMs take fp16 operands
+// scaled by powers of two (fp32 accumulation); with fp32 data they are fp32.
 #include "launch.h"
 
 namespace ldyn {
@@ -79,17 +80,82 @@ bwd_cell_kernel(float* gx, const float* __restrict__ save_c, const float* __rest
     }
 }
 
-// dh0, dc0: slot order -> batch order.
+// The same with bf16 data, one workgroup per row: the row's dz also goes to
+// dz16 in fp16, scaled by a power of two that brings its largest magnitude
+// into [2^13, 2^14), for the product dz U^T; dH of a row holds its gradient
+// times srow (the scale of the dz it was last formed from; 1 at the start).
+__global__ void __launch_bounds__(256)
+bwd_cell16_kernel(float* gx, const float* __restrict__ save_c, const float* __restrict__ dseq,
+                  const int32_t* __restrict__ perm, const int32_t* __restrict__ offsets, float* dH,
+                  float* dC, float* srow, _Float16* dz16, int t, int H, int T) {
+    __shared__ unsigned red[4];
+    const int off = offsets[t];
+    const int s = blockIdx.x, tid = threadIdx.x;
+    if (s >= offsets[t + 1] - off) return;  // uniform over the workgroup
+    const long r = off + s;
+    const float inv = 1.0f / srow[s];
+    const float* dseq_row = dseq ? dseq + ((long)perm[s] * T + t) * H : nullptr;
+    unsigned m = 0;
+    for (int u = tid; u < H; u += 256) {
+        f32x4_t* zp = reinterpret_cast<f32x4_t*>(gx + r * 4 * H + 4 * u);
+        const f32x4_t z = *zp;
+        const float ig = sigmoid_f(z[0]), fg = sigmoid_f(z[1]);
+        const float gg = tanh_f(z[2]), og = sigmoid_f(z[3]);
+        const float cp = save_c[r * H + u];
+        const float c = fg * cp + ig * gg;
+        const float tc = tanh_f(c);
+        float dh = dH[(long)s * H + u] * inv;
+        if (dseq_row) dh += dseq_row[u];
+        const float d_o = dh * tc;
+        const float dct = dC[(long)s * H + u] + dh * og * (1.0f - tc * tc);
+        f32x4_t dz;
+        dz[0] = dct * gg * ig * (1.0f - ig);
+        dz[1] = dct * cp * fg * (1.0f - fg);
+        dz[2] = dct * ig * (1.0f - gg * gg);
+        dz[3] = d_o * og * (1.0f - og);
+        *zp = dz;
+        dC[(long)s * H + u] = dct * fg;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) m = max(m, __float_as_uint(fabsf(dz[g])) & 0x7fffffffu);
+    }
+    for (int o = 32; o > 0; o >>= 1) m = max(m, (unsigned)__shfl_xor((int)m, o));
+    if ((tid & 63) == 0) red[tid >> 6] = m;
+    __syncthreads();
+    m = max(max(red[0], red[1]), max(red[2], red[3]));
+    const float mf = __uint_as_float(m);
+    float sc = 1.0f;
+    if (mf > 0.0f && mf < 3.0e38f) {
+        int e;
+        (void)frexpf(mf, &e);
+        sc = ldexpf(1.0f, min(14 - e, 126));
+    }
+    for (int u = tid; u < H; u += 256) {
+        const f32x4_t dz = *reinterpret_cast<const f32x4_t*>(gx + r * 4 * H + 4 * u);
+#pragma unroll
+        for (int g = 0; g < 4; ++g) dz16[(long)s * 4 * H + 4 * u + g] = (_Float16)(dz[g] * sc);
+    }
+    if (tid == 0) srow[s] = sc;  // every thread read the old value before the barrier
+}
+
+// dh0, dc0: slot order -> batch order (dH divided by its row's scale when
+// srow is given).
 __global__ void __launch_bounds__(256)
 bwd_state_out_kernel(const float* __restrict__ dH, const float* __restrict__ dC,
-                     const int32_t* __restrict__ perm, float* dh0, float* dc0, int B, int H) {
+                     const float* __restrict__ srow, const int32_t* __restrict__ perm, float* dh0,
+                     float* dc0, int B, int H) {
     const long n = (long)B * H;
     for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += (long)gridDim.x * 256) {
         const int s = (int)(i / H), u = (int)(i - (long)s * H);
         const long ib = (long)perm[s] * H + u;
-        dh0[ib] = dH[i];
+        dh0[ib] = srow ? dH[i] / srow[s] : dH[i];
         dc0[ib] = dC[i];
     }
+}
+
+// srow = 1.
+__global__ void bwd_ones_kernel(float* a, int n) {
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    if (i < n) a[i] = 1.0f;
 }
 
 // x rows in the compact order, fp32.
@@ -103,18 +169,6 @@ bwd_gather_x_kernel(const S* __restrict__ x, const int32_t* __restrict__ rowsrc,
         const int k = (int)(i - r * D);
         xc[i] = (float)x[(long)rowsrc[r] * D + k];
     }
-}
-
-// db in interleaved columns: the sum of dz over the compact rows, in row
-// order (one thread per column).
-__global__ void __launch_bounds__(256)
-bwd_colsum_kernel(const float* __restrict__ dz, const Meta* __restrict__ meta, float* db_il, int H4) {
-    const int cp = blockIdx.x * 256 + threadIdx.x;
-    if (cp >= H4) return;
-    const long rows = meta->total_rows;
-    float acc = 0.f;
-    for (long r = 0; r < rows; ++r) acc += dz[r * H4 + cp];
-    db_il[cp] = acc;
 }
 
 // Interleaved columns -> the caller's gate blocks: out[k][g H + u] = il[k][4u + g].
@@ -149,6 +203,30 @@ bwd_dx_kernel(const float* __restrict__ dxc, const int32_t* __restrict__ rowsrc,
     }
 }
 
+// ---------------------------------------------------------------------------
+// fp16 operands for the GEMMs of the backward with bf16 data: each operand is
+// scaled by a power of two that brings its largest magnitude to [2^13, 2^14)
+// (exact, and far from fp16 overflow; the host picks it from the largest
+// magnitude), and the GEMM's alpha undoes the scales.
+
+// Largest |a| of n floats (as bits): the bits of non-negative floats order as
+// integers, so an integer atomic maximum gives the same result in any order.
+__global__ void __launch_bounds__(256)
+bwd_absmax_kernel(const float* __restrict__ a, long n, unsigned* out) {
+    unsigned m = 0;
+    for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += (long)gridDim.x * 256)
+        m = max(m, __float_as_uint(fabsf(a[i])) & 0x7fffffffu);
+    for (int o = 32; o > 0; o >>= 1) m = max(m, (unsigned)__shfl_xor((int)m, o));
+    if ((threadIdx.x & 63) == 0) atomicMax(out, m);
+}
+
+// dst = fp16(src * scale), n elements.
+__global__ void __launch_bounds__(256)
+bwd_to_f16_kernel(const float* __restrict__ src, _Float16* dst, long n, float scale) {
+    for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += (long)gridDim.x * 256)
+        dst[i] = (_Float16)(src[i] * scale);
+}
+
 static unsigned grid_of(long n) {
     long g = (n + 255) / 256;
     if (g < 1) g = 1;
@@ -181,10 +259,23 @@ hipError_t launch_bwd_cell(const Dims& d, int t, int act, const float* save_c, c
     return hipGetLastError();
 }
 
-hipError_t launch_bwd_state_out(const Dims& d, const float* dH, const float* dC, float* dh0,
-                                float* dc0, const Workspace& ws, hipStream_t s) {
+hipError_t launch_bwd_state_out(const Dims& d, const float* dH, const float* dC, const float* srow,
+                                float* dh0, float* dc0, const Workspace& ws, hipStream_t s) {
     hipLaunchKernelGGL(bwd_state_out_kernel, dim3(grid_of((long)d.B * d.H)), dim3(256), 0, s, dH,
-                       dC, ws.perm, dh0, dc0, d.B, d.H);
+                       dC, srow, ws.perm, dh0, dc0, d.B, d.H);
+    return hipGetLastError();
+}
+
+hipError_t launch_bwd_cell16(const Dims& d, int t, int act, const float* save_c, const float* dseq,
+                             float* dH, float* dC, float* srow, _Float16* dz16, const Workspace& ws,
+                             hipStream_t s) {
+    hipLaunchKernelGGL(bwd_cell16_kernel, dim3(act), dim3(256), 0, s, ws.gx, save_c, dseq, ws.perm,
+                       ws.offsets, dH, dC, srow, dz16, t, d.H, d.T);
+    return hipGetLastError();
+}
+
+hipError_t launch_bwd_ones(float* a, int n, hipStream_t s) {
+    hipLaunchKernelGGL(bwd_ones_kernel, dim3((n + 255) / 256), dim3(256), 0, s, a, n);
     return hipGetLastError();
 }
 
@@ -200,9 +291,14 @@ hipError_t launch_bwd_gather_x(const Dims& d, const void* x, long rows, float* x
     return hipGetLastError();
 }
 
-hipError_t launch_bwd_colsum(const Dims& d, float* db_il, const Workspace& ws, hipStream_t s) {
-    hipLaunchKernelGGL(bwd_colsum_kernel, dim3((4 * d.H + 255) / 256), dim3(256), 0, s, ws.gx,
-                       ws.meta, db_il, 4 * d.H);
+hipError_t launch_bwd_absmax(const float* a, long n, unsigned* out, hipStream_t s) {
+    const unsigned g = grid_of(n) < 2048 ? grid_of(n) : 2048;
+    hipLaunchKernelGGL(bwd_absmax_kernel, dim3(g), dim3(256), 0, s, a, n, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_bwd_to_f16(const float* src, _Float16* dst, long n, float scale, hipStream_t s) {
+    hipLaunchKernelGGL(bwd_to_f16_kernel, dim3(grid_of(n)), dim3(256), 0, s, src, dst, n, scale);
     return hipGetLastError();
 }
 

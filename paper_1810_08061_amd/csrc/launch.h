@@ -116,11 +116,20 @@ hipError_t launch_bwd_init(const Dims& d, const float* dh_out, const float* dc_o
                            float* dC, const Workspace& ws, hipStream_t s);
 hipError_t launch_bwd_cell(const Dims& d, int t, int act, const float* save_c, const float* dseq,
                            float* dH, float* dC, const Workspace& ws, hipStream_t s);
-hipError_t launch_bwd_state_out(const Dims& d, const float* dH, const float* dC, float* dh0,
-                                float* dc0, const Workspace& ws, hipStream_t s);
+hipError_t launch_bwd_state_out(const Dims& d, const float* dH, const float* dC, const float* srow,
+                                float* dh0, float* dc0, const Workspace& ws, hipStream_t s);
+// bf16 data: the cell's backward with one workgroup per row, also writing the
+// row's dz in fp16 scaled by a power of two (srow) for dz U^T.
+hipError_t launch_bwd_cell16(const Dims& d, int t, int act, const float* save_c, const float* dseq,
+                             float* dH, float* dC, float* srow, _Float16* dz16, const Workspace& ws,
+                             hipStream_t s);
+hipError_t launch_bwd_ones(float* a, int n, hipStream_t s);
 hipError_t launch_bwd_gather_x(const Dims& d, const void* x, long rows, float* xc,
                                const Workspace& ws, hipStream_t s);
-hipError_t launch_bwd_colsum(const Dims& d, float* db_il, const Workspace& ws, hipStream_t s);
+// fp16 operands of the backward's GEMMs: the largest magnitude (as float bits,
+// atomic and order free) and a scaled conversion.
+hipError_t launch_bwd_absmax(const float* a, long n, unsigned* out, hipStream_t s);
+hipError_t launch_bwd_to_f16(const float* src, _Float16* dst, long n, float scale, hipStream_t s);
 hipError_t launch_bwd_permute(const Dims& d, const float* il, float* out, int rows, hipStream_t s);
 hipError_t launch_bwd_dx(const Dims& d, const float* dxc, long rows, const int32_t* lengths,
                          float* dx, const Workspace& ws, hipStream_t s);

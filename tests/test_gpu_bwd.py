@@ -131,10 +131,14 @@ def test_backward_large_workloads(name, mode):
             acc[k] = acc[k] + gp[k]
         m.close()
         torch.cuda.empty_cache()
+    # with bf16 data the weight-gradient GEMMs round dz, x and h_prev to fp16
+    # under a scale set by each run's largest values, so the halves and the
+    # whole round differently: relative 2^-11 per operand, well under 1e-3
+    add_tol = 1e-5 if w.dtype == workloads.F32 else 1e-3
     for k in acc:
         e = scaled_err(g[k], acc[k])
         say(f"  halves {k}: {e:.2e}")
-        assert e <= 1e-5, (k, e)
+        assert e <= add_tol, (k, e)
 
 
 @pytest.mark.parametrize("mode", MODES)
