@@ -15,6 +15,13 @@ roofline     the loop kernel (the dominant kernel): algorithmic recurrent
              forward's stream, against the dense bf16 (or fp32) MFMA peak
 cpu_baseline the fp64 oracle on a bounded sample of the same workload, timed
              on this host's cores
+
+Side legs on the same workload (not part of value): forward_seq (the forward
+that also writes the output sequence), forward_stop (termination computed
+from the state by a halting read-out), cells (the GRU and tanh RNN cells),
+train_step (the forward for training and the backward pass), per_step_path
+(the host-driven comparison loop) and tiny_f32 (the launch-bound small case).
+Each has a --no-* flag.
 """
 from __future__ import annotations
 
