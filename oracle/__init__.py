@@ -77,6 +77,8 @@ class _Lib:
         lib.lstm_oracle_forward_stop.restype = ctypes.c_int
         lib.lstm_oracle_backward.argtypes = [ctypes.c_int] * 4 + [P] * 16
         lib.lstm_oracle_backward.restype = ctypes.c_int
+        lib.lstm_oracle_backward_cell.argtypes = [ctypes.c_int] * 5 + [P] * 15
+        lib.lstm_oracle_backward_cell.restype = ctypes.c_int
         lib.lstm_oracle_max_threads.argtypes = []
         lib.lstm_oracle_max_threads.restype = ctypes.c_int
         self.lib = lib
@@ -281,6 +283,56 @@ def backward(x, lengths, W, U, b, h0, c0, dh_out, dc_out, dseq=None, _lib_overri
     if rc != OK:
         raise OracleError(f"oracle failed with code {rc}")
     return out
+
+
+def _backward_cell(cell, x, lengths, W, U, b, b_hh, h0, dh_out, dseq, _lib_override):
+    lib = (_lib_override or _load()).lib
+    x, W, U, b = map(_f32, (x, W, U, b))
+    bhh = _f32(b_hh) if b_hh is not None else None
+    f64 = lambda a: np.ascontiguousarray(a, dtype=np.float64)
+    h0, dh_out = f64(h0), f64(dh_out)
+    L = np.ascontiguousarray(lengths, dtype=np.int32)
+    B, T, D = x.shape
+    H = U.shape[0]
+    G = 3 * H if cell == 1 else H
+    if W.shape != (D, G) or U.shape != (H, G) or b.shape != (G,):
+        raise OracleError("weight shapes do not match x, U and the cell")
+    if h0.shape != (B, H) or dh_out.shape != (B, H):
+        raise OracleError("state shapes do not match x")
+    ds = f64(dseq) if dseq is not None else None
+    out = {"dx": np.empty((B, T, D)), "dW": np.empty((D, G)), "dU": np.empty((H, G)),
+           "db": np.empty(G), "dh0": np.empty((B, H))}
+    dbhh = np.empty(G) if cell == 1 else None
+    rc = lib.lstm_oracle_backward_cell(B, T, D, H, cell, x.ctypes.data, L.ctypes.data,
+                                       W.ctypes.data, U.ctypes.data, b.ctypes.data,
+                                       bhh.ctypes.data if bhh is not None else None,
+                                       h0.ctypes.data, dh_out.ctypes.data,
+                                       ds.ctypes.data if ds is not None else None,
+                                       out["dx"].ctypes.data, out["dW"].ctypes.data,
+                                       out["dU"].ctypes.data, out["db"].ctypes.data,
+                                       dbhh.ctypes.data if dbhh is not None else None,
+                                       out["dh0"].ctypes.data)
+    if rc == BAD_LENGTHS:
+        raise OracleError("sequence lengths must lie in [0, T]")
+    if rc != OK:
+        raise OracleError(f"oracle failed with code {rc}")
+    if dbhh is not None:
+        out["db_ih"] = out.pop("db")
+        out["db_hh"] = dbhh
+    return out
+
+
+def backward_gru(x, lengths, W, U, b_ih, b_hh, h0, dh_out, dseq=None, _lib_override=None):
+    """Gradients of the masked loop with the GRU cell: dx, dW [D, 3H],
+    dU [H, 3H], db_ih, db_hh [3H], dh0 (float64), from the upstream gradient of
+    the final h and optionally of the output sequence."""
+    return _backward_cell(1, x, lengths, W, U, b_ih, b_hh, h0, dh_out, dseq, _lib_override)
+
+
+def backward_rnn(x, lengths, W, U, b, h0, dh_out, dseq=None, _lib_override=None):
+    """Gradients of the masked loop with the tanh RNN cell: dx, dW [D, H],
+    dU [H, H], db [H], dh0 (float64)."""
+    return _backward_cell(2, x, lengths, W, U, b, None, h0, dh_out, dseq, _lib_override)
 
 
 _CELL_IDS = {"lstm": 0, "gru": 1, "rnn": 2}

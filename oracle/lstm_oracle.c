@@ -506,6 +506,120 @@ int lstm_oracle_backward(int B, int T, int D, int H, const float* x, const int32
     return ORACLE_OK;
 }
 
+/*
+ * lstm_oracle_backward_cell: the backward pass for the GRU (cell = CELL_GRU;
+ * W [D][3H], U [H][3H], bias = b_ih [3H], bhh = b_hh [3H]) and the tanh RNN
+ * (cell = CELL_RNN; W [D][H], U [H][H], bias [H]).  Same loss and masking as
+ * lstm_oracle_backward, no cell state: returns dx, dW, dU, the bias gradients
+ * (db = d b_ih, dbhh = d b_hh for the GRU; dbhh unused for the RNN) and dh0.
+ *   GRU, with a = x W + b_ih and e = h U + b_hh of the step:
+ *     dn = dh (1 - u), du = dh (h - n), dh_prev = dh u + (de) U^T
+ *     dzn = dn (1 - n^2); da_n = dzn; de_n = dzn r; dr = dzn e_n
+ *     da_r = de_r = dr r (1 - r); da_u = de_u = du u (1 - u)
+ *     dW += x^T da, dU += h^T de, db_ih += da, db_hh += de, dx = da W^T
+ *   RNN, with h' = tanh(z):  dz = dh (1 - h'^2), dh_prev = dz U^T, and the
+ *     same weight, bias and input gradients with da = de = dz.
+ */
+int lstm_oracle_backward_cell(int B, int T, int D, int H, int cell, const float* x,
+                              const int32_t* L, const float* W, const float* U,
+                              const float* bias, const float* bhh, const double* h0,
+                              const double* dh_out, const double* dseq, double* dx, double* dW,
+                              double* dU, double* db, double* dbhh, double* dh0) {
+    if (B <= 0 || T < 0 || D <= 0 || H <= 0 || !x || !L || !W || !U || !bias || !h0 ||
+        !dh_out || !dx || !dW || !dU || !db || !dh0)
+        return ORACLE_BAD_ARGS;
+    if (cell != CELL_GRU && cell != CELL_RNN) return ORACLE_BAD_ARGS;
+    if (cell == CELL_GRU && (!bhh || !dbhh)) return ORACLE_BAD_ARGS;
+    for (int b = 0; b < B; ++b)
+        if (L[b] < 0 || L[b] > T) return ORACLE_BAD_LENGTHS;
+    const int G = cell == CELL_GRU ? 3 * H : H;
+    double* hs = (double*)malloc((size_t)(T + 1) * H * sizeof(double));     /* h_{t-1}, t = 0..T */
+    double* zs = (double*)malloc((size_t)(T > 0 ? T : 1) * 2 * G * sizeof(double));
+    double* da = (double*)malloc((size_t)G * sizeof(double));              /* input-side grads */
+    double* de = (double*)malloc((size_t)G * sizeof(double));              /* recurrent-side */
+    double* dh = (double*)malloc((size_t)H * sizeof(double));
+    double* nh = (double*)malloc((size_t)H * sizeof(double));
+    double* zc = (double*)calloc((size_t)H, sizeof(double));               /* unused cell state */
+    if (!hs || !zs || !da || !de || !dh || !nh || !zc) {
+        free(hs); free(zs); free(da); free(de); free(dh); free(nh); free(zc);
+        return ORACLE_NOMEM;
+    }
+    memset(dx, 0, (size_t)B * T * D * sizeof(double));
+    memset(dW, 0, (size_t)D * G * sizeof(double));
+    memset(dU, 0, (size_t)H * G * sizeof(double));
+    memset(db, 0, (size_t)G * sizeof(double));
+    if (cell == CELL_GRU) memset(dbhh, 0, (size_t)G * sizeof(double));
+    for (int b = 0; b < B; ++b) {
+        const int n = L[b];
+        memcpy(hs, h0 + (size_t)b * H, (size_t)H * sizeof(double));
+        for (int t = 0; t < n; ++t) {           /* forward, keeping a and e (GRU) or z (RNN) */
+            const float* xr = x + ((size_t)b * T + t) * D;
+            double* za = zs + (size_t)t * 2 * G;
+            if (cell == CELL_GRU)
+                gru_cell_row(D, H, xr, W, U, bias, bhh, hs + (size_t)t * H, za, za + G,
+                             hs + (size_t)(t + 1) * H);
+            else
+                rnn_cell_row(D, H, xr, W, U, bias, hs + (size_t)t * H, za, hs + (size_t)(t + 1) * H);
+        }
+        memcpy(dh, dh_out + (size_t)b * H, (size_t)H * sizeof(double));
+        for (int t = n - 1; t >= 0; --t) {
+            if (dseq)
+                for (int v = 0; v < H; ++v) dh[v] += dseq[((size_t)b * T + t) * H + v];
+            const double* hp = hs + (size_t)t * H;
+            const double* za = zs + (size_t)t * 2 * G;
+            if (cell == CELL_GRU) {
+                const double* ze = za + G;
+                for (int v = 0; v < H; ++v) {
+                    const double rg = sig(za[v] + ze[v]);
+                    const double ug = sig(za[H + v] + ze[H + v]);
+                    const double ng = tanh(za[2 * H + v] + rg * ze[2 * H + v]);
+                    const double dn = dh[v] * (1.0 - ug);
+                    const double du = dh[v] * (hp[v] - ng);
+                    const double dzn = dn * (1.0 - ng * ng);
+                    const double dr = dzn * ze[2 * H + v];
+                    const double dzr = dr * rg * (1.0 - rg), dzu = du * ug * (1.0 - ug);
+                    da[v] = dzr;              de[v] = dzr;
+                    da[H + v] = dzu;          de[H + v] = dzu;
+                    da[2 * H + v] = dzn;      de[2 * H + v] = dzn * rg;
+                    nh[v] = dh[v] * ug;       /* h reaches h' directly through u */
+                }
+            } else {
+                const double* hnew = hs + (size_t)(t + 1) * H;
+                for (int v = 0; v < H; ++v) {
+                    const double hn = hnew[v];       /* tanh(z) of the step */
+                    da[v] = dh[v] * (1.0 - hn * hn);
+                    de[v] = da[v];
+                    nh[v] = 0.0;
+                }
+            }
+            for (int j = 0; j < G; ++j) {
+                db[j] += da[j];
+                if (cell == CELL_GRU) dbhh[j] += de[j];
+            }
+            const float* xr = x + ((size_t)b * T + t) * D;
+            for (int k = 0; k < D; ++k) {      /* dW += x^T da, dx = da W^T */
+                double acc = 0.0;
+                for (int j = 0; j < G; ++j) {
+                    dW[(size_t)k * G + j] += (double)xr[k] * da[j];
+                    acc += da[j] * (double)W[(size_t)k * G + j];
+                }
+                dx[((size_t)b * T + t) * D + k] = acc;
+            }
+            for (int k = 0; k < H; ++k) {      /* dU += h^T de, dh_prev = direct + de U^T */
+                double acc = nh[k];
+                for (int j = 0; j < G; ++j) {
+                    dU[(size_t)k * G + j] += hp[k] * de[j];
+                    acc += de[j] * (double)U[(size_t)k * G + j];
+                }
+                dh[k] = acc;
+            }
+        }
+        memcpy(dh0 + (size_t)b * H, dh, (size_t)H * sizeof(double));
+    }
+    free(hs); free(zs); free(da); free(de); free(dh); free(nh); free(zc);
+    return ORACLE_OK;
+}
+
 /* Number of OpenMP threads a call with nthreads <= 0 would use. */
 int lstm_oracle_max_threads(void) {
 #ifdef _OPENMP

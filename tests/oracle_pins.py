@@ -882,3 +882,119 @@ BWD_PINS = [
     bpin_linear_in_upstream,
     bpin_rows_add_up,
 ]
+
+
+# ---------------------------------------------------------------------------
+# The backward pass with the GRU and tanh RNN cells.  Each pin takes a
+# callable bwd(cell, x, L, W, U, b, b_hh, h0, dh, ds) returning the gradient
+# dict of ``oracle.backward_gru`` / ``oracle.backward_rnn``.
+
+def _cell_bwd_case(cell, seed, B, D, H, T, lo=0):
+    x, L, _, _, _, h0, _ = _stop_case(seed, B, D, H, T, lo=lo)
+    rng = np.random.default_rng(seed + 17)
+    g = 3 if cell == "gru" else 1
+    W = (rng.standard_normal((D, g * H)) / math.sqrt(H)).astype(np.float32)
+    U = (rng.standard_normal((H, g * H)) / math.sqrt(H)).astype(np.float32)
+    b = (rng.standard_normal(g * H) * 0.4).astype(np.float32)
+    bhh = (rng.standard_normal(g * H) * 0.4).astype(np.float32) if cell == "gru" else None
+    dh = rng.standard_normal((B, H))
+    ds = rng.standard_normal((B, T, H))
+    return x, L, W, U, b, bhh, h0.astype(np.float64), dh, ds
+
+
+def _cell_loss(cell, x, L, W, U, b, bhh, h0, dh, ds):
+    if cell == "gru":
+        h, seq = oracle.forward_gru(x, L, W, U, b, bhh, h0, return_seq=True)
+    else:
+        h, seq = oracle.forward_rnn(x, L, W, U, b, h0, return_seq=True)
+    return float(np.sum(dh * h) + np.sum(ds * seq))
+
+
+def cbpin_finite_differences(bwd):
+    """Central differences of the loss entry by entry (x, W, U, both biases,
+    h0), for both cells; fp32 parameters moved to neighbouring fp32 values and
+    divided by their exact distance; agreement to 2e-6 relative."""
+    for cell in ("gru", "rnn"):
+        x, L, W, U, b, bhh, h0, dh, ds = _cell_bwd_case(cell, 95, 3, 2, 3, 4)
+        L[:] = [4, 2, 0]
+        g = bwd(cell, x, L, W, U, b, bhh, h0, dh, ds)
+        names = [("x", x, "dx", True), ("W", W, "dW", True), ("U", U, "dU", True),
+                 ("h0", h0, "dh0", False)]
+        names += [("b_ih", b, "db_ih", True), ("b_hh", bhh, "db_hh", True)] if cell == "gru" else \
+                 [("b", b, "db", True)]
+        for name, arr, key, f32 in names:
+            flat = arr.reshape(-1)
+            for i in range(flat.size):
+                v = float(flat[i])
+                if f32:
+                    step = max(abs(v), 0.05) * 2.0 ** -10
+                    vp, vm = np.float32(v + step), np.float32(v - step)
+                else:
+                    step = max(abs(v), 0.05) * 1e-5
+                    vp, vm = v + step, v - step
+                flat[i] = vp
+                lp = _cell_loss(cell, x, L, W, U, b, bhh, h0, dh, ds)
+                flat[i] = vm
+                lm = _cell_loss(cell, x, L, W, U, b, bhh, h0, dh, ds)
+                flat[i] = v
+                fd = (lp - lm) / (float(vp) - float(vm))
+                gi = float(g[key].reshape(-1)[i])
+                assert abs(fd - gi) <= 2e-6 * max(1.0, abs(gi)), (cell, name, i, fd, gi)
+
+
+def cbpin_torch_autograd(bwd, shapes=((3, 4, 5, 6), (7, 12, 9, 10))):
+    """Agreement (<= 1e-11) with torch.nn.GRU / torch.nn.RNN (tanh) autograd in
+    float64 on packed sequences, for the same loss (the RNN's bias_hh fixed at
+    zero, its bias_ih = b)."""
+    import torch
+    from torch.nn.utils.rnn import pack_padded_sequence, pad_packed_sequence
+    for cell in ("gru", "rnn"):
+        for k, (B, D, H, T) in enumerate(shapes):
+            x, L, W, U, b, bhh, h0, dh, ds = _cell_bwd_case(cell, 9300 + k, B, D, H, T, lo=1)
+            g = bwd(cell, x, L, W, U, b, bhh, h0, dh, ds)
+            m = (torch.nn.GRU(D, H, batch_first=True) if cell == "gru" else
+                 torch.nn.RNN(D, H, nonlinearity="tanh", batch_first=True)).double()
+            with torch.no_grad():
+                m.weight_ih_l0.copy_(torch.from_numpy(W.astype(np.float64).T))
+                m.weight_hh_l0.copy_(torch.from_numpy(U.astype(np.float64).T))
+                m.bias_ih_l0.copy_(torch.from_numpy(b.astype(np.float64)))
+                if cell == "gru":
+                    m.bias_hh_l0.copy_(torch.from_numpy(bhh.astype(np.float64)))
+                else:
+                    m.bias_hh_l0.zero_()
+            xt = torch.from_numpy(x.astype(np.float64)).requires_grad_()
+            h0t = torch.from_numpy(h0).requires_grad_()
+            packed = pack_padded_sequence(xt, torch.from_numpy(L.astype(np.int64)), batch_first=True,
+                                          enforce_sorted=False)
+            out, hn = m(packed, h0t[None])
+            out, _ = pad_packed_sequence(out, batch_first=True, total_length=T)
+            loss = (torch.from_numpy(dh) * hn[0]).sum() + (torch.from_numpy(ds) * out).sum()
+            loss.backward()
+            pairs = [("dW", m.weight_ih_l0.grad.T), ("dU", m.weight_hh_l0.grad.T),
+                     ("dx", xt.grad), ("dh0", h0t.grad)]
+            if cell == "gru":
+                pairs += [("db_ih", m.bias_ih_l0.grad), ("db_hh", m.bias_hh_l0.grad)]
+            else:
+                pairs += [("db", m.bias_ih_l0.grad)]
+            for name, ref in pairs:
+                err = np.max(np.abs(g[name] - ref.numpy()))
+                assert err <= 1e-11 * max(1.0, float(np.max(np.abs(ref.numpy())))), (cell, k, name, err)
+
+
+def cbpin_masking_facts(bwd):
+    """No gradient on padding; a length-0 row passes dh to dh0 bit for bit."""
+    for cell in ("gru", "rnn"):
+        x, L, W, U, b, bhh, h0, dh, ds = _cell_bwd_case(cell, 96, 5, 3, 4, 7)
+        L[:] = [7, 0, 3, 5, 0]
+        g = bwd(cell, x, L, W, U, b, bhh, h0, dh, ds)
+        for r in range(5):
+            assert not np.any(g["dx"][r, L[r]:]), (cell, r)
+        for r in (1, 4):
+            assert _bits_equal(g["dh0"][r], dh[r]), (cell, r)
+
+
+CELL_BWD_PINS = [
+    cbpin_finite_differences,
+    cbpin_torch_autograd,
+    cbpin_masking_facts,
+]

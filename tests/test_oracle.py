@@ -99,3 +99,14 @@ def test_stop_pin(pin):
 @pytest.mark.parametrize("pin", oracle_pins.BWD_PINS, ids=lambda f: f.__name__)
 def test_backward_pin(pin):
     pin(oracle.backward)
+
+
+def _cell_bwd(cell, x, L, W, U, b, bhh, h0, dh, ds):
+    if cell == "gru":
+        return oracle.backward_gru(x, L, W, U, b, bhh, h0, dh, ds)
+    return oracle.backward_rnn(x, L, W, U, b, h0, dh, ds)
+
+
+@pytest.mark.parametrize("pin", oracle_pins.CELL_BWD_PINS, ids=lambda f: f.__name__)
+def test_cell_backward_pin(pin):
+    pin(_cell_bwd)

@@ -190,3 +190,36 @@ def test_backward_pins_catch_planted_mistake(name, tmp_path):
             caught.append(pin.__name__)
             break
     assert caught, f"no pin caught mutant {name}"
+
+
+CELL_BWD_MUTANTS = {
+    "gru_bwd_no_direct_path": ("nh[v] = dh[v] * ug;       /* h reaches h' directly through u */",
+                               "nh[v] = 0.0;"),
+    "gru_bwd_reset_on_input_side": ("da[2 * H + v] = dzn;      de[2 * H + v] = dzn * rg;",
+                                    "da[2 * H + v] = dzn * rg; de[2 * H + v] = dzn;"),
+    "gru_bwd_update_sign": ("const double du = dh[v] * (hp[v] - ng);", "const double du = dh[v] * (ng - hp[v]);"),
+    "rnn_bwd_derivative": ("da[v] = dh[v] * (1.0 - hn * hn);", "da[v] = dh[v] * (1.0 + hn * hn);"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(CELL_BWD_MUTANTS))
+def test_cell_backward_pins_catch_planted_mistake(name, tmp_path):
+    old, new = CELL_BWD_MUTANTS[name]
+    src = oracle.source_text()
+    assert src.count(old) == 1, f"mutation anchor for {name} not found exactly once"
+    lib = oracle.compile_variant(src.replace(old, new), str(tmp_path / f"mut_{name}.so"))
+    low = oracle._Lib(lib)
+
+    def bwd(cell, x, L, W, U, b, bhh, h0, dh, ds):
+        if cell == "gru":
+            return oracle.backward_gru(x, L, W, U, b, bhh, h0, dh, ds, _lib_override=low)
+        return oracle.backward_rnn(x, L, W, U, b, h0, dh, ds, _lib_override=low)
+    caught = []
+    for pin in oracle_pins.CELL_BWD_PINS:
+        try:
+            with np.errstate(all="ignore"):
+                pin(bwd)
+        except (AssertionError, oracle.OracleError):
+            caught.append(pin.__name__)
+            break
+    assert caught, f"no pin caught mutant {name}"
