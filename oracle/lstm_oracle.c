@@ -562,7 +562,7 @@ int lstm_oracle_backward_cell(int B, int T, int D, int H, int cell, const float*
                 rnn_cell_row(D, H, xr, W, U, bias, hs + (size_t)t * H, za, hs + (size_t)(t + 1) * H);
         }
         memcpy(dh, dh_out + (size_t)b * H, (size_t)H * sizeof(double));
-        for (int t = n - 1; t >= 0; --t) {
+        for (int t = n; t-- > 0;) {          /* last step first */
             if (dseq)
                 for (int v = 0; v < H; ++v) dh[v] += dseq[((size_t)b * T + t) * H + v];
             const double* hp = hs + (size_t)t * H;
