@@ -214,15 +214,14 @@ int lstm_dyn_forward_stop(lstm_dyn_t* h, const void* x, const int32_t* lengths, 
                           int32_t* out_steps, float* out_seq, void* stream);
 
 /*
- * lstm_dyn_forward_train: lstm_dyn_forward (LSTM handles), also keeping in the
- * handle what lstm_dyn_backward needs: for every valid (b, t), the cell's
- * pre-activations and the state the step started from (fp32).  The first call
+ * lstm_dyn_forward_train: lstm_dyn_forward, also keeping in the handle what
+ * lstm_dyn_backward needs: for every valid (b, t), the cell's pre-activations
+ * and the state the step started from (fp32).  The first call
  * allocates that training workspace (hipMalloc; about 8 B*T_max*H + 4 B*T_max*D
  * + 32 (D+H) H bytes, freed by destroy).  out_seq may be NULL, or receives the
  * output sequence as in lstm_dyn_forward_seq.  out_h/out_c may not alias
  * h0/c0 (the backward reads h0, c0).  Any other forward on the handle
- * discards what was kept.  Returns as lstm_dyn_forward; a GRU or RNN handle
- * is ERR_UNSUPPORTED.
+ * discards what was kept.  Returns as lstm_dyn_forward.
  */
 int lstm_dyn_forward_train(lstm_dyn_t* h, const void* x, const int32_t* lengths, const void* W,
                            const void* U, const float* b, const float* h0, const float* c0,
@@ -236,16 +235,19 @@ int lstm_dyn_forward_train(lstm_dyn_t* h, const void* x, const int32_t* lengths,
  * Upstream gradients: d_out_h, d_out_c [B][H] fp32 (of out_h, out_c) and
  * d_seq [B][T_max][H] fp32 of the output sequence, or NULL (entries at
  * t >= L[b] have no effect).  Written, all fp32, caller-owned device memory,
- * 4-byte aligned: dx [B][T_max][D] (zero at t >= L[b]), dW [D][4H],
- * dU [H][4H], db [4H], dh0, dc0 [B][H]; no output may overlap another
- * argument.  A step a row does not take passes its state through unchanged,
+ * 4-byte aligned: dx [B][T_max][D] (zero at t >= L[b]), dW, dU and db
+ * in the layouts of the handle's cell (LSTM [D][4H], [H][4H], [4H]; GRU
+ * [D][3H], [H][3H], [6H] = d b_ih ++ d b_hh; RNN [D][H], [H][H], [H]), dh0
+ * and dc0 [B][H]; no output may overlap another argument.  GRU and RNN
+ * handles have no cell state: c0 and d_out_c are ignored and dc0 may be
+ * NULL (else zeros).  A step a row does not take passes its state through unchanged,
  * so its gradient is the identity.  Step t's dz comes from the kept
  * pre-activations; dh <- dz U^T and the weight gradients (sums over all valid
  * steps) run as fp32 GEMMs.  Synchronises once with the host (the step
  * offsets) and then issues two launches per step.  Consumes what the forward
  * kept (a second backward needs another forward for training).  Returns
  * LSTM_DYN_OK, ERR_INVALID (bad arguments, or no forward for training kept),
- * ERR_UNSUPPORTED (GRU or RNN handle), ERR_HIP.
+ * ERR_HIP.
  */
 int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* lengths, const void* W,
                       const void* U, const float* b, const float* h0, const float* c0,
@@ -316,10 +318,10 @@ int lstm_dyn_check_stop_args(int B, int D, int H, int T_max, int dtype, int cell
                              const float* out_h, const float* out_c, const int32_t* out_steps,
                              const float* out_seq);
 
-/* The argument checks of lstm_dyn_backward for the given sizes (NULL,
- * alignment, overlap), without touching the memory.  Returns LSTM_DYN_OK or
- * ERR_INVALID. */
-int lstm_dyn_check_backward_args(int B, int D, int H, int T_max, int dtype, const void* x,
+/* The argument checks of lstm_dyn_backward for the given sizes and cell
+ * (LSTM_DYN_CELL_*: NULL, alignment, overlap), without touching the memory.
+ * Returns LSTM_DYN_OK or ERR_INVALID. */
+int lstm_dyn_check_backward_args(int B, int D, int H, int T_max, int dtype, int cell, const void* x,
                                  const int32_t* lengths, const void* W, const void* U,
                                  const float* b, const float* h0, const float* c0,
                                  const float* d_out_h, const float* d_out_c, const float* d_seq,

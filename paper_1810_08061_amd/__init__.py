@@ -85,7 +85,7 @@ def _load():
     lib.lstm_dyn_forward_train.restype = I
     lib.lstm_dyn_backward.argtypes = [P] * 18
     lib.lstm_dyn_backward.restype = I
-    lib.lstm_dyn_check_backward_args.argtypes = [I] * 5 + [P] * 16
+    lib.lstm_dyn_check_backward_args.argtypes = [I] * 6 + [P] * 16
     lib.lstm_dyn_check_backward_args.restype = I
     lib.lstm_dyn_forward.argtypes = [P] * 11
     lib.lstm_dyn_forward.restype = I
@@ -176,10 +176,11 @@ def lstm_dyn_backward(handle: int, x: int, lengths: int, W: int, U: int, b: int,
         raise LstmDynError(rc, "lstm_dyn_backward")
 
 
-def lstm_dyn_check_backward_args(B: int, D: int, H: int, T_max: int, dtype: int, *ptrs) -> int:
+def lstm_dyn_check_backward_args(B: int, D: int, H: int, T_max: int, dtype: int, cell: int,
+                                 *ptrs) -> int:
     """Pointers in the order of lstm_dyn_backward: x, lengths, W, U, b, h0, c0,
     d_out_h, d_out_c, d_seq, dx, dW, dU, db, dh0, dc0."""
-    return _load().lstm_dyn_check_backward_args(B, D, H, T_max, dtype, *ptrs)
+    return _load().lstm_dyn_check_backward_args(B, D, H, T_max, dtype, cell, *ptrs)
 
 
 def lstm_dyn_destroy(handle: int) -> None:
@@ -355,9 +356,9 @@ class LstmDyn:
                               out_seq.data_ptr() if out_seq is not None else 0, s)
         return (out_h, out_c, out_steps) if out_seq is None else (out_h, out_c, out_steps, out_seq)
 
-    def forward_train(self, x, lengths, W, U, b, h0, c0, out_h=None, out_c=None, out_seq=None,
+    def forward_train(self, x, lengths, W, U, b, h0, c0=None, out_h=None, out_c=None, out_seq=None,
                       with_seq=False, stream=None):
-        """``forward`` that also keeps what ``backward`` needs (LSTM handles).
+        """``forward`` that also keeps what ``backward`` needs.
         Returns (out_h, out_c) and, with ``with_seq`` or a given ``out_seq``,
         the output sequence after them."""
         import torch
@@ -371,27 +372,37 @@ class LstmDyn:
                                out_c.data_ptr(), out_seq.data_ptr() if out_seq is not None else 0, s)
         return (out_h, out_c) if out_seq is None else (out_h, out_c, out_seq)
 
-    def backward(self, x, lengths, W, U, b, h0, c0, d_out_h, d_out_c, d_seq=None, stream=None):
+    def backward(self, x, lengths, W, U, b, h0, c0, d_out_h, d_out_c=None, d_seq=None,
+                 stream=None):
         """Gradients after ``forward_train`` with the same inputs; returns a
-        dict of float32 tensors dx [B, T, D], dW [D, 4H], dU [H, 4H], db [4H],
-        dh0, dc0 [B, H]."""
+        dict of float32 tensors dx [B, T, D], dW [D, G], dU [H, G], db, dh0
+        [B, H] and, for the LSTM, dc0 [B, H] (G and db as the cell's weights:
+        LSTM 4H, [4H]; GRU 3H, [6H] = d b_ih ++ d b_hh; RNN H, [H]).  GRU and
+        RNN ignore c0 and d_out_c (None allowed)."""
         import torch
         B, D, H, T = self.B, self.D, self.H, self.T
+        g, nb = _CELL_SHAPES[self.cell]
+        lstm = self.cell == CELL_LSTM
         dev = x.device
-        for name, t, shape in (("d_out_h", d_out_h, (B, H)), ("d_out_c", d_out_c, (B, H))):
-            self._check(name, t, torch.float32, shape)
+        self._check("d_out_h", d_out_h, torch.float32, (B, H))
+        if lstm or d_out_c is not None:
+            self._check("d_out_c", d_out_c, torch.float32, (B, H))
         if d_seq is not None:
             self._check("d_seq", d_seq, torch.float32, (B, T, H))
-        out = {"dx": torch.empty((B, T, D), device=dev), "dW": torch.empty((D, 4 * H), device=dev),
-               "dU": torch.empty((H, 4 * H), device=dev), "db": torch.empty((4 * H,), device=dev),
-               "dh0": torch.empty((B, H), device=dev), "dc0": torch.empty((B, H), device=dev)}
+        out = {"dx": torch.empty((B, T, D), device=dev), "dW": torch.empty((D, g * H), device=dev),
+               "dU": torch.empty((H, g * H), device=dev), "db": torch.empty((nb * H,), device=dev),
+               "dh0": torch.empty((B, H), device=dev)}
+        if lstm:
+            out["dc0"] = torch.empty((B, H), device=dev)
         if stream is None:
             stream = torch.cuda.current_stream(dev)
         s = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+        ptr = lambda t: t.data_ptr() if t is not None else 0
         lstm_dyn_backward(self.handle, x.data_ptr(), lengths.data_ptr(), W.data_ptr(), U.data_ptr(),
-                          b.data_ptr(), h0.data_ptr(), c0.data_ptr(), d_out_h.data_ptr(),
-                          d_out_c.data_ptr(), d_seq.data_ptr() if d_seq is not None else 0,
-                          *(out[k].data_ptr() for k in ("dx", "dW", "dU", "db", "dh0", "dc0")), s)
+                          b.data_ptr(), h0.data_ptr(), ptr(c0) if lstm else 0, d_out_h.data_ptr(),
+                          ptr(d_out_c) if lstm else 0, ptr(d_seq),
+                          *(out[k].data_ptr() for k in ("dx", "dW", "dU", "db", "dh0")),
+                          out["dc0"].data_ptr() if lstm else 0, s)
         return out
 
     def query(self, what: int) -> int:

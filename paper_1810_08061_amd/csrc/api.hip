@@ -304,11 +304,9 @@ extern "C" int lstm_dyn_create_cell(lstm_dyn_t** out, int B, int D, int H, int T
         const int per_cu_stop = persistent_blocks_per_cu(bf16, plan.mt, plan.ksw, plan.kw,
                                                          plan.nstate, plan.lds_bytes, cell, 1);
         stop_ok = per_cu_stop >= 1 && plan.groups <= per_cu_stop * cus;
-        if (cell == LSTM_DYN_CELL_LSTM) {
-            const int per_cu_save = persistent_blocks_per_cu(bf16, plan.mt, plan.ksw, plan.kw,
-                                                             plan.nstate, plan.lds_bytes, cell, 2);
-            save_ok = per_cu_save >= 1 && plan.groups <= per_cu_save * cus;
-        }
+        const int per_cu_save = persistent_blocks_per_cu(bf16, plan.mt, plan.ksw, plan.kw,
+                                                         plan.nstate, plan.lds_bytes, cell, 2);
+        save_ok = per_cu_save >= 1 && plan.groups <= per_cu_save * cus;
     }
     lstm_dyn* h = new (std::nothrow) lstm_dyn();
     if (!h) return LSTM_DYN_ERR_NOMEM;
@@ -734,8 +732,8 @@ extern "C" int lstm_dyn_forward_train(lstm_dyn_t* h, const void* x, const int32_
                            : check_args_cell(h->B, h->D, h->H, h->T, h->dtype, h->cell, x, lengths,
                                              W, U, b, h0, c0, out_h, out_c);
     if (rc != LSTM_DYN_OK) return rc;
-    if (h->cell != LSTM_DYN_CELL_LSTM) return LSTM_DYN_ERR_UNSUPPORTED;
-    if (out_h == h0 || out_c == c0) return LSTM_DYN_ERR_INVALID;  // the backward reads h0, c0
+    if (out_h == h0 || (h->cell == LSTM_DYN_CELL_LSTM && out_c == c0))
+        return LSTM_DYN_ERR_INVALID;  // the backward reads h0, c0
     const int trc = ensure_train(h);
     if (trc != LSTM_DYN_OK) return trc;
     TrainWs* tw = h->train;
@@ -753,9 +751,17 @@ extern "C" int lstm_dyn_forward_train(lstm_dyn_t* h, const void* x, const int32_
     } while (0)
     auto mark = [&](int i) { return h->timing ? hipEventRecord(h->ev[i], s) : hipSuccess; };
     LD_CHECK(mark(0));
+    if (h->cell != LSTM_DYN_CELL_LSTM) {
+        // the cell's weights in the four-block layout (the backward uses them too)
+        LD_CHECK(launch_cell_pack(d, W, U, b, h->w4, h->u4, h->b4, s));
+        W = h->w4;
+        U = h->u4;
+        b = h->b4;
+        h->launches_last++;
+    }
     LD_CHECK(launch_prep(d, lengths, h->ws, s));
     LD_CHECK(mark(1));
-    h->launches_last = 1;
+    h->launches_last++;
     if (h->mode == LSTM_DYN_PERSISTENT && !h->plan.single && h->save_ok) {
         LD_CHECK(input_projection(h, x, W, b, s));
         LD_CHECK(mark(2));
@@ -792,7 +798,7 @@ extern "C" int lstm_dyn_forward_train(lstm_dyn_t* h, const void* x, const int32_
     return LSTM_DYN_OK;
 }
 
-static int check_backward_args(int B, int D, int H, int T, int dtype, const void* x,
+static int check_backward_args(int B, int D, int H, int T, int dtype, int cell, const void* x,
                                const int32_t* lengths, const void* W, const void* U,
                                const float* b, const float* h0, const float* c0,
                                const float* d_out_h, const float* d_out_c, const float* d_seq,
@@ -800,37 +806,49 @@ static int check_backward_args(int B, int D, int H, int T, int dtype, const void
                                const float* db, const float* dh0, const float* dc0) {
     if (B < 1 || D < 1 || H < 1 || T < 1) return LSTM_DYN_ERR_INVALID;
     if (dtype != LSTM_DYN_F32 && dtype != LSTM_DYN_BF16) return LSTM_DYN_ERR_INVALID;
+    if (!valid_cell(cell)) return LSTM_DYN_ERR_INVALID;
+    const bool has_c = cell == LSTM_DYN_CELL_LSTM;  // GRU, RNN: c0, d_out_c, dc0 may be NULL
+    if (!has_c) {
+        c0 = nullptr;
+        d_out_c = nullptr;
+    }
     const void* ins[] = {x, lengths, W, U, b, h0, c0, d_out_h, d_out_c, d_seq};
     const void* outs[] = {dx, dW, dU, db, dh0, dc0};
     const long long e = dtype == LSTM_DYN_BF16 ? 2 : 4;
-    const long long nin[] = {(long long)B * T * D * e, 4LL * B, (long long)D * 4 * H * e,
-                             (long long)H * 4 * H * e, 16LL * H, 4LL * B * H, 4LL * B * H,
+    const long long G = (long long)cell_cols(cell) * H, nb = 4LL * cell_bias(cell) * H;
+    const long long nin[] = {(long long)B * T * D * e, 4LL * B, (long long)D * G * e,
+                             (long long)H * G * e, nb, 4LL * B * H, 4LL * B * H,
                              4LL * B * H, 4LL * B * H, d_seq ? 4LL * B * T * H : 0};
-    const long long nout[] = {4LL * B * T * D, 16LL * D * H, 16LL * H * H, 16LL * H, 4LL * B * H,
+    const long long nout[] = {4LL * B * T * D, 4LL * D * G, 4LL * H * G, nb, 4LL * B * H,
                               4LL * B * H};
     for (int i = 0; i < 10; ++i) {
-        if (!ins[i] && i != 9) return LSTM_DYN_ERR_INVALID;
+        const bool optional = i == 9 || (!has_c && (i == 6 || i == 8));
+        if (!ins[i] && !optional) return LSTM_DYN_ERR_INVALID;
         if (ins[i] && (reinterpret_cast<uintptr_t>(ins[i]) & 3)) return LSTM_DYN_ERR_INVALID;
     }
     for (int i = 0; i < 6; ++i) {
-        if (!outs[i] || (reinterpret_cast<uintptr_t>(outs[i]) & 3)) return LSTM_DYN_ERR_INVALID;
+        if (!outs[i]) {
+            if (i == 5 && !has_c) continue;
+            return LSTM_DYN_ERR_INVALID;
+        }
+        if (reinterpret_cast<uintptr_t>(outs[i]) & 3) return LSTM_DYN_ERR_INVALID;
         for (int j = 0; j < 10; ++j)
             if (ins[j] && overlaps(outs[i], nout[i], ins[j], nin[j])) return LSTM_DYN_ERR_INVALID;
         for (int j = 0; j < i; ++j)
-            if (overlaps(outs[i], nout[i], outs[j], nout[j])) return LSTM_DYN_ERR_INVALID;
+            if (outs[j] && overlaps(outs[i], nout[i], outs[j], nout[j])) return LSTM_DYN_ERR_INVALID;
     }
     return LSTM_DYN_OK;
 }
 
-extern "C" int lstm_dyn_check_backward_args(int B, int D, int H, int T, int dtype, const void* x,
-                                            const int32_t* lengths, const void* W, const void* U,
-                                            const float* b, const float* h0, const float* c0,
-                                            const float* d_out_h, const float* d_out_c,
-                                            const float* d_seq, const float* dx, const float* dW,
-                                            const float* dU, const float* db, const float* dh0,
-                                            const float* dc0) {
-    return check_backward_args(B, D, H, T, dtype, x, lengths, W, U, b, h0, c0, d_out_h, d_out_c,
-                               d_seq, dx, dW, dU, db, dh0, dc0);
+extern "C" int lstm_dyn_check_backward_args(int B, int D, int H, int T, int dtype, int cell,
+                                            const void* x, const int32_t* lengths, const void* W,
+                                            const void* U, const float* b, const float* h0,
+                                            const float* c0, const float* d_out_h,
+                                            const float* d_out_c, const float* d_seq,
+                                            const float* dx, const float* dW, const float* dU,
+                                            const float* db, const float* dh0, const float* dc0) {
+    return check_backward_args(B, D, H, T, dtype, cell, x, lengths, W, U, b, h0, c0, d_out_h,
+                               d_out_c, d_seq, dx, dW, dU, db, dh0, dc0);
 }
 
 extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* lengths,
@@ -839,11 +857,19 @@ extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* le
                                  const float* d_seq, float* dx, float* dW, float* dU, float* db,
                                  float* dh0, float* dc0, void* stream) {
     if (!h) return LSTM_DYN_ERR_INVALID;
-    const int rc = check_backward_args(h->B, h->D, h->H, h->T, h->dtype, x, lengths, W, U, b, h0,
-                                       c0, d_out_h, d_out_c, d_seq, dx, dW, dU, db, dh0, dc0);
+    const int rc = check_backward_args(h->B, h->D, h->H, h->T, h->dtype, h->cell, x, lengths, W,
+                                       U, b, h0, c0, d_out_h, d_out_c, d_seq, dx, dW, dU, db, dh0,
+                                       dc0);
     if (rc != LSTM_DYN_OK) return rc;
-    if (h->cell != LSTM_DYN_CELL_LSTM) return LSTM_DYN_ERR_UNSUPPORTED;
     if (!h->saved || !h->train) return LSTM_DYN_ERR_INVALID;  // needs a forward for training
+    const bool packed = h->cell != LSTM_DYN_CELL_LSTM;
+    if (packed) {  // the four-block weights the forward for training packed
+        W = h->w4;
+        U = h->u4;
+        d_out_c = nullptr;
+    }
+    // GRU: the cell kernel leaves h's direct path to h' in dH, the product adds to it
+    const float beta = h->cell == LSTM_DYN_CELL_GRU ? 1.0f : 0.0f;
     TrainWs* tw = h->train;
     hipStream_t s = static_cast<hipStream_t>(stream);
     h->last_stream = s;
@@ -889,11 +915,12 @@ extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* le
     if (!d.bf16) {
         for (int t = max_len - 1; t >= 0; --t) {
             const int act = off[t + 1] - off[t];
-            LD_CHECK(launch_bwd_cell(d, t, act, tw->save_c, d_seq, tw->dH, tw->dC, h->ws, s));
-            // dH[0:act] = dz_t U^T (column-major: dH^T = U_il^T-as-stored^T dz_t^T)
+            LD_CHECK(launch_bwd_cell(d, t, act, tw->save_h, tw->save_c, d_seq, tw->dH, tw->dC,
+                                     h->ws, s));
+            // dH[0:act] (+)= dz_t U^T (column-major: dH^T = U_il^T-as-stored^T dz_t^T)
             RB_CHECK(rocblas_sgemm(tw->rb, rocblas_operation_transpose, rocblas_operation_none, d.H,
                                    act, H4, &one, tw->u_il, H4, h->ws.gx + (size_t)off[t] * H4, H4,
-                                   &zero, tw->dH, d.H));
+                                   &beta, tw->dH, d.H));
             h->launches_last += 2;
         }
         LD_CHECK(launch_bwd_state_out(d, tw->dH, tw->dC, nullptr, dh0, dc0, h->ws, s));
@@ -906,11 +933,11 @@ extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* le
         h->launches_last += 2;
         for (int t = max_len - 1; t >= 0; --t) {
             const int act = off[t + 1] - off[t];
-            LD_CHECK(launch_bwd_cell16(d, t, act, tw->save_c, d_seq, tw->dH, tw->dC, tw->srow,
-                                       tw->dzs16, h->ws, s));
+            LD_CHECK(launch_bwd_cell16(d, t, act, tw->save_h, tw->save_c, d_seq, tw->dH, tw->dC,
+                                       tw->srow, tw->dzs16, h->ws, s));
             RB_CHECK(rocblas_gemm_ex(tw->rb, rocblas_operation_transpose, rocblas_operation_none,
                                      d.H, act, H4, &alpha_u, tw->u16, rocblas_datatype_f16_r, H4,
-                                     tw->dzs16, rocblas_datatype_f16_r, H4, &zero, tw->dH,
+                                     tw->dzs16, rocblas_datatype_f16_r, H4, &beta, tw->dH,
                                      rocblas_datatype_f32_r, d.H, tw->dH, rocblas_datatype_f32_r,
                                      d.H, rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0, 0));
             h->launches_last += 2;
@@ -974,9 +1001,18 @@ extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* le
         LD_CHECK(hipMemsetAsync(tw->du_il, 0, (size_t)d.H * H4 * sizeof(float), s));
         LD_CHECK(hipMemsetAsync(tw->db_il, 0, (size_t)H4 * sizeof(float), s));
     }
-    LD_CHECK(launch_bwd_permute(d, tw->dw_il, dW, d.D, s));
-    LD_CHECK(launch_bwd_permute(d, tw->du_il, dU, d.H, s));
-    LD_CHECK(launch_bwd_permute(d, tw->db_il, db, 1, s));
+    if (!packed) {
+        LD_CHECK(launch_bwd_permute(d, tw->dw_il, dW, d.D, s));
+        LD_CHECK(launch_bwd_permute(d, tw->du_il, dU, d.H, s));
+        LD_CHECK(launch_bwd_permute(d, tw->db_il, db, 1, s));
+    } else {
+        // from the four blocks to the cell's layout; the GRU's two bias vectors
+        // take the input and the recurrent side of the packed bias gradient
+        LD_CHECK(launch_bwd_unpack(d, tw->dw_il, dW, d.D, 0, s));
+        LD_CHECK(launch_bwd_unpack(d, tw->du_il, dU, d.H, 1, s));
+        LD_CHECK(launch_bwd_unpack(d, tw->db_il, db, 1, 0, s));
+        if (h->cell == LSTM_DYN_CELL_GRU) LD_CHECK(launch_bwd_unpack(d, tw->db_il, db + 3 * d.H, 1, 1, s));
+    }
     LD_CHECK(launch_bwd_dx(d, tw->xc, rows, lengths, dx, h->ws, s));
     h->launches_last += 4;
 #undef RB_CHECK

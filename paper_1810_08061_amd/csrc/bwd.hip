@@ -45,38 +45,72 @@ bwd_init_kernel(const float* __restrict__ dh_out, const float* __restrict__ dc_o
         const int s = (int)(i / H), u = (int)(i - (long)s * H);
         const long ib = (long)perm[s] * H + u;
         dH[i] = dh_out[ib];
-        dC[i] = dc_out[ib];
+        dC[i] = dc_out ? dc_out[ib] : 0.0f;  // no cell state: no upstream gradient
     }
 }
 
-// The cell's backward for the rows of step t: one (row, unit) per thread.
+// The backward of one cell step for one (row, unit), from its pre-activations
+// z (the four gate blocks of the packed layout), the state the step started
+// from (hp, cp) and the gradients of the state after it (dh, dc).  Returns dz
+// and sets the gradient reaching the previous state other than through
+// dz U^T: dc_prev (LSTM) and dh_direct (GRU: h' depends on h through u).
+template <int CELL>
+__device__ inline f32x4_t cell_backward(f32x4_t z, float hp, float cp, float dh, float dc,
+                                        float& dc_prev, float& dh_direct) {
+    f32x4_t dz;
+    dc_prev = 0.0f;
+    dh_direct = 0.0f;
+    if constexpr (CELL == CELL_LSTM) {
+        const float ig = sigmoid_f(z[0]), fg = sigmoid_f(z[1]);
+        const float gg = tanh_f(z[2]), og = sigmoid_f(z[3]);
+        const float c = fg * cp + ig * gg;
+        const float tc = tanh_f(c);
+        const float d_o = dh * tc;
+        const float dct = dc + dh * og * (1.0f - tc * tc);
+        dz[0] = dct * gg * ig * (1.0f - ig);
+        dz[1] = dct * cp * fg * (1.0f - fg);
+        dz[2] = dct * ig * (1.0f - gg * gg);
+        dz[3] = d_o * og * (1.0f - og);
+        dc_prev = dct * fg;
+    } else if constexpr (CELL == CELL_GRU) {
+        // z = (r, u, recurrent part of n, input part of n)
+        const float rg = sigmoid_f(z[0]), ug = sigmoid_f(z[1]);
+        const float ng = tanh_f(z[3] + rg * z[2]);
+        const float dzn = dh * (1.0f - ug) * (1.0f - ng * ng);
+        dz[0] = dzn * z[2] * rg * (1.0f - rg);
+        dz[1] = dh * (hp - ng) * ug * (1.0f - ug);
+        dz[2] = dzn * rg;
+        dz[3] = dzn;
+        dh_direct = dh * ug;
+    } else {
+        const float hn = tanh_f(z[0]);
+        dz[0] = dh * (1.0f - hn * hn);
+        dz[1] = 0.0f;
+        dz[2] = 0.0f;
+        dz[3] = 0.0f;
+    }
+    return dz;
+}
+
+// The cell's backward for the rows of step t: one (row, unit) per thread; dz
+// over z, dC <- dc_prev, and dH <- dh_direct (the GEMM then adds dz U^T).
+template <int CELL>
 __global__ void __launch_bounds__(256)
-bwd_cell_kernel(float* gx, const float* __restrict__ save_c, const float* __restrict__ dseq,
-                const int32_t* __restrict__ perm, const int32_t* __restrict__ offsets, float* dH,
-                float* dC, int t, int H, int T) {
+bwd_cell_kernel(float* gx, const float* __restrict__ save_h, const float* __restrict__ save_c,
+                const float* __restrict__ dseq, const int32_t* __restrict__ perm,
+                const int32_t* __restrict__ offsets, float* dH, float* dC, int t, int H, int T) {
     const int off = offsets[t], act = offsets[t + 1] - off;
     const long n = (long)act * H;
     for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += (long)gridDim.x * 256) {
         const int s = (int)(i / H), u = (int)(i - (long)s * H);
         const long r = off + s;
         f32x4_t* zp = reinterpret_cast<f32x4_t*>(gx + r * 4 * H + 4 * u);
-        const f32x4_t z = *zp;
-        const float ig = sigmoid_f(z[0]), fg = sigmoid_f(z[1]);
-        const float gg = tanh_f(z[2]), og = sigmoid_f(z[3]);
-        const float cp = save_c[r * H + u];
-        const float c = fg * cp + ig * gg;
-        const float tc = tanh_f(c);
         float dh = dH[i];
         if (dseq) dh += dseq[((long)perm[s] * T + t) * H + u];
-        const float d_o = dh * tc;
-        const float dct = dC[i] + dh * og * (1.0f - tc * tc);
-        f32x4_t dz;
-        dz[0] = dct * gg * ig * (1.0f - ig);
-        dz[1] = dct * cp * fg * (1.0f - fg);
-        dz[2] = dct * ig * (1.0f - gg * gg);
-        dz[3] = d_o * og * (1.0f - og);
-        *zp = dz;
-        dC[i] = dct * fg;
+        float dcp, dhd;
+        *zp = cell_backward<CELL>(*zp, save_h[r * H + u], save_c[r * H + u], dh, dC[i], dcp, dhd);
+        dC[i] = dcp;
+        dH[i] = dhd;
     }
 }
 
@@ -84,10 +118,12 @@ bwd_cell_kernel(float* gx, const float* __restrict__ save_c, const float* __rest
 // dz16 in fp16, scaled by a power of two that brings its largest magnitude
 // into [2^13, 2^14), for the product dz U^T; dH of a row holds its gradient
 // times srow (the scale of the dz it was last formed from; 1 at the start).
+template <int CELL>
 __global__ void __launch_bounds__(256)
-bwd_cell16_kernel(float* gx, const float* __restrict__ save_c, const float* __restrict__ dseq,
-                  const int32_t* __restrict__ perm, const int32_t* __restrict__ offsets, float* dH,
-                  float* dC, float* srow, _Float16* dz16, int t, int H, int T) {
+bwd_cell16_kernel(float* gx, const float* __restrict__ save_h, const float* __restrict__ save_c,
+                  const float* __restrict__ dseq, const int32_t* __restrict__ perm,
+                  const int32_t* __restrict__ offsets, float* dH, float* dC, float* srow,
+                  _Float16* dz16, int t, int H, int T) {
     __shared__ unsigned red[4];
     const int off = offsets[t];
     const int s = blockIdx.x, tid = threadIdx.x;
@@ -98,23 +134,14 @@ bwd_cell16_kernel(float* gx, const float* __restrict__ save_c, const float* __re
     unsigned m = 0;
     for (int u = tid; u < H; u += 256) {
         f32x4_t* zp = reinterpret_cast<f32x4_t*>(gx + r * 4 * H + 4 * u);
-        const f32x4_t z = *zp;
-        const float ig = sigmoid_f(z[0]), fg = sigmoid_f(z[1]);
-        const float gg = tanh_f(z[2]), og = sigmoid_f(z[3]);
-        const float cp = save_c[r * H + u];
-        const float c = fg * cp + ig * gg;
-        const float tc = tanh_f(c);
         float dh = dH[(long)s * H + u] * inv;
         if (dseq_row) dh += dseq_row[u];
-        const float d_o = dh * tc;
-        const float dct = dC[(long)s * H + u] + dh * og * (1.0f - tc * tc);
-        f32x4_t dz;
-        dz[0] = dct * gg * ig * (1.0f - ig);
-        dz[1] = dct * cp * fg * (1.0f - fg);
-        dz[2] = dct * ig * (1.0f - gg * gg);
-        dz[3] = d_o * og * (1.0f - og);
+        float dcp, dhd;
+        const f32x4_t dz = cell_backward<CELL>(*zp, save_h[r * H + u], save_c[r * H + u], dh,
+                                               dC[(long)s * H + u], dcp, dhd);
         *zp = dz;
-        dC[(long)s * H + u] = dct * fg;
+        dC[(long)s * H + u] = dcp;
+        dH[(long)s * H + u] = dhd;  // scaled below, once the row's scale is known
 #pragma unroll
         for (int g = 0; g < 4; ++g) m = max(m, __float_as_uint(fabsf(dz[g])) & 0x7fffffffu);
     }
@@ -133,6 +160,7 @@ bwd_cell16_kernel(float* gx, const float* __restrict__ save_c, const float* __re
         const f32x4_t dz = *reinterpret_cast<const f32x4_t*>(gx + r * 4 * H + 4 * u);
 #pragma unroll
         for (int g = 0; g < 4; ++g) dz16[(long)s * 4 * H + 4 * u + g] = (_Float16)(dz[g] * sc);
+        dH[(long)s * H + u] *= sc;
     }
     if (tid == 0) srow[s] = sc;  // every thread read the old value before the barrier
 }
@@ -148,7 +176,7 @@ bwd_state_out_kernel(const float* __restrict__ dH, const float* __restrict__ dC,
         const int s = (int)(i / H), u = (int)(i - (long)s * H);
         const long ib = (long)perm[s] * H + u;
         dh0[ib] = srow ? dH[i] / srow[s] : dH[i];
-        dc0[ib] = dC[i];
+        if (dc0) dc0[ib] = dC[i];
     }
 }
 
@@ -179,6 +207,27 @@ bwd_permute_kernel(const float* __restrict__ il, float* out, int rows, int H) {
         const long k = i / (4 * H);
         const int cp = (int)(i - k * 4 * H);
         out[k * 4 * H + gate_col(cp, H)] = il[i];
+    }
+}
+
+// GRU and RNN gradients from the packed four-block layout (gate-interleaved
+// columns c' = 4u + g) to the cell's own: block g of column j of the output
+// comes from interleaved column 4u + src(g).  part: 0 the input side (W, b_ih
+// or b), 1 the recurrent side (U, b_hh).
+__device__ inline int unpack_src(int cell, int part, int g) {
+    if (cell == CELL_RNN) return 0;
+    if (g < 2) return g;               // r, u
+    return part == 0 ? 3 : 2;          // n: input part in block 3, recurrent in block 2
+}
+
+__global__ void __launch_bounds__(256)
+bwd_unpack_kernel(const float* __restrict__ il, float* out, int rows, int H, int cell, int part) {
+    const int G = cell == CELL_GRU ? 3 * H : H;
+    const long n = (long)rows * G;
+    for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += (long)gridDim.x * 256) {
+        const long k = i / G;
+        const int j = (int)(i - k * G), g = j / H, u = j - g * H;
+        out[i] = il[k * 4 * H + 4 * u + unpack_src(cell, part, g)];
     }
 }
 
@@ -252,10 +301,21 @@ hipError_t launch_bwd_init(const Dims& d, const float* dh_out, const float* dc_o
     return hipGetLastError();
 }
 
-hipError_t launch_bwd_cell(const Dims& d, int t, int act, const float* save_c, const float* dseq,
-                           float* dH, float* dC, const Workspace& ws, hipStream_t s) {
-    hipLaunchKernelGGL(bwd_cell_kernel, dim3(grid_of((long)act * d.H)), dim3(256), 0, s, ws.gx,
-                       save_c, dseq, ws.perm, ws.offsets, dH, dC, t, d.H, d.T);
+hipError_t launch_bwd_cell(const Dims& d, int t, int act, const float* save_h, const float* save_c,
+                           const float* dseq, float* dH, float* dC, const Workspace& ws,
+                           hipStream_t s) {
+    auto k = d.cell == CELL_GRU ? bwd_cell_kernel<CELL_GRU>
+             : d.cell == CELL_RNN ? bwd_cell_kernel<CELL_RNN> : bwd_cell_kernel<CELL_LSTM>;
+    hipLaunchKernelGGL(k, dim3(grid_of((long)act * d.H)), dim3(256), 0, s, ws.gx, save_h, save_c,
+                       dseq, ws.perm, ws.offsets, dH, dC, t, d.H, d.T);
+    return hipGetLastError();
+}
+
+hipError_t launch_bwd_unpack(const Dims& d, const float* il, float* out, int rows, int part,
+                             hipStream_t s) {
+    const long n = (long)rows * (d.cell == CELL_GRU ? 3 : 1) * d.H;
+    hipLaunchKernelGGL(bwd_unpack_kernel, dim3(grid_of(n)), dim3(256), 0, s, il, out, rows, d.H,
+                       d.cell, part);
     return hipGetLastError();
 }
 
@@ -266,10 +326,12 @@ hipError_t launch_bwd_state_out(const Dims& d, const float* dH, const float* dC,
     return hipGetLastError();
 }
 
-hipError_t launch_bwd_cell16(const Dims& d, int t, int act, const float* save_c, const float* dseq,
-                             float* dH, float* dC, float* srow, _Float16* dz16, const Workspace& ws,
-                             hipStream_t s) {
-    hipLaunchKernelGGL(bwd_cell16_kernel, dim3(act), dim3(256), 0, s, ws.gx, save_c, dseq, ws.perm,
+hipError_t launch_bwd_cell16(const Dims& d, int t, int act, const float* save_h,
+                             const float* save_c, const float* dseq, float* dH, float* dC,
+                             float* srow, _Float16* dz16, const Workspace& ws, hipStream_t s) {
+    auto k = d.cell == CELL_GRU ? bwd_cell16_kernel<CELL_GRU>
+             : d.cell == CELL_RNN ? bwd_cell16_kernel<CELL_RNN> : bwd_cell16_kernel<CELL_LSTM>;
+    hipLaunchKernelGGL(k, dim3(act), dim3(256), 0, s, ws.gx, save_h, save_c, dseq, ws.perm,
                        ws.offsets, dH, dC, srow, dz16, t, d.H, d.T);
     return hipGetLastError();
 }

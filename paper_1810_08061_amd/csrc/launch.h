@@ -81,7 +81,7 @@ hipError_t launch_persistent(const Dims& d, const PersistentConfig& pc, const vo
                              const float* h0, const float* c0, float* out_h, float* out_c,
                              const Workspace& ws, hipStream_t s);
 // Occupancy check for the co-resident grid; returns blocks per CU (0 if none).
-// mode: 0 plain, 1 termination from the state, 2 forward for training (LSTM only)
+// mode: 0 plain, 1 termination from the state, 2 forward for training
 int persistent_blocks_per_cu(int bf16, int mt, int ksw, int kw, int nst, int lds_bytes, int cell,
                              int mode);
 // Compiled variant with exactly (mt, kw, ksw) and the smallest state capacity >= nstate.
@@ -114,15 +114,20 @@ hipError_t launch_step_stop(const Dims& d, int t, const StopArgs& stop, const Wo
 hipError_t launch_bwd_weights(const Dims& d, const void* W, int rows, float* Wil, hipStream_t s);
 hipError_t launch_bwd_init(const Dims& d, const float* dh_out, const float* dc_out, float* dH,
                            float* dC, const Workspace& ws, hipStream_t s);
-hipError_t launch_bwd_cell(const Dims& d, int t, int act, const float* save_c, const float* dseq,
-                           float* dH, float* dC, const Workspace& ws, hipStream_t s);
+hipError_t launch_bwd_cell(const Dims& d, int t, int act, const float* save_h, const float* save_c,
+                           const float* dseq, float* dH, float* dC, const Workspace& ws,
+                           hipStream_t s);
+// GRU/RNN gradients, packed four-block (interleaved) layout -> the cell's own;
+// part 0: input side (W, b_ih / b), 1: recurrent side (U, b_hh).
+hipError_t launch_bwd_unpack(const Dims& d, const float* il, float* out, int rows, int part,
+                             hipStream_t s);
 hipError_t launch_bwd_state_out(const Dims& d, const float* dH, const float* dC, const float* srow,
                                 float* dh0, float* dc0, const Workspace& ws, hipStream_t s);
 // bf16 data: the cell's backward with one workgroup per row, also writing the
 // row's dz in fp16 scaled by a power of two (srow) for dz U^T.
-hipError_t launch_bwd_cell16(const Dims& d, int t, int act, const float* save_c, const float* dseq,
-                             float* dH, float* dC, float* srow, _Float16* dz16, const Workspace& ws,
-                             hipStream_t s);
+hipError_t launch_bwd_cell16(const Dims& d, int t, int act, const float* save_h,
+                             const float* save_c, const float* dseq, float* dH, float* dC,
+                             float* srow, _Float16* dz16, const Workspace& ws, hipStream_t s);
 hipError_t launch_bwd_ones(float* a, int n, hipStream_t s);
 hipError_t launch_bwd_gather_x(const Dims& d, const void* x, long rows, float* xc,
                                const Workspace& ws, hipStream_t s);

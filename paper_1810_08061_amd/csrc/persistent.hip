@@ -839,12 +839,12 @@ typedef void (*persist_fn)(PersistParams);
 
 // f[cell][mode]: the variant compiled for each CellKind and LoopMode, so the
 // gate step has no branch on either (a uniform branch on the cell there cost
-// about 4% of the loop).  The forward for training exists for the LSTM only.
+// about 4% of the loop).
 struct Variant { int bf16, mt, ksw, kw, nst, lds_bytes; persist_fn f[3][3]; };
 
 #define PV_CELL(ET, MT, KS, KW, NS, C)                                                       \
     {persistent_kernel<ET, MT, KS, KW, NS, C, LM_PLAIN>, persistent_kernel<ET, MT, KS, KW, NS, C, LM_STOP>, \
-     C == CELL_LSTM ? persistent_kernel<ET, MT, KS, KW, NS, CELL_LSTM, LM_SAVE> : nullptr}
+     persistent_kernel<ET, MT, KS, KW, NS, C, LM_SAVE>}
 #define PV(BF, ET, MT, KS, KW, NS)                                             \
     {BF, MT, KS, KW, NS, PLayout<MT, KW, NS>::BYTES,                            \
      {PV_CELL(ET, MT, KS, KW, NS, CELL_LSTM), PV_CELL(ET, MT, KS, KW, NS, CELL_GRU), \

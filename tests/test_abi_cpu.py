@@ -236,22 +236,30 @@ def test_check_backward_args():
     for s in sizes:
         p.append(at)
         at += (s + 255) // 256 * 256 + 256
-    chk = ld.lstm_dyn_check_backward_args
-    assert chk(B, D, H, T, ld.F32, *p) == ld.OK
+    chk = lambda *q: ld.lstm_dyn_check_backward_args(B, D, H, T, ld.F32, ld.CELL_LSTM, *q)
+    assert chk(*p) == ld.OK
     q = list(p)
     q[9] = 0                                      # d_seq is optional
-    assert chk(B, D, H, T, ld.F32, *q) == ld.OK
+    assert chk(*q) == ld.OK
     for i in list(range(9)) + list(range(10, 16)):
         q = list(p)
         q[i] = 0
-        assert chk(B, D, H, T, ld.F32, *q) == ld.ERR_INVALID, i
+        assert chk(*q) == ld.ERR_INVALID, i
     for i in range(10, 16):                       # an output on an input or on another output
         for j in range(16):
             if j == i:
                 continue
             q = list(p)
             q[i] = q[j]
-            assert chk(B, D, H, T, ld.F32, *q) == ld.ERR_INVALID, (i, j)
+            assert chk(*q) == ld.ERR_INVALID, (i, j)
     q = list(p)
     q[11] += 2                                    # misaligned dW
-    assert chk(B, D, H, T, ld.F32, *q) == ld.ERR_INVALID
+    assert chk(*q) == ld.ERR_INVALID
+    # GRU and RNN: smaller W, U, b; c0, d_out_c and dc0 may be NULL
+    for cell in (ld.CELL_GRU, ld.CELL_RNN):
+        q = list(p)
+        q[6] = q[8] = q[15] = 0
+        assert ld.lstm_dyn_check_backward_args(B, D, H, T, ld.F32, cell, *q) == ld.OK, cell
+        q[11] = q[2] + 4 * (D * H - 1)            # dW on W's last element (RNN W is [D][H])
+        assert ld.lstm_dyn_check_backward_args(B, D, H, T, ld.F32, cell, *q) == ld.ERR_INVALID, cell
+    assert ld.lstm_dyn_check_backward_args(B, D, H, T, ld.F32, 5, *p) == ld.ERR_INVALID
