@@ -20,7 +20,8 @@ Side legs on the same workload (not part of value): forward_seq (the forward
 that also writes the output sequence), forward_stop (termination computed
 from the state by a halting read-out), cells (the GRU and tanh RNN cells),
 train_step (the forward for training and the backward pass), per_step_path
-(the host-driven comparison loop) and tiny_f32 (the launch-bound small case).
+(the host-driven comparison loop), tiny_f32 (the launch-bound small case) and
+configs (every workload shape: the on-device loop against the per-step path).
 Each has a --no-* flag.
 """
 from __future__ import annotations
@@ -173,6 +174,8 @@ def main():
                     help="skip timing the loop with termination computed from the state")
     ap.add_argument("--no-train", action="store_true",
                     help="skip timing the forward for training and the backward pass")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the persistent vs per-step comparison over every workload shape")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain copy of known size (for scaling HBM counters)")
     args = ap.parse_args()
@@ -334,6 +337,38 @@ def main():
         tm.close()
         tps.close()
 
+    configs = None
+    if not args.no_configs:
+        # every workload shape: the forward with the loop on the device
+        # against the per-step path (one host launch pair per step), both
+        # timed back to back on the host clock between synchronisations
+        configs = {}
+        for name in workloads.ORDER:
+            cw = workloads.WORKLOADS[name]
+            _log(f"persistent vs per-step, {name}")
+            if name == args.workload:
+                cin, cdev, cout = inp, dev, out
+            else:
+                cin = workloads.workload_inputs(name)
+                cdev = to_device(cin, torch)
+                cout = (torch.empty((cw.B, cw.H), device="cuda"), torch.empty((cw.B, cw.H), device="cuda"))
+            cL = int(cin.lengths.sum())
+            cm = ld.LstmDyn(cw.B, cw.D, cw.H, cw.T, cw.dtype, "persistent")
+            t_p = time_whole(torch, cm, cdev, 50 if cw.H <= 512 else 10, 3, cout)
+            assert cm.query(ld.Q_LAST_STATUS) == ld.OK
+            cps = ld.LstmDyn(cw.B, cw.D, cw.H, cw.T, cw.dtype, "per_step")
+            t_s = time_whole(torch, cps, cdev, 10 if cw.H <= 512 else 2, 1, cout)
+            configs[name] = {"value": cL / t_p, "unit": "seq·steps/s", "dtype": cw.dtype,
+                             "sum_lengths": cL, "max_len": int(cin.lengths.max()),
+                             "persistent_ms": t_p * 1e3, "per_step_ms": t_s * 1e3,
+                             "speedup_of_persistent": t_s / t_p,
+                             "launches_persistent": cm.query(ld.Q_LAUNCHES_PER_FORWARD),
+                             "launches_per_step": cps.query(ld.Q_LAUNCHES_PER_FORWARD),
+                             "mfma_frac_forward": 8.0 * cw.H * (cw.D + cw.H) * cL / t_p / 1e12
+                             / PEAK_TFLOPS[cw.dtype]}
+            cm.close()
+            cps.close()
+
     dt = w.dtype
     flops_fwd = 8.0 * w.H * (w.D + w.H) * sumL
     flops_rec = 8.0 * w.H * w.H * sumL
@@ -377,6 +412,7 @@ def main():
         "train_step": train_leg,
         "cells": cell_legs,
         "tiny_f32": tiny,
+        "configs": configs,
     }
     if not args.no_cpu:
         _log("cpu baseline (oracle)")
