@@ -915,8 +915,8 @@ extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* le
     if (!d.bf16) {
         for (int t = max_len - 1; t >= 0; --t) {
             const int act = off[t + 1] - off[t];
-            LD_CHECK(launch_bwd_cell(d, t, act, tw->save_h, tw->save_c, d_seq, tw->dH, tw->dC,
-                                     h->ws, s));
+            LD_CHECK(launch_bwd_cell(d, t, off[t], act, tw->save_h, tw->save_c, d_seq, tw->dH,
+                                     tw->dC, h->ws, s));
             // dH[0:act] (+)= dz_t U^T (column-major: dH^T = U_il^T-as-stored^T dz_t^T)
             RB_CHECK(rocblas_sgemm(tw->rb, rocblas_operation_transpose, rocblas_operation_none, d.H,
                                    act, H4, &one, tw->u_il, H4, h->ws.gx + (size_t)off[t] * H4, H4,
@@ -933,8 +933,8 @@ extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* le
         h->launches_last += 2;
         for (int t = max_len - 1; t >= 0; --t) {
             const int act = off[t + 1] - off[t];
-            LD_CHECK(launch_bwd_cell16(d, t, act, tw->save_h, tw->save_c, d_seq, tw->dH, tw->dC,
-                                       tw->srow, tw->dzs16, h->ws, s));
+            LD_CHECK(launch_bwd_cell16(d, t, off[t], act, tw->save_h, tw->save_c, d_seq, tw->dH,
+                                       tw->dC, tw->srow, tw->dzs16, h->ws, s));
             RB_CHECK(rocblas_gemm_ex(tw->rb, rocblas_operation_transpose, rocblas_operation_none,
                                      d.H, act, H4, &alpha_u, tw->u16, rocblas_datatype_f16_r, H4,
                                      tw->dzs16, rocblas_datatype_f16_r, H4, &beta, tw->dH,

@@ -96,10 +96,10 @@ __device__ inline f32x4_t cell_backward(f32x4_t z, float hp, float cp, float dh,
 // over z, dC <- dc_prev, and dH <- dh_direct (the GEMM then adds dz U^T).
 template <int CELL>
 __global__ void __launch_bounds__(256)
-bwd_cell_kernel(float* gx, const float* __restrict__ save_h, const float* __restrict__ save_c,
-                const float* __restrict__ dseq, const int32_t* __restrict__ perm,
-                const int32_t* __restrict__ offsets, float* dH, float* dC, int t, int H, int T) {
-    const int off = offsets[t], act = offsets[t + 1] - off;
+bwd_cell_kernel(float* __restrict__ gx, const float* __restrict__ save_h,
+                const float* __restrict__ save_c, const float* __restrict__ dseq,
+                const int32_t* __restrict__ perm, float* __restrict__ dH,
+                float* __restrict__ dC, int t, int off, int act, int H, int T) {
     const long n = (long)act * H;
     for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += (long)gridDim.x * 256) {
         const int s = (int)(i / H), u = (int)(i - (long)s * H);
@@ -118,32 +118,58 @@ bwd_cell_kernel(float* gx, const float* __restrict__ save_h, const float* __rest
 // dz16 in fp16, scaled by a power of two that brings its largest magnitude
 // into [2^13, 2^14), for the product dz U^T; dH of a row holds its gradient
 // times srow (the scale of the dz it was last formed from; 1 at the start).
+// A thread takes up to VU units 256 apart and issues all their loads before
+// any store, so the row's reads are in flight together; for H <= 256 VU the
+// row's dz and dh stay in registers until the scale is known.
+constexpr int BWD_VU = 8;
+
 template <int CELL>
 __global__ void __launch_bounds__(256)
-bwd_cell16_kernel(float* gx, const float* __restrict__ save_h, const float* __restrict__ save_c,
-                  const float* __restrict__ dseq, const int32_t* __restrict__ perm,
-                  const int32_t* __restrict__ offsets, float* dH, float* dC, float* srow,
-                  _Float16* dz16, int t, int H, int T) {
+bwd_cell16_kernel(float* __restrict__ gx, const float* __restrict__ save_h,
+                  const float* __restrict__ save_c, const float* __restrict__ dseq,
+                  const int32_t* __restrict__ perm, float* __restrict__ dH,
+                  float* __restrict__ dC, float* __restrict__ srow, _Float16* __restrict__ dz16,
+                  int t, int off, int H, int T) {
     __shared__ unsigned red[4];
-    const int off = offsets[t];
-    const int s = blockIdx.x, tid = threadIdx.x;
-    if (s >= offsets[t + 1] - off) return;  // uniform over the workgroup
+    const int s = blockIdx.x, tid = threadIdx.x;  // one workgroup per row of the step
     const long r = off + s;
     const float inv = 1.0f / srow[s];
     const float* dseq_row = dseq ? dseq + ((long)perm[s] * T + t) * H : nullptr;
+    f32x4_t* const zrow = reinterpret_cast<f32x4_t*>(gx + r * 4 * H);
+    float* const dh_row = dH + (long)s * H;
+    float* const dc_row = dC + (long)s * H;
     unsigned m = 0;
-    for (int u = tid; u < H; u += 256) {
-        f32x4_t* zp = reinterpret_cast<f32x4_t*>(gx + r * 4 * H + 4 * u);
-        float dh = dH[(long)s * H + u] * inv;
-        if (dseq_row) dh += dseq_row[u];
-        float dcp, dhd;
-        const f32x4_t dz = cell_backward<CELL>(*zp, save_h[r * H + u], save_c[r * H + u], dh,
-                                               dC[(long)s * H + u], dcp, dhd);
-        *zp = dz;
-        dC[(long)s * H + u] = dcp;
-        dH[(long)s * H + u] = dhd;  // scaled below, once the row's scale is known
+    f32x4_t dz[BWD_VU];
+    float dhd[BWD_VU];
+    for (int u0 = 0; u0 < H; u0 += 256 * BWD_VU) {
+        f32x4_t z[BWD_VU];
+        float hp[BWD_VU], cp[BWD_VU], dh[BWD_VU], dc[BWD_VU];
 #pragma unroll
-        for (int g = 0; g < 4; ++g) m = max(m, __float_as_uint(fabsf(dz[g])) & 0x7fffffffu);
+        for (int j = 0; j < BWD_VU; ++j) {
+            const int u = u0 + tid + 256 * j;
+            if (u < H) {
+                z[j] = zrow[u];
+                hp[j] = save_h[r * H + u];
+                cp[j] = save_c[r * H + u];
+                dh[j] = dh_row[u] * inv;
+                dc[j] = dc_row[u];
+                if (dseq_row) dh[j] += dseq_row[u];
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < BWD_VU; ++j) {
+            const int u = u0 + tid + 256 * j;
+            if (u < H) {
+                float dcp;
+                dz[j] = cell_backward<CELL>(z[j], hp[j], cp[j], dh[j], dc[j], dcp, dhd[j]);
+                zrow[u] = dz[j];
+                dc_row[u] = dcp;
+                dh_row[u] = dhd[j];  // scaled below, once the row's scale is known
+#pragma unroll
+                for (int g = 0; g < 4; ++g)
+                    m = max(m, __float_as_uint(fabsf(dz[j][g])) & 0x7fffffffu);
+            }
+        }
     }
     for (int o = 32; o > 0; o >>= 1) m = max(m, (unsigned)__shfl_xor((int)m, o));
     if ((tid & 63) == 0) red[tid >> 6] = m;
@@ -156,11 +182,25 @@ bwd_cell16_kernel(float* gx, const float* __restrict__ save_h, const float* __re
         (void)frexpf(mf, &e);
         sc = ldexpf(1.0f, min(14 - e, 126));
     }
-    for (int u = tid; u < H; u += 256) {
-        const f32x4_t dz = *reinterpret_cast<const f32x4_t*>(gx + r * 4 * H + 4 * u);
+    typedef _Float16 h4_t __attribute__((ext_vector_type(4)));
+    h4_t* const d16 = reinterpret_cast<h4_t*>(dz16 + (long)s * 4 * H);
+    if (H <= 256 * BWD_VU) {  // the row is still in registers
 #pragma unroll
-        for (int g = 0; g < 4; ++g) dz16[(long)s * 4 * H + 4 * u + g] = (_Float16)(dz[g] * sc);
-        dH[(long)s * H + u] *= sc;
+        for (int j = 0; j < BWD_VU; ++j) {
+            const int u = tid + 256 * j;
+            if (u < H) {
+                d16[u] = h4_t{(_Float16)(dz[j][0] * sc), (_Float16)(dz[j][1] * sc),
+                              (_Float16)(dz[j][2] * sc), (_Float16)(dz[j][3] * sc)};
+                dh_row[u] = dhd[j] * sc;
+            }
+        }
+    } else {  // each thread reads back what it wrote
+        for (int u = tid; u < H; u += 256) {
+            const f32x4_t v = zrow[u];
+            d16[u] = h4_t{(_Float16)(v[0] * sc), (_Float16)(v[1] * sc), (_Float16)(v[2] * sc),
+                          (_Float16)(v[3] * sc)};
+            dh_row[u] *= sc;
+        }
     }
     if (tid == 0) srow[s] = sc;  // every thread read the old value before the barrier
 }
@@ -301,13 +341,14 @@ hipError_t launch_bwd_init(const Dims& d, const float* dh_out, const float* dc_o
     return hipGetLastError();
 }
 
-hipError_t launch_bwd_cell(const Dims& d, int t, int act, const float* save_h, const float* save_c,
-                           const float* dseq, float* dH, float* dC, const Workspace& ws,
-                           hipStream_t s) {
+hipError_t launch_bwd_cell(const Dims& d, int t, int off, int act, const float* save_h,
+                           const float* save_c, const float* dseq, float* dH, float* dC,
+                           const Workspace& ws, hipStream_t s) {
+    if (act < 1) return hipSuccess;
     auto k = d.cell == CELL_GRU ? bwd_cell_kernel<CELL_GRU>
              : d.cell == CELL_RNN ? bwd_cell_kernel<CELL_RNN> : bwd_cell_kernel<CELL_LSTM>;
     hipLaunchKernelGGL(k, dim3(grid_of((long)act * d.H)), dim3(256), 0, s, ws.gx, save_h, save_c,
-                       dseq, ws.perm, ws.offsets, dH, dC, t, d.H, d.T);
+                       dseq, ws.perm, dH, dC, t, off, act, d.H, d.T);
     return hipGetLastError();
 }
 
@@ -326,13 +367,14 @@ hipError_t launch_bwd_state_out(const Dims& d, const float* dH, const float* dC,
     return hipGetLastError();
 }
 
-hipError_t launch_bwd_cell16(const Dims& d, int t, int act, const float* save_h,
+hipError_t launch_bwd_cell16(const Dims& d, int t, int off, int act, const float* save_h,
                              const float* save_c, const float* dseq, float* dH, float* dC,
                              float* srow, _Float16* dz16, const Workspace& ws, hipStream_t s) {
     auto k = d.cell == CELL_GRU ? bwd_cell16_kernel<CELL_GRU>
              : d.cell == CELL_RNN ? bwd_cell16_kernel<CELL_RNN> : bwd_cell16_kernel<CELL_LSTM>;
-    hipLaunchKernelGGL(k, dim3(act), dim3(256), 0, s, ws.gx, save_h, save_c, dseq, ws.perm,
-                       ws.offsets, dH, dC, srow, dz16, t, d.H, d.T);
+    if (act < 1) return hipSuccess;
+    hipLaunchKernelGGL(k, dim3(act), dim3(256), 0, s, ws.gx, save_h, save_c, dseq, ws.perm, dH,
+                       dC, srow, dz16, t, off, d.H, d.T);
     return hipGetLastError();
 }
 

@@ -114,7 +114,10 @@ hipError_t launch_step_stop(const Dims& d, int t, const StopArgs& stop, const Wo
 hipError_t launch_bwd_weights(const Dims& d, const void* W, int rows, float* Wil, hipStream_t s);
 hipError_t launch_bwd_init(const Dims& d, const float* dh_out, const float* dc_out, float* dH,
                            float* dC, const Workspace& ws, hipStream_t s);
-hipError_t launch_bwd_cell(const Dims& d, int t, int act, const float* save_h, const float* save_c,
+// off, act: the step's first compact row and its number of rows (known to the
+// host from the forward's step offsets).
+hipError_t launch_bwd_cell(const Dims& d, int t, int off, int act, const float* save_h,
+                           const float* save_c,
                            const float* dseq, float* dH, float* dC, const Workspace& ws,
                            hipStream_t s);
 // GRU/RNN gradients, packed four-block (interleaved) layout -> the cell's own;
@@ -125,7 +128,7 @@ hipError_t launch_bwd_state_out(const Dims& d, const float* dH, const float* dC,
                                 float* dh0, float* dc0, const Workspace& ws, hipStream_t s);
 // bf16 data: the cell's backward with one workgroup per row, also writing the
 // row's dz in fp16 scaled by a power of two (srow) for dz U^T.
-hipError_t launch_bwd_cell16(const Dims& d, int t, int act, const float* save_h,
+hipError_t launch_bwd_cell16(const Dims& d, int t, int off, int act, const float* save_h,
                              const float* save_c, const float* dseq, float* dH, float* dC,
                              float* srow, _Float16* dz16, const Workspace& ws, hipStream_t s);
 hipError_t launch_bwd_ones(float* a, int n, hipStream_t s);
