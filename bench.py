@@ -254,6 +254,29 @@ def main():
                 "loop_algorithmic_tflops": c_rec / c_loop / 1e12,
                 "loop_frac": c_rec / c_loop / 1e12 / PEAK_TFLOPS[w.dtype],
                 "launches_per_forward": cm.query(ld.Q_LAUNCHES_PER_FORWARD)}
+            if not args.no_train:
+                # the cell's training step: forward for training, then the
+                # backward from a random upstream gradient of the final h
+                cdh = torch.from_numpy(np.random.default_rng(6).standard_normal((w.B, w.H))
+                                       .astype(np.float32)).cuda()
+                for _ in range(2):
+                    cm.forward_train(*cdev, out_h=out[0], out_c=out[1])
+                    cm.backward(*cdev, None, cdh)
+                torch.cuda.synchronize()
+                tf = tb = 0.0
+                for _ in range(3):
+                    t0 = time.perf_counter()
+                    cm.forward_train(*cdev, out_h=out[0], out_c=out[1])
+                    torch.cuda.synchronize()
+                    t1 = time.perf_counter()
+                    cm.backward(*cdev, None, cdh)
+                    torch.cuda.synchronize()
+                    tf += t1 - t0
+                    tb += time.perf_counter() - t1
+                cell_legs[cell]["train_step"] = {
+                    "forward_train_ms": tf / 3 * 1e3, "backward_ms": tb / 3 * 1e3,
+                    "step_ms": (tf + tb) / 3 * 1e3, "value": sumL / ((tf + tb) / 3),
+                    "unit": "seq·steps/s"}
             cm.close()
             del cdev, cin
 

@@ -137,3 +137,20 @@ def test_cell_backward_zero_upstream(cell):
                      np.zeros((9, 14, 48), np.float32))
     for k in KEYS:
         assert np.all(g[k] == 0), k
+
+
+@pytest.mark.parametrize("cell", CELLS)
+@pytest.mark.parametrize("mode", MODES)
+def test_cell_forward_train_outputs_equal_forward(mode, cell):
+    """The forward for training of a GRU or RNN handle gives the plain
+    forward's h bit for bit, and its output sequence (rebuilt from the kept
+    states) the forward_seq one."""
+    import torch
+    inp = workloads.random_cell_case(cell, 1603, 37, 40, 100, 17, dtype="bf16")
+    m = ld.LstmDyn(inp.B, inp.D, inp.H, inp.T, inp.dtype, mode, cell=inp.cell)
+    dev = gru_device(inp)
+    h1, _, s1 = m.forward_seq(*dev)
+    h2, _, s2 = m.forward_train(*dev, with_seq=True)
+    torch.cuda.synchronize()
+    assert m.query(ld.Q_LAST_STATUS) == ld.OK
+    assert torch.equal(h1, h2) and torch.equal(s1, s2)
