@@ -263,3 +263,19 @@ def test_check_backward_args():
         q[11] = q[2] + 4 * (D * H - 1)            # dW on W's last element (RNN W is [D][H])
         assert ld.lstm_dyn_check_backward_args(B, D, H, T, ld.F32, cell, *q) == ld.ERR_INVALID, cell
     assert ld.lstm_dyn_check_backward_args(B, D, H, T, ld.F32, 5, *p) == ld.ERR_INVALID
+
+
+@pytest.mark.parametrize("D,H,dt", [(40, 2048, ld.BF16), (40, 1024, ld.BF16), (24, 256, ld.F32),
+                                    (16, 700, ld.F32)])
+def test_plan_batch_limits(D, H, dt):
+    """512 rows is the most the persistent variants hold (8 owned row tiles per
+    wave); the per-step path takes up to the length preparation's 8192."""
+    p = ld.lstm_dyn_plan(512, D, H, 5, dt, ld.PERSISTENT, 256)
+    assert p["nstate"] == 8
+    with pytest.raises(ld.LstmDynError) as e:
+        ld.lstm_dyn_plan(513, D, H, 5, dt, ld.PERSISTENT, 256)
+    assert e.value.code == ld.ERR_UNSUPPORTED
+    ld.lstm_dyn_plan(8192, D, H, 5, dt, ld.PER_STEP, 256)
+    with pytest.raises(ld.LstmDynError) as e:
+        ld.lstm_dyn_plan(8193, D, H, 5, dt, ld.PER_STEP, 256)
+    assert e.value.code == ld.ERR_UNSUPPORTED

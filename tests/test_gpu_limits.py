@@ -1,0 +1,75 @@
+"""The largest batches the library takes, through the C ABI, against the fp64
+oracle: 512 rows (the most the register-resident state of the persistent
+variants holds: 8 owned row tiles per wave) on every persistent variant
+family, and 8192 rows (the most the length preparation takes) on the
+per-step path, which has no register-resident state.  Sampled rows are
+checked against the oracle run on those rows alone (rows are independent);
+every row of the persistent result against the per-step path's."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_1810_08061_amd as ld
+import workloads
+from tests.gpu_util import max_err, run, say
+
+pytestmark = pytest.mark.gpu
+
+TOL = {workloads.F32: 1e-5, workloads.BF16: 3e-3}
+
+
+def _sample(inp, n=10, seed=11):
+    L = inp.lengths
+    order = np.argsort(-L, kind="stable")
+    picks = {int(order[0]), int(order[-1]), int(order[len(order) // 2])}
+    picks |= set(int(v) for v in np.random.default_rng(seed).choice(len(L), size=n, replace=False))
+    return sorted(picks)
+
+
+@pytest.mark.parametrize("shape", [
+    (512, 40, 2048, 5, "bf16"),   # two gate tiles per workgroup, eight waves
+    (512, 40, 1024, 6, "bf16"),   # one gate tile, four waves
+    (512, 24, 256, 7, "f32"),
+    (512, 16, 700, 4, "f32"),     # fp32 with 64 K-steps per wave
+], ids=lambda s: "x".join(map(str, s)))
+def test_largest_persistent_batch(shape):
+    B, D, H, T, dt = shape
+    inp = workloads.random_case(4000 + H, B, D, H, T, dtype=dt)
+    say(f"case limit persistent {shape}")
+    h, c, m = run(inp, "persistent")
+    assert m.query(ld.Q_LAST_STATUS) == ld.OK
+    rows = _sample(inp)
+    ho, co = oracle.forward_inputs(inp, rows=rows)
+    eh, ec = max_err(h[rows], ho), max_err(c[rows], co)
+    say(f"  sampled rows: max|dh|={eh:.3g} max|dc|={ec:.3g}")
+    assert eh <= TOL[dt] and ec <= TOL[dt]
+    hs, cs, ms = run(inp, "per_step")
+    e2 = max(max_err(h, hs), max_err(c, cs))
+    say(f"  every row against the per-step path: {e2:.3g}")
+    assert e2 <= 2 * TOL[dt]
+    m.close()
+    ms.close()
+
+
+def test_one_row_more_needs_the_per_step_path():
+    with pytest.raises(ld.LstmDynError) as e:
+        ld.LstmDyn(513, 40, 1024, 6, "bf16", "persistent")
+    assert e.value.code == ld.ERR_UNSUPPORTED
+
+
+def test_largest_per_step_batch():
+    B, D, H, T = 8192, 8, 32, 3
+    inp = workloads.random_case(4100, B, D, H, T, dtype="f32")
+    say(f"case limit per_step {(B, D, H, T)}")
+    h, c, m = run(inp, "per_step")
+    assert m.query(ld.Q_LAST_STATUS) == ld.OK
+    rows = _sample(inp, n=30)
+    ho, co = oracle.forward_inputs(inp, rows=rows)
+    eh, ec = max_err(h[rows], ho), max_err(c[rows], co)
+    say(f"  sampled rows: max|dh|={eh:.3g} max|dc|={ec:.3g}")
+    assert eh <= TOL["f32"] and ec <= TOL["f32"]
+    # rows of length 0 keep their initial state exactly
+    z = np.flatnonzero(inp.lengths == 0)
+    assert z.size > 0
+    assert np.array_equal(h[z], inp.h0[z].astype(np.float64)) and np.array_equal(c[z], inp.c0[z].astype(np.float64))
+    m.close()
