@@ -37,6 +37,12 @@ struct TrainWs {
     unsigned* amax; // [5] largest magnitudes (float bits) of dz, x, h_prev, W, U
     int32_t* host_offsets;  // pinned [T + 8]: step offsets, the sum of lengths, then amax
     rocblas_handle rb;
+    // the reverse loop in one launch (bf16 data, persistent handles that fit)
+    int loop_groups;        // its workgroups, or 0: two launches per step
+    _Float16* dzx;          // [2][bpad][kp] each step's published dz
+    float* dzs;             // [2][bpad][nblk] their scales
+    unsigned* bar;          // [9 * 64] barrier counters
+    long long dzx_bytes, dzs_bytes;
 };
 
 using namespace ldyn;
@@ -71,6 +77,9 @@ struct lstm_dyn {
 namespace {
 
 constexpr int PREP_MAX_B = 8192;
+// Backward with bf16 data: steps with at most this many rows go to the
+// one-launch reverse loop, the others to two launches per step.
+constexpr int BWD_LOOP_ROWS = 16;
 constexpr double BARRIER_TIMEOUT_S = 5.0;
 
 long long align_up(long long v, long long a) { return (v + a - 1) / a * a; }
@@ -674,6 +683,14 @@ static int ensure_train(lstm_dyn* h) {
                     oh16 = take(h16 ? 2 * B * T * H : 0), ow16 = take(h16 ? 2 * D * 4 * H : 0),
                     ou16 = take(h16 ? 2 * H * 4 * H : 0), odzs = take(h16 ? 2 * B * 4 * H : 0),
                     osr = take(4 * B), osm = take(256);
+    tw->loop_groups =
+        h16 && h->mode == LSTM_DYN_PERSISTENT ? bwd_loop_fits(h->dims, h->num_cus) : 0;
+    int kp = 0, nblk = 0;
+    if (tw->loop_groups) bwd_loop_shape((int)H, &kp, &nblk);
+    tw->dzx_bytes = 2LL * 2 * bpad * kp;
+    tw->dzs_bytes = 4LL * 2 * bpad * nblk;
+    const long long odzx = take(tw->dzx_bytes), odzsc = take(tw->dzs_bytes),
+                    obar = take(tw->loop_groups ? 9 * 64 * 4 : 0);
     if (hipMalloc(&tw->block, (size_t)o) != hipSuccess) {
         (void)hipGetLastError();
         delete tw;
@@ -700,6 +717,9 @@ static int ensure_train(lstm_dyn* h) {
     tw->dzs16 = h16 ? reinterpret_cast<_Float16*>(base + odzs) : nullptr;
     tw->srow = reinterpret_cast<float*>(base + osr);
     tw->amax = reinterpret_cast<unsigned*>(base + osm);
+    tw->dzx = tw->loop_groups ? reinterpret_cast<_Float16*>(base + odzx) : nullptr;
+    tw->dzs = tw->loop_groups ? reinterpret_cast<float*>(base + odzsc) : nullptr;
+    tw->bar = tw->loop_groups ? reinterpret_cast<unsigned*>(base + obar) : nullptr;
     if (hipMemsetD32(reinterpret_cast<hipDeviceptr_t>(tw->ones), 0x3f800000, (size_t)(B * T)) != hipSuccess) {
         (void)hipFree(tw->block);
         delete tw;
@@ -929,9 +949,25 @@ extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* le
         // by its own power of two (kept in srow and divided out when dH is read)
         const float su = f16_scale(static_cast<unsigned>(off[d.T + 2])), alpha_u = 1.0f / su;
         LD_CHECK(launch_bwd_to_f16(tw->u_il, tw->u16, (long)d.H * H4, su, s));
+        h->launches_last++;
+        // The steps with at most BWD_LOOP_ROWS rows (the last ones, taken
+        // first) in one cooperative launch, which leaves dH complete and
+        // unscaled for the step before them; the others two launches each.
+        int t_end = max_len;
+        if (tw->loop_groups)
+            while (t_end > 0 && off[t_end] - off[t_end - 1] <= BWD_LOOP_ROWS) --t_end;
+        if (t_end < max_len) {
+            LD_CHECK(hipMemsetAsync(tw->dzx, 0, (size_t)tw->dzx_bytes, s));
+            LD_CHECK(hipMemsetAsync(tw->dzs, 0, (size_t)tw->dzs_bytes, s));
+            LD_CHECK(hipMemsetAsync(tw->bar, 0, 9 * 64 * sizeof(unsigned), s));
+            LD_CHECK(launch_bwd_loop(d, tw->u16, alpha_u, tw->save_h, tw->save_c, d_seq, tw->dH,
+                                     tw->dC, tw->dzx, tw->dzs, tw->bar, h->timeout_ticks, t_end,
+                                     h->ws, s));
+            h->launches_last++;
+        }
         LD_CHECK(launch_bwd_ones(tw->srow, d.B, s));
-        h->launches_last += 2;
-        for (int t = max_len - 1; t >= 0; --t) {
+        h->launches_last++;
+        for (int t = t_end - 1; t >= 0; --t) {
             const int act = off[t + 1] - off[t];
             LD_CHECK(launch_bwd_cell16(d, t, off[t], act, tw->save_h, tw->save_c, d_seq, tw->dH,
                                        tw->dC, tw->srow, tw->dzs16, h->ws, s));

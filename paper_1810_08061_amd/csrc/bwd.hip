@@ -420,4 +420,355 @@ hipError_t launch_bwd_dx(const Dims& d, const float* dxc, long rows, const int32
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// The reverse loop in one cooperative launch (bf16 data, persistent handles).
+//
+// Workgroup g owns the 16 units [16 g, 16 g + 16) and keeps, as MFMA
+// A-fragments in registers, the rows of U (gate-interleaved columns, fp16,
+// times su) of those units: 4H columns split over eight waves.  Step t
+// (from the last down to 0, then once more for dh0):
+//   * product: dh of the rows that ran step t+1 and of the owned units,
+//     sum_j dz_{t+1}[s][j] U[u][j] over all 4H columns, from the step's dz
+//     that every workgroup published (fp16, each 64-column block of a row --
+//     one workgroup's units -- scaled by its own power of two, undone after
+//     the block's two MFMAs); partial sums of the waves meet in LDS;
+//   * cell: the owned (row, unit) pairs of the rows that run step t take dh
+//     (plus the carried term and the output sequence's gradient), their z
+//     and saved state, give dz (kept in fp32 for the weight gradients and
+//     published in fp16 under the block's scale), dc and the carried term;
+//   * a grid barrier; the published dz alternates between two buffers.
+// The carried dh and dc live in dH, dC ([B][H], slot order): in, the upstream
+// gradients of the final state; out, dh0 and dc0.
+struct BwdLoopParams {
+    const _Float16* u16;     // [H][4H] U, gate-interleaved columns, times su
+    float* gx;               // [rows][4H] z in, dz (fp32) out
+    const float* save_h;     // [rows][H] the state each step started from
+    const float* save_c;
+    const float* dseq;       // [B][T][H] gradient of the output sequence, or null
+    const int32_t* perm;     // [B] slot -> batch row
+    const int32_t* offsets;  // [T + 1] first compact row of each step
+    Meta* meta;              // max_len in, timeout status out
+    float* dH;               // [B][H] carried dh: in d_out_h, out dh0 (slot order)
+    float* dC;               // [B][H] carried dc: in d_out_c, out dc0
+    _Float16* dzx;           // [2][bpad][kp] published dz (fp16, scaled per row and block)
+    float* dzs;              // [2][bpad][nblk] the scales (powers of two)
+    unsigned* bar;           // [9 * 64] barrier counters, zero at the launch
+    unsigned long long timeout_ticks;
+    float alpha_u;           // 1 / su
+    int B, H, T, bpad, groups, kp, nblk;
+    int t_end;               // steps max_len - 1 down to t_end; then dh of step t_end - 1
+};
+
+constexpr int BL_WAVES = 8;
+constexpr int BL_NTC = 16;  // row tiles per chunk
+constexpr int BL_LDS_BYTES = BL_WAVES * BL_NTC * 64 * 16;
+constexpr int BL_SC1 = 16;  // buffer-instruction cache policy: device scope
+
+typedef unsigned bl_u32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned bl_u32x4 __attribute__((ext_vector_type(4)));
+
+// Grid barrier k: every workgroup's stores drained, then a counter per
+// group of workgroups (blockIdx mod 8) and one over the groups.  Bounded:
+// false past the deadline (the timeout status is set).
+__device__ inline bool bl_barrier(const BwdLoopParams& p, int k, int* lds_ok) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int ok = 1;
+        if (p.groups > 1) {
+            const int x = blockIdx.x & 7;
+            const unsigned members = (unsigned)((p.groups - x + 7) >> 3);
+            const unsigned old = __hip_atomic_fetch_add(p.bar + 64 * (1 + x), 1u, __ATOMIC_RELAXED,
+                                                        __HIP_MEMORY_SCOPE_AGENT);
+            if (old + 1u == (unsigned)(k + 1) * members)
+                __hip_atomic_fetch_add(p.bar, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            const unsigned want = (unsigned)(k + 1) * (unsigned)(p.groups < 8 ? p.groups : 8);
+            const unsigned long long t0 = wall_clock64();
+            while (__hip_atomic_load(p.bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < want) {
+                if (wall_clock64() - t0 > p.timeout_ticks) {
+                    ok = 0;
+                    __hip_atomic_fetch_or(&p.meta->status, STATUS_TIMEOUT, __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT);
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
+            }
+        }
+        *lds_ok = ok;
+    }
+    __syncthreads();
+    return *lds_ok != 0;
+}
+
+template <int KSW, int CELL>
+__global__ void __launch_bounds__(BL_WAVES * 64, 1)
+bwd_loop_kernel(BwdLoopParams p) {
+    // K-steps per load group: up to 8 loaded one group ahead; with 32 K-steps
+    // per wave (the U fragments take half the registers) two groups of 16,
+    // each loaded whole before its MFMAs (two round trips per row tile)
+    constexpr bool SINGLE = KSW >= 32;
+    constexpr int G = KSW < 8 ? KSW : SINGLE ? 16 : 8;
+    constexpr int NGR = KSW / G;          // load groups per row tile
+    static_assert(KSW % 2 == 0 && G % 2 == 0, "a scale block spans two K-steps of one wave");
+    extern __shared__ __attribute__((aligned(16))) float lds[];
+    __shared__ int lds_ok;
+    const int tid = threadIdx.x, l = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = blockIdx.x;
+    const int H = p.H, H4 = 4 * H, KP = p.kp, NB = p.nblk, bpad = p.bpad;
+    const __amdgpu_buffer_rsrc_t Ru = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<_Float16*>(p.u16), (short)0, (int)((size_t)H * H4 * 2), 0x00020000);
+    const __amdgpu_buffer_rsrc_t Rz = __builtin_amdgcn_make_buffer_rsrc(
+        p.dzx, (short)0, (int)((size_t)2 * bpad * KP * 2), 0x00020000);
+    const __amdgpu_buffer_rsrc_t Rs = __builtin_amdgcn_make_buffer_rsrc(
+        p.dzs, (short)0, (int)((size_t)2 * bpad * NB * 4), 0x00020000);
+    constexpr unsigned OOB = 0x80000000u;  // past every buffer: loads give zero
+
+    // U rows of the owned units: lane l holds unit 16 g + l % 16, columns
+    // 32 (w KSW + ks) + 8 (l / 16) .. + 7 (zero past H units or 4H columns)
+    f16x8_t a[KSW];
+    {
+        const int u = 16 * g + (l & 15);
+#pragma unroll
+        for (int ks = 0; ks < KSW; ++ks) {
+            const int col = 32 * (w * KSW + ks) + 8 * (l >> 4);
+            const bool in = u < H && col < H4;
+            a[ks] = __builtin_bit_cast(f16x8_t, __builtin_amdgcn_raw_buffer_load_b128(
+                                                    Ru, in ? (unsigned)((u * H4 + col) * 2) : OOB, 0, 0));
+        }
+    }
+    const int max_len = p.meta->max_len;
+    auto act_of = [&](int t) { return p.offsets[t + 1] - p.offsets[t]; };
+
+    const int t_end = p.t_end;
+    int k = 0;
+    for (int t = max_len - 1; t >= t_end - 1; --t, ++k) {
+        const bool last = t < t_end;  // only the product: dh entering step t_end
+        const int actp = t + 1 < max_len ? act_of(t + 1) : 0;  // rows with dz_{t+1}
+        const int actc = last ? 0 : act_of(t);                // rows that run step t
+        const int rows = last ? actp : actc;
+        const int nt = (rows + 15) >> 4;
+        const unsigned pin = (unsigned)((t + 1) & 1), pout = (unsigned)((t + 2) & 1);
+        for (int ntc0 = 0; ntc0 < nt; ntc0 += BL_NTC) {
+            const int nchunk = min(BL_NTC, nt - ntc0);
+            // ---- product: partial dh of this wave's K range, row tile by row tile,
+            // its K-steps loaded in groups of G one group ahead (the group index
+            // is a constant after unrolling, so the U fragments stay in registers)
+            {
+                auto load = [&](f16x8_t* b, float* inv, int j, int q) {
+                    const int s = (ntc0 + j) * 16 + (l & 15);
+                    const bool live = s < actp;
+                    const unsigned row = (unsigned)((int)pin * bpad + s);
+#pragma unroll
+                    for (int i = 0; i < G; ++i) {
+                        const int col = 32 * (w * KSW + q * G + i) + 8 * (l >> 4);
+                        b[i] = __builtin_bit_cast(f16x8_t, __builtin_amdgcn_raw_buffer_load_b128(
+                                                               Rz, live ? (row * KP + col) * 2u : OOB, 0, BL_SC1));
+                    }
+#pragma unroll
+                    for (int i = 0; i < G / 2; ++i) {
+                        const int blk = (w * KSW + q * G) / 2 + i;
+                        const float sc = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                            Rs, live ? (row * NB + blk) * 4u : OOB, 0, BL_SC1));
+                        inv[i] = sc > 0.0f ? 1.0f / sc : 0.0f;
+                    }
+                };
+                f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+                auto compute = [&](const f16x8_t* b, const float* inv, int j, int q) {
+                    if (q == 0) acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int i = 0; i < G / 2; ++i) {
+                        f32x4_t tmp = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                            a[q * G + 2 * i], b[2 * i], f32x4_t{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+                        tmp = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[q * G + 2 * i + 1], b[2 * i + 1],
+                                                                     tmp, 0, 0, 0);
+                        acc += tmp * inv[i];
+                    }
+                    if (q == NGR - 1)
+                        *reinterpret_cast<f32x4_t*>(lds + ((w * BL_NTC + j) * 64 + l) * 4) = acc;
+                };
+                if constexpr (SINGLE) {
+                    f16x8_t b0[G];
+                    float i0[G / 2];
+                    for (int j = 0; j < nchunk; ++j) {
+#pragma unroll
+                        for (int q = 0; q < NGR; ++q) {
+                            load(b0, i0, j, q);
+                            compute(b0, i0, j, q);
+                        }
+                    }
+                } else {
+                f16x8_t b0[G], b1[G];
+                float i0[G / 2], i1[G / 2];
+                load(b0, i0, 0, 0);
+                if constexpr (NGR == 1) {
+                    for (int j = 0; j < nchunk; j += 2) {
+                        if (j + 1 < nchunk) load(b1, i1, j + 1, 0);
+                        compute(b0, i0, j, 0);
+                        if (j + 2 < nchunk) load(b0, i0, j + 2, 0);
+                        if (j + 1 < nchunk) compute(b1, i1, j + 1, 0);
+                    }
+                } else {
+                    static_assert(NGR % 2 == 0, "groups alternate between the two buffers");
+                    for (int j = 0; j < nchunk; ++j) {
+#pragma unroll
+                        for (int q = 0; q < NGR; q += 2) {
+                            load(b1, i1, j, q + 1);
+                            compute(b0, i0, j, q);
+                            if (q + 2 < NGR) load(b0, i0, j, q + 2);
+                            else if (j + 1 < nchunk) load(b0, i0, j + 1, 0);
+                            compute(b1, i1, j, q + 1);
+                        }
+                    }
+                }
+                }
+            }
+            __syncthreads();
+            // ---- cell: the owned pairs of the chunk's rows; the 16 lanes of a
+            // row are its 16 units
+            {
+                const int ul = tid & 15, u = 16 * g + ul;
+                const bool uin = u < H;
+                const int rend = min((ntc0 + nchunk) * 16, rows);
+                for (int s = ntc0 * 16 + (tid >> 4); s < rend; s += BL_WAVES * 4) {
+                    float dh = 0.0f;
+                    if (s < actp) {
+                        const int j = (s >> 4) - ntc0, ln = 16 * (ul >> 2) + (s & 15), i = ul & 3;
+                        float sum = 0.0f;
+#pragma unroll
+                        for (int ww = 0; ww < BL_WAVES; ++ww) sum += lds[((ww * BL_NTC + j) * 64 + ln) * 4 + i];
+                        dh = sum * p.alpha_u;
+                    }
+                    const size_t su = (size_t)s * H + u;
+                    if (uin) dh += p.dH[su];
+                    if (last) {  // dh entering step t_end (dh0 when t_end is 0)
+                        if (uin) p.dH[su] = dh;
+                        continue;
+                    }
+                    f32x4_t dz = f32x4_t{0.f, 0.f, 0.f, 0.f};
+                    if (uin) {
+                        if (p.dseq) dh += p.dseq[((size_t)p.perm[s] * p.T + t) * H + u];
+                        const size_t r = (size_t)p.offsets[t] + s;
+                        f32x4_t* zp = reinterpret_cast<f32x4_t*>(p.gx + r * H4 + 4 * u);
+                        float dcp, dhd;
+                        dz = cell_backward<CELL>(*zp, p.save_h[r * H + u], p.save_c[r * H + u], dh,
+                                                 p.dC[su], dcp, dhd);
+                        *zp = dz;
+                        p.dC[su] = dcp;
+                        p.dH[su] = dhd;
+                    }
+                    // the block's scale: its largest magnitude into [2^13, 2^14)
+                    unsigned m = 0;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) m = max(m, __float_as_uint(fabsf(dz[e])) & 0x7fffffffu);
+                    for (int o = 8; o > 0; o >>= 1) m = max(m, (unsigned)__shfl_xor((int)m, o));
+                    const float mf = __uint_as_float(m);
+                    float sc = 1.0f;
+                    if (mf > 0.0f && mf < 3.0e38f) {
+                        int e;
+                        (void)frexpf(mf, &e);
+                        sc = ldexpf(1.0f, min(14 - e, 126));
+                    }
+                    typedef _Float16 h4_t __attribute__((ext_vector_type(4)));
+                    const h4_t hv = h4_t{(_Float16)(dz[0] * sc), (_Float16)(dz[1] * sc),
+                                         (_Float16)(dz[2] * sc), (_Float16)(dz[3] * sc)};
+                    const unsigned row = pout * (unsigned)bpad + (unsigned)s;
+                    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(bl_u32x2, hv), Rz,
+                                                          (row * KP + 64 * g + 4 * ul) * 2u, 0, BL_SC1);
+                    if (ul == 0)
+                        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(sc), Rs, (row * NB + g) * 4u, 0,
+                                                              BL_SC1);
+                }
+            }
+            __syncthreads();  // the partial sums are read before the next chunk writes them
+        }
+        if (!last && !bl_barrier(p, k, &lds_ok)) return;
+    }
+}
+
+// 2 K-steps per wave at the least (a scale block is two K-steps of one wave),
+// 32 at the most (H = 2048); H even so 8-column groups do not straddle rows.
+int bwd_loop_ksw(int H) {
+    if (H < 65 || H > 2048 || (H & 1)) return 0;
+    const int ks = (H + 7) / 8;  // K-steps of 32 over 4H columns
+    int ksw = 2;
+    while (ksw * BL_WAVES < ks) ksw *= 2;
+    return ksw;
+}
+
+typedef void (*bwd_loop_fn)(BwdLoopParams);
+
+static bwd_loop_fn bwd_loop_pick(int ksw, int cell) {
+#define BL_CELLS(K)                                                                         \
+    if (ksw == K)                                                                           \
+        return cell == CELL_GRU ? bwd_loop_kernel<K, CELL_GRU>                              \
+               : cell == CELL_RNN ? bwd_loop_kernel<K, CELL_RNN> : bwd_loop_kernel<K, CELL_LSTM>;
+    BL_CELLS(2) BL_CELLS(4) BL_CELLS(8) BL_CELLS(16) BL_CELLS(32)
+#undef BL_CELLS
+    return nullptr;
+}
+
+// Sizes of the exchange: columns per published row and scale blocks per row.
+void bwd_loop_shape(int H, int* kp, int* nblk) {
+    const int ksw = bwd_loop_ksw(H);
+    *kp = 32 * BL_WAVES * ksw;
+    *nblk = *kp / 64;
+}
+
+// Workgroups (one per CU, all resident) the loop can run with, or 0.
+int bwd_loop_fits(const Dims& d, int num_cus) {
+    const int ksw = bwd_loop_ksw(d.H);
+    if (!ksw || !d.bf16 || d.bpad > 512) return 0;
+    const int groups = (d.H + 15) / 16;
+    if (groups > num_cus) return 0;
+    bwd_loop_fn f = bwd_loop_pick(ksw, d.cell);
+    if (!f) return 0;
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(f),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, BL_LDS_BYTES) != hipSuccess)
+        return 0;
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, reinterpret_cast<const void*>(f), BL_WAVES * 64,
+                                                     BL_LDS_BYTES) != hipSuccess || n < 1)
+        return 0;
+    return groups;
+}
+
+hipError_t launch_bwd_loop(const Dims& d, const _Float16* u16, float alpha_u, const float* save_h,
+                           const float* save_c, const float* dseq, float* dH, float* dC,
+                           _Float16* dzx, float* dzs, unsigned* bar, unsigned long long timeout_ticks,
+                           int t_end, const Workspace& ws, hipStream_t s) {
+    const int ksw = bwd_loop_ksw(d.H);
+    bwd_loop_fn f = bwd_loop_pick(ksw, d.cell);
+    if (!f) return hipErrorInvalidValue;
+    int kp, nblk;
+    bwd_loop_shape(d.H, &kp, &nblk);
+    BwdLoopParams p{};
+    p.u16 = u16;
+    p.gx = ws.gx;
+    p.save_h = save_h;
+    p.save_c = save_c;
+    p.dseq = dseq;
+    p.perm = ws.perm;
+    p.offsets = ws.offsets;
+    p.meta = ws.meta;
+    p.dH = dH;
+    p.dC = dC;
+    p.dzx = dzx;
+    p.dzs = dzs;
+    p.bar = bar;
+    p.timeout_ticks = timeout_ticks;
+    p.alpha_u = alpha_u;
+    p.B = d.B;
+    p.H = d.H;
+    p.T = d.T;
+    p.bpad = d.bpad;
+    p.groups = (d.H + 15) / 16;
+    p.kp = kp;
+    p.nblk = nblk;
+    p.t_end = t_end;
+    void* args[] = {&p};
+    return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(f), dim3(p.groups),
+                                      dim3(BL_WAVES * 64), args, (unsigned)BL_LDS_BYTES, s);
+}
+
 }  // namespace ldyn

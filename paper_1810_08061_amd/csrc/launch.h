@@ -132,6 +132,20 @@ hipError_t launch_bwd_cell16(const Dims& d, int t, int off, int act, const float
                              const float* save_c, const float* dseq, float* dH, float* dC,
                              float* srow, _Float16* dz16, const Workspace& ws, hipStream_t s);
 hipError_t launch_bwd_ones(float* a, int n, hipStream_t s);
+// bf16 data: the whole reverse loop in one cooperative launch (one workgroup
+// of 16 units per CU, U rows resident, each step's dz published in fp16 with
+// a power-of-two scale per row and 64-column block, one grid barrier per
+// step).  bwd_loop_fits: its workgroup count, or 0 where it does not apply
+// (H odd, H <= 64 or H > 2048, more than 512 rows, not all resident).
+// dzx [2][bpad][kp] fp16, dzs [2][bpad][nblk] and bar [9 * 64] must be zero
+// at the launch; dH, dC hold the upstream gradients (slot order) and receive
+// dh0, dc0.
+int bwd_loop_fits(const Dims& d, int num_cus);
+void bwd_loop_shape(int H, int* kp, int* nblk);
+hipError_t launch_bwd_loop(const Dims& d, const _Float16* u16, float alpha_u, const float* save_h,
+                           const float* save_c, const float* dseq, float* dH, float* dC,
+                           _Float16* dzx, float* dzs, unsigned* bar, unsigned long long timeout_ticks,
+                           int t_end, const Workspace& ws, hipStream_t s);
 hipError_t launch_bwd_gather_x(const Dims& d, const void* x, long rows, float* xc,
                                const Workspace& ws, hipStream_t s);
 // fp16 operands of the backward's GEMMs: the largest magnitude (as float bits,

@@ -173,3 +173,23 @@ def test_backward_exact_facts(mode):
     torch.cuda.synchronize()
     with pytest.raises(ld.LstmDynError):            # a plain forward keeps nothing
         m.backward(*dev, zt, zt)
+
+
+@pytest.mark.parametrize("seq", [True, False], ids=["dseq", "final-state"])
+def test_backward_one_launch_reverse_loop(seq):
+    """bf16 data, at most 16 rows in every step, H even and above 64: the
+    whole reverse loop is one cooperative launch (dh0 from the launch
+    itself); against the oracle, and against the per-step path's launch count."""
+    B, D, H, T = 9, 20, 96, 40
+    inp = workloads.random_case(1201, B, D, H, T, dtype="bf16", lo=20)
+    dh, dc, ds = upstream(2201, B, H, T, seq)
+    say(f"case bwd one-launch loop seq={seq} lengths={inp.lengths.tolist()}")
+    g, _, m = run_train(inp, "persistent", dh, dc, ds)
+    launches = m.query(ld.Q_LAUNCHES_PER_FORWARD)
+    go = oracle_grads(inp, dh.astype(np.float64), dc.astype(np.float64),
+                      ds.astype(np.float64) if ds is not None else None)
+    compare(g, go, GRAD_TOL["bf16"])
+    _, _, mp = run_train(inp, "per_step", dh, dc, ds)
+    per_step = mp.query(ld.Q_LAUNCHES_PER_FORWARD)
+    say(f"  backward launches: {launches} (per-step path {per_step})")
+    assert launches < 30 <= 2 * int(inp.lengths.max()) <= per_step

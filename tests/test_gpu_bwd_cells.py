@@ -154,3 +154,16 @@ def test_cell_forward_train_outputs_equal_forward(mode, cell):
     torch.cuda.synchronize()
     assert m.query(ld.Q_LAST_STATUS) == ld.OK
     assert torch.equal(h1, h2) and torch.equal(s1, s2)
+
+
+@pytest.mark.parametrize("cell", CELLS)
+def test_cell_backward_one_launch_reverse_loop(cell):
+    """The GRU and RNN backward with every step in the one-launch reverse loop
+    (bf16 data, at most 16 rows, H even and above 64) against the oracle."""
+    B, D, H, T = 9, 20, 96, 40
+    inp = workloads.random_cell_case(cell, 1604, B, D, H, T, dtype="bf16", lo=20)
+    dh, ds = upstream(2604, B, H, T)
+    say(f"case bwd {cell} one-launch loop lengths={inp.lengths.tolist()}")
+    g, m = run_train(inp, "persistent", dh, ds)
+    assert m.query(ld.Q_LAUNCHES_PER_FORWARD) < 30
+    compare(g, oracle_grads(inp, dh, ds), GRAD_TOL["bf16"], keys=KEYS)
