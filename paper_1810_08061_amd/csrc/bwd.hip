@@ -423,22 +423,25 @@ hipError_t launch_bwd_dx(const Dims& d, const float* dxc, long rows, const int32
 // ---------------------------------------------------------------------------
 // The reverse loop in one cooperative launch (bf16 data, persistent handles).
 //
-// Workgroup g owns the 16 units [16 g, 16 g + 16) and keeps, as MFMA
-// A-fragments in registers, the rows of U (gate-interleaved columns, fp16,
-// times su) of those units: 4H columns split over eight waves.  Step t
-// (from the last down to 0, then once more for dh0):
+// Workgroup g owns the 8 units [8 g, 8 g + 8) and keeps in LDS the rows of U
+// of those units (gate-interleaved columns, fp16, times su) as MFMA
+// A-fragments of 32 columns each: 8 x 4H values, 128 KB at H = 2048, which
+// leaves the registers free for a whole row tile of the exchanged dz.  Step t
+// (from the last down to t_end, then once more for dh entering t_end - 1):
 //   * product: dh of the rows that ran step t+1 and of the owned units,
 //     sum_j dz_{t+1}[s][j] U[u][j] over all 4H columns, from the step's dz
-//     that every workgroup published (fp16, each 64-column block of a row --
-//     one workgroup's units -- scaled by its own power of two, undone after
-//     the block's two MFMAs); partial sums of the waves meet in LDS;
+//     that every workgroup published (fp16; each row's 32 columns from one
+//     workgroup scaled by that workgroup's power of two, undone after the
+//     MFMA of those columns); the waves split the columns and their
+//     partial sums meet in LDS;
 //   * cell: the owned (row, unit) pairs of the rows that run step t take dh
 //     (plus the carried term and the output sequence's gradient), their z
 //     and saved state, give dz (kept in fp32 for the weight gradients and
 //     published in fp16 under the block's scale), dc and the carried term;
 //   * a grid barrier; the published dz alternates between two buffers.
 // The carried dh and dc live in dH, dC ([B][H], slot order): in, the upstream
-// gradients of the final state; out, dh0 and dc0.
+// gradients of the final state (or of the state entering the step after
+// t_end - 1 ... max_len - 1); out, dh entering step t_end - 1 and dc0 ...
 struct BwdLoopParams {
     const _Float16* u16;     // [H][4H] U, gate-interleaved columns, times su
     float* gx;               // [rows][4H] z in, dz (fp32) out
@@ -460,8 +463,7 @@ struct BwdLoopParams {
 };
 
 constexpr int BL_WAVES = 8;
-constexpr int BL_NTC = 16;  // row tiles per chunk
-constexpr int BL_LDS_BYTES = BL_WAVES * BL_NTC * 64 * 16;
+constexpr int BL_NTC = 4;  // row tiles per chunk
 constexpr int BL_SC1 = 16;  // buffer-instruction cache policy: device scope
 
 typedef unsigned bl_u32x2 __attribute__((ext_vector_type(2)));
@@ -503,19 +505,17 @@ __device__ inline bool bl_barrier(const BwdLoopParams& p, int k, int* lds_ok) {
 template <int KSW, int CELL>
 __global__ void __launch_bounds__(BL_WAVES * 64, 1)
 bwd_loop_kernel(BwdLoopParams p) {
-    // K-steps per load group: up to 8 loaded one group ahead; with 32 K-steps
-    // per wave (the U fragments take half the registers) two groups of 16,
-    // each loaded whole before its MFMAs (two round trips per row tile)
-    constexpr bool SINGLE = KSW >= 32;
-    constexpr int G = KSW < 8 ? KSW : SINGLE ? 16 : 8;
-    constexpr int NGR = KSW / G;          // load groups per row tile
-    static_assert(KSW % 2 == 0 && G % 2 == 0, "a scale block spans two K-steps of one wave");
     extern __shared__ __attribute__((aligned(16))) float lds[];
     __shared__ int lds_ok;
     const int tid = threadIdx.x, l = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = blockIdx.x;
     const int H = p.H, H4 = 4 * H, KP = p.kp, NB = p.nblk, bpad = p.bpad;
+    constexpr int KSA = BL_WAVES * KSW;  // K-steps of 32 columns over the padded 4H
+    // LDS: U fragments [KSA][32 lanes][8 halves], then the partial sums
+    // [BL_WAVES][BL_NTC][32 lanes][4]
+    _Float16* const ufr = reinterpret_cast<_Float16*>(lds);
+    float* const part = lds + KSA * 32 * 8 / 2;
     const __amdgpu_buffer_rsrc_t Ru = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<_Float16*>(p.u16), (short)0, (int)((size_t)H * H4 * 2), 0x00020000);
     const __amdgpu_buffer_rsrc_t Rz = __builtin_amdgcn_make_buffer_rsrc(
@@ -524,26 +524,28 @@ bwd_loop_kernel(BwdLoopParams p) {
         p.dzs, (short)0, (int)((size_t)2 * bpad * NB * 4), 0x00020000);
     constexpr unsigned OOB = 0x80000000u;  // past every buffer: loads give zero
 
-    // U rows of the owned units: lane l holds unit 16 g + l % 16, columns
-    // 32 (w KSW + ks) + 8 (l / 16) .. + 7 (zero past H units or 4H columns)
-    f16x8_t a[KSW];
-    {
-        const int u = 16 * g + (l & 15);
-#pragma unroll
-        for (int ks = 0; ks < KSW; ++ks) {
-            const int col = 32 * (w * KSW + ks) + 8 * (l >> 4);
-            const bool in = u < H && col < H4;
-            a[ks] = __builtin_bit_cast(f16x8_t, __builtin_amdgcn_raw_buffer_load_b128(
-                                                    Ru, in ? (unsigned)((u * H4 + col) * 2) : OOB, 0, 0));
-        }
+    // Fragment slot q (0..31) of K-step kg: unit 8 g + q % 8, columns
+    // 32 kg + 8 (q / 8) .. + 7; lane l of an A-fragment takes slot
+    // (l / 16) * 8 + l % 16 when l % 16 < 8 (units 8..15 of the 16-row tile
+    // are zero).
+    for (int e = tid; e < KSA * 32; e += BL_WAVES * 64) {
+        const int kg = e >> 5, q = e & 31;
+        const int u = 8 * g + (q & 7), col = 32 * kg + 8 * (q >> 3);
+        const bool in = u < H && col < H4;
+        const bl_u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(
+            Ru, in ? (unsigned)((u * H4 + col) * 2) : OOB, 0, 0);
+        *reinterpret_cast<bl_u32x4*>(ufr + (size_t)e * 8) = v;
     }
+    __syncthreads();
+    const bool alane = (l & 15) < 8;
+    const int aslot = (l >> 4) * 8 + (l & 15);
+
     const int max_len = p.meta->max_len;
     auto act_of = [&](int t) { return p.offsets[t + 1] - p.offsets[t]; };
-
     const int t_end = p.t_end;
     int k = 0;
     for (int t = max_len - 1; t >= t_end - 1; --t, ++k) {
-        const bool last = t < t_end;  // only the product: dh entering step t_end
+        const bool last = t < t_end;  // only the product: dh entering step t_end - 1
         const int actp = t + 1 < max_len ? act_of(t + 1) : 0;  // rows with dz_{t+1}
         const int actc = last ? 0 : act_of(t);                // rows that run step t
         const int rows = last ? actp : actc;
@@ -551,97 +553,70 @@ bwd_loop_kernel(BwdLoopParams p) {
         const unsigned pin = (unsigned)((t + 1) & 1), pout = (unsigned)((t + 2) & 1);
         for (int ntc0 = 0; ntc0 < nt; ntc0 += BL_NTC) {
             const int nchunk = min(BL_NTC, nt - ntc0);
-            // ---- product: partial dh of this wave's K range, row tile by row tile,
-            // its K-steps loaded in groups of G one group ahead (the group index
-            // is a constant after unrolling, so the U fragments stay in registers)
-            {
-                auto load = [&](f16x8_t* b, float* inv, int j, int q) {
-                    const int s = (ntc0 + j) * 16 + (l & 15);
-                    const bool live = s < actp;
-                    const unsigned row = (unsigned)((int)pin * bpad + s);
+            // ---- product: this wave's KSW K-steps of each row tile, the
+            // tile's dz fragments and scales all loaded before its MFMAs
+            for (int j = 0; j < nchunk; ++j) {
+                const int s = (ntc0 + j) * 16 + (l & 15);
+                const bool live = s < actp;
+                const unsigned row = pin * (unsigned)bpad + (unsigned)s;
+                f16x8_t b[KSW];
 #pragma unroll
-                    for (int i = 0; i < G; ++i) {
-                        const int col = 32 * (w * KSW + q * G + i) + 8 * (l >> 4);
-                        b[i] = __builtin_bit_cast(f16x8_t, __builtin_amdgcn_raw_buffer_load_b128(
-                                                               Rz, live ? (row * KP + col) * 2u : OOB, 0, BL_SC1));
+                for (int ks = 0; ks < KSW; ++ks) {
+                    const int col = 32 * (w * KSW + ks) + 8 * (l >> 4);
+                    b[ks] = __builtin_bit_cast(f16x8_t, __builtin_amdgcn_raw_buffer_load_b128(
+                                                            Rz, live ? (row * KP + col) * 2u : OOB, 0, BL_SC1));
+                }
+                float inv[KSW];
+                if constexpr (KSW % 4 == 0) {
+#pragma unroll
+                    for (int k4 = 0; k4 < KSW; k4 += 4) {
+                        const bl_u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(
+                            Rs, live ? (row * NB + w * KSW + k4) * 4u : OOB, 0, BL_SC1);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const float sc = __uint_as_float(v[e]);
+                            inv[k4 + e] = sc > 0.0f ? 1.0f / sc : 0.0f;
+                        }
                     }
+                } else {
 #pragma unroll
-                    for (int i = 0; i < G / 2; ++i) {
-                        const int blk = (w * KSW + q * G) / 2 + i;
+                    for (int ks = 0; ks < KSW; ++ks) {
                         const float sc = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
-                            Rs, live ? (row * NB + blk) * 4u : OOB, 0, BL_SC1));
-                        inv[i] = sc > 0.0f ? 1.0f / sc : 0.0f;
+                            Rs, live ? (row * NB + w * KSW + ks) * 4u : OOB, 0, BL_SC1));
+                        inv[ks] = sc > 0.0f ? 1.0f / sc : 0.0f;
                     }
-                };
+                }
                 f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
-                auto compute = [&](const f16x8_t* b, const float* inv, int j, int q) {
-                    if (q == 0) acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                    for (int i = 0; i < G / 2; ++i) {
-                        f32x4_t tmp = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-                            a[q * G + 2 * i], b[2 * i], f32x4_t{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
-                        tmp = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[q * G + 2 * i + 1], b[2 * i + 1],
-                                                                     tmp, 0, 0, 0);
-                        acc += tmp * inv[i];
-                    }
-                    if (q == NGR - 1)
-                        *reinterpret_cast<f32x4_t*>(lds + ((w * BL_NTC + j) * 64 + l) * 4) = acc;
-                };
-                if constexpr (SINGLE) {
-                    f16x8_t b0[G];
-                    float i0[G / 2];
-                    for (int j = 0; j < nchunk; ++j) {
-#pragma unroll
-                        for (int q = 0; q < NGR; ++q) {
-                            load(b0, i0, j, q);
-                            compute(b0, i0, j, q);
-                        }
-                    }
-                } else {
-                f16x8_t b0[G], b1[G];
-                float i0[G / 2], i1[G / 2];
-                load(b0, i0, 0, 0);
-                if constexpr (NGR == 1) {
-                    for (int j = 0; j < nchunk; j += 2) {
-                        if (j + 1 < nchunk) load(b1, i1, j + 1, 0);
-                        compute(b0, i0, j, 0);
-                        if (j + 2 < nchunk) load(b0, i0, j + 2, 0);
-                        if (j + 1 < nchunk) compute(b1, i1, j + 1, 0);
-                    }
-                } else {
-                    static_assert(NGR % 2 == 0, "groups alternate between the two buffers");
-                    for (int j = 0; j < nchunk; ++j) {
-#pragma unroll
-                        for (int q = 0; q < NGR; q += 2) {
-                            load(b1, i1, j, q + 1);
-                            compute(b0, i0, j, q);
-                            if (q + 2 < NGR) load(b0, i0, j, q + 2);
-                            else if (j + 1 < nchunk) load(b0, i0, j + 1, 0);
-                            compute(b1, i1, j, q + 1);
-                        }
-                    }
+                for (int ks = 0; ks < KSW; ++ks) {
+                    const int kg = w * KSW + ks;
+                    f16x8_t a = f16x8_t{};
+                    if (alane) a = *reinterpret_cast<const f16x8_t*>(ufr + ((size_t)kg * 32 + aslot) * 8);
+                    const f32x4_t tmp = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                        a, b[ks], f32x4_t{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+                    acc += tmp * inv[ks];
                 }
-                }
+                // lanes 0..31 hold the 8 real units (rows 4 (l / 16) + i of the tile)
+                if (l < 32) *reinterpret_cast<f32x4_t*>(part + ((w * BL_NTC + j) * 32 + l) * 4) = acc;
             }
             __syncthreads();
-            // ---- cell: the owned pairs of the chunk's rows; the 16 lanes of a
-            // row are its 16 units
+            // ---- cell: the owned pairs of the chunk's rows; 8 lanes per row
             {
-                const int ul = tid & 15, u = 16 * g + ul;
+                const int ul = tid & 7, u = 8 * g + ul;
                 const bool uin = u < H;
                 const int rend = min((ntc0 + nchunk) * 16, rows);
-                for (int s = ntc0 * 16 + (tid >> 4); s < rend; s += BL_WAVES * 4) {
+                for (int s = ntc0 * 16 + (tid >> 3); s < rend; s += BL_WAVES * 8) {
                     float dh = 0.0f;
                     if (s < actp) {
                         const int j = (s >> 4) - ntc0, ln = 16 * (ul >> 2) + (s & 15), i = ul & 3;
                         float sum = 0.0f;
 #pragma unroll
-                        for (int ww = 0; ww < BL_WAVES; ++ww) sum += lds[((ww * BL_NTC + j) * 64 + ln) * 4 + i];
+                        for (int ww = 0; ww < BL_WAVES; ++ww) sum += part[((ww * BL_NTC + j) * 32 + ln) * 4 + i];
                         dh = sum * p.alpha_u;
                     }
                     const size_t su = (size_t)s * H + u;
                     if (uin) dh += p.dH[su];
-                    if (last) {  // dh entering step t_end (dh0 when t_end is 0)
+                    if (last) {  // dh entering step t_end - 1 (dh0 when t_end is 0)
                         if (uin) p.dH[su] = dh;
                         continue;
                     }
@@ -661,7 +636,7 @@ bwd_loop_kernel(BwdLoopParams p) {
                     unsigned m = 0;
 #pragma unroll
                     for (int e = 0; e < 4; ++e) m = max(m, __float_as_uint(fabsf(dz[e])) & 0x7fffffffu);
-                    for (int o = 8; o > 0; o >>= 1) m = max(m, (unsigned)__shfl_xor((int)m, o));
+                    for (int o = 4; o > 0; o >>= 1) m = max(m, (unsigned)__shfl_xor((int)m, o));
                     const float mf = __uint_as_float(m);
                     float sc = 1.0f;
                     if (mf > 0.0f && mf < 3.0e38f) {
@@ -674,7 +649,7 @@ bwd_loop_kernel(BwdLoopParams p) {
                                          (_Float16)(dz[2] * sc), (_Float16)(dz[3] * sc)};
                     const unsigned row = pout * (unsigned)bpad + (unsigned)s;
                     __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(bl_u32x2, hv), Rz,
-                                                          (row * KP + 64 * g + 4 * ul) * 2u, 0, BL_SC1);
+                                                          (row * KP + 32 * g + 4 * ul) * 2u, 0, BL_SC1);
                     if (ul == 0)
                         __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(sc), Rs, (row * NB + g) * 4u, 0,
                                                               BL_SC1);
@@ -686,14 +661,18 @@ bwd_loop_kernel(BwdLoopParams p) {
     }
 }
 
-// 2 K-steps per wave at the least (a scale block is two K-steps of one wave),
-// 32 at the most (H = 2048); H even so 8-column groups do not straddle rows.
+// K-steps per wave: 32 columns each over 4H, a power of two, 32 at the most
+// (H = 2048); H even so 8-column groups do not straddle rows of U.
 int bwd_loop_ksw(int H) {
-    if (H < 65 || H > 2048 || (H & 1)) return 0;
-    const int ks = (H + 7) / 8;  // K-steps of 32 over 4H columns
-    int ksw = 2;
+    if (H < 16 || H > 2048 || (H & 1)) return 0;
+    const int ks = (H + 7) / 8;
+    int ksw = 1;
     while (ksw * BL_WAVES < ks) ksw *= 2;
     return ksw;
+}
+
+static int bwd_loop_lds_bytes(int ksw) {
+    return BL_WAVES * ksw * 32 * 16 + BL_WAVES * BL_NTC * 32 * 16;
 }
 
 typedef void (*bwd_loop_fn)(BwdLoopParams);
@@ -703,32 +682,34 @@ static bwd_loop_fn bwd_loop_pick(int ksw, int cell) {
     if (ksw == K)                                                                           \
         return cell == CELL_GRU ? bwd_loop_kernel<K, CELL_GRU>                              \
                : cell == CELL_RNN ? bwd_loop_kernel<K, CELL_RNN> : bwd_loop_kernel<K, CELL_LSTM>;
-    BL_CELLS(2) BL_CELLS(4) BL_CELLS(8) BL_CELLS(16) BL_CELLS(32)
+    BL_CELLS(1) BL_CELLS(2) BL_CELLS(4) BL_CELLS(8) BL_CELLS(16) BL_CELLS(32)
 #undef BL_CELLS
     return nullptr;
 }
 
-// Sizes of the exchange: columns per published row and scale blocks per row.
+// Sizes of the exchange: columns per published row and scale blocks per row
+// (one block of 32 columns per workgroup).
 void bwd_loop_shape(int H, int* kp, int* nblk) {
     const int ksw = bwd_loop_ksw(H);
     *kp = 32 * BL_WAVES * ksw;
-    *nblk = *kp / 64;
+    *nblk = *kp / 32;
 }
 
 // Workgroups (one per CU, all resident) the loop can run with, or 0.
 int bwd_loop_fits(const Dims& d, int num_cus) {
     const int ksw = bwd_loop_ksw(d.H);
     if (!ksw || !d.bf16 || d.bpad > 512) return 0;
-    const int groups = (d.H + 15) / 16;
+    const int groups = (d.H + 7) / 8;
     if (groups > num_cus) return 0;
     bwd_loop_fn f = bwd_loop_pick(ksw, d.cell);
     if (!f) return 0;
+    const int lds = bwd_loop_lds_bytes(ksw);
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(f),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, BL_LDS_BYTES) != hipSuccess)
+                            hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess)
         return 0;
     int n = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, reinterpret_cast<const void*>(f), BL_WAVES * 64,
-                                                     BL_LDS_BYTES) != hipSuccess || n < 1)
+                                                     lds) != hipSuccess || n < 1)
         return 0;
     return groups;
 }
@@ -762,13 +743,13 @@ hipError_t launch_bwd_loop(const Dims& d, const _Float16* u16, float alpha_u, co
     p.H = d.H;
     p.T = d.T;
     p.bpad = d.bpad;
-    p.groups = (d.H + 15) / 16;
+    p.groups = (d.H + 7) / 8;
     p.kp = kp;
     p.nblk = nblk;
     p.t_end = t_end;
     void* args[] = {&p};
     return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(f), dim3(p.groups),
-                                      dim3(BL_WAVES * 64), args, (unsigned)BL_LDS_BYTES, s);
+                                      dim3(BL_WAVES * 64), args, (unsigned)bwd_loop_lds_bytes(ksw), s);
 }
 
 }  // namespace ldyn

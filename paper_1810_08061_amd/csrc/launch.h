@@ -132,11 +132,13 @@ hipError_t launch_bwd_cell16(const Dims& d, int t, int off, int act, const float
                              const float* save_c, const float* dseq, float* dH, float* dC,
                              float* srow, _Float16* dz16, const Workspace& ws, hipStream_t s);
 hipError_t launch_bwd_ones(float* a, int n, hipStream_t s);
-// bf16 data: the whole reverse loop in one cooperative launch (one workgroup
-// of 16 units per CU, U rows resident, each step's dz published in fp16 with
-// a power-of-two scale per row and 64-column block, one grid barrier per
-// step).  bwd_loop_fits: its workgroup count, or 0 where it does not apply
-// (H odd, H <= 64 or H > 2048, more than 512 rows, not all resident).
+// bf16 data: the reverse loop over steps max_len - 1 .. t_end in one
+// cooperative launch (one workgroup of 8 units per CU, those units' rows of U
+// in LDS, each step's dz published in fp16 with a power-of-two scale per row
+// and 32-column block, one grid barrier per step), leaving in dH the
+// gradient entering step t_end - 1.  bwd_loop_fits: its workgroup count, or
+// 0 where it does not apply (H odd, below 16 or above 2048, more than 512
+// rows, not all resident).
 // dzx [2][bpad][kp] fp16, dzs [2][bpad][nblk] and bar [9 * 64] must be zero
 // at the launch; dH, dC hold the upstream gradients (slot order) and receive
 // dh0, dc0.
