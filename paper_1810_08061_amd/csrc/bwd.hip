@@ -551,6 +551,23 @@ bwd_loop_kernel(BwdLoopParams p) {
         const int rows = last ? actp : actc;
         const int nt = (rows + 15) >> 4;
         const unsigned pin = (unsigned)((t + 1) & 1), pout = (unsigned)((t + 2) & 1);
+        // The cell's inputs for this thread's pair of the first chunk depend
+        // on no other workgroup: loaded now, they travel during the product.
+        const int ul = tid & 7, u = 8 * g + ul;
+        const bool uin = u < H;
+        const int s_pre = tid >> 3;
+        const bool pre = !last && uin && s_pre < min(rows, BL_NTC * 16);
+        f32x4_t z_pre = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        float hp_pre = 0.f, cp_pre = 0.f, dh_pre = 0.f, dc_pre = 0.f, ds_pre = 0.f;
+        if (pre) {
+            const size_t r = (size_t)p.offsets[t] + s_pre, su = (size_t)s_pre * H + u;
+            z_pre = *reinterpret_cast<const f32x4_t*>(p.gx + r * H4 + 4 * u);
+            hp_pre = p.save_h[r * H + u];
+            cp_pre = p.save_c[r * H + u];
+            dh_pre = p.dH[su];
+            dc_pre = p.dC[su];
+            if (p.dseq) ds_pre = p.dseq[((size_t)p.perm[s_pre] * p.T + t) * H + u];
+        }
         for (int ntc0 = 0; ntc0 < nt; ntc0 += BL_NTC) {
             const int nchunk = min(BL_NTC, nt - ntc0);
             // ---- product: this wave's KSW K-steps of each row tile, the
@@ -602,10 +619,9 @@ bwd_loop_kernel(BwdLoopParams p) {
             __syncthreads();
             // ---- cell: the owned pairs of the chunk's rows; 8 lanes per row
             {
-                const int ul = tid & 7, u = 8 * g + ul;
-                const bool uin = u < H;
                 const int rend = min((ntc0 + nchunk) * 16, rows);
                 for (int s = ntc0 * 16 + (tid >> 3); s < rend; s += BL_WAVES * 8) {
+                    const bool have = pre && ntc0 == 0;  // s is s_pre: one pass per chunk
                     float dh = 0.0f;
                     if (s < actp) {
                         const int j = (s >> 4) - ntc0, ln = 16 * (ul >> 2) + (s & 15), i = ul & 3;
@@ -615,19 +631,24 @@ bwd_loop_kernel(BwdLoopParams p) {
                         dh = sum * p.alpha_u;
                     }
                     const size_t su = (size_t)s * H + u;
-                    if (uin) dh += p.dH[su];
+                    if (uin) dh += have ? dh_pre : p.dH[su];
                     if (last) {  // dh entering step t_end - 1 (dh0 when t_end is 0)
                         if (uin) p.dH[su] = dh;
                         continue;
                     }
                     f32x4_t dz = f32x4_t{0.f, 0.f, 0.f, 0.f};
                     if (uin) {
-                        if (p.dseq) dh += p.dseq[((size_t)p.perm[s] * p.T + t) * H + u];
                         const size_t r = (size_t)p.offsets[t] + s;
                         f32x4_t* zp = reinterpret_cast<f32x4_t*>(p.gx + r * H4 + 4 * u);
                         float dcp, dhd;
-                        dz = cell_backward<CELL>(*zp, p.save_h[r * H + u], p.save_c[r * H + u], dh,
-                                                 p.dC[su], dcp, dhd);
+                        if (have) {
+                            dh += ds_pre;
+                            dz = cell_backward<CELL>(z_pre, hp_pre, cp_pre, dh, dc_pre, dcp, dhd);
+                        } else {
+                            if (p.dseq) dh += p.dseq[((size_t)p.perm[s] * p.T + t) * H + u];
+                            dz = cell_backward<CELL>(*zp, p.save_h[r * H + u], p.save_c[r * H + u], dh,
+                                                     p.dC[su], dcp, dhd);
+                        }
                         *zp = dz;
                         p.dC[su] = dcp;
                         p.dH[su] = dhd;
