@@ -240,14 +240,19 @@ int lstm_dyn_forward_train(lstm_dyn_t* h, const void* x, const int32_t* lengths,
  * [D][3H], [H][3H], [6H] = d b_ih ++ d b_hh; RNN [D][H], [H][H], [H]), dh0
  * and dc0 [B][H]; no output may overlap another argument.  GRU and RNN
  * handles have no cell state: c0 and d_out_c are ignored and dc0 may be
- * NULL (else zeros).  A step a row does not take passes its state through unchanged,
- * so its gradient is the identity.  Step t's dz comes from the kept
- * pre-activations; dh <- dz U^T and the weight gradients (sums over all valid
- * steps) run as fp32 GEMMs.  Synchronises once with the host (the step
- * offsets) and then issues two launches per step.  Consumes what the forward
- * kept (a second backward needs another forward for training).  Returns
- * LSTM_DYN_OK, ERR_INVALID (bad arguments, or no forward for training kept),
- * ERR_HIP.
+ * NULL (else zeros).  A step a row does not take passes its state through
+ * unchanged, so its gradient is the identity.  Step t's dz comes from the
+ * kept pre-activations; dh <- dz U^T and the weight gradients (sums over all
+ * valid steps) are products with fp32 accumulation, of fp32 operands with
+ * fp32 data and of fp16 operands with bf16 data (each scaled by a power of
+ * two: U and the weight-gradient operands as a whole, dz per row or per row
+ * and 32-column block).  Synchronises once with the host (the step offsets),
+ * then issues two launches per step; a persistent handle with bf16 data (H
+ * even, 16 <= H <= 2048, B <= 512) takes the steps with at most 16 rows in
+ * one cooperative launch with a bounded grid barrier per step (a timeout
+ * shows in LSTM_DYN_Q_LAST_STATUS).  Consumes what the forward kept (a
+ * second backward needs another forward for training).  Returns LSTM_DYN_OK,
+ * ERR_INVALID (bad arguments, or no forward for training kept), ERR_HIP.
  */
 int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* lengths, const void* W,
                       const void* U, const float* b, const float* h0, const float* c0,
