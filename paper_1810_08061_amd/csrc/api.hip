@@ -22,10 +22,10 @@ struct TrainWs {
     float* dw_il;   // [D][4H] weight gradients, gate-interleaved columns
     float* du_il;   // [H][4H]
     float* db_il;   // [4H]
+    float* cs_part; // [BWD_CS_CHUNKS][4H] partial column sums of dz
     float* dH;      // [B][H] gradient of h in slot order
     float* dC;      // [B][H]
     float* z;       // [bpad][4H] per-step pre-activations (handles not in per-step mode)
-    float* ones;    // [B*T] 1.0: db = dz^T 1
     // bf16 data: fp16 operands of the weight-gradient GEMMs (scaled by powers of two)
     _Float16* dz16; // [B*T][4H]
     _Float16* x16;  // [B*T][D]
@@ -677,12 +677,12 @@ static int ensure_train(lstm_dyn* h) {
     const long long oh = take(4 * B * T * H), oc = take(4 * B * T * H), ox = take(4 * B * T * D),
                     ow = take(4 * D * 4 * H), ou = take(4 * H * 4 * H), odw = take(4 * D * 4 * H),
                     odu = take(4 * H * 4 * H), odb = take(16 * H), odh = take(4 * B * H),
-                    odc = take(4 * B * H), oz = take(16 * H * bpad), o1 = take(4 * B * T);
+                    odc = take(4 * B * H), oz = take(16 * H * bpad);
     const bool h16 = h->dtype == LSTM_DYN_BF16;
     const long long odz16 = take(h16 ? 2 * B * T * 4 * H : 0), ox16 = take(h16 ? 2 * B * T * D : 0),
                     oh16 = take(h16 ? 2 * B * T * H : 0), ow16 = take(h16 ? 2 * D * 4 * H : 0),
                     ou16 = take(h16 ? 2 * H * 4 * H : 0), odzs = take(h16 ? 2 * B * 4 * H : 0),
-                    osr = take(4 * B), osm = take(256);
+                    osr = take(4 * B), osm = take(256), ocs = take(4LL * BWD_CS_CHUNKS * 4 * H);
     tw->loop_groups =
         h16 && h->mode == LSTM_DYN_PERSISTENT ? bwd_loop_fits(h->dims, h->num_cus) : 0;
     int kp = 0, nblk = 0;
@@ -705,10 +705,10 @@ static int ensure_train(lstm_dyn* h) {
     tw->dw_il = reinterpret_cast<float*>(base + odw);
     tw->du_il = reinterpret_cast<float*>(base + odu);
     tw->db_il = reinterpret_cast<float*>(base + odb);
+    tw->cs_part = reinterpret_cast<float*>(base + ocs);
     tw->dH = reinterpret_cast<float*>(base + odh);
     tw->dC = reinterpret_cast<float*>(base + odc);
     tw->z = reinterpret_cast<float*>(base + oz);
-    tw->ones = reinterpret_cast<float*>(base + o1);
     tw->dz16 = h16 ? reinterpret_cast<_Float16*>(base + odz16) : nullptr;
     tw->x16 = h16 ? reinterpret_cast<_Float16*>(base + ox16) : nullptr;
     tw->h16 = h16 ? reinterpret_cast<_Float16*>(base + oh16) : nullptr;
@@ -720,11 +720,6 @@ static int ensure_train(lstm_dyn* h) {
     tw->dzx = tw->loop_groups ? reinterpret_cast<_Float16*>(base + odzx) : nullptr;
     tw->dzs = tw->loop_groups ? reinterpret_cast<float*>(base + odzsc) : nullptr;
     tw->bar = tw->loop_groups ? reinterpret_cast<unsigned*>(base + obar) : nullptr;
-    if (hipMemsetD32(reinterpret_cast<hipDeviceptr_t>(tw->ones), 0x3f800000, (size_t)(B * T)) != hipSuccess) {
-        (void)hipFree(tw->block);
-        delete tw;
-        return LSTM_DYN_ERR_HIP;
-    }
     if (hipHostMalloc(reinterpret_cast<void**>(&tw->host_offsets), (size_t)(T + 8) * sizeof(int32_t),
                       hipHostMallocDefault) != hipSuccess) {
         (void)hipFree(tw->block);
@@ -983,11 +978,11 @@ extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* le
     h->launches_last++;
     if (rows > 0) {
         LD_CHECK(launch_bwd_gather_x(d, x, rows, tw->xc, h->ws, s));
-        // db = dz^T 1 (K = the sum of lengths)
-        RB_CHECK(rocblas_sgemv(tw->rb, rocblas_operation_none, H4, rows, &one, h->ws.gx, H4,
-                               tw->ones, 1, &zero, tw->db_il, 1));
-        h->launches_last += 2;
+        h->launches_last++;
         if (!d.bf16) {
+            // db = dz^T 1 (K = the sum of lengths)
+            LD_CHECK(launch_bwd_colsum(h->ws.gx, rows, H4, tw->cs_part, tw->db_il, nullptr, 1.0f, s));
+            h->launches_last += 2;
             // dW = X^T dz, dU = H_prev^T dz, then dx rows = dz W^T over the gathered x
             RB_CHECK(rocblas_sgemm(tw->rb, rocblas_operation_none, rocblas_operation_transpose, H4,
                                    d.D, rows, &one, h->ws.gx, H4, tw->xc, d.D, &zero, tw->dw_il, H4));
@@ -1012,7 +1007,8 @@ extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* le
             LD_CHECK(hipStreamSynchronize(s));
             const float sz = f16_scale(am[0]), sx = f16_scale(am[1]), sh = f16_scale(am[2]),
                         sw = f16_scale(am[3]);
-            LD_CHECK(launch_bwd_to_f16(h->ws.gx, tw->dz16, n_dz, sz, s));
+            // db and the fp16 dz in one pass over dz
+            LD_CHECK(launch_bwd_colsum(h->ws.gx, rows, H4, tw->cs_part, tw->db_il, tw->dz16, sz, s));
             LD_CHECK(launch_bwd_to_f16(tw->xc, tw->x16, n_x, sx, s));
             LD_CHECK(launch_bwd_to_f16(tw->save_h, tw->h16, n_h, sh, s));
             LD_CHECK(launch_bwd_to_f16(tw->w_il, tw->w16, n_w, sw, s));
@@ -1030,7 +1026,7 @@ extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* le
                                      rows, H4, &a_x, tw->w16, f16, H4, tw->dz16, f16, H4, &zero,
                                      tw->xc, f32, d.D, tw->xc, f32, d.D, f32,
                                      rocblas_gemm_algo_standard, 0, 0));
-            h->launches_last += 11;
+            h->launches_last += 12;
         }
     } else {
         LD_CHECK(hipMemsetAsync(tw->dw_il, 0, (size_t)d.D * H4 * sizeof(float), s));

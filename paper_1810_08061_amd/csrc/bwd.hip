@@ -309,6 +309,42 @@ bwd_absmax_kernel(const float* __restrict__ a, long n, unsigned* out) {
     if ((threadIdx.x & 63) == 0) atomicMax(out, m);
 }
 
+// db = dz^T 1 over all compact rows: the rows are cut into BWD_CS_CHUNKS
+// ranges, a thread sums one group of four columns over one range in row
+// order (partial sums, then bwd_colsum_finish_kernel over the ranges in
+// order), and with CONV the same pass writes dz16 = fp16(dz * scale) for
+// the weight-gradient GEMMs.
+template <bool CONV>
+__global__ void __launch_bounds__(256)
+bwd_colsum_kernel(const float* __restrict__ dz, long rows, int n4, float* __restrict__ part,
+                  _Float16* __restrict__ dz16, float scale) {
+    const int cg = blockIdx.x * 256 + threadIdx.x;  // columns 4 cg .. 4 cg + 3
+    if (cg >= n4) return;
+    const long per = (rows + BWD_CS_CHUNKS - 1) / BWD_CS_CHUNKS;
+    const long r0 = (long)blockIdx.y * per, r1 = r0 + per < rows ? r0 + per : rows;
+    typedef _Float16 h4_t __attribute__((ext_vector_type(4)));
+    f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+    for (long r = r0; r < r1; ++r) {
+        const f32x4_t v = *reinterpret_cast<const f32x4_t*>(dz + r * 4 * n4 + 4 * cg);
+        acc += v;
+        if constexpr (CONV)
+            *reinterpret_cast<h4_t*>(dz16 + r * 4 * n4 + 4 * cg) =
+                h4_t{(_Float16)(v[0] * scale), (_Float16)(v[1] * scale), (_Float16)(v[2] * scale),
+                     (_Float16)(v[3] * scale)};
+    }
+    *reinterpret_cast<f32x4_t*>(part + (size_t)blockIdx.y * 4 * n4 + 4 * cg) = acc;
+}
+
+__global__ void __launch_bounds__(256)
+bwd_colsum_finish_kernel(const float* __restrict__ part, int ncols, float* __restrict__ out) {
+    const int c = blockIdx.x * 256 + threadIdx.x;
+    if (c >= ncols) return;
+    float s = 0.0f;
+    for (int k = 0; k < BWD_CS_CHUNKS; ++k) s += part[(size_t)k * ncols + c];
+    out[c] = s;
+}
+
 // dst = fp16(src * scale), n elements.
 __global__ void __launch_bounds__(256)
 bwd_to_f16_kernel(const float* __restrict__ src, _Float16* dst, long n, float scale) {
@@ -398,6 +434,20 @@ hipError_t launch_bwd_gather_x(const Dims& d, const void* x, long rows, float* x
 hipError_t launch_bwd_absmax(const float* a, long n, unsigned* out, hipStream_t s) {
     const unsigned g = grid_of(n) < 2048 ? grid_of(n) : 2048;
     hipLaunchKernelGGL(bwd_absmax_kernel, dim3(g), dim3(256), 0, s, a, n, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_bwd_colsum(const float* dz, long rows, int ncols, float* part, float* out,
+                             _Float16* dz16, float scale, hipStream_t s) {
+    const int n4 = ncols / 4;
+    const dim3 grid((unsigned)((n4 + 255) / 256), BWD_CS_CHUNKS);
+    if (dz16)
+        hipLaunchKernelGGL(bwd_colsum_kernel<true>, grid, dim3(256), 0, s, dz, rows, n4, part, dz16, scale);
+    else
+        hipLaunchKernelGGL(bwd_colsum_kernel<false>, grid, dim3(256), 0, s, dz, rows, n4, part, dz16,
+                           scale);
+    hipLaunchKernelGGL(bwd_colsum_finish_kernel, dim3((unsigned)((ncols + 255) / 256)), dim3(256), 0, s,
+                       part, ncols, out);
     return hipGetLastError();
 }
 

@@ -154,6 +154,11 @@ hipError_t launch_bwd_gather_x(const Dims& d, const void* x, long rows, float* x
 // atomic and order free) and a scaled conversion.
 hipError_t launch_bwd_absmax(const float* a, long n, unsigned* out, hipStream_t s);
 hipError_t launch_bwd_to_f16(const float* src, _Float16* dst, long n, float scale, hipStream_t s);
+// db = column sums of dz [rows][ncols] (ncols a multiple of 4) through
+// part [BWD_CS_CHUNKS][ncols]; with dz16, also dz16 = fp16(dz * scale).
+constexpr int BWD_CS_CHUNKS = 64;
+hipError_t launch_bwd_colsum(const float* dz, long rows, int ncols, float* part, float* out,
+                             _Float16* dz16, float scale, hipStream_t s);
 hipError_t launch_bwd_permute(const Dims& d, const float* il, float* out, int rows, hipStream_t s);
 hipError_t launch_bwd_dx(const Dims& d, const float* dxc, long rows, const int32_t* lengths,
                          float* dx, const Workspace& ws, hipStream_t s);
