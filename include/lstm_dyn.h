@@ -110,8 +110,14 @@ enum {
 /* lstm_dyn_set_option selectors. */
 enum {
     LSTM_DYN_OPT_TIMING = 0,    /* 1: record HIP events on the forward's stream around each phase */
-    LSTM_DYN_OPT_STEP_TRACE = 1 /* 1: the persistent kernel records device wall-clock
-                                   timestamps within each step (diagnostics) */
+    LSTM_DYN_OPT_STEP_TRACE = 1, /* 1: the persistent kernel records device wall-clock
+                                    timestamps within each step (diagnostics) */
+    LSTM_DYN_OPT_TIMEOUT_US = 2  /* bound, in microseconds, of every wait of the
+                                    cooperative kernels (grid barriers, polls for
+                                    other workgroups' data); 0 restores the default of
+                                    5 s, at most 60 s.  Past it a kernel stops, sets
+                                    LSTM_DYN_ERR_TIMEOUT (LSTM_DYN_Q_LAST_STATUS) and
+                                    exits normally */
 };
 
 /* Launch plan of a handle: pure host arithmetic, no device access. */

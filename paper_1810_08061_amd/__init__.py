@@ -33,7 +33,7 @@ CELL_LSTM, CELL_GRU, CELL_RNN = 0, 1, 2
 OK, ERR_INVALID, ERR_HIP, ERR_NOMEM, ERR_UNSUPPORTED, ERR_BAD_LENGTHS, ERR_TIMEOUT = range(7)
 Q_LAST_STATUS, Q_STEPS_EXECUTED, Q_LAUNCHES_PER_FORWARD, Q_GROUPS, Q_WORKSPACE_BYTES, \
     Q_TOTAL_ROWS, Q_TIME_PREP_NS, Q_TIME_INPROJ_NS, Q_TIME_LOOP_NS = range(9)
-OPT_TIMING, OPT_STEP_TRACE = 0, 1
+OPT_TIMING, OPT_STEP_TRACE, OPT_TIMEOUT_US = 0, 1, 2
 
 _DTYPES = {"f32": F32, "fp32": F32, "float32": F32, "bf16": BF16, "bfloat16": BF16}
 _MODES = {"persistent": PERSISTENT, "per_step": PER_STEP}

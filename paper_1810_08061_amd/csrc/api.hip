@@ -394,6 +394,12 @@ extern "C" int lstm_dyn_set_option(lstm_dyn_t* h, int option, long long value) {
         h->timing = value ? 1 : 0;
         return LSTM_DYN_OK;
     }
+    if (option == LSTM_DYN_OPT_TIMEOUT_US) {
+        if (value < 0 || value > 60000000LL) return LSTM_DYN_ERR_INVALID;
+        const double us = value ? (double)value : BARRIER_TIMEOUT_S * 1e6;
+        h->timeout_ticks = (unsigned long long)(us * 1e-3 * (double)h->wclk_khz);
+        return LSTM_DYN_OK;
+    }
     if (option == LSTM_DYN_OPT_STEP_TRACE) {
         if (value && !h->trace) {
             if (hipMalloc(&h->trace, sizeof(unsigned long long) * 4 * (h->T + 1)) != hipSuccess) {
@@ -726,7 +732,10 @@ static int ensure_train(lstm_dyn* h) {
         delete tw;
         return LSTM_DYN_ERR_HIP;
     }
-    if (rocblas_create_handle(&tw->rb) != rocblas_status_success) {
+    // no atomics in rocBLAS's kernels: the same inputs give the same
+    // gradients bit for bit
+    if (rocblas_create_handle(&tw->rb) != rocblas_status_success ||
+        rocblas_set_atomics_mode(tw->rb, rocblas_atomics_not_allowed) != rocblas_status_success) {
         (void)hipFree(tw->block);
         (void)hipHostFree(tw->host_offsets);
         delete tw;

@@ -279,3 +279,9 @@ def test_plan_batch_limits(D, H, dt):
     with pytest.raises(ld.LstmDynError) as e:
         ld.lstm_dyn_plan(8193, D, H, 5, dt, ld.PER_STEP, 256)
     assert e.value.code == ld.ERR_UNSUPPORTED
+
+
+def test_wait_bound_option_range():
+    """Host-side checks of LSTM_DYN_OPT_TIMEOUT_US need no device: a NULL
+    handle is refused before the value is looked at."""
+    assert ld._load().lstm_dyn_set_option(None, ld.OPT_TIMEOUT_US, 1) == ld.ERR_INVALID

@@ -1,0 +1,70 @@
+"""Failure handling of the bounded waits, forced from the host: with the wait
+bound (LSTM_DYN_OPT_TIMEOUT_US) set to 1 microsecond, the cooperative
+kernels give up at a wait that does not succeed at once, report
+LSTM_DYN_ERR_TIMEOUT through LSTM_DYN_Q_LAST_STATUS and exit normally; with
+the default bound restored, the same handle computes what a fresh handle
+computes, bit for bit."""
+import numpy as np
+import pytest
+
+import paper_1810_08061_amd as ld
+import workloads
+from tests.gpu_util import say, to_device
+
+pytestmark = pytest.mark.gpu
+
+
+def test_forward_wait_bound():
+    import torch
+    inp = workloads.random_case(1301, 64, 32, 512, 120, dtype="bf16", lo=60)
+    dev = to_device(inp)
+    m = ld.LstmDyn(inp.B, inp.D, inp.H, inp.T, inp.dtype, "persistent")
+    m.set_option(ld.OPT_TIMEOUT_US, 1)
+    say("case forward with a 1 us wait bound")
+    m.forward(*dev)
+    torch.cuda.synchronize()
+    assert m.query(ld.Q_LAST_STATUS) == ld.ERR_TIMEOUT
+    m.set_option(ld.OPT_TIMEOUT_US, 0)
+    h, c = m.forward(*dev)
+    torch.cuda.synchronize()
+    assert m.query(ld.Q_LAST_STATUS) == ld.OK
+    f = ld.LstmDyn(inp.B, inp.D, inp.H, inp.T, inp.dtype, "persistent")
+    h2, c2 = f.forward(*dev)
+    torch.cuda.synchronize()
+    assert torch.equal(h, h2) and torch.equal(c, c2)
+    m.close()
+    f.close()
+
+
+def test_backward_wait_bound():
+    """The one-launch reverse loop (bf16 data, at most 16 rows per step)."""
+    import torch
+    inp = workloads.random_case(1302, 16, 32, 512, 40, dtype="bf16", lo=20)
+    dev = to_device(inp)
+    rng = np.random.default_rng(1303)
+    dh = torch.from_numpy(rng.standard_normal((inp.B, inp.H)).astype(np.float32)).cuda()
+    dc = torch.from_numpy(rng.standard_normal((inp.B, inp.H)).astype(np.float32)).cuda()
+
+    def grads(m):
+        m.forward_train(*dev)
+        g = m.backward(*dev, dh, dc)
+        torch.cuda.synchronize()
+        return g
+
+    m = ld.LstmDyn(inp.B, inp.D, inp.H, inp.T, inp.dtype, "persistent")
+    m.forward_train(*dev)
+    torch.cuda.synchronize()
+    m.set_option(ld.OPT_TIMEOUT_US, 1)
+    say("case backward with a 1 us wait bound")
+    m.backward(*dev, dh, dc)
+    torch.cuda.synchronize()
+    assert m.query(ld.Q_LAST_STATUS) == ld.ERR_TIMEOUT
+    m.set_option(ld.OPT_TIMEOUT_US, 0)
+    g = grads(m)
+    assert m.query(ld.Q_LAST_STATUS) == ld.OK
+    f = ld.LstmDyn(inp.B, inp.D, inp.H, inp.T, inp.dtype, "persistent")
+    g2 = grads(f)
+    for k in g:
+        assert torch.equal(g[k], g2[k]), k
+    m.close()
+    f.close()
