@@ -14,11 +14,14 @@
 //   * bwd_cell_kernel: dz of the step's rows from z, c_{t-1}, dh, dc (and the
 //     gradient of the output sequence at t), written over z; dc <- dc_total f;
 //   * dh <- dz U^T for those rows, a GEMM (K = 4H) issued by the host;
-// and after the last one the weight gradients are GEMMs over all compact
-// rows (K = sum of lengths): dW = X^T dz, dU = H_prev^T dz, db = dz^T 1,
-// dx = dz W^T, in gate-interleaved columns, permuted back to the caller's
-// gate blocks at the end.  With bf16 data the three GEMMs take fp16 operands
-// scaled by powers of two (fp32 accumulation); with fp32 data they are fp32.
+// with bf16 data on a persistent handle the steps with few rows (the last
+// ones, met first) instead run in one cooperative launch (bwd_loop_kernel,
+// below).  After the last step the weight gradients are GEMMs over all
+// compact rows (K = sum of lengths): dW = X^T dz, dU = H_prev^T dz,
+// dx = dz W^T, and db = dz^T 1 a column sum, in gate-interleaved columns,
+// permuted back to the caller's gate blocks at the end.  With bf16 data the
+// three GEMMs take fp16 operands scaled by powers of two (fp32
+// accumulation); with fp32 data they are fp32.
 #include "launch.h"
 
 namespace ldyn {
@@ -490,8 +493,8 @@ hipError_t launch_bwd_dx(const Dims& d, const float* dxc, long rows, const int32
 //     published in fp16 under the block's scale), dc and the carried term;
 //   * a grid barrier; the published dz alternates between two buffers.
 // The carried dh and dc live in dH, dC ([B][H], slot order): in, the upstream
-// gradients of the final state (or of the state entering the step after
-// t_end - 1 ... max_len - 1); out, dh entering step t_end - 1 and dc0 ...
+// gradients of the final state; out, the complete dh entering step t_end - 1
+// (dh0 when t_end is 0) and the carried dc at that point.
 struct BwdLoopParams {
     const _Float16* u16;     // [H][4H] U, gate-interleaved columns, times su
     float* gx;               // [rows][4H] z in, dz (fp32) out
