@@ -360,12 +360,12 @@ def main():
         tm.close()
         tps.close()
 
-    configs = None
+    per_shape = None
     if not args.no_configs:
         # every workload shape: the forward with the loop on the device
         # against the per-step path (one host launch pair per step), both
         # timed back to back on the host clock between synchronisations
-        configs = {}
+        per_shape = {}
         for name in workloads.ORDER:
             cw = workloads.WORKLOADS[name]
             _log(f"persistent vs per-step, {name}")
@@ -381,7 +381,7 @@ def main():
             assert cm.query(ld.Q_LAST_STATUS) == ld.OK
             cps = ld.LstmDyn(cw.B, cw.D, cw.H, cw.T, cw.dtype, "per_step")
             t_s = time_whole(torch, cps, cdev, 10 if cw.H <= 512 else 2, 1, cout)
-            configs[name] = {"value": cL / t_p, "unit": "seq·steps/s", "dtype": cw.dtype,
+            per_shape[name] = {"value": cL / t_p, "unit": "seq·steps/s", "dtype": cw.dtype,
                              "sum_lengths": cL, "max_len": int(cin.lengths.max()),
                              "persistent_ms": t_p * 1e3, "per_step_ms": t_s * 1e3,
                              "speedup_of_persistent": t_s / t_p,
@@ -435,7 +435,7 @@ def main():
         "train_step": train_leg,
         "cells": cell_legs,
         "tiny_f32": tiny,
-        "configs": configs,
+        "configs": per_shape,
     }
     if not args.no_cpu:
         _log("cpu baseline (oracle)")
