@@ -73,3 +73,33 @@ def test_largest_per_step_batch():
     assert z.size > 0
     assert np.array_equal(h[z], inp.h0[z].astype(np.float64)) and np.array_equal(c[z], inp.c0[z].astype(np.float64))
     m.close()
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_largest_persistent_batch_backward(dt):
+    """The backward at 512 rows: the per-row gradients of sampled rows against
+    the oracle run on those rows alone, every gradient against the per-step
+    handle's (the two paths share no per-step code with bf16 data: the
+    persistent handle runs the one-launch reverse loop for its steps with at
+    most 16 rows)."""
+    import torch
+    from tests.test_gpu_bwd import GRAD_TOL, compare, oracle_grads, run_train, scaled_err
+    B, D, H, T = 512, 24, 256, 6
+    inp = workloads.random_case(4200, B, D, H, T, dtype=dt)
+    rng = np.random.default_rng(4201)
+    dh = rng.standard_normal((B, H)).astype(np.float32)
+    dc = rng.standard_normal((B, H)).astype(np.float32)
+    ds = rng.standard_normal((B, T, H)).astype(np.float32)
+    say(f"case limit backward {(B, D, H, T, dt)}")
+    g, _, m = run_train(inp, "persistent", dh, dc, ds)
+    rows = _sample(inp)
+    go = oracle_grads(inp, dh.astype(np.float64), dc.astype(np.float64), ds.astype(np.float64), rows)
+    compare({k: g[k][rows] for k in ("dx", "dh0", "dc0")}, go, GRAD_TOL[dt], keys=("dx", "dh0", "dc0"))
+    gs, _, ms = run_train(inp, "per_step", dh, dc, ds)
+    for k in g:
+        e = scaled_err(g[k], gs[k])
+        say(f"  {k} against the per-step path: {e:.2e}")
+        assert e <= 2 * GRAD_TOL[dt], (k, e)
+    m.close()
+    ms.close()
+    torch.cuda.empty_cache()
