@@ -519,12 +519,12 @@ static int forward_impl(lstm_dyn_t* h, const void* x, const int32_t* lengths, co
         LD_CHECK(mark(2));
         PersistentConfig pc{h->plan.mt,     h->plan.groups,    h->plan.ksw, h->plan.kw,
                             h->plan.nstate, h->plan.lds_bytes, h->timeout_ticks, h->trace,
-                            out_seq != nullptr, stop};
+                            out_seq,        stop};
         LD_CHECK(launch_persistent(d, pc, U, h0, c0, out_h, out_c, h->ws, s));
         h->launches_last++;
         LD_CHECK(mark(3));
-        if (out_seq) {
-            LD_CHECK(launch_seq_finish(d, out_seq, true, 4 * h->plan.mt, seq_ends, h->ws, h->num_cus, s));
+        if (out_seq) {  // the loop wrote the valid steps; zeros past each row's last
+            LD_CHECK(launch_seq_finish(d, out_seq, false, 4, seq_ends, h->ws, h->num_cus, s));
             h->launches_last++;
         }
         return LSTM_DYN_OK;
@@ -791,7 +791,7 @@ extern "C" int lstm_dyn_forward_train(lstm_dyn_t* h, const void* x, const int32_
         LD_CHECK(mark(2));
         PersistentConfig pc{h->plan.mt,     h->plan.groups,    h->plan.ksw, h->plan.kw,
                             h->plan.nstate, h->plan.lds_bytes, h->timeout_ticks, h->trace,
-                            0,              nullptr,           tw->save_h,  tw->save_c};
+                            nullptr,        nullptr,           tw->save_h,  tw->save_c};
         LD_CHECK(launch_persistent(d, pc, U, h0, c0, out_h, out_c, h->ws, s));
         h->launches_last++;
     } else {

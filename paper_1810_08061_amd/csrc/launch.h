@@ -71,7 +71,8 @@ struct PersistentConfig {
     int mt, groups, ksw, kw, nst, lds_bytes;
     unsigned long long timeout_ticks;  // barrier wait bound in wall-clock ticks
     unsigned long long* trace;         // per-step timestamps (diagnostics) or null
-    int seq;                           // 1: keep each step's h in the dead Gx rows (output sequence)
+    float* seq;                        // output sequence [B][T][H]: each step's h of the rows that
+                                       // ran it (zeros past them written afterwards), or null
     const StopArgs* stop;              // termination from the state, or null
     float* save_h;                     // forward for training: the state each step starts from,
     float* save_c;                     // [compact rows][H] (z is kept in place of Gx); else null

@@ -34,6 +34,7 @@
 namespace ldyn {
 
 constexpr int P_LDS_KB = 144;           // dynamic LDS for partial sums and the Gx prefetch
+constexpr int P_MAX_ROWS = 512;         // batch rows the variants hold (8 owned row tiles per wave)
 constexpr int P_SC1 = 16;               // buffer-instruction cache policy: device scope
 
 struct PersistParams {
@@ -51,7 +52,7 @@ struct PersistParams {
     int B, H, hpad, bpad, groups;
     unsigned long long timeout_ticks;
     unsigned long long* trace;  // [T + 1][4] timestamps from workgroup 0, or null
-    int seq;                    // 1: also keep each step's h (fp32) for the output sequence
+    float* seq;                 // output sequence [B][T][H] (fp32), or null
     // Termination from the state (variants with STOP): a row ends after a step
     // that leaves v . h + c > 0; steps[b] receives the steps row b ran.
     const float* stop_v;        // [H]
@@ -252,6 +253,8 @@ persistent_kernel(PersistParams p) {
     __shared__ __attribute__((aligned(16))) S vst[VST];
     __shared__ float s_part[STOP ? KW : 1][STOP ? NTC : 1][16];
     __shared__ int lds_run[2];
+    // slot -> batch row, for the output sequence's row addresses
+    __shared__ int perm_s[P_MAX_ROWS];
 
     // tid and l are re-read through empty asm statements at the top of each
     // step and chunk, so values derived from them (addresses, row indices)
@@ -276,6 +279,8 @@ persistent_kernel(PersistParams p) {
     if constexpr (STOP) {
         for (int k = tid; k < VST; k += KW * 64) vst[k] = E::from_f32(k < H ? p.stop_v[k] : 0.0f);
     }
+    if (p.seq)  // read after the prologue's barriers
+        for (int i = tid; i < B; i += KW * 64) perm_s[i] = p.perm[i];
     F afrag[MT][KSW];
 
     // ---- U slice -> registers (A-fragments of U^T; rows = gate-interleaved columns).
@@ -766,15 +771,17 @@ persistent_kernel(PersistParams p) {
                         seg_store(nxt + hx_off<E>(nt * 16 + lo, u0, hpad), &hstage[w][lo * UPW]);
                     __builtin_amdgcn_wave_barrier();
                     if (p.seq) {
-                        // the output sequence: h of (row, unit) in fp32, kept in the
-                        // first UPW floats of this workgroup's columns of the row's
-                        // Gx, which nothing reads again (its own Gx prefetch of
-                        // this step has landed; no other workgroup reads them)
-                        float* const row = const_cast<float*>(p.gx) + (size_t)(o0 + nt * 16 + (lo & 15)) * H4 + 4 * u0;
+                        // the output sequence: h of (row, unit) after step t, fp32,
+                        // at out_seq[b][t] (a row that has ended keeps storing its
+                        // state; the zeros written after the loop replace it)
+                        const int s = nt * 16 + (lo & 15);
+                        if (s < act) {
+                            float* const row = p.seq + ((size_t)perm_s[s] * p.T + t) * H + u0;
 #pragma unroll
-                        for (int mt = 0; mt < MT; ++mt) {
-                            const int u = u0 + mt * 4 + (lo >> 4);
-                            if (nt * 16 + (lo & 15) < act && u < H) row[mt * 4 + (lo >> 4)] = hst[a * MT + mt];
+                            for (int mt = 0; mt < MT; ++mt) {
+                                const int u = u0 + mt * 4 + (lo >> 4);
+                                if (u < H) row[mt * 4 + (lo >> 4)] = hst[a * MT + mt];
+                            }
                         }
                     }
                 }
@@ -910,7 +917,7 @@ hipError_t launch_persistent(const Dims& d, const PersistentConfig& pc, const vo
                              const Workspace& ws, hipStream_t s) {
     const int mode = pc.stop ? LM_STOP : pc.save_h ? LM_SAVE : LM_PLAIN;
     persist_fn f = find_variant(d.bf16, pc.mt, pc.ksw, pc.kw, pc.nst, d.cell, mode);
-    if (!f) return hipErrorInvalidValue;
+    if (!f || (pc.seq && d.B > P_MAX_ROWS)) return hipErrorInvalidValue;
     PersistParams p{};
     p.U = U;
     p.h0 = h0;
@@ -931,6 +938,7 @@ hipError_t launch_persistent(const Dims& d, const PersistentConfig& pc, const vo
     p.timeout_ticks = pc.timeout_ticks;
     p.trace = pc.trace;
     p.seq = pc.seq;
+    p.T = d.T;
     p.save_h = pc.save_h;
     p.save_c = pc.save_c;
     if (pc.stop) {
