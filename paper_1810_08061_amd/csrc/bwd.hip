@@ -778,14 +778,15 @@ int bwd_loop_fits(const Dims& d, int num_cus) {
     bwd_loop_fn f = bwd_loop_pick(ksw, d.cell);
     if (!f) return 0;
     const int lds = bwd_loop_lds_bytes(ksw);
-    if (hipFuncSetAttribute(reinterpret_cast<const void*>(f),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess)
-        return 0;
     int n = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, reinterpret_cast<const void*>(f), BL_WAVES * 64,
-                                                     lds) != hipSuccess || n < 1)
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(f),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, reinterpret_cast<const void*>(f),
+                                                     BL_WAVES * 64, lds) != hipSuccess) {
+        (void)hipGetLastError();  // not an error of a later call: the per-step path serves
         return 0;
-    return groups;
+    }
+    return n >= 1 ? groups : 0;
 }
 
 hipError_t launch_bwd_loop(const Dims& d, const _Float16* u16, float alpha_u, const float* save_h,
