@@ -193,3 +193,23 @@ def test_backward_one_launch_reverse_loop(seq):
     per_step = mp.query(ld.Q_LAUNCHES_PER_FORWARD)
     say(f"  backward launches: {launches} (per-step path {per_step})")
     assert launches < 30 <= 2 * int(inp.lengths.max()) <= per_step
+
+
+@pytest.mark.parametrize("scale", [1e-6, 1e6, 1e12])
+@pytest.mark.parametrize("mode", MODES)
+def test_backward_upstream_magnitude(scale, mode):
+    """Gradients are linear in the upstream gradients: scaled by 1e-6 to 1e12
+    they are scaled alike, and the fp16 operands of the bf16 path (powers of
+    two per operand, per row and per row block) neither overflow nor lose
+    the largest entries.  Rows of the batch run both the one-launch reverse
+    loop (steps with at most 16 rows) and the per-step path."""
+    B, D, H, T = 33, 40, 100, 14
+    inp = workloads.random_case(1401, B, D, H, T, dtype="bf16")
+    dh, dc, ds = upstream(2401, B, H, T)
+    dh, dc, ds = dh * np.float32(scale), dc * np.float32(scale), ds * np.float32(scale)
+    say(f"case bwd upstream x{scale:g} {mode}")
+    g, _, _ = run_train(inp, mode, dh, dc, ds)
+    for k in g:
+        assert np.all(np.isfinite(g[k])), k
+    go = oracle_grads(inp, dh.astype(np.float64), dc.astype(np.float64), ds.astype(np.float64))
+    compare(g, go, GRAD_TOL["bf16"])
