@@ -75,9 +75,9 @@ class _Lib:
         lib.lstm_oracle_forward_stop.argtypes = [ctypes.c_int] * 4 + [P] * 6 + [ctypes.c_int, P,
                                                  ctypes.c_double] + [P] * 7 + [ctypes.c_int]
         lib.lstm_oracle_forward_stop.restype = ctypes.c_int
-        lib.lstm_oracle_backward.argtypes = [ctypes.c_int] * 4 + [P] * 16
+        lib.lstm_oracle_backward.argtypes = [ctypes.c_int] * 4 + [P] * 16 + [ctypes.c_int]
         lib.lstm_oracle_backward.restype = ctypes.c_int
-        lib.lstm_oracle_backward_cell.argtypes = [ctypes.c_int] * 5 + [P] * 15
+        lib.lstm_oracle_backward_cell.argtypes = [ctypes.c_int] * 5 + [P] * 15 + [ctypes.c_int]
         lib.lstm_oracle_backward_cell.restype = ctypes.c_int
         lib.lstm_oracle_max_threads.argtypes = []
         lib.lstm_oracle_max_threads.restype = ctypes.c_int
@@ -250,12 +250,14 @@ def forward_rnn(x, lengths, W, U, b, h0, literal: bool = False, threads: int = 0
     return out[0] if len(out) == 1 else out
 
 
-def backward(x, lengths, W, U, b, h0, c0, dh_out, dc_out, dseq=None, _lib_override=None):
+def backward(x, lengths, W, U, b, h0, c0, dh_out, dc_out, dseq=None, _lib_override=None,
+             threads: int = 0):
     """Gradients of the masked LSTM loop (backpropagation through time): given
     the upstream gradients of the final state (dh_out, dc_out [B, H]) and
     optionally of the output sequence (dseq [B, T, H]), returns a dict of
     float64 arrays dx [B, T, D], dW [D, 4H], dU [H, 4H], db [4H], dh0, dc0
-    [B, H].  Layouts as for ``forward``."""
+    [B, H].  Layouts as for ``forward``.  ``threads`` (0: all cores) changes
+    the schedule only: every thread count gives the same bits."""
     lib = (_lib_override or _load()).lib
     x, W, U, b = map(_f32, (x, W, U, b))
     f64 = lambda a: np.ascontiguousarray(a, dtype=np.float64)
@@ -277,7 +279,8 @@ def backward(x, lengths, W, U, b, h0, c0, dh_out, dc_out, dseq=None, _lib_overri
                                   U.ctypes.data, b.ctypes.data, h0.ctypes.data, c0.ctypes.data,
                                   dh_out.ctypes.data, dc_out.ctypes.data,
                                   ds.ctypes.data if ds is not None else None,
-                                  *(out[k].ctypes.data for k in ("dx", "dW", "dU", "db", "dh0", "dc0")))
+                                  *(out[k].ctypes.data for k in ("dx", "dW", "dU", "db", "dh0", "dc0")),
+                                  int(threads))
     if rc == BAD_LENGTHS:
         raise OracleError("sequence lengths must lie in [0, T]")
     if rc != OK:
@@ -285,7 +288,7 @@ def backward(x, lengths, W, U, b, h0, c0, dh_out, dc_out, dseq=None, _lib_overri
     return out
 
 
-def _backward_cell(cell, x, lengths, W, U, b, b_hh, h0, dh_out, dseq, _lib_override):
+def _backward_cell(cell, x, lengths, W, U, b, b_hh, h0, dh_out, dseq, _lib_override, threads=0):
     lib = (_lib_override or _load()).lib
     x, W, U, b = map(_f32, (x, W, U, b))
     bhh = _f32(b_hh) if b_hh is not None else None
@@ -311,7 +314,7 @@ def _backward_cell(cell, x, lengths, W, U, b, b_hh, h0, dh_out, dseq, _lib_overr
                                        out["dx"].ctypes.data, out["dW"].ctypes.data,
                                        out["dU"].ctypes.data, out["db"].ctypes.data,
                                        dbhh.ctypes.data if dbhh is not None else None,
-                                       out["dh0"].ctypes.data)
+                                       out["dh0"].ctypes.data, int(threads))
     if rc == BAD_LENGTHS:
         raise OracleError("sequence lengths must lie in [0, T]")
     if rc != OK:
@@ -322,17 +325,19 @@ def _backward_cell(cell, x, lengths, W, U, b, b_hh, h0, dh_out, dseq, _lib_overr
     return out
 
 
-def backward_gru(x, lengths, W, U, b_ih, b_hh, h0, dh_out, dseq=None, _lib_override=None):
+def backward_gru(x, lengths, W, U, b_ih, b_hh, h0, dh_out, dseq=None, _lib_override=None,
+                 threads: int = 0):
     """Gradients of the masked loop with the GRU cell: dx, dW [D, 3H],
     dU [H, 3H], db_ih, db_hh [3H], dh0 (float64), from the upstream gradient of
     the final h and optionally of the output sequence."""
-    return _backward_cell(1, x, lengths, W, U, b_ih, b_hh, h0, dh_out, dseq, _lib_override)
+    return _backward_cell(1, x, lengths, W, U, b_ih, b_hh, h0, dh_out, dseq, _lib_override, threads)
 
 
-def backward_rnn(x, lengths, W, U, b, h0, dh_out, dseq=None, _lib_override=None):
+def backward_rnn(x, lengths, W, U, b, h0, dh_out, dseq=None, _lib_override=None,
+                 threads: int = 0):
     """Gradients of the masked loop with the tanh RNN cell: dx, dW [D, H],
     dU [H, H], db [H], dh0 (float64)."""
-    return _backward_cell(2, x, lengths, W, U, b, None, h0, dh_out, dseq, _lib_override)
+    return _backward_cell(2, x, lengths, W, U, b, None, h0, dh_out, dseq, _lib_override, threads)
 
 
 _CELL_IDS = {"lstm": 0, "gru": 1, "rnn": 2}

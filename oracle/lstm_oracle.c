@@ -419,90 +419,135 @@ int lstm_oracle_forward_stop(int B, int T, int D, int H, const float* x, const i
  *   dz = (di i (1 - i), df f (1 - f), dg (1 - g^2), do o (1 - o))
  *   db += dz, dW += x_t^T dz, dU += h_{t-1}^T dz, dx_t = dz W^T, dh <- dz U^T
  * with (i, f, g, o) and c_t recomputed by the forward in double precision.
- * Rows run one after another in order 0 .. B-1 and the weight gradients are
- * summed in that order.
+ * Rows are differentiated one after another in order 0 .. B-1 and the
+ * weight gradients summed in that order, step by step from each row's last.
+ *
+ * Threads (nthreads, <= 0: all) change only the schedule, never the order of
+ * any sum: the forward recompute runs rows of a block side by side (each
+ * row's recompute is serial), and each reverse step splits its products by
+ * k, so every entry of dW, dU and dx (and of dh through dz U^T) is summed by
+ * one thread in the order above.  The result is the same bits for every
+ * thread count.
  */
+
+/* Rows of one block whose forward recompute is held at once: at most nt,
+ * and at most about 1 GB of saved states. */
+static int bwd_block_rows(int nt, int T, int per_step_doubles) {
+    const double bytes = (double)(T > 0 ? T : 1) * per_step_doubles * sizeof(double);
+    int r = (int)(1.0e9 / bytes);
+    if (r < 1) r = 1;
+    return r < nt ? r : nt;
+}
+
 int lstm_oracle_backward(int B, int T, int D, int H, const float* x, const int32_t* L,
                          const float* W, const float* U, const float* bias, const double* h0,
                          const double* c0, const double* dh_out, const double* dc_out,
                          const double* dseq, double* dx, double* dW, double* dU, double* db,
-                         double* dh0, double* dc0) {
+                         double* dh0, double* dc0, int nthreads) {
     if (B <= 0 || T < 0 || D <= 0 || H <= 0 || !x || !L || !W || !U || !bias || !h0 || !c0 ||
         !dh_out || !dc_out || !dx || !dW || !dU || !db || !dh0 || !dc0)
         return ORACLE_BAD_ARGS;
     for (int b = 0; b < B; ++b)
         if (L[b] < 0 || L[b] > T) return ORACLE_BAD_LENGTHS;
     const int G = 4 * H;
-    double* zs = (double*)malloc((size_t)(T > 0 ? T : 1) * G * sizeof(double));   /* z_t per step */
-    double* cs = (double*)malloc((size_t)(T + 1) * H * sizeof(double));            /* c_{t-1}, t = 0..T */
-    double* hs = (double*)malloc((size_t)(T + 1) * H * sizeof(double));            /* h_{t-1} */
+    int nt = 1;
+#ifdef _OPENMP
+    nt = nthreads > 0 ? nthreads : omp_get_max_threads();
+#endif
+    /* per row of a block: z_t per step, c_{t-1} and h_{t-1} for t = 0..T */
+    const size_t zrow = (size_t)(T > 0 ? T : 1) * G, srow = (size_t)(T + 1) * H;
+    const int nb = bwd_block_rows(nt, T, 6 * H);
+    double* zblk = (double*)malloc((size_t)nb * zrow * sizeof(double));
+    double* cblk = (double*)malloc((size_t)nb * srow * sizeof(double));
+    double* hblk = (double*)malloc((size_t)nb * srow * sizeof(double));
     double* dz = (double*)malloc((size_t)G * sizeof(double));
     double* dh = (double*)malloc((size_t)H * sizeof(double));
     double* dc = (double*)malloc((size_t)H * sizeof(double));
     double* nh = (double*)malloc((size_t)H * sizeof(double));
-    if (!zs || !cs || !hs || !dz || !dh || !dc || !nh) {
-        free(zs); free(cs); free(hs); free(dz); free(dh); free(dc); free(nh);
+    if (!zblk || !cblk || !hblk || !dz || !dh || !dc || !nh) {
+        free(zblk); free(cblk); free(hblk); free(dz); free(dh); free(dc); free(nh);
         return ORACLE_NOMEM;
     }
     memset(dx, 0, (size_t)B * T * D * sizeof(double));
     memset(dW, 0, (size_t)D * G * sizeof(double));
     memset(dU, 0, (size_t)H * G * sizeof(double));
     memset(db, 0, (size_t)G * sizeof(double));
-    for (int b = 0; b < B; ++b) {
-        const int n = L[b];
-        /* forward through the row's own steps, keeping z_t, c and h */
-        memcpy(hs, h0 + (size_t)b * H, (size_t)H * sizeof(double));
-        memcpy(cs, c0 + (size_t)b * H, (size_t)H * sizeof(double));
-        for (int t = 0; t < n; ++t) {
-            const float* xin = &x[((size_t)b * T + t) * D];
-            lstm_cell_row(D, H, xin, W, U, bias, hs + (size_t)t * H, cs + (size_t)t * H,
-                          zs + (size_t)t * G, hs + (size_t)(t + 1) * H, cs + (size_t)(t + 1) * H);
+    for (int b0 = 0; b0 < B; b0 += nb) {
+        const int rows = B - b0 < nb ? B - b0 : nb;
+        /* forward through each row's own steps, keeping z_t, c and h */
+#ifdef _OPENMP
+#pragma omp parallel for num_threads(nt) schedule(dynamic, 1)
+#endif
+        for (int r = 0; r < rows; ++r) {
+            const int b = b0 + r, n = L[b];
+            double* zs = zblk + (size_t)r * zrow;
+            double* cs = cblk + (size_t)r * srow;
+            double* hs = hblk + (size_t)r * srow;
+            memcpy(hs, h0 + (size_t)b * H, (size_t)H * sizeof(double));
+            memcpy(cs, c0 + (size_t)b * H, (size_t)H * sizeof(double));
+            for (int t = 0; t < n; ++t) {
+                const float* xin = &x[((size_t)b * T + t) * D];
+                lstm_cell_row(D, H, xin, W, U, bias, hs + (size_t)t * H, cs + (size_t)t * H,
+                              zs + (size_t)t * G, hs + (size_t)(t + 1) * H, cs + (size_t)(t + 1) * H);
+            }
         }
-        memcpy(dh, dh_out + (size_t)b * H, (size_t)H * sizeof(double));
-        memcpy(dc, dc_out + (size_t)b * H, (size_t)H * sizeof(double));
-        for (int t = n - 1; t >= 0; --t) {
-            if (dseq)
-                for (int u = 0; u < H; ++u) dh[u] += dseq[((size_t)b * T + t) * H + u];
-            const double* z = zs + (size_t)t * G;
-            const double* cprev = cs + (size_t)t * H;
-            const double* cnew = cs + (size_t)(t + 1) * H;
-            for (int u = 0; u < H; ++u) {
-                const double ig = sig(z[u]), fg = sig(z[H + u]);
-                const double gg = tanh(z[2 * H + u]), og = sig(z[3 * H + u]);
-                const double tc = tanh(cnew[u]);
-                const double d_o = dh[u] * tc;
-                const double dct = dc[u] + dh[u] * og * (1.0 - tc * tc);
-                dz[u] = dct * gg * ig * (1.0 - ig);
-                dz[H + u] = dct * cprev[u] * fg * (1.0 - fg);
-                dz[2 * H + u] = dct * ig * (1.0 - gg * gg);
-                dz[3 * H + u] = d_o * og * (1.0 - og);
-                dc[u] = dct * fg;
-            }
-            for (int j = 0; j < G; ++j) db[j] += dz[j];
-            const float* xin = &x[((size_t)b * T + t) * D];
-            for (int k = 0; k < D; ++k) {      /* dW += x_t^T dz, dx_t = dz W^T */
-                double acc = 0.0;
-                for (int j = 0; j < G; ++j) {
-                    dW[(size_t)k * G + j] += (double)xin[k] * dz[j];
-                    acc += dz[j] * (double)W[(size_t)k * G + j];
+        for (int r = 0; r < rows; ++r) {
+            const int b = b0 + r, n = L[b];
+            const double* zs = zblk + (size_t)r * zrow;
+            const double* cs = cblk + (size_t)r * srow;
+            const double* hs = hblk + (size_t)r * srow;
+            memcpy(dh, dh_out + (size_t)b * H, (size_t)H * sizeof(double));
+            memcpy(dc, dc_out + (size_t)b * H, (size_t)H * sizeof(double));
+            for (int t = n - 1; t >= 0; --t) {
+                if (dseq)
+                    for (int u = 0; u < H; ++u) dh[u] += dseq[((size_t)b * T + t) * H + u];
+                const double* z = zs + (size_t)t * G;
+                const double* cprev = cs + (size_t)t * H;
+                const double* cnew = cs + (size_t)(t + 1) * H;
+                for (int u = 0; u < H; ++u) {
+                    const double ig = sig(z[u]), fg = sig(z[H + u]);
+                    const double gg = tanh(z[2 * H + u]), og = sig(z[3 * H + u]);
+                    const double tc = tanh(cnew[u]);
+                    const double d_o = dh[u] * tc;
+                    const double dct = dc[u] + dh[u] * og * (1.0 - tc * tc);
+                    dz[u] = dct * gg * ig * (1.0 - ig);
+                    dz[H + u] = dct * cprev[u] * fg * (1.0 - fg);
+                    dz[2 * H + u] = dct * ig * (1.0 - gg * gg);
+                    dz[3 * H + u] = d_o * og * (1.0 - og);
+                    dc[u] = dct * fg;
                 }
-                dx[((size_t)b * T + t) * D + k] = acc;
-            }
-            const double* hprev = hs + (size_t)t * H;
-            for (int k = 0; k < H; ++k) {      /* dU += h_{t-1}^T dz, dh = dz U^T */
-                double acc = 0.0;
-                for (int j = 0; j < G; ++j) {
-                    dU[(size_t)k * G + j] += hprev[k] * dz[j];
-                    acc += dz[j] * (double)U[(size_t)k * G + j];
+                for (int j = 0; j < G; ++j) db[j] += dz[j];
+                const float* xin = &x[((size_t)b * T + t) * D];
+#ifdef _OPENMP
+#pragma omp parallel for num_threads(nt) schedule(static)
+#endif
+                for (int k = 0; k < D; ++k) {      /* dW += x_t^T dz, dx_t = dz W^T */
+                    double acc = 0.0;
+                    for (int j = 0; j < G; ++j) {
+                        dW[(size_t)k * G + j] += (double)xin[k] * dz[j];
+                        acc += dz[j] * (double)W[(size_t)k * G + j];
+                    }
+                    dx[((size_t)b * T + t) * D + k] = acc;
                 }
-                nh[k] = acc;
+                const double* hprev = hs + (size_t)t * H;
+#ifdef _OPENMP
+#pragma omp parallel for num_threads(nt) schedule(static)
+#endif
+                for (int k = 0; k < H; ++k) {      /* dU += h_{t-1}^T dz, dh = dz U^T */
+                    double acc = 0.0;
+                    for (int j = 0; j < G; ++j) {
+                        dU[(size_t)k * G + j] += hprev[k] * dz[j];
+                        acc += dz[j] * (double)U[(size_t)k * G + j];
+                    }
+                    nh[k] = acc;
+                }
+                memcpy(dh, nh, (size_t)H * sizeof(double));
             }
-            memcpy(dh, nh, (size_t)H * sizeof(double));
+            memcpy(dh0 + (size_t)b * H, dh, (size_t)H * sizeof(double));
+            memcpy(dc0 + (size_t)b * H, dc, (size_t)H * sizeof(double));
         }
-        memcpy(dh0 + (size_t)b * H, dh, (size_t)H * sizeof(double));
-        memcpy(dc0 + (size_t)b * H, dc, (size_t)H * sizeof(double));
     }
-    free(zs); free(cs); free(hs); free(dz); free(dh); free(dc); free(nh);
+    free(zblk); free(cblk); free(hblk); free(dz); free(dh); free(dc); free(nh);
     return ORACLE_OK;
 }
 
@@ -519,12 +564,13 @@ int lstm_oracle_backward(int B, int T, int D, int H, const float* x, const int32
  *     dW += x^T da, dU += h^T de, db_ih += da, db_hh += de, dx = da W^T
  *   RNN, with h' = tanh(z):  dz = dh (1 - h'^2), dh_prev = dz U^T, and the
  *     same weight, bias and input gradients with da = de = dz.
+ * Order of the sums and threads (nthreads) as for lstm_oracle_backward.
  */
 int lstm_oracle_backward_cell(int B, int T, int D, int H, int cell, const float* x,
                               const int32_t* L, const float* W, const float* U,
                               const float* bias, const float* bhh, const double* h0,
                               const double* dh_out, const double* dseq, double* dx, double* dW,
-                              double* dU, double* db, double* dbhh, double* dh0) {
+                              double* dU, double* db, double* dbhh, double* dh0, int nthreads) {
     if (B <= 0 || T < 0 || D <= 0 || H <= 0 || !x || !L || !W || !U || !bias || !h0 ||
         !dh_out || !dx || !dW || !dU || !db || !dh0)
         return ORACLE_BAD_ARGS;
@@ -533,15 +579,21 @@ int lstm_oracle_backward_cell(int B, int T, int D, int H, int cell, const float*
     for (int b = 0; b < B; ++b)
         if (L[b] < 0 || L[b] > T) return ORACLE_BAD_LENGTHS;
     const int G = cell == CELL_GRU ? 3 * H : H;
-    double* hs = (double*)malloc((size_t)(T + 1) * H * sizeof(double));     /* h_{t-1}, t = 0..T */
-    double* zs = (double*)malloc((size_t)(T > 0 ? T : 1) * 2 * G * sizeof(double));
+    int nt = 1;
+#ifdef _OPENMP
+    nt = nthreads > 0 ? nthreads : omp_get_max_threads();
+#endif
+    /* per row of a block: h_{t-1} for t = 0..T, and a, e (GRU) or z (RNN) per step */
+    const size_t hrow = (size_t)(T + 1) * H, zrow = (size_t)(T > 0 ? T : 1) * 2 * G;
+    const int nb = bwd_block_rows(nt, T, H + 2 * G);
+    double* hblk = (double*)malloc((size_t)nb * hrow * sizeof(double));
+    double* zblk = (double*)malloc((size_t)nb * zrow * sizeof(double));
     double* da = (double*)malloc((size_t)G * sizeof(double));              /* input-side grads */
     double* de = (double*)malloc((size_t)G * sizeof(double));              /* recurrent-side */
     double* dh = (double*)malloc((size_t)H * sizeof(double));
     double* nh = (double*)malloc((size_t)H * sizeof(double));
-    double* zc = (double*)calloc((size_t)H, sizeof(double));               /* unused cell state */
-    if (!hs || !zs || !da || !de || !dh || !nh || !zc) {
-        free(hs); free(zs); free(da); free(de); free(dh); free(nh); free(zc);
+    if (!hblk || !zblk || !da || !de || !dh || !nh) {
+        free(hblk); free(zblk); free(da); free(de); free(dh); free(nh);
         return ORACLE_NOMEM;
     }
     memset(dx, 0, (size_t)B * T * D * sizeof(double));
@@ -549,74 +601,93 @@ int lstm_oracle_backward_cell(int B, int T, int D, int H, int cell, const float*
     memset(dU, 0, (size_t)H * G * sizeof(double));
     memset(db, 0, (size_t)G * sizeof(double));
     if (cell == CELL_GRU) memset(dbhh, 0, (size_t)G * sizeof(double));
-    for (int b = 0; b < B; ++b) {
-        const int n = L[b];
-        memcpy(hs, h0 + (size_t)b * H, (size_t)H * sizeof(double));
-        for (int t = 0; t < n; ++t) {           /* forward, keeping a and e (GRU) or z (RNN) */
-            const float* xr = x + ((size_t)b * T + t) * D;
-            double* za = zs + (size_t)t * 2 * G;
-            if (cell == CELL_GRU)
-                gru_cell_row(D, H, xr, W, U, bias, bhh, hs + (size_t)t * H, za, za + G,
-                             hs + (size_t)(t + 1) * H);
-            else
-                rnn_cell_row(D, H, xr, W, U, bias, hs + (size_t)t * H, za, hs + (size_t)(t + 1) * H);
-        }
-        memcpy(dh, dh_out + (size_t)b * H, (size_t)H * sizeof(double));
-        for (int t = n; t-- > 0;) {          /* last step first */
-            if (dseq)
-                for (int v = 0; v < H; ++v) dh[v] += dseq[((size_t)b * T + t) * H + v];
-            const double* hp = hs + (size_t)t * H;
-            const double* za = zs + (size_t)t * 2 * G;
-            if (cell == CELL_GRU) {
-                const double* ze = za + G;
-                for (int v = 0; v < H; ++v) {
-                    const double rg = sig(za[v] + ze[v]);
-                    const double ug = sig(za[H + v] + ze[H + v]);
-                    const double ng = tanh(za[2 * H + v] + rg * ze[2 * H + v]);
-                    const double dn = dh[v] * (1.0 - ug);
-                    const double du = dh[v] * (hp[v] - ng);
-                    const double dzn = dn * (1.0 - ng * ng);
-                    const double dr = dzn * ze[2 * H + v];
-                    const double dzr = dr * rg * (1.0 - rg), dzu = du * ug * (1.0 - ug);
-                    da[v] = dzr;              de[v] = dzr;
-                    da[H + v] = dzu;          de[H + v] = dzu;
-                    da[2 * H + v] = dzn;      de[2 * H + v] = dzn * rg;
-                    nh[v] = dh[v] * ug;       /* h reaches h' directly through u */
-                }
-            } else {
-                const double* hnew = hs + (size_t)(t + 1) * H;
-                for (int v = 0; v < H; ++v) {
-                    const double hn = hnew[v];       /* tanh(z) of the step */
-                    da[v] = dh[v] * (1.0 - hn * hn);
-                    de[v] = da[v];
-                    nh[v] = 0.0;
-                }
-            }
-            for (int j = 0; j < G; ++j) {
-                db[j] += da[j];
-                if (cell == CELL_GRU) dbhh[j] += de[j];
-            }
-            const float* xr = x + ((size_t)b * T + t) * D;
-            for (int k = 0; k < D; ++k) {      /* dW += x^T da, dx = da W^T */
-                double acc = 0.0;
-                for (int j = 0; j < G; ++j) {
-                    dW[(size_t)k * G + j] += (double)xr[k] * da[j];
-                    acc += da[j] * (double)W[(size_t)k * G + j];
-                }
-                dx[((size_t)b * T + t) * D + k] = acc;
-            }
-            for (int k = 0; k < H; ++k) {      /* dU += h^T de, dh_prev = direct + de U^T */
-                double acc = nh[k];
-                for (int j = 0; j < G; ++j) {
-                    dU[(size_t)k * G + j] += hp[k] * de[j];
-                    acc += de[j] * (double)U[(size_t)k * G + j];
-                }
-                dh[k] = acc;
+    for (int b0 = 0; b0 < B; b0 += nb) {
+        const int rows = B - b0 < nb ? B - b0 : nb;
+#ifdef _OPENMP
+#pragma omp parallel for num_threads(nt) schedule(dynamic, 1)
+#endif
+        for (int r = 0; r < rows; ++r) {        /* forward, keeping a and e (GRU) or z (RNN) */
+            const int b = b0 + r, n = L[b];
+            double* hs = hblk + (size_t)r * hrow;
+            double* zs = zblk + (size_t)r * zrow;
+            memcpy(hs, h0 + (size_t)b * H, (size_t)H * sizeof(double));
+            for (int t = 0; t < n; ++t) {
+                const float* xr = x + ((size_t)b * T + t) * D;
+                double* za = zs + (size_t)t * 2 * G;
+                if (cell == CELL_GRU)
+                    gru_cell_row(D, H, xr, W, U, bias, bhh, hs + (size_t)t * H, za, za + G,
+                                 hs + (size_t)(t + 1) * H);
+                else
+                    rnn_cell_row(D, H, xr, W, U, bias, hs + (size_t)t * H, za, hs + (size_t)(t + 1) * H);
             }
         }
-        memcpy(dh0 + (size_t)b * H, dh, (size_t)H * sizeof(double));
+        for (int r = 0; r < rows; ++r) {
+            const int b = b0 + r, n = L[b];
+            const double* hs = hblk + (size_t)r * hrow;
+            const double* zs = zblk + (size_t)r * zrow;
+            memcpy(dh, dh_out + (size_t)b * H, (size_t)H * sizeof(double));
+            for (int t = n; t-- > 0;) {          /* last step first */
+                if (dseq)
+                    for (int v = 0; v < H; ++v) dh[v] += dseq[((size_t)b * T + t) * H + v];
+                const double* hp = hs + (size_t)t * H;
+                const double* za = zs + (size_t)t * 2 * G;
+                if (cell == CELL_GRU) {
+                    const double* ze = za + G;
+                    for (int v = 0; v < H; ++v) {
+                        const double rg = sig(za[v] + ze[v]);
+                        const double ug = sig(za[H + v] + ze[H + v]);
+                        const double ng = tanh(za[2 * H + v] + rg * ze[2 * H + v]);
+                        const double dn = dh[v] * (1.0 - ug);
+                        const double du = dh[v] * (hp[v] - ng);
+                        const double dzn = dn * (1.0 - ng * ng);
+                        const double dr = dzn * ze[2 * H + v];
+                        const double dzr = dr * rg * (1.0 - rg), dzu = du * ug * (1.0 - ug);
+                        da[v] = dzr;              de[v] = dzr;
+                        da[H + v] = dzu;          de[H + v] = dzu;
+                        da[2 * H + v] = dzn;      de[2 * H + v] = dzn * rg;
+                        nh[v] = dh[v] * ug;       /* h reaches h' directly through u */
+                    }
+                } else {
+                    const double* hnew = hs + (size_t)(t + 1) * H;
+                    for (int v = 0; v < H; ++v) {
+                        const double hn = hnew[v];       /* tanh(z) of the step */
+                        da[v] = dh[v] * (1.0 - hn * hn);
+                        de[v] = da[v];
+                        nh[v] = 0.0;
+                    }
+                }
+                for (int j = 0; j < G; ++j) {
+                    db[j] += da[j];
+                    if (cell == CELL_GRU) dbhh[j] += de[j];
+                }
+                const float* xr = x + ((size_t)b * T + t) * D;
+#ifdef _OPENMP
+#pragma omp parallel for num_threads(nt) schedule(static)
+#endif
+                for (int k = 0; k < D; ++k) {      /* dW += x^T da, dx = da W^T */
+                    double acc = 0.0;
+                    for (int j = 0; j < G; ++j) {
+                        dW[(size_t)k * G + j] += (double)xr[k] * da[j];
+                        acc += da[j] * (double)W[(size_t)k * G + j];
+                    }
+                    dx[((size_t)b * T + t) * D + k] = acc;
+                }
+#ifdef _OPENMP
+#pragma omp parallel for num_threads(nt) schedule(static)
+#endif
+                for (int k = 0; k < H; ++k) {      /* dU += h^T de, dh_prev = direct + de U^T */
+                    double acc = nh[k];
+                    for (int j = 0; j < G; ++j) {
+                        dU[(size_t)k * G + j] += hp[k] * de[j];
+                        acc += de[j] * (double)U[(size_t)k * G + j];
+                    }
+                    dh[k] = acc;
+                }
+            }
+            memcpy(dh0 + (size_t)b * H, dh, (size_t)H * sizeof(double));
+        }
     }
-    free(hs); free(zs); free(da); free(de); free(dh); free(nh); free(zc);
+    free(hblk); free(zblk); free(da); free(de); free(dh); free(nh);
     return ORACLE_OK;
 }
 

@@ -110,3 +110,31 @@ def _cell_bwd(cell, x, L, W, U, b, bhh, h0, dh, ds):
 @pytest.mark.parametrize("pin", oracle_pins.CELL_BWD_PINS, ids=lambda f: f.__name__)
 def test_cell_backward_pin(pin):
     pin(_cell_bwd)
+
+
+@pytest.mark.parametrize("cell", ["lstm", "gru", "rnn"])
+def test_backward_thread_count_does_not_change_bits(cell):
+    """The backward splits its products by k over threads; every entry is
+    still summed by one thread in row, step and k order, so 1, 3 and 8
+    threads give the same bits (blocks of rows of different sizes too)."""
+    B, D, H, T = 11, 7, 9, 8
+    inp = workloads.random_case(21, B, D, H, T, state_var=0.1) if cell == "lstm" else \
+        workloads.random_cell_case(cell, 21, B, D, H, T)
+    x, W, U = inp.as_f32()
+    rng = np.random.default_rng(22)
+    dh = rng.standard_normal((B, H))
+    dc = rng.standard_normal((B, H))
+    ds = rng.standard_normal((B, T, H))
+    outs = []
+    for th in (1, 3, 8):
+        if cell == "lstm":
+            outs.append(oracle.backward(x, inp.lengths, W, U, inp.b, inp.h0, inp.c0, dh, dc, ds,
+                                        threads=th))
+        elif cell == "gru":
+            outs.append(oracle.backward_gru(x, inp.lengths, W, U, inp.b_ih, inp.b_hh, inp.h0, dh, ds,
+                                            threads=th))
+        else:
+            outs.append(oracle.backward_rnn(x, inp.lengths, W, U, inp.b, inp.h0, dh, ds, threads=th))
+    for o in outs[1:]:
+        for k in outs[0]:
+            assert np.array_equal(outs[0][k].view(np.uint64), o[k].view(np.uint64)), k
