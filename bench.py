@@ -14,7 +14,8 @@ roofline     the loop kernel (the dominant kernel): algorithmic recurrent
              duration from HIP events recorded by the library on the
              forward's stream, against the dense bf16 (or fp32) MFMA peak
 cpu_baseline the fp64 oracle on a bounded sample of the same workload, timed
-             on this host's cores
+             on this host's cores; per_config: the oracle on the smaller
+             whole workloads, on one thread and on every core
 
 Side legs on the same workload (not part of value): forward_seq (the forward
 that also writes the output sequence), forward_stop (termination computed
@@ -129,12 +130,22 @@ def copy_calibration(torch, mib=512, reps=5):
     print(json.dumps({"copy_calibration_bytes_each_way": n * 4, "dispatches": reps}), flush=True)
 
 
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(inp, budget_rows_steps):
-    """Time the fp64 oracle on the longest-first prefix of rows whose lengths
+    """Time the fp64 oracle on a sample of the workload's rows whose lengths
     sum to about `budget_rows_steps` (all host cores)."""
     import oracle
     order = np.argsort(-inp.lengths, kind="stable")
-    L = inp.lengths[order]
     # take rows from the middle of the length distribution so the sample's
     # per-step row count resembles the workload's
     mid = len(order) // 4
@@ -148,10 +159,38 @@ def cpu_baseline(inp, budget_rows_steps):
     t0 = time.perf_counter()
     oracle.forward_inputs(inp, rows=rows, threads=threads)
     dt = time.perf_counter() - t0
-    del L
     return {"value": total / dt, "unit": "seq·steps/s", "cores": threads, "kind": "oracle",
             "sample": f"{len(rows)} of {inp.B} rows of the workload (sum of lengths {total}), "
                       f"fp64 C oracle, OpenMP over rows, {dt:.1f} s"}
+
+
+# the smaller workloads timed whole: on one thread (the first three) and on
+# every core (the first four); the largest stays sampled (cpu_baseline)
+CPU_ONE_THREAD = ("tiny_f32", "lstm256_f32", "lstm512_bf16")
+CPU_ALL_CORES = ("tiny_f32", "lstm256_f32", "lstm512_bf16", "skewed1024_bf16")
+
+
+def cpu_per_config(skip):
+    """The fp64 oracle on whole workloads, in valid seq*steps/s."""
+    import oracle
+    threads = oracle.max_threads()
+    out = {}
+    for name in workloads.ORDER:
+        if name == skip or name not in CPU_ALL_CORES:
+            continue
+        inp = workloads.workload_inputs(name)
+        sumL = int(inp.lengths.sum())
+        rec = {"sum_lengths": sumL}
+        for th, key in ((1, "one_thread"), (threads, "all_cores")):
+            if th == 1 and name not in CPU_ONE_THREAD:
+                continue
+            _log(f"cpu baseline (oracle), {name}, {th} thread(s)")
+            t0 = time.perf_counter()
+            oracle.forward_inputs(inp, threads=th)
+            dt = time.perf_counter() - t0
+            rec[key] = {"value": sumL / dt, "seconds": dt, "threads": th}
+        out[name] = rec
+    return out
 
 
 def main():
@@ -161,6 +200,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=workloads.ORDER)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--no-cpu-configs", action="store_true",
+                    help="skip timing the oracle on the smaller whole workloads")
     ap.add_argument("--cpu-budget", type=int, default=24000,
                     help="seq*steps of the oracle sample (about 10-30 s on a host)")
     ap.add_argument("--per-step-reps", type=int, default=3,
@@ -400,6 +441,7 @@ def main():
     bytes_alg = sumL * w.D * e + 4 * w.H * (w.D + w.H) * e + 16 * w.H + 16 * w.B * w.H + 4 * w.B
     peak = PEAK_TFLOPS[dt]
     achieved = flops_rec / t_loop / 1e12
+    traffic = measured_traffic(args.workload)
     line = {
         "metric": METRIC,
         "value": sumL / t_fwd,
@@ -419,11 +461,15 @@ def main():
                    "parallelism": "none (1 GPU)", "persistent_groups": groups},
         "roofline": {"bound": "mfma", "kernel": "persistent time loop (recurrent h U, gates)",
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
-                     "frac": achieved / peak, "traffic": measured_traffic(args.workload),
+                     "frac": achieved / peak, "traffic": traffic,
                      "algorithmic_flops_per_launch": flops_rec,
                      "mean_launch_ms": t_loop * 1e3},
         "mfma_frac_forward": flops_fwd / t_fwd / 1e12 / peak,
-        "hbm_frac_forward": bytes_alg / t_fwd / 1e9 / HBM_PEAK_GBS,
+        # algorithmic bytes (valid x, W, U, b, states, lengths) over the forward
+        "hbm_frac_forward_algorithmic": bytes_alg / t_fwd / 1e9 / HBM_PEAK_GBS,
+        # the loop kernel's counted HBM bytes (committed rocprofv3 record) over
+        # its mean launch time
+        "hbm_frac_loop_measured": (traffic / t_loop / 1e9 / HBM_PEAK_GBS) if traffic else None,
         "phases_ms": {"prep": t_prep * 1e3, "input_projection": t_inproj * 1e3,
                       "loop": t_loop * 1e3},
         "input_projection_tflops": flops_in / t_inproj / 1e12,
@@ -439,7 +485,12 @@ def main():
     }
     if not args.no_cpu:
         _log("cpu baseline (oracle)")
-        line["cpu_baseline"] = cpu_baseline(inp, args.cpu_budget)
+        cb = cpu_baseline(inp, args.cpu_budget)
+        cb["host"] = {"cpu_model": cpu_model(), "nproc": os.cpu_count(),
+                      "affinity": len(os.sched_getaffinity(0))}
+        if not args.no_cpu_configs:
+            cb["per_config"] = cpu_per_config(skip=None)
+        line["cpu_baseline"] = cb
     print(json.dumps(line), flush=True)
     model.close()
 

@@ -54,10 +54,13 @@ enum { LSTM_DYN_F32 = 0, LSTM_DYN_BF16 = 1 };
 
 /* Execution mode.
  * PERSISTENT: the time loop runs on the device inside one persistent kernel
- *   (grid-wide synchronisation between steps, loop bound and early exit read
- *   on the device); 3 launches per forward (1 when the hidden width is at most
- *   32 and the whole forward fits one workgroup), none of them waits for the
- *   host.
+ *   (one grid barrier at its start, then each step waits only for the hidden
+ *   state it reads; loop bound and early exit read on the device).  Launches
+ *   per forward: length preparation, input projection (two launches with
+ *   bf16 data: a transpose of W, then the GEMM), the loop; one more for the
+ *   GRU and RNN cells (their weights are repacked); a single launch when the
+ *   hidden width is at most 32 and the whole forward fits one workgroup.
+ *   None of them waits for the host.
  * PER_STEP: the comparison path of the paper's eager-vs-graph experiment
  *   (Section 9, Table 1): the loop bound is copied to the host (one
  *   synchronisation), then the host issues two kernel launches per step. */
@@ -182,8 +185,8 @@ int lstm_dyn_forward(lstm_dyn_t* h, const void* x, const int32_t* lengths, const
  *     padding chosen).  Lengths outside [0, T_max] are clamped as in
  *     lstm_dyn_forward.
  * out_seq may not overlap any other argument.  One more kernel launch than
- * lstm_dyn_forward (it writes the zeros past each length and, in persistent
- * mode, moves the step outputs into place).  Returns as lstm_dyn_forward.
+ * lstm_dyn_forward (it writes the zeros past each length; the loop writes
+ * the valid steps).  Returns as lstm_dyn_forward.
  */
 int lstm_dyn_forward_seq(lstm_dyn_t* h, const void* x, const int32_t* lengths, const void* W,
                          const void* U, const float* b, const float* h0, const float* c0,
@@ -265,7 +268,10 @@ int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* lengths, cons
                       const float* d_out_h, const float* d_out_c, const float* d_seq, float* dx,
                       float* dW, float* dU, float* db, float* dh0, float* dc0, void* stream);
 
-/* Free the handle and its workspace (synchronises the device).  NULL is a no-op. */
+/* Free the handle and its workspace.  Waits for the stream of the handle's
+ * last forward or backward (the only work that may use the workspace), not
+ * for the whole device; the runtime's free may still wait for the device.
+ * NULL is a no-op. */
 int lstm_dyn_destroy(lstm_dyn_t* h);
 
 /* Read a property of the handle or of its last forward (see LSTM_DYN_Q_*). */

@@ -4,11 +4,53 @@
 #include <new>
 #include <stdint.h>
 #include <string.h>
+#include <type_traits>
 
+#include <dlfcn.h>
 #include <rocblas/rocblas.h>
 
 #include "../../include/lstm_dyn.h"
 #include "launch.h"
+
+// rocBLAS serves the backward pass's plain GEMMs only.  It is loaded at the
+// first forward for training, so processes that only run forwards never map
+// it; it is never unloaded.
+namespace {
+struct RocblasApi {
+    decltype(&rocblas_create_handle) create_handle;
+    decltype(&rocblas_destroy_handle) destroy_handle;
+    decltype(&rocblas_set_atomics_mode) set_atomics_mode;
+    decltype(&rocblas_set_stream) set_stream;
+    decltype(&rocblas_sgemm) sgemm;
+    decltype(&rocblas_gemm_ex) gemm_ex;
+};
+RocblasApi g_rb;
+bool g_rb_loaded = false;
+
+bool load_rocblas() {
+    if (g_rb_loaded) return true;
+    void* lib = dlopen("librocblas.so.5", RTLD_NOW | RTLD_LOCAL);
+    if (!lib) lib = dlopen("/opt/rocm/lib/librocblas.so.5", RTLD_NOW | RTLD_LOCAL);
+    if (!lib) lib = dlopen("librocblas.so", RTLD_NOW | RTLD_LOCAL);
+    if (!lib) return false;
+    RocblasApi a;
+    bool ok = true;
+    auto sym = [&](auto& f, const char* name) {
+        f = reinterpret_cast<std::remove_reference_t<decltype(f)>>(dlsym(lib, name));
+        ok = ok && f != nullptr;
+    };
+    sym(a.create_handle, "rocblas_create_handle");
+    sym(a.destroy_handle, "rocblas_destroy_handle");
+    sym(a.set_atomics_mode, "rocblas_set_atomics_mode");
+    sym(a.set_stream, "rocblas_set_stream");
+    sym(a.sgemm, "rocblas_sgemm");
+    sym(a.gemm_ex, "rocblas_gemm_ex");
+    if (!ok) return false;
+    g_rb = a;
+    g_rb_loaded = true;
+    return true;
+}
+}  // namespace
 
 // Workspace of the forward for training and the backward pass, allocated at
 // the first lstm_dyn_forward_train of a handle.
@@ -67,7 +109,8 @@ struct lstm_dyn {
     unsigned long long timeout_ticks;
     int inproj_grid;
     long long launches_last;
-    hipStream_t last_stream;
+    hipStream_t last_stream;   // the stream of the last forward or backward
+    int has_work;              // 1 once work has been enqueued on last_stream
     int timing;                // record phase events on the forward's stream
     unsigned long long* trace; // per-step timestamps (diagnostics), [T + 1], or null
     int wclk_khz;
@@ -376,6 +419,7 @@ extern "C" int lstm_dyn_create_cell(lstm_dyn_t** out, int B, int D, int H, int T
     }
     h->launches_last = 0;
     h->last_stream = nullptr;
+    h->has_work = 0;
     h->timing = 0;
     h->trace = nullptr;
     h->wclk_khz = wclk_khz;
@@ -407,7 +451,10 @@ extern "C" int lstm_dyn_set_option(lstm_dyn_t* h, int option, long long value) {
                 return LSTM_DYN_ERR_NOMEM;
             }
         } else if (!value && h->trace) {
-            if (hipDeviceSynchronize() != hipSuccess || hipFree(h->trace) != hipSuccess) return LSTM_DYN_ERR_HIP;
+            // the last forward may still write the trace
+            if ((h->has_work && hipStreamSynchronize(h->last_stream) != hipSuccess) ||
+                hipFree(h->trace) != hipSuccess)
+                return LSTM_DYN_ERR_HIP;
             h->trace = nullptr;
         }
         return LSTM_DYN_OK;
@@ -432,14 +479,16 @@ extern "C" int lstm_dyn_step_trace(lstm_dyn_t* h, long long* ticks, int capacity
 extern "C" int lstm_dyn_destroy(lstm_dyn_t* h) {
     if (!h) return LSTM_DYN_OK;
     int rc = LSTM_DYN_OK;
-    if (hipDeviceSynchronize() != hipSuccess) rc = LSTM_DYN_ERR_HIP;
+    // One forward or backward may be in flight per handle, on the stream it
+    // was issued on: wait for that stream only, not for the whole device.
+    if (h->has_work && hipStreamSynchronize(h->last_stream) != hipSuccess) rc = LSTM_DYN_ERR_HIP;
     if (h->block && hipFree(h->block) != hipSuccess) rc = LSTM_DYN_ERR_HIP;
     for (auto& e : h->ev)
         if (e && hipEventDestroy(e) != hipSuccess) rc = LSTM_DYN_ERR_HIP;
     if (h->host_maxlen && hipHostFree(h->host_maxlen) != hipSuccess) rc = LSTM_DYN_ERR_HIP;
     if (h->trace && hipFree(h->trace) != hipSuccess) rc = LSTM_DYN_ERR_HIP;
     if (h->train) {
-        if (h->train->rb && rocblas_destroy_handle(h->train->rb) != rocblas_status_success)
+        if (h->train->rb && g_rb.destroy_handle(h->train->rb) != rocblas_status_success)
             rc = LSTM_DYN_ERR_HIP;
         if (h->train->block && hipFree(h->train->block) != hipSuccess) rc = LSTM_DYN_ERR_HIP;
         if (h->train->host_offsets && hipHostFree(h->train->host_offsets) != hipSuccess)
@@ -473,6 +522,7 @@ static int forward_impl(lstm_dyn_t* h, const void* x, const int32_t* lengths, co
                         void* stream) {
     hipStream_t s = static_cast<hipStream_t>(stream);
     h->last_stream = s;
+    h->has_work = 1;
     h->launches_last = 0;
     h->saved = 0;  // this forward overwrites what a forward for training kept
     const Dims& d = h->dims;
@@ -506,7 +556,7 @@ static int forward_impl(lstm_dyn_t* h, const void* x, const int32_t* lengths, co
         h->launches_last = 1 + pack_launches;
         LD_CHECK(mark(3));
         if (out_seq) {
-            LD_CHECK(launch_seq_finish(d, out_seq, false, 4, seq_ends, h->ws, h->num_cus, s));
+            LD_CHECK(launch_seq_finish(d, out_seq, seq_ends, h->num_cus, s));
             h->launches_last++;
         }
         return LSTM_DYN_OK;
@@ -524,7 +574,7 @@ static int forward_impl(lstm_dyn_t* h, const void* x, const int32_t* lengths, co
         h->launches_last++;
         LD_CHECK(mark(3));
         if (out_seq) {  // the loop wrote the valid steps; zeros past each row's last
-            LD_CHECK(launch_seq_finish(d, out_seq, false, 4, seq_ends, h->ws, h->num_cus, s));
+            LD_CHECK(launch_seq_finish(d, out_seq, seq_ends, h->num_cus, s));
             h->launches_last++;
         }
         return LSTM_DYN_OK;
@@ -567,7 +617,7 @@ static int forward_impl(lstm_dyn_t* h, const void* x, const int32_t* lengths, co
     }
     LD_CHECK(mark(3));
     if (out_seq) {
-        LD_CHECK(launch_seq_finish(d, out_seq, false, 4, seq_ends, h->ws, h->num_cus, s));
+        LD_CHECK(launch_seq_finish(d, out_seq, seq_ends, h->num_cus, s));
         h->launches_last++;
     }
 #undef LD_CHECK
@@ -734,8 +784,8 @@ static int ensure_train(lstm_dyn* h) {
     }
     // no atomics in rocBLAS's kernels: the same inputs give the same
     // gradients bit for bit
-    if (rocblas_create_handle(&tw->rb) != rocblas_status_success ||
-        rocblas_set_atomics_mode(tw->rb, rocblas_atomics_not_allowed) != rocblas_status_success) {
+    if (!load_rocblas() || g_rb.create_handle(&tw->rb) != rocblas_status_success ||
+        g_rb.set_atomics_mode(tw->rb, rocblas_atomics_not_allowed) != rocblas_status_success) {
         (void)hipFree(tw->block);
         (void)hipHostFree(tw->host_offsets);
         delete tw;
@@ -763,6 +813,7 @@ extern "C" int lstm_dyn_forward_train(lstm_dyn_t* h, const void* x, const int32_
     TrainWs* tw = h->train;
     hipStream_t s = static_cast<hipStream_t>(stream);
     h->last_stream = s;
+    h->has_work = 1;
     h->launches_last = 0;
     h->saved = 0;
     const Dims& d = h->dims;
@@ -897,6 +948,7 @@ extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* le
     TrainWs* tw = h->train;
     hipStream_t s = static_cast<hipStream_t>(stream);
     h->last_stream = s;
+    h->has_work = 1;
     h->launches_last = 0;
     h->saved = 0;  // the backward overwrites the kept pre-activations
     const Dims& d = h->dims;
@@ -912,7 +964,7 @@ extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* le
     do {                                               \
         if ((call) != rocblas_status_success) return LSTM_DYN_ERR_HIP; \
     } while (0)
-    RB_CHECK(rocblas_set_stream(tw->rb, s));
+    RB_CHECK(g_rb.set_stream(tw->rb, s));
     LD_CHECK(launch_bwd_weights(d, W, d.D, tw->w_il, s));
     LD_CHECK(launch_bwd_weights(d, U, d.H, tw->u_il, s));
     h->launches_last += 2;
@@ -942,7 +994,7 @@ extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* le
             LD_CHECK(launch_bwd_cell(d, t, off[t], act, tw->save_h, tw->save_c, d_seq, tw->dH,
                                      tw->dC, h->ws, s));
             // dH[0:act] (+)= dz_t U^T (column-major: dH^T = U_il^T-as-stored^T dz_t^T)
-            RB_CHECK(rocblas_sgemm(tw->rb, rocblas_operation_transpose, rocblas_operation_none, d.H,
+            RB_CHECK(g_rb.sgemm(tw->rb, rocblas_operation_transpose, rocblas_operation_none, d.H,
                                    act, H4, &one, tw->u_il, H4, h->ws.gx + (size_t)off[t] * H4, H4,
                                    &beta, tw->dH, d.H));
             h->launches_last += 2;
@@ -975,7 +1027,7 @@ extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* le
             const int act = off[t + 1] - off[t];
             LD_CHECK(launch_bwd_cell16(d, t, off[t], act, tw->save_h, tw->save_c, d_seq, tw->dH,
                                        tw->dC, tw->srow, tw->dzs16, h->ws, s));
-            RB_CHECK(rocblas_gemm_ex(tw->rb, rocblas_operation_transpose, rocblas_operation_none,
+            RB_CHECK(g_rb.gemm_ex(tw->rb, rocblas_operation_transpose, rocblas_operation_none,
                                      d.H, act, H4, &alpha_u, tw->u16, rocblas_datatype_f16_r, H4,
                                      tw->dzs16, rocblas_datatype_f16_r, H4, &beta, tw->dH,
                                      rocblas_datatype_f32_r, d.H, tw->dH, rocblas_datatype_f32_r,
@@ -993,12 +1045,12 @@ extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* le
             LD_CHECK(launch_bwd_colsum(h->ws.gx, rows, H4, tw->cs_part, tw->db_il, nullptr, 1.0f, s));
             h->launches_last += 2;
             // dW = X^T dz, dU = H_prev^T dz, then dx rows = dz W^T over the gathered x
-            RB_CHECK(rocblas_sgemm(tw->rb, rocblas_operation_none, rocblas_operation_transpose, H4,
+            RB_CHECK(g_rb.sgemm(tw->rb, rocblas_operation_none, rocblas_operation_transpose, H4,
                                    d.D, rows, &one, h->ws.gx, H4, tw->xc, d.D, &zero, tw->dw_il, H4));
-            RB_CHECK(rocblas_sgemm(tw->rb, rocblas_operation_none, rocblas_operation_transpose, H4,
+            RB_CHECK(g_rb.sgemm(tw->rb, rocblas_operation_none, rocblas_operation_transpose, H4,
                                    d.H, rows, &one, h->ws.gx, H4, tw->save_h, d.H, &zero, tw->du_il,
                                    H4));
-            RB_CHECK(rocblas_sgemm(tw->rb, rocblas_operation_transpose, rocblas_operation_none, d.D,
+            RB_CHECK(g_rb.sgemm(tw->rb, rocblas_operation_transpose, rocblas_operation_none, d.D,
                                    rows, H4, &one, tw->w_il, H4, h->ws.gx, H4, &zero, tw->xc, d.D));
             h->launches_last += 3;
         } else {
@@ -1023,15 +1075,15 @@ extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* le
             LD_CHECK(launch_bwd_to_f16(tw->w_il, tw->w16, n_w, sw, s));
             const rocblas_datatype f16 = rocblas_datatype_f16_r, f32 = rocblas_datatype_f32_r;
             const float a_w = 1.0f / (sz * sx), a_u = 1.0f / (sz * sh), a_x = 1.0f / (sz * sw);
-            RB_CHECK(rocblas_gemm_ex(tw->rb, rocblas_operation_none, rocblas_operation_transpose, H4,
+            RB_CHECK(g_rb.gemm_ex(tw->rb, rocblas_operation_none, rocblas_operation_transpose, H4,
                                      d.D, rows, &a_w, tw->dz16, f16, H4, tw->x16, f16, d.D, &zero,
                                      tw->dw_il, f32, H4, tw->dw_il, f32, H4, f32,
                                      rocblas_gemm_algo_standard, 0, 0));
-            RB_CHECK(rocblas_gemm_ex(tw->rb, rocblas_operation_none, rocblas_operation_transpose, H4,
+            RB_CHECK(g_rb.gemm_ex(tw->rb, rocblas_operation_none, rocblas_operation_transpose, H4,
                                      d.H, rows, &a_u, tw->dz16, f16, H4, tw->h16, f16, d.H, &zero,
                                      tw->du_il, f32, H4, tw->du_il, f32, H4, f32,
                                      rocblas_gemm_algo_standard, 0, 0));
-            RB_CHECK(rocblas_gemm_ex(tw->rb, rocblas_operation_transpose, rocblas_operation_none, d.D,
+            RB_CHECK(g_rb.gemm_ex(tw->rb, rocblas_operation_transpose, rocblas_operation_none, d.D,
                                      rows, H4, &a_x, tw->w16, f16, H4, tw->dz16, f16, H4, &zero,
                                      tw->xc, f32, d.D, tw->xc, f32, d.D, f32,
                                      rocblas_gemm_algo_standard, 0, 0));

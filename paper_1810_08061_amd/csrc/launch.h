@@ -169,10 +169,9 @@ hipError_t launch_seq_from_saved(const Dims& d, float* seq, const float* save_h,
                                  const int32_t* lengths, const Workspace& ws, int num_cus,
                                  hipStream_t s);
 
-// Output sequence: moves the persistent loop's step outputs (kept in the
-// dead Gx rows, unit slices of upw) to seq [B][T][H] when from_gx, and
-// writes zeros past each length.
-hipError_t launch_seq_finish(const Dims& d, float* seq, bool from_gx, int upw, const int32_t* lengths,
-                             const Workspace& ws, int num_cus, hipStream_t s);
+// Output sequence: zeros past each row's last step (lengths: that step + 1;
+// the loops write the valid steps themselves).
+hipError_t launch_seq_finish(const Dims& d, float* seq, const int32_t* lengths, int num_cus,
+                             hipStream_t s);
 
 }  // namespace ldyn

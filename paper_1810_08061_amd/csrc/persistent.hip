@@ -8,27 +8,30 @@
 // MFMA A-fragments for the whole loop.  Per step t:
 //   1. the KW waves split K = H; each forms partial C^T = U_slice^T h_t^T for
 //      the active rows (slots [0, active(t)) after the length sort), one
-//      16-row tile at a time, with the h fragments of the next two tiles
-//      loading while the current tile's MFMAs run;
-//   2. partials meet in LDS; the owning wave adds them and the prefetched
-//      Gx[t] (input projection + bias), applies the gate non-linearities and
-//      updates c (in its registers) and h; finished rows are not touched (the
-//      per-row select of the paper);
-//   3. it writes its slice of h_{t+1} and arrives at the grid barrier, then
-//      prefetches Gx[t+1] while waiting for the other workgroups.
+//      16-row tile at a time, loading the h fragments of the next tiles while
+//      the current tile's MFMAs run;
+//   2. partials meet in LDS; the wave that owns a row tile adds them and the
+//      prefetched Gx[t] (input projection + bias), applies the gate
+//      non-linearities and updates c and h (in its registers); finished rows
+//      are not touched (the per-row select of the paper);
+//   3. the owner stores the tile's rows of this workgroup's slice of h_{t+1}
+//      and marks the same segments of the buffer that will take h_{t+3} as
+//      not yet written; Gx[t+1] goes to LDS by DMA.
 // The loop bound max_len and active(t) are read on the device; when every row
 // is done the loop ends.
 //
 // Exchange of h between workgroups (they sit on different XCDs, whose L2
 // caches are not coherent with each other): h is stored and loaded with
 // device-scope cache policy (sc1), so stores are written through to the
-// coherence point before a wave's store counter drains and loads are served
-// from it.  A wave drains its stores (s_waitcnt vmcnt(0)) before its
-// workgroup arrives at the barrier, so no L2 write-back or invalidate is
-// needed around the barrier.  The barrier is two-level: workgroups arrive on
-// one of eight group counters, the last arrival of a group bumps the global
-// counter, and every workgroup polls the global counter.  The counters are
-// zeroed by the preparation kernel that runs before this one.
+// coherence point and loads are served from it, with no L2 write-back or
+// invalidate.  There is one grid barrier, at the start (it makes h_0 and the
+// first marks visible); after it the steps synchronise through the data.  h
+// lives in a ring of four buffers, and a segment not yet written for the
+// coming step holds the all-ones pattern, a NaN that the stores never
+// produce.  A reader polls its first row tile of h_t until no active row
+// holds the marker and uses later tiles as loaded; a marker that slipped into
+// an active row shows up as a NaN pre-activation, and the chunk is then redone
+// with every tile polled.  Every wait is bounded (then ERR_TIMEOUT).
 #include "launch.h"
 
 namespace ldyn {

@@ -6,53 +6,28 @@
 // which a row ended, with termination from the state) the output is zero (no
 // value is defined there; zero is the padding convention chosen).
 //
-// The persistent loop leaves the step outputs of compact row r (one valid
-// (b, t), numbered as the input projection numbers them) inside that row's
-// Gx, whose values it no longer needs: unit u of workgroup slice q = u / UPW
-// at float q * 4 UPW + u mod UPW.  This kernel moves those rows to
-// out_seq[b][t] and writes the zeros past each length; the other modes write
-// their valid outputs directly and use it for the zeros only.
+// Every loop writes the valid outputs itself; this kernel writes the zeros
+// past each row's last step.
 #include "launch.h"
 
 namespace ldyn {
 
 struct SeqParams {
     float* seq;              // [B][T][H]
-    const float* gx;         // compact rows with the step outputs inside, or null
-    const int32_t* rowsrc;   // compact row -> b * T + t
-    const Meta* meta;        // total_rows (read only when gx is set)
     const int32_t* lengths;  // [B] last step + 1 of each row: its length as passed, or the
                              // step it ended at (clamped here to [0, T])
-    int B, T, H, upw;
+    int B, T, H;
 };
 
-// One wave per output row; float4 accesses when H is a multiple of 4 (rows of
-// out_seq and of Gx are then 16-byte aligned).
+// One wave per output row; float4 stores when H is a multiple of 4 and
+// out_seq is 16-byte aligned.
 template <bool VEC>
 __global__ void __launch_bounds__(256)
 seq_finish_kernel(SeqParams p) {
     const int lane = threadIdx.x & 63;
     const long wave = ((long)blockIdx.x * 256 + threadIdx.x) >> 6;
     const long nwaves = (long)gridDim.x * 4;
-    const int H = p.H, T = p.T, upw = p.upw;
-    if (p.gx) {
-        const long rows = p.meta->total_rows;
-        for (long r = wave; r < rows; r += nwaves) {
-            // rows at or past a row's last step belong to the zero fill below
-            // (a row that ended before its length has compact rows past it)
-            const int bt = p.rowsrc[r], b = bt / T;
-            if (bt - b * T >= min(max(p.lengths[b], 0), T)) continue;
-            const float* src = p.gx + (size_t)r * 4 * H;
-            float* dst = p.seq + (size_t)bt * H;
-            if constexpr (VEC) {
-                for (int u = 4 * lane; u < H; u += 256)  // u .. u+3 lie in one slice (upw is 4 or 8)
-                    *reinterpret_cast<f32x4_t*>(dst + u) =
-                        *reinterpret_cast<const f32x4_t*>(src + (u / upw) * 4 * upw + u % upw);
-            } else {
-                for (int u = lane; u < H; u += 64) dst[u] = src[(u / upw) * 4 * upw + u % upw];
-            }
-        }
-    }
+    const int H = p.H, T = p.T;
     const long nrows = (long)p.B * T;
     for (long row = wave; row < nrows; row += nwaves) {
         const int b = (int)(row / T), t = (int)(row - (long)b * T);
@@ -101,9 +76,9 @@ hipError_t launch_seq_from_saved(const Dims& d, float* seq, const float* save_h,
     return hipGetLastError();
 }
 
-hipError_t launch_seq_finish(const Dims& d, float* seq, bool from_gx, int upw, const int32_t* lengths,
-                             const Workspace& ws, int num_cus, hipStream_t s) {
-    SeqParams p{seq, from_gx ? ws.gx : nullptr, ws.rowsrc, ws.meta, lengths, d.B, d.T, d.H, upw};
+hipError_t launch_seq_finish(const Dims& d, float* seq, const int32_t* lengths, int num_cus,
+                             hipStream_t s) {
+    SeqParams p{seq, lengths, d.B, d.T, d.H};
     const long rows = (long)d.B * d.T;
     long grid = (rows + 3) / 4;
     if (grid > 8L * num_cus) grid = 8L * num_cus;

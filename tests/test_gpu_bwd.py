@@ -14,6 +14,7 @@ import pytest
 import oracle
 import paper_1810_08061_amd as ld
 import workloads
+from tests import oracle_cache
 from tests.gpu_util import say, to_device
 
 pytestmark = pytest.mark.gpu
@@ -102,12 +103,53 @@ def test_backward_workloads(name, mode):
 
 
 @pytest.mark.parametrize("mode", MODES)
+def test_backward_skewed_workload_full_batch(mode):
+    """skewed1024_bf16, the whole batch: every gradient (dx, dW, dU, db, dh0,
+    dc0) against the oracle's (computed once, shared by both modes)."""
+    name = "skewed1024_bf16"
+    w = workloads.WORKLOADS[name]
+    inp = workloads.workload_inputs(name)
+    dh, dc, ds = upstream(3001, w.B, w.H, w.T)
+    say(f"case bwd workload {name} {mode} (every row)")
+    g, _, _ = run_train(inp, mode, dh, dc, ds)
+    go = oracle_cache.grads((name, 3001), lambda: oracle_grads(
+        inp, dh.astype(np.float64), dc.astype(np.float64), ds.astype(np.float64)))
+    compare(g, go, GRAD_TOL[w.dtype])
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_backward_large_workload_sub_batch(mode):
+    """large2048_bf16 at its full shape (D 1024, H 2048, T_max 1000) on 20 rows
+    spread over its length range (the longest, 1000 steps, and the shortest
+    included), run on their own handle: every gradient against the oracle.
+    The first 64 steps have more than 16 rows (two launches per step on the
+    persistent handle), the rest fewer (its one-launch reverse loop)."""
+    import torch
+    name = "large2048_bf16"
+    full = workloads.workload_inputs(name)
+    rows = oracle_cache.spanning_rows(full.lengths, 20)
+    inp = workloads.Inputs(x=full.x[rows].copy(), lengths=full.lengths[rows].copy(), W=full.W,
+                           U=full.U, b=full.b, h0=full.h0[rows].copy(), c0=full.c0[rows].copy(),
+                           dtype=full.dtype)
+    del full
+    dh, dc, ds = upstream(3002, inp.B, inp.H, inp.T)
+    say(f"case bwd {name} sub-batch {mode} lengths={sorted(inp.lengths.tolist(), reverse=True)}")
+    g, _, m = run_train(inp, mode, dh, dc, ds)
+    m.close()
+    torch.cuda.empty_cache()
+    go = oracle_cache.grads((name, "sub20", 3002), lambda: oracle_grads(
+        inp, dh.astype(np.float64), dc.astype(np.float64), ds.astype(np.float64)))
+    compare(g, go, GRAD_TOL[inp.dtype])
+
+
+@pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("name", ["skewed1024_bf16", "large2048_bf16"])
-def test_backward_large_workloads(name, mode):
-    """Full-size workloads: the per-row gradients (dx, dh0, dc0) of a few short
-    rows against the oracle run on those rows alone (rows are independent);
-    the weight gradients as the sums of the gradients of two halves of the
-    batch, each run on its own handle."""
+def test_backward_large_workloads_halves(name, mode):
+    """Full-size workloads on the whole batch (beside the oracle checks
+    above): the per-row gradients (dx, dh0, dc0) of a few short rows against
+    the oracle run on those rows alone (rows are independent); the weight
+    gradients against the sums of the gradients of two halves of the batch,
+    each run on its own handle."""
     import torch
     w = workloads.WORKLOADS[name]
     inp = workloads.workload_inputs(name)

@@ -77,25 +77,37 @@ def test_largest_per_step_batch():
 
 @pytest.mark.parametrize("dt", ["bf16", "f32"])
 def test_largest_persistent_batch_backward(dt):
-    """The backward at 512 rows: the per-row gradients of sampled rows against
-    the oracle run on those rows alone, every gradient against the per-step
-    handle's (the two paths share no per-step code with bf16 data: the
-    persistent handle runs the one-launch reverse loop for its steps with at
-    most 16 rows)."""
+    """The backward at 512 rows, most of them short: steps 3 to 5 have at
+    most 16 rows, so with bf16 data the persistent handle runs them in its
+    one-launch reverse loop (fewer launches than the per-step handle, which
+    runs every step as two launches).  Per-row gradients of sampled rows
+    against the oracle run on those rows alone; every gradient against the
+    per-step handle's."""
     import torch
     from tests.test_gpu_bwd import GRAD_TOL, compare, oracle_grads, run_train, scaled_err
     B, D, H, T = 512, 24, 256, 6
     inp = workloads.random_case(4200, B, D, H, T, dtype=dt)
     rng = np.random.default_rng(4201)
+    L = rng.integers(1, 4, B).astype(np.int32)
+    L[rng.choice(B, size=16, replace=False)[:12]] = 6
+    L[np.flatnonzero(L < 4)[:4]] = 5
+    inp.lengths = L
+    active = [(L > t).sum() for t in range(T)]
+    assert active[3] <= 16 and active[4] <= 16 and active[5] <= 16 and active[2] > 16
     dh = rng.standard_normal((B, H)).astype(np.float32)
     dc = rng.standard_normal((B, H)).astype(np.float32)
     ds = rng.standard_normal((B, T, H)).astype(np.float32)
-    say(f"case limit backward {(B, D, H, T, dt)}")
+    say(f"case limit backward {(B, D, H, T, dt)} rows per step {active}")
     g, _, m = run_train(inp, "persistent", dh, dc, ds)
-    rows = _sample(inp)
+    launches = m.query(ld.Q_LAUNCHES_PER_FORWARD)
+    rows = _sample(inp) + [int(r) for r in np.flatnonzero(L == 6)[:2]]
     go = oracle_grads(inp, dh.astype(np.float64), dc.astype(np.float64), ds.astype(np.float64), rows)
     compare({k: g[k][rows] for k in ("dx", "dh0", "dc0")}, go, GRAD_TOL[dt], keys=("dx", "dh0", "dc0"))
     gs, _, ms = run_train(inp, "per_step", dh, dc, ds)
+    per_step = ms.query(ld.Q_LAUNCHES_PER_FORWARD)
+    say(f"  backward launches: persistent {launches}, per-step {per_step}")
+    if dt == "bf16":
+        assert launches < per_step
     for k in g:
         e = scaled_err(g[k], gs[k])
         say(f"  {k} against the per-step path: {e:.2e}")
@@ -103,3 +115,45 @@ def test_largest_persistent_batch_backward(dt):
     m.close()
     ms.close()
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("mode", ["persistent", "per_step"])
+def test_largest_persistent_batch_sequence(mode):
+    """The output sequence at 512 rows (the slot-to-row map of the persistent
+    loop at its bound): sampled rows against the oracle, zeros past every
+    row's length, the last valid step equal to the final h."""
+    import torch
+    from tests.test_gpu_seq import _check_padding_and_last, run_seq
+    B, D, H, T = 512, 40, 2048, 5
+    inp = workloads.random_case(4300, B, D, H, T, dtype="bf16")
+    say(f"case limit sequence {(B, D, H, T)} {mode}")
+    h, c, seq, m = run_seq(inp, mode)
+    assert m.query(ld.Q_LAST_STATUS) == ld.OK
+    h, c, seq = h.cpu().numpy(), c.cpu().numpy(), seq.cpu().numpy()
+    _check_padding_and_last(seq, h, inp.lengths)
+    rows = _sample(inp)
+    ho, co, so = oracle.forward_inputs(inp, rows=rows, seq=True)
+    es, eh, ec = max_err(seq[rows], so), max_err(h[rows], ho), max_err(c[rows], co)
+    say(f"  sampled rows: max|dseq|={es:.3g} max|dh|={eh:.3g} max|dc|={ec:.3g}")
+    assert es <= TOL["bf16"] and eh <= TOL["bf16"] and ec <= TOL["bf16"]
+    m.close()
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("mode", ["persistent", "per_step"])
+def test_largest_persistent_batch_stop_with_sequence(mode):
+    """Termination from the state with the output sequence at 512 rows:
+    sampled rows checked as in the stop tests (exact step counts away from
+    near ties, state and sequence against the oracle)."""
+    from tests.test_gpu_stop import _readout, check_against_oracle, run_stop
+    B, D, H, T = 512, 40, 2048, 5
+    inp = workloads.random_case(4400, B, D, H, T, dtype="bf16")
+    v, c = _readout(4401, H, -0.1)
+    say(f"case limit stop+sequence {(B, D, H, T)} {mode}")
+    h, cs, steps, seq, iters, m = run_stop(inp, "lstm", mode, v, c, seq=True)
+    rows = _sample(inp)
+    ties = check_against_oracle("lstm", inp, v, c, h, cs, steps, seq, iters, TOL["bf16"], rows=rows)
+    early = int((steps < inp.lengths).sum())
+    say(f"  rows ended early: {early}/{B}, iters={iters}, near-ties={ties}")
+    assert iters == int(steps.max())
+    m.close()

@@ -20,6 +20,7 @@ import pytest
 import oracle
 import paper_1810_08061_amd as ld
 import workloads
+from tests import oracle_cache
 from tests.gpu_util import max_err, say, to_device
 from tests.test_gpu_cells import gru_device
 
@@ -142,7 +143,7 @@ def test_stop_small_shapes(shape, mode, cell):
 @pytest.mark.parametrize("name", workloads.ORDER)
 def test_stop_workloads(name, mode, cell):
     """The workload shapes; many rows end before their caps, others run to
-    them (c chosen so).  large2048_bf16 on sampled rows."""
+    them (c chosen so).  large2048_bf16 on 16 rows spread over its lengths."""
     w = workloads.WORKLOADS[name]
     inp = workloads.workload_inputs(name) if cell == "lstm" else workloads.cell_workload_inputs(cell, name)
     v, c = _readout(900, w.H, -0.5)
@@ -150,9 +151,9 @@ def test_stop_workloads(name, mode, cell):
     h, cs, steps, seq, iters, m = run_stop(inp, cell, mode, v, c, seq=False)
     rows = None
     if name == "large2048_bf16":
-        L = inp.lengths
-        order = np.argsort(-L, kind="stable")
-        rows = sorted({int(order[0]), int(order[-1]), int(order[len(order) // 2]), 5, 100})
+        # 16 rows spread over the length range (the oracle's score trace of
+        # every row would take 4 GB per cell and mode)
+        rows = oracle_cache.spanning_rows(inp.lengths, 16)
     ties = check_against_oracle(cell, inp, v, c, h, cs, steps, None, iters, w.tol, rows=rows)
     early = int((steps < np.clip(inp.lengths, 0, inp.T)).sum())
     say(f"  rows ended early: {early}/{inp.B}, iters={iters} (cap {int(inp.lengths.max())}), near-ties={ties}")
