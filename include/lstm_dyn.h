@@ -91,7 +91,8 @@ enum {
     LSTM_DYN_ERR_NOMEM = 3,       /* device workspace allocation failed */
     LSTM_DYN_ERR_UNSUPPORTED = 4, /* sizes outside what the compiled kernel variants cover */
     LSTM_DYN_ERR_BAD_LENGTHS = 5, /* (device status) a length was outside [0, T_max] and was clamped */
-    LSTM_DYN_ERR_TIMEOUT = 6      /* (device status) a grid barrier wait exceeded its bound */
+    LSTM_DYN_ERR_TIMEOUT = 6,     /* (device status) a grid barrier wait exceeded its bound */
+    LSTM_DYN_ERR_TOO_LARGE = 7    /* lstm_dyn_forward_noalloc: the workspace exceeds its scratch */
 };
 
 /* lstm_dyn_query selectors. */
@@ -344,6 +345,35 @@ int lstm_dyn_check_backward_args(int B, int D, int H, int T_max, int dtype, int 
                                  const float* d_out_h, const float* d_out_c, const float* d_seq,
                                  const float* dx, const float* dW, const float* dU,
                                  const float* db, const float* dh0, const float* dc0);
+
+/*
+ * lstm_dyn_forward_noalloc: lstm_dyn_forward (LSTM cell, PERSISTENT mode)
+ * without a handle, for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation.  It calls no hipMalloc, hipFree or other allocating routine;
+ * the workspace lies in a fixed scratch array inside the library of
+ * LSTM_DYN_NOALLOC_SCRATCH_BYTES on every device it runs on (held until the
+ * process ends).  Sizes whose workspace (the input projection of all B *
+ * T_max steps, 16 H bytes each, plus the tables and the hidden-state
+ * buffers) does not fit return LSTM_DYN_ERR_TOO_LARGE before any work is
+ * enqueued; with bf16 data, B = 64 and H = 512 fit up to T_max = 200.
+ *   Arguments, layouts and results as for lstm_dyn_forward on a handle
+ *   created with lstm_dyn_create(B, D, H, T_max, dtype, LSTM_DYN_PERSISTENT)
+ *   (the same kernels: the results are the same bits).  status: NULL, or a
+ *   caller-owned device int32 that receives the forward's device status
+ *   (LSTM_DYN_OK, ERR_BAD_LENGTHS or ERR_TIMEOUT) when the work on the
+ *   stream completes; it must not overlap any other argument.
+ *   Returns LSTM_DYN_OK, ERR_INVALID (as lstm_dyn_forward's checks),
+ *   ERR_UNSUPPORTED, ERR_TOO_LARGE or ERR_HIP.
+ * Every call on one device uses that device's one scratch array: calls whose
+ * work overlaps on one device (two streams, two host threads) race and give
+ * undefined results; calls in order on one stream are safe.
+ */
+#define LSTM_DYN_NOALLOC_SCRATCH_BYTES (128LL << 20)
+int lstm_dyn_forward_noalloc(int B, int D, int H, int T_max, int dtype, const void* x,
+                             const int32_t* lengths, const void* W, const void* U, const float* b,
+                             const float* h0, const float* c0, float* out_h, float* out_c,
+                             int32_t* status, void* stream);
 
 #ifdef __cplusplus
 }

@@ -21,7 +21,8 @@ __all__ = [
     "lstm_dyn_step_trace", "lstm_dyn_forward_seq", "lstm_dyn_check_seq_args",
     "lstm_dyn_create_cell", "lstm_dyn_check_cell_args", "CELL_LSTM", "CELL_GRU", "CELL_RNN",
     "lstm_dyn_forward_stop", "lstm_dyn_check_stop_args", "lstm_dyn_forward_train",
-    "lstm_dyn_backward", "lstm_dyn_check_backward_args",
+    "lstm_dyn_backward", "lstm_dyn_check_backward_args", "lstm_dyn_forward_noalloc",
+    "NOALLOC_SCRATCH_BYTES",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -30,7 +31,9 @@ _LIB_PATH = os.path.join(_HERE, "liblstm_dyn.so")
 F32, BF16 = 0, 1
 PERSISTENT, PER_STEP = 0, 1
 CELL_LSTM, CELL_GRU, CELL_RNN = 0, 1, 2
-OK, ERR_INVALID, ERR_HIP, ERR_NOMEM, ERR_UNSUPPORTED, ERR_BAD_LENGTHS, ERR_TIMEOUT = range(7)
+OK, ERR_INVALID, ERR_HIP, ERR_NOMEM, ERR_UNSUPPORTED, ERR_BAD_LENGTHS, ERR_TIMEOUT, \
+    ERR_TOO_LARGE = range(8)
+NOALLOC_SCRATCH_BYTES = 128 << 20   # LSTM_DYN_NOALLOC_SCRATCH_BYTES
 Q_LAST_STATUS, Q_STEPS_EXECUTED, Q_LAUNCHES_PER_FORWARD, Q_GROUPS, Q_WORKSPACE_BYTES, \
     Q_TOTAL_ROWS, Q_TIME_PREP_NS, Q_TIME_INPROJ_NS, Q_TIME_LOOP_NS = range(9)
 OPT_TIMING, OPT_STEP_TRACE, OPT_TIMEOUT_US = 0, 1, 2
@@ -88,6 +91,8 @@ def _load():
     lib.lstm_dyn_check_backward_args.argtypes = [I] * 6 + [P] * 16
     lib.lstm_dyn_check_backward_args.restype = I
     lib.lstm_dyn_forward.argtypes = [P] * 11
+    lib.lstm_dyn_forward_noalloc.argtypes = [I] * 5 + [P] * 11
+    lib.lstm_dyn_forward_noalloc.restype = I
     lib.lstm_dyn_forward.restype = I
     lib.lstm_dyn_forward_seq.argtypes = [P] * 12
     lib.lstm_dyn_forward_seq.restype = I
@@ -139,6 +144,15 @@ def lstm_dyn_forward(handle: int, x: int, lengths: int, W: int, U: int, b: int, 
     rc = _load().lstm_dyn_forward(handle, x, lengths, W, U, b, h0, c0, out_h, out_c, stream)
     if rc != OK:
         raise LstmDynError(rc, "lstm_dyn_forward")
+
+
+def lstm_dyn_forward_noalloc(B: int, D: int, H: int, T_max: int, dtype: int, x: int, lengths: int,
+                             W: int, U: int, b: int, h0: int, c0: int, out_h: int, out_c: int,
+                             status: int = 0, stream: int = 0) -> None:
+    rc = _load().lstm_dyn_forward_noalloc(B, D, H, T_max, dtype, x, lengths, W, U, b, h0, c0,
+                                          out_h, out_c, status, stream)
+    if rc != OK:
+        raise LstmDynError(rc, "lstm_dyn_forward_noalloc")
 
 
 def lstm_dyn_forward_seq(handle: int, x: int, lengths: int, W: int, U: int, b: int, h0: int,

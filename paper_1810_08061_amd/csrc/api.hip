@@ -184,6 +184,33 @@ bool overlaps(const void* a, long long na, const void* b, long long nb) {
 
 }  // namespace
 
+namespace ldyn {
+// The workspace of a persistent-mode LSTM forward inside caller memory at
+// base (256-byte aligned): fills ws and returns the bytes used, and the
+// operand buffer's offset and size (the only part that must start at zero
+// on every forward: its padding columns are multiplied by zero weights).
+long long carve_forward_workspace(const Dims& d, char* base, Workspace* ws, long long* hx_off,
+                                  long long* hx_bytes) {
+    const Layout L = layout_of(d.B, d.D, d.H, d.T, d.bf16, LSTM_DYN_PERSISTENT, d.bpad, d.hpad, 0);
+    *hx_off = L.hx;
+    *hx_bytes = L.bar - L.hx;
+    if (base) {
+        *ws = Workspace{};
+        ws->meta = reinterpret_cast<Meta*>(base + L.meta);
+        ws->perm = reinterpret_cast<int32_t*>(base + L.perm);
+        ws->offsets = reinterpret_cast<int32_t*>(base + L.offsets);
+        ws->rowsrc = reinterpret_cast<int32_t*>(base + L.rowsrc);
+        ws->gx = reinterpret_cast<float*>(base + L.gx);
+        ws->hx = base + L.hx;
+        ws->bar = reinterpret_cast<unsigned*>(base + L.bar);
+        ws->wt = d.bf16 ? base + L.wt : nullptr;
+        ws->stopped = reinterpret_cast<int32_t*>(base + L.stopped);
+        ws->running = reinterpret_cast<int32_t*>(base + L.running);
+    }
+    return L.total;
+}
+}  // namespace ldyn
+
 extern "C" const char* lstm_dyn_strerror(int status) {
     switch (status) {
         case LSTM_DYN_OK: return "ok";
@@ -193,6 +220,8 @@ extern "C" const char* lstm_dyn_strerror(int status) {
         case LSTM_DYN_ERR_UNSUPPORTED: return "sizes not covered by the compiled kernel variants";
         case LSTM_DYN_ERR_BAD_LENGTHS: return "a sequence length was outside [0, T_max] and was clamped";
         case LSTM_DYN_ERR_TIMEOUT: return "a grid barrier wait exceeded its bound";
+        case LSTM_DYN_ERR_TOO_LARGE:
+            return "the workspace exceeds the allocation-free entry point's fixed scratch";
         default: return "unknown status";
     }
 }

@@ -45,6 +45,11 @@ hipError_t launch_cell_pack(const Dims& d, const void* W, const void* U, const f
 // per-step active counts and compact row offsets, compact row sources.
 hipError_t launch_prep(const Dims& d, const int32_t* lengths, const Workspace& ws, hipStream_t s);
 
+// The workspace of a persistent-mode LSTM forward carved from caller memory
+// (api.hip): returns its bytes; fills ws when base is not null.
+long long carve_forward_workspace(const Dims& d, char* base, Workspace* ws, long long* hx_off,
+                                  long long* hx_bytes);
+
 // Input projection over all valid (b, t): gx[r][c'] = x[rowsrc[r]] . W[:, col(c')] + b[col(c')].
 hipError_t launch_inproj(const Dims& d, const void* x, const void* W, const float* b,
                          const Workspace& ws, int grid, hipStream_t s);

@@ -27,7 +27,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_strerror_covers_codes():
-    for code in range(7):
+    for code in range(8):
         assert ld.lstm_dyn_strerror(code) not in ("", "unknown status")
     assert ld.lstm_dyn_strerror(99) == "unknown status"
 
