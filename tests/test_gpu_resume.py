@@ -2,8 +2,9 @@
 forward over [t1, T) that starts from the carried state (h, c) with the
 remaining lengths max(L - t1, 0) and x shifted by t1, gives the state of one
 forward over the whole sequence (the loop's state is all it carries from one
-step to the next).  Compared with the single run within the workload's
-tolerance, and with the oracle."""
+step to the next).  Compared with the single run bit for bit (no kernel's
+arithmetic for a row depends on the other rows), and with the oracle within
+the workload's tolerance."""
 import numpy as np
 import pytest
 
@@ -58,7 +59,9 @@ def test_chunked_resume_equals_one_run(case, mode):
     eh, ec = max_err(h2, h_full), max_err(c2, c_full)
     same = np.array_equal(bits(h2), bits(h_full)) and np.array_equal(bits(c2), bits(c_full))
     say(f"  resumed vs one run: max|dh|={eh:.3g} max|dc|={ec:.3g} bitwise={same}")
-    assert eh <= tol and ec <= tol
+    # every kernel computes a row the same way whatever the other rows, and
+    # the carried state is the loop's own fp32 state: the same bits
+    assert same, (eh, ec)
     ho, co = oracle.forward_inputs(inp)
     assert max_err(h2, ho) <= tol and max_err(c2, co) <= tol
     # rows that end within the first chunk are untouched by the second
