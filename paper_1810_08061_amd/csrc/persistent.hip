@@ -219,14 +219,24 @@ __device__ inline unsigned hx_off(int s, int k, int hpad) {
 }
 
 // Dynamic LDS of one workgroup during the loop: partial sums of NTC row tiles
-// ([KW][NTC][MT][64 lanes][4 floats]) followed by the prefetched Gx of the
-// owned pairs ([NST][KW][64 lanes][4 floats]).
+// ([KW][NTC][MT][64 lanes][4 floats]) followed by the prefetched Gx of G of
+// each wave's owned row tiles ([G][MT][KW][64 lanes][4 floats]).  When the
+// Gx of every owned tile fits next to the partial sums, all are staged at
+// once; otherwise (G < NOT) a chunk is G * KW row tiles, so it holds exactly
+// G owned tiles of each wave, and the Gx of an owned tile goes into the slot
+// of the tile G before it once that one is committed.  For eight waves of two
+// gate tiles this makes a chunk 8 row tiles instead of 7 (two chunks per
+// step at 256 rows instead of three).
 template <int MT, int KW, int NST>
 struct PLayout {
-    static constexpr int GX_KB = NST * KW;
-    static constexpr int NTC = (P_LDS_KB - GX_KB) / (KW * MT);  // row tiles per chunk
+    static constexpr int NOT = NST / MT;                        // owned row tiles per wave
+    static constexpr int GMAX = P_LDS_KB / (KW * MT * (KW + 1));
+    static constexpr int G = NOT <= GMAX ? NOT : GMAX;          // owned tiles with a Gx slot
+    static constexpr int GX_KB = G * MT * KW;
+    static constexpr int NTC = NOT <= GMAX ? (P_LDS_KB - GX_KB) / (KW * MT) : G * KW;  // row tiles per chunk
     static constexpr int GX_OFF = NTC * KW * MT * 256;          // in floats
     static constexpr int BYTES = (NTC * KW * MT + GX_KB) * 1024;
+    static_assert(GMAX >= 1, "no room for the Gx of one owned tile");
 };
 
 template <typename E, int MT, int KSW, int KW, int NST, int CELL, int LMODE>
@@ -409,7 +419,7 @@ persistent_kernel(PersistParams p) {
             const int s = nt * 16 + (lo & 15), u = u0 + mt * 4 + (lo >> 4);
             const bool ok = s < act && u < H;
             const float* src = p.gx + (ok ? (size_t)(off + s) * H4 + 4 * u : 0);
-            __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)(gxs + (a * MT + mt) * KW * 256),
+            __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)(gxs + ((a % LY::G) * MT + mt) * KW * 256),
                                              16, 0, 0);
         }
     };
@@ -429,7 +439,7 @@ persistent_kernel(PersistParams p) {
     if (max_len > 0) {
         grid_arrive(p, 0);
 #pragma unroll
-        for (int a = 0; a < NOT; ++a)
+        for (int a = 0; a < LY::G; ++a)
             if ((a * KW + w) * 16 < o1 - o0) prefetch_tile(a, o0, o1 - o0);
         alive = grid_wait(p, 0, &lds_ok);
     }
@@ -698,7 +708,7 @@ persistent_kernel(PersistParams p) {
 #pragma unroll
                         for (int ww = 0; ww < KW; ++ww)
                             pv[ww] = *reinterpret_cast<const f32x4_t*>(lds + ((((ww * NTC + j) * MT + mt) * 64 + lo) << 2));
-                        pv[KW] = *reinterpret_cast<const f32x4_t*>(gxs + i * KW * 256 + 4 * lo);
+                        pv[KW] = *reinterpret_cast<const f32x4_t*>(gxs + ((a % LY::G) * MT + mt) * KW * 256 + 4 * lo);
 #pragma unroll
                         for (int span = 1; span <= KW; span *= 2)
 #pragma unroll
@@ -773,6 +783,11 @@ persistent_kernel(PersistParams p) {
                     if (lo < 16 && nt * 16 + lo < act)
                         seg_store(nxt + hx_off<E>(nt * 16 + lo, u0, hpad), &hstage[w][lo * UPW]);
                     __builtin_amdgcn_wave_barrier();
+                    if constexpr (LY::G < NOT) {
+                        // the Gx of owned tile a + G (next chunk) into this tile's
+                        // slot, which the gate math of the chunk has read
+                        if (a + LY::G < NOT && ((a + LY::G) * KW + w) * 16 < act) prefetch_tile(a + LY::G, o0, act);
+                    }
                     if (p.seq) {
                         // the output sequence: h of (row, unit) after step t, fp32,
                         // at out_seq[b][t] (a row that has ended keeps storing its
@@ -800,7 +815,7 @@ persistent_kernel(PersistParams p) {
         // of a later chunk waits for every load of this wave.)
         if (t + 1 < max_len) {
 #pragma unroll
-            for (int a = 0; a < NOT; ++a)
+            for (int a = 0; a < LY::G; ++a)
                 if ((a * KW + w) * 16 < act1) prefetch_tile(a, o1, act1);
         }
         // Buffer (t+3) mod 4 still holds h_{t-1}.  This workgroup has seen rows
