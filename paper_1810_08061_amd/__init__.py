@@ -26,7 +26,9 @@ __all__ = [
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_HERE, "liblstm_dyn.so")
+# LSTM_DYN_LIB may name another build of the library (the timing-stress
+# diagnostic build, liblstm_dyn_stress.so); there is no fallback either way
+_LIB_PATH = os.environ.get("LSTM_DYN_LIB") or os.path.join(_HERE, "liblstm_dyn.so")
 
 F32, BF16 = 0, 1
 PERSISTENT, PER_STEP = 0, 1

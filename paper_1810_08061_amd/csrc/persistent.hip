@@ -40,6 +40,26 @@ constexpr int P_LDS_KB = 144;           // dynamic LDS for partial sums and the 
 constexpr int P_MAX_ROWS = 512;         // batch rows the variants hold (8 owned row tiles per wave)
 constexpr int P_SC1 = 16;               // buffer-instruction cache policy: device scope
 
+// Timing stress (a diagnostic build, LDYN_STRESS defined): a wave sleeps for a
+// pseudo-random time (0 to about 1 us, from a hash of the workgroup, wave,
+// step and site) before it stores h, marks segments or starts polling, so
+// the exchange of h is exercised under orders of arrival that the plain
+// build rarely produces.  The plain build compiles it away.
+__device__ inline void stress_delay(int t, int site) {
+#ifdef LDYN_STRESS
+    unsigned x = (unsigned)blockIdx.x * 0x9e3779b1u ^ (unsigned)(threadIdx.x >> 6) * 0x85ebca77u ^
+                 (unsigned)t * 0xc2b2ae3du ^ (unsigned)site * 0x27d4eb2fu;
+    x ^= x >> 15;
+    x *= 0x2c1b3c6du;
+    x ^= x >> 12;
+    const int n = __builtin_amdgcn_readfirstlane((int)(x & 31));
+    for (int i = 0; i < n; ++i) __builtin_amdgcn_s_sleep(1);
+#else
+    (void)t;
+    (void)site;
+#endif
+}
+
 struct PersistParams {
     const void* U;
     const float* h0;
@@ -606,6 +626,7 @@ persistent_kernel(PersistParams p) {
             unsigned ends = 0;       // STOP: owned tiles whose lane row ends before step t
             for (;;) {
                 if (!exact) {
+                    stress_delay(t, 1 + ntc0);
                     load_tile(f0, ntc0);
                     poll_tile(f0, 0);
                     if (tr && ntc0 == 0) p.trace[4 * t + 3] = wall_clock64();
@@ -780,6 +801,7 @@ persistent_kernel(PersistParams p) {
                             u < H ? IO::operand(hst[i]) : E::from_f32(0.0f);
                     }
                     __builtin_amdgcn_wave_barrier();
+                    stress_delay(t, 64 + a);
                     if (lo < 16 && nt * 16 + lo < act)
                         seg_store(nxt + hx_off<E>(nt * 16 + lo, u0, hpad), &hstage[w][lo * UPW]);
                     __builtin_amdgcn_wave_barrier();
@@ -824,6 +846,7 @@ persistent_kernel(PersistParams p) {
         // The marks drain before this wave's h_{t+2} stores of the same
         // segments (the wait before the gate math), so a reader that saw a
         // segment of h_{t+2} then sees its mark in buffer (t+3) mod 4.
+        stress_delay(t, 128);
         mark_owned((unsigned)((t + 3) & 3) * hx_part, o4 - o3);
         o0 = o1;
         o1 = o2;
