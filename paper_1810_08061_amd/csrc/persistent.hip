@@ -762,9 +762,7 @@ persistent_kernel(PersistParams p) {
                 exact = true;
             }
             if (aborted) break;
-            // Commit the owned tiles of the chunk; gather each tile's h rows in
-            // this wave's staging slot and store one segment per active row
-            // (padding units of a ragged last workgroup as zeros).
+            // Commit the owned tiles of the chunk and store their rows of h_{t+1}.
             {
                 int lo = l;
                 asm volatile("" : "+v"(lo));
@@ -797,14 +795,16 @@ persistent_kernel(PersistParams p) {
                             cst[i] = cn[i];
                             hst[i] = hn[i];
                         }
-                        hstage[w][(lo & 15) * UPW + mt * 4 + (lo >> 4)] =
-                            u < H ? IO::operand(hst[i]) : E::from_f32(0.0f);
                     }
-                    __builtin_amdgcn_wave_barrier();
+                    // each lane stores its own elements of h_{t+1} (padding units
+                    // of a ragged last workgroup as zeros); a reader checks every
+                    // element for the marker, so a segment may arrive in parts
                     stress_delay(t, 64 + a);
-                    if (lo < 16 && nt * 16 + lo < act)
-                        seg_store(nxt + hx_off<E>(nt * 16 + lo, u0, hpad), &hstage[w][lo * UPW]);
-                    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+                    for (int mt = 0; mt < MT; ++mt) {
+                        const int s = nt * 16 + (lo & 15), u = u0 + mt * 4 + (lo >> 4);
+                        if (s < act) IO::store(R, nxt + hx_off<E>(s, u, hpad), u < H ? hst[a * MT + mt] : 0.0f);
+                    }
                     if constexpr (LY::G < NOT) {
                         // the Gx of owned tile a + G (next chunk) into this tile's
                         // slot, which the gate math of the chunk has read
