@@ -288,7 +288,11 @@ int lstm_dyn_set_option(lstm_dyn_t* h, int option, long long value);
  * state update and h stores done, first row tile of h_t complete (the end of
  * the wait for the other workgroups) -- then the loop end) into
  * ticks[0 .. capacity), synchronising the forward's stream; *count receives
- * the number of entries and *khz the clock rate.
+ * the number of entries and *khz the clock rate.  A backward pass run as
+ * one launch of the whole reverse loop (bf16 data, persistent handle, H a
+ * multiple of 256) records there instead, at 4 t for step t: its start, the
+ * column blocks' shares of dh published, the first grid barrier passed,
+ * the cells done; at 4 max_len the start of the product for dh0.
  * Returns LSTM_DYN_OK, ERR_INVALID (option not set, NULL arguments) or ERR_HIP.
  */
 int lstm_dyn_step_trace(lstm_dyn_t* h, long long* ticks, int capacity, int* count, int* khz);

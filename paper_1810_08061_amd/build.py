@@ -15,7 +15,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "liblstm_dyn.so")
 LIB_STRESS = os.path.join(HERE, "liblstm_dyn_stress.so")
-SOURCES = ["api.hip", "prep.hip", "gemm.hip", "persistent.hip", "step.hip", "small.hip", "inproj.hip", "seq.hip", "pack.hip", "bwd.hip", "noalloc.hip"]
+SOURCES = ["api.hip", "prep.hip", "gemm.hip", "persistent.hip", "step.hip", "small.hip", "inproj.hip", "seq.hip", "pack.hip", "bwd.hip", "bwdblk.hip", "noalloc.hip"]
 ARCH = "gfx950"
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.environ.get("HIPCC", f"{ROCM}/bin/hipcc")

@@ -79,10 +79,14 @@ struct TrainWs {
     unsigned* amax; // [5] largest magnitudes (float bits) of dz, x, h_prev, W, U
     int32_t* host_offsets;  // pinned [T + 8]: step offsets, the sum of lengths, then amax
     rocblas_handle rb;
-    // the reverse loop in one launch (bf16 data, persistent handles that fit)
-    int loop_groups;        // its workgroups, or 0: two launches per step
+    // the reverse loop in one launch (bf16 data, persistent handles that fit):
+    // all steps with column blocks of U (bwdblk.hip), else the steps with few
+    // rows (bwd.hip) and two launches for each other step
+    int block_groups;       // workgroups of the whole-loop launch, or 0
+    int loop_groups;        // workgroups of the few-row launch, or 0
     _Float16* dzx;          // [2][bpad][kp] each step's published dz
     float* dzs;             // [2][bpad][nblk] their scales
+    float* pdh;             // [4][bpad][H] the column blocks' shares of dh
     unsigned* bar;          // [9 * 64] barrier counters
     long long dzx_bytes, dzs_bytes;
 };
@@ -768,14 +772,21 @@ static int ensure_train(lstm_dyn* h) {
                     oh16 = take(h16 ? 2 * B * T * H : 0), ow16 = take(h16 ? 2 * D * 4 * H : 0),
                     ou16 = take(h16 ? 2 * H * 4 * H : 0), odzs = take(h16 ? 2 * B * 4 * H : 0),
                     osr = take(4 * B), osm = take(256), ocs = take(4LL * BWD_CS_CHUNKS * 4 * H);
-    tw->loop_groups =
-        h16 && h->mode == LSTM_DYN_PERSISTENT ? bwd_loop_fits(h->dims, h->num_cus) : 0;
+    const bool pers16 = h16 && h->mode == LSTM_DYN_PERSISTENT;
+    tw->block_groups = pers16 ? bwd_block_fits(h->dims, h->num_cus) : 0;
+    tw->loop_groups = pers16 && !tw->block_groups ? bwd_loop_fits(h->dims, h->num_cus) : 0;
     int kp = 0, nblk = 0;
     if (tw->loop_groups) bwd_loop_shape((int)H, &kp, &nblk);
+    if (tw->block_groups) {
+        kp = (int)(4 * H);
+        nblk = (int)(H / 8);
+    }
+    const bool one_launch = tw->block_groups || tw->loop_groups;
     tw->dzx_bytes = 2LL * 2 * bpad * kp;
     tw->dzs_bytes = 4LL * 2 * bpad * nblk;
     const long long odzx = take(tw->dzx_bytes), odzsc = take(tw->dzs_bytes),
-                    obar = take(tw->loop_groups ? 9 * 64 * 4 : 0);
+                    opdh = take(tw->block_groups ? 4LL * 4 * bpad * H : 0),
+                    obar = take(one_launch ? 9 * 64 * 4 : 0);
     if (hipMalloc(&tw->block, (size_t)o) != hipSuccess) {
         (void)hipGetLastError();
         delete tw;
@@ -802,9 +813,10 @@ static int ensure_train(lstm_dyn* h) {
     tw->dzs16 = h16 ? reinterpret_cast<_Float16*>(base + odzs) : nullptr;
     tw->srow = reinterpret_cast<float*>(base + osr);
     tw->amax = reinterpret_cast<unsigned*>(base + osm);
-    tw->dzx = tw->loop_groups ? reinterpret_cast<_Float16*>(base + odzx) : nullptr;
-    tw->dzs = tw->loop_groups ? reinterpret_cast<float*>(base + odzsc) : nullptr;
-    tw->bar = tw->loop_groups ? reinterpret_cast<unsigned*>(base + obar) : nullptr;
+    tw->dzx = one_launch ? reinterpret_cast<_Float16*>(base + odzx) : nullptr;
+    tw->dzs = one_launch ? reinterpret_cast<float*>(base + odzsc) : nullptr;
+    tw->pdh = tw->block_groups ? reinterpret_cast<float*>(base + opdh) : nullptr;
+    tw->bar = one_launch ? reinterpret_cast<unsigned*>(base + obar) : nullptr;
     if (hipHostMalloc(reinterpret_cast<void**>(&tw->host_offsets), (size_t)(T + 8) * sizeof(int32_t),
                       hipHostMallocDefault) != hipSuccess) {
         (void)hipFree(tw->block);
@@ -1035,13 +1047,22 @@ extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* le
         const float su = f16_scale(static_cast<unsigned>(off[d.T + 2])), alpha_u = 1.0f / su;
         LD_CHECK(launch_bwd_to_f16(tw->u_il, tw->u16, (long)d.H * H4, su, s));
         h->launches_last++;
-        // The steps with at most BWD_LOOP_ROWS rows (the last ones, taken
-        // first) in one cooperative launch, which leaves dH complete and
-        // unscaled for the step before them; the others two launches each.
+        // The whole reverse loop in one cooperative launch where U splits into
+        // column blocks; else the steps with at most BWD_LOOP_ROWS rows (the
+        // last ones, taken first) in one, which leaves dH complete and
+        // unscaled for the step before them, and the others two launches each.
         int t_end = max_len;
-        if (tw->loop_groups)
+        if (tw->block_groups) {
+            LD_CHECK(hipMemsetAsync(tw->bar, 0, 9 * 64 * sizeof(unsigned), s));
+            LD_CHECK(launch_bwd_block(d, tw->u16, alpha_u, tw->save_h, tw->save_c, d_seq, tw->dH, tw->dC,
+                                      tw->dzx, tw->dzs, tw->pdh, tw->bar, h->timeout_ticks, h->trace,
+                                      h->ws, s));
+            h->launches_last++;
+            t_end = 0;
+        } else if (tw->loop_groups) {
             while (t_end > 0 && off[t_end] - off[t_end - 1] <= BWD_LOOP_ROWS) --t_end;
-        if (t_end < max_len) {
+        }
+        if (!tw->block_groups && t_end < max_len) {
             LD_CHECK(hipMemsetAsync(tw->dzx, 0, (size_t)tw->dzx_bytes, s));
             LD_CHECK(hipMemsetAsync(tw->dzs, 0, (size_t)tw->dzs_bytes, s));
             LD_CHECK(hipMemsetAsync(tw->bar, 0, 9 * 64 * sizeof(unsigned), s));

@@ -52,49 +52,6 @@ bwd_init_kernel(const float* __restrict__ dh_out, const float* __restrict__ dc_o
     }
 }
 
-// The backward of one cell step for one (row, unit), from its pre-activations
-// z (the four gate blocks of the packed layout), the state the step started
-// from (hp, cp) and the gradients of the state after it (dh, dc).  Returns dz
-// and sets the gradient reaching the previous state other than through
-// dz U^T: dc_prev (LSTM) and dh_direct (GRU: h' depends on h through u).
-template <int CELL>
-__device__ inline f32x4_t cell_backward(f32x4_t z, float hp, float cp, float dh, float dc,
-                                        float& dc_prev, float& dh_direct) {
-    f32x4_t dz;
-    dc_prev = 0.0f;
-    dh_direct = 0.0f;
-    if constexpr (CELL == CELL_LSTM) {
-        const float ig = sigmoid_f(z[0]), fg = sigmoid_f(z[1]);
-        const float gg = tanh_f(z[2]), og = sigmoid_f(z[3]);
-        const float c = fg * cp + ig * gg;
-        const float tc = tanh_f(c);
-        const float d_o = dh * tc;
-        const float dct = dc + dh * og * (1.0f - tc * tc);
-        dz[0] = dct * gg * ig * (1.0f - ig);
-        dz[1] = dct * cp * fg * (1.0f - fg);
-        dz[2] = dct * ig * (1.0f - gg * gg);
-        dz[3] = d_o * og * (1.0f - og);
-        dc_prev = dct * fg;
-    } else if constexpr (CELL == CELL_GRU) {
-        // z = (r, u, recurrent part of n, input part of n)
-        const float rg = sigmoid_f(z[0]), ug = sigmoid_f(z[1]);
-        const float ng = tanh_f(z[3] + rg * z[2]);
-        const float dzn = dh * (1.0f - ug) * (1.0f - ng * ng);
-        dz[0] = dzn * z[2] * rg * (1.0f - rg);
-        dz[1] = dh * (hp - ng) * ug * (1.0f - ug);
-        dz[2] = dzn * rg;
-        dz[3] = dzn;
-        dh_direct = dh * ug;
-    } else {
-        const float hn = tanh_f(z[0]);
-        dz[0] = dh * (1.0f - hn * hn);
-        dz[1] = 0.0f;
-        dz[2] = 0.0f;
-        dz[3] = 0.0f;
-    }
-    return dz;
-}
-
 // The cell's backward for the rows of step t: one (row, unit) per thread; dz
 // over z, dC <- dc_prev, and dH <- dh_direct (the GEMM then adds dz U^T).
 template <int CELL>
@@ -522,39 +479,6 @@ constexpr int BL_SC1 = 16;  // buffer-instruction cache policy: device scope
 typedef unsigned bl_u32x2 __attribute__((ext_vector_type(2)));
 typedef unsigned bl_u32x4 __attribute__((ext_vector_type(4)));
 
-// Grid barrier k: every workgroup's stores drained, then a counter per
-// group of workgroups (blockIdx mod 8) and one over the groups.  Bounded:
-// false past the deadline (the timeout status is set).
-__device__ inline bool bl_barrier(const BwdLoopParams& p, int k, int* lds_ok) {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        int ok = 1;
-        if (p.groups > 1) {
-            const int x = blockIdx.x & 7;
-            const unsigned members = (unsigned)((p.groups - x + 7) >> 3);
-            const unsigned old = __hip_atomic_fetch_add(p.bar + 64 * (1 + x), 1u, __ATOMIC_RELAXED,
-                                                        __HIP_MEMORY_SCOPE_AGENT);
-            if (old + 1u == (unsigned)(k + 1) * members)
-                __hip_atomic_fetch_add(p.bar, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            const unsigned want = (unsigned)(k + 1) * (unsigned)(p.groups < 8 ? p.groups : 8);
-            const unsigned long long t0 = wall_clock64();
-            while (__hip_atomic_load(p.bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < want) {
-                if (wall_clock64() - t0 > p.timeout_ticks) {
-                    ok = 0;
-                    __hip_atomic_fetch_or(&p.meta->status, STATUS_TIMEOUT, __ATOMIC_RELAXED,
-                                          __HIP_MEMORY_SCOPE_AGENT);
-                    break;
-                }
-                __builtin_amdgcn_s_sleep(1);
-            }
-        }
-        *lds_ok = ok;
-    }
-    __syncthreads();
-    return *lds_ok != 0;
-}
-
 template <int KSW, int CELL>
 __global__ void __launch_bounds__(BL_WAVES * 64, 1)
 bwd_loop_kernel(BwdLoopParams p) {
@@ -731,7 +655,7 @@ bwd_loop_kernel(BwdLoopParams p) {
             }
             __syncthreads();  // the partial sums are read before the next chunk writes them
         }
-        if (!last && !bl_barrier(p, k, &lds_ok)) return;
+        if (!last && !grid_barrier_bounded(p.bar, p.groups, k, p.timeout_ticks, p.meta, &lds_ok)) return;
     }
 }
 

@@ -1,0 +1,382 @@
+// bwdblk.hip -- the whole reverse loop of the backward pass in one cooperative
+// launch, for bf16 data on persistent handles with H a multiple of 256.
+//
+// Backpropagation through the masked loop of the paper's Section 9 "RNN
+// cells" experiment.  Going back from the last step, the rows of step t are
+// the prefix [0, active(t)) of the length sort, and each step takes
+//   dh_t = dz_{t+1} U^T  (the rows that ran step t+1; U is [H][4H] with
+//                          gate-interleaved columns 4u + gate)
+// then the cell's backward for the rows of step t, which gives dz_t.
+//
+// Workgroup (kb, cb), one of H / 8, keeps in registers, as MFMA A-fragments,
+// the block of U of the 32 hidden units [32 kb, 32 kb + 32) and the H gate
+// columns [H cb, H cb + H): one of four column blocks, 128 KB at H = 2048,
+// the size of the forward loop's slice.  Per step t:
+//   * product: the block's share of dh_t for the rows that ran step t+1, the
+//     sum over its H columns of dz_{t+1} U^T, from the fp16 dz of those
+//     columns (each row's 32-column block scaled by the power of two its
+//     writer chose, undone after that block's MFMA); the waves split the
+//     columns, their partial sums meet in LDS, and the workgroup's sums for
+//     its 32 units go to pdh[cb];
+//   * grid barrier;
+//   * cell: the 8 units [32 kb + 8 cb, + 8) of the rows of step t take dh =
+//     the four column blocks' shares in order (plus the carried term and the
+//     output sequence's gradient); the cell's backward gives dz (kept in
+//     fp32 over z for the weight gradients, published in fp16 under its row
+//     block's scale), dc and the carried term;
+//   * grid barrier.
+// A workgroup reads a quarter of each row's dz (4 KB of fp16 at H = 2048, as
+// much as the forward loop reads of h per row), where one holding all 4H
+// columns of a few units would read all of it; the second barrier per step,
+// which the exchange of the shares needs, is the price.
+// After the last step, one more product gives dh entering step 0: dH
+// receives dh0 (slot order, unscaled) and dC dc0.
+#include "launch.h"
+
+namespace ldyn {
+
+constexpr int BB_WAVES = 8;
+constexpr int BB_NCB = 4;     // column blocks of U
+constexpr int BB_UNITS = 32;  // hidden units (rows of U) per block
+constexpr int BB_NTC = 8;     // row tiles per chunk of the product
+constexpr int BB_SC1 = 16;    // buffer-instruction cache policy: device scope
+constexpr int BB_LDS_BYTES = BB_WAVES * BB_NTC * 2 * 64 * 16;  // the waves' partial sums
+
+typedef unsigned bb_u32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned bb_u32x4 __attribute__((ext_vector_type(4)));
+
+struct BwdBlockParams {
+    const _Float16* u16;     // [H][4H] U, gate-interleaved columns, times su
+    float* gx;               // [rows][4H] z in, dz (fp32) out
+    const float* save_h;     // [rows][H] the state each step started from
+    const float* save_c;
+    const float* dseq;       // [B][T][H] gradient of the output sequence, or null
+    const int32_t* perm;     // [B] slot -> batch row
+    const int32_t* offsets;  // [T + 1] first compact row of each step
+    Meta* meta;              // max_len in, timeout status out
+    float* dH;               // [B][H] carried dh: in d_out_h, out dh0 (slot order)
+    float* dC;               // [B][H] carried dc: in d_out_c, out dc0
+    // Published dz in MFMA fragment order: [2][bpad / 16 row tiles][4H / 32
+    // column blocks][64 chunks of 16 bytes], chunk q * 16 + r holding row r
+    // of the tile and columns 8 q .. 8 q + 7 of the block (fp16, each row's
+    // block scaled by its own power of two); a wave's load of one block is
+    // 1 KB of consecutive bytes.
+    _Float16* dzx;
+    float* dzs;              // [2][bpad / 16][4H / 32][16 rows] the scales
+    float* pdh;              // [4 column blocks][H / 32 row blocks][bpad][32] shares of dh
+    unsigned* bar;           // [9 * 64] barrier counters, zero at the launch
+    unsigned long long timeout_ticks;
+    // [T + 1][4] timestamps of workgroup 0, or null: per step t (at 4 t) its
+    // start, the shares published, the first barrier passed, the cells done;
+    // at 4 max_len the start of the product for dh0
+    unsigned long long* trace;
+    float alpha_u;           // 1 / su
+    int B, H, T, bpad, groups;
+};
+
+// A chunk length as a type, for code unrolled per length.
+template <int N> struct BbLen { static constexpr int value = N; };
+
+template <int KSW, int CELL>
+__global__ void __launch_bounds__(BB_WAVES * 64, 1)
+bwd_block_kernel(BwdBlockParams p) {
+    extern __shared__ __attribute__((aligned(16))) float lds[];  // [BB_WAVES][BB_NTC][2][64][4]
+    __shared__ int lds_ok;
+    // tid and l are re-read through empty asm statements at the top of each
+    // step, so that addresses derived from them are recomputed where used
+    // rather than kept live across the step (which made the variants with
+    // the largest U blocks spill)
+    int tid = threadIdx.x, l = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int H = p.H, H4 = 4 * H, NKB = H / BB_UNITS, NBLK = H / 8;
+    const unsigned bpad = (unsigned)p.bpad;
+    // Consecutive workgroups are dispatched to different XCDs (round robin
+    // over 8): number them so that the workgroups of one XCD share a column
+    // block, whose dz they then read through one L2.
+    const int g = (p.groups & 7) == 0 ? (blockIdx.x & 7) * (p.groups >> 3) + (blockIdx.x >> 3)
+                                      : (int)blockIdx.x;
+    const int cb = g / NKB, kb = g - cb * NKB;
+    const int k0 = kb * BB_UNITS, c0 = cb * H;
+    const int ks0 = w * KSW;  // this wave's first 32-column step within the block
+
+    // U block -> registers: lane l of afrag[kt][ks] holds row k0 + 16 kt + (l & 15),
+    // columns c0 + 32 (ks0 + ks) + 8 (l >> 4) .. + 8.
+    f16x8_t afrag[2][KSW];
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int ks = 0; ks < KSW; ++ks)
+            afrag[kt][ks] = *reinterpret_cast<const f16x8_t*>(
+                p.u16 + (size_t)(k0 + 16 * kt + (l & 15)) * H4 + c0 + 32 * (ks0 + ks) + 8 * (l >> 4));
+
+    const __amdgpu_buffer_rsrc_t Rz = __builtin_amdgcn_make_buffer_rsrc(
+        p.dzx, (short)0, (int)((size_t)2 * bpad * H4 * 2), 0x00020000);
+    const __amdgpu_buffer_rsrc_t Rs = __builtin_amdgcn_make_buffer_rsrc(
+        p.dzs, (short)0, (int)((size_t)2 * bpad * NBLK * 4), 0x00020000);
+    const __amdgpu_buffer_rsrc_t Rp = __builtin_amdgcn_make_buffer_rsrc(
+        p.pdh, (short)0, (int)((size_t)BB_NCB * bpad * H * 4), 0x00020000);
+    const unsigned NTP = bpad / 16;  // row tiles of one parity of the exchange
+    // byte offset of the share of dh of (column block c, row s, unit k) in pdh
+    auto share_off = [&](unsigned c, unsigned s, unsigned k) {
+        return (((c * (unsigned)NKB + (k >> 5)) * bpad + s) * 32u + (k & 31u)) * 4u;
+    };
+
+    // One row tile's dz fragments of this wave's columns and their scales
+    // (inverted where the tile is multiplied, so that nothing waits for the
+    // loads here).  Rows of the tile that did not run step t+1 hold values of
+    // an earlier step: they reach only those rows' sums, which are not
+    // published.
+    auto load_tile = [&](f16x8_t* b, float* sc, unsigned pin, int nt) {
+        const unsigned tb = (pin * NTP + (unsigned)nt) * (unsigned)NBLK + (unsigned)(c0 / 32 + ks0);
+#pragma unroll
+        for (int ks = 0; ks < KSW; ++ks)
+            b[ks] = __builtin_bit_cast(f16x8_t, __builtin_amdgcn_raw_buffer_load_b128(
+                                                    Rz, (tb + (unsigned)ks) * 1024u + (unsigned)l * 16u, 0, BB_SC1));
+#pragma unroll
+        for (int ks = 0; ks < KSW; ++ks)
+            sc[ks] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                Rs, ((tb + (unsigned)ks) * 16u + (unsigned)(l & 15)) * 4u, 0, BB_SC1));
+    };
+    // Tile j of the chunk: this wave's partial sums of dh (rows of the tile,
+    // the block's 32 units) into its LDS slot.
+    auto mma_tile = [&](const f16x8_t* b, const float* sc, int j) {
+        f32x4_t acc[2] = {f32x4_t{0.f, 0.f, 0.f, 0.f}, f32x4_t{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+        for (int ks = 0; ks < KSW; ++ks) {
+            const float inv = __builtin_amdgcn_rcpf(sc[ks]);  // a power of two: exact
+#pragma unroll
+            for (int kt = 0; kt < 2; ++kt)
+                acc[kt] += __builtin_amdgcn_mfma_f32_16x16x32_f16(afrag[kt][ks], b[ks],
+                                                                  f32x4_t{0.f, 0.f, 0.f, 0.f}, 0, 0, 0) *
+                           inv;
+        }
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+            *reinterpret_cast<f32x4_t*>(lds + ((((w * BB_NTC + j) * 2 + kt) * 64 + l) << 2)) = acc[kt];
+    };
+
+    const unsigned blk = (unsigned)((k0 + 8 * cb) >> 3);  // this workgroup's 32-column block of dz
+    const int32_t* const off = p.offsets;
+    const int max_len = p.meta->max_len;
+    int bk = 0;
+    for (int t = max_len - 1; t >= -1; --t) {
+        asm volatile("" : "+v"(tid), "+v"(l));
+        // this thread's cell pairs: 8 lanes per row, one unit each
+        const int ul = tid & 7, u = k0 + 8 * cb + ul;
+        const bool last = t < 0;  // only the product: dh entering step 0
+        const int actp = t + 1 < max_len ? off[t + 2] - off[t + 1] : 0;  // rows with dz_{t+1}
+        const int actc = last ? 0 : off[t + 1] - off[t];                // rows that run step t
+        const unsigned pin = (unsigned)((t + 1) & 1), pout = (unsigned)(t & 1);
+        // step trace: stamps kept in scalar registers, stored after the step
+        const bool tr = p.trace && blockIdx.x == 0 && w == 0;
+        const int ti = last ? max_len : t;
+        unsigned long long ts[4] = {0, 0, 0, 0};
+        if (tr) ts[0] = wall_clock64();
+
+        // ---- product: the block's share of dh_t, into pdh[cb]
+        const int ntp = (actp + 15) >> 4;
+        for (int ntc0 = 0; ntc0 < ntp; ntc0 += BB_NTC) {
+            const int nchunk = min(BB_NTC, ntp - ntc0);
+            // Straight-line code per chunk length: the first DEPTH tiles' loads
+            // go out together, and a tile's register set is reloaded with the
+            // tile DEPTH ahead as soon as its products are formed, so DEPTH - 1
+            // tiles are in flight behind the one being multiplied.  (With
+            // conditional loads the compiler waits for all loads in flight
+            // before every product, and a wave then has one tile in flight.)
+            auto chunk = [&](auto len) {
+                constexpr int N = decltype(len)::value;
+                constexpr int DEPTH = KSW >= 8 ? 2 : 4;
+                constexpr int D0 = N < DEPTH ? N : DEPTH;
+                f16x8_t b[DEPTH][KSW];
+                float sc[DEPTH][KSW];
+#pragma unroll
+                for (int j = 0; j < D0; ++j) load_tile(b[j], sc[j], pin, ntc0 + j);
+#pragma unroll
+                for (int j = 0; j < N; ++j) {
+                    mma_tile(b[j % DEPTH], sc[j % DEPTH], j);
+                    if (j + DEPTH < N) load_tile(b[j % DEPTH], sc[j % DEPTH], pin, ntc0 + j + DEPTH);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            };
+            switch (nchunk) {
+                case 1: chunk(BbLen<1>{}); break;
+                case 2: chunk(BbLen<2>{}); break;
+                case 3: chunk(BbLen<3>{}); break;
+                case 4: chunk(BbLen<4>{}); break;
+                case 5: chunk(BbLen<5>{}); break;
+                case 6: chunk(BbLen<6>{}); break;
+                case 7: chunk(BbLen<7>{}); break;
+                default: chunk(BbLen<BB_NTC>{}); break;
+            }
+            __syncthreads();
+            // the waves' partial sums in order; lane ln of (tile j, unit tile
+            // kt) holds units 16 kt + 4 (ln >> 4) .. + 3 of row (ln & 15)
+            for (int e = tid; e < nchunk * 128; e += BB_WAVES * 64) {
+                const int j = e >> 7, kt = (e >> 6) & 1, ln = e & 63;
+                f32x4_t sum = *reinterpret_cast<const f32x4_t*>(lds + (((j * 2 + kt) * 64 + ln) << 2));
+#pragma unroll
+                for (int ww = 1; ww < BB_WAVES; ++ww)
+                    sum += *reinterpret_cast<const f32x4_t*>(lds + ((((ww * BB_NTC + j) * 2 + kt) * 64 + ln) << 2));
+                const int s = (ntc0 + j) * 16 + (ln & 15);
+                if (s < actp) {
+                    const unsigned k = (unsigned)(k0 + 16 * kt + 4 * (ln >> 4));
+                    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(bb_u32x4, sum), Rp,
+                                                           share_off((unsigned)cb, (unsigned)s, k), 0, BB_SC1);
+                }
+            }
+            __syncthreads();  // the partial sums are read before the next chunk writes them
+        }
+        if (tr) ts[1] = wall_clock64();
+        if (!grid_barrier_bounded(p.bar, p.groups, bk++, p.timeout_ticks, p.meta, &lds_ok)) return;
+        if (tr) ts[2] = wall_clock64();
+
+        // ---- cell: this workgroup's 8 units of the rows of step t, four rows
+        // per thread at a time with all their loads issued before any use
+        // (rows past the end load row rows - 1 and store nothing)
+        const int rows = last ? actp : actc;
+        for (int sb = tid >> 3; sb < rows; sb += 4 * BB_WAVES * 8) {
+            float share[4][BB_NCB], dhc[4], dcc[4], hp[4], cp[4], ds[4];
+            f32x4_t zv[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int s = min(sb + i * BB_WAVES * 8, rows - 1);
+                // rows without a product read a row that has one (or row 0),
+                // and the sum is not used
+                const unsigned sp = (unsigned)min(s, max(actp - 1, 0));
+#pragma unroll
+                for (int c = 0; c < BB_NCB; ++c)
+                    share[i][c] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                        Rp, share_off((unsigned)c, sp, (unsigned)u), 0, BB_SC1));
+                const size_t su = (size_t)s * H + u;
+                dhc[i] = p.dH[su];
+                if (!last) {
+                    const size_t r = (size_t)off[t] + s;
+                    zv[i] = *reinterpret_cast<const f32x4_t*>(p.gx + r * H4 + 4 * u);
+                    hp[i] = p.save_h[r * H + u];
+                    cp[i] = p.save_c[r * H + u];
+                    dcc[i] = p.dC[su];
+                    ds[i] = p.dseq ? p.dseq[((size_t)p.perm[s] * p.T + t) * H + u] : 0.0f;
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int s = sb + i * BB_WAVES * 8;
+                if (s < rows) {
+                    float sum = 0.0f;
+#pragma unroll
+                    for (int c = 0; c < BB_NCB; ++c) sum += share[i][c];
+                    float dh = (s < actp ? sum * p.alpha_u : 0.0f) + dhc[i];
+                    const size_t su = (size_t)s * H + u;
+                    if (last) {  // dh entering step 0: dh0
+                        p.dH[su] = dh;
+                        continue;
+                    }
+                    dh += ds[i];
+                    const size_t r = (size_t)off[t] + s;
+                    float dcp, dhd;
+                    const f32x4_t dz = cell_backward<CELL>(zv[i], hp[i], cp[i], dh, dcc[i], dcp, dhd);
+                    *reinterpret_cast<f32x4_t*>(p.gx + r * H4 + 4 * u) = dz;
+                    p.dC[su] = dcp;
+                    p.dH[su] = dhd;
+                    // the row block's scale: its largest magnitude into [2^13, 2^14)
+                    unsigned m = 0;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) m = max(m, __float_as_uint(fabsf(dz[e])) & 0x7fffffffu);
+                    for (int o = 4; o > 0; o >>= 1) m = max(m, (unsigned)__shfl_xor((int)m, o));
+                    const float mf = __uint_as_float(m);
+                    float sc = 1.0f;
+                    if (mf > 0.0f && mf < 3.0e38f) {
+                        int ex;
+                        (void)frexpf(mf, &ex);
+                        sc = ldexpf(1.0f, min(14 - ex, 126));
+                    }
+                    typedef _Float16 h4_t __attribute__((ext_vector_type(4)));
+                    const h4_t hv = h4_t{(_Float16)(dz[0] * sc), (_Float16)(dz[1] * sc), (_Float16)(dz[2] * sc),
+                                         (_Float16)(dz[3] * sc)};
+                    // columns 4u .. 4u + 3: chunk (u & 7) / 2 of the block, its
+                    // first or second half
+                    const unsigned tb = (pout * NTP + (unsigned)(s >> 4)) * (unsigned)NBLK + blk;
+                    __builtin_amdgcn_raw_buffer_store_b64(
+                        __builtin_bit_cast(bb_u32x2, hv), Rz,
+                        tb * 1024u + ((unsigned)(ul >> 1) * 16u + (unsigned)(s & 15)) * 16u + (unsigned)(ul & 1) * 8u, 0,
+                        BB_SC1);
+                    if (ul == 0)
+                        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(sc), Rs,
+                                                              (tb * 16u + (unsigned)(s & 15)) * 4u, 0, BB_SC1);
+                }
+            }
+        }
+        if (tr) {
+            ts[3] = wall_clock64();
+            if (l == 0)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) p.trace[4 * ti + e] = ts[e];
+        }
+        if (!last && !grid_barrier_bounded(p.bar, p.groups, bk++, p.timeout_ticks, p.meta, &lds_ok)) return;
+    }
+}
+
+typedef void (*bwd_block_fn)(BwdBlockParams);
+
+static bwd_block_fn bwd_block_pick(int H, int cell) {
+#define BB_CELLS(K)                                                                         \
+    if (H == 256 * K)                                                                       \
+        return cell == CELL_GRU ? bwd_block_kernel<K, CELL_GRU>                             \
+               : cell == CELL_RNN ? bwd_block_kernel<K, CELL_RNN> : bwd_block_kernel<K, CELL_LSTM>;
+    BB_CELLS(1) BB_CELLS(2) BB_CELLS(4) BB_CELLS(8)
+#undef BB_CELLS
+    return nullptr;
+}
+
+int bwd_block_fits(const Dims& d, int num_cus) {
+    if (!d.bf16 || d.H % 256 != 0 || d.H > 2048 || d.bpad > 512) return 0;
+    const int groups = d.H / 8;
+    if (groups > num_cus) return 0;
+    bwd_block_fn f = bwd_block_pick(d.H, d.cell);
+    if (!f) return 0;
+    int n = 0;
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(f), hipFuncAttributeMaxDynamicSharedMemorySize,
+                            BB_LDS_BYTES) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, reinterpret_cast<const void*>(f), BB_WAVES * 64,
+                                                     BB_LDS_BYTES) != hipSuccess) {
+        (void)hipGetLastError();  // not an error of a later call: another path serves
+        return 0;
+    }
+    return n >= 1 ? groups : 0;
+}
+
+hipError_t launch_bwd_block(const Dims& d, const _Float16* u16, float alpha_u, const float* save_h,
+                            const float* save_c, const float* dseq, float* dH, float* dC, _Float16* dzx,
+                            float* dzs, float* pdh, unsigned* bar, unsigned long long timeout_ticks,
+                            unsigned long long* trace, const Workspace& ws, hipStream_t s) {
+    bwd_block_fn f = bwd_block_pick(d.H, d.cell);
+    if (!f || d.bpad > 512) return hipErrorInvalidValue;
+    BwdBlockParams p{};
+    p.u16 = u16;
+    p.gx = ws.gx;
+    p.save_h = save_h;
+    p.save_c = save_c;
+    p.dseq = dseq;
+    p.perm = ws.perm;
+    p.offsets = ws.offsets;
+    p.meta = ws.meta;
+    p.dH = dH;
+    p.dC = dC;
+    p.dzx = dzx;
+    p.dzs = dzs;
+    p.pdh = pdh;
+    p.bar = bar;
+    p.timeout_ticks = timeout_ticks;
+    p.trace = trace;
+    p.alpha_u = alpha_u;
+    p.B = d.B;
+    p.H = d.H;
+    p.T = d.T;
+    p.bpad = d.bpad;
+    p.groups = d.H / 8;
+    void* args[] = {&p};
+    return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(f), dim3(p.groups), dim3(BB_WAVES * 64),
+                                      args, (unsigned)BB_LDS_BYTES, s);
+}
+
+}  // namespace ldyn

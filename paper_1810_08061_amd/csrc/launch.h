@@ -154,6 +154,18 @@ hipError_t launch_bwd_loop(const Dims& d, const _Float16* u16, float alpha_u, co
                            const float* save_c, const float* dseq, float* dH, float* dC,
                            _Float16* dzx, float* dzs, unsigned* bar, unsigned long long timeout_ticks,
                            int t_end, const Workspace& ws, hipStream_t s);
+// bf16 data, H a multiple of 256 (at most 2048): the whole reverse loop in one
+// cooperative launch (H / 8 workgroups, each with a 32-unit x H-column block
+// of U in registers; per step the blocks' shares of dh = dz U^T, a grid
+// barrier, the cell's backward of 8 units, a grid barrier), leaving dh0 and
+// dc0 in dH and dC.  bwd_block_fits: its workgroup count, or 0 where it does
+// not apply.  dzx [2][bpad][4H] fp16, dzs [2][bpad][H / 8], pdh [4][bpad][H];
+// bar [9 * 64] must be zero at the launch; trace [T + 1][4] or null.
+int bwd_block_fits(const Dims& d, int num_cus);
+hipError_t launch_bwd_block(const Dims& d, const _Float16* u16, float alpha_u, const float* save_h,
+                            const float* save_c, const float* dseq, float* dH, float* dC, _Float16* dzx,
+                            float* dzs, float* pdh, unsigned* bar, unsigned long long timeout_ticks,
+                            unsigned long long* trace, const Workspace& ws, hipStream_t s);
 hipError_t launch_bwd_gather_x(const Dims& d, const void* x, long rows, float* xc,
                                const Workspace& ws, hipStream_t s);
 // fp16 operands of the backward's GEMMs: the largest magnitude (as float bits,
