@@ -86,7 +86,7 @@ struct TrainWs {
     int loop_groups;        // workgroups of the few-row launch, or 0
     _Float16* dzx;          // [2][bpad][kp] each step's published dz
     float* dzs;             // [2][bpad][nblk] their scales
-    float* pdh;             // [4][bpad][H] the column blocks' shares of dh
+    float* pdh;             // [2][4][bpad][H] the column blocks' shares of dh
     unsigned* bar;          // [9 * 64] barrier counters
     long long dzx_bytes, dzs_bytes;
 };
@@ -785,7 +785,7 @@ static int ensure_train(lstm_dyn* h) {
     tw->dzx_bytes = 2LL * 2 * bpad * kp;
     tw->dzs_bytes = 4LL * 2 * bpad * nblk;
     const long long odzx = take(tw->dzx_bytes), odzsc = take(tw->dzs_bytes),
-                    opdh = take(tw->block_groups ? 4LL * 4 * bpad * H : 0),
+                    opdh = take(tw->block_groups ? 2LL * 4 * 4 * bpad * H : 0),
                     obar = take(one_launch ? 9 * 64 * 4 : 0);
     if (hipMalloc(&tw->block, (size_t)o) != hipSuccess) {
         (void)hipGetLastError();
@@ -1054,6 +1054,9 @@ extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* le
         int t_end = max_len;
         if (tw->block_groups) {
             LD_CHECK(hipMemsetAsync(tw->bar, 0, 9 * 64 * sizeof(unsigned), s));
+            // the published dz and its scales start as the marker (all ones)
+            LD_CHECK(hipMemsetAsync(tw->dzx, 0xff, (size_t)tw->dzx_bytes, s));
+            LD_CHECK(hipMemsetAsync(tw->dzs, 0xff, (size_t)tw->dzs_bytes, s));
             LD_CHECK(launch_bwd_block(d, tw->u16, alpha_u, tw->save_h, tw->save_c, d_seq, tw->dH, tw->dC,
                                       tw->dzx, tw->dzs, tw->pdh, tw->bar, h->timeout_ticks, h->trace,
                                       h->ws, s));

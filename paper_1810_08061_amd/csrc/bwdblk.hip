@@ -18,17 +18,23 @@
 //     writer chose, undone after that block's MFMA); the waves split the
 //     columns, their partial sums meet in LDS, and the workgroup's sums for
 //     its 32 units go to pdh[cb];
-//   * grid barrier;
+//   * grid barrier (the shares are complete);
 //   * cell: the 8 units [32 kb + 8 cb, + 8) of the rows of step t take dh =
 //     the four column blocks' shares in order (plus the carried term and the
 //     output sequence's gradient); the cell's backward gives dz (kept in
 //     fp32 over z for the weight gradients, published in fp16 under its row
-//     block's scale), dc and the carried term;
-//   * grid barrier.
+//     block's scale), dc and the carried term.
+// The published dz needs no barrier: a value not yet written for the step
+// holds the all-ones marker (a NaN the writers never store), and the next
+// product polls for it.  dz alternates between two slots by step parity;
+// after the barrier of step t every workgroup has read dz_{t+1}, so each
+// writer puts the marker back into its block of that slot for the rows of
+// step t-1, and the next barrier drains those stores before anyone reads or
+// writes dz_{t-1}.
 // A workgroup reads a quarter of each row's dz (4 KB of fp16 at H = 2048, as
 // much as the forward loop reads of h per row), where one holding all 4H
-// columns of a few units would read all of it; the second barrier per step,
-// which the exchange of the shares needs, is the price.
+// columns of a few units would read all of it; the barrier per step, which
+// the exchange of the shares needs, is the price.
 // After the last step, one more product gives dh entering step 0: dH
 // receives dh0 (slot order, unscaled) and dC dc0.
 #include "launch.h"
@@ -63,7 +69,10 @@ struct BwdBlockParams {
     // 1 KB of consecutive bytes.
     _Float16* dzx;
     float* dzs;              // [2][bpad / 16][4H / 32][16 rows] the scales
-    float* pdh;              // [4 column blocks][H / 32 row blocks][bpad][32] shares of dh
+    // shares of dh: [2 step parities][4 column blocks][H / 32 unit blocks][bpad][32];
+    // by parity, since a workgroup may start the next step's product while a
+    // sibling still reads this step's shares
+    float* pdh;
     unsigned* bar;           // [9 * 64] barrier counters, zero at the launch
     unsigned long long timeout_ticks;
     // [T + 1][4] timestamps of workgroup 0, or null: per step t (at 4 t) its
@@ -81,7 +90,7 @@ template <int KSW, int CELL>
 __global__ void __launch_bounds__(BB_WAVES * 64, 1)
 bwd_block_kernel(BwdBlockParams p) {
     extern __shared__ __attribute__((aligned(16))) float lds[];  // [BB_WAVES][BB_NTC][2][64][4]
-    __shared__ int lds_ok;
+    __shared__ int lds_ok, lds_nan, lds_abort;
     // tid and l are re-read through empty asm statements at the top of each
     // step, so that addresses derived from them are recomputed where used
     // rather than kept live across the step (which made the variants with
@@ -114,11 +123,12 @@ bwd_block_kernel(BwdBlockParams p) {
     const __amdgpu_buffer_rsrc_t Rs = __builtin_amdgcn_make_buffer_rsrc(
         p.dzs, (short)0, (int)((size_t)2 * bpad * NBLK * 4), 0x00020000);
     const __amdgpu_buffer_rsrc_t Rp = __builtin_amdgcn_make_buffer_rsrc(
-        p.pdh, (short)0, (int)((size_t)BB_NCB * bpad * H * 4), 0x00020000);
+        p.pdh, (short)0, (int)((size_t)2 * BB_NCB * bpad * H * 4), 0x00020000);
     const unsigned NTP = bpad / 16;  // row tiles of one parity of the exchange
-    // byte offset of the share of dh of (column block c, row s, unit k) in pdh
-    auto share_off = [&](unsigned c, unsigned s, unsigned k) {
-        return (((c * (unsigned)NKB + (k >> 5)) * bpad + s) * 32u + (k & 31u)) * 4u;
+    // byte offset of the share of dh of (step parity, column block c, row s,
+    // unit k) in pdh
+    auto share_off = [&](unsigned par, unsigned c, unsigned s, unsigned k) {
+        return ((((par * BB_NCB + c) * (unsigned)NKB + (k >> 5)) * bpad + s) * 32u + (k & 31u)) * 4u;
     };
 
     // One row tile's dz fragments of this wave's columns and their scales
@@ -155,6 +165,39 @@ bwd_block_kernel(BwdBlockParams p) {
             *reinterpret_cast<f32x4_t*>(lds + ((((w * BB_NTC + j) * 2 + kt) * 64 + l) << 2)) = acc[kt];
     };
 
+    // Whether an active row of a loaded tile still holds the marker (all-ones
+    // halves of dz or an all-ones scale: values not yet written for the
+    // step).  Rows past actp may hold anything; their sums are not used.
+    auto marked = [&](const f16x8_t* b, const float* sc, int nt, int actp) {
+        const bool live = nt * 16 + (l & 15) < actp;
+        bool m = false;
+#pragma unroll
+        for (int ks = 0; ks < KSW; ++ks) {
+            const bb_u32x4 v = __builtin_bit_cast(bb_u32x4, b[ks]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) m |= (v[e] & 0xffffu) == 0xffffu || (v[e] >> 16) == 0xffffu;
+            m |= __float_as_uint(sc[ks]) == 0xffffffffu;
+        }
+        return __builtin_amdgcn_ballot_w64(live && m) != 0;
+    };
+    // Reloads tile nt until its active rows hold no marker; false past the
+    // deadline (the timeout status is set).
+    auto poll_tile = [&](f16x8_t* b, float* sc, unsigned pin, int nt, int actp) {
+        if (!marked(b, sc, nt, actp)) return true;
+        const unsigned long long t0 = wall_clock64();
+        do {
+            if (wall_clock64() - t0 > p.timeout_ticks) {
+                if (l == 0)
+                    __hip_atomic_fetch_or(&p.meta->status, STATUS_TIMEOUT, __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT);
+                return false;
+            }
+            __builtin_amdgcn_s_sleep(1);
+            load_tile(b, sc, pin, nt);
+        } while (marked(b, sc, nt, actp));
+        return true;
+    };
+
     const unsigned blk = (unsigned)((k0 + 8 * cb) >> 3);  // this workgroup's 32-column block of dz
     const int32_t* const off = p.offsets;
     const int max_len = p.meta->max_len;
@@ -173,16 +216,58 @@ bwd_block_kernel(BwdBlockParams p) {
         unsigned long long ts[4] = {0, 0, 0, 0};
         if (tr) ts[0] = wall_clock64();
 
-        // ---- product: the block's share of dh_t, into pdh[cb]
+        // ---- product: the block's share of dh_t, into pdh[cb].  dz_{t+1}
+        // arrives without a barrier: each chunk's first tile is polled until
+        // its active rows hold no marker (that is where a workgroup waits for
+        // the others); later tiles are nearly always complete by then and are
+        // used as loaded.  A marker that slipped into an active row is a NaN
+        // in that row's sums (an all-ones half is a NaN, and so is an all-ones
+        // scale), and the chunk is then redone with every tile polled; a NaN
+        // that the redo reproduces comes from the data and is kept.
         const int ntp = (actp + 15) >> 4;
+        if (tid == 0) {
+            lds_nan = 0;
+            lds_abort = 0;
+        }
+        __syncthreads();
         for (int ntc0 = 0; ntc0 < ntp; ntc0 += BB_NTC) {
             const int nchunk = min(BB_NTC, ntp - ntc0);
-            // Straight-line code per chunk length: the first DEPTH tiles' loads
-            // go out together, and a tile's register set is reloaded with the
-            // tile DEPTH ahead as soon as its products are formed, so DEPTH - 1
-            // tiles are in flight behind the one being multiplied.  (With
-            // conditional loads the compiler waits for all loads in flight
-            // before every product, and a wave then has one tile in flight.)
+            // the waves' partial sums in order, published; lane ln of (tile j,
+            // unit tile kt) holds units 16 kt + 4 (ln >> 4) .. + 3 of row
+            // (ln & 15).  Sets the flag if an active row's sum is a NaN.
+            auto reduce_publish = [&]() {
+                bool nan = false;
+                for (int e = tid; e < nchunk * 128; e += BB_WAVES * 64) {
+                    const int j = e >> 7, kt = (e >> 6) & 1, ln = e & 63;
+                    f32x4_t sum = *reinterpret_cast<const f32x4_t*>(lds + (((j * 2 + kt) * 64 + ln) << 2));
+#pragma unroll
+                    for (int ww = 1; ww < BB_WAVES; ++ww)
+                        sum += *reinterpret_cast<const f32x4_t*>(lds + ((((ww * BB_NTC + j) * 2 + kt) * 64 + ln) << 2));
+                    const int s = (ntc0 + j) * 16 + (ln & 15);
+                    if (s < actp) {
+                        nan |= (sum[0] != sum[0]) | (sum[1] != sum[1]) | (sum[2] != sum[2]) | (sum[3] != sum[3]);
+                        const unsigned k = (unsigned)(k0 + 16 * kt + 4 * (ln >> 4));
+                        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(bb_u32x4, sum), Rp,
+                                                               share_off(pout, (unsigned)cb, (unsigned)s, k), 0, BB_SC1);
+                    }
+                }
+                if (nan) lds_nan = 1;
+                __syncthreads();  // the partial sums and the flag are read before the next writes
+            };
+            // the first tile polled with registers of its own, which are free
+            // again before the pipeline below starts (it loads the tile once
+            // more, from L2)
+            {
+                f16x8_t bp[KSW];
+                float sp[KSW];
+                load_tile(bp, sp, pin, ntc0);
+                if (!poll_tile(bp, sp, pin, ntc0, actp)) lds_abort = 1;
+            }
+            // Straight-line code per chunk length: DEPTH tiles are in flight,
+            // and a tile's register set is reloaded with the tile DEPTH ahead
+            // as soon as its products are formed.  (With conditional loads the
+            // compiler waits for all loads in flight before every product, and
+            // a wave then has one tile in flight.)
             auto chunk = [&](auto len) {
                 constexpr int N = decltype(len)::value;
                 constexpr int DEPTH = KSW >= 8 ? 2 : 4;
@@ -209,26 +294,47 @@ bwd_block_kernel(BwdBlockParams p) {
                 default: chunk(BbLen<BB_NTC>{}); break;
             }
             __syncthreads();
-            // the waves' partial sums in order; lane ln of (tile j, unit tile
-            // kt) holds units 16 kt + 4 (ln >> 4) .. + 3 of row (ln & 15)
-            for (int e = tid; e < nchunk * 128; e += BB_WAVES * 64) {
-                const int j = e >> 7, kt = (e >> 6) & 1, ln = e & 63;
-                f32x4_t sum = *reinterpret_cast<const f32x4_t*>(lds + (((j * 2 + kt) * 64 + ln) << 2));
-#pragma unroll
-                for (int ww = 1; ww < BB_WAVES; ++ww)
-                    sum += *reinterpret_cast<const f32x4_t*>(lds + ((((ww * BB_NTC + j) * 2 + kt) * 64 + ln) << 2));
-                const int s = (ntc0 + j) * 16 + (ln & 15);
-                if (s < actp) {
-                    const unsigned k = (unsigned)(k0 + 16 * kt + 4 * (ln >> 4));
-                    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(bb_u32x4, sum), Rp,
-                                                           share_off((unsigned)cb, (unsigned)s, k), 0, BB_SC1);
+            if (lds_abort) return;  // read by every wave between the same two barriers
+            reduce_publish();
+            if (lds_nan) {  // (read by every wave between the same two barriers)
+                // a marker slipped into a tile used as loaded: once more with
+                // every tile polled
+                __syncthreads();  // every wave has read the flag
+                if (tid == 0) lds_nan = 0;
+                for (int j = 0; j < nchunk; ++j) {
+                    f16x8_t b[KSW];
+                    float sc[KSW];
+                    load_tile(b, sc, pin, ntc0 + j);
+                    if (!poll_tile(b, sc, pin, ntc0 + j, actp)) lds_abort = 1;
+                    mma_tile(b, sc, j);
                 }
+                __syncthreads();
+                if (lds_abort) return;
+                reduce_publish();
+                __syncthreads();  // every wave has read the flag (a NaN now is the data's)
+                if (tid == 0) lds_nan = 0;
             }
-            __syncthreads();  // the partial sums are read before the next chunk writes them
         }
         if (tr) ts[1] = wall_clock64();
         if (!grid_barrier_bounded(p.bar, p.groups, bk++, p.timeout_ticks, p.meta, &lds_ok)) return;
         if (tr) ts[2] = wall_clock64();
+        // Every workgroup has read dz_{t+1}: its slot, which takes dz_{t-1},
+        // gets the marker again in this workgroup's block for the rows of step
+        // t-1.  The next barrier drains these stores before any workgroup can
+        // read dz_{t-1}, and before this one writes it.
+        if (t >= 1) {
+            const int rows_m = off[t] - off[t - 1];
+            const unsigned slot = (unsigned)((t - 1) & 1);
+            for (int e = tid; e < rows_m * 4; e += BB_WAVES * 64) {
+                const int sm = e >> 2, q = e & 3;
+                const unsigned tb = (slot * NTP + (unsigned)(sm >> 4)) * (unsigned)NBLK + blk;
+                __builtin_amdgcn_raw_buffer_store_b128(bb_u32x4{~0u, ~0u, ~0u, ~0u}, Rz,
+                                                       tb * 1024u + ((unsigned)q * 16u + (unsigned)(sm & 15)) * 16u, 0,
+                                                       BB_SC1);
+                if (q == 0)
+                    __builtin_amdgcn_raw_buffer_store_b32(~0u, Rs, (tb * 16u + (unsigned)(sm & 15)) * 4u, 0, BB_SC1);
+            }
+        }
 
         // ---- cell: this workgroup's 8 units of the rows of step t, four rows
         // per thread at a time with all their loads issued before any use
@@ -246,7 +352,7 @@ bwd_block_kernel(BwdBlockParams p) {
 #pragma unroll
                 for (int c = 0; c < BB_NCB; ++c)
                     share[i][c] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
-                        Rp, share_off((unsigned)c, sp, (unsigned)u), 0, BB_SC1));
+                        Rp, share_off(pout, (unsigned)c, sp, (unsigned)u), 0, BB_SC1));
                 const size_t su = (size_t)s * H + u;
                 dhc[i] = p.dH[su];
                 if (!last) {
@@ -290,9 +396,15 @@ bwd_block_kernel(BwdBlockParams p) {
                         (void)frexpf(mf, &ex);
                         sc = ldexpf(1.0f, min(14 - ex, 126));
                     }
-                    typedef _Float16 h4_t __attribute__((ext_vector_type(4)));
-                    const h4_t hv = h4_t{(_Float16)(dz[0] * sc), (_Float16)(dz[1] * sc), (_Float16)(dz[2] * sc),
-                                         (_Float16)(dz[3] * sc)};
+                    // fp16, an all-ones half (the marker) replaced by the canonical quiet NaN
+                    unsigned short hb[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const unsigned short b16 = __builtin_bit_cast(unsigned short, (_Float16)(dz[e] * sc));
+                        hb[e] = b16 == 0xffffu ? (unsigned short)0x7e00u : b16;
+                    }
+                    typedef unsigned short h4_t __attribute__((ext_vector_type(4)));
+                    const h4_t hv = h4_t{hb[0], hb[1], hb[2], hb[3]};
                     // columns 4u .. 4u + 3: chunk (u & 7) / 2 of the block, its
                     // first or second half
                     const unsigned tb = (pout * NTP + (unsigned)(s >> 4)) * (unsigned)NBLK + blk;
@@ -312,8 +424,9 @@ bwd_block_kernel(BwdBlockParams p) {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) p.trace[4 * ti + e] = ts[e];
         }
-        if (!last && !grid_barrier_bounded(p.bar, p.groups, bk++, p.timeout_ticks, p.meta, &lds_ok)) return;
     }
+    // nothing of this wave in flight when it ends
+    __builtin_amdgcn_s_waitcnt(0x0F70);
 }
 
 typedef void (*bwd_block_fn)(BwdBlockParams);
