@@ -260,6 +260,7 @@ bwd_block_kernel(BwdBlockParams p) {
             {
                 f16x8_t bp[KSW];
                 float sp[KSW];
+                stress_delay(t, 1 + ntc0);
                 load_tile(bp, sp, pin, ntc0);
                 if (!poll_tile(bp, sp, pin, ntc0, actp)) lds_abort = 1;
             }
@@ -323,6 +324,7 @@ bwd_block_kernel(BwdBlockParams p) {
         // t-1.  The next barrier drains these stores before any workgroup can
         // read dz_{t-1}, and before this one writes it.
         if (t >= 1) {
+            stress_delay(t, 200);
             const int rows_m = off[t] - off[t - 1];
             const unsigned slot = (unsigned)((t - 1) & 1);
             for (int e = tid; e < rows_m * 4; e += BB_WAVES * 64) {
@@ -408,6 +410,7 @@ bwd_block_kernel(BwdBlockParams p) {
                     // columns 4u .. 4u + 3: chunk (u & 7) / 2 of the block, its
                     // first or second half
                     const unsigned tb = (pout * NTP + (unsigned)(s >> 4)) * (unsigned)NBLK + blk;
+                    stress_delay(t, 300 + i);
                     __builtin_amdgcn_raw_buffer_store_b64(
                         __builtin_bit_cast(bb_u32x2, hv), Rz,
                         tb * 1024u + ((unsigned)(ul >> 1) * 16u + (unsigned)(s & 15)) * 16u + (unsigned)(ul & 1) * 8u, 0,

@@ -234,4 +234,26 @@ __device__ inline bool grid_barrier_bounded(unsigned* bar, int groups, int k,
     return *lds_ok != 0;
 }
 
+// Timing stress (a diagnostic build, LDYN_STRESS defined): a wave sleeps for a
+// pseudo-random time (0 to about 1 us, from a hash of the workgroup, wave,
+// step and site) before it publishes data for other workgroups, marks a
+// buffer or starts polling, so the exchanges between workgroups (h in the
+// forward loop, dz in the reverse loop) are exercised under orders of
+// arrival that the plain build rarely produces.  The plain build compiles it
+// away.
+__device__ inline void stress_delay(int t, int site) {
+#ifdef LDYN_STRESS
+    unsigned x = (unsigned)blockIdx.x * 0x9e3779b1u ^ (unsigned)(threadIdx.x >> 6) * 0x85ebca77u ^
+                 (unsigned)t * 0xc2b2ae3du ^ (unsigned)site * 0x27d4eb2fu;
+    x ^= x >> 15;
+    x *= 0x2c1b3c6du;
+    x ^= x >> 12;
+    const int n = __builtin_amdgcn_readfirstlane((int)(x & 31));
+    for (int i = 0; i < n; ++i) __builtin_amdgcn_s_sleep(1);
+#else
+    (void)t;
+    (void)site;
+#endif
+}
+
 }  // namespace ldyn

@@ -40,26 +40,6 @@ constexpr int P_LDS_KB = 144;           // dynamic LDS for partial sums and the 
 constexpr int P_MAX_ROWS = 512;         // batch rows the variants hold (8 owned row tiles per wave)
 constexpr int P_SC1 = 16;               // buffer-instruction cache policy: device scope
 
-// Timing stress (a diagnostic build, LDYN_STRESS defined): a wave sleeps for a
-// pseudo-random time (0 to about 1 us, from a hash of the workgroup, wave,
-// step and site) before it stores h, marks segments or starts polling, so
-// the exchange of h is exercised under orders of arrival that the plain
-// build rarely produces.  The plain build compiles it away.
-__device__ inline void stress_delay(int t, int site) {
-#ifdef LDYN_STRESS
-    unsigned x = (unsigned)blockIdx.x * 0x9e3779b1u ^ (unsigned)(threadIdx.x >> 6) * 0x85ebca77u ^
-                 (unsigned)t * 0xc2b2ae3du ^ (unsigned)site * 0x27d4eb2fu;
-    x ^= x >> 15;
-    x *= 0x2c1b3c6du;
-    x ^= x >> 12;
-    const int n = __builtin_amdgcn_readfirstlane((int)(x & 31));
-    for (int i = 0; i < n; ++i) __builtin_amdgcn_s_sleep(1);
-#else
-    (void)t;
-    (void)site;
-#endif
-}
-
 struct PersistParams {
     const void* U;
     const float* h0;

@@ -219,9 +219,10 @@ def test_backward_exact_facts(mode):
 
 @pytest.mark.parametrize("seq", [True, False], ids=["dseq", "final-state"])
 def test_backward_one_launch_reverse_loop(seq):
-    """bf16 data, at most 16 rows in every step, H even and above 64: the
-    whole reverse loop is one cooperative launch (dh0 from the launch
-    itself); against the oracle, and against the per-step path's launch count."""
+    """bf16 data, at most 16 rows in every step, H even and above 64 but not
+    a multiple of 256: the whole reverse loop is the launch for the steps
+    with few rows (dh0 from the launch itself); against the oracle, and
+    against the per-step path's launch count."""
     B, D, H, T = 9, 20, 96, 40
     inp = workloads.random_case(1201, B, D, H, T, dtype="bf16", lo=20)
     dh, dc, ds = upstream(2201, B, H, T, seq)
@@ -237,14 +238,44 @@ def test_backward_one_launch_reverse_loop(seq):
     assert launches < 30 <= 2 * int(inp.lengths.max()) <= per_step
 
 
+@pytest.mark.parametrize("seq", [True, False], ids=["dseq", "final-state"])
+def test_backward_whole_loop_launch(seq):
+    """bf16 data, H a multiple of 256: the whole reverse loop is one
+    cooperative launch with column blocks of U, whatever the rows per step
+    (up to 96 here); every gradient against the oracle, the launch count
+    against the per-step path's, and a second run bit for bit equal to the
+    first (the shares of dh and the waves' partial sums are added in a fixed
+    order, whatever the order in which the data arrive)."""
+    B, D, H, T = 96, 40, 256, 30
+    inp = workloads.random_case(1211, B, D, H, T, dtype="bf16")
+    dh, dc, ds = upstream(2211, B, H, T, seq)
+    L = inp.lengths
+    say(f"case bwd whole-loop launch seq={seq} rows per step "
+        f"{[int((L > t).sum()) for t in range(0, T, 5)]}")
+    g, _, m = run_train(inp, "persistent", dh, dc, ds)
+    launches = m.query(ld.Q_LAUNCHES_PER_FORWARD)
+    go = oracle_grads(inp, dh.astype(np.float64), dc.astype(np.float64),
+                      ds.astype(np.float64) if ds is not None else None)
+    compare(g, go, GRAD_TOL["bf16"])
+    g2, _, _ = run_train(inp, "persistent", dh, dc, ds, model=m)
+    for k in KEYS:
+        assert np.array_equal(g[k], g2[k]), k
+    _, _, mp = run_train(inp, "per_step", dh, dc, ds)
+    per_step = mp.query(ld.Q_LAUNCHES_PER_FORWARD)
+    say(f"  backward launches: {launches} (per-step path {per_step})")
+    assert launches < 30 <= 2 * int(L.max()) <= per_step
+    m.close()
+    mp.close()
+
+
 @pytest.mark.parametrize("scale", [1e-6, 1e6, 1e12])
 @pytest.mark.parametrize("mode", MODES)
 def test_backward_upstream_magnitude(scale, mode):
     """Gradients are linear in the upstream gradients: scaled by 1e-6 to 1e12
     they are scaled alike, and the fp16 operands of the bf16 path (powers of
     two per operand, per row and per row block) neither overflow nor lose
-    the largest entries.  Rows of the batch run both the one-launch reverse
-    loop (steps with at most 16 rows) and the per-step path."""
+    the largest entries.  With H = 100 the persistent handle runs the steps
+    with at most 16 rows in one launch and the others on the per-step path."""
     B, D, H, T = 33, 40, 100, 14
     inp = workloads.random_case(1401, B, D, H, T, dtype="bf16")
     dh, dc, ds = upstream(2401, B, H, T)

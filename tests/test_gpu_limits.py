@@ -77,12 +77,12 @@ def test_largest_per_step_batch():
 
 @pytest.mark.parametrize("dt", ["bf16", "f32"])
 def test_largest_persistent_batch_backward(dt):
-    """The backward at 512 rows, most of them short: steps 3 to 5 have at
-    most 16 rows, so with bf16 data the persistent handle runs them in its
-    one-launch reverse loop (fewer launches than the per-step handle, which
-    runs every step as two launches).  Per-row gradients of sampled rows
-    against the oracle run on those rows alone; every gradient against the
-    per-step handle's."""
+    """The backward at 512 rows, most of them short (steps 3 to 5 have at
+    most 16 rows): with bf16 data and H = 256 the persistent handle runs the
+    whole reverse loop in one launch with column blocks of U, at its largest
+    batch (fewer launches than the per-step handle, which runs every step as
+    two launches).  Per-row gradients of sampled rows against the oracle run
+    on those rows alone; every gradient against the per-step handle's."""
     import torch
     from tests.test_gpu_bwd import GRAD_TOL, compare, oracle_grads, run_train, scaled_err
     B, D, H, T = 512, 24, 256, 6

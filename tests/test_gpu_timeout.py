@@ -36,10 +36,15 @@ def test_forward_wait_bound():
     f.close()
 
 
-def test_backward_wait_bound():
-    """The one-launch reverse loop (bf16 data, at most 16 rows per step)."""
+@pytest.mark.parametrize("H", [512, 96], ids=["whole-loop-launch", "few-row-launch"])
+def test_backward_wait_bound(H):
+    """The reverse loop's cooperative launches (bf16 data): the whole loop
+    with column blocks of U (H a multiple of 256), and the launch for the
+    steps with at most 16 rows (other H).  Past the bound the launch stops
+    with ERR_TIMEOUT; with the bound restored the gradients equal a fresh
+    handle's bit for bit."""
     import torch
-    inp = workloads.random_case(1302, 16, 32, 512, 40, dtype="bf16", lo=20)
+    inp = workloads.random_case(1302, 16, 32, H, 40, dtype="bf16", lo=20)
     dev = to_device(inp)
     rng = np.random.default_rng(1303)
     dh = torch.from_numpy(rng.standard_normal((inp.B, inp.H)).astype(np.float32)).cuda()
