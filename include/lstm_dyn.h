@@ -91,7 +91,7 @@ enum {
     LSTM_DYN_ERR_NOMEM = 3,       /* device workspace allocation failed */
     LSTM_DYN_ERR_UNSUPPORTED = 4, /* sizes outside what the compiled kernel variants cover */
     LSTM_DYN_ERR_BAD_LENGTHS = 5, /* (device status) a length was outside [0, T_max] and was clamped */
-    LSTM_DYN_ERR_TIMEOUT = 6,     /* (device status) a grid barrier wait exceeded its bound */
+    LSTM_DYN_ERR_TIMEOUT = 6,     /* (device status) a wait of a cooperative kernel exceeded its bound */
     LSTM_DYN_ERR_TOO_LARGE = 7    /* lstm_dyn_forward_noalloc: the workspace exceeds its scratch */
 };
 
@@ -290,9 +290,9 @@ int lstm_dyn_set_option(lstm_dyn_t* h, int option, long long value);
  * ticks[0 .. capacity), synchronising the forward's stream; *count receives
  * the number of entries and *khz the clock rate.  A backward pass run as
  * one launch of the whole reverse loop (bf16 data, persistent handle, H a
- * multiple of 256) records there instead, at 4 t for step t: its start, the
- * column blocks' shares of dh published, the first grid barrier passed,
- * the cells done; at 4 max_len the start of the product for dh0.
+ * multiple of 256) records there instead, at 4 t for step t: its start, its
+ * share of dh published, its cells done (the other shares awaited), the
+ * marks for later steps issued; at 4 max_len the product for dh0.
  * Returns LSTM_DYN_OK, ERR_INVALID (option not set, NULL arguments) or ERR_HIP.
  */
 int lstm_dyn_step_trace(lstm_dyn_t* h, long long* ticks, int capacity, int* count, int* khz);

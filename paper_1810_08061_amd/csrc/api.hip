@@ -86,9 +86,9 @@ struct TrainWs {
     int loop_groups;        // workgroups of the few-row launch, or 0
     _Float16* dzx;          // [2][bpad][kp] each step's published dz
     float* dzs;             // [2][bpad][nblk] their scales
-    float* pdh;             // [2][4][bpad][H] the column blocks' shares of dh
-    unsigned* bar;          // [9 * 64] barrier counters
-    long long dzx_bytes, dzs_bytes;
+    float* pdh;             // [4][4][bpad][H] the column blocks' shares of dh
+    unsigned* bar;          // [9 * 64] barrier counters (the few-row launch)
+    long long dzx_bytes, dzs_bytes, pdh_bytes;
 };
 
 using namespace ldyn;
@@ -223,7 +223,7 @@ extern "C" const char* lstm_dyn_strerror(int status) {
         case LSTM_DYN_ERR_NOMEM: return "device workspace allocation failed";
         case LSTM_DYN_ERR_UNSUPPORTED: return "sizes not covered by the compiled kernel variants";
         case LSTM_DYN_ERR_BAD_LENGTHS: return "a sequence length was outside [0, T_max] and was clamped";
-        case LSTM_DYN_ERR_TIMEOUT: return "a grid barrier wait exceeded its bound";
+        case LSTM_DYN_ERR_TIMEOUT: return "a wait of a cooperative kernel exceeded its bound";
         case LSTM_DYN_ERR_TOO_LARGE:
             return "the workspace exceeds the allocation-free entry point's fixed scratch";
         default: return "unknown status";
@@ -777,16 +777,18 @@ static int ensure_train(lstm_dyn* h) {
     tw->loop_groups = pers16 && !tw->block_groups ? bwd_loop_fits(h->dims, h->num_cus) : 0;
     int kp = 0, nblk = 0;
     if (tw->loop_groups) bwd_loop_shape((int)H, &kp, &nblk);
+    int slots = 2;  // the few-row launch: by step parity
     if (tw->block_groups) {
         kp = (int)(4 * H);
         nblk = (int)(H / 8);
+        slots = 4;
     }
     const bool one_launch = tw->block_groups || tw->loop_groups;
-    tw->dzx_bytes = 2LL * 2 * bpad * kp;
-    tw->dzs_bytes = 4LL * 2 * bpad * nblk;
-    const long long odzx = take(tw->dzx_bytes), odzsc = take(tw->dzs_bytes),
-                    opdh = take(tw->block_groups ? 2LL * 4 * 4 * bpad * H : 0),
-                    obar = take(one_launch ? 9 * 64 * 4 : 0);
+    tw->dzx_bytes = 2LL * slots * bpad * kp;
+    tw->dzs_bytes = 4LL * slots * bpad * nblk;
+    tw->pdh_bytes = tw->block_groups ? 4LL * 4 * 4 * bpad * H : 0;
+    const long long odzx = take(tw->dzx_bytes), odzsc = take(tw->dzs_bytes), opdh = take(tw->pdh_bytes),
+                    obar = take(tw->loop_groups ? 9 * 64 * 4 : 0);
     if (hipMalloc(&tw->block, (size_t)o) != hipSuccess) {
         (void)hipGetLastError();
         delete tw;
@@ -816,7 +818,7 @@ static int ensure_train(lstm_dyn* h) {
     tw->dzx = one_launch ? reinterpret_cast<_Float16*>(base + odzx) : nullptr;
     tw->dzs = one_launch ? reinterpret_cast<float*>(base + odzsc) : nullptr;
     tw->pdh = tw->block_groups ? reinterpret_cast<float*>(base + opdh) : nullptr;
-    tw->bar = one_launch ? reinterpret_cast<unsigned*>(base + obar) : nullptr;
+    tw->bar = tw->loop_groups ? reinterpret_cast<unsigned*>(base + obar) : nullptr;
     if (hipHostMalloc(reinterpret_cast<void**>(&tw->host_offsets), (size_t)(T + 8) * sizeof(int32_t),
                       hipHostMallocDefault) != hipSuccess) {
         (void)hipFree(tw->block);
@@ -1053,13 +1055,13 @@ extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* le
         // unscaled for the step before them, and the others two launches each.
         int t_end = max_len;
         if (tw->block_groups) {
-            LD_CHECK(hipMemsetAsync(tw->bar, 0, 9 * 64 * sizeof(unsigned), s));
-            // the published dz and its scales start as the marker (all ones)
+            // the published dz, its scales and the shares of dh start as the
+            // marker (all ones)
             LD_CHECK(hipMemsetAsync(tw->dzx, 0xff, (size_t)tw->dzx_bytes, s));
             LD_CHECK(hipMemsetAsync(tw->dzs, 0xff, (size_t)tw->dzs_bytes, s));
+            LD_CHECK(hipMemsetAsync(tw->pdh, 0xff, (size_t)tw->pdh_bytes, s));
             LD_CHECK(launch_bwd_block(d, tw->u16, alpha_u, tw->save_h, tw->save_c, d_seq, tw->dH, tw->dC,
-                                      tw->dzx, tw->dzs, tw->pdh, tw->bar, h->timeout_ticks, h->trace,
-                                      h->ws, s));
+                                      tw->dzx, tw->dzs, tw->pdh, h->timeout_ticks, h->trace, h->ws, s));
             h->launches_last++;
             t_end = 0;
         } else if (tw->loop_groups) {

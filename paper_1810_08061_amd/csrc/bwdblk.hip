@@ -17,24 +17,28 @@
 //     columns (each row's 32-column block scaled by the power of two its
 //     writer chose, undone after that block's MFMA); the waves split the
 //     columns, their partial sums meet in LDS, and the workgroup's sums for
-//     its 32 units go to pdh[cb];
-//   * grid barrier (the shares are complete);
+//     its 32 units are published as its share;
 //   * cell: the 8 units [32 kb + 8 cb, + 8) of the rows of step t take dh =
-//     the four column blocks' shares in order (plus the carried term and the
-//     output sequence's gradient); the cell's backward gives dz (kept in
-//     fp32 over z for the weight gradients, published in fp16 under its row
-//     block's scale), dc and the carried term.
-// The published dz needs no barrier: a value not yet written for the step
-// holds the all-ones marker (a NaN the writers never store), and the next
-// product polls for it.  dz alternates between two slots by step parity;
-// after the barrier of step t every workgroup has read dz_{t+1}, so each
-// writer puts the marker back into its block of that slot for the rows of
-// step t-1, and the next barrier drains those stores before anyone reads or
-// writes dz_{t-1}.
+//     the four siblings' shares (kb, 0..3) in order (plus the carried term
+//     and the output sequence's gradient); the cell's backward gives dz (kept
+//     in fp32 over z for the weight gradients, published in fp16 under its
+//     row block's scale), dc and the carried term.
+// Neither exchange has a barrier.  A value not yet written for its step
+// holds the all-ones marker (a NaN that the writers never publish), and the
+// reader polls for it: the product polls the first row tile of each chunk of
+// dz (a marker that slipped into a later tile is a NaN in the sums, and the
+// chunk is redone with every tile polled), the cell polls the shares.  Each
+// exchange cycles through four slots by step.  A workgroup that has read all
+// its siblings' shares of step t knows that every workgroup has finished the
+// product of step t+1 (each sibling read dz_{t+1} from every writer of its
+// column block, and the four column blocks cover all workgroups), so it puts
+// the marker back into its blocks of the slots of the shares of step t+1 and
+// of dz_{t+2}; it drains those stores before it publishes anything more, so
+// a reader that has seen its later data sees the marks.
 // A workgroup reads a quarter of each row's dz (4 KB of fp16 at H = 2048, as
 // much as the forward loop reads of h per row), where one holding all 4H
-// columns of a few units would read all of it; the barrier per step, which
-// the exchange of the shares needs, is the price.
+// columns of a few units would read all of it; the exchange of the shares is
+// the price.
 // After the last step, one more product gives dh entering step 0: dH
 // receives dh0 (slot order, unscaled) and dC dc0.
 #include "launch.h"
@@ -46,6 +50,7 @@ constexpr int BB_NCB = 4;     // column blocks of U
 constexpr int BB_UNITS = 32;  // hidden units (rows of U) per block
 constexpr int BB_NTC = 8;     // row tiles per chunk of the product
 constexpr int BB_SC1 = 16;    // buffer-instruction cache policy: device scope
+constexpr int BB_RING = 4;    // slots of each exchange (dz and the shares of dh), by step
 constexpr int BB_LDS_BYTES = BB_WAVES * BB_NTC * 2 * 64 * 16;  // the waves' partial sums
 
 typedef unsigned bb_u32x2 __attribute__((ext_vector_type(2)));
@@ -62,22 +67,19 @@ struct BwdBlockParams {
     Meta* meta;              // max_len in, timeout status out
     float* dH;               // [B][H] carried dh: in d_out_h, out dh0 (slot order)
     float* dC;               // [B][H] carried dc: in d_out_c, out dc0
-    // Published dz in MFMA fragment order: [2][bpad / 16 row tiles][4H / 32
+    // Published dz in MFMA fragment order: [4 slots][bpad / 16 row tiles][4H / 32
     // column blocks][64 chunks of 16 bytes], chunk q * 16 + r holding row r
     // of the tile and columns 8 q .. 8 q + 7 of the block (fp16, each row's
     // block scaled by its own power of two); a wave's load of one block is
     // 1 KB of consecutive bytes.
     _Float16* dzx;
-    float* dzs;              // [2][bpad / 16][4H / 32][16 rows] the scales
-    // shares of dh: [2 step parities][4 column blocks][H / 32 unit blocks][bpad][32];
-    // by parity, since a workgroup may start the next step's product while a
-    // sibling still reads this step's shares
+    float* dzs;              // [4 slots][bpad / 16][4H / 32][16 rows] the scales
+    // shares of dh: [4 slots][4 column blocks][H / 32 unit blocks][bpad][32]
     float* pdh;
-    unsigned* bar;           // [9 * 64] barrier counters, zero at the launch
     unsigned long long timeout_ticks;
     // [T + 1][4] timestamps of workgroup 0, or null: per step t (at 4 t) its
-    // start, the shares published, the first barrier passed, the cells done;
-    // at 4 max_len the start of the product for dh0
+    // start, its shares published, its cells done (the siblings' shares
+    // awaited), the marks issued; at 4 max_len the product for dh0
     unsigned long long* trace;
     float alpha_u;           // 1 / su
     int B, H, T, bpad, groups;
@@ -90,7 +92,7 @@ template <int KSW, int CELL>
 __global__ void __launch_bounds__(BB_WAVES * 64, 1)
 bwd_block_kernel(BwdBlockParams p) {
     extern __shared__ __attribute__((aligned(16))) float lds[];  // [BB_WAVES][BB_NTC][2][64][4]
-    __shared__ int lds_ok, lds_nan, lds_abort;
+    __shared__ int lds_nan, lds_abort;
     // tid and l are re-read through empty asm statements at the top of each
     // step, so that addresses derived from them are recomputed where used
     // rather than kept live across the step (which made the variants with
@@ -119,14 +121,14 @@ bwd_block_kernel(BwdBlockParams p) {
                 p.u16 + (size_t)(k0 + 16 * kt + (l & 15)) * H4 + c0 + 32 * (ks0 + ks) + 8 * (l >> 4));
 
     const __amdgpu_buffer_rsrc_t Rz = __builtin_amdgcn_make_buffer_rsrc(
-        p.dzx, (short)0, (int)((size_t)2 * bpad * H4 * 2), 0x00020000);
+        p.dzx, (short)0, (int)((size_t)BB_RING * bpad * H4 * 2), 0x00020000);
     const __amdgpu_buffer_rsrc_t Rs = __builtin_amdgcn_make_buffer_rsrc(
-        p.dzs, (short)0, (int)((size_t)2 * bpad * NBLK * 4), 0x00020000);
+        p.dzs, (short)0, (int)((size_t)BB_RING * bpad * NBLK * 4), 0x00020000);
     const __amdgpu_buffer_rsrc_t Rp = __builtin_amdgcn_make_buffer_rsrc(
-        p.pdh, (short)0, (int)((size_t)2 * BB_NCB * bpad * H * 4), 0x00020000);
-    const unsigned NTP = bpad / 16;  // row tiles of one parity of the exchange
-    // byte offset of the share of dh of (step parity, column block c, row s,
-    // unit k) in pdh
+        p.pdh, (short)0, (int)((size_t)BB_RING * BB_NCB * bpad * H * 4), 0x00020000);
+    const unsigned NTP = bpad / 16;  // row tiles of one slot of the dz exchange
+    // byte offset of the share of dh of (slot, column block c, row s, unit k)
+    // in pdh
     auto share_off = [&](unsigned par, unsigned c, unsigned s, unsigned k) {
         return ((((par * BB_NCB + c) * (unsigned)NKB + (k >> 5)) * bpad + s) * 32u + (k & 31u)) * 4u;
     };
@@ -201,7 +203,6 @@ bwd_block_kernel(BwdBlockParams p) {
     const unsigned blk = (unsigned)((k0 + 8 * cb) >> 3);  // this workgroup's 32-column block of dz
     const int32_t* const off = p.offsets;
     const int max_len = p.meta->max_len;
-    int bk = 0;
     for (int t = max_len - 1; t >= -1; --t) {
         asm volatile("" : "+v"(tid), "+v"(l));
         // this thread's cell pairs: 8 lanes per row, one unit each
@@ -209,7 +210,8 @@ bwd_block_kernel(BwdBlockParams p) {
         const bool last = t < 0;  // only the product: dh entering step 0
         const int actp = t + 1 < max_len ? off[t + 2] - off[t + 1] : 0;  // rows with dz_{t+1}
         const int actc = last ? 0 : off[t + 1] - off[t];                // rows that run step t
-        const unsigned pin = (unsigned)((t + 1) & 1), pout = (unsigned)(t & 1);
+        // slots: dz_{t+1} read, and dz_t and the shares of step t written
+        const unsigned pin = (unsigned)((t + 1) & (BB_RING - 1)), pout = (unsigned)(t & (BB_RING - 1));
         // step trace: stamps kept in scalar registers, stored after the step
         const bool tr = p.trace && blockIdx.x == 0 && w == 0;
         const int ti = last ? max_len : t;
@@ -225,6 +227,7 @@ bwd_block_kernel(BwdBlockParams p) {
         // scale), and the chunk is then redone with every tile polled; a NaN
         // that the redo reproduces comes from the data and is kept.
         const int ntp = (actp + 15) >> 4;
+        __syncthreads();  // every wave is done with the last step's flags
         if (tid == 0) {
             lds_nan = 0;
             lds_abort = 0;
@@ -232,27 +235,55 @@ bwd_block_kernel(BwdBlockParams p) {
         __syncthreads();
         for (int ntc0 = 0; ntc0 < ntp; ntc0 += BB_NTC) {
             const int nchunk = min(BB_NTC, ntp - ntc0);
-            // the waves' partial sums in order, published; lane ln of (tile j,
-            // unit tile kt) holds units 16 kt + 4 (ln >> 4) .. + 3 of row
-            // (ln & 15).  Sets the flag if an active row's sum is a NaN.
-            auto reduce_publish = [&]() {
+            // The waves' partial sums in order, for the (at most two) entries
+            // (tile j, unit tile kt, lane ln) of this thread; lane ln holds
+            // units 16 kt + 4 (ln >> 4) .. + 3 of row (ln & 15).  Returns
+            // whether an active row's sum is a NaN.  They are published only
+            // once verified: a sibling reads them as soon as they arrive.
+            static_assert(BB_NTC * 128 <= 2 * BB_WAVES * 64, "two entries per thread");
+            f32x4_t sums[2];
+            auto reduce = [&]() {
                 bool nan = false;
-                for (int e = tid; e < nchunk * 128; e += BB_WAVES * 64) {
-                    const int j = e >> 7, kt = (e >> 6) & 1, ln = e & 63;
-                    f32x4_t sum = *reinterpret_cast<const f32x4_t*>(lds + (((j * 2 + kt) * 64 + ln) << 2));
+                int tq = tid;  // (addresses recomputed here, not kept live across the step)
+                asm volatile("" : "+v"(tq));
 #pragma unroll
-                    for (int ww = 1; ww < BB_WAVES; ++ww)
-                        sum += *reinterpret_cast<const f32x4_t*>(lds + ((((ww * BB_NTC + j) * 2 + kt) * 64 + ln) << 2));
-                    const int s = (ntc0 + j) * 16 + (ln & 15);
-                    if (s < actp) {
-                        nan |= (sum[0] != sum[0]) | (sum[1] != sum[1]) | (sum[2] != sum[2]) | (sum[3] != sum[3]);
-                        const unsigned k = (unsigned)(k0 + 16 * kt + 4 * (ln >> 4));
-                        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(bb_u32x4, sum), Rp,
-                                                               share_off(pout, (unsigned)cb, (unsigned)s, k), 0, BB_SC1);
+                for (int q = 0; q < 2; ++q) {
+                    const int e = tq + q * BB_WAVES * 64;
+                    if (e < nchunk * 128) {
+                        const int j = e >> 7, kt = (e >> 6) & 1, ln = e & 63;
+                        f32x4_t sum = *reinterpret_cast<const f32x4_t*>(lds + (((j * 2 + kt) * 64 + ln) << 2));
+#pragma unroll
+                        for (int ww = 1; ww < BB_WAVES; ++ww)
+                            sum += *reinterpret_cast<const f32x4_t*>(
+                                lds + ((((ww * BB_NTC + j) * 2 + kt) * 64 + ln) << 2));
+                        sums[q] = sum;
+                        if ((ntc0 + j) * 16 + (ln & 15) < actp)
+                            nan |= (sum[0] != sum[0]) | (sum[1] != sum[1]) | (sum[2] != sum[2]) | (sum[3] != sum[3]);
                     }
                 }
-                if (nan) lds_nan = 1;
-                __syncthreads();  // the partial sums and the flag are read before the next writes
+                return nan;
+            };
+            // (the sums formed again from the partial sums, which are still in
+            // LDS, rather than kept in registers across the redo)
+            auto publish = [&]() {
+                (void)reduce();
+                int tq = tid;
+                asm volatile("" : "+v"(tq));
+#pragma unroll
+                for (int q = 0; q < 2; ++q) {
+                    const int e = tq + q * BB_WAVES * 64;
+                    const int j = e >> 7, kt = (e >> 6) & 1, ln = e & 63;
+                    const int s = (ntc0 + j) * 16 + (ln & 15);
+                    if (e < nchunk * 128 && s < actp) {
+                        // an all-ones word (the marker) goes out as the canonical quiet NaN
+                        bb_u32x4 v = __builtin_bit_cast(bb_u32x4, sums[q]);
+#pragma unroll
+                        for (int x = 0; x < 4; ++x) v[x] = v[x] == 0xffffffffu ? 0x7fc00000u : v[x];
+                        const unsigned k = (unsigned)(k0 + 16 * kt + 4 * (ln >> 4));
+                        __builtin_amdgcn_raw_buffer_store_b128(v, Rp, share_off(pout, (unsigned)cb, (unsigned)s, k), 0,
+                                                               BB_SC1);
+                    }
+                }
             };
             // the first tile polled with registers of its own, which are free
             // again before the pipeline below starts (it loads the tile once
@@ -296,11 +327,12 @@ bwd_block_kernel(BwdBlockParams p) {
             }
             __syncthreads();
             if (lds_abort) return;  // read by every wave between the same two barriers
-            reduce_publish();
+            if (reduce()) lds_nan = 1;
+            __syncthreads();
             if (lds_nan) {  // (read by every wave between the same two barriers)
                 // a marker slipped into a tile used as loaded: once more with
-                // every tile polled
-                __syncthreads();  // every wave has read the flag
+                // every tile polled (a NaN then is the data's, and is kept)
+                __syncthreads();  // every wave has read the flag and its sums
                 if (tid == 0) lds_nan = 0;
                 for (int j = 0; j < nchunk; ++j) {
                     f16x8_t b[KSW];
@@ -311,37 +343,19 @@ bwd_block_kernel(BwdBlockParams p) {
                 }
                 __syncthreads();
                 if (lds_abort) return;
-                reduce_publish();
-                __syncthreads();  // every wave has read the flag (a NaN now is the data's)
-                if (tid == 0) lds_nan = 0;
             }
+            publish();
+            __syncthreads();  // the partial sums are read before the next chunk writes them
         }
         if (tr) ts[1] = wall_clock64();
-        if (!grid_barrier_bounded(p.bar, p.groups, bk++, p.timeout_ticks, p.meta, &lds_ok)) return;
-        if (tr) ts[2] = wall_clock64();
-        // Every workgroup has read dz_{t+1}: its slot, which takes dz_{t-1},
-        // gets the marker again in this workgroup's block for the rows of step
-        // t-1.  The next barrier drains these stores before any workgroup can
-        // read dz_{t-1}, and before this one writes it.
-        if (t >= 1) {
-            stress_delay(t, 200);
-            const int rows_m = off[t] - off[t - 1];
-            const unsigned slot = (unsigned)((t - 1) & 1);
-            for (int e = tid; e < rows_m * 4; e += BB_WAVES * 64) {
-                const int sm = e >> 2, q = e & 3;
-                const unsigned tb = (slot * NTP + (unsigned)(sm >> 4)) * (unsigned)NBLK + blk;
-                __builtin_amdgcn_raw_buffer_store_b128(bb_u32x4{~0u, ~0u, ~0u, ~0u}, Rz,
-                                                       tb * 1024u + ((unsigned)q * 16u + (unsigned)(sm & 15)) * 16u, 0,
-                                                       BB_SC1);
-                if (q == 0)
-                    __builtin_amdgcn_raw_buffer_store_b32(~0u, Rs, (tb * 16u + (unsigned)(sm & 15)) * 4u, 0, BB_SC1);
-            }
-        }
 
         // ---- cell: this workgroup's 8 units of the rows of step t, four rows
         // per thread at a time with all their loads issued before any use
-        // (rows past the end load row rows - 1 and store nothing)
+        // (rows past the end load row rows - 1 and store nothing).  The
+        // siblings' shares arrive without a barrier: they are polled until no
+        // active row's share holds the marker.
         const int rows = last ? actp : actc;
+        bool drained = false;
         for (int sb = tid >> 3; sb < rows; sb += 4 * BB_WAVES * 8) {
             float share[4][BB_NCB], dhc[4], dcc[4], hp[4], cp[4], ds[4];
             f32x4_t zv[4];
@@ -357,7 +371,7 @@ bwd_block_kernel(BwdBlockParams p) {
                         Rp, share_off(pout, (unsigned)c, sp, (unsigned)u), 0, BB_SC1));
                 const size_t su = (size_t)s * H + u;
                 dhc[i] = p.dH[su];
-                if (!last) {
+                if (!last) {  // (loaded while the shares are polled)
                     const size_t r = (size_t)off[t] + s;
                     zv[i] = *reinterpret_cast<const f32x4_t*>(p.gx + r * H4 + 4 * u);
                     hp[i] = p.save_h[r * H + u];
@@ -365,6 +379,43 @@ bwd_block_kernel(BwdBlockParams p) {
                     dcc[i] = p.dC[su];
                     ds[i] = p.dseq ? p.dseq[((size_t)p.perm[s] * p.T + t) * H + u] : 0.0f;
                 }
+            }
+            auto shares_marked = [&]() {
+                bool m = false;
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int c = 0; c < BB_NCB; ++c)
+                        m |= sb + i * BB_WAVES * 8 < actp && __float_as_uint(share[i][c]) == 0xffffffffu;
+                return __builtin_amdgcn_ballot_w64(m) != 0;
+            };
+            if (shares_marked()) {
+                const unsigned long long t0 = wall_clock64();
+                do {
+                    if (wall_clock64() - t0 > p.timeout_ticks) {
+                        if (l == 0)
+                            __hip_atomic_fetch_or(&p.meta->status, STATUS_TIMEOUT, __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_AGENT);
+                        return;  // the other workgroups' waits for this one end at their bounds
+                    }
+                    __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const unsigned sp =
+                            (unsigned)min(min(sb + i * BB_WAVES * 8, rows - 1), max(actp - 1, 0));
+#pragma unroll
+                        for (int c = 0; c < BB_NCB; ++c)
+                            share[i][c] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                                Rp, share_off(pout, (unsigned)c, sp, (unsigned)u), 0, BB_SC1));
+                    }
+                } while (shares_marked());
+            }
+            if (!drained) {
+                // The marks this workgroup stored after its last cell (below)
+                // complete before it publishes anything more, so a workgroup
+                // that sees its later data also sees those marks.
+                __builtin_amdgcn_s_waitcnt(0x0F70);
+                drained = true;
             }
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
@@ -421,6 +472,38 @@ bwd_block_kernel(BwdBlockParams p) {
                 }
             }
         }
+        if (tr) ts[2] = wall_clock64();
+        // This workgroup has read every sibling's shares of step t, so every
+        // sibling has finished its product of step t; each of those read dz_{t+1}
+        // from every writer of its column block, so every workgroup has
+        // finished its cell of step t+1 and its product of step t+1 (reading
+        // dz_{t+2}).  The marker therefore goes back into this workgroup's
+        // blocks of the slots of the shares of step t+1 and of dz_{t+2}, for
+        // the rows of step t-2, which are written there next (at steps t-3 and
+        // t-2).  The drain before this workgroup's next stores orders the
+        // marks before them.
+        if (t >= 2) {
+            stress_delay(t, 200);
+            const int rows_m = off[t - 1] - off[t - 2];
+            const unsigned zslot = (unsigned)((t + 2) & (BB_RING - 1));
+            const unsigned pslot = (unsigned)((t + 1) & (BB_RING - 1));
+            for (int e = tid; e < rows_m * 4; e += BB_WAVES * 64) {
+                const int sm = e >> 2, q = e & 3;
+                const unsigned tb = (zslot * NTP + (unsigned)(sm >> 4)) * (unsigned)NBLK + blk;
+                __builtin_amdgcn_raw_buffer_store_b128(bb_u32x4{~0u, ~0u, ~0u, ~0u}, Rz,
+                                                       tb * 1024u + ((unsigned)q * 16u + (unsigned)(sm & 15)) * 16u, 0,
+                                                       BB_SC1);
+                if (q == 0)
+                    __builtin_amdgcn_raw_buffer_store_b32(~0u, Rs, (tb * 16u + (unsigned)(sm & 15)) * 4u, 0, BB_SC1);
+            }
+            for (int e = tid; e < rows_m * 8; e += BB_WAVES * 64) {  // 8 x 16 bytes per row
+                const int sm = e >> 3, q = e & 7;
+                __builtin_amdgcn_raw_buffer_store_b128(bb_u32x4{~0u, ~0u, ~0u, ~0u}, Rp,
+                                                       share_off(pslot, (unsigned)cb, (unsigned)sm,
+                                                                 (unsigned)(k0 + 4 * q)),
+                                                       0, BB_SC1);
+            }
+        }
         if (tr) {
             ts[3] = wall_clock64();
             if (l == 0)
@@ -463,7 +546,7 @@ int bwd_block_fits(const Dims& d, int num_cus) {
 
 hipError_t launch_bwd_block(const Dims& d, const _Float16* u16, float alpha_u, const float* save_h,
                             const float* save_c, const float* dseq, float* dH, float* dC, _Float16* dzx,
-                            float* dzs, float* pdh, unsigned* bar, unsigned long long timeout_ticks,
+                            float* dzs, float* pdh, unsigned long long timeout_ticks,
                             unsigned long long* trace, const Workspace& ws, hipStream_t s) {
     bwd_block_fn f = bwd_block_pick(d.H, d.cell);
     if (!f || d.bpad > 512) return hipErrorInvalidValue;
@@ -481,7 +564,6 @@ hipError_t launch_bwd_block(const Dims& d, const _Float16* u16, float alpha_u, c
     p.dzx = dzx;
     p.dzs = dzs;
     p.pdh = pdh;
-    p.bar = bar;
     p.timeout_ticks = timeout_ticks;
     p.trace = trace;
     p.alpha_u = alpha_u;

@@ -156,16 +156,16 @@ hipError_t launch_bwd_loop(const Dims& d, const _Float16* u16, float alpha_u, co
                            int t_end, const Workspace& ws, hipStream_t s);
 // bf16 data, H a multiple of 256 (at most 2048): the whole reverse loop in one
 // cooperative launch (H / 8 workgroups, each with a 32-unit x H-column block
-// of U in registers; per step the blocks' shares of dh = dz U^T, a grid
-// barrier, the cell's backward of 8 units, whose dz the next step polls
-// for), leaving dh0 and dc0 in dH and dC.  bwd_block_fits: its workgroup
-// count, or 0 where it does not apply.  dzx [2][bpad][4H] fp16 and dzs
-// [2][bpad][H / 8] must be all ones (the marker) at the launch, bar [9 * 64]
-// zero; pdh [2][4][bpad][H]; trace [T + 1][4] or null.
+// of U in registers; per step the blocks' shares of dh = dz U^T, then the
+// cell's backward of 8 units, each exchange polled for, no grid barrier),
+// leaving dh0 and dc0 in dH and dC.  bwd_block_fits: its workgroup count, or
+// 0 where it does not apply.  dzx [4][bpad][4H] fp16, dzs [4][bpad][H / 8]
+// and pdh [4][4][bpad][H] must be all ones (the marker) at the launch; trace
+// [T + 1][4] or null.
 int bwd_block_fits(const Dims& d, int num_cus);
 hipError_t launch_bwd_block(const Dims& d, const _Float16* u16, float alpha_u, const float* save_h,
                             const float* save_c, const float* dseq, float* dH, float* dC, _Float16* dzx,
-                            float* dzs, float* pdh, unsigned* bar, unsigned long long timeout_ticks,
+                            float* dzs, float* pdh, unsigned long long timeout_ticks,
                             unsigned long long* trace, const Workspace& ws, hipStream_t s);
 hipError_t launch_bwd_gather_x(const Dims& d, const void* x, long rows, float* xc,
                                const Workspace& ws, hipStream_t s);
