@@ -22,7 +22,11 @@
 //     the four siblings' shares (kb, 0..3) in order (plus the carried term
 //     and the output sequence's gradient); the cell's backward gives dz (kept
 //     in fp32 over z for the weight gradients, published in fp16 under its
-//     row block's scale), dc and the carried term.
+//     row block's scale), dc and the carried term.  A thread takes the same
+//     (row, unit) pairs in every step, so where the batch pads to at most 256
+//     rows their carried dh and dc stay in LDS for the whole loop; and a
+//     step with many rows loads the cell's z and c (from HBM) right after
+//     publishing its shares, while the siblings' shares are still on their way.
 // Neither exchange has a barrier.  A value not yet written for its step
 // holds the all-ones marker (a NaN that the writers never publish), and the
 // reader polls for it: the product polls the first row tile of each chunk of
@@ -52,6 +56,14 @@ constexpr int BB_NTC = 8;     // row tiles per chunk of the product
 constexpr int BB_SC1 = 16;    // buffer-instruction cache policy: device scope
 constexpr int BB_RING = 4;    // slots of each exchange (dz and the shares of dh), by step
 constexpr int BB_LDS_BYTES = BB_WAVES * BB_NTC * 2 * 64 * 16;  // the waves' partial sums
+// With at most 256 padded rows (one row set per thread, 4 rows), the carried
+// dh and dc of each thread's (row, unit) pairs stay in LDS for the whole
+// loop: [2][4][512 threads] floats after the partial sums.
+constexpr int BB_RES_ROWS = 4 * BB_WAVES * 8;
+constexpr int BB_RES_BYTES = 2 * 4 * BB_WAVES * 64 * 4;
+// Steps with more rows than this load the cell's inputs right after the
+// product's last chunk (see the product).
+constexpr int BB_EARLY_ROWS = 64;
 
 typedef unsigned bb_u32x2 __attribute__((ext_vector_type(2)));
 typedef unsigned bb_u32x4 __attribute__((ext_vector_type(4)));
@@ -88,10 +100,11 @@ struct BwdBlockParams {
 // A chunk length as a type, for code unrolled per length.
 template <int N> struct BbLen { static constexpr int value = N; };
 
-template <int KSW, int CELL>
+template <int KSW, int CELL, bool RES>
 __global__ void __launch_bounds__(BB_WAVES * 64, 1)
 bwd_block_kernel(BwdBlockParams p) {
-    extern __shared__ __attribute__((aligned(16))) float lds[];  // [BB_WAVES][BB_NTC][2][64][4]
+    // [BB_WAVES][BB_NTC][2][64][4] partial sums, then (RES) the carried dh and dc
+    extern __shared__ __attribute__((aligned(16))) float lds[];
     __shared__ int lds_nan, lds_abort;
     // tid and l are re-read through empty asm statements at the top of each
     // step, so that addresses derived from them are recomputed where used
@@ -203,6 +216,20 @@ bwd_block_kernel(BwdBlockParams p) {
     const unsigned blk = (unsigned)((k0 + 8 * cb) >> 3);  // this workgroup's 32-column block of dz
     const int32_t* const off = p.offsets;
     const int max_len = p.meta->max_len;
+    // RES: thread tid's carried dh and dc of row (tid >> 3) + 64 i, unit
+    // k0 + 8 cb + (tid & 7), at [i][tid] (the rows and the unit of its cell
+    // pairs, the same in every step)
+    float* const lds_dh = lds + BB_LDS_BYTES / 4;
+    float* const lds_dc = lds_dh + 4 * BB_WAVES * 64;
+    if constexpr (RES) {
+        const int uc = k0 + 8 * cb + (tid & 7);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int s = (tid >> 3) + i * BB_WAVES * 8;
+            lds_dh[i * BB_WAVES * 64 + tid] = s < p.B ? p.dH[(size_t)s * H + uc] : 0.0f;
+            lds_dc[i * BB_WAVES * 64 + tid] = s < p.B ? p.dC[(size_t)s * H + uc] : 0.0f;
+        }
+    }
     for (int t = max_len - 1; t >= -1; --t) {
         asm volatile("" : "+v"(tid), "+v"(l));
         // this thread's cell pairs: 8 lanes per row, one unit each
@@ -233,8 +260,15 @@ bwd_block_kernel(BwdBlockParams p) {
             lds_abort = 0;
         }
         __syncthreads();
-        for (int ntc0 = 0; ntc0 < ntp; ntc0 += BB_NTC) {
-            const int nchunk = min(BB_NTC, ntp - ntc0);
+        // The cell's inputs of a step with many rows are loaded as soon as the
+        // product's last chunk is formed, so that their latency passes during
+        // that chunk's reduction, the publication and the wait for the
+        // siblings' shares (rows (tid >> 3) + 64 i, clamped, as in the cell).
+        const bool early = RES && !last && ntp > 0 && actc > BB_EARLY_ROWS;
+        f32x4_t zv[4];  // the cell's z, h and c of rows (tid >> 3) + 64 i
+        float hp[4], cp[4];
+        int ntc0 = 0, nchunk = 0;
+        {
             // The waves' partial sums in order, for the (at most two) entries
             // (tile j, unit tile kt, lane ln) of this thread; lane ln holds
             // units 16 kt + 4 (ln >> 4) .. + 3 of row (ln & 15).  Returns
@@ -285,16 +319,6 @@ bwd_block_kernel(BwdBlockParams p) {
                     }
                 }
             };
-            // the first tile polled with registers of its own, which are free
-            // again before the pipeline below starts (it loads the tile once
-            // more, from L2)
-            {
-                f16x8_t bp[KSW];
-                float sp[KSW];
-                stress_delay(t, 1 + ntc0);
-                load_tile(bp, sp, pin, ntc0);
-                if (!poll_tile(bp, sp, pin, ntc0, actp)) lds_abort = 1;
-            }
             // Straight-line code per chunk length: DEPTH tiles are in flight,
             // and a tile's register set is reloaded with the tile DEPTH ahead
             // as soon as its products are formed.  (With conditional loads the
@@ -315,19 +339,13 @@ bwd_block_kernel(BwdBlockParams p) {
                     __builtin_amdgcn_sched_barrier(0);
                 }
             };
-            switch (nchunk) {
-                case 1: chunk(BbLen<1>{}); break;
-                case 2: chunk(BbLen<2>{}); break;
-                case 3: chunk(BbLen<3>{}); break;
-                case 4: chunk(BbLen<4>{}); break;
-                case 5: chunk(BbLen<5>{}); break;
-                case 6: chunk(BbLen<6>{}); break;
-                case 7: chunk(BbLen<7>{}); break;
-                default: chunk(BbLen<BB_NTC>{}); break;
-            }
-            __syncthreads();
-            if (lds_abort) return;  // read by every wave between the same two barriers
-            if (reduce()) lds_nan = 1;
+            // The chunk's sums checked, redone if a marker slipped in, and
+            // published; false if a wait ran out.  After publishing its last
+            // chunk, a step with many rows loads the cell's inputs.
+            auto finish = [&](bool last_chunk) {
+                __syncthreads();
+                if (lds_abort) return false;  // read by every wave between the same two barriers
+                if (reduce()) lds_nan = 1;
             __syncthreads();
             if (lds_nan) {  // (read by every wave between the same two barriers)
                 // a marker slipped into a tile used as loaded: once more with
@@ -342,10 +360,50 @@ bwd_block_kernel(BwdBlockParams p) {
                     mma_tile(b, sc, j);
                 }
                 __syncthreads();
-                if (lds_abort) return;
+                if (lds_abort) return false;
             }
             publish();
+            if (last_chunk && early) {
+                int tq = tid;
+                asm volatile("" : "+v"(tq));
+                const int uq = k0 + 8 * cb + (tq & 7);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const size_t r = (size_t)off[t] + min((tq >> 3) + i * BB_WAVES * 8, actc - 1);
+                    zv[i] = *reinterpret_cast<const f32x4_t*>(p.gx + r * H4 + 4 * uq);
+                    hp[i] = p.save_h[r * H + uq];
+                    cp[i] = p.save_c[r * H + uq];
+                }
+            }
             __syncthreads();  // the partial sums are read before the next chunk writes them
+            return true;
+            };
+            for (; ntc0 < ntp; ntc0 += BB_NTC) {
+                nchunk = min(BB_NTC, ntp - ntc0);
+                // the first tile polled with registers of its own, which are
+                // free again before the pipeline below starts (it loads the
+                // tile once more, from L2)
+                {
+                    f16x8_t bp[KSW];
+                    float sp[KSW];
+                    stress_delay(t, 1 + ntc0);
+                    load_tile(bp, sp, pin, ntc0);
+                    if (!poll_tile(bp, sp, pin, ntc0, actp)) lds_abort = 1;
+                }
+                switch (nchunk) {
+                    case 1: chunk(BbLen<1>{}); break;
+                    case 2: chunk(BbLen<2>{}); break;
+                    case 3: chunk(BbLen<3>{}); break;
+                    case 4: chunk(BbLen<4>{}); break;
+                    case 5: chunk(BbLen<5>{}); break;
+                    case 6: chunk(BbLen<6>{}); break;
+                    case 7: chunk(BbLen<7>{}); break;
+                    default: chunk(BbLen<BB_NTC>{}); break;
+                }
+                if (ntc0 + BB_NTC >= ntp) break;  // the last chunk is finished below
+                if (!finish(false)) return;
+            }
+            if (ntp > 0 && !finish(true)) return;
         }
         if (tr) ts[1] = wall_clock64();
 
@@ -357,8 +415,7 @@ bwd_block_kernel(BwdBlockParams p) {
         const int rows = last ? actp : actc;
         bool drained = false;
         for (int sb = tid >> 3; sb < rows; sb += 4 * BB_WAVES * 8) {
-            float share[4][BB_NCB], dhc[4], dcc[4], hp[4], cp[4], ds[4];
-            f32x4_t zv[4];
+            float share[4][BB_NCB], dhc[4], dcc[4], ds[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int s = min(sb + i * BB_WAVES * 8, rows - 1);
@@ -370,13 +427,15 @@ bwd_block_kernel(BwdBlockParams p) {
                     share[i][c] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
                         Rp, share_off(pout, (unsigned)c, sp, (unsigned)u), 0, BB_SC1));
                 const size_t su = (size_t)s * H + u;
-                dhc[i] = p.dH[su];
+                dhc[i] = RES ? lds_dh[i * BB_WAVES * 64 + tid] : p.dH[su];
                 if (!last) {  // (loaded while the shares are polled)
                     const size_t r = (size_t)off[t] + s;
-                    zv[i] = *reinterpret_cast<const f32x4_t*>(p.gx + r * H4 + 4 * u);
-                    hp[i] = p.save_h[r * H + u];
-                    cp[i] = p.save_c[r * H + u];
-                    dcc[i] = p.dC[su];
+                    if (!early) {
+                        zv[i] = *reinterpret_cast<const f32x4_t*>(p.gx + r * H4 + 4 * u);
+                        hp[i] = p.save_h[r * H + u];
+                        cp[i] = p.save_c[r * H + u];
+                    }
+                    dcc[i] = RES ? lds_dc[i * BB_WAVES * 64 + tid] : p.dC[su];
                     ds[i] = p.dseq ? p.dseq[((size_t)p.perm[s] * p.T + t) * H + u] : 0.0f;
                 }
             }
@@ -427,7 +486,8 @@ bwd_block_kernel(BwdBlockParams p) {
                     float dh = (s < actp ? sum * p.alpha_u : 0.0f) + dhc[i];
                     const size_t su = (size_t)s * H + u;
                     if (last) {  // dh entering step 0: dh0
-                        p.dH[su] = dh;
+                        if constexpr (RES) lds_dh[i * BB_WAVES * 64 + tid] = dh;
+                        else p.dH[su] = dh;
                         continue;
                     }
                     dh += ds[i];
@@ -435,8 +495,13 @@ bwd_block_kernel(BwdBlockParams p) {
                     float dcp, dhd;
                     const f32x4_t dz = cell_backward<CELL>(zv[i], hp[i], cp[i], dh, dcc[i], dcp, dhd);
                     *reinterpret_cast<f32x4_t*>(p.gx + r * H4 + 4 * u) = dz;
-                    p.dC[su] = dcp;
-                    p.dH[su] = dhd;
+                    if constexpr (RES) {
+                        lds_dc[i * BB_WAVES * 64 + tid] = dcp;
+                        lds_dh[i * BB_WAVES * 64 + tid] = dhd;
+                    } else {
+                        p.dC[su] = dcp;
+                        p.dH[su] = dhd;
+                    }
                     // the row block's scale: its largest magnitude into [2^13, 2^14)
                     unsigned m = 0;
 #pragma unroll
@@ -471,6 +536,7 @@ bwd_block_kernel(BwdBlockParams p) {
                                                               (tb * 16u + (unsigned)(s & 15)) * 4u, 0, BB_SC1);
                 }
             }
+            if constexpr (RES) break;  // at most 256 rows: one pass (and no loop for the compiler)
         }
         if (tr) ts[2] = wall_clock64();
         // This workgroup has read every sibling's shares of step t, so every
@@ -511,33 +577,49 @@ bwd_block_kernel(BwdBlockParams p) {
                 for (int e = 0; e < 4; ++e) p.trace[4 * ti + e] = ts[e];
         }
     }
+    if constexpr (RES) {
+        const int uc = k0 + 8 * cb + (tid & 7);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int s = (tid >> 3) + i * BB_WAVES * 8;
+            if (s < p.B) {
+                p.dH[(size_t)s * H + uc] = lds_dh[i * BB_WAVES * 64 + tid];
+                p.dC[(size_t)s * H + uc] = lds_dc[i * BB_WAVES * 64 + tid];
+            }
+        }
+    }
     // nothing of this wave in flight when it ends
     __builtin_amdgcn_s_waitcnt(0x0F70);
 }
 
 typedef void (*bwd_block_fn)(BwdBlockParams);
 
-static bwd_block_fn bwd_block_pick(int H, int cell) {
-#define BB_CELLS(K)                                                                         \
-    if (H == 256 * K)                                                                       \
-        return cell == CELL_GRU ? bwd_block_kernel<K, CELL_GRU>                             \
-               : cell == CELL_RNN ? bwd_block_kernel<K, CELL_RNN> : bwd_block_kernel<K, CELL_LSTM>;
-    BB_CELLS(1) BB_CELLS(2) BB_CELLS(4) BB_CELLS(8)
+static bwd_block_fn bwd_block_pick(int H, int cell, bool res) {
+#define BB_CELLS(K, R)                                                                           \
+    if (H == 256 * K && res == R)                                                                \
+        return cell == CELL_GRU ? bwd_block_kernel<K, CELL_GRU, R>                               \
+               : cell == CELL_RNN ? bwd_block_kernel<K, CELL_RNN, R> : bwd_block_kernel<K, CELL_LSTM, R>;
+    BB_CELLS(1, true) BB_CELLS(2, true) BB_CELLS(4, true) BB_CELLS(8, true)
+    BB_CELLS(1, false) BB_CELLS(2, false) BB_CELLS(4, false) BB_CELLS(8, false)
 #undef BB_CELLS
     return nullptr;
+}
+
+static int bwd_block_lds(const Dims& d) {
+    return BB_LDS_BYTES + (d.bpad <= BB_RES_ROWS ? BB_RES_BYTES : 0);
 }
 
 int bwd_block_fits(const Dims& d, int num_cus) {
     if (!d.bf16 || d.H % 256 != 0 || d.H > 2048 || d.bpad > 512) return 0;
     const int groups = d.H / 8;
     if (groups > num_cus) return 0;
-    bwd_block_fn f = bwd_block_pick(d.H, d.cell);
+    bwd_block_fn f = bwd_block_pick(d.H, d.cell, d.bpad <= BB_RES_ROWS);
     if (!f) return 0;
     int n = 0;
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(f), hipFuncAttributeMaxDynamicSharedMemorySize,
-                            BB_LDS_BYTES) != hipSuccess ||
+                            bwd_block_lds(d)) != hipSuccess ||
         hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, reinterpret_cast<const void*>(f), BB_WAVES * 64,
-                                                     BB_LDS_BYTES) != hipSuccess) {
+                                                     bwd_block_lds(d)) != hipSuccess) {
         (void)hipGetLastError();  // not an error of a later call: another path serves
         return 0;
     }
@@ -548,7 +630,7 @@ hipError_t launch_bwd_block(const Dims& d, const _Float16* u16, float alpha_u, c
                             const float* save_c, const float* dseq, float* dH, float* dC, _Float16* dzx,
                             float* dzs, float* pdh, unsigned long long timeout_ticks,
                             unsigned long long* trace, const Workspace& ws, hipStream_t s) {
-    bwd_block_fn f = bwd_block_pick(d.H, d.cell);
+    bwd_block_fn f = bwd_block_pick(d.H, d.cell, d.bpad <= BB_RES_ROWS);
     if (!f || d.bpad > 512) return hipErrorInvalidValue;
     BwdBlockParams p{};
     p.u16 = u16;
@@ -574,7 +656,7 @@ hipError_t launch_bwd_block(const Dims& d, const _Float16* u16, float alpha_u, c
     p.groups = d.H / 8;
     void* args[] = {&p};
     return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(f), dim3(p.groups), dim3(BB_WAVES * 64),
-                                      args, (unsigned)BB_LDS_BYTES, s);
+                                      args, (unsigned)bwd_block_lds(d), s);
 }
 
 }  // namespace ldyn
