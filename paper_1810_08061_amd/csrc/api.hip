@@ -1061,7 +1061,8 @@ extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* le
             LD_CHECK(hipMemsetAsync(tw->dzs, 0xff, (size_t)tw->dzs_bytes, s));
             LD_CHECK(hipMemsetAsync(tw->pdh, 0xff, (size_t)tw->pdh_bytes, s));
             LD_CHECK(launch_bwd_block(d, tw->u16, alpha_u, tw->save_h, tw->save_c, d_seq, tw->dH, tw->dC,
-                                      tw->dzx, tw->dzs, tw->pdh, h->timeout_ticks, h->trace, h->ws, s));
+                                      tw->dzx, tw->dzs, tw->pdh, tw->amax + 0, h->timeout_ticks, h->trace,
+                                      h->ws, s));
             h->launches_last++;
             t_end = 0;
         } else if (tw->loop_groups) {
@@ -1093,7 +1094,8 @@ extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* le
     }
     h->launches_last++;
     if (rows > 0) {
-        LD_CHECK(launch_bwd_gather_x(d, x, rows, tw->xc, h->ws, s));
+        // (bf16: the largest |x| of the rows for x's fp16 scale, in the same pass)
+        LD_CHECK(launch_bwd_gather_x(d, x, rows, tw->xc, d.bf16 ? tw->amax + 1 : nullptr, h->ws, s));
         h->launches_last++;
         if (!d.bf16) {
             // db = dz^T 1 (K = the sum of lengths)
@@ -1114,8 +1116,9 @@ extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* le
             // alpha undoing the scales
             const long n_dz = (long)rows * H4, n_x = (long)rows * d.D, n_h = (long)rows * d.H,
                        n_w = (long)d.D * H4;
-            LD_CHECK(launch_bwd_absmax(h->ws.gx, n_dz, tw->amax + 0, s));
-            LD_CHECK(launch_bwd_absmax(tw->xc, n_x, tw->amax + 1, s));
+            // (the whole-loop launch took the largest |dz| as it went, and the
+            // gather of x its largest |x|)
+            if (!tw->block_groups) LD_CHECK(launch_bwd_absmax(h->ws.gx, n_dz, tw->amax + 0, s));
             LD_CHECK(launch_bwd_absmax(tw->save_h, n_h, tw->amax + 2, s));
             LD_CHECK(launch_bwd_absmax(tw->w_il, n_w, tw->amax + 3, s));
             unsigned* am = reinterpret_cast<unsigned*>(tw->host_offsets + d.T + 3);
@@ -1142,7 +1145,7 @@ extern "C" int lstm_dyn_backward(lstm_dyn_t* h, const void* x, const int32_t* le
                                      rows, H4, &a_x, tw->w16, f16, H4, tw->dz16, f16, H4, &zero,
                                      tw->xc, f32, d.D, tw->xc, f32, d.D, f32,
                                      rocblas_gemm_algo_standard, 0, 0));
-            h->launches_last += 12;
+            h->launches_last += tw->block_groups ? 10 : 11;
         }
     } else {
         LD_CHECK(hipMemsetAsync(tw->dw_il, 0, (size_t)d.D * H4 * sizeof(float), s));

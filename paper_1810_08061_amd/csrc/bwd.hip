@@ -186,17 +186,49 @@ __global__ void bwd_ones_kernel(float* a, int n) {
     if (i < n) a[i] = 1.0f;
 }
 
-// x rows in the compact order, fp32.
-template <typename S>
+// The workgroup's largest value of m (256 threads) into *out by one atomic
+// maximum: many atomics on one address queue behind each other.
+__device__ inline void block_max_to(unsigned m, unsigned* out) {
+    __shared__ unsigned red[4];
+    for (int o = 32; o > 0; o >>= 1) m = max(m, (unsigned)__shfl_xor((int)m, o));
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) atomicMax(out, max(max(red[0], red[1]), max(red[2], red[3])));
+}
+
+// x rows in the compact order, fp32, one wave per row (VEC: four elements
+// per lane and load, D a multiple of 4 and x aligned to four elements).  With
+// amax, the largest |x| of those rows (as bits) goes there too.
+template <typename S, bool VEC>
 __global__ void __launch_bounds__(256)
 bwd_gather_x_kernel(const S* __restrict__ x, const int32_t* __restrict__ rowsrc,
-                    const Meta* __restrict__ meta, float* xc, int D) {
-    const long n = (long)meta->total_rows * D;
-    for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += (long)gridDim.x * 256) {
-        const long r = i / D;
-        const int k = (int)(i - r * D);
-        xc[i] = (float)x[(long)rowsrc[r] * D + k];
+                    const Meta* __restrict__ meta, float* __restrict__ xc, int D, unsigned* amax) {
+    const long rows = meta->total_rows;
+    const int lane = threadIdx.x & 63;
+    unsigned m = 0;
+    for (long r = blockIdx.x * 4L + (threadIdx.x >> 6); r < rows; r += gridDim.x * 4L) {
+        const S* src = x + (long)rowsrc[r] * D;
+        float* dst = xc + r * D;
+        if constexpr (VEC) {
+            typedef S s4_t __attribute__((ext_vector_type(4)));
+#pragma unroll 4
+            for (int k = lane; k < D / 4; k += 64) {
+                const s4_t v = reinterpret_cast<const s4_t*>(src)[k];
+                const f32x4_t f = f32x4_t{(float)v[0], (float)v[1], (float)v[2], (float)v[3]};
+                reinterpret_cast<f32x4_t*>(dst)[k] = f;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) m = max(m, __float_as_uint(f[e]) & 0x7fffffffu);
+            }
+        } else {
+#pragma unroll 4
+            for (int k = lane; k < D; k += 64) {
+                const float f = (float)src[k];
+                dst[k] = f;
+                m = max(m, __float_as_uint(f) & 0x7fffffffu);
+            }
+        }
     }
+    if (amax) block_max_to(m, amax);
 }
 
 // Interleaved columns -> the caller's gate blocks: out[k][g H + u] = il[k][4u + g].
@@ -231,24 +263,33 @@ bwd_unpack_kernel(const float* __restrict__ il, float* out, int rows, int H, int
     }
 }
 
-// dx [B][T][D]: the compact rows' dz W^T at their (b, t), zero elsewhere.  The
-// two loops write disjoint rows.
+// dx [B][T][D], one wave per row (b, t): the compact row's dz W^T where b
+// runs step t (t below its clamped length), zeros elsewhere; every element is
+// written once.  The compact row of (b, t) is offsets[t] + the slot of b in
+// the length sort, whose inverse the workgroup first builds in LDS.  VEC: four
+// elements per lane and access (D a multiple of 4, dx 16-byte aligned).
+template <bool VEC>
 __global__ void __launch_bounds__(256)
-bwd_dx_kernel(const float* __restrict__ dxc, const int32_t* __restrict__ rowsrc,
-              const Meta* __restrict__ meta, const int32_t* __restrict__ lengths, float* dx, int B,
-              int T, int D) {
-    const long rows = meta->total_rows;
-    const long n = rows * D;
-    for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += (long)gridDim.x * 256) {
-        const long r = i / D;
-        const int k = (int)(i - r * D);
-        dx[(long)rowsrc[r] * D + k] = dxc[i];
-    }
-    const long m = (long)B * T * D;
-    for (long i = blockIdx.x * 256L + threadIdx.x; i < m; i += (long)gridDim.x * 256) {
-        const long bt = i / D;
-        const int b = (int)(bt / T), t = (int)(bt - (long)b * T);
-        if (t >= min(max(lengths[b], 0), T)) dx[i] = 0.0f;
+bwd_dx_kernel(const float* __restrict__ dxc, const int32_t* __restrict__ perm,
+              const int32_t* __restrict__ offsets, const int32_t* __restrict__ lengths, float* dx,
+              int B, int T, int D) {
+    extern __shared__ int32_t slot_of[];  // [B] batch row -> slot
+    for (int i = threadIdx.x; i < B; i += 256) slot_of[perm[i]] = i;
+    __syncthreads();
+    const int lane = threadIdx.x & 63;
+    const long n = (long)B * T;
+    for (long q = blockIdx.x * 4L + (threadIdx.x >> 6); q < n; q += gridDim.x * 4L) {
+        const int b = (int)(q / T), t = (int)(q - (long)b * T);
+        const bool runs = t < min(max(lengths[b], 0), T);
+        const float* src = dxc + (runs ? (long)(offsets[t] + slot_of[b]) * D : 0);
+        float* dst = dx + q * D;
+        if constexpr (VEC) {
+            for (int k = lane; k < D / 4; k += 64)
+                reinterpret_cast<f32x4_t*>(dst)[k] =
+                    runs ? reinterpret_cast<const f32x4_t*>(src)[k] : f32x4_t{0.f, 0.f, 0.f, 0.f};
+        } else {
+            for (int k = lane; k < D; k += 64) dst[k] = runs ? src[k] : 0.0f;
+        }
     }
 }
 
@@ -260,13 +301,29 @@ bwd_dx_kernel(const float* __restrict__ dxc, const int32_t* __restrict__ rowsrc,
 
 // Largest |a| of n floats (as bits): the bits of non-negative floats order as
 // integers, so an integer atomic maximum gives the same result in any order.
+// a is 16-byte aligned: four elements per load, then the tail.
 __global__ void __launch_bounds__(256)
 bwd_absmax_kernel(const float* __restrict__ a, long n, unsigned* out) {
     unsigned m = 0;
-    for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += (long)gridDim.x * 256)
-        m = max(m, __float_as_uint(fabsf(a[i])) & 0x7fffffffu);
-    for (int o = 32; o > 0; o >>= 1) m = max(m, (unsigned)__shfl_xor((int)m, o));
-    if ((threadIdx.x & 63) == 0) atomicMax(out, m);
+    const long n4 = n >> 2, stride = (long)gridDim.x * 256;
+    long i = blockIdx.x * 256L + threadIdx.x;
+    for (; i + 3 * stride < n4; i += 4 * stride) {  // four loads in flight
+        f32x4_t v[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = reinterpret_cast<const f32x4_t*>(a)[i + j * stride];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) m = max(m, __float_as_uint(v[j][e]) & 0x7fffffffu);
+    }
+    for (; i < n4; i += stride) {
+        const f32x4_t v = reinterpret_cast<const f32x4_t*>(a)[i];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) m = max(m, __float_as_uint(v[e]) & 0x7fffffffu);
+    }
+    for (long i = 4 * n4 + blockIdx.x * 256L + threadIdx.x; i < n; i += (long)gridDim.x * 256)
+        m = max(m, __float_as_uint(a[i]) & 0x7fffffffu);
+    block_max_to(m, out);
 }
 
 // db = dz^T 1 over all compact rows: the rows are cut into BWD_CS_CHUNKS
@@ -305,10 +362,19 @@ bwd_colsum_finish_kernel(const float* __restrict__ part, int ncols, float* __res
     out[c] = s;
 }
 
-// dst = fp16(src * scale), n elements.
+// dst = fp16(src * scale), n elements (both 16-byte aligned: four elements per
+// access, then the tail).
 __global__ void __launch_bounds__(256)
 bwd_to_f16_kernel(const float* __restrict__ src, _Float16* dst, long n, float scale) {
-    for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += (long)gridDim.x * 256)
+    typedef _Float16 h4_t __attribute__((ext_vector_type(4)));
+    const long n4 = n >> 2;
+    for (long i = blockIdx.x * 256L + threadIdx.x; i < n4; i += (long)gridDim.x * 256) {
+        const f32x4_t v = reinterpret_cast<const f32x4_t*>(src)[i];
+        reinterpret_cast<h4_t*>(dst)[i] =
+            h4_t{(_Float16)(v[0] * scale), (_Float16)(v[1] * scale), (_Float16)(v[2] * scale),
+                 (_Float16)(v[3] * scale)};
+    }
+    for (long i = 4 * n4 + blockIdx.x * 256L + threadIdx.x; i < n; i += (long)gridDim.x * 256)
         dst[i] = (_Float16)(src[i] * scale);
 }
 
@@ -379,20 +445,33 @@ hipError_t launch_bwd_ones(float* a, int n, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_bwd_gather_x(const Dims& d, const void* x, long rows, float* xc,
+hipError_t launch_bwd_gather_x(const Dims& d, const void* x, long rows, float* xc, unsigned* amax,
                                const Workspace& ws, hipStream_t s) {
-    const unsigned g = grid_of(rows * d.D);
-    if (d.bf16)
-        hipLaunchKernelGGL(bwd_gather_x_kernel<__bf16>, dim3(g), dim3(256), 0, s,
-                           static_cast<const __bf16*>(x), ws.rowsrc, ws.meta, xc, d.D);
-    else
-        hipLaunchKernelGGL(bwd_gather_x_kernel<float>, dim3(g), dim3(256), 0, s,
-                           static_cast<const float*>(x), ws.rowsrc, ws.meta, xc, d.D);
+    const long g4 = (rows + 3) / 4;
+    const unsigned g = (unsigned)(g4 < 1 ? 1 : g4 > 1024 ? 1024 : g4);
+    const uintptr_t xa = reinterpret_cast<uintptr_t>(x);
+    if (d.bf16) {
+        const __bf16* xs = static_cast<const __bf16*>(x);
+        if (d.D % 4 == 0 && (xa & 7) == 0)
+            hipLaunchKernelGGL((bwd_gather_x_kernel<__bf16, true>), dim3(g), dim3(256), 0, s, xs, ws.rowsrc,
+                               ws.meta, xc, d.D, amax);
+        else
+            hipLaunchKernelGGL((bwd_gather_x_kernel<__bf16, false>), dim3(g), dim3(256), 0, s, xs, ws.rowsrc,
+                               ws.meta, xc, d.D, amax);
+    } else {
+        const float* xs = static_cast<const float*>(x);
+        if (d.D % 4 == 0 && (xa & 15) == 0)
+            hipLaunchKernelGGL((bwd_gather_x_kernel<float, true>), dim3(g), dim3(256), 0, s, xs, ws.rowsrc,
+                               ws.meta, xc, d.D, amax);
+        else
+            hipLaunchKernelGGL((bwd_gather_x_kernel<float, false>), dim3(g), dim3(256), 0, s, xs, ws.rowsrc,
+                               ws.meta, xc, d.D, amax);
+    }
     return hipGetLastError();
 }
 
 hipError_t launch_bwd_absmax(const float* a, long n, unsigned* out, hipStream_t s) {
-    const unsigned g = grid_of(n) < 2048 ? grid_of(n) : 2048;
+    const unsigned g = grid_of(n / 4) < 1024 ? grid_of(n / 4) : 1024;
     hipLaunchKernelGGL(bwd_absmax_kernel, dim3(g), dim3(256), 0, s, a, n, out);
     return hipGetLastError();
 }
@@ -424,9 +503,16 @@ hipError_t launch_bwd_permute(const Dims& d, const float* il, float* out, int ro
 
 hipError_t launch_bwd_dx(const Dims& d, const float* dxc, long rows, const int32_t* lengths,
                          float* dx, const Workspace& ws, hipStream_t s) {
-    const long n = rows * d.D > (long)d.B * d.T * d.D ? rows * d.D : (long)d.B * d.T * d.D;
-    hipLaunchKernelGGL(bwd_dx_kernel, dim3(grid_of(n)), dim3(256), 0, s, dxc, ws.rowsrc, ws.meta,
-                       lengths, dx, d.B, d.T, d.D);
+    (void)rows;
+    const long g4 = ((long)d.B * d.T + 3) / 4;
+    const unsigned g = (unsigned)(g4 < 1 ? 1 : g4 > 4096 ? 4096 : g4);
+    const size_t lds = (size_t)d.B * sizeof(int32_t);
+    if (d.D % 4 == 0 && (reinterpret_cast<uintptr_t>(dx) & 15) == 0)
+        hipLaunchKernelGGL(bwd_dx_kernel<true>, dim3(g), dim3(256), lds, s, dxc, ws.perm, ws.offsets, lengths,
+                           dx, d.B, d.T, d.D);
+    else
+        hipLaunchKernelGGL(bwd_dx_kernel<false>, dim3(g), dim3(256), lds, s, dxc, ws.perm, ws.offsets, lengths,
+                           dx, d.B, d.T, d.D);
     return hipGetLastError();
 }
 

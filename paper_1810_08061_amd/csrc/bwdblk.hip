@@ -61,6 +61,8 @@ constexpr int BB_LDS_BYTES = BB_WAVES * BB_NTC * 2 * 64 * 16;  // the waves' par
 // loop: [2][4][512 threads] floats after the partial sums.
 constexpr int BB_RES_ROWS = 4 * BB_WAVES * 8;
 constexpr int BB_RES_BYTES = 2 * 4 * BB_WAVES * 64 * 4;
+// Each thread's largest |dz| so far (float bits), after the partial sums.
+constexpr int BB_AMAX_BYTES = BB_WAVES * 64 * 4;
 // Steps with more rows than this load the cell's inputs right after the
 // product's last chunk (see the product).
 constexpr int BB_EARLY_ROWS = 64;
@@ -88,6 +90,7 @@ struct BwdBlockParams {
     float* dzs;              // [4 slots][bpad / 16][4H / 32][16 rows] the scales
     // shares of dh: [4 slots][4 column blocks][H / 32 unit blocks][bpad][32]
     float* pdh;
+    unsigned* amax;          // largest |dz| over all rows, float bits (atomic maximum)
     unsigned long long timeout_ticks;
     // [T + 1][4] timestamps of workgroup 0, or null: per step t (at 4 t) its
     // start, its shares published, its cells done (the siblings' shares
@@ -103,7 +106,8 @@ template <int N> struct BbLen { static constexpr int value = N; };
 template <int KSW, int CELL, bool RES>
 __global__ void __launch_bounds__(BB_WAVES * 64, 1)
 bwd_block_kernel(BwdBlockParams p) {
-    // [BB_WAVES][BB_NTC][2][64][4] partial sums, then (RES) the carried dh and dc
+    // [BB_WAVES][BB_NTC][2][64][4] partial sums, each thread's largest |dz|, then
+    // (RES) the carried dh and dc
     extern __shared__ __attribute__((aligned(16))) float lds[];
     __shared__ int lds_nan, lds_abort;
     // tid and l are re-read through empty asm statements at the top of each
@@ -219,8 +223,10 @@ bwd_block_kernel(BwdBlockParams p) {
     // RES: thread tid's carried dh and dc of row (tid >> 3) + 64 i, unit
     // k0 + 8 cb + (tid & 7), at [i][tid] (the rows and the unit of its cell
     // pairs, the same in every step)
-    float* const lds_dh = lds + BB_LDS_BYTES / 4;
+    unsigned* const lds_am = reinterpret_cast<unsigned*>(lds + BB_LDS_BYTES / 4);
+    float* const lds_dh = lds + (BB_LDS_BYTES + BB_AMAX_BYTES) / 4;
     float* const lds_dc = lds_dh + 4 * BB_WAVES * 64;
+    lds_am[tid] = 0u;
     if constexpr (RES) {
         const int uc = k0 + 8 * cb + (tid & 7);
 #pragma unroll
@@ -469,6 +475,7 @@ bwd_block_kernel(BwdBlockParams p) {
                     }
                 } while (shares_marked());
             }
+            unsigned am = 0;  // largest |dz| of this thread's rows in the pass
             if (!drained) {
                 // The marks this workgroup stored after its last cell (below)
                 // complete before it publishes anything more, so a workgroup
@@ -507,6 +514,7 @@ bwd_block_kernel(BwdBlockParams p) {
 #pragma unroll
                     for (int e = 0; e < 4; ++e) m = max(m, __float_as_uint(fabsf(dz[e])) & 0x7fffffffu);
                     for (int o = 4; o > 0; o >>= 1) m = max(m, (unsigned)__shfl_xor((int)m, o));
+                    am = max(am, m);
                     const float mf = __uint_as_float(m);
                     float sc = 1.0f;
                     if (mf > 0.0f && mf < 3.0e38f) {
@@ -536,6 +544,7 @@ bwd_block_kernel(BwdBlockParams p) {
                                                               (tb * 16u + (unsigned)(s & 15)) * 4u, 0, BB_SC1);
                 }
             }
+            lds_am[tid] = max(lds_am[tid], am);
             if constexpr (RES) break;  // at most 256 rows: one pass (and no loop for the compiler)
         }
         if (tr) ts[2] = wall_clock64();
@@ -588,6 +597,17 @@ bwd_block_kernel(BwdBlockParams p) {
             }
         }
     }
+    {  // the largest |dz|: one atomic maximum per workgroup
+        unsigned m = lds_am[tid];
+        for (int o = 32; o > 0; o >>= 1) m = max(m, (unsigned)__shfl_xor((int)m, o));
+        __syncthreads();  // every slot has been read
+        if (l == 0) lds_am[w] = m;
+        __syncthreads();
+        if (tid == 0) {
+            for (int ww = 1; ww < BB_WAVES; ++ww) m = max(m, lds_am[ww]);
+            atomicMax(p.amax, m);
+        }
+    }
     // nothing of this wave in flight when it ends
     __builtin_amdgcn_s_waitcnt(0x0F70);
 }
@@ -606,7 +626,7 @@ static bwd_block_fn bwd_block_pick(int H, int cell, bool res) {
 }
 
 static int bwd_block_lds(const Dims& d) {
-    return BB_LDS_BYTES + (d.bpad <= BB_RES_ROWS ? BB_RES_BYTES : 0);
+    return BB_LDS_BYTES + BB_AMAX_BYTES + (d.bpad <= BB_RES_ROWS ? BB_RES_BYTES : 0);
 }
 
 int bwd_block_fits(const Dims& d, int num_cus) {
@@ -628,7 +648,7 @@ int bwd_block_fits(const Dims& d, int num_cus) {
 
 hipError_t launch_bwd_block(const Dims& d, const _Float16* u16, float alpha_u, const float* save_h,
                             const float* save_c, const float* dseq, float* dH, float* dC, _Float16* dzx,
-                            float* dzs, float* pdh, unsigned long long timeout_ticks,
+                            float* dzs, float* pdh, unsigned* amax_dz, unsigned long long timeout_ticks,
                             unsigned long long* trace, const Workspace& ws, hipStream_t s) {
     bwd_block_fn f = bwd_block_pick(d.H, d.cell, d.bpad <= BB_RES_ROWS);
     if (!f || d.bpad > 512) return hipErrorInvalidValue;
@@ -646,6 +666,7 @@ hipError_t launch_bwd_block(const Dims& d, const _Float16* u16, float alpha_u, c
     p.dzx = dzx;
     p.dzs = dzs;
     p.pdh = pdh;
+    p.amax = amax_dz;
     p.timeout_ticks = timeout_ticks;
     p.trace = trace;
     p.alpha_u = alpha_u;

@@ -161,13 +161,16 @@ hipError_t launch_bwd_loop(const Dims& d, const _Float16* u16, float alpha_u, co
 // leaving dh0 and dc0 in dH and dC.  bwd_block_fits: its workgroup count, or
 // 0 where it does not apply.  dzx [4][bpad][4H] fp16, dzs [4][bpad][H / 8]
 // and pdh [4][4][bpad][H] must be all ones (the marker) at the launch; trace
-// [T + 1][4] or null.
+// [T + 1][4] or null.  amax_dz receives the largest |dz| over all compact
+// rows (float bits, atomic maximum: it must hold 0 or a lower bound).
 int bwd_block_fits(const Dims& d, int num_cus);
 hipError_t launch_bwd_block(const Dims& d, const _Float16* u16, float alpha_u, const float* save_h,
                             const float* save_c, const float* dseq, float* dH, float* dC, _Float16* dzx,
-                            float* dzs, float* pdh, unsigned long long timeout_ticks,
+                            float* dzs, float* pdh, unsigned* amax_dz, unsigned long long timeout_ticks,
                             unsigned long long* trace, const Workspace& ws, hipStream_t s);
-hipError_t launch_bwd_gather_x(const Dims& d, const void* x, long rows, float* xc,
+// xc = the compact rows of x in fp32; amax (or null) receives the largest
+// |x| of them, as float bits, by atomic maximum.
+hipError_t launch_bwd_gather_x(const Dims& d, const void* x, long rows, float* xc, unsigned* amax,
                                const Workspace& ws, hipStream_t s);
 // fp16 operands of the backward's GEMMs: the largest magnitude (as float bits,
 // atomic and order free) and a scaled conversion.
