@@ -122,8 +122,8 @@ def test_backward_large_workload_sub_batch(mode):
     """large2048_bf16 at its full shape (D 1024, H 2048, T_max 1000) on 20 rows
     spread over its length range (the longest, 1000 steps, and the shortest
     included), run on their own handle: every gradient against the oracle.
-    The first 64 steps have more than 16 rows (two launches per step on the
-    persistent handle), the rest fewer (its one-launch reverse loop)."""
+    On the persistent handle the whole reverse loop is one launch (bf16 data,
+    H a multiple of 256), with the carried gradients held in LDS."""
     import torch
     name = "large2048_bf16"
     full = workloads.workload_inputs(name)
