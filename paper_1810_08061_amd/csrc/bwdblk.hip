@@ -24,9 +24,9 @@
 //     in fp32 over z for the weight gradients, published in fp16 under its
 //     row block's scale), dc and the carried term.  A thread takes the same
 //     (row, unit) pairs in every step, so where the batch pads to at most 256
-//     rows their carried dh and dc stay in LDS for the whole loop; and a
-//     step with many rows loads the cell's z and c (from HBM) right after
-//     publishing its shares, while the siblings' shares are still on their way.
+//     rows their carried dh and dc stay in LDS for the whole loop, and a
+//     step loads the cell's z and c (from HBM) right after publishing its
+//     shares, while the siblings' shares are still on their way.
 // Neither exchange has a barrier.  A value not yet written for its step
 // holds the all-ones marker (a NaN that the writers never publish), and the
 // reader polls for it: the product polls the first row tile of each chunk of
@@ -63,9 +63,6 @@ constexpr int BB_RES_ROWS = 4 * BB_WAVES * 8;
 constexpr int BB_RES_BYTES = 2 * 4 * BB_WAVES * 64 * 4;
 // Each thread's largest |dz| so far (float bits), after the partial sums.
 constexpr int BB_AMAX_BYTES = BB_WAVES * 64 * 4;
-// Steps with more rows than this load the cell's inputs right after the
-// product's last chunk (see the product).
-constexpr int BB_EARLY_ROWS = 64;
 
 typedef unsigned bb_u32x2 __attribute__((ext_vector_type(2)));
 typedef unsigned bb_u32x4 __attribute__((ext_vector_type(4)));
@@ -266,11 +263,11 @@ bwd_block_kernel(BwdBlockParams p) {
             lds_abort = 0;
         }
         __syncthreads();
-        // The cell's inputs of a step with many rows are loaded as soon as the
-        // product's last chunk is formed, so that their latency passes during
-        // that chunk's reduction, the publication and the wait for the
-        // siblings' shares (rows (tid >> 3) + 64 i, clamped, as in the cell).
-        const bool early = RES && !last && ntp > 0 && actc > BB_EARLY_ROWS;
+        // The cell's inputs (fresh rows from HBM every step) are loaded as
+        // soon as the product's last chunk is published, so that their latency
+        // passes during the wait for the siblings' shares (rows (tid >> 3) +
+        // 64 i, clamped, as in the cell).
+        const bool early = RES && !last && ntp > 0;
         f32x4_t zv[4];  // the cell's z, h and c of rows (tid >> 3) + 64 i
         float hp[4], cp[4];
         int ntc0 = 0, nchunk = 0;
@@ -347,7 +344,7 @@ bwd_block_kernel(BwdBlockParams p) {
             };
             // The chunk's sums checked, redone if a marker slipped in, and
             // published; false if a wait ran out.  After publishing its last
-            // chunk, a step with many rows loads the cell's inputs.
+            // chunk, a step loads the cell's inputs.
             auto finish = [&](bool last_chunk) {
                 __syncthreads();
                 if (lds_abort) return false;  // read by every wave between the same two barriers
