@@ -326,7 +326,10 @@ bwd_block_kernel(BwdBlockParams p) {
             // and a tile's register set is reloaded with the tile DEPTH ahead
             // as soon as its products are formed.  (With conditional loads the
             // compiler waits for all loads in flight before every product, and
-            // a wave then has one tile in flight.)
+            // a wave then has one tile in flight.)  Reloading the polled first
+            // tile instead of using it cost a load round trip per chunk.
+            f16x8_t bp[KSW];  // the chunk's first tile, polled
+            float sp[KSW];
             auto chunk = [&](auto len) {
                 constexpr int N = decltype(len)::value;
                 constexpr int DEPTH = KSW >= 8 ? 2 : 4;
@@ -334,7 +337,12 @@ bwd_block_kernel(BwdBlockParams p) {
                 f16x8_t b[DEPTH][KSW];
                 float sc[DEPTH][KSW];
 #pragma unroll
-                for (int j = 0; j < D0; ++j) load_tile(b[j], sc[j], pin, ntc0 + j);
+                for (int ks = 0; ks < KSW; ++ks) {
+                    b[0][ks] = bp[ks];
+                    sc[0][ks] = sp[ks];
+                }
+#pragma unroll
+                for (int j = 1; j < D0; ++j) load_tile(b[j], sc[j], pin, ntc0 + j);
 #pragma unroll
                 for (int j = 0; j < N; ++j) {
                     mma_tile(b[j % DEPTH], sc[j % DEPTH], j);
@@ -383,16 +391,11 @@ bwd_block_kernel(BwdBlockParams p) {
             };
             for (; ntc0 < ntp; ntc0 += BB_NTC) {
                 nchunk = min(BB_NTC, ntp - ntc0);
-                // the first tile polled with registers of its own, which are
-                // free again before the pipeline below starts (it loads the
-                // tile once more, from L2)
-                {
-                    f16x8_t bp[KSW];
-                    float sp[KSW];
-                    stress_delay(t, 1 + ntc0);
-                    load_tile(bp, sp, pin, ntc0);
-                    if (!poll_tile(bp, sp, pin, ntc0, actp)) lds_abort = 1;
-                }
+                // the first tile is polled; the pipeline starts from it, its
+                // loads complete, while the next tiles are loaded
+                stress_delay(t, 1 + ntc0);
+                load_tile(bp, sp, pin, ntc0);
+                if (!poll_tile(bp, sp, pin, ntc0, actp)) lds_abort = 1;
                 switch (nchunk) {
                     case 1: chunk(BbLen<1>{}); break;
                     case 2: chunk(BbLen<2>{}); break;
