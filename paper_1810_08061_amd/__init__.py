@@ -389,12 +389,14 @@ class LstmDyn:
         return (out_h, out_c) if out_seq is None else (out_h, out_c, out_seq)
 
     def backward(self, x, lengths, W, U, b, h0, c0, d_out_h, d_out_c=None, d_seq=None,
-                 stream=None):
+                 stream=None, out=None):
         """Gradients after ``forward_train`` with the same inputs; returns a
         dict of float32 tensors dx [B, T, D], dW [D, G], dU [H, G], db, dh0
         [B, H] and, for the LSTM, dc0 [B, H] (G and db as the cell's weights:
         LSTM 4H, [4H]; GRU 3H, [6H] = d b_ih ++ d b_hh; RNN H, [H]).  GRU and
-        RNN ignore c0 and d_out_c (None allowed)."""
+        RNN ignore c0 and d_out_c (None allowed).  out: a dict with those keys
+        holding caller-owned contiguous tensors of those shapes (4-byte
+        aligned), which receive the gradients and are returned."""
         import torch
         B, D, H, T = self.B, self.D, self.H, self.T
         g, nb = _CELL_SHAPES[self.cell]
@@ -405,11 +407,16 @@ class LstmDyn:
             self._check("d_out_c", d_out_c, torch.float32, (B, H))
         if d_seq is not None:
             self._check("d_seq", d_seq, torch.float32, (B, T, H))
-        out = {"dx": torch.empty((B, T, D), device=dev), "dW": torch.empty((D, g * H), device=dev),
-               "dU": torch.empty((H, g * H), device=dev), "db": torch.empty((nb * H,), device=dev),
-               "dh0": torch.empty((B, H), device=dev)}
+        shapes = {"dx": (B, T, D), "dW": (D, g * H), "dU": (H, g * H), "db": (nb * H,), "dh0": (B, H)}
         if lstm:
-            out["dc0"] = torch.empty((B, H), device=dev)
+            shapes["dc0"] = (B, H)
+        if out is None:
+            out = {k: torch.empty(v, device=dev) for k, v in shapes.items()}
+        else:
+            if sorted(out) != sorted(shapes):
+                raise ValueError(f"out must hold exactly {sorted(shapes)}")
+            for k, v in shapes.items():
+                self._check(k, out[k], torch.float32, v)
         if stream is None:
             stream = torch.cuda.current_stream(dev)
         s = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)

@@ -286,3 +286,35 @@ def test_backward_upstream_magnitude(scale, mode):
         assert np.all(np.isfinite(g[k])), k
     go = oracle_grads(inp, dh.astype(np.float64), dc.astype(np.float64), ds.astype(np.float64))
     compare(g, go, GRAD_TOL["bf16"])
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_backward_unaligned_dx(mode):
+    """dx need only be 4-byte aligned: a dx 4 bytes past a 16-byte boundary
+    (D a multiple of 4, so only the alignment sends its writer to the scalar
+    path) receives the same bits as the default 16-byte aligned one, and so
+    do the other gradients."""
+    import torch
+    B, D, H, T = 19, 8, 256, 9
+    inp = workloads.random_case(3301, B, D, H, T, dtype="bf16")
+    dh, dc, ds = upstream(3302, B, H, T)
+    say(f"case bwd unaligned dx {mode}")
+    m = ld.LstmDyn(B, D, H, T, inp.dtype, mode)
+    dev = to_device(inp)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    m.forward_train(*dev)
+    g = m.backward(*dev, t(dh), t(dc), t(ds))
+    buf = torch.empty(B * T * D + 4, device="cuda")
+    assert buf.data_ptr() % 16 == 0
+    out = {k: torch.empty_like(v) for k, v in g.items()}
+    out["dx"] = buf[1:1 + B * T * D].view(B, T, D)
+    assert out["dx"].data_ptr() % 16 == 4
+    m.forward_train(*dev)
+    g2 = m.backward(*dev, t(dh), t(dc), t(ds), out=out)
+    torch.cuda.synchronize()
+    assert m.query(ld.Q_LAST_STATUS) == ld.OK
+    assert g2 is out
+    for k in g:
+        assert torch.equal(g[k], g2[k]), k
+    m.close()
+
