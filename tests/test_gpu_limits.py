@@ -75,17 +75,20 @@ def test_largest_per_step_batch():
     m.close()
 
 
-@pytest.mark.parametrize("dt", ["bf16", "f32"])
-def test_largest_persistent_batch_backward(dt):
+@pytest.mark.parametrize("dt,H", [("bf16", 256), ("f32", 256), ("bf16", 2048)])
+def test_largest_persistent_batch_backward(dt, H):
     """The backward at 512 rows, most of them short (steps 3 to 5 have at
-    most 16 rows): with bf16 data and H = 256 the persistent handle runs the
-    whole reverse loop in one launch with column blocks of U, at its largest
-    batch (fewer launches than the per-step handle, which runs every step as
-    two launches).  Per-row gradients of sampled rows against the oracle run
-    on those rows alone; every gradient against the per-step handle's."""
+    most 16 rows): with bf16 data and H a multiple of 256 the persistent
+    handle runs the whole reverse loop in one launch with column blocks of U,
+    at its largest batch, with the carried gradients in memory rather than
+    LDS (more than 256 padded rows), at the smallest and the largest U block
+    per wave (H = 256 and 2048); fewer launches than the per-step handle,
+    which runs every step as two launches.  Per-row gradients of sampled rows
+    against the oracle run on those rows alone; every gradient against the
+    per-step handle's."""
     import torch
     from tests.test_gpu_bwd import GRAD_TOL, compare, oracle_grads, run_train, scaled_err
-    B, D, H, T = 512, 24, 256, 6
+    B, D, T = 512, 24, 6
     inp = workloads.random_case(4200, B, D, H, T, dtype=dt)
     rng = np.random.default_rng(4201)
     L = rng.integers(1, 4, B).astype(np.int32)
