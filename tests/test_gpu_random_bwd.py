@@ -3,8 +3,9 @@ shapes (ragged batch, input and hidden widths, time extents), dtypes, modes
 and cells, with and without the output sequence's gradient, each against the
 fp64 oracle's gradients at the backward's bar (scaled max-abs error within
 1e-5 with fp32 data, 3e-3 with bf16 data).  With bf16 data on persistent
-handles, hidden widths that are even and at least 16 take the one-launch
-reverse loop for their steps with at most 16 rows."""
+handles, hidden widths that are even and at least 16 take the few-row launch
+for their steps with at most 16 rows (cases 30 to 39), and hidden widths that
+are multiples of 256 the whole reverse loop in one launch (cases 40 to 49)."""
 import numpy as np
 import pytest
 
@@ -31,13 +32,16 @@ def _draw(k):
     mode = str(rng.choice(["persistent", "per_step"]))
     cell = str(rng.choice(["lstm", "gru", "rnn"]))
     seq = bool(rng.integers(0, 2))
-    if k >= 30:  # cases for the one-launch reverse loop
+    if 30 <= k < 40:  # cases for the few-row launch
         H = int(rng.choice([16, 18, 32, 64, 66, 100, 128, 250, 300]))
+        dt, mode = "bf16", "persistent"
+    if k >= 40:  # cases for the whole-loop launch
+        H = int(rng.choice([256, 512]))
         dt, mode = "bf16", "persistent"
     return B, D, H, T, dt, mode, cell, seq
 
 
-@pytest.mark.parametrize("k", list(range(40)))
+@pytest.mark.parametrize("k", list(range(50)))
 def test_random_backward(k):
     B, D, H, T, dt, mode, cell, seq = _draw(k)
     say(f"case random bwd {k}: B={B} D={D} H={H} T={T} {dt} {mode} {cell} dseq={seq}")
