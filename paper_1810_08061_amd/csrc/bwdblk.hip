@@ -300,10 +300,10 @@ bwd_block_kernel(BwdBlockParams p) {
                 }
                 return nan;
             };
-            // (the sums formed again from the partial sums, which are still in
-            // LDS, rather than kept in registers across the redo)
-            auto publish = [&]() {
-                (void)reduce();
+            // (after a redo the sums are formed again from the partial sums,
+            // which are still in LDS, rather than kept in registers across it)
+            auto publish = [&](bool again) {
+                if (again) (void)reduce();
                 int tq = tid;
                 asm volatile("" : "+v"(tq));
 #pragma unroll
@@ -358,7 +358,8 @@ bwd_block_kernel(BwdBlockParams p) {
                 if (lds_abort) return false;  // read by every wave between the same two barriers
                 if (reduce()) lds_nan = 1;
             __syncthreads();
-            if (lds_nan) {  // (read by every wave between the same two barriers)
+            const bool redo = lds_nan != 0;  // (read by every wave between the same two barriers)
+            if (redo) {
                 // a marker slipped into a tile used as loaded: once more with
                 // every tile polled (a NaN then is the data's, and is kept)
                 __syncthreads();  // every wave has read the flag and its sums
@@ -373,7 +374,7 @@ bwd_block_kernel(BwdBlockParams p) {
                 __syncthreads();
                 if (lds_abort) return false;
             }
-            publish();
+            publish(redo);  // (the checked sums, or, after a redo, the new ones)
             if (last_chunk && early) {
                 int tq = tid;
                 asm volatile("" : "+v"(tq));
