@@ -65,6 +65,9 @@ constexpr int BB_RES_BYTES = 2 * 4 * BB_WAVES * 64 * 4;
 constexpr int BB_AMAX_BYTES = BB_WAVES * 64 * 4;
 
 typedef unsigned bb_u32x2 __attribute__((ext_vector_type(2)));
+// Data written before the kernel started and only read by it (the step
+// offsets), seen through the constant address space: scalar loads.
+typedef const __attribute__((address_space(4))) int32_t bb_const_i32;
 typedef unsigned bb_u32x4 __attribute__((ext_vector_type(4)));
 
 struct BwdBlockParams {
@@ -233,13 +236,22 @@ bwd_block_kernel(BwdBlockParams p) {
             lds_dc[i * BB_WAVES * 64 + tid] = s < p.B ? p.dC[(size_t)s * H + uc] : 0.0f;
         }
     }
+    // Step offsets off[t - 2] .. off[t + 2] travel in registers (scalars); the
+    // one for the step after next is loaded a step ahead.  Indices are
+    // clamped into [0, max_len]; the values they give outside the loop's
+    // range are not used.
+    const bb_const_i32* const offc = (const bb_const_i32*)off;
+    auto off_at = [&](int i) { return offc[max(min(i, max_len), 0)]; };
+    int o_m2 = off_at(max_len - 3), o_m1 = off_at(max_len - 2), o_0 = off_at(max_len - 1),
+        o_p1 = off_at(max_len), o_p2 = off_at(max_len + 1);
     for (int t = max_len - 1; t >= -1; --t) {
+        const int o_next = off_at(t - 3);  // off[t - 3]: off[t - 2] of the next step
         asm volatile("" : "+v"(tid), "+v"(l));
         // this thread's cell pairs: 8 lanes per row, one unit each
         const int ul = tid & 7, u = k0 + 8 * cb + ul;
         const bool last = t < 0;  // only the product: dh entering step 0
-        const int actp = t + 1 < max_len ? off[t + 2] - off[t + 1] : 0;  // rows with dz_{t+1}
-        const int actc = last ? 0 : off[t + 1] - off[t];                // rows that run step t
+        const int actp = t + 1 < max_len ? o_p2 - o_p1 : 0;  // rows with dz_{t+1}
+        const int actc = last ? 0 : o_p1 - o_0;             // rows that run step t
         // slots: dz_{t+1} read, and dz_t and the shares of step t written
         const unsigned pin = (unsigned)((t + 1) & (BB_RING - 1)), pout = (unsigned)(t & (BB_RING - 1));
         // step trace: stamps kept in scalar registers, stored after the step
@@ -381,7 +393,7 @@ bwd_block_kernel(BwdBlockParams p) {
                 const int uq = k0 + 8 * cb + (tq & 7);
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const size_t r = (size_t)off[t] + min((tq >> 3) + i * BB_WAVES * 8, actc - 1);
+                    const size_t r = (size_t)o_0 + min((tq >> 3) + i * BB_WAVES * 8, actc - 1);
                     zv[i] = *reinterpret_cast<const f32x4_t*>(p.gx + r * H4 + 4 * uq);
                     hp[i] = p.save_h[r * H + uq];
                     cp[i] = p.save_c[r * H + uq];
@@ -436,7 +448,7 @@ bwd_block_kernel(BwdBlockParams p) {
                 const size_t su = (size_t)s * H + u;
                 dhc[i] = RES ? lds_dh[i * BB_WAVES * 64 + tid] : p.dH[su];
                 if (!last) {  // (loaded while the shares are polled)
-                    const size_t r = (size_t)off[t] + s;
+                    const size_t r = (size_t)o_0 + s;
                     if (!early) {
                         zv[i] = *reinterpret_cast<const f32x4_t*>(p.gx + r * H4 + 4 * u);
                         hp[i] = p.save_h[r * H + u];
@@ -499,7 +511,7 @@ bwd_block_kernel(BwdBlockParams p) {
                         continue;
                     }
                     dh += ds[i];
-                    const size_t r = (size_t)off[t] + s;
+                    const size_t r = (size_t)o_0 + s;
                     float dcp, dhd;
                     const f32x4_t dz = cell_backward<CELL>(zv[i], hp[i], cp[i], dh, dcc[i], dcp, dhd);
                     *reinterpret_cast<f32x4_t*>(p.gx + r * H4 + 4 * u) = dz;
@@ -560,7 +572,7 @@ bwd_block_kernel(BwdBlockParams p) {
         // marks before them.
         if (t >= 2) {
             stress_delay(t, 200);
-            const int rows_m = off[t - 1] - off[t - 2];
+            const int rows_m = o_m1 - o_m2;
             const unsigned zslot = (unsigned)((t + 2) & (BB_RING - 1));
             const unsigned pslot = (unsigned)((t + 1) & (BB_RING - 1));
             for (int e = tid; e < rows_m * 4; e += BB_WAVES * 64) {
@@ -586,6 +598,11 @@ bwd_block_kernel(BwdBlockParams p) {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) p.trace[4 * ti + e] = ts[e];
         }
+        o_p2 = o_p1;
+        o_p1 = o_0;
+        o_0 = o_m1;
+        o_m1 = o_m2;
+        o_m2 = o_next;
     }
     if constexpr (RES) {
         const int uc = k0 + 8 * cb + (tid & 7);
