@@ -51,6 +51,27 @@ def test_largest_persistent_batch(shape):
     ms.close()
 
 
+@pytest.mark.parametrize("mode", ["persistent", "per_step"])
+def test_long_sequences(mode):
+    """More than 2048 steps: the length preparation hands each wave its steps
+    in batches of 64 (one offset per lane), so a bound past 2048 takes three
+    batches.  Every row against the oracle; the valid-row count and the steps
+    run against the lengths."""
+    B, D, H, T = 40, 16, 64, 2600
+    inp = workloads.random_case(4050, B, D, H, T, dtype="f32", lo=0, hi=T)
+    say(f"case limit long sequences {(B, D, H, T)} {mode} max_len {int(inp.lengths.max())}")
+    assert inp.lengths.max() > 2048
+    h, c, m = run(inp, mode)
+    assert m.query(ld.Q_LAST_STATUS) == ld.OK
+    assert m.query(ld.Q_TOTAL_ROWS) == int(inp.lengths.sum())
+    assert m.query(ld.Q_STEPS_EXECUTED) == int(inp.lengths.max())
+    ho, co = oracle.forward_inputs(inp)
+    eh, ec = max_err(h, ho), max_err(c, co)
+    say(f"  every row: max|dh|={eh:.3g} max|dc|={ec:.3g}")
+    assert eh <= TOL["f32"] and ec <= TOL["f32"]
+    m.close()
+
+
 def test_one_row_more_needs_the_per_step_path():
     with pytest.raises(ld.LstmDynError) as e:
         ld.LstmDyn(513, 40, 1024, 6, "bf16", "persistent")
