@@ -776,14 +776,31 @@ persistent_kernel(PersistParams p) {
                             hst[i] = hn[i];
                         }
                     }
-                    // each lane stores its own elements of h_{t+1} (padding units
-                    // of a ragged last workgroup as zeros); a reader checks every
-                    // element for the marker, so a segment may arrive in parts
+                    // 16-bit operands: each lane stores its own elements of
+                    // h_{t+1} (padding units of a ragged last workgroup as
+                    // zeros); a reader checks every element for the marker, so a
+                    // segment may arrive in parts.  fp32 operands: the tile's
+                    // rows are gathered in this wave's staging slot and each
+                    // active row leaves as one segment store (for fp32 the
+                    // per-element stores made the loop 12% slower).
                     stress_delay(t, 64 + a);
+                    if constexpr (E::KPL == 1) {
 #pragma unroll
-                    for (int mt = 0; mt < MT; ++mt) {
-                        const int s = nt * 16 + (lo & 15), u = u0 + mt * 4 + (lo >> 4);
-                        if (s < act) IO::store(R, nxt + hx_off<E>(s, u, hpad), u < H ? hst[a * MT + mt] : 0.0f);
+                        for (int mt = 0; mt < MT; ++mt) {
+                            const int u = u0 + mt * 4 + (lo >> 4);
+                            hstage[w][(lo & 15) * UPW + mt * 4 + (lo >> 4)] =
+                                u < H ? IO::operand(hst[a * MT + mt]) : E::from_f32(0.0f);
+                        }
+                        __builtin_amdgcn_wave_barrier();
+                        if (lo < 16 && nt * 16 + lo < act)
+                            seg_store(nxt + hx_off<E>(nt * 16 + lo, u0, hpad), &hstage[w][lo * UPW]);
+                        __builtin_amdgcn_wave_barrier();
+                    } else {
+#pragma unroll
+                        for (int mt = 0; mt < MT; ++mt) {
+                            const int s = nt * 16 + (lo & 15), u = u0 + mt * 4 + (lo >> 4);
+                            if (s < act) IO::store(R, nxt + hx_off<E>(s, u, hpad), u < H ? hst[a * MT + mt] : 0.0f);
+                        }
                     }
                     if constexpr (LY::G < NOT) {
                         // the Gx of owned tile a + G (next chunk) into this tile's
