@@ -72,6 +72,28 @@ def test_long_sequences(mode):
     m.close()
 
 
+@pytest.mark.parametrize("B", [255, 256, 257, 300, 511, 512, 513, 1000, 1024, 1025, 3001])
+def test_length_preparation_batch_sizes(B):
+    """The length preparation counts each row's rank on 4, 2 or 1 lanes as B
+    is at most 256, 512 or more, and keeps the batch rows of the first 256
+    slots in registers (the rest come from LDS): a batch on each side of those
+    bounds (the loop kernel up to 512 rows, the per-step path above), lengths
+    0..9 with many ties, every row against the oracle and the valid-row
+    count."""
+    D, H, T = 8, 64, 9
+    mode = "persistent" if B <= 512 else "per_step"
+    inp = workloads.random_case(4500 + B, B, D, H, T, dtype="f32", lo=0, hi=T)
+    say(f"case length preparation B={B} {mode}")
+    h, c, m = run(inp, mode)
+    assert m.query(ld.Q_LAST_STATUS) == ld.OK
+    assert m.query(ld.Q_TOTAL_ROWS) == int(inp.lengths.sum())
+    ho, co = oracle.forward_inputs(inp)
+    eh, ec = max_err(h, ho), max_err(c, co)
+    say(f"  every row: max|dh|={eh:.3g} max|dc|={ec:.3g}")
+    assert eh <= TOL["f32"] and ec <= TOL["f32"]
+    m.close()
+
+
 def test_one_row_more_needs_the_per_step_path():
     with pytest.raises(ld.LstmDynError) as e:
         ld.LstmDyn(513, 40, 1024, 6, "bf16", "persistent")
