@@ -35,23 +35,56 @@ constexpr int IP_LDS_BYTES = 2 * IP_STAGE * 2;
 typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
 
 // Wt[c'][k] = W[k][col(c')] for c' < 4H, k < D; zero elsewhere (np x dp).
+// A tile is 64 k by 64 c'; its 64 c' are 16 units times the four gates, so in
+// a row of W they are four runs of 16 consecutive columns.  Each thread reads
+// two 16-byte pieces of those runs (element by element when H is not a
+// multiple of 8, W is not 16-byte aligned or the tile passes the edge of W),
+// the tile turns through LDS, and each thread writes two 16-byte pieces of
+// rows of Wt (dp is a multiple of 64).
 __global__ void __launch_bounds__(256)
 transpose_w_kernel(const __bf16* __restrict__ W, __bf16* __restrict__ Wt, int D, int H, int np, int dp) {
-    __shared__ __bf16 tile[64][64 + 2];
-    const int k0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
-    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-    const int H4 = 4 * H;
-    // read: rows k, columns c' (gathered through the gate interleave)
-    for (int i = ty; i < 64; i += 4) {
-        const int k = k0 + i, cp = c0 + tx;
-        const bool ok = k < D && cp < H4;
-        const __bf16 v = W[ok ? (size_t)k * H4 + gate_col(cp, H) : 0];
-        tile[tx][i] = ok ? v : (__bf16)0.0f;
+    constexpr int LDT = 64 + 8;  // bf16 per LDS row: 144 bytes, rows 16-byte aligned
+    __shared__ __attribute__((aligned(16))) __bf16 tile[64][LDT];  // [c' in tile][k in tile]
+    const int k0 = blockIdx.x * 64, c0 = blockIdx.y * 64, u0 = c0 / 4;
+    const size_t H4 = 4 * (size_t)H;
+    // a tile inside W, H a multiple of 8 and W 16-byte aligned: both pieces
+    // by 16-byte loads, in flight together; otherwise element by element
+    const bool vec = (H % 8) == 0 && (reinterpret_cast<uintptr_t>(W) & 15) == 0 && k0 + 64 <= D &&
+                     u0 + 16 <= H;
+    bf16x8_t v[2];
+    if (vec) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int i = threadIdx.x + 256 * j;
+            const int kl = i >> 3, g = (i >> 1) & 3, ub = u0 + 8 * (i & 1);  // row, gate, first unit
+            v[j] = *reinterpret_cast<const bf16x8_t*>(W + (size_t)(k0 + kl) * H4 + (size_t)g * H + ub);
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int i = threadIdx.x + 256 * j;
+            const int kl = i >> 3, g = (i >> 1) & 3, ub = u0 + 8 * (i & 1);
+            const int k = k0 + kl;
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                v[j][e] = (k < D && ub + e < H) ? W[(size_t)k * H4 + (size_t)g * H + ub + e] : (__bf16)0.0f;
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int i = threadIdx.x + 256 * j;
+        const int kl = i >> 3, g = (i >> 1) & 3, ub = u0 + 8 * (i & 1);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) tile[4 * (ub - u0 + e) + g][kl] = v[j][e];
     }
     __syncthreads();
-    for (int i = ty; i < 64; i += 4) {
-        const int cp = c0 + i, k = k0 + tx;
-        if (cp < np && k < dp) Wt[(size_t)cp * dp + k] = tile[i][tx];
+#pragma unroll
+    for (int i = threadIdx.x; i < 512; i += 256) {
+        const int cl = i >> 3, kp = 8 * (i & 7);
+        const int cp = c0 + cl;
+        if (cp < np && k0 + kp < dp)
+            *reinterpret_cast<bf16x8_t*>(Wt + (size_t)cp * dp + k0 + kp) =
+                *reinterpret_cast<const bf16x8_t*>(&tile[cl][kp]);
     }
 }
 
