@@ -69,6 +69,7 @@ SHAPES = [
     (1, 1, 1, 3, "f32"), (5, 7, 13, 9, "bf16"), (3, 16, 32, 6, "f32"), (17, 24, 32, 11, "bf16"),
     (37, 40, 33, 17, "f32"), (37, 40, 33, 17, "bf16"), (33, 96, 100, 10, "bf16"),
     (16, 8, 260, 5, "f32"), (20, 40, 1100, 5, "bf16"), (272, 24, 1056, 4, "bf16"),
+    (9, 5, 40, 1, "f32"), (9, 8, 256, 1, "bf16"),   # one step: lengths 0 or 1
 ]
 
 

@@ -27,6 +27,7 @@ def _oracle(inp, rows=None):
 SHAPES = [
     # (B, D, H, T, dtype) -- ragged in every dimension, single- and multi-workgroup
     (1, 1, 1, 3, "f32"), (1, 1, 1, 3, "bf16"),
+    (9, 5, 40, 1, "f32"), (9, 5, 40, 1, "bf16"),          # one step: lengths 0 or 1
     (5, 7, 13, 9, "f32"), (5, 7, 13, 9, "bf16"),
     (3, 16, 32, 6, "f32"), (17, 24, 32, 11, "bf16"),
     (37, 40, 33, 17, "f32"), (37, 40, 33, 17, "bf16"),   # H just above one workgroup
