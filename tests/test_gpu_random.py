@@ -28,7 +28,7 @@ def _draw(k):
     return B, D, H, T, dt, mode, cell
 
 
-CASES = list(range(40))
+CASES = list(range(240))
 
 
 @pytest.mark.parametrize("k", CASES)
