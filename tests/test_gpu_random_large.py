@@ -3,7 +3,8 @@
 and 512 (the whole reverse loop in one launch; above 256 padded rows it keeps
 the carried gradients in memory), ragged lengths, with and without the
 output sequence's gradient.  The forward for training (final state and
-output sequence) and every gradient against the fp64 oracle."""
+output sequence) and every gradient against the fp64 oracle; the same for
+the GRU and tanh RNN cells' gradients."""
 import numpy as np
 import pytest
 
@@ -11,6 +12,9 @@ import oracle
 import workloads
 from tests.gpu_util import max_err, say
 from tests.test_gpu_bwd import GRAD_TOL, compare, oracle_grads, run_train
+from tests.test_gpu_bwd_cells import KEYS as CELL_KEYS
+from tests.test_gpu_bwd_cells import oracle_grads as cell_oracle
+from tests.test_gpu_bwd_cells import run_train as cell_run
 
 pytestmark = pytest.mark.gpu
 
@@ -44,4 +48,18 @@ def test_random_large_batch(k):
     go = oracle_grads(inp, dh.astype(np.float64), dc.astype(np.float64),
                       ds.astype(np.float64) if ds is not None else None)
     compare(g, go, GRAD_TOL[workloads.BF16])
+    m.close()
+
+
+@pytest.mark.parametrize("k", list(range(8)))
+def test_random_large_batch_cells(k):
+    B, D, H, T, seq = _draw(100 + k)
+    cell = "gru" if k % 2 == 0 else "rnn"
+    say(f"case random large {cell} {k}: B={B} D={D} H={H} T={T} dseq={seq}")
+    inp = workloads.random_cell_case(cell, 9300 + k, B, D, H, T, dtype="bf16")
+    rng = np.random.default_rng(9400 + k)
+    dh = rng.standard_normal((B, H)).astype(np.float32)
+    ds = rng.standard_normal((B, T, H)).astype(np.float32) if seq else None
+    g, m = cell_run(inp, "persistent", dh, ds)
+    compare(g, cell_oracle(inp, dh, ds), GRAD_TOL[workloads.BF16], keys=CELL_KEYS)
     m.close()
