@@ -146,6 +146,12 @@ typedef struct {
  * and allocate the handle's device workspace (hipMalloc; freed by destroy).
  *   B >= 1, D >= 1, H >= 1, T_max >= 1; dtype LSTM_DYN_F32/BF16; mode
  *   LSTM_DYN_PERSISTENT/PER_STEP.  *out receives the handle (NULL on error).
+ * Sizes covered: B <= 8192 and B * T_max < 2^31; one workgroup per compute
+ * unit owns 4 hidden units (fp32 data, and bf16 data with H <= 1024) or 8
+ * (bf16 data, H > 1024), so H <= 4 x CUs with fp32 data and H <= 8 x CUs
+ * with bf16 data (1024 and 2048 on a 256-CU device), in either mode; the
+ * persistent mode also holds at most 512 rows.  lstm_dyn_plan gives the
+ * answer for a device without a handle.
  * Returns LSTM_DYN_OK, ERR_INVALID (bad arguments; no HIP call is made),
  * ERR_UNSUPPORTED (sizes the compiled kernel variants do not cover), ERR_HIP, ERR_NOMEM.
  */

@@ -4,7 +4,10 @@ and 512 (the whole reverse loop in one launch; above 256 padded rows it keeps
 the carried gradients in memory), ragged lengths, with and without the
 output sequence's gradient.  The forward for training (final state and
 output sequence) and every gradient against the fp64 oracle; the same for
-the GRU and tanh RNN cells' gradients."""
+the GRU and tanh RNN cells' gradients.  Also the forward at the widest
+hidden layers (bf16 up to 2048, two gate tiles per workgroup above 1024;
+fp32 up to 1024), both modes, every row and the output sequence against the
+oracle."""
 import numpy as np
 import pytest
 
@@ -62,4 +65,37 @@ def test_random_large_batch_cells(k):
     ds = rng.standard_normal((B, T, H)).astype(np.float32) if seq else None
     g, m = cell_run(inp, "persistent", dh, ds)
     compare(g, cell_oracle(inp, dh, ds), GRAD_TOL[workloads.BF16], keys=CELL_KEYS)
+    m.close()
+
+
+def _draw_wide(k):
+    # the widest hidden layers each dtype takes (bf16 up to 8 units per CU,
+    # fp32 up to 4), each width once; the rest drawn
+    rng = np.random.default_rng(9600 + k)
+    B = int(rng.integers(17, 301))
+    D = int(rng.choice([16, 100]))
+    dt = ("bf16", "f32")[k // 4]
+    H = ((1024, 1100, 1536, 2048), (513, 777, 1000, 1024))[k // 4][k % 4]
+    T = int(rng.integers(2, 13))
+    mode = str(rng.choice(["persistent", "per_step"]))
+    return B, D, H, T, dt, mode
+
+
+@pytest.mark.parametrize("k", list(range(8)))
+def test_random_wide_forward(k):
+    import torch
+    from tests.gpu_util import to_device
+    import paper_1810_08061_amd as ld
+    B, D, H, T, dt, mode = _draw_wide(k)
+    say(f"case random wide {k}: B={B} D={D} H={H} T={T} {dt} {mode}")
+    inp = workloads.random_case(9650 + k, B, D, H, T, dtype=dt)
+    m = ld.LstmDyn(B, D, H, T, dt, mode)
+    h, c, seq = m.forward_seq(*to_device(inp))
+    torch.cuda.synchronize()
+    assert m.query(ld.Q_LAST_STATUS) == ld.OK
+    ho, co, so = oracle.forward_inputs(inp, seq=True)
+    tol = 1e-5 if dt == "f32" else TOL
+    eh, ec, es = max_err(h.cpu().numpy(), ho), max_err(c.cpu().numpy(), co), max_err(seq.cpu().numpy(), so)
+    say(f"  max|dh|={eh:.2e} max|dc|={ec:.2e} max|dseq|={es:.2e}")
+    assert eh <= tol and ec <= tol and es <= tol
     m.close()
